@@ -1,0 +1,178 @@
+/*
+ * mebp.h — C ABI of the MeBP checkpointed LoRA training step on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * MeBP (memory-efficient backpropagation, Sec. 3 and Algorithm 1 of the paper) trains
+ * LoRA adapters of a decoder-only transformer with gradient checkpointing at every block
+ * boundary. The forward loop stores only the block-boundary activations ("checkpoints");
+ * the backward loop walks the blocks in reverse, decompresses each block's int4 base
+ * weights just before use, recomputes the block's forward from its checkpoint, and
+ * backpropagates into the LoRA A/B gradients and the block-input gradient (the backward
+ * graph B_i(x, dE/dy, w) -> (dE/dx, dE/dw) of Sec. 3). Blocks are every transformer
+ * layer plus the final linear layer and the cross-entropy loss (Sec. 4.2), the last two
+ * fused into one call here.
+ *
+ * Conventions shared by every entry point:
+ *  - Tensor arguments are DEVICE pointers owned by the caller; structs are host memory
+ *    read during the call only. Nothing is allocated by the library: all scratch lives in
+ *    the caller's workspace `ws` of at least mebp_workspace_bytes() bytes.
+ *  - Activations are fp32, token-major: row n = b*T + t of a [B*T][hidden] matrix.
+ *    Attention columns are head-major (column h*head_dim + e).
+ *  - Compressed base weights (Sec. 3, 4-bit symmetric INT4 of every non-LoRA parameter
+ *    incl. the embedding): per projection `q4` uint8 [out][in/2] (two's-complement
+ *    nibbles, element 2j of a row in the low nibble of byte j) and `scale` raw fp16 bits
+ *    [out][ceil(in/group)]; dequantised value W[o][i] = q[o][i] * scale[o][i/group].
+ *    The last group of a row may be shorter than `group`.
+ *  - LoRA: y = x W^T + (alpha/rank) (x A^T) B^T with A fp32 [rank][in], B fp32 [out][rank].
+ *  - Every call validates all arguments first. On error it enqueues nothing, records a
+ *    message for mebp_last_error() and returns a negative mebp_status. On success it
+ *    enqueues work on `stream` and returns MEBP_OK without synchronising; outputs are
+ *    valid once the stream reaches that point. Calls on one stream are ordered; two calls
+ *    sharing one workspace must not run concurrently.
+ *  - Results are deterministic: the same inputs give bit-identical outputs (no atomics
+ *    in any reduction).
+ */
+#ifndef MEBP_H
+#define MEBP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A hipStream_t passed as an opaque pointer; NULL selects the null stream. */
+typedef void* mebp_stream_t;
+
+typedef enum {
+  MEBP_OK = 0,
+  MEBP_EINVAL = -1,       /* null pointer, negative size, inconsistent config            */
+  MEBP_EUNSUPPORTED = -2, /* valid but unsupported shape (head_dim, rank, alignment)     */
+  MEBP_EWORKSPACE = -3,   /* ws_bytes smaller than mebp_workspace_bytes()                */
+  MEBP_EHIP = -4          /* a HIP runtime call or kernel launch failed                  */
+} mebp_status;
+
+/* Projection indices used by every per-projection array. */
+enum { MEBP_Q = 0, MEBP_K = 1, MEBP_V = 2, MEBP_O = 3, MEBP_GATE = 4, MEBP_UP = 5, MEBP_DOWN = 6,
+       MEBP_NPROJ = 7 };
+
+typedef struct {
+  int32_t n_layers;      /* L >= 1                                                        */
+  int32_t hidden;        /* d, multiple of 32                                             */
+  int32_t n_heads;       /* Hq                                                            */
+  int32_t n_kv_heads;    /* Hkv, divides Hq (grouped-query attention, consecutive heads)  */
+  int32_t head_dim;      /* 64, 128 or 256                                                */
+  int32_t ffn;           /* F, multiple of 16                                             */
+  int32_t vocab;         /* V, multiple of 32; 0 when no LM head is used                  */
+  int32_t act;           /* 0 = SwiGLU (SiLU gate), 1 = GeGLU (tanh-approximated GELU)    */
+  float rms_eps;         /* RMSNorm epsilon                                               */
+  float rope_theta_global; /* RoPE base of global layers                                  */
+  float rope_theta_local;  /* RoPE base of sliding-window layers                          */
+  int32_t window;        /* sliding window W of local layers: key j visible to query i    */
+                         /* iff i-W < j <= i; 0 = no window                               */
+  int32_t global_every;  /* 0: every layer global; k > 0: layer l global iff (l+1)%k == 0 */
+  int32_t group;         /* int4 scale group along the input dim; must be 32              */
+  int32_t lora_rank;     /* r: 8 or 16                                                    */
+  float lora_alpha;      /* LoRA scale s = alpha / r                                      */
+  uint32_t lora_mask;    /* bit p set: projection p carries a LoRA adapter                */
+} mebp_config;
+
+typedef struct {
+  const uint8_t* q4;        /* [out][in/2]                                                */
+  const uint16_t* scale;    /* [out][ceil(in/group)] fp16 bits                            */
+} mebp_q4;
+
+typedef struct {
+  mebp_q4 w[MEBP_NPROJ];    /* q [Hq*dh][d], k,v [Hkv*dh][d], o [d][Hq*dh],               */
+                            /* gate,up [F][d], down [d][F]                                */
+  const float* norm_attn;   /* [d] fp32 RMSNorm weight before attention (frozen)          */
+  const float* norm_mlp;    /* [d] fp32 RMSNorm weight before the MLP (frozen)            */
+} mebp_layer_base;
+
+typedef struct {
+  const float* A[MEBP_NPROJ]; /* [r][in]; NULL where the projection is not adapted        */
+  const float* B[MEBP_NPROJ]; /* [out][r]                                                 */
+} mebp_layer_lora;
+
+typedef struct {
+  float* dA[MEBP_NPROJ];    /* [r][in], overwritten (not accumulated); NULL if not adapted */
+  float* dB[MEBP_NPROJ];    /* [out][r]                                                   */
+} mebp_layer_lora_grad;
+
+/* Bytes of workspace every entry point below needs for this config and batch shape
+ * (B sequences of T tokens). Pure host computation; returns 0 for an invalid config. */
+size_t mebp_workspace_bytes(const mebp_config* cfg, int32_t B, int32_t T);
+
+/* forward_i of Algorithm 1 for transformer layer `layer` (Sec. 3, "Runtime
+ * implementation"): x_out = F(x_in) with the int4 weights decompressed inside the GEMMs.
+ *   x_in  [B*T][d] fp32 checkpoint of the layer input (read only)
+ *   x_out [B*T][d] fp32 checkpoint of the layer output (written; must not alias x_in)   */
+int mebp_layer_forward_ckpt(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
+                            const mebp_layer_lora* lora, const float* x_in, float* x_out,
+                            int32_t B, int32_t T, void* ws, size_t ws_bytes, mebp_stream_t stream);
+
+/* backward_i of Algorithm 1 (Sec. 3 backward graph B_i(x, dE/dy, w) -> (dE/dx, dE/dw)):
+ * recomputes the layer forward from its checkpoint and backpropagates.
+ *   x_ckpt [B*T][d] fp32 layer input checkpoint
+ *   dy     [B*T][d] fp32 gradient of the loss w.r.t. the layer output
+ *   dx     [B*T][d] fp32 gradient w.r.t. the layer input, or NULL to skip it; may alias dy
+ *   grads  LoRA gradients of the adapted projections (overwritten)                       */
+int mebp_layer_recompute_backward(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
+                                  const mebp_layer_lora* lora, const float* x_ckpt, const float* dy,
+                                  float* dx, const mebp_layer_lora_grad* grads, int32_t B, int32_t T,
+                                  void* ws, size_t ws_bytes, mebp_stream_t stream);
+
+/* Final block (Sec. 4.2: the final linear layer and the cross-entropy loss layer):
+ * RMSNorm, logits against the tied int4 embedding, next-token cross-entropy averaged over
+ * the B*(T-1) positions that have a target (position T-1 of each sequence has none), and
+ * the gradient w.r.t. the last checkpoint.
+ *   emb        tied embedding [V][d/2] / [V][d/32]
+ *   norm_final [d] fp32
+ *   x_last     [B*T][d] fp32 output checkpoint of the last layer
+ *   ids        [B][T] int32 token ids in [0, V)
+ *   loss       one fp32 on the device (written)
+ *   dx_last    [B*T][d] fp32 (written)                                                    */
+int mebp_lm_head_ce_backward(const mebp_config* cfg, const mebp_q4* emb, const float* norm_final,
+                             const float* x_last, const int32_t* ids, int32_t B, int32_t T,
+                             float* loss, float* dx_last, void* ws, size_t ws_bytes,
+                             mebp_stream_t stream);
+
+/* Embedding lookup with decompression of the tied int4 table (Sec. 3: the embeddings are
+ * INT4 too): x0[b*T+t][:] = E[ids[b][t]][:] in fp32.                                    */
+int mebp_embed(const mebp_config* cfg, const mebp_q4* emb, const int32_t* ids, int32_t B, int32_t T,
+               float* x0, mebp_stream_t stream);
+
+/* Backpropagation(x) of Algorithm 1 for one batch of token ids: embedding, forward loop
+ * storing every checkpoint, final block, reverse loop recomputing each layer.
+ *   layers, lora, grads  host arrays of cfg->n_layers entries
+ *   ckpt  [(L+1)][B*T][d] fp32 checkpoint storage (written; ckpt[l] is the input of layer l)
+ *   loss  one fp32 on the device (written)
+ *   dx0   [B*T][d] fp32 gradient w.r.t. the embedding output, or NULL to skip layer 0's
+ *         input gradient (the embedding is frozen)                                       */
+int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
+                    const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids,
+                    int32_t B, int32_t T, float* ckpt, float* loss, const mebp_layer_lora_grad* grads,
+                    float* dx0, void* ws, size_t ws_bytes, mebp_stream_t stream);
+
+/* Message for the last non-zero status returned on the calling thread ("" if none). */
+const char* mebp_last_error(void);
+
+/* ---------------- test and diagnostic entry points ---------------------------------- */
+
+/* Decompression alone (Algorithm 1, decompress): out_f32[r][c] = q*s exactly and/or
+ * out_bf16[r][c] = bf16 bits of that value rounded to nearest even (either may be NULL).
+ * cols must be a multiple of 8; group as in mebp_config.                                 */
+int mebp_dequant_q4(const mebp_q4* w, int32_t rows, int32_t cols, int32_t group, float* out_f32,
+                    uint16_t* out_bf16, mebp_stream_t stream);
+
+/* Byte offset inside the workspace of an intermediate kept by the last
+ * mebp_layer_recompute_backward / mebp_layer_forward_ckpt on that workspace (for tests).
+ * Returns (size_t)-1 for an unknown slot. Slots are listed by mebp_workspace_slot_name. */
+size_t mebp_workspace_offset(const mebp_config* cfg, int32_t B, int32_t T, int32_t slot);
+const char* mebp_workspace_slot_name(int32_t slot);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MEBP_H */

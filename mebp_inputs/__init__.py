@@ -135,19 +135,11 @@ CONFIG_ORDER = ["block", "qwen2.5-0.5b", "gemma3-1b", "qwen2.5-1.5b", "gemma3-4b
 # ----------------------------------------------------------------------------------------
 # Offline int4 compression (produces the compressed input format; not part of the step)
 # ----------------------------------------------------------------------------------------
-def quantize_q4(w: np.ndarray, group: int = 32) -> Tuple[np.ndarray, np.ndarray]:
-    """Symmetric int4 group quantisation of ``w`` fp32 ``[out][in]``.
-
-    Returns ``(q4, scale_bits)``: packed codes uint8 ``[out][in/2]`` and raw fp16 scale
-    bits uint16 ``[out][ceil(in/group)]``.
-    """
-    w = np.asarray(w, dtype=np.float32)
+def _quantize_rows(w: np.ndarray, group: int) -> Tuple[np.ndarray, np.ndarray]:
     out, inn = w.shape
-    if inn % 2:
-        raise ValueError("input dimension must be even to pack two codes per byte")
     ng = -(-inn // group)
     pad = ng * group - inn
-    wp = np.pad(w, ((0, 0), (0, pad))).reshape(out, ng, group)
+    wp = (np.pad(w, ((0, 0), (0, pad))) if pad else w).reshape(out, ng, group)
     amax = np.abs(wp).max(axis=-1).astype(np.float64)
     s16 = (amax / 7.0).astype(np.float16)
     s = s16.astype(np.float64)
@@ -156,7 +148,42 @@ def quantize_q4(w: np.ndarray, group: int = 32) -> Tuple[np.ndarray, np.ndarray]
     q = np.clip(q, -7, 7).astype(np.int8).reshape(out, ng * group)[:, :inn]
     u = (q.astype(np.int16) & 0xF).astype(np.uint8)
     q4 = (u[:, 0::2] | (u[:, 1::2] << 4)).astype(np.uint8)
-    return np.ascontiguousarray(q4), np.ascontiguousarray(s16.view(np.uint16))
+    return q4, s16.view(np.uint16)
+
+
+_POOL = None
+
+
+def quantize_q4(w: np.ndarray, group: int = 32) -> Tuple[np.ndarray, np.ndarray]:
+    """Symmetric int4 group quantisation of ``w`` fp32 ``[out][in]``.
+
+    Returns ``(q4, scale_bits)``: packed codes uint8 ``[out][in/2]`` and raw fp16 scale
+    bits uint16 ``[out][ceil(in/group)]``. Rows are independent; large matrices are
+    processed in row blocks on a thread pool (same result as one block).
+    """
+    global _POOL
+    w = np.asarray(w, dtype=np.float32)
+    out, inn = w.shape
+    if inn % 2:
+        raise ValueError("input dimension must be even to pack two codes per byte")
+    rows = max(1, (1 << 18) // max(inn, 1))
+    if out <= rows:
+        q4, sb = _quantize_rows(w, group)
+        return np.ascontiguousarray(q4), np.ascontiguousarray(sb)
+    if _POOL is None:
+        import os
+        from concurrent.futures import ThreadPoolExecutor
+        _POOL = ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1)))
+    q4 = np.empty((out, inn // 2), np.uint8)
+    sb = np.empty((out, -(-inn // group)), np.uint16)
+
+    def job(r0):
+        a, b = _quantize_rows(w[r0:r0 + rows], group)
+        q4[r0:r0 + rows] = a
+        sb[r0:r0 + rows] = b
+
+    list(_POOL.map(job, range(0, out, rows)))
+    return q4, sb
 
 
 # ----------------------------------------------------------------------------------------
@@ -250,3 +277,9 @@ def layer_input(cfg: Config, seed: int) -> Tuple[np.ndarray, np.ndarray]:
 TINY = Config(name="tiny", n_layers=2, hidden=64, n_heads=4, n_kv_heads=2, head_dim=16, ffn=96,
               vocab=97, act="silu", rope_theta_global=1e4, rope_theta_local=1e4, window=3,
               global_every=2, lora_rank=2, lora_alpha=4.0, lora_modules=ALL7, batch=2, seq=7)
+
+# Small GPU-compatible shape (head_dim 64, ragged tiles everywhere: T = 160, ffn = 352,
+# vocab = 1056, a sliding-window layer and a global layer, all seven projections adapted).
+MINI = Config(name="mini", n_layers=2, hidden=128, n_heads=4, n_kv_heads=2, head_dim=64, ffn=352,
+              vocab=1056, act="gelu_tanh", rope_theta_global=1e6, rope_theta_local=1e4, window=96,
+              global_every=2, lora_rank=16, lora_alpha=32.0, lora_modules=ALL7, batch=2, seq=160)

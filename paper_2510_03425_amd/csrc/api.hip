@@ -1,0 +1,650 @@
+// C ABI of libmebp: argument validation, workspace layout and the orchestration of the
+// checkpointed LoRA step (Algorithm 1) out of the gfx950 kernels. Every entry point
+// validates everything before enqueuing anything; nothing here allocates device memory.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/mebp.h"
+#include "mebp_internal.h"
+
+using namespace mebp;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                  \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess) return fail(MEBP_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// ------------------------------------------------------------------ workspace layout
+enum Slot {
+  S_A, S_Q, S_K, S_V, S_O, S_LSE, S_H, S_C, S_G, S_U, S_Z, S_LU, S_LDU, S_DYB, S_DC, S_DH, S_DHB, S_DO,
+  S_DELTA, S_DQ, S_DK, S_DV, S_DA, S_PART, S_ROPE_G, S_ROPE_L, S_TGT, S_HF, S_LOGITS, S_STATS, S_LSEV,
+  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_COUNT
+};
+const char* kSlotNames[S_COUNT] = {
+  "a", "q", "k", "v", "o", "lse", "h", "c", "g", "u", "z", "lora_u", "lora_du", "dy_bf16", "dc", "dh",
+  "dh_bf16", "do", "delta", "dq", "dk", "dv", "da", "lora_part", "rope_global", "rope_local", "targets",
+  "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad"};
+
+struct Layout {
+  size_t off[S_COUNT];
+  size_t total;
+  int lm_splits;
+  int ntiles;
+};
+
+int lm_head_splits(int N, int d, int V) {
+  const int tiles = ((d + 127) / 128) * ((N + 127) / 128);
+  int s = (512 + tiles - 1) / tiles;
+  const int max_s = ((V + 63) / 64 + 7) / 8;
+  if (s > max_s) s = max_s;
+  if (s > 64) s = 64;
+  if (s < 1) s = 1;
+  return s;
+}
+
+bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
+  const size_t N = (size_t)B * T, d = c->hidden, qd = (size_t)c->n_heads * c->head_dim,
+               kvd = (size_t)c->n_kv_heads * c->head_dim, F = c->ffn, r = c->lora_rank > 0 ? c->lora_rank : 16,
+               V = c->vocab, H = c->n_heads;
+  size_t maxc = d > F ? d : F;
+  if (qd > maxc) maxc = qd;
+  const int splits = lora_outer_splits((int)N);
+  L->lm_splits = V ? lm_head_splits((int)N, (int)d, (int)V) : 0;
+  L->ntiles = V ? gemm_nt_tiles((int)V) : 0;
+  size_t sz[S_COUNT] = {};
+  sz[S_A] = N * d * 2;
+  sz[S_Q] = N * qd * 2;
+  sz[S_K] = N * kvd * 2;
+  sz[S_V] = N * kvd * 2;
+  sz[S_O] = N * qd * 2;
+  sz[S_LSE] = N * H * 4;
+  sz[S_H] = N * d * 4;
+  sz[S_C] = N * d * 2;
+  sz[S_G] = N * F * 2;
+  sz[S_U] = N * F * 2;
+  sz[S_Z] = N * F * 2;
+  sz[S_LU] = MEBP_NPROJ * N * r * 4;
+  sz[S_LDU] = MEBP_NPROJ * N * r * 4;
+  sz[S_DYB] = N * d * 2;
+  sz[S_DC] = N * d * 4;
+  sz[S_DH] = N * d * 4;
+  sz[S_DHB] = N * d * 2;
+  sz[S_DO] = N * qd * 2;
+  sz[S_DELTA] = N * H * 4;
+  sz[S_DQ] = N * qd * 2;
+  sz[S_DK] = N * kvd * 2;
+  sz[S_DV] = N * kvd * 2;
+  sz[S_DA] = N * d * 4;
+  sz[S_PART] = (size_t)splits * maxc * r * 4;
+  sz[S_ROPE_G] = (size_t)T * c->head_dim * 4;
+  sz[S_ROPE_L] = (size_t)T * c->head_dim * 4;
+  sz[S_TGT] = N * 4;
+  sz[S_HF] = V ? N * d * 2 : 0;
+  sz[S_LOGITS] = N * V * 2;
+  sz[S_STATS] = N * (size_t)L->ntiles * 8;
+  sz[S_LSEV] = V ? N * 4 : 0;
+  sz[S_TGTLOGIT] = V ? N * 4 : 0;
+  sz[S_ROWLOSS] = V ? N * 4 : 0;
+  sz[S_DHF] = V ? N * d * 4 : 0;
+  sz[S_LMPART] = (size_t)L->lm_splits * N * d * 4;
+  sz[S_GRAD] = N * d * 4;
+  size_t o = 0;
+  for (int i = 0; i < S_COUNT; ++i) {
+    L->off[i] = o;
+    o += (sz[i] + 255) & ~(size_t)255;
+  }
+  L->total = o;
+  return true;
+}
+
+template <class Tp>
+Tp* slot(void* ws, const Layout& L, int s) {
+  return (Tp*)((char*)ws + L.off[s]);
+}
+
+// ------------------------------------------------------------------ validation
+int check_config(const mebp_config* c) {
+  if (!c) return fail(MEBP_EINVAL, "cfg is NULL");
+  if (c->n_layers < 1 || c->hidden <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->ffn <= 0 || c->vocab < 0)
+    return fail(MEBP_EINVAL, "non-positive dimension in config");
+  if (c->n_heads % c->n_kv_heads) return fail(MEBP_EINVAL, "n_heads %% n_kv_heads != 0");
+  if (c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256)
+    return fail(MEBP_EUNSUPPORTED, "head_dim %d not in {64, 128, 256}", c->head_dim);
+  if (c->hidden % 32) return fail(MEBP_EUNSUPPORTED, "hidden %d not a multiple of 32", c->hidden);
+  if (c->ffn % 16) return fail(MEBP_EUNSUPPORTED, "ffn %d not a multiple of 16", c->ffn);
+  if (c->vocab % 32) return fail(MEBP_EUNSUPPORTED, "vocab %d not a multiple of 32", c->vocab);
+  if (c->group != 32) return fail(MEBP_EUNSUPPORTED, "group %d != 32", c->group);
+  if (c->act != 0 && c->act != 1) return fail(MEBP_EINVAL, "act %d not 0 (SiLU) or 1 (GELU-tanh)", c->act);
+  if (!(c->rms_eps >= 0.f) || !isfinite(c->rms_eps)) return fail(MEBP_EINVAL, "bad rms_eps");
+  if (!(c->rope_theta_global > 0.f) || !(c->rope_theta_local > 0.f)) return fail(MEBP_EINVAL, "bad rope theta");
+  if (c->window < 0 || c->global_every < 0) return fail(MEBP_EINVAL, "negative window / global_every");
+  if (c->lora_mask >> MEBP_NPROJ) return fail(MEBP_EINVAL, "lora_mask has bits beyond the 7 projections");
+  if (c->lora_mask && c->lora_rank != 8 && c->lora_rank != 16)
+    return fail(MEBP_EUNSUPPORTED, "lora_rank %d not in {8, 16}", c->lora_rank);
+  if (c->lora_mask && !isfinite(c->lora_alpha)) return fail(MEBP_EINVAL, "bad lora_alpha");
+  return MEBP_OK;
+}
+
+int check_shape(int B, int T) {
+  if (B < 1 || T < 1) return fail(MEBP_EINVAL, "B=%d T=%d must be >= 1", B, T);
+  if ((long long)B * T > (1LL << 24)) return fail(MEBP_EUNSUPPORTED, "B*T=%lld too large", (long long)B * T);
+  return MEBP_OK;
+}
+
+int check_ws(const mebp_config* c, int B, int T, void* ws, size_t ws_bytes) {
+  const size_t need = mebp_workspace_bytes(c, B, T);
+  if (!ws) return fail(MEBP_EINVAL, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(MEBP_EINVAL, "workspace not 256-byte aligned");
+  if (ws_bytes < need) return fail(MEBP_EWORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need);
+  return MEBP_OK;
+}
+
+int check_q4(const mebp_q4* w, const char* what) {
+  if (!w || !w->q4 || !w->scale) return fail(MEBP_EINVAL, "%s: NULL compressed weight", what);
+  if (!aligned(w->q4, 4) || !aligned(w->scale, 2)) return fail(MEBP_EINVAL, "%s: misaligned weight", what);
+  return MEBP_OK;
+}
+
+int check_act(const void* p, const char* what) {
+  if (!p) return fail(MEBP_EINVAL, "%s is NULL", what);
+  if (!aligned(p, 16)) return fail(MEBP_EINVAL, "%s not 16-byte aligned", what);
+  return MEBP_OK;
+}
+
+const char* kProjName[MEBP_NPROJ] = {"q", "k", "v", "o", "gate", "up", "down"};
+
+int check_layer(const mebp_config* c, int layer, const mebp_layer_base* base, const mebp_layer_lora* lora) {
+  if (layer < 0 || layer >= c->n_layers) return fail(MEBP_EINVAL, "layer %d out of range", layer);
+  if (!base) return fail(MEBP_EINVAL, "base is NULL");
+  if (!lora) return fail(MEBP_EINVAL, "lora is NULL");
+  for (int p = 0; p < MEBP_NPROJ; ++p) {
+    int e = check_q4(&base->w[p], kProjName[p]);
+    if (e) return e;
+    if (c->lora_mask >> p & 1) {
+      if (!lora->A[p] || !lora->B[p]) return fail(MEBP_EINVAL, "LoRA %s: NULL A or B", kProjName[p]);
+    }
+  }
+  if (!base->norm_attn || !base->norm_mlp) return fail(MEBP_EINVAL, "NULL norm weight");
+  if (!aligned(base->norm_attn, 16) || !aligned(base->norm_mlp, 16))
+    return fail(MEBP_EINVAL, "norm weight not 16-byte aligned");
+  return MEBP_OK;
+}
+
+int check_grads(const mebp_config* c, const mebp_layer_lora_grad* g) {
+  if (!g) return c->lora_mask ? fail(MEBP_EINVAL, "grads is NULL") : MEBP_OK;
+  for (int p = 0; p < MEBP_NPROJ; ++p)
+    if ((c->lora_mask >> p & 1) && (!g->dA[p] || !g->dB[p]))
+      return fail(MEBP_EINVAL, "LoRA grad %s: NULL dA or dB", kProjName[p]);
+  return MEBP_OK;
+}
+
+// ------------------------------------------------------------------ shapes
+struct Dims {
+  int N, d, qd, kvd, F, r;
+  int in[MEBP_NPROJ], out[MEBP_NPROJ];
+  float s;
+};
+Dims dims(const mebp_config* c, int B, int T) {
+  Dims D;
+  D.N = B * T;
+  D.d = c->hidden;
+  D.qd = c->n_heads * c->head_dim;
+  D.kvd = c->n_kv_heads * c->head_dim;
+  D.F = c->ffn;
+  D.r = c->lora_rank;
+  D.s = c->lora_mask ? c->lora_alpha / (float)c->lora_rank : 0.f;
+  const int in[MEBP_NPROJ] = {D.d, D.d, D.d, D.qd, D.d, D.d, D.F};
+  const int out[MEBP_NPROJ] = {D.qd, D.kvd, D.kvd, D.d, D.F, D.F, D.d};
+  for (int p = 0; p < MEBP_NPROJ; ++p) {
+    D.in[p] = in[p];
+    D.out[p] = out[p];
+  }
+  return D;
+}
+bool is_global(const mebp_config* c, int l) { return c->global_every == 0 || (l + 1) % c->global_every == 0; }
+
+// ------------------------------------------------------------------ building blocks
+struct Ctx {
+  const mebp_config* c;
+  Dims D;
+  int B, T;
+  void* ws;
+  Layout L;
+  hipStream_t st;
+};
+
+float* lu(const Ctx& x, int p) { return slot<float>(x.ws, x.L, S_LU) + (size_t)p * x.D.N * x.D.r; }
+float* ldu(const Ctx& x, int p) { return slot<float>(x.ws, x.L, S_LDU) + (size_t)p * x.D.N * x.D.r; }
+bool adapted(const Ctx& x, int p) { return (x.c->lora_mask >> p) & 1; }
+
+NtSeg nt_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* lora, int p, void* out, int ldo,
+             const float* resid, int ldr) {
+  NtSeg s{};
+  s.q4 = base->w[p].q4;
+  s.scale = base->w[p].scale;
+  s.N = x.D.out[p];
+  s.lora_u = adapted(x, p) ? lu(x, p) : nullptr;
+  s.lora_B = adapted(x, p) ? lora->B[p] : nullptr;
+  s.out = out;
+  s.ldo = ldo;
+  s.resid = resid;
+  s.ldr = ldr;
+  return s;
+}
+
+hipError_t run_nt(const Ctx& x, const bf16* X, int K, int nseg, NtSeg* segs, int epi) {
+  NtArgs a{};
+  a.X = X;
+  a.lda = K;
+  a.M = x.D.N;
+  a.K = K;
+  a.nseg = nseg;
+  int t = 0;
+  for (int i = 0; i < nseg; ++i) {
+    segs[i].tile0 = t;
+    t += gemm_nt_tiles(segs[i].N);
+    a.seg[i] = segs[i];
+  }
+  a.lora_s = x.D.s;
+  a.r = x.D.r;
+  return launch_gemm_nt(a, epi, x.st);
+}
+
+TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* lora, int p, const bf16* G) {
+  TnSeg s{};
+  s.G = G;
+  s.ldg = x.D.out[p];
+  s.q4 = base->w[p].q4;
+  s.scale = base->w[p].scale;
+  s.N = x.D.out[p];
+  s.lora_du = adapted(x, p) ? ldu(x, p) : nullptr;
+  s.lora_A = adapted(x, p) ? lora->A[p] : nullptr;
+  return s;
+}
+
+// u_p = X A_p^T for each adapted projection p in `ps` (LoRA down-projection)
+hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const bf16* X, int K, std::initializer_list<int> ps) {
+  for (int p : ps) {
+    if (!adapted(x, p)) continue;
+    hipError_t e = launch_lora_rows(X, K, x.D.N, K, lora->A[p], 0, x.D.r, 1.0f, lu(x, p), x.st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// LoRA backward of projection p with output gradient G (bf16 [N][out]) and input X
+// (bf16 [N][in]): du = s G B, dB = s G^T u, dA = du^T X.
+hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_lora_grad* grads, int p,
+                    const bf16* G, const bf16* X) {
+  if (!adapted(x, p)) return hipSuccess;
+  const Dims& D = x.D;
+  const int splits = lora_outer_splits(D.N);
+  float* part = slot<float>(x.ws, x.L, S_PART);
+  hipError_t e = launch_lora_rows(G, D.out[p], D.N, D.out[p], lora->B[p], 1, D.r, D.s, ldu(x, p), x.st);
+  if (e != hipSuccess) return e;
+  e = launch_lora_outer(G, D.out[p], D.N, D.out[p], lu(x, p), D.r, D.s, grads->dB[p], 0, part, splits, x.st);
+  if (e != hipSuccess) return e;
+  return launch_lora_outer(X, D.in[p], D.N, D.in[p], ldu(x, p), D.r, 1.0f, grads->dA[p], 1, part, splits, x.st);
+}
+
+// Forward of one layer. keep=false: full forward to x_out. keep=true: recompute for the
+// backward (stops after z and its LoRA down-projection; x_out unused).
+int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora, const float* x_in,
+                  float* x_out, const float* rope, bool keep) {
+  const mebp_config* c = x.c;
+  const Dims& D = x.D;
+  bf16* a = slot<bf16>(x.ws, x.L, S_A);
+  bf16* q = slot<bf16>(x.ws, x.L, S_Q);
+  bf16* k = slot<bf16>(x.ws, x.L, S_K);
+  bf16* v = slot<bf16>(x.ws, x.L, S_V);
+  bf16* o = slot<bf16>(x.ws, x.L, S_O);
+  float* h = slot<float>(x.ws, x.L, S_H);
+  bf16* cc = slot<bf16>(x.ws, x.L, S_C);
+  bf16* g = slot<bf16>(x.ws, x.L, S_G);
+  bf16* u = slot<bf16>(x.ws, x.L, S_U);
+  bf16* z = slot<bf16>(x.ws, x.L, S_Z);
+
+  HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
+  HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}));
+  NtSeg qkv[3] = {nt_seg(x, base, lora, MEBP_Q, q, D.qd, nullptr, 0), nt_seg(x, base, lora, MEBP_K, k, D.kvd, nullptr, 0),
+                  nt_seg(x, base, lora, MEBP_V, v, D.kvd, nullptr, 0)};
+  HIP_TRY(run_nt(x, a, D.d, 3, qkv, NT_STORE_BF16));
+  HIP_TRY(launch_rope_fwd(q, D.qd, x.B, x.T, c->n_heads, c->head_dim, rope, x.st));
+  HIP_TRY(launch_rope_fwd(k, D.kvd, x.B, x.T, c->n_kv_heads, c->head_dim, rope, x.st));
+  AttnArgs at{};
+  at.q = q; at.k = k; at.v = v; at.ldq = D.qd; at.ldk = D.kvd;
+  at.B = x.B; at.T = x.T; at.Hq = c->n_heads; at.Hkv = c->n_kv_heads; at.dh = c->head_dim;
+  at.window = is_global(c, l) ? 0 : c->window;
+  at.o = o; at.lse = slot<float>(x.ws, x.L, S_LSE);
+  HIP_TRY(launch_attn_fwd(at, x.st));
+  HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}));
+  NtSeg os[1] = {nt_seg(x, base, lora, MEBP_O, h, D.d, x_in, D.d)};
+  HIP_TRY(run_nt(x, o, D.qd, 1, os, NT_STORE_F32));
+  HIP_TRY(launch_rmsnorm_fwd(h, base->norm_mlp, D.N, D.d, c->rms_eps, cc, nullptr, x.st));
+  HIP_TRY(lora_down(x, lora, cc, D.d, {MEBP_GATE, MEBP_UP}));
+  NtSeg gu[2] = {nt_seg(x, base, lora, MEBP_GATE, g, D.F, nullptr, 0), nt_seg(x, base, lora, MEBP_UP, u, D.F, nullptr, 0)};
+  HIP_TRY(run_nt(x, cc, D.d, 2, gu, NT_STORE_BF16));
+  HIP_TRY(launch_act_fwd(g, u, z, (size_t)D.N * D.F, c->act, x.st));
+  HIP_TRY(lora_down(x, lora, z, D.F, {MEBP_DOWN}));
+  if (!keep) {
+    NtSeg ds[1] = {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)};
+    HIP_TRY(run_nt(x, z, D.F, 1, ds, NT_STORE_F32));
+  }
+  return MEBP_OK;
+}
+
+int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora,
+                   const float* x_ckpt, const float* dy, float* dx, const mebp_layer_lora_grad* grads,
+                   const float* rope) {
+  const mebp_config* c = x.c;
+  const Dims& D = x.D;
+  int e = layer_forward(x, l, base, lora, x_ckpt, nullptr, rope, true);
+  if (e) return e;
+  bf16* a = slot<bf16>(x.ws, x.L, S_A);
+  bf16* q = slot<bf16>(x.ws, x.L, S_Q);
+  bf16* k = slot<bf16>(x.ws, x.L, S_K);
+  bf16* v = slot<bf16>(x.ws, x.L, S_V);
+  bf16* o = slot<bf16>(x.ws, x.L, S_O);
+  float* h = slot<float>(x.ws, x.L, S_H);
+  bf16* cc = slot<bf16>(x.ws, x.L, S_C);
+  bf16* g = slot<bf16>(x.ws, x.L, S_G);
+  bf16* u = slot<bf16>(x.ws, x.L, S_U);
+  bf16* z = slot<bf16>(x.ws, x.L, S_Z);
+  bf16* dyb = slot<bf16>(x.ws, x.L, S_DYB);
+  float* dc = slot<float>(x.ws, x.L, S_DC);
+  float* dh = slot<float>(x.ws, x.L, S_DH);
+  bf16* dhb = slot<bf16>(x.ws, x.L, S_DHB);
+  bf16* dO = slot<bf16>(x.ws, x.L, S_DO);
+  bf16* dq = slot<bf16>(x.ws, x.L, S_DQ);
+  bf16* dk = slot<bf16>(x.ws, x.L, S_DK);
+  bf16* dv = slot<bf16>(x.ws, x.L, S_DV);
+  float* da = slot<float>(x.ws, x.L, S_DA);
+
+  // y = h + down(z)
+  HIP_TRY(launch_f32_to_bf16(dy, dyb, (size_t)D.N * D.d, x.st));
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_DOWN, dyb, z));
+  {
+    TnArgs t{};
+    t.M = D.N; t.Kout = D.F; t.nseg = 1; t.r = D.r;
+    t.seg[0] = tn_seg(x, base, lora, MEBP_DOWN, dyb);
+    t.g = g; t.u = u; t.ldgu = D.F; t.act = c->act;
+    HIP_TRY(launch_gemm_tn(t, TN_ACT_BWD, TN_A_BF16, x.st));  // g <- dg, u <- d(up)
+  }
+  // z = act(gate(c)) * up(c)
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_GATE, g, cc));
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_UP, u, cc));
+  {
+    TnArgs t{};
+    t.M = D.N; t.Kout = D.d; t.nseg = 2; t.r = D.r;
+    t.seg[0] = tn_seg(x, base, lora, MEBP_GATE, g);
+    t.seg[1] = tn_seg(x, base, lora, MEBP_UP, u);
+    t.out = dc; t.ldo = D.d;
+    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
+  }
+  // c = RMSNorm(h); h = x + o(O)
+  HIP_TRY(launch_rmsnorm_bwd(h, base->norm_mlp, dc, dy, D.N, D.d, c->rms_eps, dh, dhb, x.st));
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_O, dhb, o));
+  {
+    TnArgs t{};
+    t.M = D.N; t.Kout = D.qd; t.nseg = 1; t.r = D.r;
+    t.seg[0] = tn_seg(x, base, lora, MEBP_O, dhb);
+    t.outb = dO; t.ldo = D.qd;
+    HIP_TRY(launch_gemm_tn(t, TN_STORE_BF16, TN_A_BF16, x.st));
+  }
+  // attention (RoPE backward fused into the dq / dk stores)
+  {
+    AttnArgs at{};
+    at.q = q; at.k = k; at.v = v; at.ldq = D.qd; at.ldk = D.kvd;
+    at.B = x.B; at.T = x.T; at.Hq = c->n_heads; at.Hkv = c->n_kv_heads; at.dh = c->head_dim;
+    at.window = is_global(c, l) ? 0 : c->window;
+    at.o = o; at.lse = slot<float>(x.ws, x.L, S_LSE);
+    at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
+    HIP_TRY(launch_attn_bwd(at, slot<float>(x.ws, x.L, S_DELTA), x.st));
+  }
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_Q, dq, a));
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_K, dk, a));
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_V, dv, a));
+  if (dx) {
+    TnArgs t{};
+    t.M = D.N; t.Kout = D.d; t.nseg = 3; t.r = D.r;
+    t.seg[0] = tn_seg(x, base, lora, MEBP_Q, dq);
+    t.seg[1] = tn_seg(x, base, lora, MEBP_K, dk);
+    t.seg[2] = tn_seg(x, base, lora, MEBP_V, dv);
+    t.out = da; t.ldo = D.d;
+    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
+    // a = RMSNorm(x): dx = dh + rmsnorm_bwd(x, da)  (dx may alias dy: dy is no longer read)
+    HIP_TRY(launch_rmsnorm_bwd(x_ckpt, base->norm_attn, da, dh, D.N, D.d, c->rms_eps, dx, nullptr, x.st));
+  }
+  return MEBP_OK;
+}
+
+int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const float* x_last, const int32_t* ids,
+            float* loss, float* dx_last) {
+  const mebp_config* c = x.c;
+  const Dims& D = x.D;
+  const int V = c->vocab;
+  int32_t* tgt = slot<int32_t>(x.ws, x.L, S_TGT);
+  bf16* hf = slot<bf16>(x.ws, x.L, S_HF);
+  _Float16* logits = slot<_Float16>(x.ws, x.L, S_LOGITS);
+  float2* stats = slot<float2>(x.ws, x.L, S_STATS);
+  float* lse = slot<float>(x.ws, x.L, S_LSEV);
+  float* tl = slot<float>(x.ws, x.L, S_TGTLOGIT);
+  float* rl = slot<float>(x.ws, x.L, S_ROWLOSS);
+  float* dhf = slot<float>(x.ws, x.L, S_DHF);
+  float* part = slot<float>(x.ws, x.L, S_LMPART);
+  const float inv_n = 1.0f / (float)((long long)x.B * (x.T - 1));
+
+  HIP_TRY(launch_targets(ids, x.B, x.T, c->vocab, tgt, x.st));
+  HIP_TRY(launch_rmsnorm_fwd(x_last, norm_final, D.N, D.d, c->rms_eps, hf, nullptr, x.st));
+  {
+    NtArgs a{};
+    a.X = hf; a.lda = D.d; a.M = D.N; a.K = D.d; a.nseg = 1;
+    a.seg[0].q4 = emb->q4; a.seg[0].scale = emb->scale; a.seg[0].N = V; a.seg[0].tile0 = 0;
+    a.seg[0].out = logits; a.seg[0].ldo = V;
+    a.stats = stats; a.tgt = tgt; a.tgt_logit = tl; a.ntiles = x.L.ntiles;
+    HIP_TRY(launch_gemm_nt(a, NT_LOGITS, x.st));
+  }
+  HIP_TRY(launch_ce_rows(stats, x.L.ntiles, tl, tgt, D.N, lse, rl, x.st));
+  HIP_TRY(launch_ce_loss(rl, tgt, D.N, inv_n, loss, x.st));
+  {
+    TnArgs t{};
+    t.M = D.N; t.Kout = D.d; t.nseg = 1; t.r = 0;
+    t.seg[0].G = (const bf16*)logits; t.seg[0].ldg = V;
+    t.seg[0].q4 = emb->q4; t.seg[0].scale = emb->scale; t.seg[0].N = V;
+    t.out = part; t.ldo = D.d; t.splits = x.L.lm_splits;
+    t.lse = lse; t.tgt = tgt;
+    HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_SOFTMAX, x.st));
+  }
+  HIP_TRY(launch_ce_dh_reduce(part, x.L.lm_splits, D.N, D.d, emb->q4, emb->scale, tgt, inv_n, dhf, x.st));
+  HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, D.N, D.d, c->rms_eps, dx_last, nullptr, x.st));
+  return MEBP_OK;
+}
+
+Ctx make_ctx(const mebp_config* c, int B, int T, void* ws, mebp_stream_t stream) {
+  Ctx x;
+  x.c = c;
+  x.D = dims(c, B, T);
+  x.B = B;
+  x.T = T;
+  x.ws = ws;
+  make_layout(c, B, T, &x.L);
+  x.st = (hipStream_t)stream;
+  return x;
+}
+
+int rope_table(const Ctx& x, int l, float** out) {
+  const bool glob = is_global(x.c, l);
+  float* cs = slot<float>(x.ws, x.L, glob ? S_ROPE_G : S_ROPE_L);
+  HIP_TRY(launch_rope_table(x.T, x.c->head_dim, glob ? x.c->rope_theta_global : x.c->rope_theta_local, cs, x.st));
+  *out = cs;
+  return MEBP_OK;
+}
+
+}  // namespace
+
+// ==================================================================== public entry points
+extern "C" {
+
+size_t mebp_workspace_bytes(const mebp_config* cfg, int32_t B, int32_t T) {
+  std::string saved = g_last_error;
+  if (check_config(cfg) || check_shape(B, T)) {
+    g_last_error = saved;
+    return 0;
+  }
+  Layout L;
+  make_layout(cfg, B, T, &L);
+  return L.total;
+}
+
+size_t mebp_workspace_offset(const mebp_config* cfg, int32_t B, int32_t T, int32_t s) {
+  if (s < 0 || s >= S_COUNT || check_config(cfg) || check_shape(B, T)) return (size_t)-1;
+  Layout L;
+  make_layout(cfg, B, T, &L);
+  return L.off[s];
+}
+
+const char* mebp_workspace_slot_name(int32_t s) { return (s >= 0 && s < S_COUNT) ? kSlotNames[s] : nullptr; }
+
+const char* mebp_last_error(void) { return g_last_error.c_str(); }
+
+int mebp_layer_forward_ckpt(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
+                            const mebp_layer_lora* lora, const float* x_in, float* x_out, int32_t B, int32_t T,
+                            void* ws, size_t ws_bytes, mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg)) || (e = check_shape(B, T)) || (e = check_layer(cfg, layer, base, lora)) ||
+      (e = check_act(x_in, "x_in")) || (e = check_act(x_out, "x_out")) || (e = check_ws(cfg, B, T, ws, ws_bytes)))
+    return e;
+  if (x_in == x_out) return fail(MEBP_EINVAL, "x_out must not alias x_in");
+  Ctx x = make_ctx(cfg, B, T, ws, stream);
+  float* rope;
+  if ((e = rope_table(x, layer, &rope))) return e;
+  return layer_forward(x, layer, base, lora, x_in, x_out, rope, false);
+}
+
+int mebp_layer_recompute_backward(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
+                                  const mebp_layer_lora* lora, const float* x_ckpt, const float* dy, float* dx,
+                                  const mebp_layer_lora_grad* grads, int32_t B, int32_t T, void* ws, size_t ws_bytes,
+                                  mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg)) || (e = check_shape(B, T)) || (e = check_layer(cfg, layer, base, lora)) ||
+      (e = check_act(x_ckpt, "x_ckpt")) || (e = check_act(dy, "dy")) || (e = check_grads(cfg, grads)) ||
+      (e = check_ws(cfg, B, T, ws, ws_bytes)))
+    return e;
+  if (dx && !aligned(dx, 16)) return fail(MEBP_EINVAL, "dx not 16-byte aligned");
+  if (dx && dx == x_ckpt) return fail(MEBP_EINVAL, "dx must not alias x_ckpt");
+  Ctx x = make_ctx(cfg, B, T, ws, stream);
+  float* rope;
+  if ((e = rope_table(x, layer, &rope))) return e;
+  return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
+}
+
+int mebp_lm_head_ce_backward(const mebp_config* cfg, const mebp_q4* emb, const float* norm_final,
+                             const float* x_last, const int32_t* ids, int32_t B, int32_t T, float* loss,
+                             float* dx_last, void* ws, size_t ws_bytes, mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg)) || (e = check_shape(B, T))) return e;
+  if (cfg->vocab <= 0) return fail(MEBP_EINVAL, "vocab must be > 0 for the LM head");
+  if (T < 2) return fail(MEBP_EINVAL, "T must be >= 2 (no next-token target otherwise)");
+  if ((e = check_q4(emb, "embedding")) || (e = check_act(norm_final, "norm_final")) ||
+      (e = check_act(x_last, "x_last")) || (e = check_act(dx_last, "dx_last")) || (e = check_ws(cfg, B, T, ws, ws_bytes)))
+    return e;
+  if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
+  if (!loss || !aligned(loss, 4)) return fail(MEBP_EINVAL, "loss NULL or misaligned");
+  Ctx x = make_ctx(cfg, B, T, ws, stream);
+  return lm_head(x, emb, norm_final, x_last, ids, loss, dx_last);
+}
+
+int mebp_embed(const mebp_config* cfg, const mebp_q4* emb, const int32_t* ids, int32_t B, int32_t T, float* x0,
+               mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg)) || (e = check_shape(B, T))) return e;
+  if (cfg->vocab <= 0) return fail(MEBP_EINVAL, "vocab must be > 0 for the embedding");
+  if ((e = check_q4(emb, "embedding")) || (e = check_act(x0, "x0"))) return e;
+  if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
+  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, B * T, cfg->vocab, x0, (hipStream_t)stream));
+  return MEBP_OK;
+}
+
+int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
+                    const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids, int32_t B, int32_t T,
+                    float* ckpt, float* loss, const mebp_layer_lora_grad* grads, float* dx0, void* ws,
+                    size_t ws_bytes, mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg)) || (e = check_shape(B, T))) return e;
+  if (cfg->vocab <= 0) return fail(MEBP_EINVAL, "vocab must be > 0 for a training step");
+  if (T < 2) return fail(MEBP_EINVAL, "T must be >= 2 (no next-token target otherwise)");
+  if (!layers || !lora) return fail(MEBP_EINVAL, "layers / lora array is NULL");
+  if (!grads && cfg->lora_mask) return fail(MEBP_EINVAL, "grads array is NULL");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    if ((e = check_layer(cfg, l, &layers[l], &lora[l]))) return e;
+    if ((e = check_grads(cfg, grads ? &grads[l] : nullptr))) return e;
+  }
+  if ((e = check_q4(emb, "embedding")) || (e = check_act(norm_final, "norm_final")) || (e = check_act(ckpt, "ckpt")) ||
+      (e = check_ws(cfg, B, T, ws, ws_bytes)))
+    return e;
+  if (dx0 && !aligned(dx0, 16)) return fail(MEBP_EINVAL, "dx0 not 16-byte aligned");
+  if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
+  if (!loss || !aligned(loss, 4)) return fail(MEBP_EINVAL, "loss NULL or misaligned");
+
+  Ctx x = make_ctx(cfg, B, T, ws, stream);
+  const size_t stride = (size_t)x.D.N * x.D.d;
+  float* rope_g = slot<float>(ws, x.L, S_ROPE_G);
+  float* rope_l = slot<float>(ws, x.L, S_ROPE_L);
+  HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_global, rope_g, x.st));
+  HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_local, rope_l, x.st));
+  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ckpt, x.st));
+  // forward loop: ckpt[l+1] = forward_l(ckpt[l])
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+    if ((e = layer_forward(x, l, &layers[l], &lora[l], ckpt + l * stride, ckpt + (l + 1) * stride, rope, false)))
+      return e;
+  }
+  // final linear + loss block
+  float* g = slot<float>(ws, x.L, S_GRAD);
+  if ((e = lm_head(x, emb, norm_final, ckpt + cfg->n_layers * stride, ids, loss, g))) return e;
+  // reverse loop: recompute layer l from ckpt[l], backpropagate the upstream gradient
+  for (int l = cfg->n_layers - 1; l >= 0; --l) {
+    const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+    float* dxl = l > 0 ? g : dx0;
+    if ((e = layer_backward(x, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr, rope)))
+      return e;
+  }
+  return MEBP_OK;
+}
+
+int mebp_dequant_q4(const mebp_q4* w, int32_t rows, int32_t cols, int32_t group, float* out_f32, uint16_t* out_bf16,
+                    mebp_stream_t stream) {
+  int e;
+  if ((e = check_q4(w, "weight"))) return e;
+  if (rows < 0 || cols < 0) return fail(MEBP_EINVAL, "negative size");
+  if (cols % 8) return fail(MEBP_EUNSUPPORTED, "cols %d not a multiple of 8", cols);
+  if (group != 32) return fail(MEBP_EUNSUPPORTED, "group %d != 32", group);
+  if (!out_f32 && !out_bf16) return fail(MEBP_EINVAL, "no output requested");
+  if ((out_f32 && !aligned(out_f32, 16)) || (out_bf16 && !aligned(out_bf16, 16)))
+    return fail(MEBP_EINVAL, "outputs must be 16-byte aligned");
+  HIP_TRY(launch_dequant(w->q4, w->scale, rows, cols, group, out_f32, out_bf16, (hipStream_t)stream));
+  return MEBP_OK;
+}
+
+}  // extern "C"

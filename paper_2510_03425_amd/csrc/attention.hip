@@ -1,0 +1,437 @@
+// Causal grouped-query attention with optional sliding window on gfx950 (bf16 MFMA,
+// fp32 softmax), forward and backward, flash-style: scores never reach HBM; the forward
+// keeps the row log-sum-exp for the backward.
+//
+// Layout trick used throughout: the 16x16 C tile of v_mfma_f32_16x16x32_bf16 gives lane l
+// the rows 4*(l/16)+r (r = 0..3) of column l%16. Two such tiles stacked along the rows
+// therefore hand lane l eight values of column l%16 at rows {4g..4g+3, 16+4g..16+4g+3}
+// (g = l/16) -- exactly an MFMA operand for a 32-deep reduction over those rows, up to a
+// fixed permutation of the reduction index. Softmax probabilities and their gradients are
+// fed from registers into the next product this way; the other operand is read from an
+// LDS tile stored reduction-contiguous (transposed at load time) with the same
+// permutation (two 8-byte reads per lane).
+//
+//  forward : S^T = K Q^T (A = K rows from LDS, B = Q rows kept in registers);
+//            O^T += V^T P^T (A = V^T from LDS, B = P from registers); row stats live in
+//            the lane of their query, so rescaling needs no cross-lane traffic.
+//  backward: dK/dV kernel owns a key block (GQA heads of a group summed in-kernel, no
+//            atomics); dQ kernel owns a query block. RoPE backward (rotation by minus the
+//            angle) is applied in both epilogues before the bf16 store.
+#include "device_common.h"
+#include "mebp_internal.h"
+
+namespace mebp {
+namespace {
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+// Row-major tile [R][C] of bf16 from global (row pitch ld, rows beyond `rows_ok` zero)
+// into LDS dst[R][C + pad]; 8-element chunks.
+template <int R, int C, int LD>
+DEV void load_tile_n(const bf16* src, size_t ld, int rows_ok, bf16* dst, int tid, int nthr) {
+  constexpr int CH = C / 8;
+  for (int i = tid; i < R * CH; i += nthr) {
+    const int r = i / CH, c = (i % CH) * 8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (r < rows_ok) v = *(const uint4*)(src + (size_t)r * ld + c);
+    *(uint4*)(dst + r * LD + c) = v;
+  }
+}
+
+// Transposed: global [R][C] -> LDS dst[C][R + pad]; each thread moves 8x8 blocks.
+template <int R, int C, int LD>
+DEV void load_tile_t(const bf16* src, size_t ld, int rows_ok, bf16* dst, int tid, int nthr) {
+  constexpr int RB = R / 8, CB = C / 8;
+  for (int b = tid; b < RB * CB; b += nthr) {
+    const int rb = b % RB, cb = b / RB;
+    uint32_t in[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = rb * 8 + i;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (r < rows_ok) v = *(const uint4*)(src + (size_t)r * ld + cb * 8);
+      in[i][0] = v.x; in[i][1] = v.y; in[i][2] = v.z; in[i][3] = v.w;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      uint4 o;
+      if (j & 1) {
+        o.x = perm_hi16(in[0][j >> 1], in[1][j >> 1]);
+        o.y = perm_hi16(in[2][j >> 1], in[3][j >> 1]);
+        o.z = perm_hi16(in[4][j >> 1], in[5][j >> 1]);
+        o.w = perm_hi16(in[6][j >> 1], in[7][j >> 1]);
+      } else {
+        o.x = perm_lo16(in[0][j >> 1], in[1][j >> 1]);
+        o.y = perm_lo16(in[2][j >> 1], in[3][j >> 1]);
+        o.z = perm_lo16(in[4][j >> 1], in[5][j >> 1]);
+        o.w = perm_lo16(in[6][j >> 1], in[7][j >> 1]);
+      }
+      *(uint4*)(dst + (cb * 8 + j) * LD + rb * 8) = o;
+    }
+  }
+}
+
+// A/B fragment from an LDS tile stored [row][k] (k contiguous): lane l reads
+// row row0 + l%16, k0 + 8*(l/16) .. +8.
+DEV bf16x8 frag_rows(const bf16* s, int ld, int row0, int k0, int lane) {
+  return *(const bf16x8*)(s + (row0 + (lane & 15)) * ld + k0 + 8 * (lane >> 4));
+}
+// Permuted fragment: row row0 + l%16, columns c0 + 4g .. +4 and c0 + 16 + 4g .. +4.
+DEV bf16x8 frag_perm(const bf16* s, int ld, int row0, int c0, int lane) {
+  const bf16* p = s + (row0 + (lane & 15)) * ld + c0 + 4 * (lane >> 4);
+  const uint2 a = *(const uint2*)p, b = *(const uint2*)(p + 16);
+  uint4 v = make_uint4(a.x, a.y, b.x, b.y);
+  return __builtin_bit_cast(bf16x8, v);
+}
+// Pack two C tiles (8 floats: tile0 rows r=0..3, tile1 rows r=0..3) into an operand.
+DEV bf16x8 pack_frag(const f32x4& t0, const f32x4& t1) {
+  uint4 v = make_uint4(pack_bf16x2(t0[0], t0[1]), pack_bf16x2(t0[2], t0[3]), pack_bf16x2(t1[0], t1[1]),
+                       pack_bf16x2(t1[2], t1[3]));
+  return __builtin_bit_cast(bf16x8, v);
+}
+DEV bf16x8 load_frag_global(const bf16* p, bool ok) {
+  uint4 v = ok ? *(const uint4*)p : make_uint4(0, 0, 0, 0);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// ------------------------------------------------------------------------------ forward
+template <int DH>
+__global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
+  constexpr int KB = 64, LDK = DH + 8, LDV = KB + 8, NKS = DH / 32, NT = DH / 16;
+  __shared__ __attribute__((aligned(16))) bf16 Ks[KB * LDK];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * LDV];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
+  const int q0 = blockIdx.x * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
+  const float sc = LOG2E / sqrtf((float)DH);
+  const size_t rowb = (size_t)b * T;
+
+  bf16x8 qf[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks)
+    qf[ks] = load_frag_global(a.q + (rowb + q) * a.ldq + h * DH + 32 * ks + 8 * (lane >> 4), q < T);
+  f32x4 oacc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) oacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_i = -1e30f, l_i = 0.f;
+
+  int kv_lo = 0;
+  if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
+  const int kv_hi = min(T, q0 + 64);
+  for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += KB) {
+    const bf16* kb = a.k + (rowb + kv0) * a.ldk + kvh * DH;
+    const bf16* vb = a.v + (rowb + kv0) * a.ldk + kvh * DH;
+    load_tile_n<KB, DH, LDK>(kb, a.ldk, T - kv0, Ks, tid, 256);
+    load_tile_t<KB, DH, LDV>(vb, a.ldk, T - kv0, Vt, tid, 256);
+    __syncthreads();
+    f32x4 s[4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) s[kt] = mfma16(frag_rows(Ks, LDK, kt * 16, ks * 32, lane), qf[ks], s[kt]);
+    }
+    float mloc = -1e30f;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kv0 + kt * 16 + 4 * (lane >> 4) + r;
+        const bool vis = key <= q && key < T && (a.window == 0 || q - key < a.window);
+        const float v = vis ? s[kt][r] * sc : -INFINITY;
+        s[kt][r] = v;
+        mloc = fmaxf(mloc, v);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m_i, mloc);
+    const float alpha = exp2f(m_i - m_new);
+    float ls = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = exp2f(s[kt][r] - m_new);
+        s[kt][r] = p;
+        ls += p;
+      }
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    l_i = l_i * alpha + ls;
+    m_i = m_new;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) oacc[t] *= alpha;
+#pragma unroll
+    for (int kp = 0; kp < 2; ++kp) {
+      const bf16x8 pf = pack_frag(s[2 * kp], s[2 * kp + 1]);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) oacc[t] = mfma16(frag_perm(Vt, LDV, t * 16, kp * 32, lane), pf, oacc[t]);
+    }
+    __syncthreads();
+  }
+  if (q < T) {
+    const float inv = 1.0f / l_i;
+    bf16* orow = a.o + (rowb + q) * a.ldq + h * DH;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int e = t * 16 + 4 * (lane >> 4);
+      *(uint2*)(orow + e) = make_uint2(pack_bf16x2(oacc[t][0] * inv, oacc[t][1] * inv),
+                                       pack_bf16x2(oacc[t][2] * inv, oacc[t][3] * inv));
+    }
+    if ((lane >> 4) == 0) a.lse[((size_t)b * a.Hq + h) * T + q] = (m_i + log2f(l_i)) / LOG2E;
+  }
+}
+
+// ------------------------------------------------------------------------------ backward
+// delta[b][h][t] = sum_e dO[b*T+t][h*dh+e] * O[b*T+t][h*dh+e]
+__global__ void k_attn_delta(const bf16* dO, const bf16* O, int ld, int B, int T, int H, int dh, float* delta) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (size_t)B * T * H) return;
+  const int h = (int)(i % H);
+  const size_t row = i / H;
+  const uint4* pa = (const uint4*)(dO + row * ld + h * dh);
+  const uint4* pb = (const uint4*)(O + row * ld + h * dh);
+  float acc = 0.f;
+  for (int c = 0; c < dh / 8; ++c) {
+    const uint4 x = pa[c], y = pb[c];
+    const uint32_t* xp = (const uint32_t*)&x;
+    const uint32_t* yp = (const uint32_t*)&y;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc += bf16_lo(xp[j]) * bf16_lo(yp[j]) + bf16_hi(xp[j]) * bf16_hi(yp[j]);
+  }
+  const int b = (int)(row / T), t = (int)(row % T);
+  delta[((size_t)b * H + h) * T + t] = acc;
+}
+
+// dK, dV for a block of 64 keys of one KV head; sums over the query heads of its group.
+template <int DH, int QB>
+__global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
+  constexpr int LDN = DH + 8, LDT_ = QB + 8, NKS = DH / 32, NT = DH / 16, NQT = QB / 16;
+  __shared__ __attribute__((aligned(16))) bf16 Qs[QB * LDN];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[QB * LDN];
+  __shared__ __attribute__((aligned(16))) bf16 Qt[DH * LDT_];
+  __shared__ __attribute__((aligned(16))) bf16 dOt[DH * LDT_];
+  __shared__ float lse_s[QB], del_s[QB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int T = a.T, kvh = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv;
+  const int k0 = blockIdx.x * 64, kw = k0 + 16 * w, key = kw + (lane & 15);
+  const float sc = LOG2E / sqrtf((float)DH);
+  const size_t rowb = (size_t)b * T;
+
+  bf16x8 kf[NKS], vf[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const size_t off = (rowb + key) * a.ldk + kvh * DH + 32 * ks + 8 * (lane >> 4);
+    kf[ks] = load_frag_global(a.k + off, key < T);
+    vf[ks] = load_frag_global(a.v + off, key < T);
+  }
+  f32x4 dk[NT], dv[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    dk[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    dv[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int q_lo = k0 & ~(QB - 1);
+  int q_hi = T;
+  if (a.window) q_hi = min(T, k0 + 64 + a.window - 1);
+  for (int hh = 0; hh < grp; ++hh) {
+    const int h = kvh * grp + hh;
+    for (int qb0 = q_lo; qb0 < q_hi; qb0 += QB) {
+      const bf16* qsrc = a.q + (rowb + qb0) * a.ldq + h * DH;
+      const bf16* dsrc = a.dO + (rowb + qb0) * a.ldq + h * DH;
+      load_tile_n<QB, DH, LDN>(qsrc, a.ldq, T - qb0, Qs, tid, 256);
+      load_tile_n<QB, DH, LDN>(dsrc, a.ldq, T - qb0, dOs, tid, 256);
+      load_tile_t<QB, DH, LDT_>(qsrc, a.ldq, T - qb0, Qt, tid, 256);
+      load_tile_t<QB, DH, LDT_>(dsrc, a.ldq, T - qb0, dOt, tid, 256);
+      if (tid < QB) {
+        const int qq = qb0 + tid;
+        const size_t si = ((size_t)b * a.Hq + h) * T + qq;
+        lse_s[tid] = qq < T ? a.lse[si] * LOG2E : 0.f;
+        del_s[tid] = qq < T ? a.delta[si] : 0.f;
+      }
+      __syncthreads();
+      f32x4 s[NQT], dp[NQT];
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) {
+        s[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        dp[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+          s[qt] = mfma16(frag_rows(Qs, LDN, qt * 16, ks * 32, lane), kf[ks], s[qt]);
+          dp[qt] = mfma16(frag_rows(dOs, LDN, qt * 16, ks * 32, lane), vf[ks], dp[qt]);
+        }
+      }
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ql = qt * 16 + 4 * (lane >> 4) + r, qq = qb0 + ql;
+          const bool vis = key <= qq && qq < T && key < T && (a.window == 0 || qq - key < a.window);
+          const float p = vis ? exp2f(s[qt][r] * sc - lse_s[ql]) : 0.f;
+          s[qt][r] = p;
+          dp[qt][r] = p * (dp[qt][r] - del_s[ql]);
+        }
+#pragma unroll
+      for (int qp = 0; qp < NQT / 2; ++qp) {
+        const bf16x8 pf = pack_frag(s[2 * qp], s[2 * qp + 1]);
+        const bf16x8 df = pack_frag(dp[2 * qp], dp[2 * qp + 1]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          dv[t] = mfma16(pf, frag_perm(dOt, LDT_, t * 16, qp * 32, lane), dv[t]);
+          dk[t] = mfma16(df, frag_perm(Qt, LDT_, t * 16, qp * 32, lane), dk[t]);
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // epilogue: lane holds rows key kw + 4g + r, column e = 16t + lane%16
+  const float scale = 1.0f / sqrtf((float)DH);
+  const int half = DH / 2;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int kk = kw + 4 * (lane >> 4) + r;
+    if (kk >= T) continue;
+    bf16* dvr = a.dv + (rowb + kk) * a.ldk + kvh * DH;
+    bf16* dkr = a.dk + (rowb + kk) * a.ldk + kvh * DH;
+#pragma unroll
+    for (int t = 0; t < NT / 2; ++t) {
+      const int e = t * 16 + (lane & 15);
+      const float2 cs = *(const float2*)(a.cs + 2 * ((size_t)kk * half + e));
+      const float d1 = dk[t][r] * scale, d2 = dk[t + NT / 2][r] * scale;
+      dkr[e] = to_bf16(d1 * cs.x + d2 * cs.y);
+      dkr[e + half] = to_bf16(d2 * cs.x - d1 * cs.y);
+      dvr[e] = to_bf16(dv[t][r]);
+      dvr[e + half] = to_bf16(dv[t + NT / 2][r]);
+    }
+  }
+}
+
+// dQ for a block of 64 queries of one head.
+template <int DH, int KB>
+__global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
+  constexpr int LDN = DH + 8, LDT_ = KB + 8, NKS = DH / 32, NT = DH / 16, NKT = KB / 16;
+  __shared__ __attribute__((aligned(16))) bf16 Ks[KB * LDN];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[KB * LDN];
+  __shared__ __attribute__((aligned(16))) bf16 Kt[DH * LDT_];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
+  const int q0 = blockIdx.x * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
+  const float sc = LOG2E / sqrtf((float)DH);
+  const size_t rowb = (size_t)b * T;
+
+  bf16x8 qf[NKS], dof[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const size_t off = (rowb + q) * a.ldq + h * DH + 32 * ks + 8 * (lane >> 4);
+    qf[ks] = load_frag_global(a.q + off, q < T);
+    dof[ks] = load_frag_global(a.dO + off, q < T);
+  }
+  const size_t si = ((size_t)b * a.Hq + h) * T + q;
+  const float lse2 = q < T ? a.lse[si] * LOG2E : 0.f;
+  const float del = q < T ? a.delta[si] : 0.f;
+  f32x4 dq[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) dq[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  int kv_lo = 0;
+  if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
+  const int kv_hi = min(T, q0 + 64);
+  for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += KB) {
+    const bf16* kb = a.k + (rowb + kv0) * a.ldk + kvh * DH;
+    const bf16* vb = a.v + (rowb + kv0) * a.ldk + kvh * DH;
+    load_tile_n<KB, DH, LDN>(kb, a.ldk, T - kv0, Ks, tid, 256);
+    load_tile_n<KB, DH, LDN>(vb, a.ldk, T - kv0, Vs, tid, 256);
+    load_tile_t<KB, DH, LDT_>(kb, a.ldk, T - kv0, Kt, tid, 256);
+    __syncthreads();
+    f32x4 s[NKT], dp[NKT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+      s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        s[kt] = mfma16(frag_rows(Ks, LDN, kt * 16, ks * 32, lane), qf[ks], s[kt]);
+        dp[kt] = mfma16(frag_rows(Vs, LDN, kt * 16, ks * 32, lane), dof[ks], dp[kt]);
+      }
+    }
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kv0 + kt * 16 + 4 * (lane >> 4) + r;
+        const bool vis = key <= q && key < T && q < T && (a.window == 0 || q - key < a.window);
+        const float p = vis ? exp2f(s[kt][r] * sc - lse2) : 0.f;
+        dp[kt][r] = p * (dp[kt][r] - del);
+      }
+#pragma unroll
+    for (int kp = 0; kp < NKT / 2; ++kp) {
+      const bf16x8 df = pack_frag(dp[2 * kp], dp[2 * kp + 1]);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) dq[t] = mfma16(frag_perm(Kt, LDT_, t * 16, kp * 32, lane), df, dq[t]);
+    }
+    __syncthreads();
+  }
+  if (q < T) {
+    // lane holds dQ^T rows e = 16t + 4g + r of query q; pairs (e, e + dh/2) share the lane
+    const float scale = 1.0f / sqrtf((float)DH);
+    const int half = DH / 2;
+    bf16* dqr = a.dq + (rowb + q) * a.ldq + h * DH;
+#pragma unroll
+    for (int t = 0; t < NT / 2; ++t) {
+      float lo[4], hi[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int e = t * 16 + 4 * (lane >> 4) + r;
+        const float2 cs = *(const float2*)(a.cs + 2 * ((size_t)q * half + e));
+        const float d1 = dq[t][r] * scale, d2 = dq[t + NT / 2][r] * scale;
+        lo[r] = d1 * cs.x + d2 * cs.y;
+        hi[r] = d2 * cs.x - d1 * cs.y;
+      }
+      const int e0 = t * 16 + 4 * (lane >> 4);
+      *(uint2*)(dqr + e0) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+      *(uint2*)(dqr + e0 + half) = make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st) {
+  dim3 grid((a.T + 63) / 64, a.Hq, a.B);
+  switch (a.dh) {
+    case 64: hipLaunchKernelGGL(k_attn_fwd<64>, grid, dim3(256), 0, st, a); break;
+    case 128: hipLaunchKernelGGL(k_attn_fwd<128>, grid, dim3(256), 0, st, a); break;
+    case 256: hipLaunchKernelGGL(k_attn_fwd<256>, grid, dim3(256), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, hipStream_t st) {
+  const size_t nd = (size_t)a0.B * a0.T * a0.Hq;
+  hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd + 255) / 256)), dim3(256), 0, st, a0.dO, (const bf16*)a0.o,
+                     a0.ldq, a0.B, a0.T, a0.Hq, a0.dh, delta_ws);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  AttnArgs a = a0;
+  a.delta = delta_ws;
+  dim3 gkv((a.T + 63) / 64, a.Hkv, a.B), gq((a.T + 63) / 64, a.Hq, a.B);
+  switch (a.dh) {
+    case 64:
+      hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a);
+      hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, st, a);
+      break;
+    case 128:
+      hipLaunchKernelGGL((k_attn_bwd_dkdv<128, 64>), gkv, dim3(256), 0, st, a);
+      hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, st, a);
+      break;
+    case 256:
+      hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a);
+      hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, st, a);
+      break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mebp

@@ -1,0 +1,82 @@
+// Device-side helpers shared by the gfx950 kernels of libmebp.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define DEV static __device__ __forceinline__
+
+DEV int lane_id() { return threadIdx.x & 63; }
+
+// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+DEV bf16 to_bf16(float x) { return (bf16)x; }
+DEV float bf2f(bf16 x) { return (float)x; }
+DEV uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 p = {(bf16)lo, (bf16)hi};
+  return __builtin_bit_cast(uint32_t, p);
+}
+DEV float bf16_lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
+DEV float bf16_hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xffff0000u); }
+DEV float half_bits_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+
+// One 16x16x32 bf16 MFMA: D = A(16x32) * B(32x16) + C.
+// Lane l supplies A[l%16][8*(l/16) .. +8] and B[8*(l/16) .. +8][l%16];
+// lane l receives D[4*(l/16) + r][l%16], r = 0..3.
+DEV f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Decompress 8 int4 codes (one dword, element i in bits [4i, 4i+4)) times scale s into
+// 8 bf16 (4 dwords, element 2j in the low half of dword j). The product q*s is exact in
+// fp32; the bf16 conversion rounds to nearest even.
+DEV uint4 dequant8(uint32_t w, float s) {
+  float f[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = (float)__builtin_amdgcn_sbfe(w, 4 * i, 4) * s;
+  uint4 r;
+  r.x = pack_bf16x2(f[0], f[1]);
+  r.y = pack_bf16x2(f[2], f[3]);
+  r.z = pack_bf16x2(f[4], f[5]);
+  r.w = pack_bf16x2(f[6], f[7]);
+  return r;
+}
+
+DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// 16-bit element transpose helpers: select the low (or high) halves of two dwords.
+DEV uint32_t perm_lo16(uint32_t a, uint32_t b) {  // (a.lo, b.lo) -> lo=a.lo, hi=b.lo
+  return __builtin_amdgcn_perm(b, a, 0x05040100u);
+}
+DEV uint32_t perm_hi16(uint32_t a, uint32_t b) {  // (a.hi, b.hi) -> lo=a.hi, hi=b.hi
+  return __builtin_amdgcn_perm(b, a, 0x07060302u);
+}
+
+DEV float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+DEV float gelu_tanh_f(float g) {
+  const float c = 0.7978845608028654f;
+  return 0.5f * g * (1.0f + tanhf(c * (g + 0.044715f * g * g * g)));
+}
+DEV float act_f(float g, int kind) { return kind == 0 ? silu_f(g) : gelu_tanh_f(g); }
+DEV float act_grad_f(float g, int kind) {
+  if (kind == 0) {
+    float s = 1.0f / (1.0f + __expf(-g));
+    return s * (1.0f + g * (1.0f - s));
+  }
+  const float c = 0.7978845608028654f;
+  float t = tanhf(c * (g + 0.044715f * g * g * g));
+  return 0.5f * (1.0f + t) + 0.5f * g * (1.0f - t * t) * c * (1.0f + 3.0f * 0.044715f * g * g);
+}

@@ -1,0 +1,444 @@
+// Memory-bound kernels of the checkpointed LoRA step on gfx950: decompression and
+// embedding gather, RMSNorm forward/backward, RoPE, gated activation, the rank-r LoRA
+// projections and weight gradients, and the cross-entropy reductions of the final block.
+// All reductions run in a fixed order (no atomics), so results are bit-reproducible.
+#include "device_common.h"
+#include "mebp_internal.h"
+
+namespace mebp {
+namespace {
+
+// ------------------------------------------------------------------ decompression
+// out[r][c] = q[r][c] * s[r][c/group]; one thread per 8 codes (one dword).
+__global__ void k_dequant(const uint8_t* q4, const uint16_t* scale, int rows, int cols, int group,
+                          float* out_f32, uint16_t* out_bf16) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t per_row = cols >> 3;
+  if (i >= (size_t)rows * per_row) return;
+  const size_t r = i / per_row;
+  const int c = (int)(i % per_row) * 8;
+  const int ng = (cols + group - 1) / group;
+  const uint32_t w = *(const uint32_t*)(q4 + r * (cols >> 1) + (c >> 1));
+  const float s = half_bits_to_f32(scale[r * ng + c / group]);
+  float f[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (float)__builtin_amdgcn_sbfe(w, 4 * j, 4) * s;
+  if (out_f32) {
+    float4* o = (float4*)(out_f32 + r * cols + c);
+    o[0] = make_float4(f[0], f[1], f[2], f[3]);
+    o[1] = make_float4(f[4], f[5], f[6], f[7]);
+  }
+  if (out_bf16) {
+    uint4 v = make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                         pack_bf16x2(f[6], f[7]));
+    *(uint4*)(out_bf16 + r * cols + c) = v;
+  }
+}
+
+// x0[n][:] = E[ids[n]][:] decompressed to fp32; one thread per 8 codes.
+// An id outside [0, V) yields a NaN row instead of an out-of-bounds read.
+__global__ void k_embed(const uint8_t* q4, const uint16_t* scale, int d, int group, const int32_t* ids,
+                        int n, int V, float* x0) {
+  const int per_row = d >> 3;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (size_t)n * per_row) return;
+  const int row = (int)(i / per_row), c = (int)(i % per_row) * 8;
+  const int id = ids[row];
+  if (id < 0 || id >= V) {
+    float4* o = (float4*)(x0 + (size_t)row * d + c);
+    o[0] = o[1] = make_float4(NAN, NAN, NAN, NAN);
+    return;
+  }
+  const size_t v = (size_t)id;
+  const int ng = (d + group - 1) / group;
+  const uint32_t w = *(const uint32_t*)(q4 + v * (d >> 1) + (c >> 1));
+  const float s = half_bits_to_f32(scale[v * ng + c / group]);
+  float f[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (float)__builtin_amdgcn_sbfe(w, 4 * j, 4) * s;
+  float4* o = (float4*)(x0 + (size_t)row * d + c);
+  o[0] = make_float4(f[0], f[1], f[2], f[3]);
+  o[1] = make_float4(f[4], f[5], f[6], f[7]);
+}
+
+// ------------------------------------------------------------------ RMSNorm
+// One wave per row, float4 accesses (d % 4 == 0).
+__global__ __launch_bounds__(256) void k_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps,
+                                                     bf16* y, float* rstd_out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const float4* xr = (const float4*)(x + (size_t)row * d);
+  const int d4 = d >> 2;
+  float ss = 0.f;
+  for (int c = lane; c < d4; c += 64) {
+    const float4 v = xr[c];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+  if (rstd_out && lane == 0) rstd_out[row] = rs;
+  const float4* wr = (const float4*)w;
+  uint2* yr = (uint2*)(y + (size_t)row * d);
+  for (int c = lane; c < d4; c += 64) {
+    const float4 v = xr[c], g = wr[c];
+    yr[c] = make_uint2(pack_bf16x2(v.x * rs * g.x, v.y * rs * g.y), pack_bf16x2(v.z * rs * g.z, v.w * rs * g.w));
+  }
+}
+
+// dx = resid + rstd * (w*dy - xhat * mean(xhat*w*dy)), xhat = x*rstd (weight frozen).
+__global__ __launch_bounds__(256) void k_rmsnorm_bwd(const float* x, const float* w, const float* dy,
+                                                     const float* resid, int n, int d, float eps, float* dx,
+                                                     bf16* dxb) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const size_t off = (size_t)row * d;
+  const float4* xr = (const float4*)(x + off);
+  const float4* gr = (const float4*)(dy + off);
+  const float4* wr = (const float4*)w;
+  const int d4 = d >> 2;
+  float ss = 0.f, sd = 0.f;
+  for (int c = lane; c < d4; c += 64) {
+    const float4 v = xr[c], g = gr[c], ww = wr[c];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    sd += v.x * ww.x * g.x + v.y * ww.y * g.y + v.z * ww.z * g.z + v.w * ww.w * g.w;
+  }
+  ss = wave_sum(ss);
+  sd = wave_sum(sd);
+  const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+  const float mean_term = rs * sd / (float)d;  // mean(xhat * w * dy)
+  const float4* rr = (const float4*)(resid ? resid + off : nullptr);
+  float4* o = (float4*)(dx + off);
+  uint2* ob = dxb ? (uint2*)(dxb + off) : nullptr;
+  for (int c = lane; c < d4; c += 64) {
+    const float4 v = xr[c], g = gr[c], ww = wr[c];
+    float4 res = rr ? rr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    res.x += rs * (ww.x * g.x - v.x * rs * mean_term);
+    res.y += rs * (ww.y * g.y - v.y * rs * mean_term);
+    res.z += rs * (ww.z * g.z - v.z * rs * mean_term);
+    res.w += rs * (ww.w * g.w - v.w * rs * mean_term);
+    o[c] = res;
+    if (ob) ob[c] = make_uint2(pack_bf16x2(res.x, res.y), pack_bf16x2(res.z, res.w));
+  }
+}
+
+__global__ void k_f32_to_bf16(const float* x, bf16* y, size_t n4) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  const float4 v = ((const float4*)x)[i];
+  ((uint2*)y)[i] = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+}
+
+// ------------------------------------------------------------------ RoPE
+// cs[t][i] = (cos, sin)(t * theta^(-2i/dh)), computed in fp64.
+__global__ void k_rope_table(int T, int dh, double theta, float* cs) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int half = dh >> 1;
+  if (i >= T * half) return;
+  const int t = i / half, j = i % half;
+  const double inv = pow(theta, -(2.0 * j) / (double)dh);
+  const double ang = (double)t * inv;
+  cs[2 * i] = (float)cos(ang);
+  cs[2 * i + 1] = (float)sin(ang);
+}
+
+// In place: pairs (e, e + dh/2) of every head rotate by the angle of (t, e).
+__global__ void k_rope_fwd(bf16* x, int ld, int B, int T, int H, int dh, const float* cs) {
+  const int half = dh >> 1;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t total = (size_t)B * T * H * half;
+  if (i >= total) return;
+  const int e = (int)(i % half);
+  const int h = (int)((i / half) % H);
+  const size_t row = i / ((size_t)half * H);
+  const int t = (int)(row % T);
+  bf16* p = x + row * ld + h * dh;
+  const float x1 = bf2f(p[e]), x2 = bf2f(p[e + half]);
+  const float c = cs[2 * (t * half + e)], s = cs[2 * (t * half + e) + 1];
+  p[e] = to_bf16(x1 * c - x2 * s);
+  p[e + half] = to_bf16(x2 * c + x1 * s);
+}
+
+// z = act(g) * u, 8 elements per thread
+__global__ void k_act_fwd(const bf16* g, const bf16* u, bf16* z, size_t n8, int act) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n8) return;
+  const uint4 gv = ((const uint4*)g)[i], uv = ((const uint4*)u)[i];
+  const uint32_t* gp = (const uint32_t*)&gv;
+  const uint32_t* up = (const uint32_t*)&uv;
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    o[j] = pack_bf16x2(act_f(bf16_lo(gp[j]), act) * bf16_lo(up[j]), act_f(bf16_hi(gp[j]), act) * bf16_hi(up[j]));
+  ((uint4*)z)[i] = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// ------------------------------------------------------------------ LoRA
+// out[m][j] = s * sum_k X[m][k] * W(j,k). Workgroup: ROWS = 256/r rows x r outputs.
+constexpr int LR_KC = 128;
+__global__ __launch_bounds__(256) void k_lora_rows(const bf16* X, int ldx, int M, int K, const float* W, int wt,
+                                                   int r, float s, float* out) {
+  __shared__ float Xs[32][LR_KC + 1];
+  __shared__ float Ws[16][LR_KC + 1];
+  const int rows = 256 / r;
+  const int tid = threadIdx.x, lr = tid / r, j = tid % r;
+  const int m0 = blockIdx.x * rows;
+  float acc = 0.f;
+  for (int k0 = 0; k0 < K; k0 += LR_KC) {
+    for (int i = tid; i < rows * LR_KC; i += 256) {
+      const int rr = i / LR_KC, kk = i % LR_KC;
+      const int m = m0 + rr, k = k0 + kk;
+      Xs[rr][kk] = (m < M && k < K) ? bf2f(X[(size_t)m * ldx + k]) : 0.f;
+    }
+    for (int i = tid; i < r * LR_KC; i += 256) {
+      int jj, kk;
+      if (wt) { kk = i / r; jj = i % r; } else { jj = i / LR_KC; kk = i % LR_KC; }
+      const int k = k0 + kk;
+      Ws[jj][kk] = k < K ? (wt ? W[(size_t)k * r + jj] : W[(size_t)jj * K + k]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < LR_KC; ++kk) acc += Xs[lr][kk] * Ws[j][kk];
+    __syncthreads();
+  }
+  const int m = m0 + lr;
+  if (m < M) out[(size_t)m * r + j] = s * acc;
+}
+
+// part[split][c][j] = sum_{m in split} Mx[m][c] * V[m][j]; one thread per column c.
+constexpr int LO_MC = 64;
+__global__ __launch_bounds__(256) void k_lora_outer_part(const bf16* Mx, int ldm, int M, int C, const float* V,
+                                                         int r, int splits, float* part) {
+  __shared__ float4 Vs[LO_MC][4];
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int split = blockIdx.y;
+  const int mb = (int)((long long)M * split / splits), me = (int)((long long)M * (split + 1) / splits);
+  float acc[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) acc[j] = 0.f;
+  const int r4 = r >> 2;
+  for (int m0 = mb; m0 < me; m0 += LO_MC) {
+    const int mc = min(LO_MC, me - m0);
+    for (int i = threadIdx.x; i < LO_MC * r4; i += 256) {
+      const int mm = i / r4, q = i % r4;
+      Vs[mm][q] = mm < mc ? ((const float4*)(V + (size_t)(m0 + mm) * r))[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    __syncthreads();
+    if (c < C) {
+      for (int mm = 0; mm < mc; ++mm) {
+        const float x = bf2f(Mx[(size_t)(m0 + mm) * ldm + c]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (q < r4) {
+            const float4 v = Vs[mm][q];
+            acc[4 * q + 0] += x * v.x;
+            acc[4 * q + 1] += x * v.y;
+            acc[4 * q + 2] += x * v.z;
+            acc[4 * q + 3] += x * v.w;
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (c < C) {
+    float* p = part + ((size_t)split * C + c) * r;
+    for (int j = 0; j < r; ++j) p[j] = acc[j];
+  }
+}
+
+__global__ void k_lora_outer_reduce(const float* part, int splits, int C, int r, float s, float* out, int layout) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;  // index into out
+  if (i >= C * r) return;
+  int c, j;
+  if (layout == 0) { c = i / r; j = i % r; } else { j = i / C; c = i % C; }
+  float acc = 0.f;
+  for (int sp = 0; sp < splits; ++sp) acc += part[((size_t)sp * C + c) * r + j];
+  out[i] = s * acc;
+}
+
+// ------------------------------------------------------------------ cross-entropy
+// tgt[b*T+t] = ids[b][t+1] for t < T-1, -1 (no target) for t = T-1; an id outside
+// [0, V) becomes -2, which the loss turns into NaN instead of an out-of-bounds read.
+__global__ void k_targets(const int32_t* ids, int B, int T, int V, int32_t* tgt) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * T) return;
+  const int t = i % T;
+  int v = -1;
+  if (t < T - 1) {
+    v = ids[i + 1];
+    if (v < 0 || v >= V) v = -2;
+  }
+  tgt[i] = v;
+}
+
+// one wave per row: lse = M + log(sum s_i exp(m_i - M)); row_loss = lse - logit[target]
+__global__ __launch_bounds__(256) void k_ce_rows(const float2* stats, int ntiles, const float* tgt_logit,
+                                                 const int32_t* tgt, int M, float* lse, float* row_loss) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const float2* st = stats + (size_t)row * ntiles;
+  float mx = -INFINITY;
+  for (int i = lane; i < ntiles; i += 64) mx = fmaxf(mx, st[i].x);
+  mx = wave_max(mx);
+  float se = 0.f;
+  for (int i = lane; i < ntiles; i += 64) se += st[i].y * __expf(st[i].x - mx);
+  se = wave_sum(se);
+  if (lane == 0) {
+    const float l = mx + logf(se);
+    lse[row] = l;
+    const int tg = tgt[row];
+    row_loss[row] = tg >= 0 ? l - tgt_logit[row] : (tg == -1 ? 0.f : NAN);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_ce_loss(const float* row_loss, int M, float inv_n, float* loss) {
+  __shared__ float red[4];
+  float acc = 0.f;
+  for (int i = threadIdx.x; i < M; i += 256) acc += row_loss[i];
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) loss[0] = ((red[0] + red[1]) + (red[2] + red[3])) * inv_n;
+}
+
+// dhf[m][k] = inv_n * (sum_s part[s][m][k] - E[tgt[m]][k]) for rows with a target, else 0
+__global__ void k_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
+                               const uint16_t* escale, const int32_t* tgt, float inv_n, float* dhf) {
+  const int per_row = d >> 3;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (size_t)M * per_row) return;
+  const int m = (int)(i / per_row), c = (int)(i % per_row) * 8;
+  const int tg = tgt[m];
+  float o[8];
+  if (tg < 0) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = 0.f;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = 0.f;
+    for (int sp = 0; sp < splits; ++sp) {
+      const float4* p = (const float4*)(part + ((size_t)sp * M + m) * d + c);
+      const float4 a = p[0], b = p[1];
+      o[0] += a.x; o[1] += a.y; o[2] += a.z; o[3] += a.w;
+      o[4] += b.x; o[5] += b.y; o[6] += b.z; o[7] += b.w;
+    }
+    const int ng = (d + 31) >> 5;
+    const uint32_t w = *(const uint32_t*)(eq4 + (size_t)tg * (d >> 1) + (c >> 1));
+    const float s = half_bits_to_f32(escale[(size_t)tg * ng + (c >> 5)]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = inv_n * (o[j] - (float)__builtin_amdgcn_sbfe(w, 4 * j, 4) * s);
+  }
+  float4* out = (float4*)(dhf + (size_t)m * d + c);
+  out[0] = make_float4(o[0], o[1], o[2], o[3]);
+  out[1] = make_float4(o[4], o[5], o[6], o[7]);
+}
+
+__global__ void k_splitk_reduce(const float* part, int splits, size_t n4, float* out) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  float4 acc = ((const float4*)part)[i];
+  for (int s = 1; s < splits; ++s) {
+    const float4 v = ((const float4*)part)[(size_t)s * n4 + i];
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  ((float4*)out)[i] = acc;
+}
+
+inline unsigned blocks_for(size_t n, unsigned bs) { return (unsigned)((n + bs - 1) / bs); }
+
+}  // namespace
+
+hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, int cols, int group,
+                          float* out_f32, uint16_t* out_bf16, hipStream_t st) {
+  const size_t n = (size_t)rows * (cols >> 3);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_dequant, dim3(blocks_for(n, 256)), dim3(256), 0, st, q4, scale, rows, cols, group, out_f32,
+                     out_bf16);
+  return hipGetLastError();
+}
+hipError_t launch_embed(const uint8_t* q4, const uint16_t* scale, int d, int group, const int32_t* ids, int n,
+                        int V, float* x0, hipStream_t st) {
+  const size_t tot = (size_t)n * (d >> 3);
+  hipLaunchKernelGGL(k_embed, dim3(blocks_for(tot, 256)), dim3(256), 0, st, q4, scale, d, group, ids, n, V, x0);
+  return hipGetLastError();
+}
+hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, bf16* y, float* rstd,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(k_rmsnorm_fwd, dim3(blocks_for(n, 4)), dim3(256), 0, st, x, w, n, d, eps, y, rstd);
+  return hipGetLastError();
+}
+hipError_t launch_rmsnorm_bwd(const float* x, const float* w, const float* dy, const float* resid, int n, int d,
+                              float eps, float* dx, bf16* dxb, hipStream_t st) {
+  hipLaunchKernelGGL(k_rmsnorm_bwd, dim3(blocks_for(n, 4)), dim3(256), 0, st, x, w, dy, resid, n, d, eps, dx, dxb);
+  return hipGetLastError();
+}
+hipError_t launch_f32_to_bf16(const float* x, bf16* y, size_t n, hipStream_t st) {
+  const size_t n4 = n >> 2;
+  hipLaunchKernelGGL(k_f32_to_bf16, dim3(blocks_for(n4, 256)), dim3(256), 0, st, x, y, n4);
+  return hipGetLastError();
+}
+hipError_t launch_rope_table(int T, int dh, double theta, float* cs, hipStream_t st) {
+  hipLaunchKernelGGL(k_rope_table, dim3(blocks_for((size_t)T * (dh / 2), 256)), dim3(256), 0, st, T, dh, theta, cs);
+  return hipGetLastError();
+}
+hipError_t launch_rope_fwd(bf16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st) {
+  const size_t tot = (size_t)B * T * H * (dh / 2);
+  hipLaunchKernelGGL(k_rope_fwd, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, B, T, H, dh, cs);
+  return hipGetLastError();
+}
+hipError_t launch_act_fwd(const bf16* g, const bf16* u, bf16* z, size_t n, int act, hipStream_t st) {
+  const size_t n8 = n >> 3;
+  hipLaunchKernelGGL(k_act_fwd, dim3(blocks_for(n8, 256)), dim3(256), 0, st, g, u, z, n8, act);
+  return hipGetLastError();
+}
+hipError_t launch_lora_rows(const bf16* X, int ldx, int M, int K, const float* W, int wt, int r, float s, float* out,
+                            hipStream_t st) {
+  const int rows = 256 / r;
+  hipLaunchKernelGGL(k_lora_rows, dim3(blocks_for(M, rows)), dim3(256), 0, st, X, ldx, M, K, W, wt, r, s, out);
+  return hipGetLastError();
+}
+int lora_outer_splits(int M) {
+  int s = (M + 255) / 256;
+  return s < 1 ? 1 : (s > 64 ? 64 : s);
+}
+hipError_t launch_lora_outer(const bf16* Mx, int ldm, int M, int C, const float* V, int r, float s, float* out,
+                             int layout, float* part, int splits, hipStream_t st) {
+  hipLaunchKernelGGL(k_lora_outer_part, dim3(blocks_for(C, 256), splits), dim3(256), 0, st, Mx, ldm, M, C, V, r,
+                     splits, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_lora_outer_reduce, dim3(blocks_for((size_t)C * r, 256)), dim3(256), 0, st, part, splits, C, r,
+                     s, out, layout);
+  return hipGetLastError();
+}
+hipError_t launch_targets(const int32_t* ids, int B, int T, int V, int32_t* tgt, hipStream_t st) {
+  hipLaunchKernelGGL(k_targets, dim3(blocks_for((size_t)B * T, 256)), dim3(256), 0, st, ids, B, T, V, tgt);
+  return hipGetLastError();
+}
+hipError_t launch_ce_rows(const float2* stats, int ntiles, const float* tgt_logit, const int32_t* tgt, int M,
+                          float* lse, float* row_loss, hipStream_t st) {
+  hipLaunchKernelGGL(k_ce_rows, dim3(blocks_for(M, 4)), dim3(256), 0, st, stats, ntiles, tgt_logit, tgt, M, lse,
+                     row_loss);
+  return hipGetLastError();
+}
+hipError_t launch_ce_loss(const float* row_loss, const int32_t* tgt, int M, float inv_n, float* loss,
+                          hipStream_t st) {
+  (void)tgt;
+  hipLaunchKernelGGL(k_ce_loss, dim3(1), dim3(256), 0, st, row_loss, M, inv_n, loss);
+  return hipGetLastError();
+}
+hipError_t launch_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
+                               const uint16_t* escale, const int32_t* tgt, float inv_n, float* dhf,
+                               hipStream_t st) {
+  const size_t tot = (size_t)M * (d >> 3);
+  hipLaunchKernelGGL(k_ce_dh_reduce, dim3(blocks_for(tot, 256)), dim3(256), 0, st, part, splits, M, d, eq4, escale,
+                     tgt, inv_n, dhf);
+  return hipGetLastError();
+}
+hipError_t launch_splitk_reduce(const float* part, int splits, size_t n, float* out, hipStream_t st) {
+  const size_t n4 = n >> 2;
+  hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks_for(n4, 256)), dim3(256), 0, st, part, splits, n4, out);
+  return hipGetLastError();
+}
+
+}  // namespace mebp

@@ -1,0 +1,122 @@
+"""Host-only checks of the C ABI: the library loads, exports every function that
+include/mebp.h declares, and rejects invalid arguments before touching the GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from mebp_inputs import CONFIGS, MINI
+from paper_2510_03425_amd import _lib as L
+from paper_2510_03425_amd.device import make_config
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "mebp.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mebp_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_symbols_exported(built_lib):
+    names = header_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(built_lib, n), n
+    assert set(names) == set(L.EXPORTED)
+
+
+def test_struct_sizes_match_header(built_lib):
+    # mebp_config: 17 four-byte fields; the structs are arrays of pointers
+    assert C.sizeof(L.MebpConfig) == 17 * 4
+    assert C.sizeof(L.MebpQ4) == 16
+    assert C.sizeof(L.MebpLayerBase) == 7 * 16 + 16
+    assert C.sizeof(L.MebpLayerLora) == 14 * 8
+
+
+def test_workspace_bytes(built_lib):
+    for cfg in CONFIGS.values():
+        assert L.mebp_workspace_bytes(make_config(cfg), cfg.batch, cfg.seq) > 0
+    c = make_config(MINI)
+    small = L.mebp_workspace_bytes(c, 1, 64)
+    assert small < L.mebp_workspace_bytes(c, 2, 160)
+    assert L.mebp_workspace_bytes(c, 0, 64) == 0
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 96, L.MEBP_EUNSUPPORTED), ("hidden", 100, L.MEBP_EUNSUPPORTED),
+    ("n_kv_heads", 3, L.MEBP_EINVAL), ("group", 64, L.MEBP_EUNSUPPORTED),
+    ("lora_rank", 4, L.MEBP_EUNSUPPORTED), ("act", 5, L.MEBP_EINVAL), ("ffn", 100, L.MEBP_EUNSUPPORTED),
+    ("lora_mask", 1 << 9, L.MEBP_EINVAL), ("n_layers", 0, L.MEBP_EINVAL), ("vocab", 1000, L.MEBP_EUNSUPPORTED),
+])
+def test_config_rejected(built_lib, field, value, code):
+    c = make_config(MINI)
+    setattr(c, field, value)
+    r = L.mebp_layer_forward_ckpt(c, 0, None, None, 0, 0, 2, 160, 0, 0, 0, check=False)
+    assert r == code
+    assert L.mebp_last_error()
+
+
+def _fake_layer():
+    base = L.MebpLayerBase()
+    lora = L.MebpLayerLora()
+    for i in range(7):
+        base.w[i].q4 = 0x1000 * (i + 1)
+        base.w[i].scale = 0x1000 * (i + 1) + 0x800
+        lora.A[i] = 0x100000 + 0x1000 * i
+        lora.B[i] = 0x200000 + 0x1000 * i
+    base.norm_attn = 0x300000
+    base.norm_mlp = 0x300100
+    return base, lora
+
+
+def test_argument_errors_enqueue_nothing(built_lib):
+    c = make_config(MINI)
+    base, lora = _fake_layer()
+    need = L.mebp_workspace_bytes(c, 2, 160)
+    X, Y, WS = 0x400000, 0x800000, 0x1000000
+    f = lambda **kw: L.mebp_layer_forward_ckpt(
+        c, kw.get("layer", 0), kw.get("base", base), kw.get("lora", lora), kw.get("x", X), kw.get("y", Y),
+        kw.get("B", 2), kw.get("T", 160), kw.get("ws", WS), kw.get("wsb", need), 0, check=False)
+    assert f(layer=2) == L.MEBP_EINVAL
+    assert f(layer=-1) == L.MEBP_EINVAL
+    assert f(x=0) == L.MEBP_EINVAL
+    assert f(x=X + 4) == L.MEBP_EINVAL  # misaligned activation
+    assert f(y=X) == L.MEBP_EINVAL      # aliasing
+    assert f(ws=0) == L.MEBP_EINVAL
+    assert f(ws=WS + 16) == L.MEBP_EINVAL
+    assert f(wsb=need - 1) == L.MEBP_EWORKSPACE
+    assert f(B=0) == L.MEBP_EINVAL
+    assert f(base=None) == L.MEBP_EINVAL
+    bad = L.MebpLayerLora()
+    C.memmove(C.byref(bad), C.byref(lora), C.sizeof(lora))
+    bad.B[3] = None
+    assert f(lora=bad) == L.MEBP_EINVAL
+    assert "LoRA o" in L.mebp_last_error()
+    badb = L.MebpLayerBase()
+    C.memmove(C.byref(badb), C.byref(base), C.sizeof(base))
+    badb.w[6].q4 = 0x1001
+    assert f(base=badb) == L.MEBP_EINVAL
+    # backward: missing gradient buffers
+    g = L.MebpLayerLoraGrad()
+    r = L.mebp_layer_recompute_backward(c, 0, base, lora, X, Y, 0, g, 2, 160, WS, need, 0, check=False)
+    assert r == L.MEBP_EINVAL and "grad" in L.mebp_last_error()
+    # LM head needs T >= 2 and a vocabulary
+    emb = L.MebpQ4(q4=0x1000, scale=0x2000)
+    r = L.mebp_lm_head_ce_backward(c, emb, 0x300000, X, 0x500000, 2, 1, 0x600000, Y, WS, need, 0, check=False)
+    assert r == L.MEBP_EINVAL
+    c0 = make_config(CONFIGS["block"])
+    r = L.mebp_lm_head_ce_backward(c0, emb, 0x300000, X, 0x500000, 1, 128, 0x600000, Y, WS, 1 << 30, 0,
+                                   check=False)
+    assert r == L.MEBP_EINVAL and "vocab" in L.mebp_last_error()
+    # dequant: unsupported column count
+    assert L.mebp_dequant_q4(emb, 4, 12, 32, 0x10000, 0, 0, check=False) == L.MEBP_EUNSUPPORTED
+    assert L.mebp_dequant_q4(emb, 4, 16, 32, 0, 0, 0, check=False) == L.MEBP_EINVAL
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "nope.so"))
+    monkeypatch.setattr(L, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        L.lib()

@@ -1,0 +1,228 @@
+"""GPU parity of the HIP path against the CPU fp64 oracle, through the C ABI.
+
+Bar: bit-exact for int4 unpacking / decompression; rel-L2 <= 2e-2 for every bf16-operand,
+fp32-accumulate output and gradient; exact zeros where the mathematics gives zero
+(LoRA B = 0); bit-identical reruns (no atomics anywhere).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from mebp_inputs import CONFIGS, MINI, PROJ, layer_input, make_inputs
+from paper_2510_03425_amd import _lib as L
+from paper_2510_03425_amd.device import DeviceModel, slot_index
+
+from gpu_util import TOL, rel_l2, say, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _dm(inp, gpu):
+    return DeviceModel(inp, device=str(gpu))
+
+
+# ------------------------------------------------------------------------ decompression
+@pytest.mark.parametrize("name", ["block", "mini"])
+def test_dequant_bit_exact(built_lib, gpu, name):
+    cfg = CONFIGS.get(name, MINI)
+    inp = make_inputs(cfg, seed=0)
+    mats = [(p, inp.base[0][p], cfg.proj_shape(p)) for p in PROJ]
+    if inp.emb is not None:
+        mats.append(("emb", inp.emb, (cfg.vocab, cfg.hidden)))
+    for p, (q4, sb), (rows, cols) in mats:
+        say("dequant", name, p, rows, cols)
+        tq = torch.from_numpy(q4).to(gpu)
+        ts = torch.from_numpy(sb.view(np.int16)).to(gpu)
+        f32 = torch.empty((rows, cols), dtype=torch.float32, device=gpu)
+        b16 = torch.empty((rows, cols), dtype=torch.int16, device=gpu)
+        w = L.MebpQ4(q4=tq.data_ptr(), scale=ts.data_ptr())
+        L.mebp_dequant_q4(w, rows, cols, 32, f32.data_ptr(), b16.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        ref = O.dequant(q4, sb, cols, 32)
+        np.testing.assert_array_equal(f32.cpu().numpy().astype(np.float64), ref)
+        np.testing.assert_array_equal(b16.cpu().numpy().view(np.uint16), O.dequant_bf16_bits(q4, sb, cols, 32))
+
+
+def test_embed_exact(built_lib, gpu):
+    inp = make_inputs(MINI, seed=1)
+    dm = _dm(inp, gpu)
+    x0 = torch.empty((dm.N, MINI.hidden), dtype=torch.float32, device=gpu)
+    say("embed mini")
+    dm.embed(x0)
+    torch.cuda.synchronize()
+    E = O.decompress_embedding(MINI, inp)
+    np.testing.assert_array_equal(x0.cpu().numpy().astype(np.float64), O.embed(E, inp.ids))
+
+
+# ------------------------------------------------------------------------ one layer
+LAYER_CASES = [("block", 0, "ones"), ("block", 0, "random"), ("mini", 0, "random"), ("mini", 1, "random")]
+
+
+def _layer_setup(name, layer, norm, gpu, seed=0, **kw):
+    cfg = CONFIGS.get(name, MINI)
+    inp = make_inputs(cfg, seed=seed, norm=norm, **kw)
+    x, dy = (inp.x, inp.dy) if inp.x is not None else layer_input(cfg, seed + 100)
+    return cfg, inp, x, dy, _dm(inp, gpu)
+
+
+def _intermediates(dm, cfg):
+    N, d, F = dm.N, cfg.hidden, cfg.ffn
+    qd, kvd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
+    bf = torch.bfloat16
+    return {
+        "a": dm.ws_view(slot_index("a"), bf, (N, d)), "q": dm.ws_view(slot_index("q"), bf, (N, qd)),
+        "k": dm.ws_view(slot_index("k"), bf, (N, kvd)), "v": dm.ws_view(slot_index("v"), bf, (N, kvd)),
+        "o": dm.ws_view(slot_index("o"), bf, (N, qd)), "h": dm.ws_view(slot_index("h"), torch.float32, (N, d)),
+        "c": dm.ws_view(slot_index("c"), bf, (N, d)), "z": dm.ws_view(slot_index("z"), bf, (N, F)),
+        "lse": dm.ws_view(slot_index("lse"), torch.float32, (cfg.batch, cfg.n_heads, cfg.seq)),
+    }
+
+
+@pytest.mark.parametrize("name,layer,norm", LAYER_CASES)
+def test_layer_forward_parity(built_lib, gpu, name, layer, norm):
+    cfg, inp, x, dy, dm = _layer_setup(name, layer, norm, gpu)
+    tx = torch.from_numpy(x).to(gpu)
+    ty = torch.empty_like(tx)
+    say("layer forward", name, layer, norm)
+    dm.layer_forward(layer, tx, ty)
+    torch.cuda.synchronize()
+    P = O.decompress_layer(cfg, inp, layer)
+    y_ref, cache = O.layer_forward(cfg, layer, P, x, keep=True)
+    got = _intermediates(dm, cfg)
+    N = dm.N
+    ref = {"a": cache["a"], "q": cache["q4d"].reshape(N, -1), "k": cache["k4d"].reshape(N, -1),
+           "v": cache["v4d"].reshape(N, -1), "o": cache["O"], "h": cache["h"], "c": cache["c"], "z": cache["z"]}
+    errs = {k: rel_l2(to_np(got[k]), v) for k, v in ref.items()}
+    errs["y"] = rel_l2(to_np(ty), y_ref)
+    say("rel-L2", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL, (k, e)
+
+
+@pytest.mark.parametrize("name,layer,norm", LAYER_CASES)
+def test_layer_backward_parity(built_lib, gpu, name, layer, norm):
+    cfg, inp, x, dy, dm = _layer_setup(name, layer, norm, gpu)
+    tx = torch.from_numpy(x).to(gpu)
+    tdy = torch.from_numpy(dy).to(gpu)
+    tdx = torch.empty_like(tx)
+    say("layer backward", name, layer, norm)
+    dm.layer_backward(layer, tx, tdy, tdx)
+    torch.cuda.synchronize()
+    P = O.decompress_layer(cfg, inp, layer)
+    dx_ref, grads = O.layer_backward(cfg, layer, P, x, dy)
+    errs = {"dx": rel_l2(to_np(tdx), dx_ref)}
+    for p, (dA, dB) in grads.items():
+        errs["dA_" + p] = rel_l2(to_np(dm.dA[layer][p]), dA)
+        errs["dB_" + p] = rel_l2(to_np(dm.dB[layer][p]), dB)
+    say("rel-L2", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL, (k, e)
+
+
+def test_dx_may_alias_dy(built_lib, gpu):
+    cfg, inp, x, dy, dm = _layer_setup("mini", 0, "random", gpu)
+    tx = torch.from_numpy(x).to(gpu)
+    tdy = torch.from_numpy(dy).to(gpu)
+    tdx = torch.empty_like(tx)
+    say("alias dx=dy mini")
+    dm.layer_backward(0, tx, tdy, tdx)
+    g = tdy.clone()
+    dm.layer_backward(0, tx, g, g)
+    torch.cuda.synchronize()
+    assert torch.equal(g, tdx)
+
+
+def test_lora_b_zero_invariant(built_lib, gpu):
+    cfg, inp, x, dy, dm = _layer_setup("mini", 1, "random", gpu, lora_b_zero=True)
+    tx = torch.from_numpy(x).to(gpu)
+    ty = torch.empty_like(tx)
+    say("B=0 forward/backward mini")
+    dm.layer_forward(1, tx, ty)
+    base = DeviceModel(make_inputs(MINI.with_(lora_modules=()), seed=0, norm="random"), device=str(gpu))
+    ty0 = torch.empty_like(tx)
+    base.layer_forward(1, tx, ty0)
+    dm.layer_backward(1, tx, torch.from_numpy(dy).to(gpu), None)
+    torch.cuda.synchronize()
+    assert torch.equal(ty, ty0)  # adapter output exactly zero
+    for p in PROJ:
+        assert torch.count_nonzero(dm.dA[1][p]).item() == 0, p
+        assert torch.count_nonzero(dm.dB[1][p]).item() > 0, p
+
+
+def test_deterministic_and_recompute_equals_forward(built_lib, gpu):
+    cfg, inp, x, dy, dm = _layer_setup("mini", 0, "random", gpu)
+    tx = torch.from_numpy(x).to(gpu)
+    tdy = torch.from_numpy(dy).to(gpu)
+    y1, y2 = torch.empty_like(tx), torch.empty_like(tx)
+    say("determinism mini")
+    dm.layer_forward(0, tx, y1)
+    fwd = {k: v.clone() for k, v in _intermediates(dm, cfg).items()}
+    dm.layer_forward(0, tx, y2)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    dx1, dx2 = torch.empty_like(tx), torch.empty_like(tx)
+    dm.layer_backward(0, tx, tdy, dx1)
+    rec = {k: v.clone() for k, v in _intermediates(dm, cfg).items()}
+    g1 = {p: (dm.dA[0][p].clone(), dm.dB[0][p].clone()) for p in PROJ}
+    dm.layer_backward(0, tx, tdy, dx2)
+    torch.cuda.synchronize()
+    assert torch.equal(dx1, dx2)
+    for p in PROJ:
+        assert torch.equal(g1[p][0], dm.dA[0][p]) and torch.equal(g1[p][1], dm.dB[0][p])
+    # the recompute inside backward reproduces the stored forward's intermediates bit for bit
+    for k in fwd:
+        assert torch.equal(fwd[k], rec[k]), k
+
+
+# ------------------------------------------------------------------------ LM head, full step
+def test_lm_head_parity(built_lib, gpu):
+    cfg = MINI
+    inp = make_inputs(cfg, seed=3, norm="random")
+    dm = _dm(inp, gpu)
+    xL = np.random.default_rng(5).standard_normal((dm.N, cfg.hidden)).astype(np.float32)
+    tx = torch.from_numpy(xL).to(gpu)
+    tdx = torch.empty_like(tx)
+    say("lm head mini")
+    dm.lm_head(tx, tdx)
+    torch.cuda.synchronize()
+    E = O.decompress_embedding(cfg, inp)
+    loss, dx = O.lm_head_ce(cfg, E, inp.norm_final, xL, inp.ids)
+    say("loss", dm.loss.item(), loss, "dx rel-L2", rel_l2(to_np(tdx), dx))
+    assert abs(dm.loss.item() - loss) <= 1e-3 * abs(loss)
+    assert rel_l2(to_np(tdx), dx) <= TOL
+    # rows without a target (last position of each sequence) get exactly zero gradient
+    assert torch.count_nonzero(tdx.view(cfg.batch, cfg.seq, -1)[:, -1]).item() == 0
+
+
+def _step_parity(cfg, inp, gpu, ref=None):
+    dm = _dm(inp, gpu)
+    dx0 = torch.empty((dm.N, cfg.hidden), dtype=torch.float32, device=gpu)
+    say("train step", cfg.name)
+    dm.train_step(dx0)
+    torch.cuda.synchronize()
+    if ref is None:
+        ref = O.train_step(cfg, inp)
+    errs = {"dx0": rel_l2(to_np(dx0), ref.dx0)}
+    for l in range(cfg.n_layers):
+        for p, (dA, dB) in ref.grads[l].items():
+            errs[f"dA{l}_{p}"] = rel_l2(to_np(dm.dA[l][p]), dA)
+            errs[f"dB{l}_{p}"] = rel_l2(to_np(dm.dB[l][p]), dB)
+    if ref.ckpts:
+        for l in range(cfg.n_layers + 1):
+            errs[f"ckpt{l}"] = rel_l2(to_np(dm.ckpt[l]), ref.ckpts[l])
+    worst = max(errs, key=errs.get)
+    say("loss", dm.loss.item(), ref.loss, "worst", worst, f"{errs[worst]:.2e}")
+    assert abs(dm.loss.item() - ref.loss) <= 1e-3 * abs(ref.loss)
+    for k, e in errs.items():
+        assert e <= TOL, (k, e)
+    return dm
+
+
+def test_train_step_parity_mini(built_lib, gpu):
+    _step_parity(MINI, make_inputs(MINI, seed=4, norm="random"), gpu)
+
+
+def test_train_step_parity_qwen05b(built_lib, gpu):
+    cfg = CONFIGS["qwen2.5-0.5b"]
+    _step_parity(cfg, make_inputs(cfg, seed=0), gpu)
