@@ -253,7 +253,7 @@ NtSeg nt_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* l
   return s;
 }
 
-hipError_t run_nt(const Ctx& x, const bf16* X, int K, int nseg, NtSeg* segs, int epi) {
+hipError_t run_nt(const Ctx& x, const f16* X, int K, int nseg, NtSeg* segs, int epi) {
   NtArgs a{};
   a.X = X;
   a.lda = K;
@@ -283,29 +283,29 @@ TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* l
   return s;
 }
 
-// u_p = X A_p^T for each adapted projection p in `ps` (LoRA down-projection)
-hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const bf16* X, int K, std::initializer_list<int> ps) {
+// u_p = X A_p^T for each adapted projection p in `ps` (LoRA down-projection; X fp16)
+hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const f16* X, int K, std::initializer_list<int> ps) {
   for (int p : ps) {
     if (!adapted(x, p)) continue;
-    hipError_t e = launch_lora_rows(X, K, x.D.N, K, lora->A[p], 0, x.D.r, 1.0f, lu(x, p), x.st);
+    hipError_t e = launch_lora_rows(X, 0, K, x.D.N, K, lora->A[p], 0, x.D.r, 1.0f, lu(x, p), x.st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
 // LoRA backward of projection p with output gradient G (bf16 [N][out]) and input X
-// (bf16 [N][in]): du = s G B, dB = s G^T u, dA = du^T X.
+// (fp16 [N][in]): du = s G B, dB = s G^T u, dA = du^T X.
 hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_lora_grad* grads, int p,
-                    const bf16* G, const bf16* X) {
+                    const bf16* G, const f16* X) {
   if (!adapted(x, p)) return hipSuccess;
   const Dims& D = x.D;
   const int splits = lora_outer_splits(D.N);
   float* part = slot<float>(x.ws, x.L, S_PART);
-  hipError_t e = launch_lora_rows(G, D.out[p], D.N, D.out[p], lora->B[p], 1, D.r, D.s, ldu(x, p), x.st);
+  hipError_t e = launch_lora_rows(G, 1, D.out[p], D.N, D.out[p], lora->B[p], 1, D.r, D.s, ldu(x, p), x.st);
   if (e != hipSuccess) return e;
-  e = launch_lora_outer(G, D.out[p], D.N, D.out[p], lu(x, p), D.r, D.s, grads->dB[p], 0, part, splits, x.st);
+  e = launch_lora_outer(G, 1, D.out[p], D.N, D.out[p], lu(x, p), D.r, D.s, grads->dB[p], 0, part, splits, x.st);
   if (e != hipSuccess) return e;
-  return launch_lora_outer(X, D.in[p], D.N, D.in[p], ldu(x, p), D.r, 1.0f, grads->dA[p], 1, part, splits, x.st);
+  return launch_lora_outer(X, 0, D.in[p], D.N, D.in[p], ldu(x, p), D.r, 1.0f, grads->dA[p], 1, part, splits, x.st);
 }
 
 // Forward of one layer. keep=false: full forward to x_out. keep=true: recompute for the
@@ -314,22 +314,22 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
                   float* x_out, const float* rope, bool keep) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
-  bf16* a = slot<bf16>(x.ws, x.L, S_A);
-  bf16* q = slot<bf16>(x.ws, x.L, S_Q);
-  bf16* k = slot<bf16>(x.ws, x.L, S_K);
-  bf16* v = slot<bf16>(x.ws, x.L, S_V);
-  bf16* o = slot<bf16>(x.ws, x.L, S_O);
+  f16* a = slot<f16>(x.ws, x.L, S_A);
+  f16* q = slot<f16>(x.ws, x.L, S_Q);
+  f16* k = slot<f16>(x.ws, x.L, S_K);
+  f16* v = slot<f16>(x.ws, x.L, S_V);
+  f16* o = slot<f16>(x.ws, x.L, S_O);
   float* h = slot<float>(x.ws, x.L, S_H);
-  bf16* cc = slot<bf16>(x.ws, x.L, S_C);
-  bf16* g = slot<bf16>(x.ws, x.L, S_G);
-  bf16* u = slot<bf16>(x.ws, x.L, S_U);
-  bf16* z = slot<bf16>(x.ws, x.L, S_Z);
+  f16* cc = slot<f16>(x.ws, x.L, S_C);
+  f16* g = slot<f16>(x.ws, x.L, S_G);
+  f16* u = slot<f16>(x.ws, x.L, S_U);
+  f16* z = slot<f16>(x.ws, x.L, S_Z);
 
   HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
   HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}));
   NtSeg qkv[3] = {nt_seg(x, base, lora, MEBP_Q, q, D.qd, nullptr, 0), nt_seg(x, base, lora, MEBP_K, k, D.kvd, nullptr, 0),
                   nt_seg(x, base, lora, MEBP_V, v, D.kvd, nullptr, 0)};
-  HIP_TRY(run_nt(x, a, D.d, 3, qkv, NT_STORE_BF16));
+  HIP_TRY(run_nt(x, a, D.d, 3, qkv, NT_STORE_F16));
   HIP_TRY(launch_rope_fwd(q, D.qd, x.B, x.T, c->n_heads, c->head_dim, rope, x.st));
   HIP_TRY(launch_rope_fwd(k, D.kvd, x.B, x.T, c->n_kv_heads, c->head_dim, rope, x.st));
   AttnArgs at{};
@@ -344,7 +344,7 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   HIP_TRY(launch_rmsnorm_fwd(h, base->norm_mlp, D.N, D.d, c->rms_eps, cc, nullptr, x.st));
   HIP_TRY(lora_down(x, lora, cc, D.d, {MEBP_GATE, MEBP_UP}));
   NtSeg gu[2] = {nt_seg(x, base, lora, MEBP_GATE, g, D.F, nullptr, 0), nt_seg(x, base, lora, MEBP_UP, u, D.F, nullptr, 0)};
-  HIP_TRY(run_nt(x, cc, D.d, 2, gu, NT_STORE_BF16));
+  HIP_TRY(run_nt(x, cc, D.d, 2, gu, NT_STORE_F16));
   HIP_TRY(launch_act_fwd(g, u, z, (size_t)D.N * D.F, c->act, x.st));
   HIP_TRY(lora_down(x, lora, z, D.F, {MEBP_DOWN}));
   if (!keep) {
@@ -361,16 +361,16 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   const Dims& D = x.D;
   int e = layer_forward(x, l, base, lora, x_ckpt, nullptr, rope, true);
   if (e) return e;
-  bf16* a = slot<bf16>(x.ws, x.L, S_A);
-  bf16* q = slot<bf16>(x.ws, x.L, S_Q);
-  bf16* k = slot<bf16>(x.ws, x.L, S_K);
-  bf16* v = slot<bf16>(x.ws, x.L, S_V);
-  bf16* o = slot<bf16>(x.ws, x.L, S_O);
+  f16* a = slot<f16>(x.ws, x.L, S_A);
+  f16* q = slot<f16>(x.ws, x.L, S_Q);
+  f16* k = slot<f16>(x.ws, x.L, S_K);
+  f16* v = slot<f16>(x.ws, x.L, S_V);
+  f16* o = slot<f16>(x.ws, x.L, S_O);
   float* h = slot<float>(x.ws, x.L, S_H);
-  bf16* cc = slot<bf16>(x.ws, x.L, S_C);
-  bf16* g = slot<bf16>(x.ws, x.L, S_G);
-  bf16* u = slot<bf16>(x.ws, x.L, S_U);
-  bf16* z = slot<bf16>(x.ws, x.L, S_Z);
+  f16* cc = slot<f16>(x.ws, x.L, S_C);
+  f16* g = slot<f16>(x.ws, x.L, S_G);
+  f16* u = slot<f16>(x.ws, x.L, S_U);
+  f16* z = slot<f16>(x.ws, x.L, S_Z);
   bf16* dyb = slot<bf16>(x.ws, x.L, S_DYB);
   float* dc = slot<float>(x.ws, x.L, S_DC);
   float* dh = slot<float>(x.ws, x.L, S_DH);
@@ -392,13 +392,15 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
     HIP_TRY(launch_gemm_tn(t, TN_ACT_BWD, TN_A_BF16, x.st));  // g <- dg, u <- d(up)
   }
   // z = act(gate(c)) * up(c)
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_GATE, g, cc));
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_UP, u, cc));
+  bf16* dg = (bf16*)g;  // the act-backward epilogue left bf16 dg / du in the g / u buffers
+  bf16* dup = (bf16*)u;
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_GATE, dg, cc));
+  HIP_TRY(lora_bwd(x, lora, grads, MEBP_UP, dup, cc));
   {
     TnArgs t{};
     t.M = D.N; t.Kout = D.d; t.nseg = 2; t.r = D.r;
-    t.seg[0] = tn_seg(x, base, lora, MEBP_GATE, g);
-    t.seg[1] = tn_seg(x, base, lora, MEBP_UP, u);
+    t.seg[0] = tn_seg(x, base, lora, MEBP_GATE, dg);
+    t.seg[1] = tn_seg(x, base, lora, MEBP_UP, dup);
     t.out = dc; t.ldo = D.d;
     HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
   }
@@ -445,7 +447,7 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
   const Dims& D = x.D;
   const int V = c->vocab;
   int32_t* tgt = slot<int32_t>(x.ws, x.L, S_TGT);
-  bf16* hf = slot<bf16>(x.ws, x.L, S_HF);
+  f16* hf = slot<f16>(x.ws, x.L, S_HF);
   _Float16* logits = slot<_Float16>(x.ws, x.L, S_LOGITS);
   float2* stats = slot<float2>(x.ws, x.L, S_STATS);
   float* lse = slot<float>(x.ws, x.L, S_LSEV);

@@ -1,6 +1,8 @@
-// Causal grouped-query attention with optional sliding window on gfx950 (bf16 MFMA,
-// fp32 softmax), forward and backward, flash-style: scores never reach HBM; the forward
-// keeps the row log-sum-exp for the backward.
+// Causal grouped-query attention with optional sliding window on gfx950, forward and
+// backward, flash-style: scores never reach HBM; the forward keeps the row log-sum-exp
+// for the backward. Softmax statistics are fp32. Activations q, k, v, O are fp16 and the
+// score / output products run on fp16 MFMA; products with gradients (dO, dS) run on bf16
+// MFMA with the activation operand converted to bf16 while it is staged.
 //
 // Layout trick used throughout: the 16x16 C tile of v_mfma_f32_16x16x32_bf16 gives lane l
 // the rows 4*(l/16)+r (r = 0..3) of column l%16. Two such tiles stacked along the rows
@@ -27,20 +29,24 @@ constexpr float LOG2E = 1.4426950408889634f;
 
 // Row-major tile [R][C] of bf16 from global (row pitch ld, rows beyond `rows_ok` zero)
 // into LDS dst[R][C + pad]; 8-element chunks.
-template <int R, int C, int LD>
-DEV void load_tile_n(const bf16* src, size_t ld, int rows_ok, bf16* dst, int tid, int nthr) {
+typedef uint16_t u16;
+
+// CONV: convert fp16 source elements to bf16 while staging.
+template <int R, int C, int LD, bool CONV = false>
+DEV void load_tile_n(const u16* src, size_t ld, int rows_ok, u16* dst, int tid, int nthr) {
   constexpr int CH = C / 8;
   for (int i = tid; i < R * CH; i += nthr) {
     const int r = i / CH, c = (i % CH) * 8;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (r < rows_ok) v = *(const uint4*)(src + (size_t)r * ld + c);
+    if (CONV) v = f16x8_to_bf16x8(v);
     *(uint4*)(dst + r * LD + c) = v;
   }
 }
 
 // Transposed: global [R][C] -> LDS dst[C][R + pad]; each thread moves 8x8 blocks.
-template <int R, int C, int LD>
-DEV void load_tile_t(const bf16* src, size_t ld, int rows_ok, bf16* dst, int tid, int nthr) {
+template <int R, int C, int LD, bool CONV = false>
+DEV void load_tile_t(const u16* src, size_t ld, int rows_ok, u16* dst, int tid, int nthr) {
   constexpr int RB = R / 8, CB = C / 8;
   for (int b = tid; b < RB * CB; b += nthr) {
     const int rb = b % RB, cb = b / RB;
@@ -50,6 +56,7 @@ DEV void load_tile_t(const bf16* src, size_t ld, int rows_ok, bf16* dst, int tid
       const int r = rb * 8 + i;
       uint4 v = make_uint4(0, 0, 0, 0);
       if (r < rows_ok) v = *(const uint4*)(src + (size_t)r * ld + cb * 8);
+      if (CONV) v = f16x8_to_bf16x8(v);
       in[i][0] = v.x; in[i][1] = v.y; in[i][2] = v.z; in[i][3] = v.w;
     }
 #pragma unroll
@@ -73,40 +80,35 @@ DEV void load_tile_t(const bf16* src, size_t ld, int rows_ok, bf16* dst, int tid
 
 // A/B fragment from an LDS tile stored [row][k] (k contiguous): lane l reads
 // row row0 + l%16, k0 + 8*(l/16) .. +8.
-DEV bf16x8 frag_rows(const bf16* s, int ld, int row0, int k0, int lane) {
-  return *(const bf16x8*)(s + (row0 + (lane & 15)) * ld + k0 + 8 * (lane >> 4));
+DEV uint4 frag_rows(const u16* s, int ld, int row0, int k0, int lane) {
+  return *(const uint4*)(s + (row0 + (lane & 15)) * ld + k0 + 8 * (lane >> 4));
 }
 // Permuted fragment: row row0 + l%16, columns c0 + 4g .. +4 and c0 + 16 + 4g .. +4.
-DEV bf16x8 frag_perm(const bf16* s, int ld, int row0, int c0, int lane) {
-  const bf16* p = s + (row0 + (lane & 15)) * ld + c0 + 4 * (lane >> 4);
+DEV uint4 frag_perm(const u16* s, int ld, int row0, int c0, int lane) {
+  const u16* p = s + (row0 + (lane & 15)) * ld + c0 + 4 * (lane >> 4);
   const uint2 a = *(const uint2*)p, b = *(const uint2*)(p + 16);
-  uint4 v = make_uint4(a.x, a.y, b.x, b.y);
-  return __builtin_bit_cast(bf16x8, v);
+  return make_uint4(a.x, a.y, b.x, b.y);
 }
 // Pack two C tiles (8 floats: tile0 rows r=0..3, tile1 rows r=0..3) into an operand.
-DEV bf16x8 pack_frag(const f32x4& t0, const f32x4& t1) {
-  uint4 v = make_uint4(pack_bf16x2(t0[0], t0[1]), pack_bf16x2(t0[2], t0[3]), pack_bf16x2(t1[0], t1[1]),
-                       pack_bf16x2(t1[2], t1[3]));
-  return __builtin_bit_cast(bf16x8, v);
+template <class Op>
+DEV uint4 pack_frag(const f32x4& t0, const f32x4& t1) {
+  return make_uint4(Op::pack(t0[0], t0[1]), Op::pack(t0[2], t0[3]), Op::pack(t1[0], t1[1]), Op::pack(t1[2], t1[3]));
 }
-DEV bf16x8 load_frag_global(const bf16* p, bool ok) {
-  uint4 v = ok ? *(const uint4*)p : make_uint4(0, 0, 0, 0);
-  return __builtin_bit_cast(bf16x8, v);
-}
+DEV uint4 load_frag_global(const void* p, bool ok) { return ok ? *(const uint4*)p : make_uint4(0, 0, 0, 0); }
 
 // ------------------------------------------------------------------------------ forward
 template <int DH>
 __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
   constexpr int KB = 64, LDK = DH + 8, LDV = KB + 8, NKS = DH / 32, NT = DH / 16;
-  __shared__ __attribute__((aligned(16))) bf16 Ks[KB * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * LDV];
+  __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDK];
+  __shared__ __attribute__((aligned(16))) u16 Vt[DH * LDV];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
   const int q0 = blockIdx.x * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
-  bf16x8 qf[NKS];
+  uint4 qf[NKS];
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks)
     qf[ks] = load_frag_global(a.q + (rowb + q) * a.ldq + h * DH + 32 * ks + 8 * (lane >> 4), q < T);
@@ -119,8 +121,8 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
   if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
   const int kv_hi = min(T, q0 + 64);
   for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += KB) {
-    const bf16* kb = a.k + (rowb + kv0) * a.ldk + kvh * DH;
-    const bf16* vb = a.v + (rowb + kv0) * a.ldk + kvh * DH;
+    const u16* kb = (const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH;
+    const u16* vb = (const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH;
     load_tile_n<KB, DH, LDK>(kb, a.ldk, T - kv0, Ks, tid, 256);
     load_tile_t<KB, DH, LDV>(vb, a.ldk, T - kv0, Vt, tid, 256);
     __syncthreads();
@@ -129,7 +131,8 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
     for (int kt = 0; kt < 4; ++kt) {
       s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) s[kt] = mfma16(frag_rows(Ks, LDK, kt * 16, ks * 32, lane), qf[ks], s[kt]);
+      for (int ks = 0; ks < NKS; ++ks)
+        s[kt] = mfma16_raw<OpF16>(frag_rows(Ks, LDK, kt * 16, ks * 32, lane), qf[ks], s[kt]);
     }
     float mloc = -1e30f;
 #pragma unroll
@@ -163,20 +166,20 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
     for (int t = 0; t < NT; ++t) oacc[t] *= alpha;
 #pragma unroll
     for (int kp = 0; kp < 2; ++kp) {
-      const bf16x8 pf = pack_frag(s[2 * kp], s[2 * kp + 1]);
+      const uint4 pf = pack_frag<OpF16>(s[2 * kp], s[2 * kp + 1]);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) oacc[t] = mfma16(frag_perm(Vt, LDV, t * 16, kp * 32, lane), pf, oacc[t]);
+      for (int t = 0; t < NT; ++t) oacc[t] = mfma16_raw<OpF16>(frag_perm(Vt, LDV, t * 16, kp * 32, lane), pf, oacc[t]);
     }
     __syncthreads();
   }
   if (q < T) {
     const float inv = 1.0f / l_i;
-    bf16* orow = a.o + (rowb + q) * a.ldq + h * DH;
+    f16* orow = a.o + (rowb + q) * a.ldq + h * DH;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int e = t * 16 + 4 * (lane >> 4);
-      *(uint2*)(orow + e) = make_uint2(pack_bf16x2(oacc[t][0] * inv, oacc[t][1] * inv),
-                                       pack_bf16x2(oacc[t][2] * inv, oacc[t][3] * inv));
+      *(uint2*)(orow + e) = make_uint2(pack_f16x2(oacc[t][0] * inv, oacc[t][1] * inv),
+                                       pack_f16x2(oacc[t][2] * inv, oacc[t][3] * inv));
     }
     if ((lane >> 4) == 0) a.lse[((size_t)b * a.Hq + h) * T + q] = (m_i + log2f(l_i)) / LOG2E;
   }
@@ -184,7 +187,7 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
 
 // ------------------------------------------------------------------------------ backward
 // delta[b][h][t] = sum_e dO[b*T+t][h*dh+e] * O[b*T+t][h*dh+e]
-__global__ void k_attn_delta(const bf16* dO, const bf16* O, int ld, int B, int T, int H, int dh, float* delta) {
+__global__ void k_attn_delta(const bf16* dO, const f16* O, int ld, int B, int T, int H, int dh, float* delta) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (size_t)B * T * H) return;
   const int h = (int)(i % H);
@@ -197,7 +200,7 @@ __global__ void k_attn_delta(const bf16* dO, const bf16* O, int ld, int B, int T
     const uint32_t* xp = (const uint32_t*)&x;
     const uint32_t* yp = (const uint32_t*)&y;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc += bf16_lo(xp[j]) * bf16_lo(yp[j]) + bf16_hi(xp[j]) * bf16_hi(yp[j]);
+    for (int j = 0; j < 4; ++j) acc += bf16_lo(xp[j]) * f16_lo(yp[j]) + bf16_hi(xp[j]) * f16_hi(yp[j]);
   }
   const int b = (int)(row / T), t = (int)(row % T);
   delta[((size_t)b * H + h) * T + t] = acc;
@@ -207,10 +210,10 @@ __global__ void k_attn_delta(const bf16* dO, const bf16* O, int ld, int B, int T
 template <int DH, int QB>
 __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
   constexpr int LDN = DH + 8, LDT_ = QB + 8, NKS = DH / 32, NT = DH / 16, NQT = QB / 16;
-  __shared__ __attribute__((aligned(16))) bf16 Qs[QB * LDN];
-  __shared__ __attribute__((aligned(16))) bf16 dOs[QB * LDN];
-  __shared__ __attribute__((aligned(16))) bf16 Qt[DH * LDT_];
-  __shared__ __attribute__((aligned(16))) bf16 dOt[DH * LDT_];
+  __shared__ __attribute__((aligned(16))) u16 Qs[QB * LDN];   // fp16 (scores)
+  __shared__ __attribute__((aligned(16))) u16 dOs[QB * LDN];  // bf16
+  __shared__ __attribute__((aligned(16))) u16 Qt[DH * LDT_];  // bf16 (dK product)
+  __shared__ __attribute__((aligned(16))) u16 dOt[DH * LDT_]; // bf16
   __shared__ float lse_s[QB], del_s[QB];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int T = a.T, kvh = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv;
@@ -218,12 +221,12 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
-  bf16x8 kf[NKS], vf[NKS];
+  uint4 kf[NKS], vf[NKS];  // K fp16 (scores), V converted to bf16 (dP = dO V^T)
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks) {
     const size_t off = (rowb + key) * a.ldk + kvh * DH + 32 * ks + 8 * (lane >> 4);
     kf[ks] = load_frag_global(a.k + off, key < T);
-    vf[ks] = load_frag_global(a.v + off, key < T);
+    vf[ks] = f16x8_to_bf16x8(load_frag_global(a.v + off, key < T));
   }
   f32x4 dk[NT], dv[NT];
 #pragma unroll
@@ -237,11 +240,11 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
   for (int hh = 0; hh < grp; ++hh) {
     const int h = kvh * grp + hh;
     for (int qb0 = q_lo; qb0 < q_hi; qb0 += QB) {
-      const bf16* qsrc = a.q + (rowb + qb0) * a.ldq + h * DH;
-      const bf16* dsrc = a.dO + (rowb + qb0) * a.ldq + h * DH;
+      const u16* qsrc = (const u16*)a.q + (rowb + qb0) * a.ldq + h * DH;
+      const u16* dsrc = (const u16*)a.dO + (rowb + qb0) * a.ldq + h * DH;
       load_tile_n<QB, DH, LDN>(qsrc, a.ldq, T - qb0, Qs, tid, 256);
       load_tile_n<QB, DH, LDN>(dsrc, a.ldq, T - qb0, dOs, tid, 256);
-      load_tile_t<QB, DH, LDT_>(qsrc, a.ldq, T - qb0, Qt, tid, 256);
+      load_tile_t<QB, DH, LDT_, true>(qsrc, a.ldq, T - qb0, Qt, tid, 256);
       load_tile_t<QB, DH, LDT_>(dsrc, a.ldq, T - qb0, dOt, tid, 256);
       if (tid < QB) {
         const int qq = qb0 + tid;
@@ -257,8 +260,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
         dp[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-          s[qt] = mfma16(frag_rows(Qs, LDN, qt * 16, ks * 32, lane), kf[ks], s[qt]);
-          dp[qt] = mfma16(frag_rows(dOs, LDN, qt * 16, ks * 32, lane), vf[ks], dp[qt]);
+          s[qt] = mfma16_raw<OpF16>(frag_rows(Qs, LDN, qt * 16, ks * 32, lane), kf[ks], s[qt]);
+          dp[qt] = mfma16_raw<OpBF16>(frag_rows(dOs, LDN, qt * 16, ks * 32, lane), vf[ks], dp[qt]);
         }
       }
 #pragma unroll
@@ -273,12 +276,12 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
         }
 #pragma unroll
       for (int qp = 0; qp < NQT / 2; ++qp) {
-        const bf16x8 pf = pack_frag(s[2 * qp], s[2 * qp + 1]);
-        const bf16x8 df = pack_frag(dp[2 * qp], dp[2 * qp + 1]);
+        const uint4 pf = pack_frag<OpBF16>(s[2 * qp], s[2 * qp + 1]);
+        const uint4 df = pack_frag<OpBF16>(dp[2 * qp], dp[2 * qp + 1]);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-          dv[t] = mfma16(pf, frag_perm(dOt, LDT_, t * 16, qp * 32, lane), dv[t]);
-          dk[t] = mfma16(df, frag_perm(Qt, LDT_, t * 16, qp * 32, lane), dk[t]);
+          dv[t] = mfma16_raw<OpBF16>(pf, frag_perm(dOt, LDT_, t * 16, qp * 32, lane), dv[t]);
+          dk[t] = mfma16_raw<OpBF16>(df, frag_perm(Qt, LDT_, t * 16, qp * 32, lane), dk[t]);
         }
       }
       __syncthreads();
@@ -310,16 +313,16 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
 template <int DH, int KB>
 __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
   constexpr int LDN = DH + 8, LDT_ = KB + 8, NKS = DH / 32, NT = DH / 16, NKT = KB / 16;
-  __shared__ __attribute__((aligned(16))) bf16 Ks[KB * LDN];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[KB * LDN];
-  __shared__ __attribute__((aligned(16))) bf16 Kt[DH * LDT_];
+  __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDN];   // fp16 (scores)
+  __shared__ __attribute__((aligned(16))) u16 Vs[KB * LDN];   // bf16 (dP)
+  __shared__ __attribute__((aligned(16))) u16 Kt[DH * LDT_];  // bf16 (dQ product)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
   const int q0 = blockIdx.x * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
-  bf16x8 qf[NKS], dof[NKS];
+  uint4 qf[NKS], dof[NKS];  // Q fp16, dO bf16
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks) {
     const size_t off = (rowb + q) * a.ldq + h * DH + 32 * ks + 8 * (lane >> 4);
@@ -337,11 +340,11 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
   if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
   const int kv_hi = min(T, q0 + 64);
   for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += KB) {
-    const bf16* kb = a.k + (rowb + kv0) * a.ldk + kvh * DH;
-    const bf16* vb = a.v + (rowb + kv0) * a.ldk + kvh * DH;
+    const u16* kb = (const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH;
+    const u16* vb = (const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH;
     load_tile_n<KB, DH, LDN>(kb, a.ldk, T - kv0, Ks, tid, 256);
-    load_tile_n<KB, DH, LDN>(vb, a.ldk, T - kv0, Vs, tid, 256);
-    load_tile_t<KB, DH, LDT_>(kb, a.ldk, T - kv0, Kt, tid, 256);
+    load_tile_n<KB, DH, LDN, true>(vb, a.ldk, T - kv0, Vs, tid, 256);
+    load_tile_t<KB, DH, LDT_, true>(kb, a.ldk, T - kv0, Kt, tid, 256);
     __syncthreads();
     f32x4 s[NKT], dp[NKT];
 #pragma unroll
@@ -350,8 +353,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
       dp[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        s[kt] = mfma16(frag_rows(Ks, LDN, kt * 16, ks * 32, lane), qf[ks], s[kt]);
-        dp[kt] = mfma16(frag_rows(Vs, LDN, kt * 16, ks * 32, lane), dof[ks], dp[kt]);
+        s[kt] = mfma16_raw<OpF16>(frag_rows(Ks, LDN, kt * 16, ks * 32, lane), qf[ks], s[kt]);
+        dp[kt] = mfma16_raw<OpBF16>(frag_rows(Vs, LDN, kt * 16, ks * 32, lane), dof[ks], dp[kt]);
       }
     }
 #pragma unroll
@@ -365,9 +368,9 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
       }
 #pragma unroll
     for (int kp = 0; kp < NKT / 2; ++kp) {
-      const bf16x8 df = pack_frag(dp[2 * kp], dp[2 * kp + 1]);
+      const uint4 df = pack_frag<OpBF16>(dp[2 * kp], dp[2 * kp + 1]);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) dq[t] = mfma16(frag_perm(Kt, LDT_, t * 16, kp * 32, lane), df, dq[t]);
+      for (int t = 0; t < NT; ++t) dq[t] = mfma16_raw<OpBF16>(frag_perm(Kt, LDT_, t * 16, kp * 32, lane), df, dq[t]);
     }
     __syncthreads();
   }
@@ -409,7 +412,7 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st) {
 
 hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, hipStream_t st) {
   const size_t nd = (size_t)a0.B * a0.T * a0.Hq;
-  hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd + 255) / 256)), dim3(256), 0, st, a0.dO, (const bf16*)a0.o,
+  hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd + 255) / 256)), dim3(256), 0, st, a0.dO, (const f16*)a0.o,
                      a0.ldq, a0.B, a0.T, a0.Hq, a0.dh, delta_ws);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -7,6 +7,8 @@ typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 #define DEV static __device__ __forceinline__
 
@@ -23,6 +25,31 @@ DEV uint32_t pack_bf16x2(float lo, float hi) {
 DEV float bf16_lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
 DEV float bf16_hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xffff0000u); }
 DEV float half_bits_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+// fp32 -> fp16, round to nearest even.
+DEV uint32_t pack_f16x2(float lo, float hi) {
+  typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+  f16x2 p = {(_Float16)lo, (_Float16)hi};
+  return __builtin_bit_cast(uint32_t, p);
+}
+DEV float f16_lo(uint32_t w) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xffffu)); }
+DEV float f16_hi(uint32_t w) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16)); }
+// two fp16 -> two bf16 (round to nearest even)
+DEV uint32_t f16x2_to_bf16x2(uint32_t w) { return pack_bf16x2(f16_lo(w), f16_hi(w)); }
+DEV uint4 f16x8_to_bf16x8(uint4 v) {
+  return make_uint4(f16x2_to_bf16x2(v.x), f16x2_to_bf16x2(v.y), f16x2_to_bf16x2(v.z), f16x2_to_bf16x2(v.w));
+}
+
+// Operand element types of the two MFMA flavours used here.
+struct OpF16 {
+  static __device__ __forceinline__ uint32_t pack(float lo, float hi) { return pack_f16x2(lo, hi); }
+  static __device__ __forceinline__ float lo(uint32_t w) { return f16_lo(w); }
+  static __device__ __forceinline__ float hi(uint32_t w) { return f16_hi(w); }
+};
+struct OpBF16 {
+  static __device__ __forceinline__ uint32_t pack(float lo, float hi) { return pack_bf16x2(lo, hi); }
+  static __device__ __forceinline__ float lo(uint32_t w) { return bf16_lo(w); }
+  static __device__ __forceinline__ float hi(uint32_t w) { return bf16_hi(w); }
+};
 
 // One 16x16x32 bf16 MFMA: D = A(16x32) * B(32x16) + C.
 // Lane l supplies A[l%16][8*(l/16) .. +8] and B[8*(l/16) .. +8][l%16];
@@ -30,19 +57,32 @@ DEV float half_bits_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float
 DEV f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+DEV f32x4 mfma16(f16x8 a, f16x8 b, f32x4 c) { return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0); }
+// MFMA on raw 16-byte operands interpreted as Op's element type.
+template <class Op>
+__device__ __forceinline__ f32x4 mfma16_raw(uint4 a, uint4 b, f32x4 c) {
+  if constexpr (__is_same(Op, OpF16))
+    return mfma16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c);
+  else
+    return mfma16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c);
+}
+
+// Signed 4-bit code j (bits [4j, 4j+4)) of a packed dword (v_bfe_i32).
+DEV int nib_s(uint32_t w, int j) { return (int)(w << (28 - 4 * j)) >> 28; }
 
 // Decompress 8 int4 codes (one dword, element i in bits [4i, 4i+4)) times scale s into
-// 8 bf16 (4 dwords, element 2j in the low half of dword j). The product q*s is exact in
-// fp32; the bf16 conversion rounds to nearest even.
+// 8 16-bit operands (4 dwords, element 2j in the low half of dword j). The product q*s is
+// exact in fp32; the conversion to fp16 / bf16 rounds to nearest even.
+template <class Op>
 DEV uint4 dequant8(uint32_t w, float s) {
   float f[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) f[i] = (float)__builtin_amdgcn_sbfe(w, 4 * i, 4) * s;
+  for (int i = 0; i < 8; ++i) f[i] = (float)nib_s(w, i) * s;
   uint4 r;
-  r.x = pack_bf16x2(f[0], f[1]);
-  r.y = pack_bf16x2(f[2], f[3]);
-  r.z = pack_bf16x2(f[4], f[5]);
-  r.w = pack_bf16x2(f[6], f[7]);
+  r.x = Op::pack(f[0], f[1]);
+  r.y = Op::pack(f[2], f[3]);
+  r.z = Op::pack(f[4], f[5]);
+  r.w = Op::pack(f[6], f[7]);
   return r;
 }
 

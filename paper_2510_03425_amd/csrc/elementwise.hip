@@ -22,7 +22,7 @@ __global__ void k_dequant(const uint8_t* q4, const uint16_t* scale, int rows, in
   const float s = half_bits_to_f32(scale[r * ng + c / group]);
   float f[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) f[j] = (float)__builtin_amdgcn_sbfe(w, 4 * j, 4) * s;
+  for (int j = 0; j < 8; ++j) f[j] = (float)nib_s(w, j) * s;
   if (out_f32) {
     float4* o = (float4*)(out_f32 + r * cols + c);
     o[0] = make_float4(f[0], f[1], f[2], f[3]);
@@ -55,7 +55,7 @@ __global__ void k_embed(const uint8_t* q4, const uint16_t* scale, int d, int gro
   const float s = half_bits_to_f32(scale[v * ng + c / group]);
   float f[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) f[j] = (float)__builtin_amdgcn_sbfe(w, 4 * j, 4) * s;
+  for (int j = 0; j < 8; ++j) f[j] = (float)nib_s(w, j) * s;
   float4* o = (float4*)(x0 + (size_t)row * d + c);
   o[0] = make_float4(f[0], f[1], f[2], f[3]);
   o[1] = make_float4(f[4], f[5], f[6], f[7]);
@@ -64,7 +64,7 @@ __global__ void k_embed(const uint8_t* q4, const uint16_t* scale, int d, int gro
 // ------------------------------------------------------------------ RMSNorm
 // One wave per row, float4 accesses (d % 4 == 0).
 __global__ __launch_bounds__(256) void k_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps,
-                                                     bf16* y, float* rstd_out) {
+                                                     f16* y, float* rstd_out) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= n) return;
   const float4* xr = (const float4*)(x + (size_t)row * d);
@@ -81,7 +81,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm_fwd(const float* x, const float
   uint2* yr = (uint2*)(y + (size_t)row * d);
   for (int c = lane; c < d4; c += 64) {
     const float4 v = xr[c], g = wr[c];
-    yr[c] = make_uint2(pack_bf16x2(v.x * rs * g.x, v.y * rs * g.y), pack_bf16x2(v.z * rs * g.z, v.w * rs * g.w));
+    yr[c] = make_uint2(pack_f16x2(v.x * rs * g.x, v.y * rs * g.y), pack_f16x2(v.z * rs * g.z, v.w * rs * g.w));
   }
 }
 
@@ -142,7 +142,7 @@ __global__ void k_rope_table(int T, int dh, double theta, float* cs) {
 }
 
 // In place: pairs (e, e + dh/2) of every head rotate by the angle of (t, e).
-__global__ void k_rope_fwd(bf16* x, int ld, int B, int T, int H, int dh, const float* cs) {
+__global__ void k_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const float* cs) {
   const int half = dh >> 1;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t total = (size_t)B * T * H * half;
@@ -151,15 +151,15 @@ __global__ void k_rope_fwd(bf16* x, int ld, int B, int T, int H, int dh, const f
   const int h = (int)((i / half) % H);
   const size_t row = i / ((size_t)half * H);
   const int t = (int)(row % T);
-  bf16* p = x + row * ld + h * dh;
-  const float x1 = bf2f(p[e]), x2 = bf2f(p[e + half]);
+  f16* p = x + row * ld + h * dh;
+  const float x1 = (float)p[e], x2 = (float)p[e + half];
   const float c = cs[2 * (t * half + e)], s = cs[2 * (t * half + e) + 1];
-  p[e] = to_bf16(x1 * c - x2 * s);
-  p[e + half] = to_bf16(x2 * c + x1 * s);
+  p[e] = (f16)(x1 * c - x2 * s);
+  p[e + half] = (f16)(x2 * c + x1 * s);
 }
 
 // z = act(g) * u, 8 elements per thread
-__global__ void k_act_fwd(const bf16* g, const bf16* u, bf16* z, size_t n8, int act) {
+__global__ void k_act_fwd(const f16* g, const f16* u, f16* z, size_t n8, int act) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n8) return;
   const uint4 gv = ((const uint4*)g)[i], uv = ((const uint4*)u)[i];
@@ -168,14 +168,15 @@ __global__ void k_act_fwd(const bf16* g, const bf16* u, bf16* z, size_t n8, int 
   uint32_t o[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-    o[j] = pack_bf16x2(act_f(bf16_lo(gp[j]), act) * bf16_lo(up[j]), act_f(bf16_hi(gp[j]), act) * bf16_hi(up[j]));
+    o[j] = pack_f16x2(act_f(f16_lo(gp[j]), act) * f16_lo(up[j]), act_f(f16_hi(gp[j]), act) * f16_hi(up[j]));
   ((uint4*)z)[i] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // ------------------------------------------------------------------ LoRA
 // out[m][j] = s * sum_k X[m][k] * W(j,k). Workgroup: ROWS = 256/r rows x r outputs.
 constexpr int LR_KC = 128;
-__global__ __launch_bounds__(256) void k_lora_rows(const bf16* X, int ldx, int M, int K, const float* W, int wt,
+template <class T>
+__global__ __launch_bounds__(256) void k_lora_rows(const T* X, int ldx, int M, int K, const float* W, int wt,
                                                    int r, float s, float* out) {
   __shared__ float Xs[32][LR_KC + 1];
   __shared__ float Ws[16][LR_KC + 1];
@@ -187,7 +188,7 @@ __global__ __launch_bounds__(256) void k_lora_rows(const bf16* X, int ldx, int M
     for (int i = tid; i < rows * LR_KC; i += 256) {
       const int rr = i / LR_KC, kk = i % LR_KC;
       const int m = m0 + rr, k = k0 + kk;
-      Xs[rr][kk] = (m < M && k < K) ? bf2f(X[(size_t)m * ldx + k]) : 0.f;
+      Xs[rr][kk] = (m < M && k < K) ? (float)X[(size_t)m * ldx + k] : 0.f;
     }
     for (int i = tid; i < r * LR_KC; i += 256) {
       int jj, kk;
@@ -206,7 +207,8 @@ __global__ __launch_bounds__(256) void k_lora_rows(const bf16* X, int ldx, int M
 
 // part[split][c][j] = sum_{m in split} Mx[m][c] * V[m][j]; one thread per column c.
 constexpr int LO_MC = 64;
-__global__ __launch_bounds__(256) void k_lora_outer_part(const bf16* Mx, int ldm, int M, int C, const float* V,
+template <class T>
+__global__ __launch_bounds__(256) void k_lora_outer_part(const T* Mx, int ldm, int M, int C, const float* V,
                                                          int r, int splits, float* part) {
   __shared__ float4 Vs[LO_MC][4];
   const int c = blockIdx.x * 256 + threadIdx.x;
@@ -225,7 +227,7 @@ __global__ __launch_bounds__(256) void k_lora_outer_part(const bf16* Mx, int ldm
     __syncthreads();
     if (c < C) {
       for (int mm = 0; mm < mc; ++mm) {
-        const float x = bf2f(Mx[(size_t)(m0 + mm) * ldm + c]);
+        const float x = (float)Mx[(size_t)(m0 + mm) * ldm + c];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (q < r4) {
@@ -326,7 +328,7 @@ __global__ void k_ce_dh_reduce(const float* part, int splits, int M, int d, cons
     const uint32_t w = *(const uint32_t*)(eq4 + (size_t)tg * (d >> 1) + (c >> 1));
     const float s = half_bits_to_f32(escale[(size_t)tg * ng + (c >> 5)]);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) o[j] = inv_n * (o[j] - (float)__builtin_amdgcn_sbfe(w, 4 * j, 4) * s);
+    for (int j = 0; j < 8; ++j) o[j] = inv_n * (o[j] - (float)nib_s(w, j) * s);
   }
   float4* out = (float4*)(dhf + (size_t)m * d + c);
   out[0] = make_float4(o[0], o[1], o[2], o[3]);
@@ -362,7 +364,7 @@ hipError_t launch_embed(const uint8_t* q4, const uint16_t* scale, int d, int gro
   hipLaunchKernelGGL(k_embed, dim3(blocks_for(tot, 256)), dim3(256), 0, st, q4, scale, d, group, ids, n, V, x0);
   return hipGetLastError();
 }
-hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, bf16* y, float* rstd,
+hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, f16* y, float* rstd,
                               hipStream_t st) {
   hipLaunchKernelGGL(k_rmsnorm_fwd, dim3(blocks_for(n, 4)), dim3(256), 0, st, x, w, n, d, eps, y, rstd);
   return hipGetLastError();
@@ -381,30 +383,39 @@ hipError_t launch_rope_table(int T, int dh, double theta, float* cs, hipStream_t
   hipLaunchKernelGGL(k_rope_table, dim3(blocks_for((size_t)T * (dh / 2), 256)), dim3(256), 0, st, T, dh, theta, cs);
   return hipGetLastError();
 }
-hipError_t launch_rope_fwd(bf16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st) {
+hipError_t launch_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st) {
   const size_t tot = (size_t)B * T * H * (dh / 2);
   hipLaunchKernelGGL(k_rope_fwd, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, B, T, H, dh, cs);
   return hipGetLastError();
 }
-hipError_t launch_act_fwd(const bf16* g, const bf16* u, bf16* z, size_t n, int act, hipStream_t st) {
+hipError_t launch_act_fwd(const f16* g, const f16* u, f16* z, size_t n, int act, hipStream_t st) {
   const size_t n8 = n >> 3;
   hipLaunchKernelGGL(k_act_fwd, dim3(blocks_for(n8, 256)), dim3(256), 0, st, g, u, z, n8, act);
   return hipGetLastError();
 }
-hipError_t launch_lora_rows(const bf16* X, int ldx, int M, int K, const float* W, int wt, int r, float s, float* out,
-                            hipStream_t st) {
+hipError_t launch_lora_rows(const void* X, int xbf16, int ldx, int M, int K, const float* W, int wt, int r, float s,
+                            float* out, hipStream_t st) {
   const int rows = 256 / r;
-  hipLaunchKernelGGL(k_lora_rows, dim3(blocks_for(M, rows)), dim3(256), 0, st, X, ldx, M, K, W, wt, r, s, out);
+  if (xbf16)
+    hipLaunchKernelGGL(k_lora_rows<bf16>, dim3(blocks_for(M, rows)), dim3(256), 0, st, (const bf16*)X, ldx, M, K, W,
+                       wt, r, s, out);
+  else
+    hipLaunchKernelGGL(k_lora_rows<f16>, dim3(blocks_for(M, rows)), dim3(256), 0, st, (const f16*)X, ldx, M, K, W,
+                       wt, r, s, out);
   return hipGetLastError();
 }
 int lora_outer_splits(int M) {
   int s = (M + 255) / 256;
   return s < 1 ? 1 : (s > 64 ? 64 : s);
 }
-hipError_t launch_lora_outer(const bf16* Mx, int ldm, int M, int C, const float* V, int r, float s, float* out,
-                             int layout, float* part, int splits, hipStream_t st) {
-  hipLaunchKernelGGL(k_lora_outer_part, dim3(blocks_for(C, 256), splits), dim3(256), 0, st, Mx, ldm, M, C, V, r,
-                     splits, part);
+hipError_t launch_lora_outer(const void* Mx, int mbf16, int ldm, int M, int C, const float* V, int r, float s,
+                             float* out, int layout, float* part, int splits, hipStream_t st) {
+  if (mbf16)
+    hipLaunchKernelGGL(k_lora_outer_part<bf16>, dim3(blocks_for(C, 256), splits), dim3(256), 0, st, (const bf16*)Mx,
+                       ldm, M, C, V, r, splits, part);
+  else
+    hipLaunchKernelGGL(k_lora_outer_part<f16>, dim3(blocks_for(C, 256), splits), dim3(256), 0, st, (const f16*)Mx,
+                       ldm, M, C, V, r, splits, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_lora_outer_reduce, dim3(blocks_for((size_t)C * r, 256)), dim3(256), 0, st, part, splits, C, r,

@@ -2,10 +2,15 @@
 // fused into the matrix products of every base projection and of the tied LM head.
 //
 // Both orientations use one 128x128 output tile per 256-thread workgroup (2x2 waves of
-// 64x64, v_mfma_f32_16x16x32_bf16, fp32 accumulation) and a K step of 64. Activations
-// are staged global -> registers -> LDS; weights are fetched as packed int4 plus one fp16
-// scale per 32-group, decompressed once per workgroup into LDS as bf16 (q*s exact in
-// fp32, then rounded to nearest even), and never exist as a bf16 matrix in HBM.
+// 64x64, 16x16x32 MFMA, fp32 accumulation) and a K step of 64. Activations are staged
+// global -> registers -> LDS; weights are fetched as packed int4 plus one fp16 scale per
+// 32-group, decompressed once per workgroup into LDS (q*s exact in fp32, then rounded to
+// nearest even), and never exist as a 16-bit matrix in HBM.
+//
+// Operand precision: the forward orientation multiplies activations by weights and runs
+// in fp16 (v_mfma_f32_16x16x32_f16: same rate as bf16, 3 more mantissa bits, which keeps
+// the 24-34 layer recompute within the parity bound); the transposed orientation
+// multiplies gradients, whose magnitudes need bf16's exponent range, and runs in bf16.
 //
 //  * forward  ("NT"): C[m][n] = sum_k X[m][k] W[n][k]. A lane's MFMA B operand is 8
 //    consecutive k of one weight row, i.e. one dword of packed codes with one scale.
@@ -21,25 +26,28 @@ namespace {
 constexpr int BM = 128, BN = 128, BK = 64, LDT = BK + 8;  // LDS pitch in bf16 (144 B)
 constexpr int NTHREADS = 256;
 
-DEV void mma_tile(const bf16* As, const bf16* Bs, int wm, int wn, int lane, f32x4 (&acc)[4][4]) {
+typedef uint16_t u16;
+
+template <class Op>
+DEV void mma_tile(const u16* As, const u16* Bs, int wm, int wn, int lane, f32x4 (&acc)[4][4]) {
 #pragma unroll
   for (int ks = 0; ks < BK; ks += 32) {
-    bf16x8 af[4], bfr[4];
+    uint4 af[4], bfr[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      af[t] = *(const bf16x8*)(As + (wm * 64 + t * 16 + (lane & 15)) * LDT + ks + 8 * (lane >> 4));
-      bfr[t] = *(const bf16x8*)(Bs + (wn * 64 + t * 16 + (lane & 15)) * LDT + ks + 8 * (lane >> 4));
+      af[t] = *(const uint4*)(As + (wm * 64 + t * 16 + (lane & 15)) * LDT + ks + 8 * (lane >> 4));
+      bfr[t] = *(const uint4*)(Bs + (wn * 64 + t * 16 + (lane & 15)) * LDT + ks + 8 * (lane >> 4));
     }
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
-      for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = mfma16(af[tm], bfr[tn], acc[tm][tn]);
+      for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = mfma16_raw<Op>(af[tm], bfr[tn], acc[tm][tn]);
   }
 }
 
 // A-operand staging: 4 chunks of 8 bf16 per thread; chunk c = tid + 256 i covers row c>>3,
 // columns (c&7)*8 .. +8 of the 128x64 tile.
-DEV void load_a_tile(const bf16* X, int lda, int M, int Kred, int m0, int k0, int tid, uint4 (&ra)[4]) {
+DEV void load_a_tile(const u16* X, int lda, int M, int Kred, int m0, int k0, int tid, uint4 (&ra)[4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int c = tid + NTHREADS * i;
@@ -47,7 +55,7 @@ DEV void load_a_tile(const bf16* X, int lda, int M, int Kred, int m0, int k0, in
     ra[i] = (m < M && kc < Kred) ? *(const uint4*)(X + (size_t)m * lda + kc) : make_uint4(0, 0, 0, 0);
   }
 }
-DEV void store_a_tile(bf16* As, int tid, const uint4 (&ra)[4]) {
+DEV void store_a_tile(u16* As, int tid, const uint4 (&ra)[4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int c = tid + NTHREADS * i;
@@ -58,8 +66,8 @@ DEV void store_a_tile(bf16* As, int tid, const uint4 (&ra)[4]) {
 // ------------------------------------------------------------------------------ forward
 template <int EPI>
 __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16 As[BM * LDT];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[BN * LDT];
+  __shared__ __attribute__((aligned(16))) u16 As[BM * LDT];
+  __shared__ __attribute__((aligned(16))) u16 Bs[BN * LDT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int nt = blockIdx.x;
@@ -79,7 +87,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
 
   auto gload = [&](int kt) {
     const int k0 = kt * BK;
-    load_a_tile(a.X, a.lda, a.M, K, m0, k0, tid, ra);
+    load_a_tile((const u16*)a.X, a.lda, a.M, K, m0, k0, tid, ra);
     const int kb = k0 + 32 * bhalf;
     if (bn < Nn && kb < K) {
 #pragma unroll
@@ -96,7 +104,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
   auto sstore = [&]() {
     store_a_tile(As, tid, ra);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) *(uint4*)(Bs + brow * LDT + 32 * bhalf + 8 * j) = dequant8(rb[j], rsc);
+    for (int j = 0; j < 4; ++j) *(uint4*)(Bs + brow * LDT + 32 * bhalf + 8 * j) = dequant8<OpF16>(rb[j], rsc);
   };
 
   f32x4 acc[4][4];
@@ -110,7 +118,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 1 < nk) gload(kt + 1);
-    mma_tile(As, Bs, wm, wn, lane, acc);
+    mma_tile<OpF16>(As, Bs, wm, wn, lane, acc);
     __syncthreads();
     if (kt + 1 < nk) {
       sstore();
@@ -199,8 +207,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
             v += l;
           }
           if (sg.resid) v += sg.resid[(size_t)m * sg.ldr + n];
-          if constexpr (EPI == NT_STORE_BF16)
-            ((bf16*)sg.out)[(size_t)m * sg.ldo + n] = to_bf16(v);
+          if constexpr (EPI == NT_STORE_F16)
+            ((f16*)sg.out)[(size_t)m * sg.ldo + n] = (f16)v;
           else
             ((float*)sg.out)[(size_t)m * sg.ldo + n] = v;
         }
@@ -212,8 +220,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
 // ---------------------------------------------------------------------------- transposed
 template <int EPI, int AMODE>
 __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16 As[BM * LDT];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[BN * LDT];
+  __shared__ __attribute__((aligned(16))) u16 As[BM * LDT];
+  __shared__ __attribute__((aligned(16))) u16 Bs[BN * LDT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int c0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
@@ -268,7 +276,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     const TnSeg& sg = a.seg[s];
     cur_n0 = n0;
     cur_N = sg.N;
-    load_a_tile(sg.G, sg.ldg, a.M, sg.N, m0, n0, tid, ra);
+    load_a_tile((const u16*)sg.G, sg.ldg, a.M, sg.N, m0, n0, tid, ra);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int n = n0 + 4 * rq + i;
@@ -304,7 +312,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[i][j] = (float)__builtin_amdgcn_sbfe(rw[i], 4 * j, 4) * rsc[i];
+      for (int j = 0; j < 8; ++j) v[i][j] = (float)nib_s(rw[i], j) * rsc[i];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       uint2 pk;
@@ -326,7 +334,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     __syncthreads();
     for (int t = t_begin; t < t_end; ++t) {
       if (t + 1 < t_end) gload(t + 1);
-      mma_tile(As, Bs, wm, wn, lane, acc);
+      mma_tile<OpBF16>(As, Bs, wm, wn, lane, acc);
       __syncthreads();
       if (t + 1 < t_end) {
         sstore();
@@ -387,9 +395,10 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
           a.out[((size_t)blockIdx.z * a.M + m) * a.ldo + c] = v;
         } else {  // TN_ACT_BWD: v = dz
           const size_t idx = (size_t)m * a.ldgu + c;
-          const float g = bf2f(a.g[idx]), u = bf2f(a.u[idx]);
-          a.g[idx] = to_bf16(v * u * act_grad_f(g, a.act));
-          a.u[idx] = to_bf16(v * act_f(g, a.act));
+          // reads fp16 g, u; overwrites them in place with bf16 dg, du
+          const float g = (float)((const f16*)a.g)[idx], u = (float)((const f16*)a.u)[idx];
+          ((bf16*)a.g)[idx] = to_bf16(v * u * act_grad_f(g, a.act));
+          ((bf16*)a.u)[idx] = to_bf16(v * act_f(g, a.act));
         }
       }
     }
@@ -405,7 +414,7 @@ hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st) {
   for (int s = 0; s < a.nseg; ++s) tiles += gemm_nt_tiles(a.seg[s].N);
   dim3 grid(tiles, (a.M + BM - 1) / BM);
   switch (epi) {
-    case NT_STORE_BF16: hipLaunchKernelGGL(k_gemm_nt<NT_STORE_BF16>, grid, dim3(NTHREADS), 0, st, a); break;
+    case NT_STORE_F16: hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F16>, grid, dim3(NTHREADS), 0, st, a); break;
     case NT_STORE_F32: hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F32>, grid, dim3(NTHREADS), 0, st, a); break;
     case NT_LOGITS: hipLaunchKernelGGL(k_gemm_nt<NT_LOGITS>, grid, dim3(NTHREADS), 0, st, a); break;
     default: return hipErrorInvalidValue;

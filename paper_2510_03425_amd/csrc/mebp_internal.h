@@ -6,15 +6,16 @@
 #include <stdint.h>
 
 typedef __bf16 bf16;
+typedef _Float16 f16;
 
 namespace mebp {
 
 // ---------------------------------------------------------------- dequant GEMMs
 // Forward orientation: C[m][n] = sum_k X[m][k] * W[n][k] with W int4 [N][K/2] + fp16
-// scales [N][ceil(K/32)], X bf16 [M][lda]. Up to three weight segments along N share X
+// scales [N][ceil(K/32)], X fp16 [M][lda] (fp16 MFMA operands). Up to three weight segments along N share X
 // (q|k|v, gate|up). Epilogue adds s * u[m][:] . B[n][:] (LoRA up-projection) when
 // `lora_B` is set, then the fp32 residual when `resid` is set.
-enum NtEpi { NT_STORE_BF16 = 0, NT_STORE_F32 = 1, NT_LOGITS = 2 };
+enum NtEpi { NT_STORE_F16 = 0, NT_STORE_F32 = 1, NT_LOGITS = 2 };
 
 struct NtSeg {
   const uint8_t* q4;
@@ -23,14 +24,14 @@ struct NtSeg {
   int tile0;              // first N-tile index of this segment in the grid
   const float* lora_u;    // [M][r] (LoRA down-projection output), or null
   const float* lora_B;    // [N][r], or null
-  void* out;              // bf16 or fp32 [M][ldo]
+  void* out;              // fp16 or fp32 [M][ldo]
   int ldo;
   const float* resid;     // fp32 [M][ldr] added in the epilogue, or null
   int ldr;
 };
 
 struct NtArgs {
-  const bf16* X;
+  const void* X;          // fp16
   int lda, M, K;
   int nseg;
   NtSeg seg[3];
@@ -47,7 +48,8 @@ hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st);
 int gemm_nt_tiles(int N);  // number of 128-wide N tiles
 
 // Transposed orientation (input gradients): C[m][c] = sum_seg sum_n G_seg[m][n] * W_seg[n][c]
-// with W_seg int4 [N_seg][Kout/2]; reduction over the weight's output dim.
+// with W_seg int4 [N_seg][Kout/2]; reduction over the weight's output dim; G bf16 (bf16
+// MFMA operands).
 enum TnEpi { TN_STORE_F32 = 0, TN_ACT_BWD = 1, TN_PARTIAL_F32 = 2, TN_STORE_BF16 = 3 };
 enum TnAMode { TN_A_BF16 = 0, TN_A_SOFTMAX = 1 };
 
@@ -70,9 +72,10 @@ struct TnArgs {
   bf16* outb;              // bf16 [M][ldo] (TN_STORE_BF16)
   int ldo;
   int splits;              // split of the reduction (TN_PARTIAL_F32 only)
-  // TN_ACT_BWD: dz -> dg = dz*u*act'(g), du = dz*act(g); g,u read from, dg,du written to
-  bf16* g;
-  bf16* u;
+  // TN_ACT_BWD: dz -> dg = dz*u*act'(g), du = dz*act(g); fp16 g,u are read and overwritten
+  // in place by bf16 dg,du
+  void* g;
+  void* u;
   int ldgu;
   int act;
   // TN_A_SOFTMAX: p[m][v] = exp(logit - lse[m]) for rows with a target, else 0
@@ -86,36 +89,36 @@ hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, in
                           float* out_f32, uint16_t* out_bf16, hipStream_t st);
 hipError_t launch_embed(const uint8_t* q4, const uint16_t* scale, int d, int group, const int32_t* ids,
                         int n, int V, float* x0, hipStream_t st);
-// y = bf16(x * w * rstd); rstd optional
-hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, bf16* y,
+// y = fp16(x * w * rstd); rstd optional
+hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, f16* y,
                               float* rstd, hipStream_t st);
 // dx = resid + rmsnorm_bwd(x, w, dy); writes fp32 dx (may alias resid) and optional bf16 copy
 hipError_t launch_rmsnorm_bwd(const float* x, const float* w, const float* dy, const float* resid,
                               int n, int d, float eps, float* dx, bf16* dx_bf16, hipStream_t st);
 hipError_t launch_f32_to_bf16(const float* x, bf16* y, size_t n, hipStream_t st);
 hipError_t launch_rope_table(int T, int dh, double theta, float* cs, hipStream_t st);
-// in-place rotate-half RoPE on bf16 rows [B*T][H*dh] (columns head-major)
-hipError_t launch_rope_fwd(bf16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st);
-hipError_t launch_act_fwd(const bf16* g, const bf16* u, bf16* z, size_t n, int act, hipStream_t st);
+// in-place rotate-half RoPE on fp16 rows [B*T][H*dh] (columns head-major)
+hipError_t launch_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st);
+hipError_t launch_act_fwd(const f16* g, const f16* u, f16* z, size_t n, int act, hipStream_t st);
 
 // ---------------------------------------------------------------- LoRA skinny kernels
 // out[m][j] = s * sum_k X[m][k] * W(j, k), W(j,k) = W[j*K + k] (Wt=0, A [r][K]) or
-// W[k*r + j] (Wt=1, B [K][r]). X bf16 [M][ldx].
-hipError_t launch_lora_rows(const bf16* X, int ldx, int M, int K, const float* W, int wt, int r, float s,
-                            float* out, hipStream_t st);
+// W[k*r + j] (Wt=1, B [K][r]). X [M][ldx] fp16 (xbf16 = 0) or bf16 (xbf16 = 1).
+hipError_t launch_lora_rows(const void* X, int xbf16, int ldx, int M, int K, const float* W, int wt, int r,
+                            float s, float* out, hipStream_t st);
 // R(c, j) = s * sum_m Mx[m][c] * V[m][j]: out[c*r + j] (layout 0, dB [C][r]) or
-// out[j*C + c] (layout 1, dA [r][C]). Mx bf16 [M][ldm], V fp32 [M][r]. `part` is a
-// workspace of splits*C*r floats.
-hipError_t launch_lora_outer(const bf16* Mx, int ldm, int M, int C, const float* V, int r, float s,
+// out[j*C + c] (layout 1, dA [r][C]). Mx [M][ldm] fp16 (mbf16 = 0) or bf16 (mbf16 = 1),
+// V fp32 [M][r]. `part` is a workspace of splits*C*r floats.
+hipError_t launch_lora_outer(const void* Mx, int mbf16, int ldm, int M, int C, const float* V, int r, float s,
                              float* out, int layout, float* part, int splits, hipStream_t st);
 int lora_outer_splits(int M);
 
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
-  const bf16* q; const bf16* k; const bf16* v;   // [B*T][H*dh] row-major, head-major cols
+  const f16* q; const f16* k; const f16* v;      // [B*T][H*dh] row-major, head-major cols
   int ldq, ldk;                                  // row pitch of q (Hq*dh) and k/v (Hkv*dh)
   int B, T, Hq, Hkv, dh, window;
-  bf16* o;                                       // [B*T][Hq*dh]
+  f16* o;                                        // [B*T][Hq*dh]
   float* lse;                                    // [B][Hq][T]
   // backward
   const bf16* dO; const float* delta;            // delta [B][Hq][T]

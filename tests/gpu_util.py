@@ -18,7 +18,7 @@ def say(*a):
 
 def to_np(t):
     import torch
-    if t.dtype == torch.bfloat16:
+    if t.dtype in (torch.bfloat16, torch.float16):
         return t.float().cpu().numpy()
     return t.cpu().numpy()
 

@@ -1,6 +1,6 @@
 """GPU parity of the HIP path against the CPU fp64 oracle, through the C ABI.
 
-Bar: bit-exact for int4 unpacking / decompression; rel-L2 <= 2e-2 for every bf16-operand,
+Bar: bit-exact for int4 unpacking / decompression; rel-L2 <= 2e-2 for every 16-bit-operand,
 fp32-accumulate output and gradient; exact zeros where the mathematics gives zero
 (LoRA B = 0); bit-identical reruns (no atomics anywhere).
 """
@@ -69,7 +69,7 @@ def _layer_setup(name, layer, norm, gpu, seed=0, **kw):
 def _intermediates(dm, cfg):
     N, d, F = dm.N, cfg.hidden, cfg.ffn
     qd, kvd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
-    bf = torch.bfloat16
+    bf = torch.float16  # forward activations are fp16
     return {
         "a": dm.ws_view(slot_index("a"), bf, (N, d)), "q": dm.ws_view(slot_index("q"), bf, (N, qd)),
         "k": dm.ws_view(slot_index("k"), bf, (N, kvd)), "v": dm.ws_view(slot_index("v"), bf, (N, kvd)),
