@@ -1,0 +1,165 @@
+"""Benchmark: checkpointed LoRA training steps (MeBP, Algorithm 1) on one MI355X.
+
+One step = embedding, forward over every layer storing the layer-boundary checkpoints,
+final RMSNorm + tied int4 LM head + cross-entropy and its gradient, then every layer in
+reverse: recompute from its checkpoint, backpropagate into the LoRA A/B gradients and the
+layer-input gradient. Inputs are synthetic, seeded, resident in device memory before the
+timed region. Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X published dense peaks
+PEAK_TFLOPS_16BIT = 2516.6  # fp16 / bf16 dense MFMA, TFLOP/s
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def algorithmic_flops(cfg):
+    """Work the method must do per step (see the design notes): base GEMMs
+    fwd + recompute + input-gradient = 6 N P L; LM head logits + gradient = 4 N d V;
+    attention 16 dh per visible (query, key) pair per query head; LoRA 8 N r (in + out)."""
+    from mebp_inputs import PROJ
+    N, L = cfg.n_tokens, cfg.n_layers
+    P = sum(o * i for o, i in (cfg.proj_shape(p) for p in PROJ))
+    base = 6.0 * N * P * L
+    head = 4.0 * N * cfg.hidden * cfg.vocab
+    attn = 0.0
+    for l in range(L):
+        W = cfg.layer_window(l)
+        pairs = sum(min(t + 1, W) if W else t + 1 for t in range(cfg.seq))
+        attn += 16.0 * cfg.head_dim * pairs * cfg.n_heads * cfg.batch
+    lora = sum(8.0 * N * cfg.lora_rank * sum(cfg.proj_shape(p)) for p in cfg.lora_modules) * L
+    return base + head + attn + lora
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen2.5-0.5b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=3, help="extra steps with per-kernel event timing")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}); the multi-GPU path is not "
+              "part of this build", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from mebp_inputs import CONFIGS, make_inputs
+    from paper_2510_03425_amd import _lib as L
+    from paper_2510_03425_amd.device import DeviceModel
+
+    cfg = CONFIGS[args.workload]
+    t0 = time.time()
+    inp = make_inputs(cfg, seed=0)
+    log(f"inputs {cfg.name} drawn in {time.time() - t0:.1f}s")
+    dm = DeviceModel(inp, device="cuda:0")
+    dx0 = None
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        dm.train_step(dx0)
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dm.train_step(dx0)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    tokens = cfg.n_tokens
+    value = tokens / (ms / 1e3)
+    log(f"{ms:.3f} ms/step, {value:.0f} tokens/s (wall {wall / args.steps * 1e3:.3f} ms/step)")
+    loss = dm.loss.item()
+
+    # per-kernel timing pass (HIP events around every launch on the step's stream)
+    L.mebp_kernel_timing(True, 1 << 16)
+    for _ in range(args.profile_steps):
+        dm.train_step(dx0)
+    torch.cuda.synchronize()
+    rep = L.mebp_kernel_timing_report()
+    L.mebp_kernel_timing(False)
+    total_k = sum(r["ms"] for r in rep)
+    rep.sort(key=lambda r: -r["ms"])
+    for r in rep[:12]:
+        log(f"  {r['kernel']:22s} {r['ms'] / args.profile_steps:8.3f} ms/step  {r['launches'] // args.profile_steps:4d}"
+            f" launches  {r['flops'] / r['ms'] / 1e9 if r['ms'] else 0:8.1f} TFLOP/s"
+            f"  {r['bytes'] / r['ms'] / 1e6 if r['ms'] else 0:8.1f} GB/s")
+    dom = rep[0]
+    per_launch_ms = dom["ms"] / dom["launches"]
+    if dom["flops"] > 0:
+        ach = dom["flops"] / dom["launches"] / (per_launch_ms / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS_16BIT, "unit": "TFLOP/s",
+                "frac": round(ach / PEAK_TFLOPS_16BIT, 4), "traffic": None, "kernel": dom["kernel"],
+                "avg_launch_us": round(per_launch_ms * 1e3, 2), "kernel_share_of_step": round(dom["ms"] / total_k, 3)}
+    else:
+        ach = dom["bytes"] / dom["launches"] / (per_launch_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "kernel": dom["kernel"],
+                "avg_launch_us": round(per_launch_ms * 1e3, 2), "kernel_share_of_step": round(dom["ms"] / total_k, 3)}
+    step_flops = algorithmic_flops(cfg)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle as O
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+        except Exception:
+            cores = os.cpu_count()
+        t0 = time.perf_counter()
+        ref = O.train_step(cfg, inp, keep_ckpts=False)
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(tokens / dt, 3), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+               "sample": f"one full fp64 step of the same workload ({tokens} tokens), {dt:.1f} s",
+               "loss_oracle": ref.loss}
+        log(f"oracle step {dt:.1f}s on {cores} threads; loss gpu {loss:.6f} oracle {ref.loss:.6f}")
+
+    out = {
+        "metric": "LoRA train tokens/s per checkpointed step",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16/bf16 MFMA, fp32 accumulate",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shaped full LoRA step", "layers": cfg.n_layers, "hidden": cfg.hidden,
+                   "heads": f"{cfg.n_heads}x{cfg.head_dim}/{cfg.n_kv_heads}kv", "ffn": cfg.ffn, "vocab": cfg.vocab,
+                   "global_batch": cfg.batch, "seq_len": cfg.seq, "lora": f"r{cfg.lora_rank} a{cfg.lora_alpha:g} "
+                   + ",".join(cfg.lora_modules), "weights": "int4 group-32, fp16 scales", "parallelism": "none"},
+        "step_mfma_frac": round(step_flops / (ms / 1e3) / 1e12 / PEAK_TFLOPS_16BIT, 4),
+        "loss": loss,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

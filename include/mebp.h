@@ -172,6 +172,18 @@ int mebp_dequant_q4(const mebp_q4* w, int32_t rows, int32_t cols, int32_t group,
 size_t mebp_workspace_offset(const mebp_config* cfg, int32_t B, int32_t T, int32_t slot);
 const char* mebp_workspace_slot_name(int32_t slot);
 
+/* Diagnostic per-kernel timing. mebp_kernel_timing(1) creates a pool of HIP events
+ * (no device memory is allocated) and from then on brackets every kernel launch of this
+ * library with an event pair tagged by kernel name and algorithmic flops / bytes;
+ * mebp_kernel_timing(0) stops and frees the pool. Records beyond the pool's capacity
+ * (`capacity` launches) are not timed. mebp_kernel_timing_report synchronises on the
+ * recorded events and writes a JSON array
+ *   [{"kernel": name, "launches": n, "ms": total, "flops": total, "bytes": total}, ...]
+ * into buf (truncated to len); it returns the length the full report needs including the
+ * terminating NUL, or a negative mebp_status. Host-thread-unsafe; for benchmarks only.  */
+int mebp_kernel_timing(int32_t enable, int32_t capacity);
+int mebp_kernel_timing_report(char* buf, size_t len);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,7 +19,8 @@ NPROJ = 7
 EXPORTED = (
     "mebp_workspace_bytes", "mebp_layer_forward_ckpt", "mebp_layer_recompute_backward",
     "mebp_lm_head_ce_backward", "mebp_embed", "mebp_train_step", "mebp_last_error",
-    "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name",
+    "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name", "mebp_kernel_timing",
+    "mebp_kernel_timing_report",
 )
 
 
@@ -84,6 +85,8 @@ def lib() -> C.CDLL:
             "mebp_dequant_q4": (C.c_int, [C.POINTER(MebpQ4), I32, I32, I32, P, P, P]),
             "mebp_workspace_offset": (SZ, [cfgp, I32, I32, I32]),
             "mebp_workspace_slot_name": (C.c_char_p, [I32]),
+            "mebp_kernel_timing": (C.c_int, [I32, I32]),
+            "mebp_kernel_timing_report": (C.c_int, [C.c_char_p, SZ]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -155,3 +158,19 @@ def mebp_train_step(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt, loss, g
 def mebp_dequant_q4(w, rows, cols, group, out_f32, out_bf16, stream=0, check=True):
     r = lib().mebp_dequant_q4(_ref(w), rows, cols, group, out_f32, out_bf16, stream)
     return _check(r) if check else r
+
+
+def mebp_kernel_timing(enable: bool, capacity: int = 65536) -> int:
+    return _check(lib().mebp_kernel_timing(int(enable), capacity))
+
+
+def mebp_kernel_timing_report() -> list:
+    import json
+    n = lib().mebp_kernel_timing_report(None, 0)
+    if n < 0:
+        raise MebpError(n, mebp_last_error())
+    buf = C.create_string_buffer(n)
+    r = lib().mebp_kernel_timing_report(buf, n)
+    if r < 0:
+        raise MebpError(r, mebp_last_error())
+    return json.loads(buf.value.decode())

@@ -39,19 +39,39 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 enum Slot {
   S_A, S_Q, S_K, S_V, S_O, S_LSE, S_H, S_C, S_G, S_U, S_Z, S_LU, S_LDU, S_DYB, S_DC, S_DH, S_DHB, S_DO,
   S_DELTA, S_DQ, S_DK, S_DV, S_DA, S_PART, S_ROPE_G, S_ROPE_L, S_TGT, S_HF, S_LOGITS, S_STATS, S_LSEV,
-  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_COUNT
+  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_CNT, S_COUNT
 };
+constexpr int kCounters = 1 << 16;
 const char* kSlotNames[S_COUNT] = {
   "a", "q", "k", "v", "o", "lse", "h", "c", "g", "u", "z", "lora_u", "lora_du", "dy_bf16", "dc", "dh",
   "dh_bf16", "do", "delta", "dq", "dk", "dv", "da", "lora_part", "rope_global", "rope_local", "targets",
-  "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad"};
+  "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part",
+  "split_counters"};
 
 struct Layout {
   size_t off[S_COUNT];
   size_t total;
   int lm_splits;
   int ntiles;
+  size_t split_floats;
 };
+
+size_t nt_part(int M, int K, std::initializer_list<int> Ns) {
+  int tiles = 0, ncat = 0;
+  for (int n : Ns) {
+    tiles += gemm_nt_tiles(n);
+    ncat += n;
+  }
+  const int mt = (M + kGemmBM - 1) / kGemmBM;
+  (void)ncat;
+  return gemm_part_floats(tiles * mt, gemm_splits(tiles * mt, (K + kGemmBK - 1) / kGemmBK));
+}
+size_t tn_part(int M, int Kout, std::initializer_list<int> Ns) {
+  int kt = 0;
+  for (int n : Ns) kt += (n + kGemmBK - 1) / kGemmBK;
+  const int tiles = ((Kout + kGemmBN - 1) / kGemmBN) * ((M + kGemmBM - 1) / kGemmBM);
+  return gemm_part_floats(tiles, gemm_splits(tiles, kt));
+}
 
 int lm_head_splits(int N, int d, int V) {
   const int tiles = ((d + 127) / 128) * ((N + 127) / 128);
@@ -67,9 +87,6 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   const size_t N = (size_t)B * T, d = c->hidden, qd = (size_t)c->n_heads * c->head_dim,
                kvd = (size_t)c->n_kv_heads * c->head_dim, F = c->ffn, r = c->lora_rank > 0 ? c->lora_rank : 16,
                V = c->vocab, H = c->n_heads;
-  size_t maxc = d > F ? d : F;
-  if (qd > maxc) maxc = qd;
-  const int splits = lora_outer_splits((int)N);
   L->lm_splits = V ? lm_head_splits((int)N, (int)d, (int)V) : 0;
   L->ntiles = V ? gemm_nt_tiles((int)V) : 0;
   size_t sz[S_COUNT] = {};
@@ -96,7 +113,7 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   sz[S_DK] = N * kvd * 2;
   sz[S_DV] = N * kvd * 2;
   sz[S_DA] = N * d * 4;
-  sz[S_PART] = (size_t)splits * maxc * r * 4;
+  sz[S_PART] = 0;  // unused (LoRA partials live in the shared split scratch)
   sz[S_ROPE_G] = (size_t)T * c->head_dim * 4;
   sz[S_ROPE_L] = (size_t)T * c->head_dim * 4;
   sz[S_TGT] = N * 4;
@@ -109,6 +126,27 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   sz[S_DHF] = V ? N * d * 4 : 0;
   sz[S_LMPART] = (size_t)L->lm_splits * N * d * 4;
   sz[S_GRAD] = N * d * 4;
+  {
+    const int M = (int)N, D = (int)d, Q = (int)qd, KV = (int)kvd, FF = (int)F, R = (int)r;
+    size_t m = 0;
+    auto mx = [&](size_t v) { m = v > m ? v : m; };
+    mx(nt_part(M, D, {Q, KV, KV}));
+    mx(nt_part(M, Q, {D}));
+    mx(nt_part(M, D, {FF, FF}));
+    mx(nt_part(M, FF, {D}));
+    mx(tn_part(M, FF, {D}));
+    mx(tn_part(M, D, {FF, FF}));
+    mx(tn_part(M, Q, {D}));
+    mx(tn_part(M, D, {Q, KV, KV}));
+    for (int dim : {D, Q, KV, FF}) {
+      mx(lora_rows_part_floats(M, dim, R));
+      mx(lora_outer_part_floats(M, dim, R));
+    }
+    mx(attn_bwd_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim));
+    L->split_floats = m;
+    sz[S_SPLIT] = m * 4;
+    sz[S_CNT] = (size_t)kCounters * 4;
+  }
   size_t o = 0;
   for (int i = 0; i < S_COUNT; ++i) {
     L->off[i] = o;
@@ -234,6 +272,15 @@ struct Ctx {
   hipStream_t st;
 };
 
+SplitScratch scratch(const Ctx& x) {
+  SplitScratch sc;
+  sc.part = slot<float>(x.ws, x.L, S_SPLIT);
+  sc.part_floats = x.L.split_floats;
+  sc.counters = slot<int>(x.ws, x.L, S_CNT);
+  sc.ncounters = kCounters;
+  return sc;
+}
+
 float* lu(const Ctx& x, int p) { return slot<float>(x.ws, x.L, S_LU) + (size_t)p * x.D.N * x.D.r; }
 float* ldu(const Ctx& x, int p) { return slot<float>(x.ws, x.L, S_LDU) + (size_t)p * x.D.N * x.D.r; }
 bool adapted(const Ctx& x, int p) { return (x.c->lora_mask >> p) & 1; }
@@ -268,7 +315,20 @@ hipError_t run_nt(const Ctx& x, const f16* X, int K, int nseg, NtSeg* segs, int 
   }
   a.lora_s = x.D.s;
   a.r = x.D.r;
+  const SplitScratch sc = scratch(x);
+  a.part = sc.part;
+  a.part_floats = sc.part_floats;
+  a.counters = sc.counters;
+  a.ncounters = sc.ncounters;
   return launch_gemm_nt(a, epi, x.st);
+}
+
+void set_scratch(const Ctx& x, TnArgs& t) {
+  const SplitScratch sc = scratch(x);
+  t.part = sc.part;
+  t.part_floats = sc.part_floats;
+  t.counters = sc.counters;
+  t.ncounters = sc.ncounters;
 }
 
 TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* lora, int p, const bf16* G) {
@@ -287,7 +347,7 @@ TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* l
 hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const f16* X, int K, std::initializer_list<int> ps) {
   for (int p : ps) {
     if (!adapted(x, p)) continue;
-    hipError_t e = launch_lora_rows(X, 0, K, x.D.N, K, lora->A[p], 0, x.D.r, 1.0f, lu(x, p), x.st);
+    hipError_t e = launch_lora_rows(X, 0, K, x.D.N, K, lora->A[p], 0, x.D.r, 1.0f, lu(x, p), scratch(x), x.st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -299,13 +359,12 @@ hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_
                     const bf16* G, const f16* X) {
   if (!adapted(x, p)) return hipSuccess;
   const Dims& D = x.D;
-  const int splits = lora_outer_splits(D.N);
-  float* part = slot<float>(x.ws, x.L, S_PART);
-  hipError_t e = launch_lora_rows(G, 1, D.out[p], D.N, D.out[p], lora->B[p], 1, D.r, D.s, ldu(x, p), x.st);
+  const SplitScratch sc = scratch(x);
+  hipError_t e = launch_lora_rows(G, 1, D.out[p], D.N, D.out[p], lora->B[p], 1, D.r, D.s, ldu(x, p), sc, x.st);
   if (e != hipSuccess) return e;
-  e = launch_lora_outer(G, 1, D.out[p], D.N, D.out[p], lu(x, p), D.r, D.s, grads->dB[p], 0, part, splits, x.st);
+  e = launch_lora_outer(G, 1, D.out[p], D.N, D.out[p], lu(x, p), D.r, D.s, grads->dB[p], 0, sc, x.st);
   if (e != hipSuccess) return e;
-  return launch_lora_outer(X, 0, D.in[p], D.N, D.in[p], ldu(x, p), D.r, 1.0f, grads->dA[p], 1, part, splits, x.st);
+  return launch_lora_outer(X, 0, D.in[p], D.N, D.in[p], ldu(x, p), D.r, 1.0f, grads->dA[p], 1, sc, x.st);
 }
 
 // Forward of one layer. keep=false: full forward to x_out. keep=true: recompute for the
@@ -386,6 +445,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   HIP_TRY(lora_bwd(x, lora, grads, MEBP_DOWN, dyb, z));
   {
     TnArgs t{};
+    set_scratch(x, t);
     t.M = D.N; t.Kout = D.F; t.nseg = 1; t.r = D.r;
     t.seg[0] = tn_seg(x, base, lora, MEBP_DOWN, dyb);
     t.g = g; t.u = u; t.ldgu = D.F; t.act = c->act;
@@ -398,6 +458,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   HIP_TRY(lora_bwd(x, lora, grads, MEBP_UP, dup, cc));
   {
     TnArgs t{};
+    set_scratch(x, t);
     t.M = D.N; t.Kout = D.d; t.nseg = 2; t.r = D.r;
     t.seg[0] = tn_seg(x, base, lora, MEBP_GATE, dg);
     t.seg[1] = tn_seg(x, base, lora, MEBP_UP, dup);
@@ -409,6 +470,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   HIP_TRY(lora_bwd(x, lora, grads, MEBP_O, dhb, o));
   {
     TnArgs t{};
+    set_scratch(x, t);
     t.M = D.N; t.Kout = D.qd; t.nseg = 1; t.r = D.r;
     t.seg[0] = tn_seg(x, base, lora, MEBP_O, dhb);
     t.outb = dO; t.ldo = D.qd;
@@ -422,13 +484,14 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
     at.window = is_global(c, l) ? 0 : c->window;
     at.o = o; at.lse = slot<float>(x.ws, x.L, S_LSE);
     at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
-    HIP_TRY(launch_attn_bwd(at, slot<float>(x.ws, x.L, S_DELTA), x.st));
+    HIP_TRY(launch_attn_bwd(at, slot<float>(x.ws, x.L, S_DELTA), scratch(x), x.st));
   }
   HIP_TRY(lora_bwd(x, lora, grads, MEBP_Q, dq, a));
   HIP_TRY(lora_bwd(x, lora, grads, MEBP_K, dk, a));
   HIP_TRY(lora_bwd(x, lora, grads, MEBP_V, dv, a));
   if (dx) {
     TnArgs t{};
+    set_scratch(x, t);
     t.M = D.N; t.Kout = D.d; t.nseg = 3; t.r = D.r;
     t.seg[0] = tn_seg(x, base, lora, MEBP_Q, dq);
     t.seg[1] = tn_seg(x, base, lora, MEBP_K, dk);
@@ -471,6 +534,7 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
   HIP_TRY(launch_ce_loss(rl, tgt, D.N, inv_n, loss, x.st));
   {
     TnArgs t{};
+    set_scratch(x, t);
     t.M = D.N; t.Kout = D.d; t.nseg = 1; t.r = 0;
     t.seg[0].G = (const bf16*)logits; t.seg[0].ldg = V;
     t.seg[0].q4 = emb->q4; t.seg[0].scale = emb->scale; t.seg[0].N = V;
@@ -493,6 +557,11 @@ Ctx make_ctx(const mebp_config* c, int B, int T, void* ws, mebp_stream_t stream)
   make_layout(c, B, T, &x.L);
   x.st = (hipStream_t)stream;
   return x;
+}
+
+int zero_counters(const Ctx& x) {
+  HIP_TRY(launch_fill_i32(slot<int>(x.ws, x.L, S_CNT), kCounters, 0, x.st));
+  return MEBP_OK;
 }
 
 int rope_table(const Ctx& x, int l, float** out) {
@@ -540,7 +609,7 @@ int mebp_layer_forward_ckpt(const mebp_config* cfg, int32_t layer, const mebp_la
   if (x_in == x_out) return fail(MEBP_EINVAL, "x_out must not alias x_in");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
   float* rope;
-  if ((e = rope_table(x, layer, &rope))) return e;
+  if ((e = zero_counters(x)) || (e = rope_table(x, layer, &rope))) return e;
   return layer_forward(x, layer, base, lora, x_in, x_out, rope, false);
 }
 
@@ -557,7 +626,7 @@ int mebp_layer_recompute_backward(const mebp_config* cfg, int32_t layer, const m
   if (dx && dx == x_ckpt) return fail(MEBP_EINVAL, "dx must not alias x_ckpt");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
   float* rope;
-  if ((e = rope_table(x, layer, &rope))) return e;
+  if ((e = zero_counters(x)) || (e = rope_table(x, layer, &rope))) return e;
   return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
 }
 
@@ -574,6 +643,7 @@ int mebp_lm_head_ce_backward(const mebp_config* cfg, const mebp_q4* emb, const f
   if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
   if (!loss || !aligned(loss, 4)) return fail(MEBP_EINVAL, "loss NULL or misaligned");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
+  if ((e = zero_counters(x))) return e;
   return lm_head(x, emb, norm_final, x_last, ids, loss, dx_last);
 }
 
@@ -613,6 +683,7 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   const size_t stride = (size_t)x.D.N * x.D.d;
   float* rope_g = slot<float>(ws, x.L, S_ROPE_G);
   float* rope_l = slot<float>(ws, x.L, S_ROPE_L);
+  if ((e = zero_counters(x))) return e;
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_global, rope_g, x.st));
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_local, rope_l, x.st));
   HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ckpt, x.st));
@@ -647,6 +718,18 @@ int mebp_dequant_q4(const mebp_q4* w, int32_t rows, int32_t cols, int32_t group,
     return fail(MEBP_EINVAL, "outputs must be 16-byte aligned");
   HIP_TRY(launch_dequant(w->q4, w->scale, rows, cols, group, out_f32, out_bf16, (hipStream_t)stream));
   return MEBP_OK;
+}
+
+int mebp_kernel_timing(int32_t enable, int32_t capacity) {
+  if (enable && capacity <= 0) return fail(MEBP_EINVAL, "capacity must be > 0");
+  if (timing_enable(enable, capacity) != 0) return fail(MEBP_EHIP, "hipEventCreate failed");
+  return MEBP_OK;
+}
+
+int mebp_kernel_timing_report(char* buf, size_t len) {
+  const int n = timing_report(buf, len);
+  if (n < 0) return fail(MEBP_EHIP, "event synchronisation failed");
+  return n;
 }
 
 }  // extern "C"

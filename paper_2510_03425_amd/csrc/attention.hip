@@ -16,8 +16,9 @@
 //  forward : S^T = K Q^T (A = K rows from LDS, B = Q rows kept in registers);
 //            O^T += V^T P^T (A = V^T from LDS, B = P from registers); row stats live in
 //            the lane of their query, so rescaling needs no cross-lane traffic.
-//  backward: dK/dV kernel owns a key block (GQA heads of a group summed in-kernel, no
-//            atomics); dQ kernel owns a query block. RoPE backward (rotation by minus the
+//  backward: dK/dV kernel owns a key block of one query head (the heads of a GQA group
+//            are summed by the group's last workgroup, in head order); dQ kernel owns a
+//            query block. RoPE backward (rotation by minus the
 //            angle) is applied in both epilogues before the bf16 store.
 #include "device_common.h"
 #include "mebp_internal.h"
@@ -206,9 +207,11 @@ __global__ void k_attn_delta(const bf16* dO, const f16* O, int ld, int B, int T,
   delta[((size_t)b * H + h) * T + t] = acc;
 }
 
-// dK, dV for a block of 64 keys of one KV head; sums over the query heads of its group.
+// dK, dV for a block of 64 keys and one query head. With grouped-query attention the
+// heads of a KV group run in separate workgroups; each stores its partial dK/dV and the
+// last of the group to arrive sums them in head order (deterministic) and writes.
 template <int DH, int QB>
-__global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
+__global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* part, int* counters) {
   constexpr int LDN = DH + 8, LDT_ = QB + 8, NKS = DH / 32, NT = DH / 16, NQT = QB / 16;
   __shared__ __attribute__((aligned(16))) u16 Qs[QB * LDN];   // fp16 (scores)
   __shared__ __attribute__((aligned(16))) u16 dOs[QB * LDN];  // bf16
@@ -216,7 +219,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) u16 dOt[DH * LDT_]; // bf16
   __shared__ float lse_s[QB], del_s[QB];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int T = a.T, kvh = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv;
+  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
   const int k0 = blockIdx.x * 64, kw = k0 + 16 * w, key = kw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
@@ -237,8 +240,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
   const int q_lo = k0 & ~(QB - 1);
   int q_hi = T;
   if (a.window) q_hi = min(T, k0 + 64 + a.window - 1);
-  for (int hh = 0; hh < grp; ++hh) {
-    const int h = kvh * grp + hh;
+  {
     for (int qb0 = q_lo; qb0 < q_hi; qb0 += QB) {
       const u16* qsrc = (const u16*)a.q + (rowb + qb0) * a.ldq + h * DH;
       const u16* dsrc = (const u16*)a.dO + (rowb + qb0) * a.ldq + h * DH;
@@ -288,6 +290,37 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a) {
     }
   }
   // epilogue: lane holds rows key kw + 4g + r, column e = 16t + lane%16
+  if (grp > 1) {
+    const size_t plane = (size_t)a.B * T * a.Hkv * DH;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int kk = kw + 4 * (lane >> 4) + r;
+      if (kk >= T) continue;
+      const size_t o = (rowb + kk) * (size_t)(a.Hkv * DH) + kvh * DH + (lane & 15);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        st_dev(&part[(size_t)hh * plane + o + 16 * t], dk[t][r]);
+        st_dev(&part[(size_t)(grp + hh) * plane + o + 16 * t], dv[t][r]);
+      }
+    }
+    if (!arrive_last(counters + ((size_t)b * a.Hkv + kvh) * gridDim.x + blockIdx.x, grp)) return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int kk = kw + 4 * (lane >> 4) + r;
+      if (kk >= T) continue;
+      const size_t o = (rowb + kk) * (size_t)(a.Hkv * DH) + kvh * DH + (lane & 15);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        float sk = 0.f, sv = 0.f;
+        for (int g = 0; g < grp; ++g) {
+          sk += ld_dev(&part[(size_t)g * plane + o + 16 * t]);
+          sv += ld_dev(&part[(size_t)(grp + g) * plane + o + 16 * t]);
+        }
+        dk[t][r] = sk;
+        dv[t][r] = sv;
+      }
+    }
+  }
   const float scale = 1.0f / sqrtf((float)DH);
   const int half = DH / 2;
 #pragma unroll
@@ -399,38 +432,60 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
 
 }  // namespace
 
+// visible (query, key) pairs of one sequence and head
+double visible_pairs(int T, int W) {
+  double p = 0;
+  for (int i = 0; i < T; ++i) p += (W && W < i + 1) ? W : i + 1;
+  return p;
+}
+
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st) {
   dim3 grid((a.T + 63) / 64, a.Hq, a.B);
+  const double pairs = visible_pairs(a.T, a.window) * a.Hq * a.B;
+  const double flops = 4.0 * a.dh * pairs;
+  const double bytes = (double)a.B * a.T * (2.0 * a.Hq * a.dh * 2 + 2.0 * a.Hkv * a.dh * 2 + a.Hq * 4);
   switch (a.dh) {
-    case 64: hipLaunchKernelGGL(k_attn_fwd<64>, grid, dim3(256), 0, st, a); break;
-    case 128: hipLaunchKernelGGL(k_attn_fwd<128>, grid, dim3(256), 0, st, a); break;
-    case 256: hipLaunchKernelGGL(k_attn_fwd<256>, grid, dim3(256), 0, st, a); break;
+    case 64: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<64>, grid, dim3(256), 0, st, a)); break;
+    case 128: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<128>, grid, dim3(256), 0, st, a)); break;
+    case 256: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<256>, grid, dim3(256), 0, st, a)); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, hipStream_t st) {
+size_t attn_bwd_part_floats(int B, int T, int Hq, int Hkv, int dh) {
+  return Hq > Hkv ? 2ull * B * T * Hq * dh : 0;
+}
+
+hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScratch& sc, hipStream_t st) {
   const size_t nd = (size_t)a0.B * a0.T * a0.Hq;
-  hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd + 255) / 256)), dim3(256), 0, st, a0.dO, (const f16*)a0.o,
-                     a0.ldq, a0.B, a0.T, a0.Hq, a0.dh, delta_ws);
+  MEBP_TIMED(st, "attn_delta", 0.0, (double)nd * (4.0 * a0.dh + 4),
+             hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd + 255) / 256)), dim3(256), 0, st, a0.dO,
+                                (const f16*)a0.o, a0.ldq, a0.B, a0.T, a0.Hq, a0.dh, delta_ws));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   AttnArgs a = a0;
   a.delta = delta_ws;
-  dim3 gkv((a.T + 63) / 64, a.Hkv, a.B), gq((a.T + 63) / 64, a.Hq, a.B);
+  dim3 gkv((a.T + 63) / 64, a.Hq, a.B), gq((a.T + 63) / 64, a.Hq, a.B);
+  if (a.Hq > a.Hkv && (!sc.part || sc.part_floats < attn_bwd_part_floats(a.B, a.T, a.Hq, a.Hkv, a.dh) ||
+                       (size_t)a.B * a.Hkv * gkv.x > (size_t)sc.ncounters))
+    return hipErrorInvalidValue;
+  const double pairs = visible_pairs(a.T, a.window) * a.Hq * a.B;
+  // algorithmic: dV, dK and dP products in the key-block kernel, dQ in the query-block kernel
+  const double f_kv = 6.0 * a.dh * pairs, f_q = 2.0 * a.dh * pairs;
+  const double io = (double)a.B * a.T * (a.Hq * a.dh * 2.0 * 2 + a.Hkv * a.dh * 2.0 * 4);
   switch (a.dh) {
     case 64:
-      hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a);
-      hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, st, a);
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, sc.part, sc.counters));
+      MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, st, a));
       break;
     case 128:
-      hipLaunchKernelGGL((k_attn_bwd_dkdv<128, 64>), gkv, dim3(256), 0, st, a);
-      hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, st, a);
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<128, 64>), gkv, dim3(256), 0, st, a, sc.part, sc.counters));
+      MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, st, a));
       break;
     case 256:
-      hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a);
-      hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, st, a);
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, sc.part, sc.counters));
+      MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, st, a));
       break;
     default: return hipErrorInvalidValue;
   }

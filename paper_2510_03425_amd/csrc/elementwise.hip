@@ -172,92 +172,6 @@ __global__ void k_act_fwd(const f16* g, const f16* u, f16* z, size_t n8, int act
   ((uint4*)z)[i] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
-// ------------------------------------------------------------------ LoRA
-// out[m][j] = s * sum_k X[m][k] * W(j,k). Workgroup: ROWS = 256/r rows x r outputs.
-constexpr int LR_KC = 128;
-template <class T>
-__global__ __launch_bounds__(256) void k_lora_rows(const T* X, int ldx, int M, int K, const float* W, int wt,
-                                                   int r, float s, float* out) {
-  __shared__ float Xs[32][LR_KC + 1];
-  __shared__ float Ws[16][LR_KC + 1];
-  const int rows = 256 / r;
-  const int tid = threadIdx.x, lr = tid / r, j = tid % r;
-  const int m0 = blockIdx.x * rows;
-  float acc = 0.f;
-  for (int k0 = 0; k0 < K; k0 += LR_KC) {
-    for (int i = tid; i < rows * LR_KC; i += 256) {
-      const int rr = i / LR_KC, kk = i % LR_KC;
-      const int m = m0 + rr, k = k0 + kk;
-      Xs[rr][kk] = (m < M && k < K) ? (float)X[(size_t)m * ldx + k] : 0.f;
-    }
-    for (int i = tid; i < r * LR_KC; i += 256) {
-      int jj, kk;
-      if (wt) { kk = i / r; jj = i % r; } else { jj = i / LR_KC; kk = i % LR_KC; }
-      const int k = k0 + kk;
-      Ws[jj][kk] = k < K ? (wt ? W[(size_t)k * r + jj] : W[(size_t)jj * K + k]) : 0.f;
-    }
-    __syncthreads();
-#pragma unroll 8
-    for (int kk = 0; kk < LR_KC; ++kk) acc += Xs[lr][kk] * Ws[j][kk];
-    __syncthreads();
-  }
-  const int m = m0 + lr;
-  if (m < M) out[(size_t)m * r + j] = s * acc;
-}
-
-// part[split][c][j] = sum_{m in split} Mx[m][c] * V[m][j]; one thread per column c.
-constexpr int LO_MC = 64;
-template <class T>
-__global__ __launch_bounds__(256) void k_lora_outer_part(const T* Mx, int ldm, int M, int C, const float* V,
-                                                         int r, int splits, float* part) {
-  __shared__ float4 Vs[LO_MC][4];
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  const int split = blockIdx.y;
-  const int mb = (int)((long long)M * split / splits), me = (int)((long long)M * (split + 1) / splits);
-  float acc[16];
-#pragma unroll
-  for (int j = 0; j < 16; ++j) acc[j] = 0.f;
-  const int r4 = r >> 2;
-  for (int m0 = mb; m0 < me; m0 += LO_MC) {
-    const int mc = min(LO_MC, me - m0);
-    for (int i = threadIdx.x; i < LO_MC * r4; i += 256) {
-      const int mm = i / r4, q = i % r4;
-      Vs[mm][q] = mm < mc ? ((const float4*)(V + (size_t)(m0 + mm) * r))[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    __syncthreads();
-    if (c < C) {
-      for (int mm = 0; mm < mc; ++mm) {
-        const float x = (float)Mx[(size_t)(m0 + mm) * ldm + c];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (q < r4) {
-            const float4 v = Vs[mm][q];
-            acc[4 * q + 0] += x * v.x;
-            acc[4 * q + 1] += x * v.y;
-            acc[4 * q + 2] += x * v.z;
-            acc[4 * q + 3] += x * v.w;
-          }
-        }
-      }
-    }
-    __syncthreads();
-  }
-  if (c < C) {
-    float* p = part + ((size_t)split * C + c) * r;
-    for (int j = 0; j < r; ++j) p[j] = acc[j];
-  }
-}
-
-__global__ void k_lora_outer_reduce(const float* part, int splits, int C, int r, float s, float* out, int layout) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;  // index into out
-  if (i >= C * r) return;
-  int c, j;
-  if (layout == 0) { c = i / r; j = i % r; } else { j = i / C; c = i % C; }
-  float acc = 0.f;
-  for (int sp = 0; sp < splits; ++sp) acc += part[((size_t)sp * C + c) * r + j];
-  out[i] = s * acc;
-}
-
 // ------------------------------------------------------------------ cross-entropy
 // tgt[b*T+t] = ids[b][t+1] for t < T-1, -1 (no target) for t = T-1; an id outside
 // [0, V) becomes -2, which the loss turns into NaN instead of an out-of-bounds read.
@@ -354,101 +268,85 @@ hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, in
                           float* out_f32, uint16_t* out_bf16, hipStream_t st) {
   const size_t n = (size_t)rows * (cols >> 3);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_dequant, dim3(blocks_for(n, 256)), dim3(256), 0, st, q4, scale, rows, cols, group, out_f32,
-                     out_bf16);
+  MEBP_TIMED(st, "dequant", 0.0, (double)n * 4 * (1 + (out_f32 ? 32 : 0) + (out_bf16 ? 16 : 0)),
+             hipLaunchKernelGGL(k_dequant, dim3(blocks_for(n, 256)), dim3(256), 0, st, q4, scale, rows, cols, group, out_f32,
+                     out_bf16));
   return hipGetLastError();
 }
 hipError_t launch_embed(const uint8_t* q4, const uint16_t* scale, int d, int group, const int32_t* ids, int n,
                         int V, float* x0, hipStream_t st) {
   const size_t tot = (size_t)n * (d >> 3);
-  hipLaunchKernelGGL(k_embed, dim3(blocks_for(tot, 256)), dim3(256), 0, st, q4, scale, d, group, ids, n, V, x0);
+  MEBP_TIMED(st, "embed", 0.0, (double)tot * 36,
+             hipLaunchKernelGGL(k_embed, dim3(blocks_for(tot, 256)), dim3(256), 0, st, q4, scale, d, group, ids, n, V, x0));
   return hipGetLastError();
 }
 hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, f16* y, float* rstd,
                               hipStream_t st) {
-  hipLaunchKernelGGL(k_rmsnorm_fwd, dim3(blocks_for(n, 4)), dim3(256), 0, st, x, w, n, d, eps, y, rstd);
+  MEBP_TIMED(st, "rmsnorm_fwd", 0.0, (double)n * d * 6,
+             hipLaunchKernelGGL(k_rmsnorm_fwd, dim3(blocks_for(n, 4)), dim3(256), 0, st, x, w, n, d, eps, y, rstd));
   return hipGetLastError();
 }
 hipError_t launch_rmsnorm_bwd(const float* x, const float* w, const float* dy, const float* resid, int n, int d,
                               float eps, float* dx, bf16* dxb, hipStream_t st) {
-  hipLaunchKernelGGL(k_rmsnorm_bwd, dim3(blocks_for(n, 4)), dim3(256), 0, st, x, w, dy, resid, n, d, eps, dx, dxb);
+  MEBP_TIMED(st, "rmsnorm_bwd", 0.0, (double)n * d * ((resid ? 16 : 12) + (dxb ? 2 : 0)),
+             hipLaunchKernelGGL(k_rmsnorm_bwd, dim3(blocks_for(n, 4)), dim3(256), 0, st, x, w, dy, resid, n, d, eps, dx, dxb));
   return hipGetLastError();
 }
 hipError_t launch_f32_to_bf16(const float* x, bf16* y, size_t n, hipStream_t st) {
   const size_t n4 = n >> 2;
-  hipLaunchKernelGGL(k_f32_to_bf16, dim3(blocks_for(n4, 256)), dim3(256), 0, st, x, y, n4);
+  MEBP_TIMED(st, "f32_to_bf16", 0.0, (double)n4 * 24,
+             hipLaunchKernelGGL(k_f32_to_bf16, dim3(blocks_for(n4, 256)), dim3(256), 0, st, x, y, n4));
   return hipGetLastError();
 }
 hipError_t launch_rope_table(int T, int dh, double theta, float* cs, hipStream_t st) {
-  hipLaunchKernelGGL(k_rope_table, dim3(blocks_for((size_t)T * (dh / 2), 256)), dim3(256), 0, st, T, dh, theta, cs);
+  MEBP_TIMED(st, "rope_table", 0.0, (double)T * dh * 4,
+             hipLaunchKernelGGL(k_rope_table, dim3(blocks_for((size_t)T * (dh / 2), 256)), dim3(256), 0, st, T, dh, theta, cs));
   return hipGetLastError();
 }
 hipError_t launch_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st) {
   const size_t tot = (size_t)B * T * H * (dh / 2);
-  hipLaunchKernelGGL(k_rope_fwd, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, B, T, H, dh, cs);
+  MEBP_TIMED(st, "rope_fwd", 0.0, (double)tot * 8,
+             hipLaunchKernelGGL(k_rope_fwd, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, B, T, H, dh, cs));
   return hipGetLastError();
 }
 hipError_t launch_act_fwd(const f16* g, const f16* u, f16* z, size_t n, int act, hipStream_t st) {
   const size_t n8 = n >> 3;
-  hipLaunchKernelGGL(k_act_fwd, dim3(blocks_for(n8, 256)), dim3(256), 0, st, g, u, z, n8, act);
-  return hipGetLastError();
-}
-hipError_t launch_lora_rows(const void* X, int xbf16, int ldx, int M, int K, const float* W, int wt, int r, float s,
-                            float* out, hipStream_t st) {
-  const int rows = 256 / r;
-  if (xbf16)
-    hipLaunchKernelGGL(k_lora_rows<bf16>, dim3(blocks_for(M, rows)), dim3(256), 0, st, (const bf16*)X, ldx, M, K, W,
-                       wt, r, s, out);
-  else
-    hipLaunchKernelGGL(k_lora_rows<f16>, dim3(blocks_for(M, rows)), dim3(256), 0, st, (const f16*)X, ldx, M, K, W,
-                       wt, r, s, out);
-  return hipGetLastError();
-}
-int lora_outer_splits(int M) {
-  int s = (M + 255) / 256;
-  return s < 1 ? 1 : (s > 64 ? 64 : s);
-}
-hipError_t launch_lora_outer(const void* Mx, int mbf16, int ldm, int M, int C, const float* V, int r, float s,
-                             float* out, int layout, float* part, int splits, hipStream_t st) {
-  if (mbf16)
-    hipLaunchKernelGGL(k_lora_outer_part<bf16>, dim3(blocks_for(C, 256), splits), dim3(256), 0, st, (const bf16*)Mx,
-                       ldm, M, C, V, r, splits, part);
-  else
-    hipLaunchKernelGGL(k_lora_outer_part<f16>, dim3(blocks_for(C, 256), splits), dim3(256), 0, st, (const f16*)Mx,
-                       ldm, M, C, V, r, splits, part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_lora_outer_reduce, dim3(blocks_for((size_t)C * r, 256)), dim3(256), 0, st, part, splits, C, r,
-                     s, out, layout);
+  MEBP_TIMED(st, "act_fwd", 0.0, (double)n8 * 48,
+             hipLaunchKernelGGL(k_act_fwd, dim3(blocks_for(n8, 256)), dim3(256), 0, st, g, u, z, n8, act));
   return hipGetLastError();
 }
 hipError_t launch_targets(const int32_t* ids, int B, int T, int V, int32_t* tgt, hipStream_t st) {
-  hipLaunchKernelGGL(k_targets, dim3(blocks_for((size_t)B * T, 256)), dim3(256), 0, st, ids, B, T, V, tgt);
+  MEBP_TIMED(st, "targets", 0.0, (double)B * T * 8,
+             hipLaunchKernelGGL(k_targets, dim3(blocks_for((size_t)B * T, 256)), dim3(256), 0, st, ids, B, T, V, tgt));
   return hipGetLastError();
 }
 hipError_t launch_ce_rows(const float2* stats, int ntiles, const float* tgt_logit, const int32_t* tgt, int M,
                           float* lse, float* row_loss, hipStream_t st) {
-  hipLaunchKernelGGL(k_ce_rows, dim3(blocks_for(M, 4)), dim3(256), 0, st, stats, ntiles, tgt_logit, tgt, M, lse,
-                     row_loss);
+  MEBP_TIMED(st, "ce_rows", 0.0, (double)M * ntiles * 8,
+             hipLaunchKernelGGL(k_ce_rows, dim3(blocks_for(M, 4)), dim3(256), 0, st, stats, ntiles, tgt_logit, tgt, M, lse,
+                     row_loss));
   return hipGetLastError();
 }
 hipError_t launch_ce_loss(const float* row_loss, const int32_t* tgt, int M, float inv_n, float* loss,
                           hipStream_t st) {
   (void)tgt;
-  hipLaunchKernelGGL(k_ce_loss, dim3(1), dim3(256), 0, st, row_loss, M, inv_n, loss);
+  MEBP_TIMED(st, "ce_loss", 0.0, (double)M * 4,
+             hipLaunchKernelGGL(k_ce_loss, dim3(1), dim3(256), 0, st, row_loss, M, inv_n, loss));
   return hipGetLastError();
 }
 hipError_t launch_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
                                const uint16_t* escale, const int32_t* tgt, float inv_n, float* dhf,
                                hipStream_t st) {
   const size_t tot = (size_t)M * (d >> 3);
-  hipLaunchKernelGGL(k_ce_dh_reduce, dim3(blocks_for(tot, 256)), dim3(256), 0, st, part, splits, M, d, eq4, escale,
-                     tgt, inv_n, dhf);
+  MEBP_TIMED(st, "ce_dh_reduce", 0.0, (double)tot * 8 * 4 * (splits + 1),
+             hipLaunchKernelGGL(k_ce_dh_reduce, dim3(blocks_for(tot, 256)), dim3(256), 0, st, part, splits, M, d, eq4, escale,
+                     tgt, inv_n, dhf));
   return hipGetLastError();
 }
 hipError_t launch_splitk_reduce(const float* part, int splits, size_t n, float* out, hipStream_t st) {
   const size_t n4 = n >> 2;
-  hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks_for(n4, 256)), dim3(256), 0, st, part, splits, n4, out);
+  MEBP_TIMED(st, "splitk_reduce", 0.0, (double)n4 * 16 * (splits + 1),
+             hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks_for(n4, 256)), dim3(256), 0, st, part, splits, n4, out));
   return hipGetLastError();
 }
 

@@ -1,4 +1,4 @@
-// Int4 group-dequant GEMMs on bf16 MFMA (gfx950), the lazy decompression of Algorithm 1
+// Int4 group-dequant GEMMs on MFMA (gfx950), the lazy decompression of Algorithm 1
 // fused into the matrix products of every base projection and of the tied LM head.
 //
 // Both orientations use one 128x128 output tile per 256-thread workgroup (2x2 waves of
@@ -7,25 +7,30 @@
 // 32-group, decompressed once per workgroup into LDS (q*s exact in fp32, then rounded to
 // nearest even), and never exist as a 16-bit matrix in HBM.
 //
-// Operand precision: the forward orientation multiplies activations by weights and runs
-// in fp16 (v_mfma_f32_16x16x32_f16: same rate as bf16, 3 more mantissa bits, which keeps
-// the 24-34 layer recompute within the parity bound); the transposed orientation
-// multiplies gradients, whose magnitudes need bf16's exponent range, and runs in bf16.
-//
 //  * forward  ("NT"): C[m][n] = sum_k X[m][k] W[n][k]. A lane's MFMA B operand is 8
 //    consecutive k of one weight row, i.e. one dword of packed codes with one scale.
 //  * transposed ("TN", input gradients): C[m][c] = sum_n G[m][n] W[n][c]. The reduction
 //    runs over the weight's output dim, so each thread decompresses a 4-row x 8-column
 //    block and transposes it while packing, writing k-contiguous columns to LDS.
+//
+// Operand precision: the forward orientation multiplies activations by weights and runs
+// in fp16 (v_mfma_f32_16x16x32_f16: same rate as bf16, 3 more mantissa bits, which keeps
+// the 24-34 layer recompute within the parity bound); the transposed orientation
+// multiplies gradients, whose magnitudes need bf16's exponent range, and runs in bf16.
+//
+// Split-K: when the output has too few tiles to fill the chip (few tokens), the reduction
+// is split over gridDim.z workgroups per tile. Each writes its fp32 partial tile, then the
+// last one to arrive (counted with one atomic per tile) sums all partials in split order --
+// so the result does not depend on arrival order -- and runs the epilogue. The counter is
+// reset by that workgroup for the next launch.
 #include "device_common.h"
 #include "mebp_internal.h"
 
 namespace mebp {
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 64, LDT = BK + 8;  // LDS pitch in bf16 (144 B)
+constexpr int BM = 128, BN = 128, BK = 64, LDT = BK + 8;  // LDS pitch in 16-bit elements (144 B)
 constexpr int NTHREADS = 256;
-
 typedef uint16_t u16;
 
 template <class Op>
@@ -45,8 +50,8 @@ DEV void mma_tile(const u16* As, const u16* Bs, int wm, int wn, int lane, f32x4 
   }
 }
 
-// A-operand staging: 4 chunks of 8 bf16 per thread; chunk c = tid + 256 i covers row c>>3,
-// columns (c&7)*8 .. +8 of the 128x64 tile.
+// A-operand staging: 4 chunks of 8 elements per thread; chunk c = tid + 256 i covers row
+// c>>3, columns (c&7)*8 .. +8 of the 128x64 tile.
 DEV void load_a_tile(const u16* X, int lda, int M, int Kred, int m0, int k0, int tid, uint4 (&ra)[4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -63,11 +68,60 @@ DEV void store_a_tile(u16* As, int tid, const uint4 (&ra)[4]) {
   }
 }
 
+DEV void zero_acc(f32x4 (&acc)[4][4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+template <int N>
+struct IC {
+  static constexpr int value = N;
+};
+
+// Split-K exchange. Every workgroup of a tile stores its partial accumulators in MFMA
+// register order (lane-contiguous, 8-byte device-scope stores) into the plane of its
+// split; the last to arrive sums the planes in split order into acc and returns true.
+// The others return false and must exit.
+DEV bool splitk_reduce(f32x4 (&acc)[4][4], float* part, int* counter, int tile, int splits, int z, int tid) {
+  typedef unsigned long long u64;
+  u64* mine = (u64*)(part + (((size_t)tile * splits + z) * 256 + tid) * 64);
+#pragma unroll
+  for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < 4; ++tn) {
+      u64 w2[2];
+      __builtin_memcpy(w2, &acc[tm][tn], 16);
+      __hip_atomic_store(mine + (tm * 4 + tn) * 2, w2[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(mine + (tm * 4 + tn) * 2 + 1, w2[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  if (!arrive_last(counter, splits)) return false;
+  zero_acc(acc);
+  for (int zz = 0; zz < splits; ++zz) {
+    const u64* src = (const u64*)(part + (((size_t)tile * splits + zz) * 256 + tid) * 64);
+    u64 w[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) w[i] = __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < 4; ++tn) {
+        f32x4 v;
+        __builtin_memcpy(&v, &w[(tm * 4 + tn) * 2], 16);
+        acc[tm][tn] += v;
+      }
+  }
+  return true;
+}
+
 // ------------------------------------------------------------------------------ forward
 template <int EPI>
 __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 As[BM * LDT];
-  __shared__ __attribute__((aligned(16))) u16 Bs[BN * LDT];
+  __shared__ __attribute__((aligned(16))) u16 As2[2][BM * LDT];
+  __shared__ __attribute__((aligned(16))) u16 Bs2[2][BN * LDT];
+  u16* As = As2[0];
+  u16* Bs = Bs2[0];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int nt = blockIdx.x;
@@ -78,51 +132,65 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
   const int n0 = (nt - sg.tile0) * BN, m0 = blockIdx.y * BM;
   const int K = a.K, Nn = sg.N;
   const int nk = (K + BK - 1) / BK, kgroups = (K + 31) >> 5;
+  const int z = blockIdx.z, S = gridDim.z;
+  const int kt_begin = (int)((long long)nk * z / S), kt_end = (int)((long long)nk * (z + 1) / S);
 
-  uint4 ra[4];
-  uint32_t rb[4];
-  float rsc;
+  // three register stages of prefetched tiles, two LDS buffers
+  uint4 ra[3][4];
+  uint32_t rb[3][4];
+  float rsc[3];
   const int brow = tid >> 1, bhalf = tid & 1, bn = n0 + brow;
   const uint8_t* wrow = sg.q4 + (size_t)bn * (K >> 1);
 
-  auto gload = [&](int kt) {
+  auto gload = [&](auto S_, int kt) {
+    constexpr int st = decltype(S_)::value;
     const int k0 = kt * BK;
-    load_a_tile((const u16*)a.X, a.lda, a.M, K, m0, k0, tid, ra);
+    load_a_tile((const u16*)a.X, a.lda, a.M, K, m0, k0, tid, ra[st]);
     const int kb = k0 + 32 * bhalf;
     if (bn < Nn && kb < K) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int kk = kb + 8 * j;
-        rb[j] = kk < K ? *(const uint32_t*)(wrow + (kk >> 1)) : 0u;
+        rb[st][j] = kk < K ? *(const uint32_t*)(wrow + (kk >> 1)) : 0u;
       }
-      rsc = half_bits_to_f32(sg.scale[(size_t)bn * kgroups + (kb >> 5)]);
+      rsc[st] = half_bits_to_f32(sg.scale[(size_t)bn * kgroups + (kb >> 5)]);
     } else {
-      rb[0] = rb[1] = rb[2] = rb[3] = 0u;
-      rsc = 0.f;
+      rb[st][0] = rb[st][1] = rb[st][2] = rb[st][3] = 0u;
+      rsc[st] = 0.f;
     }
   };
-  auto sstore = [&]() {
-    store_a_tile(As, tid, ra);
+  auto sstore = [&](auto S_, auto B_) {
+    constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
+    store_a_tile(As2[bf], tid, ra[st]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) *(uint4*)(Bs + brow * LDT + 32 * bhalf + 8 * j) = dequant8<OpF16>(rb[j], rsc);
+    for (int j = 0; j < 4; ++j)
+      *(uint4*)(Bs2[bf] + brow * LDT + 32 * bhalf + 8 * j) = dequant8<OpF16>(rb[st][j], rsc[st]);
   };
 
   f32x4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  gload(0);
-  sstore();
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(kt + 1);
-    mma_tile<OpF16>(As, Bs, wm, wn, lane, acc);
+  zero_acc(acc);
+  // step for tile k (I = (k - kt_begin) % 6): prefetch k+3 into the stage k just vacated,
+  // multiply the LDS buffer of k, stage k+1 into the other buffer, one barrier.
+  auto step = [&](auto I_, int k) {
+    constexpr int I = decltype(I_)::value;
+    if (k + 3 < kt_end) gload(IC<I % 3>{}, k + 3);
+    mma_tile<OpF16>(As2[I % 2], Bs2[I % 2], wm, wn, lane, acc);
+    if (k + 1 < kt_end) sstore(IC<(I + 1) % 3>{}, IC<(I + 1) % 2>{});
     __syncthreads();
-    if (kt + 1 < nk) {
-      sstore();
-      __syncthreads();
+  };
+  if (kt_begin < kt_end) {
+    gload(IC<0>{}, kt_begin);
+    if (kt_begin + 1 < kt_end) gload(IC<1>{}, kt_begin + 1);
+    if (kt_begin + 2 < kt_end) gload(IC<2>{}, kt_begin + 2);
+    sstore(IC<0>{}, IC<0>{});
+    __syncthreads();
+    for (int k = kt_begin; k < kt_end; k += 6) {
+      step(IC<0>{}, k);
+      if (k + 1 < kt_end) step(IC<1>{}, k + 1);
+      if (k + 2 < kt_end) step(IC<2>{}, k + 2);
+      if (k + 3 < kt_end) step(IC<3>{}, k + 3);
+      if (k + 4 < kt_end) step(IC<4>{}, k + 4);
+      if (k + 5 < kt_end) step(IC<5>{}, k + 5);
     }
   }
 
@@ -173,11 +241,17 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
     }
     return;
   } else {
+    if (S > 1) {
+      const int tile = blockIdx.y * gridDim.x + blockIdx.x;
+      if (!splitk_reduce(acc, a.part, a.counters + tile, tile, S, z, tid))
+        return;
+    }
     const int r = a.r;
     const bool lora = sg.lora_B != nullptr;
     float* Us = (float*)As;  // [BM][r+1]
     float* Vs = (float*)Bs;  // [BN][r+1]
     if (lora) {
+      __syncthreads();
       for (int i = tid; i < BM * r; i += NTHREADS) {
         const int m = m0 + i / r;
         Us[(i / r) * (r + 1) + i % r] = m < a.M ? a.lora_s * sg.lora_u[(size_t)m * r + i % r] : 0.f;
@@ -220,12 +294,15 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
 // ---------------------------------------------------------------------------- transposed
 template <int EPI, int AMODE>
 __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 As[BM * LDT];
-  __shared__ __attribute__((aligned(16))) u16 Bs[BN * LDT];
+  __shared__ __attribute__((aligned(16))) u16 As2[2][BM * LDT];
+  __shared__ __attribute__((aligned(16))) u16 Bs2[2][BN * LDT];
+  u16* As = As2[0];
+  u16* Bs = Bs2[0];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int c0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
   const int Kout = a.Kout, kgroups = (Kout + 31) >> 5;
+  const int z = blockIdx.z, S = gridDim.z;
 
   int ntl[3], total = 0;
 #pragma unroll
@@ -233,11 +310,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     ntl[s] = s < a.nseg ? (a.seg[s].N + BK - 1) / BK : 0;
     total += ntl[s];
   }
-  int t_begin = 0, t_end = total;
-  if (EPI == TN_PARTIAL_F32) {
-    t_begin = (int)((long long)total * blockIdx.z / a.splits);
-    t_end = (int)((long long)total * (blockIdx.z + 1) / a.splits);
-  }
+  const int t_begin = (int)((long long)total * z / S), t_end = (int)((long long)total * (z + 1) / S);
 
   // softmax-mode row data (rows fixed per thread for the 4 A chunks)
   float rlse[4];
@@ -251,12 +324,13 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     }
   }
 
-  uint4 ra[4];
-  uint32_t rw[4];
-  float rsc[4];
+  // three register stages of prefetched tiles, two LDS buffers
+  uint4 ra[3][4];
+  uint32_t rw[3][4];
+  float rsc[3][4];
+  int cur_n0[3], cur_N[3];  // reduction offset / length of the tile held in a stage
   const int rq = tid >> 4, co = tid & 15;
   const int kc = c0 + 8 * co;
-  int cur_n0 = 0, cur_N = 0;  // reduction offset / length of the tile held in ra
 
   auto locate = [&](int t, int& s, int& n0) {
     if (t < ntl[0]) {
@@ -270,135 +344,155 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     }
     n0 = t * BK;
   };
-  auto gload = [&](int t) {
+  auto gload = [&](auto S_, int t) {
+    constexpr int st = decltype(S_)::value;
     int s, n0;
     locate(t, s, n0);
     const TnSeg& sg = a.seg[s];
-    cur_n0 = n0;
-    cur_N = sg.N;
-    load_a_tile((const u16*)sg.G, sg.ldg, a.M, sg.N, m0, n0, tid, ra);
+    cur_n0[st] = n0;
+    cur_N[st] = sg.N;
+    load_a_tile((const u16*)sg.G, sg.ldg, a.M, sg.N, m0, n0, tid, ra[st]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int n = n0 + 4 * rq + i;
       const bool ok = n < sg.N && kc < Kout;
-      rw[i] = ok ? *(const uint32_t*)(sg.q4 + (size_t)n * (Kout >> 1) + (kc >> 1)) : 0u;
-      rsc[i] = ok ? half_bits_to_f32(sg.scale[(size_t)n * kgroups + (kc >> 5)]) : 0.f;
+      rw[st][i] = ok ? *(const uint32_t*)(sg.q4 + (size_t)n * (Kout >> 1) + (kc >> 1)) : 0u;
+      rsc[st][i] = ok ? half_bits_to_f32(sg.scale[(size_t)n * kgroups + (kc >> 5)]) : 0.f;
     }
   };
-  auto sstore = [&]() {
+  auto sstore = [&](auto S_, auto B_) {
+    constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
     if constexpr (AMODE == TN_A_SOFTMAX) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int c = tid + NTHREADS * i;
         uint4 p = make_uint4(0, 0, 0, 0);
         // chunks past the reduction length were zero-filled; they must stay 0, not exp(-lse)
-        if (rval[i] && cur_n0 + (c & 7) * 8 < cur_N) {
-          const uint32_t* h = (const uint32_t*)&ra[i];
+        if (rval[i] && cur_n0[st] + (c & 7) * 8 < cur_N[st]) {
+          const uint32_t* h = (const uint32_t*)&ra[st][i];
           uint32_t o[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float lo = (float)__builtin_bit_cast(_Float16, (uint16_t)(h[j] & 0xffff));
-            const float hi = (float)__builtin_bit_cast(_Float16, (uint16_t)(h[j] >> 16));
-            o[j] = pack_bf16x2(__expf(lo - rlse[i]), __expf(hi - rlse[i]));
-          }
+          for (int j = 0; j < 4; ++j) o[j] = pack_bf16x2(__expf(f16_lo(h[j]) - rlse[i]), __expf(f16_hi(h[j]) - rlse[i]));
           p = make_uint4(o[0], o[1], o[2], o[3]);
         }
-        *(uint4*)(As + (c >> 3) * LDT + (c & 7) * 8) = p;
+        *(uint4*)(As2[bf] + (c >> 3) * LDT + (c & 7) * 8) = p;
       }
     } else {
-      store_a_tile(As, tid, ra);
+      store_a_tile(As2[bf], tid, ra[st]);
     }
     float v[4][8];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[i][j] = (float)nib_s(rw[i], j) * rsc[i];
+      for (int j = 0; j < 8; ++j) v[i][j] = (float)nib_s(rw[st][i], j) * rsc[st][i];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       uint2 pk;
       pk.x = pack_bf16x2(v[0][j], v[1][j]);
       pk.y = pack_bf16x2(v[2][j], v[3][j]);
-      *(uint2*)(Bs + (8 * co + j) * LDT + 4 * rq) = pk;
+      *(uint2*)(Bs2[bf] + (8 * co + j) * LDT + 4 * rq) = pk;
     }
   };
 
   f32x4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  if (t_begin < t_end) {
-    gload(t_begin);
-    sstore();
+  zero_acc(acc);
+  auto step = [&](auto I_, int t) {
+    constexpr int I = decltype(I_)::value;
+    if (t + 3 < t_end) gload(IC<I % 3>{}, t + 3);
+    mma_tile<OpBF16>(As2[I % 2], Bs2[I % 2], wm, wn, lane, acc);
+    if (t + 1 < t_end) sstore(IC<(I + 1) % 3>{}, IC<(I + 1) % 2>{});
     __syncthreads();
-    for (int t = t_begin; t < t_end; ++t) {
-      if (t + 1 < t_end) gload(t + 1);
-      mma_tile<OpBF16>(As, Bs, wm, wn, lane, acc);
-      __syncthreads();
-      if (t + 1 < t_end) {
-        sstore();
-        __syncthreads();
-      }
+  };
+  if (t_begin < t_end) {
+    gload(IC<0>{}, t_begin);
+    if (t_begin + 1 < t_end) gload(IC<1>{}, t_begin + 1);
+    if (t_begin + 2 < t_end) gload(IC<2>{}, t_begin + 2);
+    sstore(IC<0>{}, IC<0>{});
+    __syncthreads();
+    for (int t = t_begin; t < t_end; t += 6) {
+      step(IC<0>{}, t);
+      if (t + 1 < t_end) step(IC<1>{}, t + 1);
+      if (t + 2 < t_end) step(IC<2>{}, t + 2);
+      if (t + 3 < t_end) step(IC<3>{}, t + 3);
+      if (t + 4 < t_end) step(IC<4>{}, t + 4);
+      if (t + 5 < t_end) step(IC<5>{}, t + 5);
     }
   }
 
-  // LoRA term sum_seg du_seg[m][:] . A_seg[:][c] (split 0 only when split)
-  const int r = a.r;
-  const bool add_lora = (EPI != TN_PARTIAL_F32) || blockIdx.z == 0;
-  float* Us = (float*)As;  // [BM][r+1]
-  float* Vs = (float*)Bs;  // [BN][r+1]
-  for (int s = 0; s < a.nseg; ++s) {
-    const TnSeg& sg = a.seg[s];
-    if (!add_lora || sg.lora_A == nullptr) continue;
-    for (int i = tid; i < BM * r; i += NTHREADS) {
-      const int m = m0 + i / r;
-      Us[(i / r) * (r + 1) + i % r] = m < a.M ? sg.lora_du[(size_t)m * r + i % r] : 0.f;
-    }
-    for (int i = tid; i < BN * r; i += NTHREADS) {
-      const int j = i / BN, c = c0 + i % BN;
-      Vs[(i % BN) * (r + 1) + j] = c < Kout ? sg.lora_A[(size_t)j * Kout + c] : 0.f;
-    }
-    __syncthreads();
+  if constexpr (EPI == TN_PARTIAL_F32) {
+    // raw partial planes, reduced by the caller
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
-        const int ml = wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
+        const int m = m0 + wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
+        if (m >= a.M) continue;
 #pragma unroll
         for (int tn = 0; tn < 4; ++tn) {
-          const int nl = wn * 64 + tn * 16 + (lane & 15);
-          float l = 0.f;
-          for (int j = 0; j < r; ++j) l += Us[ml * (r + 1) + j] * Vs[nl * (r + 1) + j];
-          acc[tm][tn][rr] += l;
+          const int c = c0 + wn * 64 + tn * 16 + (lane & 15);
+          if (c < Kout) a.out[((size_t)z * a.M + m) * a.ldo + c] = acc[tm][tn][rr];
         }
       }
-    __syncthreads();
-  }
+    return;
+  } else {
+    if (S > 1) {
+      const int tile = blockIdx.y * gridDim.x + blockIdx.x;
+      if (!splitk_reduce(acc, a.part, a.counters + tile, tile, S, z, tid))
+        return;
+    }
+    // LoRA term sum_seg du_seg[m][:] . A_seg[:][c]
+    const int r = a.r;
+    float* Us = (float*)As;  // [BM][r+1]
+    float* Vs = (float*)Bs;  // [BN][r+1]
+    for (int s = 0; s < a.nseg; ++s) {
+      const TnSeg& sg = a.seg[s];
+      if (sg.lora_A == nullptr) continue;
+      __syncthreads();
+      for (int i = tid; i < BM * r; i += NTHREADS) {
+        const int m = m0 + i / r;
+        Us[(i / r) * (r + 1) + i % r] = m < a.M ? sg.lora_du[(size_t)m * r + i % r] : 0.f;
+      }
+      for (int i = tid; i < BN * r; i += NTHREADS) {
+        const int j = i / BN, c = c0 + i % BN;
+        Vs[(i % BN) * (r + 1) + j] = c < Kout ? sg.lora_A[(size_t)j * Kout + c] : 0.f;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int ml = wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
+#pragma unroll
+          for (int tn = 0; tn < 4; ++tn) {
+            const int nl = wn * 64 + tn * 16 + (lane & 15);
+            float l = 0.f;
+            for (int j = 0; j < r; ++j) l += Us[ml * (r + 1) + j] * Vs[nl * (r + 1) + j];
+            acc[tm][tn][rr] += l;
+          }
+        }
+    }
 
 #pragma unroll
-  for (int tm = 0; tm < 4; ++tm) {
+    for (int tm = 0; tm < 4; ++tm) {
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int m = m0 + wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
-      if (m >= a.M) continue;
+      for (int rr = 0; rr < 4; ++rr) {
+        const int m = m0 + wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
+        if (m >= a.M) continue;
 #pragma unroll
-      for (int tn = 0; tn < 4; ++tn) {
-        const int c = c0 + wn * 64 + tn * 16 + (lane & 15);
-        if (c >= Kout) continue;
-        const float v = acc[tm][tn][rr];
-        if constexpr (EPI == TN_STORE_F32) {
-          a.out[(size_t)m * a.ldo + c] = v;
-        } else if constexpr (EPI == TN_STORE_BF16) {
-          a.outb[(size_t)m * a.ldo + c] = to_bf16(v);
-        } else if constexpr (EPI == TN_PARTIAL_F32) {
-          a.out[((size_t)blockIdx.z * a.M + m) * a.ldo + c] = v;
-        } else {  // TN_ACT_BWD: v = dz
-          const size_t idx = (size_t)m * a.ldgu + c;
-          // reads fp16 g, u; overwrites them in place with bf16 dg, du
-          const float g = (float)((const f16*)a.g)[idx], u = (float)((const f16*)a.u)[idx];
-          ((bf16*)a.g)[idx] = to_bf16(v * u * act_grad_f(g, a.act));
-          ((bf16*)a.u)[idx] = to_bf16(v * act_f(g, a.act));
+        for (int tn = 0; tn < 4; ++tn) {
+          const int c = c0 + wn * 64 + tn * 16 + (lane & 15);
+          if (c >= Kout) continue;
+          const float v = acc[tm][tn][rr];
+          if constexpr (EPI == TN_STORE_F32) {
+            a.out[(size_t)m * a.ldo + c] = v;
+          } else if constexpr (EPI == TN_STORE_BF16) {
+            a.outb[(size_t)m * a.ldo + c] = to_bf16(v);
+          } else {  // TN_ACT_BWD: v = dz; reads fp16 g, u and overwrites them with bf16 dg, du
+            const size_t idx = (size_t)m * a.ldgu + c;
+            const float g = (float)((const f16*)a.g)[idx], u = (float)((const f16*)a.u)[idx];
+            ((bf16*)a.g)[idx] = to_bf16(v * u * act_grad_f(g, a.act));
+            ((bf16*)a.u)[idx] = to_bf16(v * act_f(g, a.act));
+          }
         }
       }
     }
@@ -409,30 +503,98 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
 
 int gemm_nt_tiles(int N) { return (N + BN - 1) / BN; }
 
-hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st) {
-  int tiles = 0;
-  for (int s = 0; s < a.nseg; ++s) tiles += gemm_nt_tiles(a.seg[s].N);
-  dim3 grid(tiles, (a.M + BM - 1) / BM);
+int gemm_splits(int tiles, int ktiles) {
+  if (tiles >= 160) return 1;
+  int s = (256 + tiles - 1) / tiles;
+  const int max_s = ktiles / 4;
+  if (s > max_s) s = max_s;
+  if (s > 8) s = 8;
+  return s < 1 ? 1 : s;
+}
+
+size_t gemm_part_floats(int tiles, int splits) { return splits > 1 ? (size_t)tiles * splits * NTHREADS * 64 : 0; }
+
+hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
+  NtArgs a = a0;
+  int tiles = 0, ncat = 0;
+  double flops = 0, bytes = (double)a.M * a.K * 2;
+  const int kg = (a.K + 31) / 32;
+  for (int s = 0; s < a.nseg; ++s) {
+    a.seg[s].tile0 = tiles;
+    a.seg[s].col0 = ncat;
+    tiles += gemm_nt_tiles(a.seg[s].N);
+    ncat += a.seg[s].N;
+    const double n = a.seg[s].N;
+    flops += 2.0 * a.M * n * a.K;
+    bytes += n * (a.K / 2 + 2 * kg) + (double)a.M * n * (epi == NT_STORE_F32 ? 4 : 2);
+    if (a.seg[s].resid) bytes += (double)a.M * n * 4;
+  }
+  const int mt = (a.M + BM - 1) / BM;
+  int S = epi == NT_LOGITS ? 1 : gemm_splits(tiles * mt, (a.K + BK - 1) / BK);
+  if (S > 1 && (!a.part || !a.counters || a.part_floats < gemm_part_floats(tiles * mt, S) || tiles * mt > a.ncounters))
+    S = 1;
+  a.ldp = ncat;
+  dim3 grid(tiles, mt, S);
   switch (epi) {
-    case NT_STORE_F16: hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F16>, grid, dim3(NTHREADS), 0, st, a); break;
-    case NT_STORE_F32: hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F32>, grid, dim3(NTHREADS), 0, st, a); break;
-    case NT_LOGITS: hipLaunchKernelGGL(k_gemm_nt<NT_LOGITS>, grid, dim3(NTHREADS), 0, st, a); break;
+    case NT_STORE_F16:
+      MEBP_TIMED(st, "gemm_nt_f16out", flops, bytes,
+                 hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F16>, grid, dim3(NTHREADS), 0, st, a));
+      break;
+    case NT_STORE_F32:
+      MEBP_TIMED(st, "gemm_nt_f32out", flops, bytes,
+                 hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F32>, grid, dim3(NTHREADS), 0, st, a));
+      break;
+    case NT_LOGITS:
+      MEBP_TIMED(st, "gemm_nt_logits", flops, bytes,
+                 hipLaunchKernelGGL(k_gemm_nt<NT_LOGITS>, grid, dim3(NTHREADS), 0, st, a));
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st) {
-  dim3 grid((a.Kout + BN - 1) / BN, (a.M + BM - 1) / BM, epi == TN_PARTIAL_F32 ? a.splits : 1);
+hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) {
+  TnArgs a = a0;
+  const int ct = (a.Kout + BN - 1) / BN, mt = (a.M + BM - 1) / BM;
+  int ktiles = 0;
+  double flops = 0, bytes = 0;
+  const int kg = (a.Kout + 31) / 32;
+  for (int s = 0; s < a.nseg; ++s) {
+    const double n = a.seg[s].N;
+    ktiles += (a.seg[s].N + BK - 1) / BK;
+    flops += 2.0 * a.M * n * a.Kout;
+    bytes += (double)a.M * n * 2 + n * (a.Kout / 2 + 2 * kg);
+  }
+  int S;
+  if (epi == TN_PARTIAL_F32) {
+    S = a.splits;
+  } else {
+    S = gemm_splits(ct * mt, ktiles);
+    if (S > 1 && (!a.part || !a.counters || a.part_floats < gemm_part_floats(ct * mt, S) || ct * mt > a.ncounters))
+      S = 1;
+  }
+  const double outb = (double)a.M * a.Kout;
+  bytes += epi == TN_STORE_BF16 ? 2 * outb : epi == TN_ACT_BWD ? 8 * outb
+         : epi == TN_PARTIAL_F32 ? 4 * outb * S : 4 * outb;
+  dim3 grid(ct, mt, S);
   if (amode == TN_A_SOFTMAX) {
     if (epi != TN_PARTIAL_F32) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32, TN_A_SOFTMAX>), grid, dim3(NTHREADS), 0, st, a);
+    MEBP_TIMED(st, "gemm_tn_softmax_dh", flops, bytes,
+               hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32, TN_A_SOFTMAX>), grid, dim3(NTHREADS), 0, st, a));
   } else {
     switch (epi) {
-      case TN_STORE_F32: hipLaunchKernelGGL((k_gemm_tn<TN_STORE_F32, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a); break;
-      case TN_ACT_BWD: hipLaunchKernelGGL((k_gemm_tn<TN_ACT_BWD, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a); break;
-      case TN_PARTIAL_F32: hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a); break;
-      case TN_STORE_BF16: hipLaunchKernelGGL((k_gemm_tn<TN_STORE_BF16, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a); break;
+      case TN_STORE_F32:
+        MEBP_TIMED(st, "gemm_tn_f32out", flops, bytes,
+                   hipLaunchKernelGGL((k_gemm_tn<TN_STORE_F32, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+        break;
+      case TN_ACT_BWD:
+        MEBP_TIMED(st, "gemm_tn_act_bwd", flops, bytes,
+                   hipLaunchKernelGGL((k_gemm_tn<TN_ACT_BWD, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+        break;
+      case TN_STORE_BF16:
+        MEBP_TIMED(st, "gemm_tn_bf16out", flops, bytes,
+                   hipLaunchKernelGGL((k_gemm_tn<TN_STORE_BF16, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+        break;
       default: return hipErrorInvalidValue;
     }
   }

@@ -21,7 +21,8 @@ struct NtSeg {
   const uint8_t* q4;
   const uint16_t* scale;
   int N;
-  int tile0;              // first N-tile index of this segment in the grid
+  int tile0;              // first N-tile index of this segment in the grid (set by the launcher)
+  int col0;               // first column of this segment in the split-K partial planes
   const float* lora_u;    // [M][r] (LoRA down-projection output), or null
   const float* lora_B;    // [N][r], or null
   void* out;              // fp16 or fp32 [M][ldo]
@@ -43,9 +44,18 @@ struct NtArgs {
   const int32_t* tgt;     // [M] target id or -1
   float* tgt_logit;
   int ntiles;
+  // split-K scratch (unused when the launcher picks one split)
+  float* part;
+  size_t part_floats;
+  int* counters;          // zero on entry; left zero on exit
+  int ncounters;
+  int ldp;                // set by the launcher
 };
 hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st);
 int gemm_nt_tiles(int N);  // number of 128-wide N tiles
+int gemm_splits(int tiles, int ktiles);
+size_t gemm_part_floats(int tiles, int splits);
+constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 64;
 
 // Transposed orientation (input gradients): C[m][c] = sum_seg sum_n G_seg[m][n] * W_seg[n][c]
 // with W_seg int4 [N_seg][Kout/2]; reduction over the weight's output dim; G bf16 (bf16
@@ -81,6 +91,11 @@ struct TnArgs {
   // TN_A_SOFTMAX: p[m][v] = exp(logit - lse[m]) for rows with a target, else 0
   const float* lse;
   const int32_t* tgt;
+  // split-K scratch for the stored epilogues (unused with one split)
+  float* part;
+  size_t part_floats;
+  int* counters;
+  int ncounters;
 };
 hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st);
 
@@ -102,16 +117,25 @@ hipError_t launch_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const fl
 hipError_t launch_act_fwd(const f16* g, const f16* u, f16* z, size_t n, int act, hipStream_t st);
 
 // ---------------------------------------------------------------- LoRA skinny kernels
+// Split scratch shared by the LoRA kernels: partial planes plus per-block counters.
+struct SplitScratch {
+  float* part;
+  size_t part_floats;
+  int* counters;           // zero on entry; left zero on exit
+  int ncounters;
+};
 // out[m][j] = s * sum_k X[m][k] * W(j, k), W(j,k) = W[j*K + k] (Wt=0, A [r][K]) or
 // W[k*r + j] (Wt=1, B [K][r]). X [M][ldx] fp16 (xbf16 = 0) or bf16 (xbf16 = 1).
 hipError_t launch_lora_rows(const void* X, int xbf16, int ldx, int M, int K, const float* W, int wt, int r,
-                            float s, float* out, hipStream_t st);
+                            float s, float* out, const SplitScratch& sc, hipStream_t st);
 // R(c, j) = s * sum_m Mx[m][c] * V[m][j]: out[c*r + j] (layout 0, dB [C][r]) or
 // out[j*C + c] (layout 1, dA [r][C]). Mx [M][ldm] fp16 (mbf16 = 0) or bf16 (mbf16 = 1),
-// V fp32 [M][r]. `part` is a workspace of splits*C*r floats.
+// V fp32 [M][r].
 hipError_t launch_lora_outer(const void* Mx, int mbf16, int ldm, int M, int C, const float* V, int r, float s,
-                             float* out, int layout, float* part, int splits, hipStream_t st);
-int lora_outer_splits(int M);
+                             float* out, int layout, const SplitScratch& sc, hipStream_t st);
+size_t lora_rows_part_floats(int M, int K, int r);
+size_t lora_outer_part_floats(int M, int C, int r);
+hipError_t launch_fill_i32(int* p, int n, int v, hipStream_t st);
 
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
@@ -126,7 +150,10 @@ struct AttnArgs {
   bf16* dq; bf16* dk; bf16* dv;                  // gradients (dq, dk pre-RoPE)
 };
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st);
-hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, hipStream_t st);
+// scratch: delta [B][Hq][T]; when Hq > Hkv, per-head dK/dV partials (2*B*T*Hq*dh floats)
+// reduced in-kernel by the last workgroup of each key block (counters: B*Hkv*ceil(T/64)).
+hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, const SplitScratch& sc, hipStream_t st);
+size_t attn_bwd_part_floats(int B, int T, int Hq, int Hkv, int dh);
 
 // ---------------------------------------------------------------- LM head / CE
 // lse[m], loss term per row from partial stats; loss = mean over rows with target
@@ -140,5 +167,20 @@ hipError_t launch_ce_dh_reduce(const float* part, int splits, int M, int d, cons
                                hipStream_t st);
 hipError_t launch_targets(const int32_t* ids, int B, int T, int V, int32_t* tgt, hipStream_t st);
 hipError_t launch_splitk_reduce(const float* part, int splits, size_t n, float* out, hipStream_t st);
+
+// ---------------------------------------------------------------- diagnostics
+// Per-kernel event timing (see timing.hip). timer_begin returns -1 when disabled.
+int timer_begin(hipStream_t st, const char* name, double flops, double bytes);
+void timer_end(hipStream_t st, int token);
+int timing_enable(int enable, int capacity);
+int timing_report(char* buf, size_t len);
+
+// Bracket one launch statement with the optional timer.
+#define MEBP_TIMED(st, name, flops, bytes, stmt)                \
+  do {                                                          \
+    const int tok_ = ::mebp::timer_begin((st), (name), (flops), (bytes)); \
+    stmt;                                                       \
+    ::mebp::timer_end((st), tok_);                              \
+  } while (0)
 
 }  // namespace mebp
