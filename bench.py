@@ -52,6 +52,7 @@ def main():
     ap.add_argument("--workload", default="qwen2.5-0.5b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=3, help="extra steps with per-kernel event timing")
+    ap.add_argument("--graph", type=int, default=1, help="replay the step as one captured HIP graph (1) or launch eagerly (0)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}); the multi-GPU path is not "
@@ -77,13 +78,29 @@ def main():
         dm.train_step(dx0)
     torch.cuda.synchronize()
     log("warmup done")
+    run_step = lambda: dm.train_step(dx0)
+    graph = None
+    if args.graph:
+        # capture one whole step (every kernel of the library, no allocation, no host sync)
+        # on a side stream, then replay it; the eager step above already validated inputs
+        s_cap = torch.cuda.Stream()
+        s_cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s_cap):
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=s_cap):
+                dm.train_step(dx0)
+        torch.cuda.current_stream().wait_stream(s_cap)
+        graph.replay()
+        torch.cuda.synchronize()
+        run_step = graph.replay
+        log("captured the step as a HIP graph")
 
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     ev0.record(stream)
     for _ in range(args.steps):
-        dm.train_step(dx0)
+        run_step()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -154,6 +171,7 @@ def main():
                    "global_batch": cfg.batch, "seq_len": cfg.seq, "lora": f"r{cfg.lora_rank} a{cfg.lora_alpha:g} "
                    + ",".join(cfg.lora_modules), "weights": "int4 group-32, fp16 scales", "parallelism": "none"},
         "step_mfma_frac": round(step_flops / (ms / 1e3) / 1e12 / PEAK_TFLOPS_16BIT, 4),
+        "launch": "hip_graph" if graph is not None else "eager",
         "loss": loss,
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -63,14 +63,13 @@ size_t nt_part(int M, int K, std::initializer_list<int> Ns) {
     ncat += n;
   }
   const int mt = (M + kGemmBM - 1) / kGemmBM;
-  (void)ncat;
-  return gemm_part_floats(tiles * mt, gemm_splits(tiles * mt, (K + kGemmBK - 1) / kGemmBK));
+  return gemm_part_floats(M, ncat, gemm_splits(tiles * mt, (K + kGemmBK - 1) / kGemmBK));
 }
 size_t tn_part(int M, int Kout, std::initializer_list<int> Ns) {
   int kt = 0;
   for (int n : Ns) kt += (n + kGemmBK - 1) / kGemmBK;
   const int tiles = ((Kout + kGemmBN - 1) / kGemmBN) * ((M + kGemmBM - 1) / kGemmBM);
-  return gemm_part_floats(tiles, gemm_splits(tiles, kt));
+  return gemm_part_floats(M, Kout, gemm_splits(tiles, kt));
 }
 
 int lm_head_splits(int N, int d, int V) {
@@ -138,10 +137,8 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
     mx(tn_part(M, D, {FF, FF}));
     mx(tn_part(M, Q, {D}));
     mx(tn_part(M, D, {Q, KV, KV}));
-    for (int dim : {D, Q, KV, FF}) {
-      mx(lora_rows_part_floats(M, dim, R));
-      mx(lora_outer_part_floats(M, dim, R));
-    }
+    mx(lora_outer_part_floats(M, D > Q ? D : Q, R, 3));
+    mx(lora_outer_part_floats(M, FF > D ? FF : D, R, 2));
     mx(attn_bwd_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim));
     L->split_floats = m;
     sz[S_SPLIT] = m * 4;
@@ -221,6 +218,8 @@ int check_layer(const mebp_config* c, int layer, const mebp_layer_base* base, co
     if (e) return e;
     if (c->lora_mask >> p & 1) {
       if (!lora->A[p] || !lora->B[p]) return fail(MEBP_EINVAL, "LoRA %s: NULL A or B", kProjName[p]);
+      if (!aligned(lora->A[p], 16) || !aligned(lora->B[p], 16))
+        return fail(MEBP_EINVAL, "LoRA %s: A or B not 16-byte aligned", kProjName[p]);
     }
   }
   if (!base->norm_attn || !base->norm_mlp) return fail(MEBP_EINVAL, "NULL norm weight");
@@ -343,28 +342,55 @@ TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* l
   return s;
 }
 
-// u_p = X A_p^T for each adapted projection p in `ps` (LoRA down-projection; X fp16)
+// u_p = X A_p^T for the adapted projections among `ps` (LoRA down-projection; X fp16),
+// one launch for all of them.
 hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const f16* X, int K, std::initializer_list<int> ps) {
+  LoraRowsArgs a{};
+  a.M = x.D.N;
+  a.r = x.D.r;
+  a.wt = 0;
+  a.s = 1.0f;
   for (int p : ps) {
     if (!adapted(x, p)) continue;
-    hipError_t e = launch_lora_rows(X, 0, K, x.D.N, K, lora->A[p], 0, x.D.r, 1.0f, lu(x, p), scratch(x), x.st);
-    if (e != hipSuccess) return e;
+    a.job[a.njobs++] = LoraRowsJob{X, K, K, lora->A[p], lu(x, p)};
   }
-  return hipSuccess;
+  if (a.njobs == 0) return hipSuccess;
+  return launch_lora_rows(a, 0, x.st);
 }
 
-// LoRA backward of projection p with output gradient G (bf16 [N][out]) and input X
-// (fp16 [N][in]): du = s G B, dB = s G^T u, dA = du^T X.
-hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_lora_grad* grads, int p,
-                    const bf16* G, const f16* X) {
-  if (!adapted(x, p)) return hipSuccess;
+// LoRA backward of the adapted projections among `ps`, with output gradients G_p (bf16
+// [N][out_p]) and the shared input X (fp16 [N][in]): du = s G B, dB = s G^T u, dA = du^T X.
+// Three launches for all of them.
+hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_lora_grad* grads,
+                    std::initializer_list<int> ps, std::initializer_list<const bf16*> Gs, const f16* X) {
   const Dims& D = x.D;
+  LoraRowsArgs ra{};
+  ra.M = D.N;
+  ra.r = D.r;
+  ra.wt = 1;
+  ra.s = D.s;
+  LoraOuterArgs ob{}, oa{};
+  ob.M = oa.M = D.N;
+  ob.r = oa.r = D.r;
+  ob.layout = 0;
+  oa.layout = 1;
   const SplitScratch sc = scratch(x);
-  hipError_t e = launch_lora_rows(G, 1, D.out[p], D.N, D.out[p], lora->B[p], 1, D.r, D.s, ldu(x, p), sc, x.st);
+  ob.part = oa.part = sc.part;
+  ob.part_floats = oa.part_floats = sc.part_floats;
+  auto g = Gs.begin();
+  for (int p : ps) {
+    const bf16* G = *g++;
+    if (!adapted(x, p)) continue;
+    ra.job[ra.njobs++] = LoraRowsJob{G, D.out[p], D.out[p], lora->B[p], ldu(x, p)};
+    ob.job[ob.njobs++] = LoraOuterJob{G, D.out[p], D.out[p], lu(x, p), grads->dB[p], D.s};
+    oa.job[oa.njobs++] = LoraOuterJob{X, D.in[p], D.in[p], ldu(x, p), grads->dA[p], 1.0f};
+  }
+  if (ra.njobs == 0) return hipSuccess;
+  hipError_t e = launch_lora_rows(ra, 1, x.st);
   if (e != hipSuccess) return e;
-  e = launch_lora_outer(G, 1, D.out[p], D.N, D.out[p], lu(x, p), D.r, D.s, grads->dB[p], 0, sc, x.st);
+  e = launch_lora_outer(ob, 1, x.st);
   if (e != hipSuccess) return e;
-  return launch_lora_outer(X, 0, D.in[p], D.N, D.in[p], ldu(x, p), D.r, 1.0f, grads->dA[p], 1, sc, x.st);
+  return launch_lora_outer(oa, 0, x.st);
 }
 
 // Forward of one layer. keep=false: full forward to x_out. keep=true: recompute for the
@@ -413,9 +439,12 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   return MEBP_OK;
 }
 
+// dy_bf16_ready: the workspace's dy_bf16 slot already holds bf16(dy) (written by the
+// block above in the same training step). On return the slot holds bf16(dx) when dx is
+// computed.
 int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora,
                    const float* x_ckpt, const float* dy, float* dx, const mebp_layer_lora_grad* grads,
-                   const float* rope) {
+                   const float* rope, bool dy_bf16_ready = false) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
   int e = layer_forward(x, l, base, lora, x_ckpt, nullptr, rope, true);
@@ -441,8 +470,8 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   float* da = slot<float>(x.ws, x.L, S_DA);
 
   // y = h + down(z)
-  HIP_TRY(launch_f32_to_bf16(dy, dyb, (size_t)D.N * D.d, x.st));
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_DOWN, dyb, z));
+  if (!dy_bf16_ready) HIP_TRY(launch_f32_to_bf16(dy, dyb, (size_t)D.N * D.d, x.st));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_DOWN}, {dyb}, z));
   {
     TnArgs t{};
     set_scratch(x, t);
@@ -454,8 +483,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   // z = act(gate(c)) * up(c)
   bf16* dg = (bf16*)g;  // the act-backward epilogue left bf16 dg / du in the g / u buffers
   bf16* dup = (bf16*)u;
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_GATE, dg, cc));
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_UP, dup, cc));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_GATE, MEBP_UP}, {dg, dup}, cc));
   {
     TnArgs t{};
     set_scratch(x, t);
@@ -467,7 +495,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   }
   // c = RMSNorm(h); h = x + o(O)
   HIP_TRY(launch_rmsnorm_bwd(h, base->norm_mlp, dc, dy, D.N, D.d, c->rms_eps, dh, dhb, x.st));
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_O, dhb, o));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_O}, {dhb}, o));
   {
     TnArgs t{};
     set_scratch(x, t);
@@ -486,9 +514,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
     at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
     HIP_TRY(launch_attn_bwd(at, slot<float>(x.ws, x.L, S_DELTA), scratch(x), x.st));
   }
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_Q, dq, a));
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_K, dk, a));
-  HIP_TRY(lora_bwd(x, lora, grads, MEBP_V, dv, a));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_Q, MEBP_K, MEBP_V}, {dq, dk, dv}, a));
   if (dx) {
     TnArgs t{};
     set_scratch(x, t);
@@ -499,7 +525,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
     t.out = da; t.ldo = D.d;
     HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
     // a = RMSNorm(x): dx = dh + rmsnorm_bwd(x, da)  (dx may alias dy: dy is no longer read)
-    HIP_TRY(launch_rmsnorm_bwd(x_ckpt, base->norm_attn, da, dh, D.N, D.d, c->rms_eps, dx, nullptr, x.st));
+    HIP_TRY(launch_rmsnorm_bwd(x_ckpt, base->norm_attn, da, dh, D.N, D.d, c->rms_eps, dx, dyb, x.st));
   }
   return MEBP_OK;
 }
@@ -543,7 +569,8 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
     HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_SOFTMAX, x.st));
   }
   HIP_TRY(launch_ce_dh_reduce(part, x.L.lm_splits, D.N, D.d, emb->q4, emb->scale, tgt, inv_n, dhf, x.st));
-  HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, D.N, D.d, c->rms_eps, dx_last, nullptr, x.st));
+  HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, D.N, D.d, c->rms_eps, dx_last,
+                             slot<bf16>(x.ws, x.L, S_DYB), x.st));
   return MEBP_OK;
 }
 
@@ -700,7 +727,8 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   for (int l = cfg->n_layers - 1; l >= 0; --l) {
     const float* rope = is_global(cfg, l) ? rope_g : rope_l;
     float* dxl = l > 0 ? g : dx0;
-    if ((e = layer_backward(x, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr, rope)))
+    if ((e = layer_backward(x, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr, rope,
+                            true)))
       return e;
   }
   return MEBP_OK;

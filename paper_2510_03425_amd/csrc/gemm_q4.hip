@@ -19,10 +19,11 @@
 // multiplies gradients, whose magnitudes need bf16's exponent range, and runs in bf16.
 //
 // Split-K: when the output has too few tiles to fill the chip (few tokens), the reduction
-// is split over gridDim.z workgroups per tile. Each writes its fp32 partial tile, then the
-// last one to arrive (counted with one atomic per tile) sums all partials in split order --
-// so the result does not depend on arrival order -- and runs the epilogue. The counter is
-// reset by that workgroup for the next launch.
+// is split over gridDim.z workgroups per tile. Each writes its fp32 partial plane; a
+// finalize kernel spread over the whole chip sums the planes in split order (so the
+// result does not depend on scheduling) and applies the epilogue.
+#include <stdlib.h>
+
 #include "device_common.h"
 #include "mebp_internal.h"
 
@@ -80,39 +81,22 @@ struct IC {
   static constexpr int value = N;
 };
 
-// Split-K exchange. Every workgroup of a tile stores its partial accumulators in MFMA
-// register order (lane-contiguous, 8-byte device-scope stores) into the plane of its
-// split; the last to arrive sums the planes in split order into acc and returns true.
-// The others return false and must exit.
-DEV bool splitk_reduce(f32x4 (&acc)[4][4], float* part, int* counter, int tile, int splits, int z, int tid) {
-  typedef unsigned long long u64;
-  u64* mine = (u64*)(part + (((size_t)tile * splits + z) * 256 + tid) * 64);
+// Split-K: store this workgroup's partial tile into the plane of its split, row-major
+// [M][ldp] fp32 at column offset c0 (the finalize kernel reduces the planes in order).
+DEV void store_partial(const f32x4 (&acc)[4][4], float* plane, int M, int ldp, int ncols, int m0, int c0, int wm,
+                       int wn, int lane) {
 #pragma unroll
   for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-      u64 w2[2];
-      __builtin_memcpy(w2, &acc[tm][tn], 16);
-      __hip_atomic_store(mine + (tm * 4 + tn) * 2, w2[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(mine + (tm * 4 + tn) * 2 + 1, w2[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  if (!arrive_last(counter, splits)) return false;
-  zero_acc(acc);
-  for (int zz = 0; zz < splits; ++zz) {
-    const u64* src = (const u64*)(part + (((size_t)tile * splits + zz) * 256 + tid) * 64);
-    u64 w[32];
-#pragma unroll
-    for (int i = 0; i < 32; ++i) w[i] = __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-    for (int tm = 0; tm < 4; ++tm)
+    for (int rr = 0; rr < 4; ++rr) {
+      const int m = m0 + wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
+      if (m >= M) continue;
 #pragma unroll
       for (int tn = 0; tn < 4; ++tn) {
-        f32x4 v;
-        __builtin_memcpy(&v, &w[(tm * 4 + tn) * 2], 16);
-        acc[tm][tn] += v;
+        const int c = wn * 64 + tn * 16 + (lane & 15);
+        if (c < ncols) plane[(size_t)m * ldp + c0 + c] = acc[tm][tn][rr];
       }
-  }
-  return true;
+    }
 }
 
 // ------------------------------------------------------------------------------ forward
@@ -242,9 +226,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
     return;
   } else {
     if (S > 1) {
-      const int tile = blockIdx.y * gridDim.x + blockIdx.x;
-      if (!splitk_reduce(acc, a.part, a.counters + tile, tile, S, z, tid))
-        return;
+      store_partial(acc, a.part + (size_t)z * a.M * a.ldp, a.M, a.ldp, Nn - n0, m0, sg.col0 + n0, wm, wn, lane);
+      return;
     }
     const int r = a.r;
     const bool lora = sg.lora_B != nullptr;
@@ -436,9 +419,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     return;
   } else {
     if (S > 1) {
-      const int tile = blockIdx.y * gridDim.x + blockIdx.x;
-      if (!splitk_reduce(acc, a.part, a.counters + tile, tile, S, z, tid))
-        return;
+      store_partial(acc, a.part + (size_t)z * a.M * Kout, a.M, Kout, Kout - c0, m0, c0, wm, wn, lane);
+      return;
     }
     // LoRA term sum_seg du_seg[m][:] . A_seg[:][c]
     const int r = a.r;
@@ -499,20 +481,112 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
   }
 }
 
+// ------------------------------------------------------------------------ split finalize
+// Sum the split planes in split order and apply the stored epilogue; one thread per 4
+// consecutive output columns of one row (all segment widths are multiples of 4).
+template <int EPI>
+__global__ __launch_bounds__(256) void k_nt_finalize(const NtArgs a, int S) {
+  const int c4n = a.ldp >> 2;
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)a.M * c4n) return;
+  const int m = (int)(i / c4n), col = (int)(i % c4n) * 4;
+  int s = 0;
+  if (a.nseg > 1 && col >= a.seg[1].col0) s = 1;
+  if (a.nseg > 2 && col >= a.seg[2].col0) s = 2;
+  const NtSeg& sg = a.seg[s];
+  const int n = col - sg.col0;
+  float4 v = *(const float4*)(a.part + (size_t)m * a.ldp + col);
+  for (int z = 1; z < S; ++z) {
+    const float4 w = *(const float4*)(a.part + ((size_t)z * a.M + m) * a.ldp + col);
+    v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+  }
+  float o[4] = {v.x, v.y, v.z, v.w};
+  if (sg.lora_B) {
+    const int r = a.r;
+    const float* u = sg.lora_u + (size_t)m * r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float* b = sg.lora_B + (size_t)(n + q) * r;
+      float l = 0.f;
+      for (int j = 0; j < r; ++j) l += u[j] * b[j];
+      o[q] += a.lora_s * l;
+    }
+  }
+  if (sg.resid) {
+    const float4 rv = *(const float4*)(sg.resid + (size_t)m * sg.ldr + n);
+    o[0] += rv.x; o[1] += rv.y; o[2] += rv.z; o[3] += rv.w;
+  }
+  if constexpr (EPI == NT_STORE_F16) {
+    *(uint2*)((f16*)sg.out + (size_t)m * sg.ldo + n) = make_uint2(pack_f16x2(o[0], o[1]), pack_f16x2(o[2], o[3]));
+  } else {
+    *(float4*)((float*)sg.out + (size_t)m * sg.ldo + n) = make_float4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void k_tn_finalize(const TnArgs a, int S) {
+  const int c4n = a.Kout >> 2;
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)a.M * c4n) return;
+  const int m = (int)(i / c4n), c = (int)(i % c4n) * 4;
+  float4 v = *(const float4*)(a.part + (size_t)m * a.Kout + c);
+  for (int z = 1; z < S; ++z) {
+    const float4 w = *(const float4*)(a.part + ((size_t)z * a.M + m) * a.Kout + c);
+    v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+  }
+  float o[4] = {v.x, v.y, v.z, v.w};
+  for (int sgi = 0; sgi < a.nseg; ++sgi) {
+    const TnSeg& sg = a.seg[sgi];
+    if (!sg.lora_A) continue;
+    const float* du = sg.lora_du + (size_t)m * a.r;
+    for (int j = 0; j < a.r; ++j) {
+      const float4 av = *(const float4*)(sg.lora_A + (size_t)j * a.Kout + c);
+      o[0] += du[j] * av.x; o[1] += du[j] * av.y; o[2] += du[j] * av.z; o[3] += du[j] * av.w;
+    }
+  }
+  if constexpr (EPI == TN_STORE_F32) {
+    *(float4*)(a.out + (size_t)m * a.ldo + c) = make_float4(o[0], o[1], o[2], o[3]);
+  } else if constexpr (EPI == TN_STORE_BF16) {
+    *(uint2*)(a.outb + (size_t)m * a.ldo + c) = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+  } else {  // TN_ACT_BWD
+    const size_t idx = (size_t)m * a.ldgu + c;
+    const uint2 gv = *(const uint2*)((const f16*)a.g + idx), uv = *(const uint2*)((const f16*)a.u + idx);
+    const float g[4] = {f16_lo(gv.x), f16_hi(gv.x), f16_lo(gv.y), f16_hi(gv.y)};
+    const float u[4] = {f16_lo(uv.x), f16_hi(uv.x), f16_lo(uv.y), f16_hi(uv.y)};
+    float dg[4], dup[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      dg[q] = o[q] * u[q] * act_grad_f(g[q], a.act);
+      dup[q] = o[q] * act_f(g[q], a.act);
+    }
+    *(uint2*)((bf16*)a.g + idx) = make_uint2(pack_bf16x2(dg[0], dg[1]), pack_bf16x2(dg[2], dg[3]));
+    *(uint2*)((bf16*)a.u + idx) = make_uint2(pack_bf16x2(dup[0], dup[1]), pack_bf16x2(dup[2], dup[3]));
+  }
+}
+
 }  // namespace
 
 int gemm_nt_tiles(int N) { return (N + BN - 1) / BN; }
 
+// Tuning knobs (environment, read once): MEBP_SPLIT_MAX caps the split count, MEBP_SPLIT_TARGET
+// is the workgroup count the split aims for, MEBP_SPLIT_MIN_KTILES the smallest slice.
+static int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  return v && *v ? atoi(v) : dflt;
+}
 int gemm_splits(int tiles, int ktiles) {
-  if (tiles >= 160) return 1;
-  int s = (256 + tiles - 1) / tiles;
-  const int max_s = ktiles / 4;
+  static const int max_splits = env_int("MEBP_SPLIT_MAX", 16);
+  static const int target = env_int("MEBP_SPLIT_TARGET", 256);
+  static const int min_kt = env_int("MEBP_SPLIT_MIN_KTILES", 2);
+  if (tiles >= target * 5 / 8) return 1;
+  int s = (target + tiles - 1) / tiles;
+  const int max_s = ktiles / (min_kt > 0 ? min_kt : 1);
   if (s > max_s) s = max_s;
-  if (s > 8) s = 8;
+  if (s > max_splits) s = max_splits;
   return s < 1 ? 1 : s;
 }
 
-size_t gemm_part_floats(int tiles, int splits) { return splits > 1 ? (size_t)tiles * splits * NTHREADS * 64 : 0; }
+size_t gemm_part_floats(int M, int ncols, int splits) { return splits > 1 ? (size_t)splits * M * ncols : 0; }
 
 hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
   NtArgs a = a0;
@@ -531,8 +605,7 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
   }
   const int mt = (a.M + BM - 1) / BM;
   int S = epi == NT_LOGITS ? 1 : gemm_splits(tiles * mt, (a.K + BK - 1) / BK);
-  if (S > 1 && (!a.part || !a.counters || a.part_floats < gemm_part_floats(tiles * mt, S) || tiles * mt > a.ncounters))
-    S = 1;
+  if (S > 1 && (!a.part || a.part_floats < gemm_part_floats(a.M, ncat, S))) S = 1;
   a.ldp = ncat;
   dim3 grid(tiles, mt, S);
   switch (epi) {
@@ -550,6 +623,15 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
       break;
     default: return hipErrorInvalidValue;
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || S == 1) return e;
+  const size_t nthr = (size_t)a.M * (ncat / 4);
+  const dim3 fg((unsigned)((nthr + 255) / 256));
+  const double fb = 4.0 * S * a.M * ncat + (double)a.M * ncat * (epi == NT_STORE_F16 ? 2 : 4);
+  if (epi == NT_STORE_F16)
+    MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_nt_finalize<NT_STORE_F16>, fg, dim3(256), 0, st, a, S));
+  else
+    MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_nt_finalize<NT_STORE_F32>, fg, dim3(256), 0, st, a, S));
   return hipGetLastError();
 }
 
@@ -570,8 +652,7 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
     S = a.splits;
   } else {
     S = gemm_splits(ct * mt, ktiles);
-    if (S > 1 && (!a.part || !a.counters || a.part_floats < gemm_part_floats(ct * mt, S) || ct * mt > a.ncounters))
-      S = 1;
+    if (S > 1 && (!a.part || a.part_floats < gemm_part_floats(a.M, a.Kout, S))) S = 1;
   }
   const double outb = (double)a.M * a.Kout;
   bytes += epi == TN_STORE_BF16 ? 2 * outb : epi == TN_ACT_BWD ? 8 * outb
@@ -597,6 +678,22 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
         break;
       default: return hipErrorInvalidValue;
     }
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || S == 1 || epi == TN_PARTIAL_F32) return e;
+  const size_t nthr = (size_t)a.M * (a.Kout / 4);
+  const dim3 fg((unsigned)((nthr + 255) / 256));
+  const double fb = 4.0 * S * a.M * a.Kout + outb * (epi == TN_ACT_BWD ? 8 : epi == TN_STORE_BF16 ? 2 : 4);
+  switch (epi) {
+    case TN_STORE_F32:
+      MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_STORE_F32>, fg, dim3(256), 0, st, a, S));
+      break;
+    case TN_ACT_BWD:
+      MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_ACT_BWD>, fg, dim3(256), 0, st, a, S));
+      break;
+    default:
+      MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_STORE_BF16>, fg, dim3(256), 0, st, a, S));
+      break;
   }
   return hipGetLastError();
 }

@@ -54,7 +54,7 @@ struct NtArgs {
 hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st);
 int gemm_nt_tiles(int N);  // number of 128-wide N tiles
 int gemm_splits(int tiles, int ktiles);
-size_t gemm_part_floats(int tiles, int splits);
+size_t gemm_part_floats(int M, int ncols, int splits);
 constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 64;
 
 // Transposed orientation (input gradients): C[m][c] = sum_seg sum_n G_seg[m][n] * W_seg[n][c]
@@ -124,17 +124,41 @@ struct SplitScratch {
   int* counters;           // zero on entry; left zero on exit
   int ncounters;
 };
-// out[m][j] = s * sum_k X[m][k] * W(j, k), W(j,k) = W[j*K + k] (Wt=0, A [r][K]) or
-// W[k*r + j] (Wt=1, B [K][r]). X [M][ldx] fp16 (xbf16 = 0) or bf16 (xbf16 = 1).
-hipError_t launch_lora_rows(const void* X, int xbf16, int ldx, int M, int K, const float* W, int wt, int r,
-                            float s, float* out, const SplitScratch& sc, hipStream_t st);
-// R(c, j) = s * sum_m Mx[m][c] * V[m][j]: out[c*r + j] (layout 0, dB [C][r]) or
-// out[j*C + c] (layout 1, dA [r][C]). Mx [M][ldm] fp16 (mbf16 = 0) or bf16 (mbf16 = 1),
-// V fp32 [M][r].
-hipError_t launch_lora_outer(const void* Mx, int mbf16, int ldm, int M, int C, const float* V, int r, float s,
-                             float* out, int layout, const SplitScratch& sc, hipStream_t st);
-size_t lora_rows_part_floats(int M, int K, int r);
-size_t lora_outer_part_floats(int M, int C, int r);
+// Rows: out[m][j] = s * sum_k X[m][k] * W(j, k) for each job, W(j,k) = W[j*K + k]
+// (wt = 0, A [r][K]) or W[k*r + j] (wt = 1, B [K][r]); X [M][ldx], fp16 (xbf16 = 0) or
+// bf16 (xbf16 = 1), the same type for every job of a launch.
+struct LoraRowsJob {
+  const void* X;
+  int ldx, K;
+  const float* W;
+  float* out;             // [M][r]
+};
+struct LoraRowsArgs {
+  LoraRowsJob job[3];
+  int njobs, M, r, wt;
+  float s;
+};
+hipError_t launch_lora_rows(const LoraRowsArgs& a, int xbf16, hipStream_t st);
+// Outer: R(c, j) = s_job * sum_m Mx[m][c] * V[m][j] for each job, written as out[c*r + j]
+// (layout 0, dB [C][r]) or out[j*C + c] (layout 1, dA [r][C]). Mx [M][ldm] fp16 (mbf16 = 0)
+// or bf16 (mbf16 = 1), V fp32 [M][r]. Token-split partials use `part` when the token count
+// is large (lora_outer_part_floats).
+struct LoraOuterJob {
+  const void* Mx;
+  int ldm, C;
+  const float* V;
+  float* out;
+  float s;
+};
+struct LoraOuterArgs {
+  LoraOuterJob job[3];
+  int njobs, M, r, layout;
+  float* part;
+  size_t part_floats;
+  int cmax;               // set by the launcher
+};
+hipError_t launch_lora_outer(const LoraOuterArgs& a, int mbf16, hipStream_t st);
+size_t lora_outer_part_floats(int M, int cmax, int r, int njobs);
 hipError_t launch_fill_i32(int* p, int n, int v, hipStream_t st);
 
 // ---------------------------------------------------------------- attention

@@ -226,3 +226,40 @@ def test_train_step_parity_mini(built_lib, gpu):
 def test_train_step_parity_qwen05b(built_lib, gpu):
     cfg = CONFIGS["qwen2.5-0.5b"]
     _step_parity(cfg, make_inputs(cfg, seed=0), gpu)
+
+
+def test_hip_graph_replay_matches_eager(built_lib, gpu):
+    """The whole step captured as one HIP graph and replayed several times (with eager
+    work and synchronisations between replays) reproduces the eager step bit for bit."""
+    cfg = MINI
+    inp = make_inputs(cfg, seed=6, norm="random")
+    dm = _dm(inp, gpu)
+    dx0 = torch.empty((dm.N, cfg.hidden), dtype=torch.float32, device=gpu)
+    say("graph replay mini: eager reference")
+    dm.train_step(dx0)
+    torch.cuda.synchronize()
+    ref_loss = dm.loss.clone()
+    ref_dx = dx0.clone()
+    ref = {(l, p): (dm.dA[l][p].clone(), dm.dB[l][p].clone()) for l in range(cfg.n_layers) for p in PROJ}
+    s_cap = torch.cuda.Stream()
+    s_cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s_cap):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s_cap):
+            dm.train_step(dx0)
+    torch.cuda.current_stream().wait_stream(s_cap)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        dx0.zero_()
+        dm.loss.zero_()
+        for (l, p) in ref:
+            dm.dA[l][p].zero_()
+        torch.cuda.synchronize()
+        say("graph replay", rep)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dm.loss, ref_loss)
+        assert torch.equal(dx0, ref_dx)
+        for (l, p), (a, b) in ref.items():
+            assert torch.equal(dm.dA[l][p], a) and torch.equal(dm.dB[l][p], b)
+        dm.layer_forward(0, dm.ckpt[0].clone(), torch.empty_like(dm.ckpt[0]))  # eager work in between
