@@ -39,14 +39,12 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 enum Slot {
   S_A, S_Q, S_K, S_V, S_O, S_LSE, S_H, S_C, S_G, S_U, S_Z, S_LU, S_LDU, S_DYB, S_DC, S_DH, S_DHB, S_DO,
   S_DELTA, S_DQ, S_DK, S_DV, S_DA, S_PART, S_ROPE_G, S_ROPE_L, S_TGT, S_HF, S_LOGITS, S_STATS, S_LSEV,
-  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_CNT, S_COUNT
+  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_COUNT
 };
-constexpr int kCounters = 1 << 16;
 const char* kSlotNames[S_COUNT] = {
   "a", "q", "k", "v", "o", "lse", "h", "c", "g", "u", "z", "lora_u", "lora_du", "dy_bf16", "dc", "dh",
   "dh_bf16", "do", "delta", "dq", "dk", "dv", "da", "lora_part", "rope_global", "rope_local", "targets",
-  "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part",
-  "split_counters"};
+  "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part"};
 
 struct Layout {
   size_t off[S_COUNT];
@@ -142,7 +140,6 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
     mx(attn_bwd_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim));
     L->split_floats = m;
     sz[S_SPLIT] = m * 4;
-    sz[S_CNT] = (size_t)kCounters * 4;
   }
   size_t o = 0;
   for (int i = 0; i < S_COUNT; ++i) {
@@ -275,8 +272,6 @@ SplitScratch scratch(const Ctx& x) {
   SplitScratch sc;
   sc.part = slot<float>(x.ws, x.L, S_SPLIT);
   sc.part_floats = x.L.split_floats;
-  sc.counters = slot<int>(x.ws, x.L, S_CNT);
-  sc.ncounters = kCounters;
   return sc;
 }
 
@@ -299,35 +294,26 @@ NtSeg nt_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* l
   return s;
 }
 
-hipError_t run_nt(const Ctx& x, const f16* X, int K, int nseg, NtSeg* segs, int epi) {
+NtArgs nt_args(const Ctx& x, const f16* X, int K, std::initializer_list<NtSeg> segs) {
   NtArgs a{};
   a.X = X;
   a.lda = K;
   a.M = x.D.N;
   a.K = K;
-  a.nseg = nseg;
-  int t = 0;
-  for (int i = 0; i < nseg; ++i) {
-    segs[i].tile0 = t;
-    t += gemm_nt_tiles(segs[i].N);
-    a.seg[i] = segs[i];
-  }
+  for (const NtSeg& s : segs) a.seg[a.nseg++] = s;
   a.lora_s = x.D.s;
   a.r = x.D.r;
   const SplitScratch sc = scratch(x);
   a.part = sc.part;
   a.part_floats = sc.part_floats;
-  a.counters = sc.counters;
-  a.ncounters = sc.ncounters;
-  return launch_gemm_nt(a, epi, x.st);
+  a.eps = x.c->rms_eps;
+  return a;
 }
 
 void set_scratch(const Ctx& x, TnArgs& t) {
   const SplitScratch sc = scratch(x);
   t.part = sc.part;
   t.part_floats = sc.part_floats;
-  t.counters = sc.counters;
-  t.ncounters = sc.ncounters;
 }
 
 TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* lora, int p, const bf16* G) {
@@ -412,11 +398,16 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
 
   HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
   HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}));
-  NtSeg qkv[3] = {nt_seg(x, base, lora, MEBP_Q, q, D.qd, nullptr, 0), nt_seg(x, base, lora, MEBP_K, k, D.kvd, nullptr, 0),
-                  nt_seg(x, base, lora, MEBP_V, v, D.kvd, nullptr, 0)};
-  HIP_TRY(run_nt(x, a, D.d, 3, qkv, NT_STORE_F16));
-  HIP_TRY(launch_rope_fwd(q, D.qd, x.B, x.T, c->n_heads, c->head_dim, rope, x.st));
-  HIP_TRY(launch_rope_fwd(k, D.kvd, x.B, x.T, c->n_kv_heads, c->head_dim, rope, x.st));
+  {
+    // q, k, v projections with RoPE applied to q and k on the way out
+    NtSeg qs = nt_seg(x, base, lora, MEBP_Q, q, D.qd, nullptr, 0), ks = nt_seg(x, base, lora, MEBP_K, k, D.kvd, nullptr, 0);
+    qs.rope = ks.rope = 1;
+    NtArgs na = nt_args(x, a, D.d, {qs, ks, nt_seg(x, base, lora, MEBP_V, v, D.kvd, nullptr, 0)});
+    na.rope_cs = rope;
+    na.rope_T = x.T;
+    na.rope_dh = c->head_dim;
+    HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st));
+  }
   AttnArgs at{};
   at.q = q; at.k = k; at.v = v; at.ldq = D.qd; at.ldk = D.kvd;
   at.B = x.B; at.T = x.T; at.Hq = c->n_heads; at.Hkv = c->n_kv_heads; at.dh = c->head_dim;
@@ -424,18 +415,27 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   at.o = o; at.lse = slot<float>(x.ws, x.L, S_LSE);
   HIP_TRY(launch_attn_fwd(at, x.st));
   HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}));
-  NtSeg os[1] = {nt_seg(x, base, lora, MEBP_O, h, D.d, x_in, D.d)};
-  HIP_TRY(run_nt(x, o, D.qd, 1, os, NT_STORE_F32));
-  HIP_TRY(launch_rmsnorm_fwd(h, base->norm_mlp, D.N, D.d, c->rms_eps, cc, nullptr, x.st));
-  HIP_TRY(lora_down(x, lora, cc, D.d, {MEBP_GATE, MEBP_UP}));
-  NtSeg gu[2] = {nt_seg(x, base, lora, MEBP_GATE, g, D.F, nullptr, 0), nt_seg(x, base, lora, MEBP_UP, u, D.F, nullptr, 0)};
-  HIP_TRY(run_nt(x, cc, D.d, 2, gu, NT_STORE_F16));
-  HIP_TRY(launch_act_fwd(g, u, z, (size_t)D.N * D.F, c->act, x.st));
-  HIP_TRY(lora_down(x, lora, z, D.F, {MEBP_DOWN}));
-  if (!keep) {
-    NtSeg ds[1] = {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)};
-    HIP_TRY(run_nt(x, z, D.F, 1, ds, NT_STORE_F32));
+  {
+    // h = x + o-projection, then c = RMSNorm(h)
+    NtArgs na = nt_args(x, o, D.qd, {nt_seg(x, base, lora, MEBP_O, h, D.d, x_in, D.d)});
+    na.norm_w = base->norm_mlp;
+    na.norm_out = cc;
+    HIP_TRY(launch_gemm_nt(na, NT_STORE_F32, x.st));
   }
+  HIP_TRY(lora_down(x, lora, cc, D.d, {MEBP_GATE, MEBP_UP}));
+  {
+    // g, u projections and z = act(g) * u (g and u kept only for the backward)
+    NtArgs na = nt_args(x, cc, D.d, {nt_seg(x, base, lora, MEBP_GATE, g, D.F, nullptr, 0),
+                                     nt_seg(x, base, lora, MEBP_UP, u, D.F, nullptr, 0)});
+    na.gated = 1;
+    na.act = c->act;
+    na.z_out = z;
+    na.store_gu = keep;
+    HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st));
+  }
+  HIP_TRY(lora_down(x, lora, z, D.F, {MEBP_DOWN}));
+  if (!keep)
+    HIP_TRY(launch_gemm_nt(nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)}), NT_STORE_F32, x.st));
   return MEBP_OK;
 }
 
@@ -491,10 +491,11 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
     t.seg[0] = tn_seg(x, base, lora, MEBP_GATE, dg);
     t.seg[1] = tn_seg(x, base, lora, MEBP_UP, dup);
     t.out = dc; t.ldo = D.d;
+    // c = RMSNorm(h): dh = dy + rmsnorm_bwd(h, dc)
+    t.norm_x = h; t.norm_w = base->norm_mlp; t.resid2 = dy; t.out2 = dh; t.out2b = dhb; t.eps = c->rms_eps;
     HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
   }
-  // c = RMSNorm(h); h = x + o(O)
-  HIP_TRY(launch_rmsnorm_bwd(h, base->norm_mlp, dc, dy, D.N, D.d, c->rms_eps, dh, dhb, x.st));
+  // h = x + o(O)
   HIP_TRY(lora_bwd(x, lora, grads, {MEBP_O}, {dhb}, o));
   {
     TnArgs t{};
@@ -523,9 +524,9 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
     t.seg[1] = tn_seg(x, base, lora, MEBP_K, dk);
     t.seg[2] = tn_seg(x, base, lora, MEBP_V, dv);
     t.out = da; t.ldo = D.d;
-    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
     // a = RMSNorm(x): dx = dh + rmsnorm_bwd(x, da)  (dx may alias dy: dy is no longer read)
-    HIP_TRY(launch_rmsnorm_bwd(x_ckpt, base->norm_attn, da, dh, D.N, D.d, c->rms_eps, dx, dyb, x.st));
+    t.norm_x = x_ckpt; t.norm_w = base->norm_attn; t.resid2 = dh; t.out2 = dx; t.out2b = dyb; t.eps = c->rms_eps;
+    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
   }
   return MEBP_OK;
 }
@@ -586,11 +587,6 @@ Ctx make_ctx(const mebp_config* c, int B, int T, void* ws, mebp_stream_t stream)
   return x;
 }
 
-int zero_counters(const Ctx& x) {
-  HIP_TRY(launch_fill_i32(slot<int>(x.ws, x.L, S_CNT), kCounters, 0, x.st));
-  return MEBP_OK;
-}
-
 int rope_table(const Ctx& x, int l, float** out) {
   const bool glob = is_global(x.c, l);
   float* cs = slot<float>(x.ws, x.L, glob ? S_ROPE_G : S_ROPE_L);
@@ -636,7 +632,7 @@ int mebp_layer_forward_ckpt(const mebp_config* cfg, int32_t layer, const mebp_la
   if (x_in == x_out) return fail(MEBP_EINVAL, "x_out must not alias x_in");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
   float* rope;
-  if ((e = zero_counters(x)) || (e = rope_table(x, layer, &rope))) return e;
+  if ((e = rope_table(x, layer, &rope))) return e;
   return layer_forward(x, layer, base, lora, x_in, x_out, rope, false);
 }
 
@@ -653,7 +649,7 @@ int mebp_layer_recompute_backward(const mebp_config* cfg, int32_t layer, const m
   if (dx && dx == x_ckpt) return fail(MEBP_EINVAL, "dx must not alias x_ckpt");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
   float* rope;
-  if ((e = zero_counters(x)) || (e = rope_table(x, layer, &rope))) return e;
+  if ((e = rope_table(x, layer, &rope))) return e;
   return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
 }
 
@@ -670,7 +666,6 @@ int mebp_lm_head_ce_backward(const mebp_config* cfg, const mebp_q4* emb, const f
   if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
   if (!loss || !aligned(loss, 4)) return fail(MEBP_EINVAL, "loss NULL or misaligned");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
-  if ((e = zero_counters(x))) return e;
   return lm_head(x, emb, norm_final, x_last, ids, loss, dx_last);
 }
 
@@ -710,7 +705,6 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   const size_t stride = (size_t)x.D.N * x.D.d;
   float* rope_g = slot<float>(ws, x.L, S_ROPE_G);
   float* rope_l = slot<float>(ws, x.L, S_ROPE_L);
-  if ((e = zero_counters(x))) return e;
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_global, rope_g, x.st));
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_local, rope_l, x.st));
   HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ckpt, x.st));

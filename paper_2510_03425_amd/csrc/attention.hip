@@ -208,10 +208,10 @@ __global__ void k_attn_delta(const bf16* dO, const f16* O, int ld, int B, int T,
 }
 
 // dK, dV for a block of 64 keys and one query head. With grouped-query attention the
-// heads of a KV group run in separate workgroups; each stores its partial dK/dV and the
-// last of the group to arrive sums them in head order (deterministic) and writes.
+// heads of a KV group run in separate workgroups; each stores its fp32 partial dK/dV and
+// a reduce kernel sums them in head order (deterministic).
 template <int DH, int QB>
-__global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* part, int* counters) {
+__global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* part) {
   constexpr int LDN = DH + 8, LDT_ = QB + 8, NKS = DH / 32, NT = DH / 16, NQT = QB / 16;
   __shared__ __attribute__((aligned(16))) u16 Qs[QB * LDN];   // fp16 (scores)
   __shared__ __attribute__((aligned(16))) u16 dOs[QB * LDN];  // bf16
@@ -291,6 +291,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
   }
   // epilogue: lane holds rows key kw + 4g + r, column e = 16t + lane%16
   if (grp > 1) {
+    // grouped-query attention: store this head's fp32 partials; k_attn_dkdv_reduce sums
+    // the heads of the group in head order and finishes dK (scale, RoPE backward) and dV
     const size_t plane = (size_t)a.B * T * a.Hkv * DH;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -299,27 +301,11 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
       const size_t o = (rowb + kk) * (size_t)(a.Hkv * DH) + kvh * DH + (lane & 15);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        st_dev(&part[(size_t)hh * plane + o + 16 * t], dk[t][r]);
-        st_dev(&part[(size_t)(grp + hh) * plane + o + 16 * t], dv[t][r]);
+        part[(size_t)hh * plane + o + 16 * t] = dk[t][r];
+        part[(size_t)(grp + hh) * plane + o + 16 * t] = dv[t][r];
       }
     }
-    if (!arrive_last(counters + ((size_t)b * a.Hkv + kvh) * gridDim.x + blockIdx.x, grp)) return;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kk = kw + 4 * (lane >> 4) + r;
-      if (kk >= T) continue;
-      const size_t o = (rowb + kk) * (size_t)(a.Hkv * DH) + kvh * DH + (lane & 15);
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        float sk = 0.f, sv = 0.f;
-        for (int g = 0; g < grp; ++g) {
-          sk += ld_dev(&part[(size_t)g * plane + o + 16 * t]);
-          sv += ld_dev(&part[(size_t)(grp + g) * plane + o + 16 * t]);
-        }
-        dk[t][r] = sk;
-        dv[t][r] = sv;
-      }
-    }
+    return;
   }
   const float scale = 1.0f / sqrtf((float)DH);
   const int half = DH / 2;
@@ -430,6 +416,45 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
   }
 }
 
+// dK/dV of grouped-query attention: sum the per-head partials of each KV head in head
+// order, scale dK by 1/sqrt(dh), rotate it back (RoPE backward), store bf16. One thread
+// per (token, kv head, 4 columns of the first half of the head) and their partners.
+__global__ void k_attn_dkdv_reduce(const AttnArgs a, const float* part) {
+  const int half = a.dh / 2, q4 = half / 4;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t total = (size_t)a.B * a.T * a.Hkv * q4;
+  if (i >= total) return;
+  const int e = (int)(i % q4) * 4;
+  const int kvh = (int)((i / q4) % a.Hkv);
+  const size_t row = i / ((size_t)q4 * a.Hkv);
+  const int t = (int)(row % a.T), grp = a.Hq / a.Hkv;
+  const size_t plane = (size_t)a.B * a.T * a.Hkv * a.dh;
+  const size_t o = row * (size_t)(a.Hkv * a.dh) + kvh * a.dh + e;
+  float k1[4] = {0, 0, 0, 0}, k2[4] = {0, 0, 0, 0}, v1[4] = {0, 0, 0, 0}, v2[4] = {0, 0, 0, 0};
+  for (int g = 0; g < grp; ++g) {
+    const float4 a1 = *(const float4*)(part + g * plane + o), a2 = *(const float4*)(part + g * plane + o + half);
+    const float4 b1 = *(const float4*)(part + (grp + g) * plane + o);
+    const float4 b2 = *(const float4*)(part + (grp + g) * plane + o + half);
+    k1[0] += a1.x; k1[1] += a1.y; k1[2] += a1.z; k1[3] += a1.w;
+    k2[0] += a2.x; k2[1] += a2.y; k2[2] += a2.z; k2[3] += a2.w;
+    v1[0] += b1.x; v1[1] += b1.y; v1[2] += b1.z; v1[3] += b1.w;
+    v2[0] += b2.x; v2[1] += b2.y; v2[2] += b2.z; v2[3] += b2.w;
+  }
+  const float scale = 1.0f / sqrtf((float)a.dh);
+  float lo[4], hi[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float2 cs = *(const float2*)(a.cs + 2 * ((size_t)t * half + e + j));
+    const float d1 = k1[j] * scale, d2 = k2[j] * scale;
+    lo[j] = d1 * cs.x + d2 * cs.y;
+    hi[j] = d2 * cs.x - d1 * cs.y;
+  }
+  *(uint2*)(a.dk + o) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+  *(uint2*)(a.dk + o + half) = make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
+  *(uint2*)(a.dv + o) = make_uint2(pack_bf16x2(v1[0], v1[1]), pack_bf16x2(v1[2], v1[3]));
+  *(uint2*)(a.dv + o + half) = make_uint2(pack_bf16x2(v2[0], v2[1]), pack_bf16x2(v2[2], v2[3]));
+}
+
 }  // namespace
 
 // visible (query, key) pairs of one sequence and head
@@ -467,8 +492,7 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
   AttnArgs a = a0;
   a.delta = delta_ws;
   dim3 gkv((a.T + 63) / 64, a.Hq, a.B), gq((a.T + 63) / 64, a.Hq, a.B);
-  if (a.Hq > a.Hkv && (!sc.part || sc.part_floats < attn_bwd_part_floats(a.B, a.T, a.Hq, a.Hkv, a.dh) ||
-                       (size_t)a.B * a.Hkv * gkv.x > (size_t)sc.ncounters))
+  if (a.Hq > a.Hkv && (!sc.part || sc.part_floats < attn_bwd_part_floats(a.B, a.T, a.Hq, a.Hkv, a.dh)))
     return hipErrorInvalidValue;
   const double pairs = visible_pairs(a.T, a.window) * a.Hq * a.B;
   // algorithmic: dV, dK and dP products in the key-block kernel, dQ in the query-block kernel
@@ -476,19 +500,25 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
   const double io = (double)a.B * a.T * (a.Hq * a.dh * 2.0 * 2 + a.Hkv * a.dh * 2.0 * 4);
   switch (a.dh) {
     case 64:
-      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, sc.part, sc.counters));
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, sc.part));
       MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, st, a));
       break;
     case 128:
-      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<128, 64>), gkv, dim3(256), 0, st, a, sc.part, sc.counters));
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<128, 64>), gkv, dim3(256), 0, st, a, sc.part));
       MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, st, a));
       break;
     case 256:
-      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, sc.part, sc.counters));
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, sc.part));
       MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, st, a));
       break;
     default: return hipErrorInvalidValue;
   }
+  e = hipGetLastError();
+  if (e != hipSuccess || a.Hq == a.Hkv) return e;
+  const size_t nr = (size_t)a.B * a.T * a.Hkv * (a.dh / 8);
+  MEBP_TIMED(st, "attn_dkdv_reduce", 0.0, (double)a.B * a.T * a.Hq * a.dh * 8 + (double)a.B * a.T * a.Hkv * a.dh * 4,
+             hipLaunchKernelGGL(k_attn_dkdv_reduce, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, st, a,
+                                (const float*)sc.part));
   return hipGetLastError();
 }
 

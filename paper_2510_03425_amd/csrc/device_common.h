@@ -120,26 +120,3 @@ DEV float act_grad_f(float g, int kind) {
   float t = tanhf(c * (g + 0.044715f * g * g * g));
   return 0.5f * (1.0f + t) + 0.5f * g * (1.0f - t * t) * c * (1.0f + 3.0f * 0.044715f * g * g);
 }
-
-// ---- cross-workgroup exchange without whole-cache writebacks -----------------------------
-// Split reductions hand fp32 partials between workgroups that may sit on different XCDs
-// (separate L2s). Partials are written and read with device-scope relaxed atomics, which
-// on gfx950 write through to / read from the device coherence point, so no L2 writeback or
-// invalidate (a device-scope fence) is needed: a producer waits for its own stores to
-// complete, then bumps a counter; the last arrival reads everything back.
-DEV void st_dev(float* p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-DEV float ld_dev(const float* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-
-// Call after every thread of the workgroup has stored its partials with st_dev. Returns
-// true in the workgroup that arrives last (which also re-arms the counter to 0).
-DEV bool arrive_last(int* counter, int splits) {
-  __shared__ int s_last;
-  __builtin_amdgcn_s_waitcnt(0);  // this thread's write-through stores have completed
-  __syncthreads();
-  if (threadIdx.x == 0)
-    s_last = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == splits - 1;
-  __syncthreads();
-  if (!s_last) return false;
-  if (threadIdx.x == 0) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return true;
-}

@@ -482,44 +482,172 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
 }
 
 // ------------------------------------------------------------------------ split finalize
-// Sum the split planes in split order and apply the stored epilogue; one thread per 4
-// consecutive output columns of one row (all segment widths are multiples of 4).
-template <int EPI>
-__global__ __launch_bounds__(256) void k_nt_finalize(const NtArgs a, int S) {
-  const int c4n = a.ldp >> 2;
-  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (size_t)a.M * c4n) return;
-  const int m = (int)(i / c4n), col = (int)(i % c4n) * 4;
-  int s = 0;
-  if (a.nseg > 1 && col >= a.seg[1].col0) s = 1;
-  if (a.nseg > 2 && col >= a.seg[2].col0) s = 2;
-  const NtSeg& sg = a.seg[s];
-  const int n = col - sg.col0;
-  float4 v = *(const float4*)(a.part + (size_t)m * a.ldp + col);
-  for (int z = 1; z < S; ++z) {
-    const float4 w = *(const float4*)(a.part + ((size_t)z * a.M + m) * a.ldp + col);
+// Sum the split planes in split order and apply the epilogue plus any fused follow-up.
+// Plain mapping: one thread per 4 consecutive output columns of one row (all segment
+// widths are multiples of 4).
+
+DEV float4 sum_planes(const float* part, int S, size_t plane, size_t off) {
+  // four planes in flight at a time; the sum still runs in split order
+  const float* p = part + off;
+  float4 v = *(const float4*)p;
+  int z = 1;
+  for (; z + 4 <= S; z += 4) {
+    const float4 w0 = *(const float4*)(p + z * plane), w1 = *(const float4*)(p + (z + 1) * plane);
+    const float4 w2 = *(const float4*)(p + (z + 2) * plane), w3 = *(const float4*)(p + (z + 3) * plane);
+    v.x += w0.x; v.y += w0.y; v.z += w0.z; v.w += w0.w;
+    v.x += w1.x; v.y += w1.y; v.z += w1.z; v.w += w1.w;
+    v.x += w2.x; v.y += w2.y; v.z += w2.z; v.w += w2.w;
+    v.x += w3.x; v.y += w3.y; v.z += w3.z; v.w += w3.w;
+  }
+  for (; z < S; ++z) {
+    const float4 w = *(const float4*)(p + z * plane);
     v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
   }
-  float o[4] = {v.x, v.y, v.z, v.w};
-  if (sg.lora_B) {
-    const int r = a.r;
-    const float* u = sg.lora_u + (size_t)m * r;
+  return v;
+}
+
+// sum over the 256 threads of a workgroup (every thread gets the result)
+DEV float2 block_sum2(float2 v, float2* red) {
+  v.x = wave_sum(v.x);
+  v.y = wave_sum(v.y);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return make_float2(red[0].x + red[1].x + red[2].x + red[3].x, red[0].y + red[1].y + red[2].y + red[3].y);
+}
+
+// LoRA up-projection term s * u[m] . B[n] for 4 consecutive columns n..n+3
+DEV void add_lora4(float (&o)[4], const NtSeg& sg, float s, int r, int m, int n) {
+  if (!sg.lora_B) return;
+  const float* u = sg.lora_u + (size_t)m * r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float* b = sg.lora_B + (size_t)(n + q) * r;
+    float l = 0.f;
+    for (int j = 0; j < r; ++j) l += u[j] * b[j];
+    o[q] += s * l;
+  }
+}
+
+DEV void store4_f16(f16* p, const float (&o)[4]) {
+  *(uint2*)p = make_uint2(pack_f16x2(o[0], o[1]), pack_f16x2(o[2], o[3]));
+}
+
+// Work items per row: a RoPE segment contributes one item per 4 columns of the first half
+// of each head (the item also covers the partner columns dh/2 further), other segments
+// one item per 4 columns.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_nt_finalize(const NtArgs a, int S, int items) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)a.M * items) return;
+  const int m = (int)(i / items), it = (int)(i % items);
+  int s = 0;
+  if (a.nseg > 1 && it >= a.seg[1].item0) s = 1;
+  if (a.nseg > 2 && it >= a.seg[2].item0) s = 2;
+  const NtSeg& sg = a.seg[s];
+  const size_t plane = (size_t)a.M * a.ldp;
+  const int li = it - sg.item0;
+  if (sg.rope) {
+    const int dh = a.rope_dh, half = dh / 2, per_head = half / 4;
+    const int n1 = (li / per_head) * dh + (li % per_head) * 4, n2 = n1 + half, e = n1 % dh;
+    const float4 v1 = sum_planes(a.part, S, plane, (size_t)m * a.ldp + sg.col0 + n1);
+    const float4 v2 = sum_planes(a.part, S, plane, (size_t)m * a.ldp + sg.col0 + n2);
+    float o1[4] = {v1.x, v1.y, v1.z, v1.w}, o2[4] = {v2.x, v2.y, v2.z, v2.w};
+    add_lora4(o1, sg, a.lora_s, a.r, m, n1);
+    add_lora4(o2, sg, a.lora_s, a.r, m, n2);
+    const int t = m % a.rope_T;
+    float r1[4], r2[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float* b = sg.lora_B + (size_t)(n + q) * r;
-      float l = 0.f;
-      for (int j = 0; j < r; ++j) l += u[j] * b[j];
-      o[q] += a.lora_s * l;
+      const float2 cs = *(const float2*)(a.rope_cs + 2 * ((size_t)t * half + e + q));
+      r1[q] = o1[q] * cs.x - o2[q] * cs.y;
+      r2[q] = o2[q] * cs.x + o1[q] * cs.y;
     }
+    store4_f16((f16*)sg.out + (size_t)m * sg.ldo + n1, r1);
+    store4_f16((f16*)sg.out + (size_t)m * sg.ldo + n2, r2);
+    return;
   }
+  const int n = li * 4;
+  const float4 v = sum_planes(a.part, S, plane, (size_t)m * a.ldp + sg.col0 + n);
+  float o[4] = {v.x, v.y, v.z, v.w};
+  add_lora4(o, sg, a.lora_s, a.r, m, n);
   if (sg.resid) {
     const float4 rv = *(const float4*)(sg.resid + (size_t)m * sg.ldr + n);
     o[0] += rv.x; o[1] += rv.y; o[2] += rv.z; o[3] += rv.w;
   }
-  if constexpr (EPI == NT_STORE_F16) {
-    *(uint2*)((f16*)sg.out + (size_t)m * sg.ldo + n) = make_uint2(pack_f16x2(o[0], o[1]), pack_f16x2(o[2], o[3]));
-  } else {
+  if constexpr (EPI == NT_STORE_F16)
+    store4_f16((f16*)sg.out + (size_t)m * sg.ldo + n, o);
+  else
     *(float4*)((float*)sg.out + (size_t)m * sg.ldo + n) = make_float4(o[0], o[1], o[2], o[3]);
+}
+
+// gate/up: z = act(g) * u for 4 columns; g, u themselves stored only when asked
+__global__ __launch_bounds__(256) void k_nt_finalize_gated(const NtArgs a, int S) {
+  const int c4n = a.seg[0].N >> 2;
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)a.M * c4n) return;
+  const int m = (int)(i / c4n), n = (int)(i % c4n) * 4;
+  const size_t plane = (size_t)a.M * a.ldp;
+  const NtSeg& sgg = a.seg[0];
+  const NtSeg& sgu = a.seg[1];
+  const float4 gv = sum_planes(a.part, S, plane, (size_t)m * a.ldp + sgg.col0 + n);
+  const float4 uv = sum_planes(a.part, S, plane, (size_t)m * a.ldp + sgu.col0 + n);
+  float g[4] = {gv.x, gv.y, gv.z, gv.w}, u[4] = {uv.x, uv.y, uv.z, uv.w};
+  add_lora4(g, sgg, a.lora_s, a.r, m, n);
+  add_lora4(u, sgu, a.lora_s, a.r, m, n);
+  // the activation sees the same fp16-rounded g and u the backward will read
+  float z[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    g[q] = (float)(f16)g[q];
+    u[q] = (float)(f16)u[q];
+    z[q] = act_f(g[q], a.act) * u[q];
+  }
+  if (a.store_gu) {
+    store4_f16((f16*)sgg.out + (size_t)m * sgg.ldo + n, g);
+    store4_f16((f16*)sgu.out + (size_t)m * sgu.ldo + n, u);
+  }
+  store4_f16(a.z_out + (size_t)m * a.seg[0].N + n, z);
+}
+
+// single fp32-output segment h (+ residual): also c = fp16(h * w * rstd(h)); one workgroup
+// per row, each thread 4 columns out of every 1024
+__global__ __launch_bounds__(256) void k_nt_finalize_norm(const NtArgs a, int S) {
+  __shared__ float2 red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const NtSeg& sg = a.seg[0];
+  const int N = sg.N, c4n = N >> 2;
+  const size_t plane = (size_t)a.M * a.ldp;
+  constexpr int MAXC = 4;  // up to 4096 columns
+  float4 h[MAXC];
+  float ss = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = tid + 256 * q;
+    if (c < c4n) {
+      const int n = c * 4;
+      const float4 v = sum_planes(a.part, S, plane, (size_t)row * a.ldp + sg.col0 + n);
+      float o[4] = {v.x, v.y, v.z, v.w};
+      add_lora4(o, sg, a.lora_s, a.r, row, n);
+      if (sg.resid) {
+        const float4 rv = *(const float4*)(sg.resid + (size_t)row * sg.ldr + n);
+        o[0] += rv.x; o[1] += rv.y; o[2] += rv.z; o[3] += rv.w;
+      }
+      h[q] = make_float4(o[0], o[1], o[2], o[3]);
+      *(float4*)((float*)sg.out + (size_t)row * sg.ldo + n) = h[q];
+      ss += o[0] * o[0] + o[1] * o[1] + o[2] * o[2] + o[3] * o[3];
+    }
+  }
+  ss = block_sum2(make_float2(ss, 0.f), red).x;
+  const float rs = 1.0f / sqrtf(ss / (float)N + a.eps);
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = tid + 256 * q;
+    if (c < c4n) {
+      const float4 w = *(const float4*)(a.norm_w + c * 4);
+      const float o[4] = {h[q].x * rs * w.x, h[q].y * rs * w.y, h[q].z * rs * w.z, h[q].w * rs * w.w};
+      store4_f16(a.norm_out + (size_t)row * N + c * 4, o);
+    }
   }
 }
 
@@ -529,11 +657,7 @@ __global__ __launch_bounds__(256) void k_tn_finalize(const TnArgs a, int S) {
   const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= (size_t)a.M * c4n) return;
   const int m = (int)(i / c4n), c = (int)(i % c4n) * 4;
-  float4 v = *(const float4*)(a.part + (size_t)m * a.Kout + c);
-  for (int z = 1; z < S; ++z) {
-    const float4 w = *(const float4*)(a.part + ((size_t)z * a.M + m) * a.Kout + c);
-    v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
-  }
+  const float4 v = sum_planes(a.part, S, (size_t)a.M * a.Kout, (size_t)m * a.Kout + c);
   float o[4] = {v.x, v.y, v.z, v.w};
   for (int sgi = 0; sgi < a.nseg; ++sgi) {
     const TnSeg& sg = a.seg[sgi];
@@ -564,6 +688,59 @@ __global__ __launch_bounds__(256) void k_tn_finalize(const TnArgs a, int S) {
   }
 }
 
+// v (= the gradient at a norm's output) stays in registers and feeds the norm backward:
+// out2 = resid2 + rstd * (w*v - xhat * mean(xhat*w*v)), xhat = x * rstd; one workgroup per row
+__global__ __launch_bounds__(256) void k_tn_finalize_norm(const TnArgs a, int S) {
+  __shared__ float2 red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int N = a.Kout, c4n = N >> 2;
+  constexpr int MAXC = 4;
+  float4 g[MAXC], xv[MAXC];
+  float ss = 0.f, sd = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = tid + 256 * q;
+    if (c < c4n) {
+      const int n = c * 4;
+      const float4 v = sum_planes(a.part, S, (size_t)a.M * N, (size_t)row * N + n);
+      float o[4] = {v.x, v.y, v.z, v.w};
+      for (int sgi = 0; sgi < a.nseg; ++sgi) {
+        const TnSeg& sg = a.seg[sgi];
+        if (!sg.lora_A) continue;
+        const float* du = sg.lora_du + (size_t)row * a.r;
+        for (int j = 0; j < a.r; ++j) {
+          const float4 av = *(const float4*)(sg.lora_A + (size_t)j * N + n);
+          o[0] += du[j] * av.x; o[1] += du[j] * av.y; o[2] += du[j] * av.z; o[3] += du[j] * av.w;
+        }
+      }
+      g[q] = make_float4(o[0], o[1], o[2], o[3]);
+      xv[q] = *(const float4*)(a.norm_x + (size_t)row * N + n);
+      const float4 w = *(const float4*)(a.norm_w + n);
+      ss += xv[q].x * xv[q].x + xv[q].y * xv[q].y + xv[q].z * xv[q].z + xv[q].w * xv[q].w;
+      sd += xv[q].x * w.x * o[0] + xv[q].y * w.y * o[1] + xv[q].z * w.z * o[2] + xv[q].w * w.w * o[3];
+    }
+  }
+  const float2 t = block_sum2(make_float2(ss, sd), red);
+  const float rs = 1.0f / sqrtf(t.x / (float)N + a.eps);
+  const float mt = rs * t.y / (float)N;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = tid + 256 * q;
+    if (c < c4n) {
+      const int n = c * 4;
+      const float4 w = *(const float4*)(a.norm_w + n);
+      float4 r = a.resid2 ? *(const float4*)(a.resid2 + (size_t)row * N + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+      r.x += rs * (w.x * g[q].x - xv[q].x * rs * mt);
+      r.y += rs * (w.y * g[q].y - xv[q].y * rs * mt);
+      r.z += rs * (w.z * g[q].z - xv[q].z * rs * mt);
+      r.w += rs * (w.w * g[q].w - xv[q].w * rs * mt);
+      *(float4*)(a.out2 + (size_t)row * N + n) = r;
+      if (a.out2b)
+        *(uint2*)(a.out2b + (size_t)row * N + n) = make_uint2(pack_bf16x2(r.x, r.y), pack_bf16x2(r.z, r.w));
+    }
+  }
+}
+
 }  // namespace
 
 int gemm_nt_tiles(int N) { return (N + BN - 1) / BN; }
@@ -590,14 +767,16 @@ size_t gemm_part_floats(int M, int ncols, int splits) { return splits > 1 ? (siz
 
 hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
   NtArgs a = a0;
-  int tiles = 0, ncat = 0;
+  int tiles = 0, ncat = 0, items = 0;
   double flops = 0, bytes = (double)a.M * a.K * 2;
   const int kg = (a.K + 31) / 32;
   for (int s = 0; s < a.nseg; ++s) {
     a.seg[s].tile0 = tiles;
     a.seg[s].col0 = ncat;
+    a.seg[s].item0 = items;
     tiles += gemm_nt_tiles(a.seg[s].N);
     ncat += a.seg[s].N;
+    items += a.seg[s].rope ? a.seg[s].N / 8 : a.seg[s].N / 4;
     const double n = a.seg[s].N;
     flops += 2.0 * a.M * n * a.K;
     bytes += n * (a.K / 2 + 2 * kg) + (double)a.M * n * (epi == NT_STORE_F32 ? 4 : 2);
@@ -606,6 +785,7 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
   const int mt = (a.M + BM - 1) / BM;
   int S = epi == NT_LOGITS ? 1 : gemm_splits(tiles * mt, (a.K + BK - 1) / BK);
   if (S > 1 && (!a.part || a.part_floats < gemm_part_floats(a.M, ncat, S))) S = 1;
+  if (a.norm_w && a.seg[0].N > 4096) S = 1;  // the fused row norm keeps a row in one wave
   a.ldp = ncat;
   dim3 grid(tiles, mt, S);
   switch (epi) {
@@ -624,14 +804,39 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || S == 1) return e;
-  const size_t nthr = (size_t)a.M * (ncat / 4);
-  const dim3 fg((unsigned)((nthr + 255) / 256));
+  if (e != hipSuccess || epi == NT_LOGITS) return e;
+  if (S == 1) {
+    // unsplit: the GEMM epilogue stored the outputs; run the follow-ups as their own kernels
+    for (int s = 0; s < a.nseg; ++s) {
+      if (!a.seg[s].rope) continue;
+      e = launch_rope_fwd((f16*)a.seg[s].out, a.seg[s].ldo, a.M / a.rope_T, a.rope_T, a.seg[s].N / a.rope_dh,
+                          a.rope_dh, a.rope_cs, st);
+      if (e != hipSuccess) return e;
+    }
+    if (a.gated)
+      return launch_act_fwd((const f16*)a.seg[0].out, (const f16*)a.seg[1].out, a.z_out, (size_t)a.M * a.seg[0].N,
+                            a.act, st);
+    if (a.norm_w)
+      return launch_rmsnorm_fwd((const float*)a.seg[0].out, a.norm_w, a.M, a.seg[0].N, a.eps, a.norm_out, nullptr, st);
+    return hipSuccess;
+  }
   const double fb = 4.0 * S * a.M * ncat + (double)a.M * ncat * (epi == NT_STORE_F16 ? 2 : 4);
-  if (epi == NT_STORE_F16)
-    MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_nt_finalize<NT_STORE_F16>, fg, dim3(256), 0, st, a, S));
-  else
-    MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_nt_finalize<NT_STORE_F32>, fg, dim3(256), 0, st, a, S));
+  if (a.gated) {
+    const size_t n = (size_t)a.M * (a.seg[0].N / 4);
+    MEBP_TIMED(st, "splitk_finalize_gated", 0.0, fb,
+               hipLaunchKernelGGL(k_nt_finalize_gated, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a, S));
+  } else if (a.norm_w) {
+    MEBP_TIMED(st, "splitk_finalize_norm", 0.0, fb,
+               hipLaunchKernelGGL(k_nt_finalize_norm, dim3((unsigned)a.M), dim3(256), 0, st, a, S));
+  } else {
+    const size_t n = (size_t)a.M * items;
+    const dim3 fg((unsigned)((n + 255) / 256));
+    if (epi == NT_STORE_F16)
+      MEBP_TIMED(st, a.seg[0].rope ? "splitk_finalize_rope" : "splitk_finalize", 0.0, fb,
+                 hipLaunchKernelGGL(k_nt_finalize<NT_STORE_F16>, fg, dim3(256), 0, st, a, S, items));
+    else
+      MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_nt_finalize<NT_STORE_F32>, fg, dim3(256), 0, st, a, S, items));
+  }
   return hipGetLastError();
 }
 
@@ -653,6 +858,7 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
   } else {
     S = gemm_splits(ct * mt, ktiles);
     if (S > 1 && (!a.part || a.part_floats < gemm_part_floats(a.M, a.Kout, S))) S = 1;
+    if (a.out2 && a.Kout > 4096) S = 1;
   }
   const double outb = (double)a.M * a.Kout;
   bytes += epi == TN_STORE_BF16 ? 2 * outb : epi == TN_ACT_BWD ? 8 * outb
@@ -680,10 +886,20 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
     }
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || S == 1 || epi == TN_PARTIAL_F32) return e;
+  if (e != hipSuccess || epi == TN_PARTIAL_F32) return e;
+  const bool norm = epi == TN_STORE_F32 && a.out2;
+  if (S == 1) {
+    if (norm) return launch_rmsnorm_bwd(a.norm_x, a.norm_w, a.out, a.resid2, a.M, a.Kout, a.eps, a.out2, a.out2b, st);
+    return hipSuccess;
+  }
+  const double fb = 4.0 * S * a.M * a.Kout + outb * (epi == TN_ACT_BWD ? 8 : epi == TN_STORE_BF16 ? 2 : 4);
+  if (norm) {
+    MEBP_TIMED(st, "splitk_finalize_normbwd", 0.0, fb + 16 * outb,
+               hipLaunchKernelGGL(k_tn_finalize_norm, dim3((unsigned)a.M), dim3(256), 0, st, a, S));
+    return hipGetLastError();
+  }
   const size_t nthr = (size_t)a.M * (a.Kout / 4);
   const dim3 fg((unsigned)((nthr + 255) / 256));
-  const double fb = 4.0 * S * a.M * a.Kout + outb * (epi == TN_ACT_BWD ? 8 : epi == TN_STORE_BF16 ? 2 : 4);
   switch (epi) {
     case TN_STORE_F32:
       MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_STORE_F32>, fg, dim3(256), 0, st, a, S));

@@ -29,6 +29,8 @@ struct NtSeg {
   int ldo;
   const float* resid;     // fp32 [M][ldr] added in the epilogue, or null
   int ldr;
+  int rope;               // 1: rotate-half RoPE on the (fp16) output, heads of rope_dh columns
+  int item0;              // set by the launcher (finalize work-item offset)
 };
 
 struct NtArgs {
@@ -47,9 +49,17 @@ struct NtArgs {
   // split-K scratch (unused when the launcher picks one split)
   float* part;
   size_t part_floats;
-  int* counters;          // zero on entry; left zero on exit
-  int ncounters;
   int ldp;                // set by the launcher
+  // fused follow-ups, done by the split finalize kernel or, unsplit, by extra kernels:
+  const float* rope_cs;   // RoPE table [T][dh/2] (cos, sin) for segments with rope = 1
+  int rope_T, rope_dh;
+  int gated;              // seg[0] = gate, seg[1] = up: z = act(g) * u into z_out (fp16)
+  int act;
+  f16* z_out;
+  int store_gu;           // gated: also store g and u (fp16) into seg[0].out / seg[1].out
+  const float* norm_w;    // single fp32-output segment h: c = fp16(rmsnorm(h) * w) into norm_out
+  f16* norm_out;
+  float eps;
 };
 hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st);
 int gemm_nt_tiles(int N);  // number of 128-wide N tiles
@@ -94,8 +104,13 @@ struct TnArgs {
   // split-K scratch for the stored epilogues (unused with one split)
   float* part;
   size_t part_floats;
-  int* counters;
-  int ncounters;
+  // TN_STORE_F32 follow-up: out2 = resid2 + rmsnorm_bwd(norm_x, norm_w, v), plus a bf16 copy
+  const float* norm_x;
+  const float* norm_w;
+  const float* resid2;
+  float* out2;
+  bf16* out2b;
+  float eps;
 };
 hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st);
 
@@ -117,12 +132,10 @@ hipError_t launch_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const fl
 hipError_t launch_act_fwd(const f16* g, const f16* u, f16* z, size_t n, int act, hipStream_t st);
 
 // ---------------------------------------------------------------- LoRA skinny kernels
-// Split scratch shared by the LoRA kernels: partial planes plus per-block counters.
+// Split scratch: fp32 partial planes of split reductions (LoRA outer, attention dK/dV).
 struct SplitScratch {
   float* part;
   size_t part_floats;
-  int* counters;           // zero on entry; left zero on exit
-  int ncounters;
 };
 // Rows: out[m][j] = s * sum_k X[m][k] * W(j, k) for each job, W(j,k) = W[j*K + k]
 // (wt = 0, A [r][K]) or W[k*r + j] (wt = 1, B [K][r]); X [M][ldx], fp16 (xbf16 = 0) or
@@ -175,7 +188,7 @@ struct AttnArgs {
 };
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st);
 // scratch: delta [B][Hq][T]; when Hq > Hkv, per-head dK/dV partials (2*B*T*Hq*dh floats)
-// reduced in-kernel by the last workgroup of each key block (counters: B*Hkv*ceil(T/64)).
+// summed over each GQA group by a reduce kernel.
 hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, const SplitScratch& sc, hipStream_t st);
 size_t attn_bwd_part_floats(int B, int T, int Hq, int Hkv, int dh);
 
