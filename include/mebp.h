@@ -184,6 +184,15 @@ const char* mebp_workspace_slot_name(int32_t slot);
 int mebp_kernel_timing(int32_t enable, int32_t capacity);
 int mebp_kernel_timing_report(char* buf, size_t len);
 
+/* Measurement aid. From this call on, every launch of the kernel named `kernel` (a name
+ * as it appears in the timing report) is issued `times` times back to back on its stream;
+ * kernel = NULL or times <= 1 switches it off. Results are unchanged, since every such
+ * kernel computes its outputs from inputs it does not overwrite; the two kernels that
+ * update a buffer in place ("gemm_tn_act_bwd", "splitk_finalize_actbwd") are refused with
+ * MEBP_EINVAL. The difference between step times with and without repetition is the
+ * kernel's in-stream duration. Host-thread-unsafe; for benchmarks only. */
+int mebp_kernel_repeat(const char* kernel, int32_t times);
+
 #ifdef __cplusplus
 }
 #endif

@@ -20,7 +20,7 @@ EXPORTED = (
     "mebp_workspace_bytes", "mebp_layer_forward_ckpt", "mebp_layer_recompute_backward",
     "mebp_lm_head_ce_backward", "mebp_embed", "mebp_train_step", "mebp_last_error",
     "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name", "mebp_kernel_timing",
-    "mebp_kernel_timing_report",
+    "mebp_kernel_timing_report", "mebp_kernel_repeat",
 )
 
 
@@ -87,6 +87,7 @@ def lib() -> C.CDLL:
             "mebp_workspace_slot_name": (C.c_char_p, [I32]),
             "mebp_kernel_timing": (C.c_int, [I32, I32]),
             "mebp_kernel_timing_report": (C.c_int, [C.c_char_p, SZ]),
+            "mebp_kernel_repeat": (C.c_int, [C.c_char_p, I32]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -174,3 +175,7 @@ def mebp_kernel_timing_report() -> list:
     if r < 0:
         raise MebpError(r, mebp_last_error())
     return json.loads(buf.value.decode())
+
+
+def mebp_kernel_repeat(kernel, times: int) -> int:
+    return _check(lib().mebp_kernel_repeat(None if kernel is None else kernel.encode(), times))

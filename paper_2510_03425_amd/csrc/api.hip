@@ -748,6 +748,11 @@ int mebp_kernel_timing(int32_t enable, int32_t capacity) {
   return MEBP_OK;
 }
 
+int mebp_kernel_repeat(const char* kernel, int32_t times) {
+  if (set_repeat(kernel, times) != 0) return fail(MEBP_EINVAL, "kernel '%s' overwrites its own input and cannot be repeated", kernel);
+  return MEBP_OK;
+}
+
 int mebp_kernel_timing_report(char* buf, size_t len) {
   const int n = timing_report(buf, len);
   if (n < 0) return fail(MEBP_EHIP, "event synchronisation failed");

@@ -905,7 +905,7 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
       MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_STORE_F32>, fg, dim3(256), 0, st, a, S));
       break;
     case TN_ACT_BWD:
-      MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_ACT_BWD>, fg, dim3(256), 0, st, a, S));
+      MEBP_TIMED(st, "splitk_finalize_actbwd", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_ACT_BWD>, fg, dim3(256), 0, st, a, S));
       break;
     default:
       MEBP_TIMED(st, "splitk_finalize", 0.0, fb, hipLaunchKernelGGL(k_tn_finalize<TN_STORE_BF16>, fg, dim3(256), 0, st, a, S));

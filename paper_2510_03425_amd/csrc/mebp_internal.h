@@ -211,13 +211,18 @@ int timer_begin(hipStream_t st, const char* name, double flops, double bytes);
 void timer_end(hipStream_t st, int token);
 int timing_enable(int enable, int capacity);
 int timing_report(char* buf, size_t len);
+int repeat_count(const char* name);
+int set_repeat(const char* name, int times);
 
 // Bracket one launch statement with the optional timer.
-#define MEBP_TIMED(st, name, flops, bytes, stmt)                \
-  do {                                                          \
-    const int tok_ = ::mebp::timer_begin((st), (name), (flops), (bytes)); \
-    stmt;                                                       \
-    ::mebp::timer_end((st), tok_);                              \
+#define MEBP_TIMED(st, name, flops, bytes, stmt)                            \
+  do {                                                                      \
+    const char* name_ = (name);                                             \
+    for (int rep_ = ::mebp::repeat_count(name_); rep_ > 0; --rep_) {        \
+      const int tok_ = ::mebp::timer_begin((st), name_, (flops), (bytes));  \
+      stmt;                                                                 \
+      ::mebp::timer_end((st), tok_);                                        \
+    }                                                                       \
   } while (0)
 
 }  // namespace mebp

@@ -1,8 +1,10 @@
 // Optional per-kernel event timing for diagnostics (mebp_kernel_timing*): when enabled,
 // every instrumented launch is bracketed by a pair of HIP events from a pool created at
 // enable time, tagged with the kernel's name and its algorithmic flops and bytes. The
-// report synchronises on the recorded events and aggregates per kernel name. Not
-// thread-safe: enable, run and report from one host thread.
+// report synchronises on the recorded events and aggregates per kernel name.
+// mebp_kernel_repeat makes every launch of one named kernel run several times back to
+// back, so that the kernel's in-stream duration can be measured as a step-time difference.
+// Not thread-safe: configure, run and report from one host thread.
 #include <stdio.h>
 #include <string.h>
 
@@ -23,6 +25,8 @@ struct State {
   bool on = false;
   std::vector<hipEvent_t> ev;  // 2 per record
   std::vector<Rec> recs;
+  std::string repeat_name;  // launches of this kernel run repeat_times times in a row
+  int repeat_times = 1;
 };
 State& S() {
   static State s;
@@ -40,6 +44,25 @@ int timer_begin(hipStream_t st, const char* name, double flops, double bytes) {
 }
 void timer_end(hipStream_t st, int idx) {
   if (idx >= 0) (void)hipEventRecord(S().ev[2 * idx + 1], st);
+}
+
+int repeat_count(const char* name) {
+  const State& s = S();
+  return (s.repeat_times > 1 && s.repeat_name == name) ? s.repeat_times : 1;
+}
+
+int set_repeat(const char* name, int times) {
+  State& s = S();
+  if (!name || times <= 1) {
+    s.repeat_name.clear();
+    s.repeat_times = 1;
+    return 0;
+  }
+  // kernels that overwrite one of their own inputs would not give the same result twice
+  if (!strcmp(name, "gemm_tn_act_bwd") || !strcmp(name, "splitk_finalize_actbwd")) return -1;
+  s.repeat_name = name;
+  s.repeat_times = times;
+  return 0;
 }
 
 int timing_enable(int enable, int capacity) {

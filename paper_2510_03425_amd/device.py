@@ -136,6 +136,11 @@ class DeviceModel:
                           self.T, ptr(ck), ptr(self.loss), self.grads, ptr(dx0), ptr(self.ws), self.ws_bytes,
                           stream_handle())
 
+    def grad_probe(self) -> torch.Tensor:
+        """First and last layers' LoRA gradients, concatenated (a cheap result fingerprint)."""
+        parts = [t.reshape(-1) for l in {0, self.L - 1} for d in (self.dA[l], self.dB[l]) for t in d.values()]
+        return torch.cat(parts) if parts else torch.zeros(1, device=self.device)
+
     def ws_view(self, slot: int, dtype: torch.dtype, shape) -> torch.Tensor:
         """A view of a workspace intermediate (tests)."""
         off = L.mebp_workspace_offset(self.ccfg, self.B, self.T, slot)
