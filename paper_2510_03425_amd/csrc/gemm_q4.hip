@@ -34,6 +34,22 @@ constexpr int BM = 128, BN = 128, BK = 64, LDT = BK + 8;  // LDS pitch in 16-bit
 constexpr int NTHREADS = 256;
 typedef uint16_t u16;
 
+// Raw buffer resources: loads through them return 0 past `bytes` (no per-element bounds
+// branches), and offsets are 32-bit VGPR values. Every resource is based at the first row
+// a workgroup touches, so a region stays far below 4 GiB.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+DEV rsrc_t make_rsrc(const void* base, size_t bytes) {
+  const uint32_t n = bytes > 0xffffffffull ? 0xffffffffu : (uint32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+DEV uint4 bload128(rsrc_t r, uint32_t off) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+DEV uint32_t bload32(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0); }
+DEV uint32_t bload16(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0); }
+
 template <class Op>
 DEV void mma_tile(const u16* As, const u16* Bs, int wm, int wn, int lane, f32x4 (&acc)[4][4]) {
 #pragma unroll
@@ -119,63 +135,99 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
   const int z = blockIdx.z, S = gridDim.z;
   const int kt_begin = (int)((long long)nk * z / S), kt_end = (int)((long long)nk * (z + 1) / S);
 
-  // three register stages of prefetched tiles, two LDS buffers
+  // three register stages of prefetched tiles, two LDS buffers. Loads go through buffer
+  // resources based at this tile's first row: rows past M (activations) or N (weights)
+  // read as 0. Only the last K tile, when K is not a multiple of BK, masks columns.
   uint4 ra[3][4];
-  uint32_t rb[3][4];
-  float rsc[3];
-  const int brow = tid >> 1, bhalf = tid & 1, bn = n0 + brow;
-  const uint8_t* wrow = sg.q4 + (size_t)bn * (K >> 1);
-
-  auto gload = [&](auto S_, int kt) {
-    constexpr int st = decltype(S_)::value;
-    const int k0 = kt * BK;
-    load_a_tile((const u16*)a.X, a.lda, a.M, K, m0, k0, tid, ra[st]);
-    const int kb = k0 + 32 * bhalf;
-    if (bn < Nn && kb < K) {
+  uint4 rb[3];
+  uint32_t rsc[3];  // raw fp16 scale bits, converted when the tile is written to LDS
+  const int brow = tid >> 1, bhalf = tid & 1;
+  const int Kh = K >> 1;
+  const rsrc_t rA = make_rsrc((const u16*)a.X + (size_t)m0 * a.lda, (size_t)min(BM, a.M - m0) * a.lda * 2);
+  const int nrows = min(BN, Nn - n0);
+  const rsrc_t rB = make_rsrc(sg.q4 + (size_t)n0 * Kh, (size_t)nrows * Kh);
+  const rsrc_t rS = make_rsrc(sg.scale + (size_t)n0 * kgroups, (size_t)nrows * kgroups * 2);
+  uint32_t offA[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int kk = kb + 8 * j;
-        rb[st][j] = kk < K ? *(const uint32_t*)(wrow + (kk >> 1)) : 0u;
-      }
-      rsc[st] = half_bits_to_f32(sg.scale[(size_t)bn * kgroups + (kb >> 5)]);
-    } else {
-      rb[st][0] = rb[st][1] = rb[st][2] = rb[st][3] = 0u;
-      rsc[st] = 0.f;
-    }
-  };
-  auto sstore = [&](auto S_, auto B_) {
-    constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
-    store_a_tile(As2[bf], tid, ra[st]);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *(uint4*)(Bs2[bf] + brow * LDT + 32 * bhalf + 8 * j) = dequant8<OpF16>(rb[st][j], rsc[st]);
-  };
+  for (int i = 0; i < 4; ++i) {
+    const int c = tid + NTHREADS * i;
+    offA[i] = (uint32_t)(((c >> 3) * a.lda + (c & 7) * 8) * 2);
+  }
+  const uint32_t offB = (uint32_t)(brow * Kh + 16 * bhalf), offS = (uint32_t)((brow * kgroups + bhalf) * 2);
 
   f32x4 acc[4][4];
   zero_acc(acc);
-  // step for tile k (I = (k - kt_begin) % 6): prefetch k+3 into the stage k just vacated,
-  // multiply the LDS buffer of k, stage k+1 into the other buffer, one barrier.
-  auto step = [&](auto I_, int k) {
-    constexpr int I = decltype(I_)::value;
-    if (k + 3 < kt_end) gload(IC<I % 3>{}, k + 3);
-    mma_tile<OpF16>(As2[I % 2], Bs2[I % 2], wm, wn, lane, acc);
-    if (k + 1 < kt_end) sstore(IC<(I + 1) % 3>{}, IC<(I + 1) % 2>{});
-    __syncthreads();
-  };
-  if (kt_begin < kt_end) {
+
+  // TAIL: K is not a multiple of BK, so the last K tile masks the columns past K.
+  auto run = [&](auto TAIL_) {
+    constexpr bool TAIL = decltype(TAIL_)::value;
+    auto gload = [&](auto S_, int kt) {
+      constexpr int st = decltype(S_)::value;
+      const int k0 = kt * BK;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ra[st][i] = bload128(rA, offA[i] + 2 * k0);
+      rb[st] = bload128(rB, offB + (k0 >> 1));
+      rsc[st] = bload16(rS, offS + 2 * (k0 >> 5));
+      if constexpr (TAIL) {
+        if (k0 + BK > K) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (((tid + NTHREADS * i) & 7) * 8 + k0 >= K) ra[st][i] = make_uint4(0, 0, 0, 0);
+          const int kb = k0 + 32 * bhalf;
+          if (kb >= K) rsc[st] = 0u;
+          if (kb + 0 >= K) rb[st].x = 0u;
+          if (kb + 8 >= K) rb[st].y = 0u;
+          if (kb + 16 >= K) rb[st].z = 0u;
+          if (kb + 24 >= K) rb[st].w = 0u;
+        }
+      }
+    };
+    auto sstore = [&](auto S_, auto B_) {
+      constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
+      store_a_tile(As2[bf], tid, ra[st]);
+      const float sc = half_bits_to_f32((uint16_t)rsc[st]);
+      u16* dst = Bs2[bf] + brow * LDT + 32 * bhalf;
+      *(uint4*)(dst + 0) = dequant8<OpF16>(rb[st].x, sc);
+      *(uint4*)(dst + 8) = dequant8<OpF16>(rb[st].y, sc);
+      *(uint4*)(dst + 16) = dequant8<OpF16>(rb[st].z, sc);
+      *(uint4*)(dst + 24) = dequant8<OpF16>(rb[st].w, sc);
+    };
+    // step for tile k (I = (k - kt_begin) % 6): prefetch tile k+3 into the register stage
+    // tile k vacated (clamped to the last tile: a redundant load, no branch), multiply
+    // the LDS buffer of tile k, write tile k+1 into the other buffer, one barrier. The
+    // six-step body is straight-line code, so the prefetches stay in flight across it.
+    auto step = [&](auto I_, int k) {
+      constexpr int I = decltype(I_)::value;
+      gload(IC<I % 3>{}, min(k + 3, kt_end - 1));
+      mma_tile<OpF16>(As2[I % 2], Bs2[I % 2], wm, wn, lane, acc);
+      sstore(IC<(I + 1) % 3>{}, IC<(I + 1) % 2>{});
+      __syncthreads();
+    };
     gload(IC<0>{}, kt_begin);
-    if (kt_begin + 1 < kt_end) gload(IC<1>{}, kt_begin + 1);
-    if (kt_begin + 2 < kt_end) gload(IC<2>{}, kt_begin + 2);
+    gload(IC<1>{}, min(kt_begin + 1, kt_end - 1));
+    gload(IC<2>{}, min(kt_begin + 2, kt_end - 1));
     sstore(IC<0>{}, IC<0>{});
     __syncthreads();
-    for (int k = kt_begin; k < kt_end; k += 6) {
+    int k = kt_begin;
+    for (; k + 6 <= kt_end; k += 6) {
       step(IC<0>{}, k);
-      if (k + 1 < kt_end) step(IC<1>{}, k + 1);
-      if (k + 2 < kt_end) step(IC<2>{}, k + 2);
-      if (k + 3 < kt_end) step(IC<3>{}, k + 3);
-      if (k + 4 < kt_end) step(IC<4>{}, k + 4);
-      if (k + 5 < kt_end) step(IC<5>{}, k + 5);
+      step(IC<1>{}, k + 1);
+      step(IC<2>{}, k + 2);
+      step(IC<3>{}, k + 3);
+      step(IC<4>{}, k + 4);
+      step(IC<5>{}, k + 5);
     }
+    if (k < kt_end) step(IC<0>{}, k);
+    if (k + 1 < kt_end) step(IC<1>{}, k + 1);
+    if (k + 2 < kt_end) step(IC<2>{}, k + 2);
+    if (k + 3 < kt_end) step(IC<3>{}, k + 3);
+    if (k + 4 < kt_end) step(IC<4>{}, k + 4);
+  };
+  if (kt_begin < kt_end) {
+    if (K % BK)
+      run(IC<1>{});
+    else
+      run(IC<0>{});
   }
 
   if constexpr (EPI == NT_LOGITS) {
@@ -307,13 +359,26 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     }
   }
 
-  // three register stages of prefetched tiles, two LDS buffers
+  // three register stages of prefetched tiles, two LDS buffers; loads through buffer
+  // resources (rows past M or past a segment's N read as 0, see the forward kernel)
   uint4 ra[3][4];
   uint32_t rw[3][4];
-  float rsc[3][4];
+  uint32_t rsc[3][4];  // raw fp16 scale bits
   int cur_n0[3], cur_N[3];  // reduction offset / length of the tile held in a stage
   const int rq = tid >> 4, co = tid & 15;
   const int kc = c0 + 8 * co;
+  const int Kh = Kout >> 1;
+  rsrc_t rA[3], rB[3], rS[3];
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    const TnSeg& sg = a.seg[s < a.nseg ? s : 0];
+    rA[s] = make_rsrc((const u16*)sg.G + (size_t)m0 * sg.ldg, (size_t)min(BM, a.M - m0) * sg.ldg * 2);
+    rB[s] = make_rsrc(sg.q4, (size_t)sg.N * Kh);
+    rS[s] = make_rsrc(sg.scale, (size_t)sg.N * kgroups * 2);
+  }
+  // columns past Kout read neighbouring bytes (kept inside the resource) and only feed
+  // output columns that are never stored
+  const uint32_t offB = (uint32_t)(4 * rq * Kh + (kc >> 1)), offS = (uint32_t)((4 * rq * kgroups + (kc >> 5)) * 2);
 
   auto locate = [&](int t, int& s, int& n0) {
     if (t < ntl[0]) {
@@ -327,79 +392,110 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     }
     n0 = t * BK;
   };
-  auto gload = [&](auto S_, int t) {
-    constexpr int st = decltype(S_)::value;
-    int s, n0;
-    locate(t, s, n0);
-    const TnSeg& sg = a.seg[s];
-    cur_n0[st] = n0;
-    cur_N[st] = sg.N;
-    load_a_tile((const u16*)sg.G, sg.ldg, a.M, sg.N, m0, n0, tid, ra[st]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int n = n0 + 4 * rq + i;
-      const bool ok = n < sg.N && kc < Kout;
-      rw[st][i] = ok ? *(const uint32_t*)(sg.q4 + (size_t)n * (Kout >> 1) + (kc >> 1)) : 0u;
-      rsc[st][i] = ok ? half_bits_to_f32(sg.scale[(size_t)n * kgroups + (kc >> 5)]) : 0.f;
-    }
-  };
-  auto sstore = [&](auto S_, auto B_) {
-    constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
-    if constexpr (AMODE == TN_A_SOFTMAX) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = tid + NTHREADS * i;
-        uint4 p = make_uint4(0, 0, 0, 0);
-        // chunks past the reduction length were zero-filled; they must stay 0, not exp(-lse)
-        if (rval[i] && cur_n0[st] + (c & 7) * 8 < cur_N[st]) {
-          const uint32_t* h = (const uint32_t*)&ra[st][i];
-          uint32_t o[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) o[j] = pack_bf16x2(__expf(f16_lo(h[j]) - rlse[i]), __expf(f16_hi(h[j]) - rlse[i]));
-          p = make_uint4(o[0], o[1], o[2], o[3]);
-        }
-        *(uint4*)(As2[bf] + (c >> 3) * LDT + (c & 7) * 8) = p;
-      }
-    } else {
-      store_a_tile(As2[bf], tid, ra[st]);
-    }
-    float v[4][8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[i][j] = (float)nib_s(rw[st][i], j) * rsc[st][i];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      uint2 pk;
-      pk.x = pack_bf16x2(v[0][j], v[1][j]);
-      pk.y = pack_bf16x2(v[2][j], v[3][j]);
-      *(uint2*)(Bs2[bf] + (8 * co + j) * LDT + 4 * rq) = pk;
-    }
-  };
-
   f32x4 acc[4][4];
   zero_acc(acc);
-  auto step = [&](auto I_, int t) {
-    constexpr int I = decltype(I_)::value;
-    if (t + 3 < t_end) gload(IC<I % 3>{}, t + 3);
-    mma_tile<OpBF16>(As2[I % 2], Bs2[I % 2], wm, wn, lane, acc);
-    if (t + 1 < t_end) sstore(IC<(I + 1) % 3>{}, IC<(I + 1) % 2>{});
-    __syncthreads();
-  };
-  if (t_begin < t_end) {
+
+  // TAIL: some segment's N is not a multiple of BK (its last tile masks A columns).
+  auto run = [&](auto TAIL_) {
+    constexpr bool TAIL = decltype(TAIL_)::value;
+    auto gload = [&](auto S_, int t) {
+      constexpr int st = decltype(S_)::value;
+      int s, n0;
+      locate(t, s, n0);
+      const TnSeg& sg = a.seg[s];
+      const rsrc_t ra_ = s == 0 ? rA[0] : s == 1 ? rA[1] : rA[2];
+      const rsrc_t rb_ = s == 0 ? rB[0] : s == 1 ? rB[1] : rB[2];
+      const rsrc_t rs_ = s == 0 ? rS[0] : s == 1 ? rS[1] : rS[2];
+      cur_n0[st] = n0;
+      cur_N[st] = sg.N;
+  #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = tid + NTHREADS * i;
+        ra[st][i] = bload128(ra_, (uint32_t)(((c >> 3) * sg.ldg + (c & 7) * 8 + n0) * 2));
+      }
+  #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        rw[st][i] = bload32(rb_, offB + (uint32_t)((n0 + i) * Kh));
+        rsc[st][i] = bload16(rs_, offS + (uint32_t)((n0 + i) * kgroups * 2));
+      }
+      if constexpr (TAIL) {
+        if (n0 + BK > sg.N) {  // reduction tail: A columns past N must be 0 (B rows already are)
+  #pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (n0 + ((tid + NTHREADS * i) & 7) * 8 >= sg.N) ra[st][i] = make_uint4(0, 0, 0, 0);
+        }
+      }
+    };
+    auto sstore = [&](auto S_, auto B_) {
+      constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
+      if constexpr (AMODE == TN_A_SOFTMAX) {
+  #pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int c = tid + NTHREADS * i;
+          uint4 p = make_uint4(0, 0, 0, 0);
+          // chunks past the reduction length were zero-filled; they must stay 0, not exp(-lse)
+          if (rval[i] && cur_n0[st] + (c & 7) * 8 < cur_N[st]) {
+            const uint32_t* h = (const uint32_t*)&ra[st][i];
+            uint32_t o[4];
+  #pragma unroll
+            for (int j = 0; j < 4; ++j) o[j] = pack_bf16x2(__expf(f16_lo(h[j]) - rlse[i]), __expf(f16_hi(h[j]) - rlse[i]));
+            p = make_uint4(o[0], o[1], o[2], o[3]);
+          }
+          *(uint4*)(As2[bf] + (c >> 3) * LDT + (c & 7) * 8) = p;
+        }
+      } else {
+        store_a_tile(As2[bf], tid, ra[st]);
+      }
+      float v[4][8];
+  #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sc = half_bits_to_f32((uint16_t)rsc[st][i]);
+  #pragma unroll
+        for (int j = 0; j < 8; ++j) v[i][j] = (float)nib_s(rw[st][i], j) * sc;
+      }
+  #pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        uint2 pk;
+        pk.x = pack_bf16x2(v[0][j], v[1][j]);
+        pk.y = pack_bf16x2(v[2][j], v[3][j]);
+        *(uint2*)(Bs2[bf] + (8 * co + j) * LDT + 4 * rq) = pk;
+      }
+    };
+    // same pipeline as the forward kernel
+    auto step = [&](auto I_, int t) {
+      constexpr int I = decltype(I_)::value;
+      gload(IC<I % 3>{}, min(t + 3, t_end - 1));
+      mma_tile<OpBF16>(As2[I % 2], Bs2[I % 2], wm, wn, lane, acc);
+      sstore(IC<(I + 1) % 3>{}, IC<(I + 1) % 2>{});
+      __syncthreads();
+    };
     gload(IC<0>{}, t_begin);
-    if (t_begin + 1 < t_end) gload(IC<1>{}, t_begin + 1);
-    if (t_begin + 2 < t_end) gload(IC<2>{}, t_begin + 2);
+    gload(IC<1>{}, min(t_begin + 1, t_end - 1));
+    gload(IC<2>{}, min(t_begin + 2, t_end - 1));
     sstore(IC<0>{}, IC<0>{});
     __syncthreads();
-    for (int t = t_begin; t < t_end; t += 6) {
+    int t = t_begin;
+    for (; t + 6 <= t_end; t += 6) {
       step(IC<0>{}, t);
-      if (t + 1 < t_end) step(IC<1>{}, t + 1);
-      if (t + 2 < t_end) step(IC<2>{}, t + 2);
-      if (t + 3 < t_end) step(IC<3>{}, t + 3);
-      if (t + 4 < t_end) step(IC<4>{}, t + 4);
-      if (t + 5 < t_end) step(IC<5>{}, t + 5);
+      step(IC<1>{}, t + 1);
+      step(IC<2>{}, t + 2);
+      step(IC<3>{}, t + 3);
+      step(IC<4>{}, t + 4);
+      step(IC<5>{}, t + 5);
     }
+    if (t < t_end) step(IC<0>{}, t);
+    if (t + 1 < t_end) step(IC<1>{}, t + 1);
+    if (t + 2 < t_end) step(IC<2>{}, t + 2);
+    if (t + 3 < t_end) step(IC<3>{}, t + 3);
+    if (t + 4 < t_end) step(IC<4>{}, t + 4);
+  };
+  if (t_begin < t_end) {
+    bool tail = false;
+    for (int s = 0; s < a.nseg; ++s) tail |= (a.seg[s].N % BK) != 0;
+    if (tail)
+      run(IC<1>{});
+    else
+      run(IC<0>{});
   }
 
   if constexpr (EPI == TN_PARTIAL_F32) {
