@@ -378,6 +378,34 @@ def lm_head_ce(cfg, E_hat: np.ndarray, norm_final: np.ndarray, xL: np.ndarray, i
     return loss, dxL
 
 
+def lm_head_ce_rows(cfg, E_hat: np.ndarray, norm_final: np.ndarray, x_rows: np.ndarray, tgt: np.ndarray,
+                    n: int):
+    """The LM head's per-row terms for selected rows only. Every row's share of the loss
+    and of dL/dx_L depends on that row alone (RMSNorm, logits and softmax are row-wise):
+    ``row_loss = lse(z) - z[tgt]`` and ``dx = rmsnorm_bwd((softmax(z) - onehot(tgt)) E_hat / n)``
+    with ``z = RMSNorm(x) E_hat^T``. ``tgt < 0`` marks a row without a target (zero term,
+    zero gradient); ``n`` is the full problem's number of target positions. Used to check
+    sampled rows of shapes whose full logits the CPU cannot afford. Returns
+    (row_loss [k], dx_rows [k][d])."""
+    x_rows = np.asarray(x_rows, F64)
+    tgt = np.asarray(tgt, np.int64)
+    hf, rstd = rmsnorm(x_rows, norm_final, cfg.rms_eps)
+    row_loss = np.zeros(len(tgt))
+    dhf = np.zeros_like(hf)
+    rows = np.nonzero(tgt >= 0)[0]
+    if rows.size:
+        z = hf[rows] @ E_hat.T
+        m = z.max(axis=-1, keepdims=True)
+        e = np.exp(z - m)
+        ssum = e.sum(axis=-1, keepdims=True)
+        t = tgt[rows]
+        row_loss[rows] = (m + np.log(ssum))[:, 0] - z[np.arange(rows.size), t]
+        dz = e / ssum
+        dz[np.arange(rows.size), t] -= 1.0
+        dhf[rows] = (dz / n) @ E_hat
+    return row_loss, rmsnorm_bwd(x_rows, norm_final, rstd, dhf)
+
+
 def lm_head_logits(cfg, E_hat, norm_final, xL):
     """Full logits ``[B*T][V]`` (small shapes only; used by pins)."""
     hf, _ = rmsnorm(np.asarray(xL, F64), norm_final, cfg.rms_eps)

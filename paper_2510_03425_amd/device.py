@@ -55,7 +55,9 @@ class DeviceModel:
         self.ccfg = make_config(cfg)
         self.L = len(inp.base)
         if self.L != cfg.n_layers:
-            self.ccfg.n_layers = self.L
+            # a truncated input set (per-layer or LM-head-only use); with no layer at all the
+            # config still needs one for validation, and train_step is refused
+            self.ccfg.n_layers = max(self.L, 1)
         self.keep: List[torch.Tensor] = []
         self.base = (L.MebpLayerBase * self.L)()
         self.lora = (L.MebpLayerLora * self.L)()
@@ -131,6 +133,8 @@ class DeviceModel:
         return self.ckpt
 
     def train_step(self, dx0: Optional[torch.Tensor] = None):
+        if self.L == 0:
+            raise ValueError("this input set has no layers")
         ck = self.alloc_ckpt()
         L.mebp_train_step(self.ccfg, self.emb, self.base, ptr(self.norm_final), self.lora, ptr(self.ids), self.B,
                           self.T, ptr(ck), ptr(self.loss), self.grads, ptr(dx0), ptr(self.ws), self.ws_bytes,

@@ -228,6 +228,13 @@ def test_train_step_parity_qwen05b(built_lib, gpu):
     _step_parity(cfg, make_inputs(cfg, seed=0), gpu)
 
 
+def test_train_step_parity_gemma1b(built_lib, gpu):
+    # 26 layers with the 5 local : 1 global pattern, GeGLU, head_dim 256, one KV head,
+    # LoRA r16, V = 262144: the whole step against the fp64 oracle
+    cfg = CONFIGS["gemma3-1b"]
+    _step_parity(cfg, make_inputs(cfg, seed=0), gpu)
+
+
 def test_hip_graph_replay_matches_eager(built_lib, gpu):
     """The whole step captured as one HIP graph and replayed several times (with eager
     work and synchronisations between replays) reproduces the eager step bit for bit."""

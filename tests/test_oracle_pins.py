@@ -387,6 +387,30 @@ def test_block_backward_elementwise_fd_few_entries():
         assert abs(fd - dx[n, i]) <= 1e-6 * max(1.0, abs(dx[n, i]))
 
 
+def test_lm_head_rows_pins():
+    # per-row form: FD of its own partial loss, consistency with the whole-batch head,
+    # uniform logits give ln V per row, rows without a target contribute nothing
+    cfg = TINY
+    inp = make_inputs(cfg, seed=4, norm="random")
+    E = O.decompress_embedding(cfg, inp)
+    rng = np.random.default_rng(8)
+    xL = rng.standard_normal((cfg.n_tokens, cfg.hidden))
+    n = cfg.batch * (cfg.seq - 1)
+    tgt = np.full(cfg.n_tokens, -1)
+    tgt.reshape(cfg.batch, cfg.seq)[:, :-1] = inp.ids[:, 1:]
+    rows = np.array([0, 3, cfg.seq - 1, cfg.seq + 2])
+    rl, dx = O.lm_head_ce_rows(cfg, E, inp.norm_final, xL[rows], tgt[rows], n)
+    _assert_fd(lambda xx: float(np.sum(O.lm_head_ce_rows(cfg, E, inp.norm_final, xx, tgt[rows], n)[0])) / n,
+               xL[rows], dx)
+    assert rl[2] == 0 and np.all(dx[2] == 0)  # position T-1: no target
+    loss, dx_all = O.lm_head_ce(cfg, E, inp.norm_final, xL, inp.ids)
+    rl_all, dx_rows_all = O.lm_head_ce_rows(cfg, E, inp.norm_final, xL, tgt, n)
+    assert abs(rl_all.sum() / n - loss) <= 1e-12 * abs(loss)
+    np.testing.assert_allclose(dx_rows_all, dx_all, rtol=0, atol=1e-15)
+    rl0, dx0 = O.lm_head_ce_rows(cfg, np.zeros_like(E), inp.norm_final, xL[rows], tgt[rows], n)
+    np.testing.assert_allclose(rl0[[0, 1, 3]], math.log(cfg.vocab), rtol=1e-14)
+
+
 def test_lm_head_block_finite_differences():
     cfg = TINY
     inp = make_inputs(cfg, seed=9, norm="random")
