@@ -55,19 +55,17 @@ struct Layout {
 };
 
 size_t nt_part(int M, int K, std::initializer_list<int> Ns) {
-  int tiles = 0, ncat = 0;
-  for (int n : Ns) {
-    tiles += gemm_nt_tiles(n);
-    ncat += n;
+  int v[3], n = 0, ncat = 0;
+  for (int x : Ns) {
+    v[n++] = x;
+    ncat += x;
   }
-  const int mt = (M + kGemmBM - 1) / kGemmBM;
-  return gemm_part_floats(M, ncat, gemm_splits(tiles * mt, (K + kGemmBK - 1) / kGemmBK));
+  return gemm_part_floats(M, ncat, plan_nt(M, v, n, K, NT_STORE_F32).splits);
 }
 size_t tn_part(int M, int Kout, std::initializer_list<int> Ns) {
-  int kt = 0;
-  for (int n : Ns) kt += (n + kGemmBK - 1) / kGemmBK;
-  const int tiles = ((Kout + kGemmBN - 1) / kGemmBN) * ((M + kGemmBM - 1) / kGemmBM);
-  return gemm_part_floats(M, Kout, gemm_splits(tiles, kt));
+  int v[3], n = 0;
+  for (int x : Ns) v[n++] = x;
+  return gemm_part_floats(M, Kout, plan_tn(M, Kout, v, n).splits);
 }
 
 int lm_head_splits(int N, int d, int V) {
@@ -85,7 +83,7 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
                kvd = (size_t)c->n_kv_heads * c->head_dim, F = c->ffn, r = c->lora_rank > 0 ? c->lora_rank : 16,
                V = c->vocab, H = c->n_heads;
   L->lm_splits = V ? lm_head_splits((int)N, (int)d, (int)V) : 0;
-  L->ntiles = V ? gemm_nt_tiles((int)V) : 0;
+  L->ntiles = V ? gemm_logit_stat_tiles((int)N, (int)V, (int)d) : 0;
   size_t sz[S_COUNT] = {};
   sz[S_A] = N * d * 2;
   sz[S_Q] = N * qd * 2;

@@ -97,6 +97,27 @@ DEV float wave_max(float v) {
   return v;
 }
 
+// Raw buffer resources: loads through them return 0 past `bytes` (no per-element bounds
+// branches), and offsets are 32-bit VGPR values. Every resource is based at the first row
+// a workgroup touches, so a region stays far below 4 GiB.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+DEV rsrc_t make_rsrc(const void* base, size_t bytes) {
+  const uint32_t n = bytes > 0xffffffffull ? 0xffffffffu : (uint32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+DEV uint4 bload128(rsrc_t r, uint32_t off) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+DEV uint2 bload64(rsrc_t r, uint32_t off) {
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+  return make_uint2(v.x, v.y);
+}
+DEV uint32_t bload32(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0); }
+DEV uint32_t bload16(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0); }
+
 // 16-bit element transpose helpers: select the low (or high) halves of two dwords.
 DEV uint32_t perm_lo16(uint32_t a, uint32_t b) {  // (a.lo, b.lo) -> lo=a.lo, hi=b.lo
   return __builtin_amdgcn_perm(b, a, 0x05040100u);

@@ -1,0 +1,778 @@
+// Large-tile int4 group-dequant GEMMs for many tokens (M = B*T in the thousands): the same
+// products as gemm_q4.hip (forward "NT" and transposed "TN", Algorithm 1's lazily
+// decompressed weights fused into the operand load), with a tiling sized for MFMA
+// throughput rather than for latency.
+//
+// One 256 x BN output tile per 256-thread workgroup (BN = 256 or 128), 2 x 2 waves of
+// 128 x BN/2, v_mfma_f32_32x32x16 (fp16 operands forward, bf16 backward), K step 64.
+// Per wave and K step the fragments read from LDS are (128 + BN/2) x 64 16-bit values for
+// 128 x BN/2 x 64 MACs: 32 MACs per LDS byte at BN = 256 (16 for the 128 x 128 tiles of
+// gemm_q4.hip), so LDS reads take about half of the MFMA time at the chip's 128 B/clk/CU.
+// One workgroup per CU (up to 144 KB of LDS, 256 fp32 accumulators per lane). Pipeline:
+// the global loads of K tile t+2 are issued before the MFMAs of tile t, and tile t+1 is
+// decompressed from registers into the other LDS buffer after them.
+//
+// MFMA 32x32x16 lane layout: lane l supplies A[l%32][8(l/32) .. +8] and
+// B[8(l/32) .. +8][l%32]; accumulator element q of lane l is D[8(q/4) + 4(l/32) + q%4][l%32].
+//
+// The LoRA up-projection (unsplit case) is three extra bf16 MFMAs per accumulator tile on
+// the fp32 factors split into bf16 hi + lo parts (hi*hi + hi*lo + lo*hi, relative error
+// below 2^-16), so no scalar epilogue loop is needed.
+#include "device_common.h"
+#include "mebp_internal.h"
+
+namespace mebp {
+namespace {
+
+constexpr int BM = 256, BK = 64, LDT = BK + 8, NTH = 256;
+typedef uint16_t u16;
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+template <int N>
+struct IC {
+  static constexpr int value = N;
+};
+
+template <class Op>
+DEV f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
+  if constexpr (__is_same(Op, OpF16))
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0,
+                                                  0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                   0, 0);
+}
+
+template <int NJ>
+DEV void zero_acc(f32x16 (&acc)[4][NJ]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+}
+
+// tile-local row of accumulator element q of row block i, and column of column block j
+DEV int acc_row(int wm, int i, int q, int lane) { return wm * 128 + 32 * i + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3); }
+template <int NJ>
+DEV int acc_col(int wn, int j, int lane) {
+  return wn * 32 * NJ + 32 * j + (lane & 31);
+}
+
+// One K tile of the wave's 128 x 32NJ block from the LDS tiles (row pitch LDT; A rows are
+// M, B rows are N, both K-contiguous).
+template <class Op, int NJ>
+DEV void mma_tile(const u16* As, const u16* Bs, int wm, int wn, int lane, f32x16 (&acc)[4][NJ]) {
+  const int r = lane & 31, kh = 8 * (lane >> 5);
+  const u16* pa = As + (wm * 128 + r) * LDT + kh;
+  const u16* pb = Bs + (wn * 32 * NJ + r) * LDT + kh;
+#pragma unroll
+  for (int ks = 0; ks < BK; ks += 16) {
+    uint4 af[4], bfr[NJ];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[i] = *(const uint4*)(pa + 32 * i * LDT + ks);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) bfr[j] = *(const uint4*)(pb + 32 * j * LDT + ks);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<Op>(af[i], bfr[j], acc[i][j]);
+  }
+}
+
+// v (8 fp32) -> bf16 hi and lo parts with v ~ hi + lo
+DEV void split_bf16(const float (&v)[8], uint4& hi, uint4& lo) {
+  float h[8], l[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    h[e] = (float)(bf16)v[e];
+    l[e] = v[e] - h[e];
+  }
+  hi = make_uint4(pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]), pack_bf16x2(h[4], h[5]), pack_bf16x2(h[6], h[7]));
+  lo = make_uint4(pack_bf16x2(l[0], l[1]), pack_bf16x2(l[2], l[3]), pack_bf16x2(l[4], l[5]), pack_bf16x2(l[6], l[7]));
+}
+
+// acc += s * U[m][:r] . V(col)[:r] for the wave's block: U fp32 [M][r] (rows from mrow0),
+// V(col)[q] = V[col * vcol + q * vq] fp32 (columns from ccol0, < ncols); r = 8 or 16 (the
+// rank is the MFMA's K = 16; lanes past r supply zeros). All loads go through buffer
+// resources (rows past M, columns past ncols read 0) and are issued before any use, so
+// they overlap instead of waiting one by one.
+template <int NJ>
+DEV void lora_mfma(f32x16 (&acc)[4][NJ], const float* U, int r, int mrow0, int M, float s, const float* V,
+                   int vcol, int vq, int ccol0, int ncols, int lane) {
+  const int q0 = 8 * (lane >> 5);
+  const bool keep = q0 < r;  // select, not multiply: a neighbouring row's value may be non-finite
+  const rsrc_t rU = make_rsrc(U, (size_t)M * r * 4);
+  const rsrc_t rV = make_rsrc(V, (size_t)((ncols - 1) * vcol + (r - 1) * vq + 1) * 4);
+  float vv[NJ][8], uu[4][8];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int c = ccol0 + 32 * j + (lane & 31);
+    const bool cok = c < ncols;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      vv[j][e] = __builtin_bit_cast(float, bload32(rV, cok ? (uint32_t)((c * vcol + (q0 + e) * vq) * 4) : 0xffffffffu));
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = mrow0 + 32 * i + (lane & 31);
+    const uint4 a0 = bload128(rU, (uint32_t)((m * r + q0) * 4)), a1 = bload128(rU, (uint32_t)((m * r + q0 + 4) * 4));
+    uu[i][0] = __builtin_bit_cast(float, a0.x); uu[i][1] = __builtin_bit_cast(float, a0.y);
+    uu[i][2] = __builtin_bit_cast(float, a0.z); uu[i][3] = __builtin_bit_cast(float, a0.w);
+    uu[i][4] = __builtin_bit_cast(float, a1.x); uu[i][5] = __builtin_bit_cast(float, a1.y);
+    uu[i][6] = __builtin_bit_cast(float, a1.z); uu[i][7] = __builtin_bit_cast(float, a1.w);
+  }
+  uint4 bh[NJ], bl[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = keep ? vv[j][e] : 0.f;
+    split_bf16(v, bh[j], bl[j]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float u[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) u[e] = keep ? s * uu[i][e] : 0.f;
+    uint4 ah, al;
+    split_bf16(u, ah, al);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      acc[i][j] = mfma32<OpBF16>(ah, bh[j], acc[i][j]);
+      acc[i][j] = mfma32<OpBF16>(ah, bl[j], acc[i][j]);
+      acc[i][j] = mfma32<OpBF16>(al, bh[j], acc[i][j]);
+    }
+  }
+}
+
+// split-K: the workgroup's partial tile into the plane of its split ([M][ldp] fp32, columns
+// from c0), reduced in split order by a finalize kernel
+template <int NJ>
+DEV void store_partial(const f32x16 (&acc)[4][NJ], float* plane, int M, int ldp, int ncols, int m0, int c0, int wm,
+                       int wn, int lane) {
+  auto put = [&](auto FULL_) {
+    constexpr bool FULL = decltype(FULL_)::value;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int m = m0 + acc_row(wm, i, q, lane);
+        if (!FULL && m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int c = acc_col<NJ>(wn, j, lane);
+          if (!FULL && c >= ncols) continue;
+          plane[(size_t)m * ldp + c0 + c] = acc[i][j][q];
+        }
+      }
+  };
+  if (m0 + BM <= M && 64 * NJ <= ncols)
+    put(IC<1>{});
+  else
+    put(IC<0>{});
+}
+
+// A-operand staging: 8 chunks of 8 16-bit elements per thread; chunk c = tid + 256 i covers
+// row c >> 3 (= tid/8 + 32 i), columns (c & 7) * 8 .. +8 of the 256 x 64 tile.
+DEV void store_a_tile(u16* As, int tid, const uint4 (&ra)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int c = tid + NTH * i;
+    *(uint4*)(As + (c >> 3) * LDT + (c & 7) * 8) = ra[i];
+  }
+}
+
+// ------------------------------------------------------------------------------ forward
+// C[m][n] = sum_k X[m][k] W[n][k] (+ s u B^T + resid), fp16 operands.
+//
+// The weight operand does not go through LDS: for MFMA column j of its block a lane needs
+// 8 reduction indices of one weight row, i.e. one dword of codes. Within a K tile of 64 a
+// lane of half h (= lane / 32) takes the four consecutive dwords 4h .. 4h+3 of its row (one
+// 16-byte load, one 32-group, one scale) and uses dword 4h+s in substep s; the activation
+// fragments read from LDS follow the same assignment of reduction indices. Decompression is
+// done with packed fp16 arithmetic, which orders the eight values of a dword as
+// (k0,k4),(k1,k5),(k2,k6),(k3,k7); activation chunks are stored into LDS in that order too.
+// Each wave thus decompresses only the weights it multiplies, and LDS carries the
+// activation tile alone.
+
+// 8 int4 codes (two's complement, element i in bits 4i..4i+3) times scale into fp16 pairs
+// (k0,k4),(k1,k5),(k2,k6),(k3,k7): 0x6400 | (q + 8) is the fp16 value 1024 + q + 8, so one
+// packed subtraction of 1032 gives q exactly and one packed multiply rounds q * s to nearest.
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+DEV uint4 dequant8_paired(uint32_t w, f16x2 s2) {
+  const uint32_t x = w ^ 0x88888888u;
+  const f16x2 off = {(_Float16)1032.0f, (_Float16)1032.0f};
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t t = ((x >> (4 * j)) & 0x000F000Fu) | 0x64006400u;
+    const f16x2 v = (__builtin_bit_cast(f16x2, t) - off) * s2;
+    o[j] = __builtin_bit_cast(uint32_t, v);
+  }
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// (k0..k7) -> (k0,k4),(k1,k5),(k2,k6),(k3,k7), the order of dequant8_paired
+DEV uint4 pair_order(uint4 d) {
+  return make_uint4(perm_lo16(d.x, d.z), perm_hi16(d.x, d.z), perm_lo16(d.y, d.w), perm_hi16(d.y, d.w));
+}
+
+// The segment's fields as scalar values: indexing the argument struct with a run-time
+// segment number would make the compiler copy it to scratch memory.
+DEV NtSeg pick_seg(const NtArgs& a, int s) {
+  NtSeg r;
+#define PICK(f) r.f = s == 0 ? a.seg[0].f : (s == 1 ? a.seg[1].f : a.seg[2].f)
+  PICK(q4);
+  PICK(scale);
+  PICK(N);
+  PICK(tile0);
+  PICK(col0);
+  PICK(lora_u);
+  PICK(lora_B);
+  PICK(out);
+  PICK(ldo);
+  PICK(resid);
+  PICK(ldr);
+#undef PICK
+  r.rope = 0;
+  r.item0 = 0;
+  return r;
+}
+
+// WNW waves along n (2 or 4), two along m: 128 x WNW threads, each wave 128 x BN/WNW. With
+// four (512 threads) two waves share each SIMD, so one wave's decompression (VALU) runs
+// beside the other's MFMAs.
+template <int BN, int WNW, int EPI>
+__global__ __launch_bounds__(128 * WNW, 1) void k_gemm_nt_big(const NtArgs a) {
+  constexpr int NT = 128 * WNW;
+  constexpr int NJ = BN / (32 * WNW);  // 32-column blocks per wave
+  constexpr int NA = 2048 / NT;        // 16-byte activation chunks per thread and K tile
+  __shared__ __attribute__((aligned(16))) u16 As2[2][BM * LDT];
+  // the wave index is wave-uniform; saying so keeps the weight resources in SGPRs
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WNW, wn = wave % WNW, h = lane >> 5;
+  const int nt = blockIdx.x;
+  int s = 0;
+  if (a.nseg > 1 && nt >= a.seg[1].tile0) s = 1;
+  if (a.nseg > 2 && nt >= a.seg[2].tile0) s = 2;
+  const NtSeg sg = pick_seg(a, s);
+  const int n0 = (nt - sg.tile0) * BN, m0 = blockIdx.y * BM;
+  const int K = a.K, Nn = sg.N, Kh = K >> 1;
+  const int nk = (K + BK - 1) / BK, kgroups = (K + 31) >> 5;
+  const int z = blockIdx.z, S = gridDim.z;
+  const int kt_begin = (int)((long long)nk * z / S), kt_end = (int)((long long)nk * (z + 1) / S);
+
+  const rsrc_t rA = make_rsrc((const u16*)a.X + (size_t)m0 * a.lda, (size_t)min(BM, a.M - m0) * a.lda * 2);
+  const int wcol0 = n0 + wn * 32 * NJ;  // first weight row (output column) of this wave
+  const int wrows = max(0, min(32 * NJ, Nn - wcol0));
+  const rsrc_t rB = make_rsrc(sg.q4 + (size_t)min(wcol0, Nn) * Kh, (size_t)wrows * Kh);
+  const rsrc_t rS = make_rsrc(sg.scale + (size_t)min(wcol0, Nn) * kgroups, (size_t)wrows * kgroups * 2);
+  uint32_t offA[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int c = tid + NT * i;
+    offA[i] = (uint32_t)(((c >> 3) * a.lda + (c & 7) * 8) * 2);
+  }
+  const uint32_t offB = (uint32_t)((lane & 31) * Kh + 16 * h), offS = (uint32_t)(((lane & 31) * kgroups + h) * 2);
+
+  uint4 ra[2][NA];
+  uint4 rb[2][NJ];
+  uint32_t rsc[2][NJ];  // raw fp16 scale bits
+  f32x16 acc[4][NJ];
+  zero_acc(acc);
+
+  auto run = [&](auto TAIL_) {
+    constexpr bool TAIL = decltype(TAIL_)::value;
+    auto gload_a = [&](auto S_, int kt) {
+      constexpr int st = decltype(S_)::value;
+      const int k0 = kt * BK;
+#pragma unroll
+      for (int i = 0; i < NA; ++i) ra[st][i] = bload128(rA, offA[i] + 2 * k0);
+      if constexpr (TAIL) {
+        if (k0 + BK > K) {  // zero what lies past the reduction length
+#pragma unroll
+          for (int i = 0; i < NA; ++i)
+            if (((tid + NT * i) & 7) * 8 + k0 >= K) ra[st][i] = make_uint4(0, 0, 0, 0);
+        }
+      }
+    };
+    auto gload_b = [&](auto S_, int kt) {
+      constexpr int st = decltype(S_)::value;
+      const int k0 = kt * BK;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        rb[st][j] = bload128(rB, offB + (uint32_t)(32 * j * Kh) + (k0 >> 1));
+        rsc[st][j] = bload16(rS, offS + (uint32_t)(32 * j * kgroups * 2) + 2 * (k0 >> 5));
+      }
+      if constexpr (TAIL) {
+        if (k0 + BK > K) {
+          const int kb = k0 + 32 * h;
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            if (kb >= K) rsc[st][j] = 0u;
+            if (kb + 0 >= K) rb[st][j].x = 0u;
+            if (kb + 8 >= K) rb[st][j].y = 0u;
+            if (kb + 16 >= K) rb[st][j].z = 0u;
+            if (kb + 24 >= K) rb[st][j].w = 0u;
+          }
+        }
+      }
+    };
+    auto sstore = [&](auto S_, auto B_) {
+      constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const int c = tid + NT * i;
+        *(uint4*)(As2[bf] + (c >> 3) * LDT + (c & 7) * 8) = pair_order(ra[st][i]);
+      }
+    };
+    // the MFMAs of one K tile: substep t uses chunk 4h + t of the lane's reduction range
+    auto mma = [&](auto S_, auto B_) {
+      constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
+      const u16* pa = As2[bf] + (wm * 128 + (lane & 31)) * LDT + 32 * h;
+      f16x2 sc[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)rsc[st][j]);
+        sc[j] = f16x2{v, v};
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        uint4 af[4], bfr[NJ];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = *(const uint4*)(pa + 32 * i * LDT + 8 * t);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const uint32_t w = t == 0 ? rb[st][j].x : t == 1 ? rb[st][j].y : t == 2 ? rb[st][j].z : rb[st][j].w;
+          bfr[j] = dequant8_paired(w, sc[j]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpF16>(af[i], bfr[j], acc[i][j]);
+      }
+    };
+    // step for tile k (I = parity): loads of tile k+2 into the A stage tile k vacated, the
+    // MFMAs of tile k (LDS buffer I, weights of stage I), tile k+1's activations into the
+    // other LDS buffer, one barrier. The weight stage of tile k is consumed by the MFMAs, so
+    // tile k+2's weights are loaded after them.
+    auto step = [&](auto I_, int k) {
+      constexpr int I = decltype(I_)::value;
+      const int kn = min(k + 2, kt_end - 1);
+      gload_a(IC<I>{}, kn);
+      mma(IC<I>{}, IC<I>{});
+      gload_b(IC<I>{}, kn);
+      sstore(IC<1 - I>{}, IC<1 - I>{});
+      __syncthreads();
+    };
+    gload_a(IC<0>{}, kt_begin);
+    gload_b(IC<0>{}, kt_begin);
+    gload_a(IC<1>{}, min(kt_begin + 1, kt_end - 1));
+    gload_b(IC<1>{}, min(kt_begin + 1, kt_end - 1));
+    sstore(IC<0>{}, IC<0>{});
+    __syncthreads();
+    int k = kt_begin;
+    for (; k + 2 <= kt_end; k += 2) {
+      step(IC<0>{}, k);
+      step(IC<1>{}, k + 1);
+    }
+    if (k < kt_end) step(IC<0>{}, k);
+  };
+  if (kt_begin < kt_end) {
+    if (K % BK)
+      run(IC<1>{});
+    else
+      run(IC<0>{});
+  }
+
+  if constexpr (EPI == NT_LOGITS) {
+    // every wave covers one statistics tile of 32 NJ columns
+    _Float16* out = (_Float16*)sg.out;
+    const int cw0 = wcol0;
+    const int stile = cw0 / (32 * NJ);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int m = m0 + acc_row(wm, i, q, lane);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          if (cw0 + 32 * j + (lane & 31) < Nn) mx = fmaxf(mx, acc[i][j][q]);
+#pragma unroll
+        for (int o = 1; o < 32; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+        const int tg = m < a.M ? a.tgt[m] : -1;
+        float se = 0.f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int n = cw0 + 32 * j + (lane & 31);
+          if (n < Nn) {
+            const float v = acc[i][j][q];
+            se += __expf(v - mx);
+            if (m < a.M) {
+              out[(size_t)m * sg.ldo + n] = (_Float16)v;
+              if (n == tg) a.tgt_logit[m] = v;
+            }
+          }
+        }
+#pragma unroll
+        for (int o = 1; o < 32; o <<= 1) se += __shfl_xor(se, o, 64);
+        if ((lane & 31) == 0 && m < a.M && cw0 < Nn) a.stats[(size_t)m * a.ntiles + stile] = make_float2(mx, se);
+      }
+    }
+    return;
+  } else {
+    if (S > 1) {
+      store_partial<NJ>(acc, a.part + (size_t)z * a.M * a.ldp, a.M, a.ldp, Nn - n0, m0, sg.col0 + n0, wm, wn, lane);
+      return;
+    }
+    if (sg.lora_B)
+      lora_mfma<NJ>(acc, sg.lora_u, a.r, m0 + wm * 128, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, Nn, lane);
+    auto put = [&](auto FULL_, auto RES_) {
+      constexpr bool FULL = decltype(FULL_)::value, RES = decltype(RES_)::value;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int m = m0 + acc_row(wm, i, q, lane);
+          if (!FULL && m >= a.M) continue;
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int n = n0 + acc_col<NJ>(wn, j, lane);
+            if (!FULL && n >= Nn) continue;
+            float v = acc[i][j][q];
+            if constexpr (RES) v += sg.resid[(size_t)m * sg.ldr + n];
+            if constexpr (EPI == NT_STORE_F16)
+              ((f16*)sg.out)[(size_t)m * sg.ldo + n] = (f16)v;
+            else
+              ((float*)sg.out)[(size_t)m * sg.ldo + n] = v;
+          }
+        }
+    };
+    const bool full = m0 + BM <= a.M && n0 + BN <= Nn;
+    if (sg.resid) {
+      if (full) put(IC<1>{}, IC<1>{}); else put(IC<0>{}, IC<1>{});
+    } else {
+      if (full) put(IC<1>{}, IC<0>{}); else put(IC<0>{}, IC<0>{});
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------- transposed
+// C[m][c] = sum_seg sum_n G_seg[m][n] W_seg[n][c] (+ sum_seg du_seg A_seg), bf16 operands.
+// The weight tile (64 rows n x BN columns c) is decompressed per thread as RPT rows x 16
+// columns and written transposed, n-contiguous, into LDS.
+template <int BN, int EPI, int AMODE>
+__global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
+  constexpr int NJ = BN / 64;
+  constexpr int CG = BN / 16;   // 16-column groups
+  constexpr int RG = NTH / CG;  // row groups
+  constexpr int RPT = BK / RG;  // weight rows per thread (4 or 2)
+  __shared__ __attribute__((aligned(16))) u16 As2[2][BM * LDT];
+  __shared__ __attribute__((aligned(16))) u16 Bs2[2][BN * LDT];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int c0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  const int Kout = a.Kout, Kh = Kout >> 1, kgroups = (Kout + 31) >> 5;
+  const int z = blockIdx.z, S = gridDim.z;
+
+  int ntl[3], total = 0;
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    ntl[s] = s < a.nseg ? (a.seg[s].N + BK - 1) / BK : 0;
+    total += ntl[s];
+  }
+  const int t_begin = (int)((long long)total * z / S), t_end = (int)((long long)total * (z + 1) / S);
+
+  float rlse[8];
+  bool rval[8];
+  if constexpr (AMODE == TN_A_SOFTMAX) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int m = m0 + ((tid + NTH * i) >> 3);
+      rval[i] = m < a.M && a.tgt[m] >= 0;
+      rlse[i] = rval[i] ? a.lse[m] : 0.f;
+    }
+  }
+
+  rsrc_t rA[3], rB[3], rS[3];
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    const TnSeg& sg = a.seg[s < a.nseg ? s : 0];
+    rA[s] = make_rsrc((const u16*)sg.G + (size_t)m0 * sg.ldg, (size_t)min(BM, a.M - m0) * sg.ldg * 2);
+    rB[s] = make_rsrc(sg.q4, (size_t)sg.N * Kh);
+    rS[s] = make_rsrc(sg.scale, (size_t)sg.N * kgroups * 2);
+  }
+  // row group varies fastest across lanes so that the transposed LDS writes do not collide
+  const int rq = tid % RG, cq = tid / RG;
+  const int kc = c0 + 16 * cq;
+  const uint32_t offB = (uint32_t)(RPT * rq * Kh + (kc >> 1));
+  const uint32_t offS = (uint32_t)((RPT * rq * kgroups + (kc >> 5)) * 2);
+
+  uint4 ra[2][8];
+  uint2 rw[2][RPT];
+  uint32_t rsc[2][RPT];
+  int cur_n0[2], cur_N[2];
+  f32x16 acc[4][NJ];
+  zero_acc(acc);
+
+  auto locate = [&](int t, int& s, int& n0) {
+    if (t < ntl[0]) {
+      s = 0;
+    } else if (t < ntl[0] + ntl[1]) {
+      s = 1;
+      t -= ntl[0];
+    } else {
+      s = 2;
+      t -= ntl[0] + ntl[1];
+    }
+    n0 = t * BK;
+  };
+
+  auto run = [&](auto TAIL_) {
+    constexpr bool TAIL = decltype(TAIL_)::value;
+    auto gload = [&](auto S_, int t) {
+      constexpr int st = decltype(S_)::value;
+      int s, n0;
+      locate(t, s, n0);
+      const TnSeg& sg = a.seg[s];
+      const rsrc_t ra_ = s == 0 ? rA[0] : s == 1 ? rA[1] : rA[2];
+      const rsrc_t rb_ = s == 0 ? rB[0] : s == 1 ? rB[1] : rB[2];
+      const rsrc_t rs_ = s == 0 ? rS[0] : s == 1 ? rS[1] : rS[2];
+      cur_n0[st] = n0;
+      cur_N[st] = sg.N;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int c = tid + NTH * i;
+        ra[st][i] = bload128(ra_, (uint32_t)(((c >> 3) * sg.ldg + (c & 7) * 8 + n0) * 2));
+      }
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        rw[st][i] = bload64(rb_, offB + (uint32_t)((n0 + i) * Kh));
+        rsc[st][i] = bload16(rs_, offS + (uint32_t)((n0 + i) * kgroups * 2));
+      }
+      if constexpr (TAIL) {
+        if (n0 + BK > sg.N) {  // reduction tail: A columns past N must be 0 (B rows already are)
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            if (n0 + ((tid + NTH * i) & 7) * 8 >= sg.N) ra[st][i] = make_uint4(0, 0, 0, 0);
+        }
+      }
+    };
+    auto sstore = [&](auto S_, auto B_) {
+      constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
+      if constexpr (AMODE == TN_A_SOFTMAX) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int c = tid + NTH * i;
+          uint4 p = make_uint4(0, 0, 0, 0);
+          // chunks past the reduction length were zero-filled; they must stay 0, not exp(-lse)
+          if (rval[i] && cur_n0[st] + (c & 7) * 8 < cur_N[st]) {
+            const uint32_t* h = (const uint32_t*)&ra[st][i];
+            uint32_t o[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              o[j] = pack_bf16x2(__expf(f16_lo(h[j]) - rlse[i]), __expf(f16_hi(h[j]) - rlse[i]));
+            p = make_uint4(o[0], o[1], o[2], o[3]);
+          }
+          *(uint4*)(As2[bf] + (c >> 3) * LDT + (c & 7) * 8) = p;
+        }
+      } else {
+        store_a_tile(As2[bf], tid, ra[st]);
+      }
+      float v[RPT][16];
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        const float sc = half_bits_to_f32((uint16_t)rsc[st][i]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          v[i][e] = (float)nib_s(rw[st][i].x, e) * sc;
+          v[i][8 + e] = (float)nib_s(rw[st][i].y, e) * sc;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        u16* dst = Bs2[bf] + (16 * cq + e) * LDT + RPT * rq;
+        if constexpr (RPT == 4)
+          *(uint2*)dst = make_uint2(pack_bf16x2(v[0][e], v[1][e]), pack_bf16x2(v[2][e], v[3][e]));
+        else
+          *(uint32_t*)dst = pack_bf16x2(v[0][e], v[1][e]);
+      }
+    };
+    auto step = [&](auto I_, int t) {
+      constexpr int I = decltype(I_)::value;
+      gload(IC<I>{}, min(t + 2, t_end - 1));
+      mma_tile<OpBF16, NJ>(As2[I], Bs2[I], wm, wn, lane, acc);
+      sstore(IC<1 - I>{}, IC<1 - I>{});
+      __syncthreads();
+    };
+    gload(IC<0>{}, t_begin);
+    gload(IC<1>{}, min(t_begin + 1, t_end - 1));
+    sstore(IC<0>{}, IC<0>{});
+    __syncthreads();
+    int t = t_begin;
+    for (; t + 2 <= t_end; t += 2) {
+      step(IC<0>{}, t);
+      step(IC<1>{}, t + 1);
+    }
+    if (t < t_end) step(IC<0>{}, t);
+  };
+  if (t_begin < t_end) {
+    bool tail = false;
+    for (int s = 0; s < a.nseg; ++s) tail |= (a.seg[s].N % BK) != 0;
+    if (tail)
+      run(IC<1>{});
+    else
+      run(IC<0>{});
+  }
+
+  if constexpr (EPI == TN_PARTIAL_F32) {
+    store_partial<NJ>(acc, a.out + (size_t)z * a.M * a.ldo, a.M, a.ldo, Kout - c0, m0, c0, wm, wn, lane);
+    return;
+  } else {
+    if (S > 1) {
+      store_partial<NJ>(acc, a.part + (size_t)z * a.M * Kout, a.M, Kout, Kout - c0, m0, c0, wm, wn, lane);
+      return;
+    }
+    for (int s = 0; s < a.nseg; ++s) {
+      const TnSeg& sg = a.seg[s];
+      if (sg.lora_A)
+        lora_mfma<NJ>(acc, sg.lora_du, a.r, m0 + wm * 128, a.M, 1.0f, sg.lora_A, 1, Kout, c0 + wn * 32 * NJ, Kout,
+                      lane);
+    }
+    auto put = [&](auto FULL_) {
+      constexpr bool FULL = decltype(FULL_)::value;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int m = m0 + acc_row(wm, i, q, lane);
+        if (!FULL && m >= a.M) continue;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int c = c0 + acc_col<NJ>(wn, j, lane);
+          if (!FULL && c >= Kout) continue;
+          const float v = acc[i][j][q];
+          if constexpr (EPI == TN_STORE_F32) {
+            a.out[(size_t)m * a.ldo + c] = v;
+          } else if constexpr (EPI == TN_STORE_BF16) {
+            a.outb[(size_t)m * a.ldo + c] = (bf16)v;
+          } else {  // TN_ACT_BWD: v = dz; g, u (fp16) -> dg, du (bf16) in place
+            const size_t idx = (size_t)m * a.ldgu + c;
+            const float g = (float)((const f16*)a.g)[idx], u = (float)((const f16*)a.u)[idx];
+            ((bf16*)a.g)[idx] = (bf16)(v * u * act_grad_f(g, a.act));
+            ((bf16*)a.u)[idx] = (bf16)(v * act_f(g, a.act));
+          }
+        }
+      }
+    };
+    if (m0 + BM <= a.M && c0 + BN <= Kout)
+      put(IC<1>{});
+    else
+      put(IC<0>{});
+  }
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------ planning
+static int env_big() {
+  static const int v = [] {
+    const char* e = getenv("MEBP_BIG_TILES");
+    return e && *e ? atoi(e) : 1;
+  }();
+  return v;
+}
+
+GemmPlan plan_big(int M, int ntiles256, int ntiles128, int ktiles, bool logits, int max_bn) {
+  GemmPlan p{0, 0, 1};
+  if (!env_big() || M < 1024) return p;
+  const int mt = (M + BM - 1) / BM;
+  p.big = 1;
+  if (max_bn >= 256 && (logits || mt * ntiles256 >= 192)) {
+    p.bn = 256;
+    return p;
+  }
+  p.bn = 128;
+  if (logits) return p;
+  const int t = mt * ntiles128;
+  if (t >= 160) return p;
+  int s = (256 + t - 1) / t;
+  const int max_s = ktiles / 4;
+  if (s > max_s) s = max_s;
+  if (s > 8) s = 8;
+  p.splits = s < 1 ? 1 : s;
+  return p;
+}
+
+hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double flops, double bytes, hipStream_t st) {
+  int tiles = 0;
+  for (int s = 0; s < a.nseg; ++s) tiles += (a.seg[s].N + bn - 1) / bn;
+  const dim3 grid(tiles, (a.M + BM - 1) / BM, S);
+  NtArgs b = a;
+  int t = 0;
+  for (int s = 0; s < b.nseg; ++s) {
+    b.seg[s].tile0 = t;
+    t += (b.seg[s].N + bn - 1) / bn;
+  }
+  const char* name = epi == NT_STORE_F16 ? "gemm_nt_f16out" : epi == NT_STORE_F32 ? "gemm_nt_f32out" : "gemm_nt_logits";
+#define NT_BIG(BN_, EPI_)                                                                                 \
+  MEBP_TIMED(st, name, flops, bytes,                                                                      \
+             hipLaunchKernelGGL((k_gemm_nt_big<BN_, BN_ / 64, EPI_>), grid, dim3(2 * BN_), 0, st, b))
+  if (bn == 256) {
+    if (epi == NT_LOGITS)
+      NT_BIG(256, NT_LOGITS);
+    else if (epi == NT_STORE_F16)
+      NT_BIG(256, NT_STORE_F16);
+    else
+      NT_BIG(256, NT_STORE_F32);
+  } else if (bn == 128) {
+    if (epi == NT_LOGITS)
+      NT_BIG(128, NT_LOGITS);
+    else if (epi == NT_STORE_F16)
+      NT_BIG(128, NT_STORE_F16);
+    else
+      NT_BIG(128, NT_STORE_F32);
+  } else {
+    return hipErrorInvalidValue;
+  }
+#undef NT_BIG
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S, double flops, double bytes,
+                              hipStream_t st) {
+  const dim3 grid((a.Kout + bn - 1) / bn, (a.M + BM - 1) / BM, S);
+  const char* name = amode == TN_A_SOFTMAX ? "gemm_tn_softmax_dh"
+                     : epi == TN_STORE_F32  ? "gemm_tn_f32out"
+                     : epi == TN_ACT_BWD    ? "gemm_tn_act_bwd"
+                                            : "gemm_tn_bf16out";
+#define TN_BIG(BN_, EPI_, AM_) \
+  MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_big<BN_, EPI_, AM_>), grid, dim3(NTH), 0, st, a))
+#define TN_BIG_EPI(BN_)                                              \
+  do {                                                               \
+    if (amode == TN_A_SOFTMAX) {                                     \
+      if (epi != TN_PARTIAL_F32) return hipErrorInvalidValue;        \
+      TN_BIG(BN_, TN_PARTIAL_F32, TN_A_SOFTMAX);                     \
+    } else if (epi == TN_STORE_F32) {                                \
+      TN_BIG(BN_, TN_STORE_F32, TN_A_BF16);                          \
+    } else if (epi == TN_ACT_BWD) {                                  \
+      TN_BIG(BN_, TN_ACT_BWD, TN_A_BF16);                            \
+    } else if (epi == TN_STORE_BF16) {                               \
+      TN_BIG(BN_, TN_STORE_BF16, TN_A_BF16);                         \
+    } else {                                                         \
+      return hipErrorInvalidValue;                                   \
+    }                                                                \
+  } while (0)
+  // the transposed weight tile goes through LDS; 256-wide tiles would need more than the
+  // 512 registers a lane has next to 256 accumulators
+  if (bn != 128) return hipErrorInvalidValue;
+  TN_BIG_EPI(128);
+#undef TN_BIG_EPI
+#undef TN_BIG
+  return hipGetLastError();
+}
+
+}  // namespace mebp

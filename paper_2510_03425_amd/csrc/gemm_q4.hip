@@ -34,22 +34,6 @@ constexpr int BM = 128, BN = 128, BK = 64, LDT = BK + 8;  // LDS pitch in 16-bit
 constexpr int NTHREADS = 256;
 typedef uint16_t u16;
 
-// Raw buffer resources: loads through them return 0 past `bytes` (no per-element bounds
-// branches), and offsets are 32-bit VGPR values. Every resource is based at the first row
-// a workgroup touches, so a region stays far below 4 GiB.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-DEV rsrc_t make_rsrc(const void* base, size_t bytes) {
-  const uint32_t n = bytes > 0xffffffffull ? 0xffffffffu : (uint32_t)bytes;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
-}
-DEV uint4 bload128(rsrc_t r, uint32_t off) {
-  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
-DEV uint32_t bload32(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0); }
-DEV uint32_t bload16(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0); }
-
 template <class Op>
 DEV void mma_tile(const u16* As, const u16* Bs, int wm, int wn, int lane, f32x4 (&acc)[4][4]) {
 #pragma unroll
@@ -861,6 +845,32 @@ int gemm_splits(int tiles, int ktiles) {
 
 size_t gemm_part_floats(int M, int ncols, int splits) { return splits > 1 ? (size_t)splits * M * ncols : 0; }
 
+GemmPlan plan_nt(int M, const int* Ns, int nseg, int K, int epi) {
+  int t256 = 0, t128 = 0;
+  for (int s = 0; s < nseg; ++s) {
+    t256 += (Ns[s] + 255) / 256;
+    t128 += (Ns[s] + 127) / 128;
+  }
+  const int nk = (K + BK - 1) / BK;
+  GemmPlan p = plan_big(M, t256, t128, nk, epi == NT_LOGITS, env_int("MEBP_NT_MAX_BN", 256));
+  if (!p.big) p.splits = epi == NT_LOGITS ? 1 : gemm_splits(t128 * ((M + BM - 1) / BM), nk);
+  return p;
+}
+
+int gemm_logit_stat_tiles(int M, int V, int K) {
+  // the large-tile kernels give every wave 64 columns, the 128 x 128 kernel 128 per tile
+  const GemmPlan p = plan_nt(M, &V, 1, K, NT_LOGITS);
+  return p.big ? (V + 63) / 64 : (V + BN - 1) / BN;
+}
+
+GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg) {
+  int kt = 0;
+  for (int s = 0; s < nseg; ++s) kt += (Ns[s] + BK - 1) / BK;
+  GemmPlan p = plan_big(M, (Kout + 255) / 256, (Kout + 127) / 128, kt, false, 128);
+  if (!p.big) p.splits = gemm_splits(((Kout + BN - 1) / BN) * ((M + BM - 1) / BM), kt);
+  return p;
+}
+
 hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
   NtArgs a = a0;
   int tiles = 0, ncat = 0, items = 0;
@@ -879,12 +889,18 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
     if (a.seg[s].resid) bytes += (double)a.M * n * 4;
   }
   const int mt = (a.M + BM - 1) / BM;
-  int S = epi == NT_LOGITS ? 1 : gemm_splits(tiles * mt, (a.K + BK - 1) / BK);
+  int Ns[3];
+  for (int s = 0; s < a.nseg; ++s) Ns[s] = a.seg[s].N;
+  const GemmPlan plan = plan_nt(a.M, Ns, a.nseg, a.K, epi);
+  int S = plan.splits;
   if (S > 1 && (!a.part || a.part_floats < gemm_part_floats(a.M, ncat, S))) S = 1;
-  if (a.norm_w && a.seg[0].N > 4096) S = 1;  // the fused row norm keeps a row in one wave
+  if (a.norm_w && a.seg[0].N > 4096) S = 1;  // the fused row norm keeps a row in one workgroup
   a.ldp = ncat;
   dim3 grid(tiles, mt, S);
-  switch (epi) {
+  if (plan.big) {
+    hipError_t eb = launch_gemm_nt_big(a, epi, plan.bn, S, flops, bytes, st);
+    if (eb != hipSuccess) return eb;
+  } else switch (epi) {
     case NT_STORE_F16:
       MEBP_TIMED(st, "gemm_nt_f16out", flops, bytes,
                  hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F16>, grid, dim3(NTHREADS), 0, st, a));
@@ -939,20 +955,21 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
 hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) {
   TnArgs a = a0;
   const int ct = (a.Kout + BN - 1) / BN, mt = (a.M + BM - 1) / BM;
-  int ktiles = 0;
   double flops = 0, bytes = 0;
   const int kg = (a.Kout + 31) / 32;
   for (int s = 0; s < a.nseg; ++s) {
     const double n = a.seg[s].N;
-    ktiles += (a.seg[s].N + BK - 1) / BK;
     flops += 2.0 * a.M * n * a.Kout;
     bytes += (double)a.M * n * 2 + n * (a.Kout / 2 + 2 * kg);
   }
+  int Ns[3];
+  for (int s = 0; s < a.nseg; ++s) Ns[s] = a.seg[s].N;
+  GemmPlan plan = plan_tn(a.M, a.Kout, Ns, a.nseg);
   int S;
   if (epi == TN_PARTIAL_F32) {
     S = a.splits;
   } else {
-    S = gemm_splits(ct * mt, ktiles);
+    S = plan.splits;
     if (S > 1 && (!a.part || a.part_floats < gemm_part_floats(a.M, a.Kout, S))) S = 1;
     if (a.out2 && a.Kout > 4096) S = 1;
   }
@@ -960,7 +977,10 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
   bytes += epi == TN_STORE_BF16 ? 2 * outb : epi == TN_ACT_BWD ? 8 * outb
          : epi == TN_PARTIAL_F32 ? 4 * outb * S : 4 * outb;
   dim3 grid(ct, mt, S);
-  if (amode == TN_A_SOFTMAX) {
+  if (plan.big) {
+    hipError_t eb = launch_gemm_tn_big(a, epi, amode, plan.bn, S, flops, bytes, st);
+    if (eb != hipSuccess) return eb;
+  } else if (amode == TN_A_SOFTMAX) {
     if (epi != TN_PARTIAL_F32) return hipErrorInvalidValue;
     MEBP_TIMED(st, "gemm_tn_softmax_dh", flops, bytes,
                hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32, TN_A_SOFTMAX>), grid, dim3(NTHREADS), 0, st, a));

@@ -67,6 +67,18 @@ int gemm_splits(int tiles, int ktiles);
 size_t gemm_part_floats(int M, int ncols, int splits);
 constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 64;
 
+// Tiling plan: big = 1 selects the 256 x bn tiles of gemm_big.hip (many tokens), else the
+// 128 x 128 tiles of gemm_q4.hip; splits = split-K factor before the scratch-capacity check.
+struct GemmPlan {
+  int big, bn, splits;
+};
+GemmPlan plan_big(int M, int ntiles256, int ntiles128, int ktiles, bool logits, int max_bn);
+GemmPlan plan_nt(int M, const int* Ns, int nseg, int K, int epi);
+GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg);
+// statistics tiles per row of the LM-head logits GEMM (the column width its waves cover)
+int gemm_logit_stat_tiles(int M, int V, int K);
+hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double flops, double bytes, hipStream_t st);
+
 // Transposed orientation (input gradients): C[m][c] = sum_seg sum_n G_seg[m][n] * W_seg[n][c]
 // with W_seg int4 [N_seg][Kout/2]; reduction over the weight's output dim; G bf16 (bf16
 // MFMA operands).
@@ -113,6 +125,8 @@ struct TnArgs {
   float eps;
 };
 hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st);
+hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S, double flops, double bytes,
+                              hipStream_t st);
 
 // ---------------------------------------------------------------- elementwise / norms
 hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, int cols, int group,
