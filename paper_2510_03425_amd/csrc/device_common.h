@@ -126,18 +126,22 @@ DEV uint32_t perm_hi16(uint32_t a, uint32_t b) {  // (a.hi, b.hi) -> lo=a.hi, hi
   return __builtin_amdgcn_perm(b, a, 0x07060302u);
 }
 
-DEV float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+// tanh(x) = 1 - 2 / (exp(2x) + 1) with the hardware exp and reciprocal (absolute error
+// around 1e-7, saturating to +-1 for large |x|)
+DEV float tanh_fast(float x) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * x) + 1.0f); }
+DEV float sigmoid_fast(float x) { return __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
+DEV float silu_f(float g) { return g * sigmoid_fast(g); }
 DEV float gelu_tanh_f(float g) {
   const float c = 0.7978845608028654f;
-  return 0.5f * g * (1.0f + tanhf(c * (g + 0.044715f * g * g * g)));
+  return 0.5f * g * (1.0f + tanh_fast(c * (g + 0.044715f * g * g * g)));
 }
 DEV float act_f(float g, int kind) { return kind == 0 ? silu_f(g) : gelu_tanh_f(g); }
 DEV float act_grad_f(float g, int kind) {
   if (kind == 0) {
-    float s = 1.0f / (1.0f + __expf(-g));
+    const float s = sigmoid_fast(g);
     return s * (1.0f + g * (1.0f - s));
   }
   const float c = 0.7978845608028654f;
-  float t = tanhf(c * (g + 0.044715f * g * g * g));
+  const float t = tanh_fast(c * (g + 0.044715f * g * g * g));
   return 0.5f * (1.0f + t) + 0.5f * g * (1.0f - t * t) * c * (1.0f + 3.0f * 0.044715f * g * g);
 }
