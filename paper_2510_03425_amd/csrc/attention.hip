@@ -20,6 +20,8 @@
 //            are summed by the group's last workgroup, in head order); dQ kernel owns a
 //            query block. RoPE backward (rotation by minus the
 //            angle) is applied in both epilogues before the bf16 store.
+#include <stdlib.h>
+
 #include "device_common.h"
 #include "mebp_internal.h"
 
@@ -183,6 +185,177 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
                                        pack_f16x2(oacc[t][2] * inv, oacc[t][3] * inv));
     }
     if ((lane >> 4) == 0) a.lse[((size_t)b * a.Hq + h) * T + q] = (m_i + log2f(l_i)) / LOG2E;
+  }
+}
+
+// ------------------------------------------------------------- forward, 32-query waves
+// For longer sequences: every wave owns 32 queries and uses v_mfma_f32_32x32x16_f16, so
+// each K / V^T fragment read from LDS feeds twice the MACs of the 16-query kernel above.
+// S^T = K Q^T puts one query per lane column (keys 8(r/4)+4h+r%4 of a 32-key tile in lane
+// register r, h = lane/32), so the row statistics need one cross-lane exchange (lane^32)
+// and O^T's rescaling is lane-local. P^T enters O^T += V^T P^T straight from registers as
+// the B operand: registers 0..7 (then 8..15) of an S^T tile are the keys
+// {4h..4h+3, 8+4h..8+4h+3} of a 16-key step, and the V^T fragment is read with the same
+// key order (two 8-byte LDS reads). The next K / V block is loaded into registers while
+// the current one is multiplied.
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+DEV f32x16 mfma32_f16(uint4 a, uint4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+template <int DH, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
+  constexpr int NTH = 64 * NW, KB = 64, LDK = DH + 8, LDV = KB + 8;
+  constexpr int NKS = DH / 16, NTO = DH / 32;
+  constexpr int KCH = KB * DH / 8 / NTH;                // K chunks (8 halves) per thread
+  constexpr int NVB = (KB / 8) * (DH / 8);               // 8x8 blocks of the V tile
+  constexpr int VBL = (NVB + NTH - 1) / NTH;             // per thread (threads past NVB idle)
+  static_assert(KCH >= 1 && KB * DH / 8 % NTH == 0, "K tile does not divide over the threads");
+  __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDK];
+  __shared__ __attribute__((aligned(16))) u16 Vt[DH * LDV];
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), hl = lane >> 5;
+  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
+  const int q0 = blockIdx.x * (32 * NW), qw = q0 + 32 * w, q = qw + (lane & 31);
+  const float sc = LOG2E / sqrtf((float)DH);
+  const size_t rowb = (size_t)b * T;
+
+  uint4 qf[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks)
+    qf[ks] = load_frag_global(a.q + (rowb + q) * a.ldq + h * DH + 16 * ks + 8 * hl, q < T);
+  f32x16 oacc[NTO];
+#pragma unroll
+  for (int t = 0; t < NTO; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[t][r] = 0.f;
+  float m_i = -1e30f, l_i = 0.f;
+
+  int kv_lo = 0;
+  if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
+  const int kv_hi = min(T, q0 + 32 * NW);
+  // wave's own visible key range (for skipping fully masked blocks)
+  const int w_lo = a.window ? max(0, qw - a.window + 1) : 0, w_hi = min(T, qw + 32) - 1;
+
+  uint4 kr[KCH], vr[VBL][8];
+  auto gload = [&](int kv0) {
+    const u16* kb = (const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH;
+    const u16* vb = (const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH;
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + NTH * i, r = c / (DH / 8), col = (c % (DH / 8)) * 8;
+      kr[i] = load_frag_global(kb + (size_t)r * a.ldk + col, kv0 + r < T);
+    }
+#pragma unroll
+    for (int i = 0; i < VBL; ++i) {
+      const int bl = tid + NTH * i, rb = bl % (KB / 8), cb = bl / (KB / 8);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int r = rb * 8 + j;
+        vr[i][j] = load_frag_global(vb + (size_t)r * a.ldk + cb * 8, bl < NVB && kv0 + r < T);
+      }
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + NTH * i, r = c / (DH / 8), col = (c % (DH / 8)) * 8;
+      *(uint4*)(Ks + r * LDK + col) = kr[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VBL; ++i) {
+      const int bl = tid + NTH * i, rb = bl % (KB / 8), cb = bl / (KB / 8);
+      if (bl >= NVB) continue;
+      const uint32_t* in = (const uint32_t*)vr[i];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int d = j >> 1;
+        uint4 o;
+        if (j & 1) {
+          o.x = perm_hi16(in[0 * 4 + d], in[1 * 4 + d]);
+          o.y = perm_hi16(in[2 * 4 + d], in[3 * 4 + d]);
+          o.z = perm_hi16(in[4 * 4 + d], in[5 * 4 + d]);
+          o.w = perm_hi16(in[6 * 4 + d], in[7 * 4 + d]);
+        } else {
+          o.x = perm_lo16(in[0 * 4 + d], in[1 * 4 + d]);
+          o.y = perm_lo16(in[2 * 4 + d], in[3 * 4 + d]);
+          o.z = perm_lo16(in[4 * 4 + d], in[5 * 4 + d]);
+          o.w = perm_lo16(in[6 * 4 + d], in[7 * 4 + d]);
+        }
+        *(uint4*)(Vt + (cb * 8 + j) * LDV + rb * 8) = o;
+      }
+    }
+  };
+
+  if (kv_lo < kv_hi) gload(kv_lo);
+  for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += KB) {
+    __syncthreads();  // every wave is done with the previous block's tiles
+    sstore();
+    __syncthreads();
+    if (kv0 + KB < kv_hi) gload(kv0 + KB);  // next block in flight during this one
+    if (kv0 > w_hi || kv0 + KB - 1 < w_lo) continue;  // nothing visible for this wave
+    f32x16 s[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kt][r] = 0.f;
+      const u16* kp = Ks + (kt * 32 + (lane & 31)) * LDK + 8 * hl;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) s[kt] = mfma32_f16(*(const uint4*)(kp + 16 * ks), qf[ks], s[kt]);
+    }
+    float mloc = -1e30f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kv0 + kt * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+        const bool vis = key <= q && key < T && (a.window == 0 || q - key < a.window);
+        const float v = vis ? s[kt][r] * sc : -INFINITY;
+        s[kt][r] = v;
+        mloc = fmaxf(mloc, v);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m_i, mloc);
+    const float alpha = exp2f(m_i - m_new);
+    float ls = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(s[kt][r] - m_new);
+        s[kt][r] = p;
+        ls += p;
+      }
+    ls += __shfl_xor(ls, 32, 64);
+    l_i = l_i * alpha + ls;
+    m_i = m_new;
+#pragma unroll
+    for (int t = 0; t < NTO; ++t) oacc[t] *= alpha;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const f32x16& st = s[kk >> 1];
+      const int r0 = 8 * (kk & 1);
+      const uint4 pf = make_uint4(pack_f16x2(st[r0 + 0], st[r0 + 1]), pack_f16x2(st[r0 + 2], st[r0 + 3]),
+                                  pack_f16x2(st[r0 + 4], st[r0 + 5]), pack_f16x2(st[r0 + 6], st[r0 + 7]));
+#pragma unroll
+      for (int t = 0; t < NTO; ++t) {
+        const u16* vp = Vt + (t * 32 + (lane & 31)) * LDV + kk * 16 + 4 * hl;
+        const uint2 x0 = *(const uint2*)vp, x1 = *(const uint2*)(vp + 8);
+        oacc[t] = mfma32_f16(make_uint4(x0.x, x0.y, x1.x, x1.y), pf, oacc[t]);
+      }
+    }
+  }
+  if (q < T) {
+    const float inv = 1.0f / l_i;
+    f16* orow = a.o + (rowb + q) * a.ldq + h * DH;
+#pragma unroll
+    for (int t = 0; t < NTO; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int e = t * 32 + 8 * g + 4 * hl;
+        *(uint2*)(orow + e) = make_uint2(pack_f16x2(oacc[t][4 * g] * inv, oacc[t][4 * g + 1] * inv),
+                                         pack_f16x2(oacc[t][4 * g + 2] * inv, oacc[t][4 * g + 3] * inv));
+      }
+    if (hl == 0) a.lse[((size_t)b * a.Hq + h) * T + q] = (m_i + log2f(l_i)) / LOG2E;
   }
 }
 
@@ -469,6 +642,25 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st) {
   const double pairs = visible_pairs(a.T, a.window) * a.Hq * a.B;
   const double flops = 4.0 * a.dh * pairs;
   const double bytes = (double)a.B * a.T * (2.0 * a.Hq * a.dh * 2 + 2.0 * a.Hkv * a.dh * 2 + a.Hq * 4);
+  static const int use32 = [] {
+    const char* e = getenv("MEBP_ATTN32");
+    return e && *e ? atoi(e) : 1;
+  }();
+  const size_t wg128 = (size_t)((a.T + 127) / 128) * a.Hq * a.B;
+  if (use32 && wg128 >= 256) {
+    // 128 queries per workgroup (4 waves of 32) when that still fills the chip
+    const dim3 g2((a.T + 127) / 128, a.Hq, a.B);
+#define FWD32(D) \
+  MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL((k_attn_fwd32<D, 4>), g2, dim3(256), 0, st, a))
+    switch (a.dh) {
+      case 64: FWD32(64); break;
+      case 128: FWD32(128); break;
+      case 256: FWD32(256); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef FWD32
+    return hipGetLastError();
+  }
   switch (a.dh) {
     case 64: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<64>, grid, dim3(256), 0, st, a)); break;
     case 128: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<128>, grid, dim3(256), 0, st, a)); break;
