@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <map>
+#include <mutex>
 #include <string>
 
 #include "../../include/mebp.h"
@@ -46,8 +48,22 @@ const char* kSlotNames[S_COUNT] = {
   "dh_bf16", "do", "delta", "dq", "dk", "dv", "da", "lora_part", "rope_global", "rope_local", "targets",
   "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part"};
 
+// Slots written by a layer's (re)computed forward and read by its backward, plus the
+// split-K scratch: the training step keeps two copies, so that the recompute of layer l-1
+// (on the side stream) can run while layer l is backpropagated.
+bool per_set(int s) {
+  switch (s) {
+    case S_A: case S_Q: case S_K: case S_V: case S_O: case S_LSE: case S_H: case S_C: case S_G: case S_U:
+    case S_Z: case S_LU: case S_SPLIT:
+      return true;
+    default:
+      return false;
+  }
+}
+
 struct Layout {
   size_t off[S_COUNT];
+  size_t off1[S_COUNT];  // second copy of the per-set slots (equal to off[] for the others)
   size_t total;
   int lm_splits;
   int ntiles;
@@ -142,6 +158,12 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   size_t o = 0;
   for (int i = 0; i < S_COUNT; ++i) {
     L->off[i] = o;
+    o += (sz[i] + 255) & ~(size_t)255;
+  }
+  for (int i = 0; i < S_COUNT; ++i) {
+    L->off1[i] = L->off[i];
+    if (!per_set(i)) continue;
+    L->off1[i] = o;
     o += (sz[i] + 255) & ~(size_t)255;
   }
   L->total = o;
@@ -264,17 +286,26 @@ struct Ctx {
   void* ws;
   Layout L;
   hipStream_t st;
+  int set;        // copy of the per-layer activation slots (0 or 1)
+  int split_set;  // copy of the split-K scratch (0 or 1)
 };
+
+// The workspace slot `s` as seen by this context (its activation set and scratch copy).
+template <class Tp>
+Tp* xs(const Ctx& x, int s) {
+  const int which = s == S_SPLIT ? x.split_set : x.set;
+  return (Tp*)((char*)x.ws + (which ? x.L.off1[s] : x.L.off[s]));
+}
 
 SplitScratch scratch(const Ctx& x) {
   SplitScratch sc;
-  sc.part = slot<float>(x.ws, x.L, S_SPLIT);
+  sc.part = xs<float>(x, S_SPLIT);
   sc.part_floats = x.L.split_floats;
   return sc;
 }
 
-float* lu(const Ctx& x, int p) { return slot<float>(x.ws, x.L, S_LU) + (size_t)p * x.D.N * x.D.r; }
-float* ldu(const Ctx& x, int p) { return slot<float>(x.ws, x.L, S_LDU) + (size_t)p * x.D.N * x.D.r; }
+float* lu(const Ctx& x, int p) { return xs<float>(x, S_LU) + (size_t)p * x.D.N * x.D.r; }
+float* ldu(const Ctx& x, int p) { return xs<float>(x, S_LDU) + (size_t)p * x.D.N * x.D.r; }
 bool adapted(const Ctx& x, int p) { return (x.c->lora_mask >> p) & 1; }
 
 NtSeg nt_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* lora, int p, void* out, int ldo,
@@ -383,16 +414,16 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
                   float* x_out, const float* rope, bool keep) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
-  f16* a = slot<f16>(x.ws, x.L, S_A);
-  f16* q = slot<f16>(x.ws, x.L, S_Q);
-  f16* k = slot<f16>(x.ws, x.L, S_K);
-  f16* v = slot<f16>(x.ws, x.L, S_V);
-  f16* o = slot<f16>(x.ws, x.L, S_O);
-  float* h = slot<float>(x.ws, x.L, S_H);
-  f16* cc = slot<f16>(x.ws, x.L, S_C);
-  f16* g = slot<f16>(x.ws, x.L, S_G);
-  f16* u = slot<f16>(x.ws, x.L, S_U);
-  f16* z = slot<f16>(x.ws, x.L, S_Z);
+  f16* a = xs<f16>(x, S_A);
+  f16* q = xs<f16>(x, S_Q);
+  f16* k = xs<f16>(x, S_K);
+  f16* v = xs<f16>(x, S_V);
+  f16* o = xs<f16>(x, S_O);
+  float* h = xs<float>(x, S_H);
+  f16* cc = xs<f16>(x, S_C);
+  f16* g = xs<f16>(x, S_G);
+  f16* u = xs<f16>(x, S_U);
+  f16* z = xs<f16>(x, S_Z);
 
   HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
   HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}));
@@ -410,7 +441,7 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   at.q = q; at.k = k; at.v = v; at.ldq = D.qd; at.ldk = D.kvd;
   at.B = x.B; at.T = x.T; at.Hq = c->n_heads; at.Hkv = c->n_kv_heads; at.dh = c->head_dim;
   at.window = is_global(c, l) ? 0 : c->window;
-  at.o = o; at.lse = slot<float>(x.ws, x.L, S_LSE);
+  at.o = o; at.lse = xs<float>(x, S_LSE);
   HIP_TRY(launch_attn_fwd(at, x.st));
   HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}));
   {
@@ -440,32 +471,32 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
 // dy_bf16_ready: the workspace's dy_bf16 slot already holds bf16(dy) (written by the
 // block above in the same training step). On return the slot holds bf16(dx) when dx is
 // computed.
-int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora,
-                   const float* x_ckpt, const float* dy, float* dx, const mebp_layer_lora_grad* grads,
-                   const float* rope, bool dy_bf16_ready = false) {
+// The backward of one layer from the intermediates of its recomputed forward (already in
+// the context's activation set).
+int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora,
+                        const float* x_ckpt, const float* dy, float* dx, const mebp_layer_lora_grad* grads,
+                        const float* rope, bool dy_bf16_ready) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
-  int e = layer_forward(x, l, base, lora, x_ckpt, nullptr, rope, true);
-  if (e) return e;
-  f16* a = slot<f16>(x.ws, x.L, S_A);
-  f16* q = slot<f16>(x.ws, x.L, S_Q);
-  f16* k = slot<f16>(x.ws, x.L, S_K);
-  f16* v = slot<f16>(x.ws, x.L, S_V);
-  f16* o = slot<f16>(x.ws, x.L, S_O);
-  float* h = slot<float>(x.ws, x.L, S_H);
-  f16* cc = slot<f16>(x.ws, x.L, S_C);
-  f16* g = slot<f16>(x.ws, x.L, S_G);
-  f16* u = slot<f16>(x.ws, x.L, S_U);
-  f16* z = slot<f16>(x.ws, x.L, S_Z);
-  bf16* dyb = slot<bf16>(x.ws, x.L, S_DYB);
-  float* dc = slot<float>(x.ws, x.L, S_DC);
-  float* dh = slot<float>(x.ws, x.L, S_DH);
-  bf16* dhb = slot<bf16>(x.ws, x.L, S_DHB);
-  bf16* dO = slot<bf16>(x.ws, x.L, S_DO);
-  bf16* dq = slot<bf16>(x.ws, x.L, S_DQ);
-  bf16* dk = slot<bf16>(x.ws, x.L, S_DK);
-  bf16* dv = slot<bf16>(x.ws, x.L, S_DV);
-  float* da = slot<float>(x.ws, x.L, S_DA);
+  f16* a = xs<f16>(x, S_A);
+  f16* q = xs<f16>(x, S_Q);
+  f16* k = xs<f16>(x, S_K);
+  f16* v = xs<f16>(x, S_V);
+  f16* o = xs<f16>(x, S_O);
+  float* h = xs<float>(x, S_H);
+  f16* cc = xs<f16>(x, S_C);
+  f16* g = xs<f16>(x, S_G);
+  f16* u = xs<f16>(x, S_U);
+  f16* z = xs<f16>(x, S_Z);
+  bf16* dyb = xs<bf16>(x, S_DYB);
+  float* dc = xs<float>(x, S_DC);
+  float* dh = xs<float>(x, S_DH);
+  bf16* dhb = xs<bf16>(x, S_DHB);
+  bf16* dO = xs<bf16>(x, S_DO);
+  bf16* dq = xs<bf16>(x, S_DQ);
+  bf16* dk = xs<bf16>(x, S_DK);
+  bf16* dv = xs<bf16>(x, S_DV);
+  float* da = xs<float>(x, S_DA);
 
   // y = h + down(z)
   if (!dy_bf16_ready) HIP_TRY(launch_f32_to_bf16(dy, dyb, (size_t)D.N * D.d, x.st));
@@ -509,9 +540,9 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
     at.q = q; at.k = k; at.v = v; at.ldq = D.qd; at.ldk = D.kvd;
     at.B = x.B; at.T = x.T; at.Hq = c->n_heads; at.Hkv = c->n_kv_heads; at.dh = c->head_dim;
     at.window = is_global(c, l) ? 0 : c->window;
-    at.o = o; at.lse = slot<float>(x.ws, x.L, S_LSE);
+    at.o = o; at.lse = xs<float>(x, S_LSE);
     at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
-    HIP_TRY(launch_attn_bwd(at, slot<float>(x.ws, x.L, S_DELTA), scratch(x), x.st));
+    HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), scratch(x), x.st));
   }
   HIP_TRY(lora_bwd(x, lora, grads, {MEBP_Q, MEBP_K, MEBP_V}, {dq, dk, dv}, a));
   if (dx) {
@@ -529,20 +560,29 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   return MEBP_OK;
 }
 
+// Recompute (Algorithm 1's second loop: forward from the checkpoint) then backward.
+int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora,
+                   const float* x_ckpt, const float* dy, float* dx, const mebp_layer_lora_grad* grads,
+                   const float* rope, bool dy_bf16_ready = false) {
+  const int e = layer_forward(x, l, base, lora, x_ckpt, nullptr, rope, true);
+  if (e) return e;
+  return layer_backward_only(x, l, base, lora, x_ckpt, dy, dx, grads, rope, dy_bf16_ready);
+}
+
 int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const float* x_last, const int32_t* ids,
             float* loss, float* dx_last) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
   const int V = c->vocab;
-  int32_t* tgt = slot<int32_t>(x.ws, x.L, S_TGT);
-  f16* hf = slot<f16>(x.ws, x.L, S_HF);
-  _Float16* logits = slot<_Float16>(x.ws, x.L, S_LOGITS);
-  float2* stats = slot<float2>(x.ws, x.L, S_STATS);
-  float* lse = slot<float>(x.ws, x.L, S_LSEV);
-  float* tl = slot<float>(x.ws, x.L, S_TGTLOGIT);
-  float* rl = slot<float>(x.ws, x.L, S_ROWLOSS);
-  float* dhf = slot<float>(x.ws, x.L, S_DHF);
-  float* part = slot<float>(x.ws, x.L, S_LMPART);
+  int32_t* tgt = xs<int32_t>(x, S_TGT);
+  f16* hf = xs<f16>(x, S_HF);
+  _Float16* logits = xs<_Float16>(x, S_LOGITS);
+  float2* stats = xs<float2>(x, S_STATS);
+  float* lse = xs<float>(x, S_LSEV);
+  float* tl = xs<float>(x, S_TGTLOGIT);
+  float* rl = xs<float>(x, S_ROWLOSS);
+  float* dhf = xs<float>(x, S_DHF);
+  float* part = xs<float>(x, S_LMPART);
   const float inv_n = 1.0f / (float)((long long)x.B * (x.T - 1));
 
   HIP_TRY(launch_targets(ids, x.B, x.T, c->vocab, tgt, x.st));
@@ -569,7 +609,7 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
   }
   HIP_TRY(launch_ce_dh_reduce(part, x.L.lm_splits, D.N, D.d, emb->q4, emb->scale, tgt, inv_n, dhf, x.st));
   HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, D.N, D.d, c->rms_eps, dx_last,
-                             slot<bf16>(x.ws, x.L, S_DYB), x.st));
+                             xs<bf16>(x, S_DYB), x.st));
   return MEBP_OK;
 }
 
@@ -582,15 +622,51 @@ Ctx make_ctx(const mebp_config* c, int B, int T, void* ws, mebp_stream_t stream)
   x.ws = ws;
   make_layout(c, B, T, &x.L);
   x.st = (hipStream_t)stream;
+  x.set = 0;
+  x.split_set = 0;
   return x;
 }
 
 int rope_table(const Ctx& x, int l, float** out) {
   const bool glob = is_global(x.c, l);
-  float* cs = slot<float>(x.ws, x.L, glob ? S_ROPE_G : S_ROPE_L);
+  float* cs = xs<float>(x, glob ? S_ROPE_G : S_ROPE_L);
   HIP_TRY(launch_rope_table(x.T, x.c->head_dim, glob ? x.c->rope_theta_global : x.c->rope_theta_local, cs, x.st));
   *out = cs;
   return MEBP_OK;
+}
+
+// ------------------------------------------------------------------ side stream
+// The training step runs the recompute of layer l-1 on a second stream of the caller's
+// device while layer l is backpropagated on the caller's stream. The stream and its three
+// events are created on the first step on a device outside of stream capture (a step
+// captured before that runs on the caller's stream alone). Enqueueing a step holds the
+// device's lock, so concurrent host threads do not interleave on the shared events.
+struct SideStream {
+  hipStream_t st = nullptr;
+  hipEvent_t ev_fwd = nullptr, ev_rec = nullptr, ev_bwd = nullptr;
+  std::mutex mu;
+};
+
+SideStream* side_stream(hipStream_t main) {
+  static std::mutex map_mu;
+  static std::map<int, SideStream*> by_dev;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> g(map_mu);
+  auto it = by_dev.find(dev);
+  if (it != by_dev.end()) return it->second;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(main, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
+  SideStream* s = new SideStream();
+  if (hipStreamCreateWithFlags(&s->st, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&s->ev_fwd, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&s->ev_rec, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&s->ev_bwd, hipEventDisableTiming) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;  // (leaks the partial set; the step then runs on one stream)
+  }
+  by_dev[dev] = s;
+  return s;
 }
 
 }  // namespace
@@ -712,16 +788,59 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
     if ((e = layer_forward(x, l, &layers[l], &lora[l], ckpt + l * stride, ckpt + (l + 1) * stride, rope, false)))
       return e;
   }
-  // final linear + loss block
   float* g = slot<float>(ws, x.L, S_GRAD);
-  if ((e = lm_head(x, emb, norm_final, ckpt + cfg->n_layers * stride, ids, loss, g))) return e;
   // reverse loop: recompute layer l from ckpt[l], backpropagate the upstream gradient
-  for (int l = cfg->n_layers - 1; l >= 0; --l) {
+  SideStream* side = side_stream(x.st);
+  if (!side) {
+    // final linear + loss block, then the layers in reverse on the caller's stream
+    if ((e = lm_head(x, emb, norm_final, ckpt + cfg->n_layers * stride, ids, loss, g))) return e;
+    for (int l = cfg->n_layers - 1; l >= 0; --l) {
+      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+      float* dxl = l > 0 ? g : dx0;
+      if ((e = layer_backward(x, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr,
+                              rope, true)))
+        return e;
+    }
+    return MEBP_OK;
+  }
+  // Two streams: the recompute of layer l writes activation set l & 1 on the side stream
+  // (with its own split-K scratch) and may start as soon as the backward of layer l + 2,
+  // the previous user of that set, is done; the backward of layer l waits for it. The
+  // side stream's first wait is on the end of the forward loop (the checkpoints and the
+  // LM head's inputs), its last record is waited for by the caller's stream.
+  std::lock_guard<std::mutex> lock(side->mu);
+  Ctx r = x;
+  r.st = side->st;
+  r.split_set = 1;
+  auto recompute = [&](int l) -> int {
+    r.set = l & 1;
+    const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+    return layer_forward(r, l, &layers[l], &lora[l], ckpt + l * stride, nullptr, rope, true);
+  };
+  HIP_TRY(hipEventRecord(side->ev_fwd, x.st));
+  HIP_TRY(hipStreamWaitEvent(side->st, side->ev_fwd, 0));
+  // (the LM head below is enqueued after this point on the caller's stream and overlaps
+  // the first recompute)
+  const int L = cfg->n_layers;
+  if ((e = recompute(L - 1))) return e;
+  HIP_TRY(hipEventRecord(side->ev_rec, side->st));
+  if ((e = lm_head(x, emb, norm_final, ckpt + L * stride, ids, loss, g))) return e;
+  for (int l = L - 1; l >= 0; --l) {
+    HIP_TRY(hipStreamWaitEvent(x.st, side->ev_rec, 0));  // recompute(l) done
+    if (l >= 1) {
+      // set (l - 1) & 1 was last read by the backward of layer l + 1 (or the forward loop)
+      if (l + 1 < L) HIP_TRY(hipStreamWaitEvent(side->st, side->ev_bwd, 0));
+      if ((e = recompute(l - 1))) return e;
+      HIP_TRY(hipEventRecord(side->ev_rec, side->st));
+    }
+    Ctx b = x;
+    b.set = l & 1;
     const float* rope = is_global(cfg, l) ? rope_g : rope_l;
     float* dxl = l > 0 ? g : dx0;
-    if ((e = layer_backward(x, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr, rope,
-                            true)))
+    if ((e = layer_backward_only(b, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr,
+                                 rope, true)))
       return e;
+    HIP_TRY(hipEventRecord(side->ev_bwd, x.st));
   }
   return MEBP_OK;
 }
