@@ -596,16 +596,61 @@ DEV float2 block_sum2(float2 v, float2* red) {
   return make_float2(red[0].x + red[1].x + red[2].x + red[3].x, red[0].y + red[1].y + red[2].y + red[3].y);
 }
 
-// LoRA up-projection term s * u[m] . B[n] for 4 consecutive columns n..n+3
-DEV void add_lora4(float (&o)[4], const NtSeg& sg, float s, int r, int m, int n) {
-  if (!sg.lora_B) return;
-  const float* u = sg.lora_u + (size_t)m * r;
+// R consecutive fp32 values (16-byte aligned) into registers, all loads issued together
+template <int R>
+DEV void load_row(const float* p, float (&v)[R]) {
+#pragma unroll
+  for (int j = 0; j < R; j += 4) {
+    const float4 t = *(const float4*)(p + j);
+    v[j] = t.x; v[j + 1] = t.y; v[j + 2] = t.z; v[j + 3] = t.w;
+  }
+}
+
+// LoRA up-projection term s * u[m] . B[n] for 4 consecutive columns n..n+3 (rank R; the
+// dot product runs in rank order)
+template <int R>
+DEV void add_lora4_r(float (&o)[4], const float* urow, const float* B, float s, int n) {
+  float u[R], b[4][R];
+  load_row<R>(urow, u);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) load_row<R>(B + (size_t)(n + q) * R, b[q]);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const float* b = sg.lora_B + (size_t)(n + q) * r;
     float l = 0.f;
-    for (int j = 0; j < r; ++j) l += u[j] * b[j];
+#pragma unroll
+    for (int j = 0; j < R; ++j) l += u[j] * b[q][j];
     o[q] += s * l;
+  }
+}
+DEV void add_lora4(float (&o)[4], const NtSeg& sg, float s, int r, int m, int n) {
+  if (!sg.lora_B) return;
+  if (r == 8)
+    add_lora4_r<8>(o, sg.lora_u + (size_t)m * 8, sg.lora_B, s, n);
+  else
+    add_lora4_r<16>(o, sg.lora_u + (size_t)m * 16, sg.lora_B, s, n);
+}
+
+// o[0..3] += sum_j du[m][j] * A[j][c..c+3] over the adapted segments (rank R, rank order)
+template <int R>
+DEV void add_lora_dx4_r(float (&o)[4], const float* durow, const float* A, int ldA, int c) {
+  float du[R];
+  float4 av[R];
+  load_row<R>(durow, du);
+#pragma unroll
+  for (int j = 0; j < R; ++j) av[j] = *(const float4*)(A + (size_t)j * ldA + c);
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    o[0] += du[j] * av[j].x; o[1] += du[j] * av[j].y; o[2] += du[j] * av[j].z; o[3] += du[j] * av[j].w;
+  }
+}
+DEV void add_lora_dx4(float (&o)[4], const TnArgs& a, int m, int c) {
+  for (int sgi = 0; sgi < a.nseg; ++sgi) {
+    const TnSeg& sg = a.seg[sgi];
+    if (!sg.lora_A) continue;
+    if (a.r == 8)
+      add_lora_dx4_r<8>(o, sg.lora_du + (size_t)m * 8, sg.lora_A, a.Kout, c);
+    else
+      add_lora_dx4_r<16>(o, sg.lora_du + (size_t)m * 16, sg.lora_A, a.Kout, c);
   }
 }
 
@@ -739,15 +784,7 @@ __global__ __launch_bounds__(256) void k_tn_finalize(const TnArgs a, int S) {
   const int m = (int)(i / c4n), c = (int)(i % c4n) * 4;
   const float4 v = sum_planes(a.part, S, (size_t)a.M * a.Kout, (size_t)m * a.Kout + c);
   float o[4] = {v.x, v.y, v.z, v.w};
-  for (int sgi = 0; sgi < a.nseg; ++sgi) {
-    const TnSeg& sg = a.seg[sgi];
-    if (!sg.lora_A) continue;
-    const float* du = sg.lora_du + (size_t)m * a.r;
-    for (int j = 0; j < a.r; ++j) {
-      const float4 av = *(const float4*)(sg.lora_A + (size_t)j * a.Kout + c);
-      o[0] += du[j] * av.x; o[1] += du[j] * av.y; o[2] += du[j] * av.z; o[3] += du[j] * av.w;
-    }
-  }
+  add_lora_dx4(o, a, m, c);
   if constexpr (EPI == TN_STORE_F32) {
     *(float4*)(a.out + (size_t)m * a.ldo + c) = make_float4(o[0], o[1], o[2], o[3]);
   } else if constexpr (EPI == TN_STORE_BF16) {
@@ -784,15 +821,7 @@ __global__ __launch_bounds__(256) void k_tn_finalize_norm(const TnArgs a, int S)
       const int n = c * 4;
       const float4 v = sum_planes(a.part, S, (size_t)a.M * N, (size_t)row * N + n);
       float o[4] = {v.x, v.y, v.z, v.w};
-      for (int sgi = 0; sgi < a.nseg; ++sgi) {
-        const TnSeg& sg = a.seg[sgi];
-        if (!sg.lora_A) continue;
-        const float* du = sg.lora_du + (size_t)row * a.r;
-        for (int j = 0; j < a.r; ++j) {
-          const float4 av = *(const float4*)(sg.lora_A + (size_t)j * N + n);
-          o[0] += du[j] * av.x; o[1] += du[j] * av.y; o[2] += du[j] * av.z; o[3] += du[j] * av.w;
-        }
-      }
+      add_lora_dx4(o, a, row, n);
       g[q] = make_float4(o[0], o[1], o[2], o[3]);
       xv[q] = *(const float4*)(a.norm_x + (size_t)row * N + n);
       const float4 w = *(const float4*)(a.norm_w + n);
