@@ -50,11 +50,13 @@ const char* kSlotNames[S_COUNT] = {
 
 // Slots written by a layer's (re)computed forward and read by its backward, plus the
 // split-K scratch: the training step keeps two copies, so that the recompute of layer l-1
-// (on the side stream) can run while layer l is backpropagated.
+// (on the side stream) can run while layer l is backpropagated. The bf16 copy of the
+// upstream gradient alternates too: layer l reads its set's copy and writes bf16(dx) into
+// the other one, which the LoRA gradient kernels of layer l may still be reading from.
 bool per_set(int s) {
   switch (s) {
     case S_A: case S_Q: case S_K: case S_V: case S_O: case S_LSE: case S_H: case S_C: case S_G: case S_U:
-    case S_Z: case S_LU: case S_SPLIT:
+    case S_Z: case S_LU: case S_DYB: case S_SPLIT:
       return true;
     default:
       return false;
@@ -68,6 +70,7 @@ struct Layout {
   int lm_splits;
   int ntiles;
   size_t split_floats;
+  size_t lora_part_floats;
 };
 
 size_t nt_part(int M, int K, std::initializer_list<int> Ns) {
@@ -124,7 +127,7 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   sz[S_DK] = N * kvd * 2;
   sz[S_DV] = N * kvd * 2;
   sz[S_DA] = N * d * 4;
-  sz[S_PART] = 0;  // unused (LoRA partials live in the shared split scratch)
+  sz[S_PART] = 0;  // LoRA dA / dB token-split partials (sized below)
   sz[S_ROPE_G] = (size_t)T * c->head_dim * 4;
   sz[S_ROPE_L] = (size_t)T * c->head_dim * 4;
   sz[S_TGT] = N * 4;
@@ -149,11 +152,15 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
     mx(tn_part(M, D, {FF, FF}));
     mx(tn_part(M, Q, {D}));
     mx(tn_part(M, D, {Q, KV, KV}));
-    mx(lora_outer_part_floats(M, D > Q ? D : Q, R, 3));
-    mx(lora_outer_part_floats(M, FF > D ? FF : D, R, 2));
     mx(attn_bwd_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim));
     L->split_floats = m;
     sz[S_SPLIT] = m * 4;
+    size_t lp = 0;
+    for (size_t v : {lora_outer_part_floats(M, D > Q ? D : Q, R, 3), lora_outer_part_floats(M, FF > D ? FF : D, R, 2),
+                     lora_outer_part_floats(M, D, R, 1)})
+      lp = v > lp ? v : lp;
+    L->lora_part_floats = lp;
+    sz[S_PART] = lp * 4;
   }
   size_t o = 0;
   for (int i = 0; i < S_COUNT; ++i) {
@@ -288,6 +295,12 @@ struct Ctx {
   hipStream_t st;
   int set;        // copy of the per-layer activation slots (0 or 1)
   int split_set;  // copy of the split-K scratch (0 or 1)
+  // When set: the LoRA weight-gradient kernels of the backward run on `aux` after waiting
+  // for `ev_lr` (recorded on st); the caller joins aux before the activations they read
+  // are rewritten.
+  hipStream_t aux;
+  hipEvent_t ev_lr;
+  bool* aux_used;
 };
 
 // The workspace slot `s` as seen by this context (its activation set and scratch copy).
@@ -389,9 +402,8 @@ hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_
   ob.r = oa.r = D.r;
   ob.layout = 0;
   oa.layout = 1;
-  const SplitScratch sc = scratch(x);
-  ob.part = oa.part = sc.part;
-  ob.part_floats = oa.part_floats = sc.part_floats;
+  ob.part = oa.part = xs<float>(x, S_PART);
+  ob.part_floats = oa.part_floats = x.L.lora_part_floats;
   auto g = Gs.begin();
   for (int p : ps) {
     const bf16* G = *g++;
@@ -403,9 +415,17 @@ hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_
   if (ra.njobs == 0) return hipSuccess;
   hipError_t e = launch_lora_rows(ra, 1, x.st);
   if (e != hipSuccess) return e;
-  e = launch_lora_outer(ob, 1, x.st);
+  hipStream_t so = x.st;
+  if (x.aux) {
+    // dB and dA feed nothing later in the backward: off the caller's stream
+    if ((e = hipEventRecord(x.ev_lr, x.st)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(x.aux, x.ev_lr, 0)) != hipSuccess) return e;
+    so = x.aux;
+    *x.aux_used = true;
+  }
+  e = launch_lora_outer(ob, 1, so);
   if (e != hipSuccess) return e;
-  return launch_lora_outer(oa, 0, x.st);
+  return launch_lora_outer(oa, 0, so);
 }
 
 // Forward of one layer. keep=false: full forward to x_out. keep=true: recompute for the
@@ -468,9 +488,9 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   return MEBP_OK;
 }
 
-// dy_bf16_ready: the workspace's dy_bf16 slot already holds bf16(dy) (written by the
-// block above in the same training step). On return the slot holds bf16(dx) when dx is
-// computed.
+// dy_bf16_ready: the context's dy_bf16 slot already holds bf16(dy) (written by the
+// block above in the same training step). On return the other set's slot holds bf16(dx)
+// when dx is computed.
 // The backward of one layer from the intermediates of its recomputed forward (already in
 // the context's activation set).
 int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora,
@@ -489,6 +509,9 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
   f16* u = xs<f16>(x, S_U);
   f16* z = xs<f16>(x, S_Z);
   bf16* dyb = xs<bf16>(x, S_DYB);
+  Ctx other = x;
+  other.set ^= 1;
+  bf16* dxb = xs<bf16>(other, S_DYB);  // bf16(dx) for the layer below
   float* dc = xs<float>(x, S_DC);
   float* dh = xs<float>(x, S_DH);
   bf16* dhb = xs<bf16>(x, S_DHB);
@@ -554,7 +577,7 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     t.seg[2] = tn_seg(x, base, lora, MEBP_V, dv);
     t.out = da; t.ldo = D.d;
     // a = RMSNorm(x): dx = dh + rmsnorm_bwd(x, da)  (dx may alias dy: dy is no longer read)
-    t.norm_x = x_ckpt; t.norm_w = base->norm_attn; t.resid2 = dh; t.out2 = dx; t.out2b = dyb; t.eps = c->rms_eps;
+    t.norm_x = x_ckpt; t.norm_w = base->norm_attn; t.resid2 = dh; t.out2 = dx; t.out2b = dxb; t.eps = c->rms_eps;
     HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
   }
   return MEBP_OK;
@@ -570,7 +593,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
 }
 
 int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const float* x_last, const int32_t* ids,
-            float* loss, float* dx_last) {
+            float* loss, float* dx_last, bf16* dx_last_bf16) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
   const int V = c->vocab;
@@ -609,7 +632,7 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
   }
   HIP_TRY(launch_ce_dh_reduce(part, x.L.lm_splits, D.N, D.d, emb->q4, emb->scale, tgt, inv_n, dhf, x.st));
   HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, D.N, D.d, c->rms_eps, dx_last,
-                             xs<bf16>(x, S_DYB), x.st));
+                             dx_last_bf16, x.st));
   return MEBP_OK;
 }
 
@@ -624,6 +647,9 @@ Ctx make_ctx(const mebp_config* c, int B, int T, void* ws, mebp_stream_t stream)
   x.st = (hipStream_t)stream;
   x.set = 0;
   x.split_set = 0;
+  x.aux = nullptr;
+  x.ev_lr = nullptr;
+  x.aux_used = nullptr;
   return x;
 }
 
@@ -637,13 +663,14 @@ int rope_table(const Ctx& x, int l, float** out) {
 
 // ------------------------------------------------------------------ side stream
 // The training step runs the recompute of layer l-1 on a second stream of the caller's
-// device while layer l is backpropagated on the caller's stream. The stream and its three
-// events are created on the first step on a device outside of stream capture (a step
-// captured before that runs on the caller's stream alone). Enqueueing a step holds the
+// device while layer l is backpropagated on the caller's stream, and the LoRA dA / dB
+// kernels on a third. The streams and their events are created on the first step on a
+// device outside of stream capture (a step captured before that runs on the caller's
+// stream alone). Enqueueing a step holds the
 // device's lock, so concurrent host threads do not interleave on the shared events.
 struct SideStream {
-  hipStream_t st = nullptr;
-  hipEvent_t ev_fwd = nullptr, ev_rec = nullptr, ev_bwd = nullptr;
+  hipStream_t st = nullptr, aux = nullptr;
+  hipEvent_t ev_fwd = nullptr, ev_rec = nullptr, ev_bwd = nullptr, ev_lr = nullptr, ev_aux = nullptr;
   std::mutex mu;
 };
 
@@ -659,6 +686,9 @@ SideStream* side_stream(hipStream_t main) {
   if (hipStreamIsCapturing(main, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
   SideStream* s = new SideStream();
   if (hipStreamCreateWithFlags(&s->st, hipStreamNonBlocking) != hipSuccess ||
+      hipStreamCreateWithFlags(&s->aux, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&s->ev_lr, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&s->ev_aux, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_fwd, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_rec, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_bwd, hipEventDisableTiming) != hipSuccess) {
@@ -740,7 +770,7 @@ int mebp_lm_head_ce_backward(const mebp_config* cfg, const mebp_q4* emb, const f
   if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
   if (!loss || !aligned(loss, 4)) return fail(MEBP_EINVAL, "loss NULL or misaligned");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
-  return lm_head(x, emb, norm_final, x_last, ids, loss, dx_last);
+  return lm_head(x, emb, norm_final, x_last, ids, loss, dx_last, xs<bf16>(x, S_DYB));
 }
 
 int mebp_embed(const mebp_config* cfg, const mebp_q4* emb, const int32_t* ids, int32_t B, int32_t T, float* x0,
@@ -791,13 +821,19 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   float* g = slot<float>(ws, x.L, S_GRAD);
   // reverse loop: recompute layer l from ckpt[l], backpropagate the upstream gradient
   SideStream* side = side_stream(x.st);
+  const int L = cfg->n_layers;
+  Ctx top = x;
+  top.set = (L - 1) & 1;  // layer l reads bf16(dy) from set l & 1
+  bf16* dyb_top = xs<bf16>(top, S_DYB);
   if (!side) {
     // final linear + loss block, then the layers in reverse on the caller's stream
-    if ((e = lm_head(x, emb, norm_final, ckpt + cfg->n_layers * stride, ids, loss, g))) return e;
-    for (int l = cfg->n_layers - 1; l >= 0; --l) {
+    if ((e = lm_head(x, emb, norm_final, ckpt + L * stride, ids, loss, g, dyb_top))) return e;
+    for (int l = L - 1; l >= 0; --l) {
+      Ctx b = x;
+      b.set = l & 1;
       const float* rope = is_global(cfg, l) ? rope_g : rope_l;
       float* dxl = l > 0 ? g : dx0;
-      if ((e = layer_backward(x, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr,
+      if ((e = layer_backward(b, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr,
                               rope, true)))
         return e;
     }
@@ -821,10 +857,9 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   HIP_TRY(hipStreamWaitEvent(side->st, side->ev_fwd, 0));
   // (the LM head below is enqueued after this point on the caller's stream and overlaps
   // the first recompute)
-  const int L = cfg->n_layers;
   if ((e = recompute(L - 1))) return e;
   HIP_TRY(hipEventRecord(side->ev_rec, side->st));
-  if ((e = lm_head(x, emb, norm_final, ckpt + L * stride, ids, loss, g))) return e;
+  if ((e = lm_head(x, emb, norm_final, ckpt + L * stride, ids, loss, g, dyb_top))) return e;
   for (int l = L - 1; l >= 0; --l) {
     HIP_TRY(hipStreamWaitEvent(x.st, side->ev_rec, 0));  // recompute(l) done
     if (l >= 1) {
@@ -835,11 +870,21 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
     }
     Ctx b = x;
     b.set = l & 1;
+    bool aux_used = false;
+    b.aux = side->aux;
+    b.ev_lr = side->ev_lr;
+    b.aux_used = &aux_used;
     const float* rope = is_global(cfg, l) ? rope_g : rope_l;
     float* dxl = l > 0 ? g : dx0;
     if ((e = layer_backward_only(b, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr,
                                  rope, true)))
       return e;
+    if (aux_used) {
+      // the dA / dB kernels of this layer read set l & 1, its bf16(dy) and the shared
+      // gradient slots: join them before the next layer's backward or recompute
+      HIP_TRY(hipEventRecord(side->ev_aux, side->aux));
+      HIP_TRY(hipStreamWaitEvent(x.st, side->ev_aux, 0));
+    }
     HIP_TRY(hipEventRecord(side->ev_bwd, x.st));
   }
   return MEBP_OK;
