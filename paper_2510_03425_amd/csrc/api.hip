@@ -299,7 +299,8 @@ struct Ctx {
   // for `ev_lr` (recorded on st); the caller joins aux before the activations they read
   // are rewritten.
   hipStream_t aux;
-  hipEvent_t ev_lr;
+  hipEvent_t ev_lr;  // recorded on st, waited for by aux
+  hipEvent_t ev_du;  // recorded on aux, waited for by st
   bool* aux_used;
 };
 
@@ -370,9 +371,27 @@ TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* l
   return s;
 }
 
+// Run `launch` on the context's auxiliary stream once everything enqueued so far on its
+// main stream is done (or inline without one); *ready gets the event that marks its end.
+template <class F>
+hipError_t on_aux(const Ctx& x, hipEvent_t* ready, F&& launch) {
+  *ready = nullptr;
+  if (!x.aux) return launch(x.st);
+  hipError_t e;
+  if ((e = hipEventRecord(x.ev_lr, x.st)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(x.aux, x.ev_lr, 0)) != hipSuccess) return e;
+  if (x.aux_used) *x.aux_used = true;
+  if ((e = launch(x.aux)) != hipSuccess) return e;
+  if ((e = hipEventRecord(x.ev_du, x.aux)) != hipSuccess) return e;
+  *ready = x.ev_du;
+  return hipSuccess;
+}
+
 // u_p = X A_p^T for the adapted projections among `ps` (LoRA down-projection; X fp16),
-// one launch for all of them.
-hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const f16* X, int K, std::initializer_list<int> ps) {
+// one launch for all of them; the consuming GEMM waits for *ready.
+hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const f16* X, int K, std::initializer_list<int> ps,
+                     hipEvent_t* ready) {
+  *ready = nullptr;
   LoraRowsArgs a{};
   a.M = x.D.N;
   a.r = x.D.r;
@@ -383,14 +402,17 @@ hipError_t lora_down(const Ctx& x, const mebp_layer_lora* lora, const f16* X, in
     a.job[a.njobs++] = LoraRowsJob{X, K, K, lora->A[p], lu(x, p)};
   }
   if (a.njobs == 0) return hipSuccess;
-  return launch_lora_rows(a, 0, x.st);
+  return on_aux(x, ready, [&](hipStream_t st) { return launch_lora_rows(a, 0, st); });
 }
 
 // LoRA backward of the adapted projections among `ps`, with output gradients G_p (bf16
 // [N][out_p]) and the shared input X (fp16 [N][in]): du = s G B, dB = s G^T u, dA = du^T X.
-// Three launches for all of them.
+// Three launches for all of them. The input-gradient GEMM that adds du A waits for *ready;
+// dB and dA feed nothing later in the backward and follow du on the same stream.
 hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_lora_grad* grads,
-                    std::initializer_list<int> ps, std::initializer_list<const bf16*> Gs, const f16* X) {
+                    std::initializer_list<int> ps, std::initializer_list<const bf16*> Gs, const f16* X,
+                    hipEvent_t* ready) {
+  *ready = nullptr;
   const Dims& D = x.D;
   LoraRowsArgs ra{};
   ra.M = D.N;
@@ -413,16 +435,9 @@ hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_
     oa.job[oa.njobs++] = LoraOuterJob{X, D.in[p], D.in[p], ldu(x, p), grads->dA[p], 1.0f};
   }
   if (ra.njobs == 0) return hipSuccess;
-  hipError_t e = launch_lora_rows(ra, 1, x.st);
+  hipError_t e = on_aux(x, ready, [&](hipStream_t st) { return launch_lora_rows(ra, 1, st); });
   if (e != hipSuccess) return e;
-  hipStream_t so = x.st;
-  if (x.aux) {
-    // dB and dA feed nothing later in the backward: off the caller's stream
-    if ((e = hipEventRecord(x.ev_lr, x.st)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(x.aux, x.ev_lr, 0)) != hipSuccess) return e;
-    so = x.aux;
-    *x.aux_used = true;
-  }
+  hipStream_t so = x.aux ? x.aux : x.st;
   e = launch_lora_outer(ob, 1, so);
   if (e != hipSuccess) return e;
   return launch_lora_outer(oa, 0, so);
@@ -446,7 +461,8 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   f16* z = xs<f16>(x, S_Z);
 
   HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
-  HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}));
+  hipEvent_t lr;
+  HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}, &lr));
   {
     // q, k, v projections with RoPE applied to q and k on the way out
     NtSeg qs = nt_seg(x, base, lora, MEBP_Q, q, D.qd, nullptr, 0), ks = nt_seg(x, base, lora, MEBP_K, k, D.kvd, nullptr, 0);
@@ -455,7 +471,7 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
     na.rope_cs = rope;
     na.rope_T = x.T;
     na.rope_dh = c->head_dim;
-    HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st));
+    HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st, lr));
   }
   AttnArgs at{};
   at.q = q; at.k = k; at.v = v; at.ldq = D.qd; at.ldk = D.kvd;
@@ -463,15 +479,15 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   at.window = is_global(c, l) ? 0 : c->window;
   at.o = o; at.lse = xs<float>(x, S_LSE);
   HIP_TRY(launch_attn_fwd(at, x.st));
-  HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}));
+  HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}, &lr));
   {
     // h = x + o-projection, then c = RMSNorm(h)
     NtArgs na = nt_args(x, o, D.qd, {nt_seg(x, base, lora, MEBP_O, h, D.d, x_in, D.d)});
     na.norm_w = base->norm_mlp;
     na.norm_out = cc;
-    HIP_TRY(launch_gemm_nt(na, NT_STORE_F32, x.st));
+    HIP_TRY(launch_gemm_nt(na, NT_STORE_F32, x.st, lr));
   }
-  HIP_TRY(lora_down(x, lora, cc, D.d, {MEBP_GATE, MEBP_UP}));
+  HIP_TRY(lora_down(x, lora, cc, D.d, {MEBP_GATE, MEBP_UP}, &lr));
   {
     // g, u projections and z = act(g) * u (g and u kept only for the backward)
     NtArgs na = nt_args(x, cc, D.d, {nt_seg(x, base, lora, MEBP_GATE, g, D.F, nullptr, 0),
@@ -480,11 +496,14 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
     na.act = c->act;
     na.z_out = z;
     na.store_gu = keep;
-    HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st));
+    HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st, lr));
   }
-  HIP_TRY(lora_down(x, lora, z, D.F, {MEBP_DOWN}));
+  HIP_TRY(lora_down(x, lora, z, D.F, {MEBP_DOWN}, &lr));
   if (!keep)
-    HIP_TRY(launch_gemm_nt(nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)}), NT_STORE_F32, x.st));
+    HIP_TRY(launch_gemm_nt(nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)}), NT_STORE_F32, x.st,
+                           lr));
+  else if (lr)
+    HIP_TRY(hipStreamWaitEvent(x.st, lr, 0));  // u of the down projection is read by the backward
   return MEBP_OK;
 }
 
@@ -523,19 +542,20 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
 
   // y = h + down(z)
   if (!dy_bf16_ready) HIP_TRY(launch_f32_to_bf16(dy, dyb, (size_t)D.N * D.d, x.st));
-  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_DOWN}, {dyb}, z));
+  hipEvent_t lr;
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_DOWN}, {dyb}, z, &lr));
   {
     TnArgs t{};
     set_scratch(x, t);
     t.M = D.N; t.Kout = D.F; t.nseg = 1; t.r = D.r;
     t.seg[0] = tn_seg(x, base, lora, MEBP_DOWN, dyb);
     t.g = g; t.u = u; t.ldgu = D.F; t.act = c->act;
-    HIP_TRY(launch_gemm_tn(t, TN_ACT_BWD, TN_A_BF16, x.st));  // g <- dg, u <- d(up)
+    HIP_TRY(launch_gemm_tn(t, TN_ACT_BWD, TN_A_BF16, x.st, lr));  // g <- dg, u <- d(up)
   }
   // z = act(gate(c)) * up(c)
   bf16* dg = (bf16*)g;  // the act-backward epilogue left bf16 dg / du in the g / u buffers
   bf16* dup = (bf16*)u;
-  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_GATE, MEBP_UP}, {dg, dup}, cc));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_GATE, MEBP_UP}, {dg, dup}, cc, &lr));
   {
     TnArgs t{};
     set_scratch(x, t);
@@ -545,17 +565,17 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     t.out = dc; t.ldo = D.d;
     // c = RMSNorm(h): dh = dy + rmsnorm_bwd(h, dc)
     t.norm_x = h; t.norm_w = base->norm_mlp; t.resid2 = dy; t.out2 = dh; t.out2b = dhb; t.eps = c->rms_eps;
-    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
+    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st, lr));
   }
   // h = x + o(O)
-  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_O}, {dhb}, o));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_O}, {dhb}, o, &lr));
   {
     TnArgs t{};
     set_scratch(x, t);
     t.M = D.N; t.Kout = D.qd; t.nseg = 1; t.r = D.r;
     t.seg[0] = tn_seg(x, base, lora, MEBP_O, dhb);
     t.outb = dO; t.ldo = D.qd;
-    HIP_TRY(launch_gemm_tn(t, TN_STORE_BF16, TN_A_BF16, x.st));
+    HIP_TRY(launch_gemm_tn(t, TN_STORE_BF16, TN_A_BF16, x.st, lr));
   }
   // attention (RoPE backward fused into the dq / dk stores)
   {
@@ -565,9 +585,10 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     at.window = is_global(c, l) ? 0 : c->window;
     at.o = o; at.lse = xs<float>(x, S_LSE);
     at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
-    HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), scratch(x), x.st));
+    if (x.aux && x.aux_used) *x.aux_used = true;
+    HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), scratch(x), x.st, x.aux, x.ev_lr, x.ev_du));
   }
-  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_Q, MEBP_K, MEBP_V}, {dq, dk, dv}, a));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_Q, MEBP_K, MEBP_V}, {dq, dk, dv}, a, &lr));
   if (dx) {
     TnArgs t{};
     set_scratch(x, t);
@@ -578,7 +599,7 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     t.out = da; t.ldo = D.d;
     // a = RMSNorm(x): dx = dh + rmsnorm_bwd(x, da)  (dx may alias dy: dy is no longer read)
     t.norm_x = x_ckpt; t.norm_w = base->norm_attn; t.resid2 = dh; t.out2 = dx; t.out2b = dxb; t.eps = c->rms_eps;
-    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st));
+    HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st, lr));
   }
   return MEBP_OK;
 }
@@ -649,6 +670,7 @@ Ctx make_ctx(const mebp_config* c, int B, int T, void* ws, mebp_stream_t stream)
   x.split_set = 0;
   x.aux = nullptr;
   x.ev_lr = nullptr;
+  x.ev_du = nullptr;
   x.aux_used = nullptr;
   return x;
 }
@@ -671,6 +693,7 @@ int rope_table(const Ctx& x, int l, float** out) {
 struct SideStream {
   hipStream_t st = nullptr, aux = nullptr;
   hipEvent_t ev_fwd = nullptr, ev_rec = nullptr, ev_bwd = nullptr, ev_lr = nullptr, ev_aux = nullptr;
+  hipEvent_t ev_du = nullptr;
   std::mutex mu;
 };
 
@@ -689,6 +712,7 @@ SideStream* side_stream(hipStream_t main) {
       hipStreamCreateWithFlags(&s->aux, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_lr, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_aux, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&s->ev_du, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_fwd, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_rec, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->ev_bwd, hipEventDisableTiming) != hipSuccess) {
@@ -812,15 +836,26 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_global, rope_g, x.st));
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_local, rope_l, x.st));
   HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ckpt, x.st));
-  // forward loop: ckpt[l+1] = forward_l(ckpt[l])
-  for (int l = 0; l < cfg->n_layers; ++l) {
-    const float* rope = is_global(cfg, l) ? rope_g : rope_l;
-    if ((e = layer_forward(x, l, &layers[l], &lora[l], ckpt + l * stride, ckpt + (l + 1) * stride, rope, false)))
-      return e;
+  SideStream* side = side_stream(x.st);
+  std::unique_lock<std::mutex> lock;
+  if (side) lock = std::unique_lock<std::mutex>(side->mu);
+  // forward loop: ckpt[l+1] = forward_l(ckpt[l]); the LoRA down-projections run on the
+  // auxiliary stream beside the base GEMMs whose finalize adds them
+  {
+    Ctx xf = x;
+    if (side) {
+      xf.aux = side->aux;
+      xf.ev_lr = side->ev_lr;
+      xf.ev_du = side->ev_du;
+    }
+    for (int l = 0; l < cfg->n_layers; ++l) {
+      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+      if ((e = layer_forward(xf, l, &layers[l], &lora[l], ckpt + l * stride, ckpt + (l + 1) * stride, rope, false)))
+        return e;
+    }
   }
   float* g = slot<float>(ws, x.L, S_GRAD);
   // reverse loop: recompute layer l from ckpt[l], backpropagate the upstream gradient
-  SideStream* side = side_stream(x.st);
   const int L = cfg->n_layers;
   Ctx top = x;
   top.set = (L - 1) & 1;  // layer l reads bf16(dy) from set l & 1
@@ -844,7 +879,6 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   // the previous user of that set, is done; the backward of layer l waits for it. The
   // side stream's first wait is on the end of the forward loop (the checkpoints and the
   // LM head's inputs), its last record is waited for by the caller's stream.
-  std::lock_guard<std::mutex> lock(side->mu);
   Ctx r = x;
   r.st = side->st;
   r.split_set = 1;
@@ -873,6 +907,7 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
     bool aux_used = false;
     b.aux = side->aux;
     b.ev_lr = side->ev_lr;
+    b.ev_du = side->ev_du;
     b.aux_used = &aux_used;
     const float* rope = is_global(cfg, l) ? rope_g : rope_l;
     float* dxl = l > 0 ? g : dx0;

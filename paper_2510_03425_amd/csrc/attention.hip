@@ -674,7 +674,8 @@ size_t attn_bwd_part_floats(int B, int T, int Hq, int Hkv, int dh) {
   return Hq > Hkv ? 2ull * B * T * Hq * dh : 0;
 }
 
-hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScratch& sc, hipStream_t st) {
+hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScratch& sc, hipStream_t st,
+                           hipStream_t aux, hipEvent_t ev_go, hipEvent_t ev_done) {
   const size_t nd = (size_t)a0.B * a0.T * a0.Hq;
   MEBP_TIMED(st, "attn_delta", 0.0, (double)nd * (4.0 * a0.dh + 4),
              hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd + 255) / 256)), dim3(256), 0, st, a0.dO,
@@ -690,28 +691,42 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
   // algorithmic: dV, dK and dP products in the key-block kernel, dQ in the query-block kernel
   const double f_kv = 6.0 * a.dh * pairs, f_q = 2.0 * a.dh * pairs;
   const double io = (double)a.B * a.T * (a.Hq * a.dh * 2.0 * 2 + a.Hkv * a.dh * 2.0 * 4);
+  // dQ depends only on delta and the forward tensors: with an auxiliary stream it runs
+  // there while dK / dV run here
+  const bool split = aux && ev_go && ev_done;
+  hipStream_t sq = split ? aux : st;
+  if (split) {
+    if ((e = hipEventRecord(ev_go, st)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(aux, ev_go, 0)) != hipSuccess) return e;
+  }
   switch (a.dh) {
     case 64:
+      MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, sq, a));
       MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, sc.part));
-      MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, st, a));
       break;
     case 128:
+      MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, sq, a));
       MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<128, 64>), gkv, dim3(256), 0, st, a, sc.part));
-      MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, st, a));
       break;
     case 256:
+      MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, sq, a));
       MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, sc.part));
-      MEBP_TIMED(st, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, st, a));
       break;
     default: return hipErrorInvalidValue;
   }
   e = hipGetLastError();
-  if (e != hipSuccess || a.Hq == a.Hkv) return e;
+  if (e != hipSuccess) return e;
+  if (split) {
+    if ((e = hipEventRecord(ev_done, aux)) != hipSuccess) return e;
+  }
+  if (a.Hq == a.Hkv) return split ? hipStreamWaitEvent(st, ev_done, 0) : hipSuccess;
   const size_t nr = (size_t)a.B * a.T * a.Hkv * (a.dh / 8);
   MEBP_TIMED(st, "attn_dkdv_reduce", 0.0, (double)a.B * a.T * a.Hq * a.dh * 8 + (double)a.B * a.T * a.Hkv * a.dh * 4,
              hipLaunchKernelGGL(k_attn_dkdv_reduce, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, st, a,
                                 (const float*)sc.part));
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess || !split) return e;
+  return hipStreamWaitEvent(st, ev_done, 0);
 }
 
 }  // namespace mebp

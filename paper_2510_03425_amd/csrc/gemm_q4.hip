@@ -900,7 +900,7 @@ GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg) {
   return p;
 }
 
-hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
+hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st, hipEvent_t lora_ready) {
   NtArgs a = a0;
   int tiles = 0, ncat = 0, items = 0;
   double flops = 0, bytes = (double)a.M * a.K * 2;
@@ -926,6 +926,10 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
   if (a.norm_w && a.seg[0].N > 4096) S = 1;  // the fused row norm keeps a row in one workgroup
   a.ldp = ncat;
   dim3 grid(tiles, mt, S);
+  if (lora_ready && S == 1) {
+    const hipError_t ew = hipStreamWaitEvent(st, lora_ready, 0);
+    if (ew != hipSuccess) return ew;
+  }
   if (plan.big) {
     hipError_t eb = launch_gemm_nt_big(a, epi, plan.bn, S, flops, bytes, st);
     if (eb != hipSuccess) return eb;
@@ -962,6 +966,7 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
     return hipSuccess;
   }
   const double fb = 4.0 * S * a.M * ncat + (double)a.M * ncat * (epi == NT_STORE_F16 ? 2 : 4);
+  if (lora_ready && (e = hipStreamWaitEvent(st, lora_ready, 0)) != hipSuccess) return e;
   if (a.gated) {
     const size_t n = (size_t)a.M * (a.seg[0].N / 4);
     MEBP_TIMED(st, "splitk_finalize_gated", 0.0, fb,
@@ -981,7 +986,7 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) {
+hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, hipEvent_t lora_ready) {
   TnArgs a = a0;
   const int ct = (a.Kout + BN - 1) / BN, mt = (a.M + BM - 1) / BM;
   double flops = 0, bytes = 0;
@@ -1006,6 +1011,10 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
   bytes += epi == TN_STORE_BF16 ? 2 * outb : epi == TN_ACT_BWD ? 8 * outb
          : epi == TN_PARTIAL_F32 ? 4 * outb * S : 4 * outb;
   dim3 grid(ct, mt, S);
+  if (lora_ready && S == 1) {
+    const hipError_t ew = hipStreamWaitEvent(st, lora_ready, 0);
+    if (ew != hipSuccess) return ew;
+  }
   if (plan.big) {
     hipError_t eb = launch_gemm_tn_big(a, epi, amode, plan.bn, S, flops, bytes, st);
     if (eb != hipSuccess) return eb;
@@ -1038,6 +1047,7 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st) 
     return hipSuccess;
   }
   const double fb = 4.0 * S * a.M * a.Kout + outb * (epi == TN_ACT_BWD ? 8 : epi == TN_STORE_BF16 ? 2 : 4);
+  if (lora_ready && (e = hipStreamWaitEvent(st, lora_ready, 0)) != hipSuccess) return e;
   if (norm) {
     MEBP_TIMED(st, "splitk_finalize_normbwd", 0.0, fb + 16 * outb,
                hipLaunchKernelGGL(k_tn_finalize_norm, dim3((unsigned)a.M), dim3(256), 0, st, a, S));

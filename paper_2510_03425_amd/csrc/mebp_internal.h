@@ -61,7 +61,10 @@ struct NtArgs {
   f16* norm_out;
   float eps;
 };
-hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st);
+// lora_ready (optional): an event the launch waits on right before the first kernel that
+// reads the LoRA factors (the GEMM itself when unsplit, else the split finalize), so that
+// the LoRA projection may run on another stream beside the GEMM's main loop.
+hipError_t launch_gemm_nt(const NtArgs& a, int epi, hipStream_t st, hipEvent_t lora_ready = nullptr);
 int gemm_nt_tiles(int N);  // number of 128-wide N tiles
 int gemm_splits(int tiles, int ktiles);
 size_t gemm_part_floats(int M, int ncols, int splits);
@@ -124,7 +127,7 @@ struct TnArgs {
   bf16* out2b;
   float eps;
 };
-hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st);
+hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st, hipEvent_t lora_ready = nullptr);
 hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S, double flops, double bytes,
                               hipStream_t st);
 
@@ -203,7 +206,10 @@ struct AttnArgs {
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st);
 // scratch: delta [B][Hq][T]; when Hq > Hkv, per-head dK/dV partials (2*B*T*Hq*dh floats)
 // summed over each GQA group by a reduce kernel.
-hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, const SplitScratch& sc, hipStream_t st);
+// With `aux` (and two events), the dQ kernel runs there beside dK/dV; `st` waits for it
+// before returning.
+hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, const SplitScratch& sc, hipStream_t st,
+                           hipStream_t aux = nullptr, hipEvent_t ev_go = nullptr, hipEvent_t ev_done = nullptr);
 size_t attn_bwd_part_floats(int B, int T, int Hq, int Hkv, int dh);
 
 // ---------------------------------------------------------------- LM head / CE
