@@ -189,8 +189,9 @@ int mebp_kernel_timing_report(char* buf, size_t len);
  * kernel = NULL or times <= 1 switches it off. Results are unchanged, since every such
  * kernel computes its outputs from inputs it does not overwrite; the two kernels that
  * update a buffer in place ("gemm_tn_act_bwd", "splitk_finalize_actbwd") are refused with
- * MEBP_EINVAL. The difference between step times with and without repetition is the
- * kernel's in-stream duration. Host-thread-unsafe; for benchmarks only. */
+ * MEBP_EINVAL. With timing enabled, each burst of repeated launches is bracketed by one
+ * event pair and reported as `times` launches, so the report's average is the kernel's
+ * back-to-back in-stream duration. Host-thread-unsafe; for benchmarks only. */
 int mebp_kernel_repeat(const char* kernel, int32_t times);
 
 #ifdef __cplusplus

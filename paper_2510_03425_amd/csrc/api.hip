@@ -84,11 +84,13 @@ size_t nt_part(int M, int K, std::initializer_list<int> Ns) {
 size_t tn_part(int M, int Kout, std::initializer_list<int> Ns) {
   int v[3], n = 0;
   for (int x : Ns) v[n++] = x;
-  return gemm_part_floats(M, Kout, plan_tn(M, Kout, v, n).splits);
+  return gemm_part_floats(M, Kout, plan_tn(M, Kout, v, n, false).splits);
 }
 
 int lm_head_splits(int N, int d, int V) {
-  const int tiles = ((d + 127) / 128) * ((N + 127) / 128);
+  // token tiles are 256 rows in the large-tile kernel, 128 in the other
+  const int bm = plan_tn(N, d, &V, 1, true).big ? 256 : 128;
+  const int tiles = ((d + 127) / 128) * ((N + bm - 1) / bm);
   int s = (512 + tiles - 1) / tiles;
   const int max_s = ((V + 63) / 64 + 7) / 8;
   if (s > max_s) s = max_s;

@@ -688,7 +688,9 @@ static int env_big() {
 
 GemmPlan plan_big(int M, int ntiles256, int ntiles128, int ktiles, bool logits, int max_bn) {
   GemmPlan p{0, 0, 1};
-  if (!env_big() || M < 1024) return p;
+  // the LM head's GEMMs have hundreds of column tiles (the vocabulary) even for one 256-row
+  // tile of tokens; the layer GEMMs need many token tiles to fill the chip
+  if (!env_big() || M < (logits ? BM : 1024)) return p;
   const int mt = (M + BM - 1) / BM;
   p.big = 1;
   if (max_bn >= 256 && (logits || mt * ntiles256 >= 192)) {

@@ -881,6 +881,9 @@ GemmPlan plan_nt(int M, const int* Ns, int nseg, int K, int epi) {
     t128 += (Ns[s] + 127) / 128;
   }
   const int nk = (K + BK - 1) / BK;
+  // (the logits GEMM gains from the large tiles only from two token tiles on; the dH GEMM
+  // of the LM head already from one)
+  if (epi == NT_LOGITS && M < 512) return GemmPlan{0, 0, 1};
   GemmPlan p = plan_big(M, t256, t128, nk, epi == NT_LOGITS, env_int("MEBP_NT_MAX_BN", 256));
   if (!p.big) p.splits = epi == NT_LOGITS ? 1 : gemm_splits(t128 * ((M + BM - 1) / BM), nk);
   return p;
@@ -892,10 +895,10 @@ int gemm_logit_stat_tiles(int M, int V, int K) {
   return p.big ? (V + 63) / 64 : (V + BN - 1) / BN;
 }
 
-GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg) {
+GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg, bool softmax) {
   int kt = 0;
   for (int s = 0; s < nseg; ++s) kt += (Ns[s] + BK - 1) / BK;
-  GemmPlan p = plan_big(M, (Kout + 255) / 256, (Kout + 127) / 128, kt, false, 128);
+  GemmPlan p = plan_big(M, (Kout + 255) / 256, (Kout + 127) / 128, kt, softmax, 128);
   if (!p.big) p.splits = gemm_splits(((Kout + BN - 1) / BN) * ((M + BM - 1) / BM), kt);
   return p;
 }
@@ -998,7 +1001,7 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, 
   }
   int Ns[3];
   for (int s = 0; s < a.nseg; ++s) Ns[s] = a.seg[s].N;
-  GemmPlan plan = plan_tn(a.M, a.Kout, Ns, a.nseg);
+  GemmPlan plan = plan_tn(a.M, a.Kout, Ns, a.nseg, amode == TN_A_SOFTMAX);
   int S;
   if (epi == TN_PARTIAL_F32) {
     S = a.splits;

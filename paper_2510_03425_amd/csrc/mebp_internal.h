@@ -77,7 +77,7 @@ struct GemmPlan {
 };
 GemmPlan plan_big(int M, int ntiles256, int ntiles128, int ktiles, bool logits, int max_bn);
 GemmPlan plan_nt(int M, const int* Ns, int nseg, int K, int epi);
-GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg);
+GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg, bool softmax);  // softmax: the LM head's dH
 // statistics tiles per row of the LM-head logits GEMM (the column width its waves cover)
 int gemm_logit_stat_tiles(int M, int V, int K);
 hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double flops, double bytes, hipStream_t st);
@@ -227,22 +227,25 @@ hipError_t launch_splitk_reduce(const float* part, int splits, size_t n, float* 
 
 // ---------------------------------------------------------------- diagnostics
 // Per-kernel event timing (see timing.hip). timer_begin returns -1 when disabled.
-int timer_begin(hipStream_t st, const char* name, double flops, double bytes);
+// count: launches bracketed by this record (a repeated burst counts as `count` launches)
+int timer_begin(hipStream_t st, const char* name, double flops, double bytes, int count);
 void timer_end(hipStream_t st, int token);
 int timing_enable(int enable, int capacity);
 int timing_report(char* buf, size_t len);
 int repeat_count(const char* name);
 int set_repeat(const char* name, int times);
 
-// Bracket one launch statement with the optional timer.
-#define MEBP_TIMED(st, name, flops, bytes, stmt)                            \
-  do {                                                                      \
-    const char* name_ = (name);                                             \
-    for (int rep_ = ::mebp::repeat_count(name_); rep_ > 0; --rep_) {        \
-      const int tok_ = ::mebp::timer_begin((st), name_, (flops), (bytes));  \
-      stmt;                                                                 \
-      ::mebp::timer_end((st), tok_);                                        \
-    }                                                                       \
+// Bracket one launch statement (issued repeat_count times back to back) with the
+// optional timer.
+#define MEBP_TIMED(st, name, flops, bytes, stmt)                                  \
+  do {                                                                            \
+    const char* name_ = (name);                                                   \
+    const int reps_ = ::mebp::repeat_count(name_);                                \
+    const int tok_ = ::mebp::timer_begin((st), name_, (flops), (bytes), reps_);   \
+    for (int rep_ = reps_; rep_ > 0; --rep_) {                                    \
+      stmt;                                                                       \
+    }                                                                             \
+    ::mebp::timer_end((st), tok_);                                                \
   } while (0)
 
 }  // namespace mebp

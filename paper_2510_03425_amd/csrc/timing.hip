@@ -3,7 +3,9 @@
 // enable time, tagged with the kernel's name and its algorithmic flops and bytes. The
 // report synchronises on the recorded events and aggregates per kernel name.
 // mebp_kernel_repeat makes every launch of one named kernel run several times back to
-// back, so that the kernel's in-stream duration can be measured as a step-time difference.
+// back; with timing enabled the whole burst is bracketed by one event pair and counted as
+// that many launches, so the report gives the kernel's back-to-back in-stream duration
+// without the event and dispatch latency that a pair around a single launch includes.
 // Not thread-safe: configure, run and report from one host thread.
 #include <stdio.h>
 #include <string.h>
@@ -19,7 +21,7 @@ namespace {
 struct Rec {
   const char* name;
   double flops, bytes;
-  int idx;
+  int idx, count;
 };
 struct State {
   bool on = false;
@@ -34,11 +36,11 @@ State& S() {
 }
 }  // namespace
 
-int timer_begin(hipStream_t st, const char* name, double flops, double bytes) {
+int timer_begin(hipStream_t st, const char* name, double flops, double bytes, int count) {
   State& s = S();
   if (!s.on || 2 * (s.recs.size() + 1) > s.ev.size()) return -1;
   const int idx = (int)s.recs.size();
-  s.recs.push_back({name, flops, bytes, idx});
+  s.recs.push_back({name, flops * count, bytes * count, idx, count});
   (void)hipEventRecord(s.ev[2 * idx], st);
   return idx;
 }
@@ -91,7 +93,7 @@ int timing_report(char* buf, size_t len) {
     if (hipEventSynchronize(s.ev[2 * r.idx + 1]) != hipSuccess) return -1;
     if (hipEventElapsedTime(&ms, s.ev[2 * r.idx], s.ev[2 * r.idx + 1]) != hipSuccess) return -1;
     Agg& a = agg[r.name];
-    a.n += 1;
+    a.n += r.count;
     a.ms += ms;
     a.flops += r.flops;
     a.bytes += r.bytes;
