@@ -241,6 +241,86 @@ DEV NtSeg pick_seg(const NtArgs& a, int s) {
   return r;
 }
 
+// Epilogue of the forward large-tile kernels: logits statistics, split-K partial planes, or
+// LoRA up-projection + residual + fp16 / fp32 store of the wave's 128 x 32NJ block.
+template <int BN, int WNW, int EPI>
+DEV void nt_big_epilogue(f32x16 (&acc)[4][BN / (32 * WNW)], const NtArgs& a, const NtSeg& sg, int m0, int n0,
+                         int wcol0, int wm, int wn, int lane, int z, int S) {
+  constexpr int NJ = BN / (32 * WNW);
+  const int Nn = sg.N;
+  if constexpr (EPI == NT_LOGITS) {
+    // every wave covers one statistics tile of 32 NJ columns
+    _Float16* out = (_Float16*)sg.out;
+    const int cw0 = wcol0;
+    const int stile = cw0 / (32 * NJ);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int m = m0 + acc_row(wm, i, q, lane);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          if (cw0 + 32 * j + (lane & 31) < Nn) mx = fmaxf(mx, acc[i][j][q]);
+#pragma unroll
+        for (int o = 1; o < 32; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+        const int tg = m < a.M ? a.tgt[m] : -1;
+        float se = 0.f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int n = cw0 + 32 * j + (lane & 31);
+          if (n < Nn) {
+            const float v = acc[i][j][q];
+            se += __expf(v - mx);
+            if (m < a.M) {
+              out[(size_t)m * sg.ldo + n] = (_Float16)v;
+              if (n == tg) a.tgt_logit[m] = v;
+            }
+          }
+        }
+#pragma unroll
+        for (int o = 1; o < 32; o <<= 1) se += __shfl_xor(se, o, 64);
+        if ((lane & 31) == 0 && m < a.M && cw0 < Nn) a.stats[(size_t)m * a.ntiles + stile] = make_float2(mx, se);
+      }
+    }
+    return;
+  } else {
+    if (S > 1) {
+      store_partial<NJ>(acc, a.part + (size_t)z * a.M * a.ldp, a.M, a.ldp, Nn - n0, m0, sg.col0 + n0, wm, wn, lane);
+      return;
+    }
+    if (sg.lora_B)
+      lora_mfma<NJ>(acc, sg.lora_u, a.r, m0 + wm * 128, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, Nn, lane);
+    auto put = [&](auto FULL_, auto RES_) {
+      constexpr bool FULL = decltype(FULL_)::value, RES = decltype(RES_)::value;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int m = m0 + acc_row(wm, i, q, lane);
+          if (!FULL && m >= a.M) continue;
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int n = n0 + acc_col<NJ>(wn, j, lane);
+            if (!FULL && n >= Nn) continue;
+            float v = acc[i][j][q];
+            if constexpr (RES) v += sg.resid[(size_t)m * sg.ldr + n];
+            if constexpr (EPI == NT_STORE_F16)
+              ((f16*)sg.out)[(size_t)m * sg.ldo + n] = (f16)v;
+            else
+              ((float*)sg.out)[(size_t)m * sg.ldo + n] = v;
+          }
+        }
+    };
+    const bool full = m0 + BM <= a.M && n0 + BN <= Nn;
+    if (sg.resid) {
+      if (full) put(IC<1>{}, IC<1>{}); else put(IC<0>{}, IC<1>{});
+    } else {
+      if (full) put(IC<1>{}, IC<0>{}); else put(IC<0>{}, IC<0>{});
+    }
+  }
+}
+
 // WNW waves along n (2 or 4), two along m: 128 x WNW threads, each wave 128 x BN/WNW. With
 // four (512 threads) two waves share each SIMD, so one wave's decompression (VALU) runs
 // beside the other's MFMAs.
@@ -387,77 +467,176 @@ __global__ __launch_bounds__(128 * WNW, 1) void k_gemm_nt_big(const NtArgs a) {
       run(IC<0>{});
   }
 
-  if constexpr (EPI == NT_LOGITS) {
-    // every wave covers one statistics tile of 32 NJ columns
-    _Float16* out = (_Float16*)sg.out;
-    const int cw0 = wcol0;
-    const int stile = cw0 / (32 * NJ);
+  nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
+}
+
+
+// ---------------------------------------------------------------- forward, LDS-direct tiles
+// Natural-order decompression: 8 int4 codes k0..k7 of a dword times scale into fp16 pairs
+// (k0,k1),(k2,k3),(k4,k5),(k6,k7). Offset-binary nibbles (code ^ 8) of the even and the odd
+// elements are gathered into bytes, a byte permute places one even and one odd code in the
+// two halves, 0x6400 | (q + 8) is the fp16 value 1024 + q + 8, and one packed subtraction of
+// 1032 and one packed multiply give q exactly and then q * s rounded to nearest.
+DEV uint4 dequant8_natural(uint32_t w, f16x2 s2) {
+  const uint32_t ev = (w & 0x0F0F0F0Fu) ^ 0x08080808u;         // k0, k2, k4, k6
+  const uint32_t od = ((w >> 4) & 0x0F0F0F0Fu) ^ 0x08080808u;  // k1, k3, k5, k7
+  const f16x2 off = {(_Float16)1032.0f, (_Float16)1032.0f};
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    // byte 0 <- even byte j, byte 2 <- odd byte j, bytes 1 and 3 <- 0
+    const uint32_t t = __builtin_amdgcn_perm(od, ev, (uint32_t)j | 0x0C00u | ((4u + j) << 16) | 0x0C000000u) | 0x64006400u;
+    o[j] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, t) - off) * s2);
+  }
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// vmcnt-only wait (expcnt and lgkmcnt left open), gfx9 encoding
+template <int N>
+DEV void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Forward product with 256 x 256 tiles and 8 waves (2 along m x 4 along n, 128 x 64 each),
+// K step 64. The activation tile goes from global memory straight into LDS (buffer loads
+// with the LDS flag: no staging registers, no LDS stores) through a ring of three stages
+// filled two K tiles ahead. A stage holds the 256 x 64 fp16 tile as 128-byte rows whose
+// eight 16-byte chunks are stored at position chunk ^ (row & 7), so that the MFMA fragment
+// reads (32 rows, one chunk each) spread over all banks. The weights are loaded into
+// registers, also two tiles ahead, and decompressed by each wave for its own columns.
+constexpr int LDS_STAGES = 3, LDS_STAGE_BYTES = BM * BK * 2;
+template <int EPI>
+__global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
+  constexpr int BN = 256, WNW = 4, NJ = 2;
+  // one LDS object per ring stage, so that the compiler can tell the fragment reads of one
+  // stage from the LDS-direct loads in flight into another
+  __shared__ __attribute__((aligned(1024))) uint8_t lds0[LDS_STAGE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds1[LDS_STAGE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds2[LDS_STAGE_BYTES];
+  auto stage_ptr = [&](auto S_) -> uint8_t* {
+    constexpr int st = decltype(S_)::value;
+    return st == 0 ? lds0 : st == 1 ? lds1 : lds2;
+  };
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WNW, wn = wave % WNW, h = lane >> 5;
+  const int nt = blockIdx.x;
+  int s = 0;
+  if (a.nseg > 1 && nt >= a.seg[1].tile0) s = 1;
+  if (a.nseg > 2 && nt >= a.seg[2].tile0) s = 2;
+  const NtSeg sg = pick_seg(a, s);
+  const int n0 = (nt - sg.tile0) * BN, m0 = blockIdx.y * BM;
+  const int K = a.K, Nn = sg.N, Kh = K >> 1;
+  const int nk = (K + BK - 1) / BK, kgroups = (K + 31) >> 5;
+  const int z = blockIdx.z, S = gridDim.z;
+  const int kt_begin = (int)((long long)nk * z / S), kt_end = (int)((long long)nk * (z + 1) / S);
+
+  const rsrc_t rA = make_rsrc((const u16*)a.X + (size_t)m0 * a.lda, (size_t)min(BM, a.M - m0) * a.lda * 2);
+  const int wcol0 = n0 + wn * 32 * NJ;
+  const int wrows = max(0, min(32 * NJ, Nn - wcol0));
+  const rsrc_t rB = make_rsrc(sg.q4 + (size_t)min(wcol0, Nn) * Kh, (size_t)wrows * Kh);
+  const rsrc_t rS = make_rsrc(sg.scale + (size_t)min(wcol0, Nn) * kgroups, (size_t)wrows * kgroups * 2);
+  // activation loads: instruction i of wave w fills tile rows 8 (w + 8 i) .. +8, lane l row
+  // 8 (w + 8 i) + l / 8, LDS position l % 8, i.e. global chunk (l % 8) ^ (row & 7)
+  uint32_t offA[4];
+  int chunkA[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 8 * (wave + 8 * i) + (lane >> 3);
+    chunkA[i] = (lane & 7) ^ (row & 7);
+    offA[i] = (uint32_t)((row * a.lda + 8 * chunkA[i]) * 2);
+  }
+  const uint32_t offB = (uint32_t)((lane & 31) * Kh + 16 * h), offS = (uint32_t)(((lane & 31) * kgroups + h) * 2);
+  // fragment reads: row wm*128 + 32 i + (l % 32), chunk 4h + t at position (4h + t) ^ (l & 7)
+  const uint32_t rowA = (uint32_t)((wm * 128 + (lane & 31)) * 128);
+
+  uint4 rb[LDS_STAGES][NJ];
+  uint32_t rsc[LDS_STAGES][NJ];
+  f32x16 acc[4][NJ];
+  zero_acc(acc);
+  const bool tail = (K % BK) != 0;
+
+  auto gload = [&](auto S_, int kt) {
+    constexpr int st = decltype(S_)::value;  // ring stage (registers and LDS)
+    const int k0 = kt * BK;
+    __attribute__((address_space(3))) uint8_t* dst = (__attribute__((address_space(3))) uint8_t*)stage_ptr(S_);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+      // chunks past the reduction length read as zero (out-of-range offset)
+      const uint32_t off = (!tail || k0 + 8 * chunkA[i] < K) ? offA[i] + 2 * k0 : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, dst + 1024 * (wave + 8 * i), 16, off, 0, 0, 0);
+    }
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int m = m0 + acc_row(wm, i, q, lane);
-        float mx = -INFINITY;
+    for (int j = 0; j < NJ; ++j) {
+      rb[st][j] = bload128(rB, offB + (uint32_t)(32 * j * Kh) + (k0 >> 1));
+      rsc[st][j] = bload16(rS, offS + (uint32_t)(32 * j * kgroups * 2) + 2 * (k0 >> 5));
+    }
+    if (tail && k0 + BK > K) {
+      const int kb = k0 + 32 * h;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j)
-          if (cw0 + 32 * j + (lane & 31) < Nn) mx = fmaxf(mx, acc[i][j][q]);
-#pragma unroll
-        for (int o = 1; o < 32; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-        const int tg = m < a.M ? a.tgt[m] : -1;
-        float se = 0.f;
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-          const int n = cw0 + 32 * j + (lane & 31);
-          if (n < Nn) {
-            const float v = acc[i][j][q];
-            se += __expf(v - mx);
-            if (m < a.M) {
-              out[(size_t)m * sg.ldo + n] = (_Float16)v;
-              if (n == tg) a.tgt_logit[m] = v;
-            }
-          }
-        }
-#pragma unroll
-        for (int o = 1; o < 32; o <<= 1) se += __shfl_xor(se, o, 64);
-        if ((lane & 31) == 0 && m < a.M && cw0 < Nn) a.stats[(size_t)m * a.ntiles + stile] = make_float2(mx, se);
+      for (int j = 0; j < NJ; ++j) {
+        if (kb >= K) rsc[st][j] = 0u;
+        if (kb + 0 >= K) rb[st][j].x = 0u;
+        if (kb + 8 >= K) rb[st][j].y = 0u;
+        if (kb + 16 >= K) rb[st][j].z = 0u;
+        if (kb + 24 >= K) rb[st][j].w = 0u;
       }
     }
-    return;
-  } else {
-    if (S > 1) {
-      store_partial<NJ>(acc, a.part + (size_t)z * a.M * a.ldp, a.M, a.ldp, Nn - n0, m0, sg.col0 + n0, wm, wn, lane);
-      return;
+  };
+  auto mma = [&](auto S_) {
+    constexpr int st = decltype(S_)::value;
+    const uint8_t* As = stage_ptr(S_) + rowA;
+    f16x2 sc[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)rsc[st][j]);
+      sc[j] = f16x2{v, v};
     }
-    if (sg.lora_B)
-      lora_mfma<NJ>(acc, sg.lora_u, a.r, m0 + wm * 128, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, Nn, lane);
-    auto put = [&](auto FULL_, auto RES_) {
-      constexpr bool FULL = decltype(FULL_)::value, RES = decltype(RES_)::value;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int pos = ((4 * h + t) ^ (lane & 7)) * 16;
+      uint4 af[4], bfr[NJ];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *(const uint4*)(As + 4096 * i + pos);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const uint32_t w = t == 0 ? rb[st][j].x : t == 1 ? rb[st][j].y : t == 2 ? rb[st][j].z : rb[st][j].w;
+        bfr[j] = dequant8_natural(w, sc[j]);
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int m = m0 + acc_row(wm, i, q, lane);
-          if (!FULL && m >= a.M) continue;
-#pragma unroll
-          for (int j = 0; j < NJ; ++j) {
-            const int n = n0 + acc_col<NJ>(wn, j, lane);
-            if (!FULL && n >= Nn) continue;
-            float v = acc[i][j][q];
-            if constexpr (RES) v += sg.resid[(size_t)m * sg.ldr + n];
-            if constexpr (EPI == NT_STORE_F16)
-              ((f16*)sg.out)[(size_t)m * sg.ldo + n] = (f16)v;
-            else
-              ((float*)sg.out)[(size_t)m * sg.ldo + n] = v;
-          }
-        }
-    };
-    const bool full = m0 + BM <= a.M && n0 + BN <= Nn;
-    if (sg.resid) {
-      if (full) put(IC<1>{}, IC<1>{}); else put(IC<0>{}, IC<1>{});
-    } else {
-      if (full) put(IC<1>{}, IC<0>{}); else put(IC<0>{}, IC<0>{});
+        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpF16>(af[i], bfr[j], acc[i][j]);
     }
+  };
+  // Step of tile k (ring stage I): issue the loads of tile k+2 into stage I+2 (last read by
+  // tile k-1, before the previous barrier), the MFMAs of tile k, then wait until this
+  // thread's activation loads of tile k+1 have landed (the loads issued after them: the
+  // weights of k+1 and all of k+2, 2 NJ + 4 + 2 NJ) and meet the other waves at the barrier.
+  auto step = [&](auto I_, int k) {
+    constexpr int I = decltype(I_)::value;
+    gload(IC<(I + 2) % LDS_STAGES>{}, min(k + 2, kt_end - 1));
+    mma(IC<I>{});
+    wait_vmcnt<4 * NJ + 4>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");  // no LDS access moves across the barrier
+  };
+  if (kt_begin < kt_end) {
+    gload(IC<0>{}, kt_begin);
+    gload(IC<1>{}, min(kt_begin + 1, kt_end - 1));
+    wait_vmcnt<4 * NJ + 4>();  // tile kt_begin's activations (weights and tile +1 may fly)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    int k = kt_begin;
+    for (; k + 3 <= kt_end; k += 3) {
+      step(IC<0>{}, k);
+      step(IC<1>{}, k + 1);
+      step(IC<2>{}, k + 2);
+    }
+    if (k < kt_end) step(IC<0>{}, k);
+    if (k + 1 < kt_end) step(IC<1>{}, k + 1);
   }
+  nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
 }
 
 // ---------------------------------------------------------------------------- transposed
@@ -723,7 +902,21 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
 #define NT_BIG(BN_, EPI_)                                                                                 \
   MEBP_TIMED(st, name, flops, bytes,                                                                      \
              hipLaunchKernelGGL((k_gemm_nt_big<BN_, BN_ / 64, EPI_>), grid, dim3(2 * BN_), 0, st, b))
-  if (bn == 256) {
+  static const int use_lds = [] {
+    const char* e = getenv("MEBP_NT_LDS");
+    return e && *e ? atoi(e) : 1;
+  }();
+  if (bn == 256 && use_lds && a.K % 8 == 0) {
+#define NT_LDS(EPI_) \
+  MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_nt_lds<EPI_>), grid, dim3(512), 0, st, b))
+    if (epi == NT_LOGITS)
+      NT_LDS(NT_LOGITS);
+    else if (epi == NT_STORE_F16)
+      NT_LDS(NT_STORE_F16);
+    else
+      NT_LDS(NT_STORE_F32);
+#undef NT_LDS
+  } else if (bn == 256) {
     if (epi == NT_LOGITS)
       NT_BIG(256, NT_LOGITS);
     else if (epi == NT_STORE_F16)
