@@ -33,17 +33,20 @@ DEV void split_hi_lo(const float (&f)[8], uint4& hi, uint4& lo) {
 }
 
 // ------------------------------------------------------------------------------ rows
-// out[m][j] = s * sum_k X[m][k] W(j,k); workgroup = 64 rows x 16 outputs of one job; the
-// 4 waves take interleaved 32-wide k steps, two steps in flight per iteration.
-constexpr int LR_ROWS = 64;
+// out[m][j] = s * sum_k X[m][k] W(j,k); workgroup = 64 rows x 16 outputs of one job and
+// LR_WAVES waves that take interleaved 64-wide K super-steps (every row segment a lane
+// group loads is 128 contiguous bytes), two super-steps in flight per iteration; the
+// per-wave partial tiles are summed through LDS in wave order. The many waves keep enough
+// loads in flight to stream X near the HBM rate even with few row blocks.
+constexpr int LR_ROWS = 64, LR_WAVES = 8;
 template <class Op>
-__global__ __launch_bounds__(256) void k_lora_rows(const LoraRowsArgs a) {
-  __shared__ float red[4][LR_ROWS][17];
+__global__ __launch_bounds__(64 * LR_WAVES) void k_lora_rows(const LoraRowsArgs a) {
+  __shared__ float red[LR_WAVES][LR_ROWS][17];
   const LoraRowsJob& jb = a.job[blockIdx.y];
   const u16* X = (const u16*)jb.X;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int m0 = blockIdx.x * LR_ROWS, M = a.M, K = jb.K, r = a.r;
-  const int nsteps = (K + 31) / 32;
+  const int nsup = (K + 63) / 64;
   const int j = lane & 15;
 
   auto load_w = [&](int k, uint4& bh, uint4& bl) {
@@ -62,31 +65,41 @@ __global__ __launch_bounds__(256) void k_lora_rows(const LoraRowsArgs a) {
     }
     split_hi_lo<Op>(f, bh, bl);
   };
-  auto load_x = [&](int k, uint4 (&xv)[4]) {
+  // the super-step's two 32-wide halves of rows t*16 + lane%16 (K is a multiple of 8, so a
+  // chunk is either wholly inside the row or wholly past it)
+  auto load_x = [&](int k, uint4 (&xv)[2][4]) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int m = m0 + t * 16 + (lane & 15);
-      xv[t] = (k < K && m < M) ? *(const uint4*)(X + (size_t)m * jb.ldx + k) : make_uint4(0, 0, 0, 0);
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int m = m0 + t * 16 + (lane & 15), kk = k + 32 * hh;
+        xv[hh][t] = (kk < K && m < M) ? *(const uint4*)(X + (size_t)m * jb.ldx + kk) : make_uint4(0, 0, 0, 0);
+      }
+  };
+  auto mma = [&](int k, const uint4 (&xv)[2][4], f32x4 (&acc)[4]) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      uint4 bh, bl;
+      load_w(k + 32 * hh, bh, bl);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        acc[t] = mfma16_raw<Op>(xv[hh][t], bh, acc[t]);
+        acc[t] = mfma16_raw<Op>(xv[hh][t], bl, acc[t]);
+      }
     }
   };
 
   f32x4 acc[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int st = w; st < nsteps; st += 8) {
-    const int k0 = st * 32 + 8 * (lane >> 4), k1 = (st + 4) * 32 + 8 * (lane >> 4);
-    uint4 bh0, bl0, bh1, bl1, x0[4], x1[4];
-    load_w(k0, bh0, bl0);
+  const int ko = 8 * (lane >> 4);
+  for (int ss = w; ss < nsup; ss += 2 * LR_WAVES) {
+    const int k0 = ss * 64 + ko, k1 = (ss + LR_WAVES) * 64 + ko;
+    uint4 x0[2][4], x1[2][4];
     load_x(k0, x0);
-    load_w(k1, bh1, bl1);
     load_x(k1, x1);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      acc[t] = mfma16_raw<Op>(x0[t], bh0, acc[t]);
-      acc[t] = mfma16_raw<Op>(x0[t], bl0, acc[t]);
-      acc[t] = mfma16_raw<Op>(x1[t], bh1, acc[t]);
-      acc[t] = mfma16_raw<Op>(x1[t], bl1, acc[t]);
-    }
+    mma(k0, x0, acc);
+    mma(k1, x1, acc);
   }
   // lane holds rows t*16 + 4g + rr, column j
 #pragma unroll
@@ -94,11 +107,14 @@ __global__ __launch_bounds__(256) void k_lora_rows(const LoraRowsArgs a) {
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr) red[w][t * 16 + 4 * (lane >> 4) + rr][j] = acc[t][rr];
   __syncthreads();
+  for (int o = tid; o < LR_ROWS * 16; o += 64 * LR_WAVES) {
+    const int mm = o >> 4, jj = o & 15, m = m0 + mm;
+    if (m < M && jj < r) {
+      float v = 0.f;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int o = tid + 256 * q, mm = o >> 4, jj = o & 15, m = m0 + mm;
-    if (m < M && jj < r)
-      jb.out[(size_t)m * r + jj] = a.s * ((red[0][mm][jj] + red[1][mm][jj]) + (red[2][mm][jj] + red[3][mm][jj]));
+      for (int ww = 0; ww < LR_WAVES; ++ww) v += red[ww][mm][jj];
+      jb.out[(size_t)m * r + jj] = a.s * v;
+    }
   }
 }
 
@@ -106,13 +122,15 @@ __global__ __launch_bounds__(256) void k_lora_rows(const LoraRowsArgs a) {
 // R(c, j) = s * sum_m Mx[m][c] V[m][j]; workgroup = 128 columns c x 16 j of one job (each
 // wave 32 c); per iteration 64 tokens are staged transposed in LDS (c-major,
 // token-contiguous) together with V^T as hi/lo planes. The products run in bf16 (V may be
-// a tiny gradient); an fp16 Mx is converted to bf16 while staged.
+// a tiny gradient); an fp16 Mx is converted to bf16 while staged. The LDS tiles are
+// double-buffered and the next iteration's tokens are loaded into registers while the
+// current ones are multiplied, so one barrier per iteration suffices and loads overlap.
 constexpr int LO_C = 128, LO_M = 64, LO_LD = LO_M + 8;
 template <bool MX_F16>
 __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 Mt[LO_C * LO_LD];
-  __shared__ __attribute__((aligned(16))) u16 Vh[16 * LO_LD];
-  __shared__ __attribute__((aligned(16))) u16 Vl[16 * LO_LD];
+  __shared__ __attribute__((aligned(16))) u16 Mt[2][LO_C * LO_LD];
+  __shared__ __attribute__((aligned(16))) u16 Vh[2][16 * LO_LD];
+  __shared__ __attribute__((aligned(16))) u16 Vl[2][16 * LO_LD];
   const LoraOuterJob& jb = a.job[blockIdx.y];
   const u16* Mx = (const u16*)jb.Mx;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -121,20 +139,38 @@ __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
   if (c0 >= C) return;
   const int nsteps = (M + LO_M - 1) / LO_M;
   const int sb = (int)((long long)nsteps * ms / MS), se = (int)((long long)nsteps * (ms + 1) / MS);
-  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-  for (int st = sb; st < se; ++st) {
+  // threads 0..127: one 8x8 block of Mx (8 tokens x 8 columns); 128..255: 8 tokens of V
+  const bool mx_role = tid < 128;
+  const int rb = tid & 7, cb = (tid >> 3) & 15;      // Mx role: token block, column block
+  const int jv = (tid - 128) & 15, mq = (tid - 128) >> 4;  // V role: output j, token group
+  uint32_t in[8][4];
+  float f[8];
+  auto load = [&](int st) {
     const int mb = st * LO_M;
-    if (tid < 128) {
-      // one 8x8 block of Mx (8 tokens x 8 columns) per thread, transposed into Mt[c][m]
-      const int rb = tid & 7, cb = tid >> 3;  // 8 token blocks x 16 column blocks
-      uint32_t in[8][4];
+    if (mx_role) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int m = mb + rb * 8 + i, c = c0 + cb * 8;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (m < M && c < C) v = *(const uint4*)(Mx + (size_t)m * jb.ldm + c);
-        if (MX_F16) v = f16x8_to_bf16x8(v);
         in[i][0] = v.x; in[i][1] = v.y; in[i][2] = v.z; in[i][3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int m = mb + mq * 8 + i;
+        f[i] = (m < M && jv < r) ? jb.V[(size_t)m * r + jv] : 0.f;
+      }
+    }
+  };
+  auto store = [&](int buf) {
+    if (mx_role) {
+      if (MX_F16) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const uint4 v = f16x8_to_bf16x8(make_uint4(in[i][0], in[i][1], in[i][2], in[i][3]));
+          in[i][0] = v.x; in[i][1] = v.y; in[i][2] = v.z; in[i][3] = v.w;
+        }
       }
 #pragma unroll
       for (int jc = 0; jc < 8; ++jc) {
@@ -146,35 +182,33 @@ __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
           o = make_uint4(perm_lo16(in[0][jc >> 1], in[1][jc >> 1]), perm_lo16(in[2][jc >> 1], in[3][jc >> 1]),
                          perm_lo16(in[4][jc >> 1], in[5][jc >> 1]), perm_lo16(in[6][jc >> 1], in[7][jc >> 1]));
         }
-        *(uint4*)(Mt + (cb * 8 + jc) * LO_LD + rb * 8) = o;
+        *(uint4*)(Mt[buf] + (cb * 8 + jc) * LO_LD + rb * 8) = o;
       }
     } else {
-      // V^T hi/lo planes: 16 j x 64 tokens, 8 tokens per thread
-      const int t = tid - 128, jv = t & 15, mq = t >> 4;  // mq: 8 token groups of 8
-      float f[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int m = mb + mq * 8 + i;
-        f[i] = (m < M && jv < r) ? jb.V[(size_t)m * r + jv] : 0.f;
-      }
       uint4 hi, lo;
       split_hi_lo<OpBF16>(f, hi, lo);
-      *(uint4*)(Vh + jv * LO_LD + mq * 8) = hi;
-      *(uint4*)(Vl + jv * LO_LD + mq * 8) = lo;
+      *(uint4*)(Vh[buf] + jv * LO_LD + mq * 8) = hi;
+      *(uint4*)(Vl[buf] + jv * LO_LD + mq * 8) = lo;
     }
+  };
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  if (sb < se) load(sb);
+  for (int st = sb; st < se; ++st) {
+    const int buf = (st - sb) & 1;
+    store(buf);
     __syncthreads();
+    if (st + 1 < se) load(st + 1);
 #pragma unroll
     for (int kk = 0; kk < LO_M; kk += 32) {
-      const uint4 bh = *(const uint4*)(Vh + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
-      const uint4 bl = *(const uint4*)(Vl + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
+      const uint4 bh = *(const uint4*)(Vh[buf] + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
+      const uint4 bl = *(const uint4*)(Vl[buf] + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
 #pragma unroll
       for (int ct = 0; ct < 2; ++ct) {
-        const uint4 av = *(const uint4*)(Mt + (w * 32 + ct * 16 + (lane & 15)) * LO_LD + kk + 8 * (lane >> 4));
+        const uint4 av = *(const uint4*)(Mt[buf] + (w * 32 + ct * 16 + (lane & 15)) * LO_LD + kk + 8 * (lane >> 4));
         acc[ct] = mfma16_raw<OpBF16>(av, bh, acc[ct]);
         acc[ct] = mfma16_raw<OpBF16>(av, bl, acc[ct]);
       }
     }
-    __syncthreads();
   }
   // lane holds R rows c = c0 + w*32 + ct*16 + 4g + rr, column j = lane%16
   const int j = lane & 15;
@@ -212,7 +246,7 @@ int outer_splits(int M, int cmax, int njobs) {
   const int cb = ((cmax + LO_C - 1) / LO_C) * njobs, steps = (M + LO_M - 1) / LO_M;
   if (steps < 16) return 1;
   int s = (256 + cb - 1) / cb;
-  if (s > steps / 8) s = steps / 8;
+  if (s > steps / 4) s = steps / 4;
   if (s > 64) s = 64;
   return s < 1 ? 1 : s;
 }
@@ -232,9 +266,11 @@ hipError_t launch_lora_rows(const LoraRowsArgs& a, int xbf16, hipStream_t st) {
     bytes += (double)a.M * a.job[i].K * 2 + (double)a.job[i].K * a.r * 4 + (double)a.M * a.r * 4;
   }
   if (xbf16)
-    MEBP_TIMED(st, "lora_rows", flops, bytes, hipLaunchKernelGGL(k_lora_rows<OpBF16>, grid, dim3(256), 0, st, a));
+    MEBP_TIMED(st, "lora_rows", flops, bytes,
+               hipLaunchKernelGGL(k_lora_rows<OpBF16>, grid, dim3(64 * LR_WAVES), 0, st, a));
   else
-    MEBP_TIMED(st, "lora_rows", flops, bytes, hipLaunchKernelGGL(k_lora_rows<OpF16>, grid, dim3(256), 0, st, a));
+    MEBP_TIMED(st, "lora_rows", flops, bytes,
+               hipLaunchKernelGGL(k_lora_rows<OpF16>, grid, dim3(64 * LR_WAVES), 0, st, a));
   return hipGetLastError();
 }
 
