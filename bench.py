@@ -174,6 +174,72 @@ def traffic_summary(args, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir):
     print("\n".join(lines))
 
 
+def counter_summary(args, fetch_dir, write_dir, sq_dir, cal_fetch_dir, cal_write_dir):
+    """Per-kernel table from rocprofv3 --pmc runs of the same command: serialized duration (the
+    counter runs' own timestamps), HBM bytes per launch (FETCH_SIZE + WRITE_SIZE scaled by a
+    plain-copy calibration) and GB/s against the 8 TB/s peak, and MFMA busy cycles as a share
+    of all SIMD cycles (SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs))."""
+    import csv
+    import glob
+    cal_n = args.calibrate_copy << 20 if args.calibrate_copy else 1 << 30
+    cf, cw = pmc_per_dispatch(cal_fetch_dir, "FETCH_SIZE"), pmc_per_dispatch(cal_write_dir, "WRITE_SIZE")
+    kf = cal_n / (max(max(v) for v in cf.values()) * 1024.0)
+    kw = cal_n / (max(max(v) for v in cw.values()) * 1024.0)
+
+    def per_dispatch(d, counters):
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        out = {}
+        for r in csv.DictReader(open(path)):
+            key = (r["Dispatch_Id"], _kname(r["Kernel_Name"]))
+            rec = out.setdefault(key, {"dur": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3})
+            if r["Counter_Name"] in counters:
+                rec[r["Counter_Name"]] = rec.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        return out
+    fe = per_dispatch(fetch_dir, ["FETCH_SIZE"])
+    wr = per_dispatch(write_dir, ["WRITE_SIZE"])
+    sq = per_dispatch(sq_dir, ["SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", "SQ_INSTS_VALU", "SQ_INSTS_MFMA"])
+    agg = {}
+    for (d, n), rec in fe.items():
+        a = agg.setdefault(n, {"n": 0, "dur": 0.0, "f": 0.0, "w": 0.0, "mb": 0.0, "gr": 0.0, "valu": 0.0, "mfma": 0.0,
+                               "nsq": 0})
+        a["n"] += 1
+        a["dur"] += rec["dur"]
+        a["f"] += rec.get("FETCH_SIZE", 0.0) * 1024.0 * kf
+    for (d, n), rec in wr.items():
+        if n in agg:
+            agg[n]["w"] += rec.get("WRITE_SIZE", 0.0) * 1024.0 * kw
+    for (d, n), rec in sq.items():
+        if n in agg:
+            a = agg[n]
+            a["mb"] += rec.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            a["gr"] += rec.get("GRBM_GUI_ACTIVE", 0.0)
+            a["valu"] += rec.get("SQ_INSTS_VALU", 0.0)
+            a["mfma"] += rec.get("SQ_INSTS_MFMA", 0.0)
+            a["nsq"] += 1
+    lines = [f"# per-kernel counters, workload {args.workload} (rocprofv3 --pmc, kernels serialized by the counter runs)",
+             f"# copy calibration: reads x{kf:.4f}, writes x{kw:.4f} (a plain {cal_n} B device copy)",
+             f"# HBM GB/s = (fetch + write bytes) / serialized duration, against {PEAK_HBM_GBS:.0f} GB/s; MFMA busy = "
+             "SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs)",
+             f"{'kernel':48s} {'calls':>6s} {'avg_us':>9s} {'MB/launch':>10s} {'GB/s':>8s} {'%HBM':>6s} {'%MFMA':>6s} "
+             f"{'VALU/MFMA':>9s} {'total_ms':>9s}"]
+    tot = sum(a["dur"] for a in agg.values())
+    for n, a in sorted(agg.items(), key=lambda kv: -kv[1]["dur"]):
+        if a["dur"] < 0.002 * tot:
+            continue
+        dur = a["dur"] / a["n"]
+        mbytes = (a["f"] + a["w"]) / a["n"] / 1e6
+        gbs = mbytes * 1e6 / (dur * 1e-6) / 1e9
+        mf = 100.0 * a["mb"] * 8.0 / (1024.0 * a["gr"]) if a["gr"] else 0.0
+        vm = a["valu"] / a["mfma"] if a["mfma"] else float("nan")
+        lines.append(f"{n[:48]:48s} {a['n']:6d} {dur:9.2f} {mbytes:10.2f} {gbs:8.1f} {100 * gbs / PEAK_HBM_GBS:6.1f} "
+                     f"{mf:6.1f} {vm:9.2f} {a['dur'] / 1e3:9.2f}")
+    lines.append(f"digest {kernel_source_digest()}")
+    path = os.path.join(ROOT, "profiles", f"kernel_counters_{args.workload}.txt")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -189,7 +255,14 @@ def main():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs of this bench and of "
                          "--calibrate-copy (no GPU); writes profiles/hbm_traffic_<workload>.txt")
+    ap.add_argument("--counter-summary", nargs=5,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "SQ_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
+                    help="per-kernel HBM GB/s and MFMA busy share from rocprofv3 --pmc runs (no GPU); writes "
+                         "profiles/kernel_counters_<workload>.txt")
     args = ap.parse_args()
+    if args.counter_summary:
+        counter_summary(args, *args.counter_summary)
+        return
     if args.rocprof_summary:
         print(rocprof_summary(args.rocprof_summary))
         return
