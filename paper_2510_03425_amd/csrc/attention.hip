@@ -203,6 +203,11 @@ DEV f32x16 mfma32_f16(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
+DEV f32x16 mfma32_bf16(uint4 a, uint4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0,
+                                                 0);
+}
+
 template <int DH, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
   constexpr int NTH = 64 * NW, KB = 64, LDK = DH + 8, LDV = KB + 8;
@@ -589,6 +594,198 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
   }
 }
 
+
+// dK, dV with 32-key waves (v_mfma_f32_32x32x16). Each wave keeps its 32 keys' K (fp16)
+// and V (bf16) as B operands in registers and its dK^T, dV^T accumulators for all head
+// dims; the workgroup walks the query tiles (32 queries) that can see its keys. Per tile:
+// S = Q K^T and dP = dO V^T put one key per lane column and 16 queries in its registers
+// (queries 8(r/4) + 4h + r%4), P = exp(S - lse) and dS = P (dP - delta) read the row
+// statistics from LDS, and dV^T += dO^T P, dK^T += Q^T dS take P, dS straight from
+// registers as B operands (queries {4h..4h+3, 8+4h..8+4h+3} of a 16-query step) with the
+// dO^T / Q^T fragments read in the same query order. Q and dO are staged row-major (Q
+// fp16 for the scores, dO bf16) and transposed (bf16) from 8x8 register blocks; the next
+// tile is loaded into registers while the current one is multiplied. With grouped-query
+// attention every query head stores fp32 partials that k_attn_dkdv_reduce sums in head
+// order; otherwise the epilogue scales dK, applies the RoPE backward and stores bf16.
+template <int DH, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, float* part) {
+  constexpr int NTH = 64 * NW, QB = 32, LDN = DH + 8, LDT = QB + 8;
+  constexpr int NKS = DH / 16, NTO = DH / 32;
+  constexpr int NBT = (QB / 8) * (DH / 8);   // 8x8 blocks per tensor (Q, dO) and tile
+  constexpr int BPT = (2 * NBT + NTH - 1) / NTH;
+  __shared__ __attribute__((aligned(16))) u16 Qs[QB * LDN];   // fp16 [q][e]
+  __shared__ __attribute__((aligned(16))) u16 dOs[QB * LDN];  // bf16 [q][e]
+  __shared__ __attribute__((aligned(16))) u16 Qt[DH * LDT];   // bf16 [e][q]
+  __shared__ __attribute__((aligned(16))) u16 dOt[DH * LDT];  // bf16 [e][q]
+  __shared__ __attribute__((aligned(16))) float lse_s[QB], del_s[QB];
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), hl = lane >> 5;
+  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
+  const int k0 = blockIdx.x * (32 * NW), kw = k0 + 32 * w, key = kw + (lane & 31);
+  const float sc = LOG2E / sqrtf((float)DH);
+  const size_t rowb = (size_t)b * T;
+
+  uint4 kf[NKS], vf[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const size_t off = (rowb + key) * a.ldk + kvh * DH + 16 * ks + 8 * hl;
+    kf[ks] = load_frag_global(a.k + off, key < T);
+    vf[ks] = f16x8_to_bf16x8(load_frag_global(a.v + off, key < T));
+  }
+  f32x16 dk[NTO], dv[NTO];
+#pragma unroll
+  for (int t = 0; t < NTO; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dk[t][r] = dv[t][r] = 0.f;
+
+  const int q_lo = k0 & ~(QB - 1);
+  const int q_hi = a.window ? min(T, k0 + 32 * NW - 1 + a.window) : T;
+
+  uint4 br[BPT][8];
+  float st_lse = 0.f, st_del = 0.f;
+  auto gload = [&](int qb0) {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int bl = tid + NTH * i, tens = bl / NBT, lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
+      const u16* src = tens == 0 ? (const u16*)a.q : (const u16*)a.dO;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int qq = qb0 + rb * 8 + j;
+        br[i][j] = load_frag_global(src + (rowb + qq) * a.ldq + h * DH + cb * 8, bl < 2 * NBT && qq < T);
+      }
+    }
+    if (tid < QB) {
+      const int qq = qb0 + tid;
+      const size_t si = ((size_t)b * a.Hq + h) * T + qq;
+      st_lse = qq < T ? a.lse[si] * LOG2E : 0.f;
+      st_del = qq < T ? a.delta[si] : 0.f;
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int bl = tid + NTH * i, tens = bl / NBT, lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
+      if (bl >= 2 * NBT) continue;
+      u16* nrm = tens == 0 ? Qs : dOs;
+      u16* trn = tens == 0 ? Qt : dOt;
+      uint32_t in[8][4];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        *(uint4*)(nrm + (rb * 8 + j) * LDN + cb * 8) = br[i][j];
+        const uint4 v = tens == 0 ? f16x8_to_bf16x8(br[i][j]) : br[i][j];
+        in[j][0] = v.x; in[j][1] = v.y; in[j][2] = v.z; in[j][3] = v.w;
+      }
+#pragma unroll
+      for (int jc = 0; jc < 8; ++jc) {
+        const int d = jc >> 1;
+        uint4 o;
+        if (jc & 1) {
+          o = make_uint4(perm_hi16(in[0][d], in[1][d]), perm_hi16(in[2][d], in[3][d]), perm_hi16(in[4][d], in[5][d]),
+                         perm_hi16(in[6][d], in[7][d]));
+        } else {
+          o = make_uint4(perm_lo16(in[0][d], in[1][d]), perm_lo16(in[2][d], in[3][d]), perm_lo16(in[4][d], in[5][d]),
+                         perm_lo16(in[6][d], in[7][d]));
+        }
+        *(uint4*)(trn + (cb * 8 + jc) * LDT + rb * 8) = o;
+      }
+    }
+    if (tid < QB) {
+      lse_s[tid] = st_lse;
+      del_s[tid] = st_del;
+    }
+  };
+
+  if (q_lo < q_hi) gload(q_lo);
+  for (int qb0 = q_lo; qb0 < q_hi; qb0 += QB) {
+    __syncthreads();  // every wave is done with the previous tile
+    sstore();
+    __syncthreads();
+    if (qb0 + QB < q_hi) gload(qb0 + QB);  // next tile in flight during this one
+    // nothing visible for this wave: all queries before its keys, or past its window
+    if (qb0 + QB - 1 < kw || (a.window && qb0 > kw + 31 + a.window - 1)) continue;
+    f32x16 sv, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sv[r] = dp[r] = 0.f;
+    {
+      const u16* qp = Qs + (lane & 31) * LDN + 8 * hl;
+      const u16* op = dOs + (lane & 31) * LDN + 8 * hl;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        sv = mfma32_f16(*(const uint4*)(qp + 16 * ks), kf[ks], sv);
+        dp = mfma32_bf16(*(const uint4*)(op + 16 * ks), vf[ks], dp);
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 l4 = *(const float4*)(lse_s + 8 * g + 4 * hl), d4 = *(const float4*)(del_s + 8 * g + 4 * hl);
+      const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dl[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int r = 4 * g + rr, qq = qb0 + 8 * g + 4 * hl + rr;
+        const bool vis = key <= qq && qq < T && key < T && (a.window == 0 || qq - key < a.window);
+        const float p = vis ? exp2f(sv[r] * sc - lv[rr]) : 0.f;
+        sv[r] = p;
+        dp[r] = p * (dp[r] - dl[rr]);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int r0 = 8 * kk;
+      const uint4 pf = make_uint4(pack_bf16x2(sv[r0 + 0], sv[r0 + 1]), pack_bf16x2(sv[r0 + 2], sv[r0 + 3]),
+                                  pack_bf16x2(sv[r0 + 4], sv[r0 + 5]), pack_bf16x2(sv[r0 + 6], sv[r0 + 7]));
+      const uint4 df = make_uint4(pack_bf16x2(dp[r0 + 0], dp[r0 + 1]), pack_bf16x2(dp[r0 + 2], dp[r0 + 3]),
+                                  pack_bf16x2(dp[r0 + 4], dp[r0 + 5]), pack_bf16x2(dp[r0 + 6], dp[r0 + 7]));
+#pragma unroll
+      for (int t = 0; t < NTO; ++t) {
+        const int rowoff = (t * 32 + (lane & 31)) * LDT + kk * 16 + 4 * hl;
+        const uint2 o0 = *(const uint2*)(dOt + rowoff), o1 = *(const uint2*)(dOt + rowoff + 8);
+        dv[t] = mfma32_bf16(make_uint4(o0.x, o0.y, o1.x, o1.y), pf, dv[t]);
+        const uint2 q0v = *(const uint2*)(Qt + rowoff), q1v = *(const uint2*)(Qt + rowoff + 8);
+        dk[t] = mfma32_bf16(make_uint4(q0v.x, q0v.y, q1v.x, q1v.y), df, dk[t]);
+      }
+    }
+  }
+  if (key >= T) return;
+  // lane holds dK^T, dV^T rows e = 32t + 8g + 4h + rr of key `key`
+  if (grp > 1) {
+    const size_t plane = (size_t)a.B * T * a.Hkv * DH;
+    const size_t o = (rowb + key) * (size_t)(a.Hkv * DH) + kvh * DH;
+#pragma unroll
+    for (int t = 0; t < NTO; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int e0 = 32 * t + 8 * g + 4 * hl;
+        *(float4*)(part + (size_t)hh * plane + o + e0) =
+            make_float4(dk[t][4 * g], dk[t][4 * g + 1], dk[t][4 * g + 2], dk[t][4 * g + 3]);
+        *(float4*)(part + (size_t)(grp + hh) * plane + o + e0) =
+            make_float4(dv[t][4 * g], dv[t][4 * g + 1], dv[t][4 * g + 2], dv[t][4 * g + 3]);
+      }
+    return;
+  }
+  const float scale = 1.0f / sqrtf((float)DH);
+  constexpr int half = DH / 2;
+  bf16* dvr = a.dv + (rowb + key) * a.ldk + kvh * DH;
+  bf16* dkr = a.dk + (rowb + key) * a.ldk + kvh * DH;
+#pragma unroll
+  for (int t = 0; t < NTO / 2; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int e0 = 32 * t + 8 * g + 4 * hl;
+      float lo[4], hi[4];
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const float2 cs = *(const float2*)(a.cs + 2 * ((size_t)key * half + e0 + rr));
+        const float d1 = dk[t][4 * g + rr] * scale, d2 = dk[t + NTO / 2][4 * g + rr] * scale;
+        lo[rr] = d1 * cs.x + d2 * cs.y;
+        hi[rr] = d2 * cs.x - d1 * cs.y;
+      }
+      *(uint2*)(dkr + e0) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+      *(uint2*)(dkr + e0 + half) = make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
+      *(uint2*)(dvr + e0) = make_uint2(pack_bf16x2(dv[t][4 * g], dv[t][4 * g + 1]), pack_bf16x2(dv[t][4 * g + 2], dv[t][4 * g + 3]));
+      *(uint2*)(dvr + e0 + half) = make_uint2(pack_bf16x2(dv[t + NTO / 2][4 * g], dv[t + NTO / 2][4 * g + 1]),
+                                              pack_bf16x2(dv[t + NTO / 2][4 * g + 2], dv[t + NTO / 2][4 * g + 3]));
+    }
+}
+
 // dK/dV of grouped-query attention: sum the per-head partials of each KV head in head
 // order, scale dK by 1/sqrt(dh), rotate it back (RoPE backward), store bf16. One thread
 // per (token, kv head, 4 columns of the first half of the head) and their partners.
@@ -700,16 +897,23 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
     if ((e = hipStreamWaitEvent(aux, ev_go, 0)) != hipSuccess) return e;
   }
   switch (a.dh) {
+    case 64: MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, sq, a)); break;
+    case 128: MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, sq, a)); break;
+    case 256: MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, sq, a)); break;
+    default: return hipErrorInvalidValue;
+  }
+  // head dim 128: 32-key waves (four per workgroup). Head dim 64 keeps the 16-key kernel,
+  // which is faster at the short sequences that use it, and 256 too: there dK^T and dV^T
+  // alone fill the accumulation registers.
+  if (a.dh == 128) {
+    const dim3 gkv32((a.T + 127) / 128, a.Hq, a.B);
+    MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io,
+               hipLaunchKernelGGL((k_attn_bwd_kv32<128, 4>), gkv32, dim3(256), 0, st, a, sc.part));
+  } else switch (a.dh) {
     case 64:
-      MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, sq, a));
       MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, sc.part));
       break;
-    case 128:
-      MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, sq, a));
-      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<128, 64>), gkv, dim3(256), 0, st, a, sc.part));
-      break;
     case 256:
-      MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, sq, a));
       MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, sc.part));
       break;
     default: return hipErrorInvalidValue;

@@ -120,6 +120,42 @@ def test_layer_backward_parity(built_lib, gpu, name, layer, norm):
         assert e <= TOL, (k, e)
 
 
+# Attention head dims 128 and 256, multi-head (one query head per KV head) and grouped-query,
+# at a ragged length (T = 200: not a multiple of the 32/64/128-row attention tiles) and with
+# a sliding-window layer (0) and a global layer (1).
+HEAD_DIM_CASES = {
+    "dh128_mha": MINI.with_(name="dh128_mha", hidden=256, n_heads=2, n_kv_heads=2, head_dim=128, seq=200),
+    "dh128_gqa": MINI.with_(name="dh128_gqa", hidden=256, n_heads=4, n_kv_heads=1, head_dim=128, seq=200),
+    "dh256_mha": MINI.with_(name="dh256_mha", hidden=256, n_heads=2, n_kv_heads=2, head_dim=256, seq=200),
+    "dh256_gqa": MINI.with_(name="dh256_gqa", hidden=256, n_heads=4, n_kv_heads=2, head_dim=256, seq=200),
+}
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+@pytest.mark.parametrize("name", list(HEAD_DIM_CASES))
+def test_layer_head_dims_parity(built_lib, gpu, name, layer):
+    cfg = HEAD_DIM_CASES[name]
+    inp = make_inputs(cfg, seed=7, norm="random")
+    x, dy = layer_input(cfg, 107)
+    dm = _dm(inp, gpu)
+    tx, tdy = torch.from_numpy(x).to(gpu), torch.from_numpy(dy).to(gpu)
+    ty, tdx = torch.empty_like(tx), torch.empty_like(tx)
+    say("head-dim case", name, "layer", layer, "window", cfg.layer_window(layer))
+    dm.layer_forward(layer, tx, ty)
+    dm.layer_backward(layer, tx, tdy, tdx)
+    torch.cuda.synchronize()
+    P = O.decompress_layer(cfg, inp, layer)
+    y_ref = O.layer_forward(cfg, layer, P, x)
+    dx_ref, grads = O.layer_backward(cfg, layer, P, x, dy)
+    errs = {"y": rel_l2(to_np(ty), y_ref), "dx": rel_l2(to_np(tdx), dx_ref)}
+    for p, (dA, dB) in grads.items():
+        errs["dA_" + p] = rel_l2(to_np(dm.dA[layer][p]), dA)
+        errs["dB_" + p] = rel_l2(to_np(dm.dB[layer][p]), dB)
+    say("rel-L2", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL, (k, e)
+
+
 def test_dx_may_alias_dy(built_lib, gpu):
     cfg, inp, x, dy, dm = _layer_setup("mini", 0, "random", gpu)
     tx = torch.from_numpy(x).to(gpu)
