@@ -154,7 +154,9 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
     mx(tn_part(M, D, {FF, FF}));
     mx(tn_part(M, Q, {D}));
     mx(tn_part(M, D, {Q, KV, KV}));
-    mx(attn_bwd_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim));
+    // attention scratch for the sliding-window layers and the global ones
+    mx(attn_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim, c->window));
+    mx(attn_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim, 0));
     L->split_floats = m;
     sz[S_SPLIT] = m * 4;
     size_t lp = 0;
@@ -480,7 +482,7 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   at.B = x.B; at.T = x.T; at.Hq = c->n_heads; at.Hkv = c->n_kv_heads; at.dh = c->head_dim;
   at.window = is_global(c, l) ? 0 : c->window;
   at.o = o; at.lse = xs<float>(x, S_LSE);
-  HIP_TRY(launch_attn_fwd(at, x.st));
+  HIP_TRY(launch_attn_fwd(at, scratch(x), x.st));
   HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}, &lr));
   {
     // h = x + o-projection, then c = RMSNorm(h)

@@ -22,6 +22,8 @@
 //            angle) is applied in both epilogues before the bf16 store.
 #include <stdlib.h>
 
+#include <algorithm>
+
 #include "device_common.h"
 #include "mebp_internal.h"
 
@@ -30,56 +32,95 @@ namespace {
 
 constexpr float LOG2E = 1.4426950408889634f;
 
-// Row-major tile [R][C] of bf16 from global (row pitch ld, rows beyond `rows_ok` zero)
-// into LDS dst[R][C + pad]; 8-element chunks.
 typedef uint16_t u16;
 
-// CONV: convert fp16 source elements to bf16 while staging.
-template <int R, int C, int LD, bool CONV = false>
-DEV void load_tile_n(const u16* src, size_t ld, int rows_ok, u16* dst, int tid, int nthr) {
-  constexpr int CH = C / 8;
-  for (int i = tid; i < R * CH; i += nthr) {
-    const int r = i / CH, c = (i % CH) * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < rows_ok) v = *(const uint4*)(src + (size_t)r * ld + c);
-    if (CONV) v = f16x8_to_bf16x8(v);
-    *(uint4*)(dst + r * LD + c) = v;
-  }
-}
+DEV uint4 load_frag_global(const void* p, bool ok) { return ok ? *(const uint4*)p : make_uint4(0, 0, 0, 0); }
 
-// Transposed: global [R][C] -> LDS dst[C][R + pad]; each thread moves 8x8 blocks.
-template <int R, int C, int LD, bool CONV = false>
-DEV void load_tile_t(const u16* src, size_t ld, int rows_ok, u16* dst, int tid, int nthr) {
-  constexpr int RB = R / 8, CB = C / 8;
-  for (int b = tid; b < RB * CB; b += nthr) {
-    const int rb = b % RB, cb = b / RB;
-    uint32_t in[8][4];
+// Tile staging through registers: load() issues every global load of a tile at once (rows
+// at or past `rows_ok` read as zero), the store functions write it to LDS. Kernels load
+// the next tile before the products of the current one and store it after them, so the
+// global-memory latency overlaps the MFMA work.
+//
+// Row chunks of an R x C tile of 16-bit values: chunk c is row c / (C/8), columns
+// 8 (c % (C/8)) .. +8; thread t holds chunks t, t + NTH, ...
+template <int R, int C, int NTH>
+struct StageN {
+  static constexpr int CH = C / 8, NC = R * CH, N = (NC + NTH - 1) / NTH;
+  uint4 v[N];
+  __device__ __forceinline__ void load(const u16* src, size_t ld, int rows_ok, int tid) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int r = rb * 8 + i;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (r < rows_ok) v = *(const uint4*)(src + (size_t)r * ld + cb * 8);
-      if (CONV) v = f16x8_to_bf16x8(v);
-      in[i][0] = v.x; in[i][1] = v.y; in[i][2] = v.z; in[i][3] = v.w;
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      uint4 o;
-      if (j & 1) {
-        o.x = perm_hi16(in[0][j >> 1], in[1][j >> 1]);
-        o.y = perm_hi16(in[2][j >> 1], in[3][j >> 1]);
-        o.z = perm_hi16(in[4][j >> 1], in[5][j >> 1]);
-        o.w = perm_hi16(in[6][j >> 1], in[7][j >> 1]);
-      } else {
-        o.x = perm_lo16(in[0][j >> 1], in[1][j >> 1]);
-        o.y = perm_lo16(in[2][j >> 1], in[3][j >> 1]);
-        o.z = perm_lo16(in[4][j >> 1], in[5][j >> 1]);
-        o.w = perm_lo16(in[6][j >> 1], in[7][j >> 1]);
-      }
-      *(uint4*)(dst + (cb * 8 + j) * LD + rb * 8) = o;
+    for (int i = 0; i < N; ++i) {
+      const int c = tid + NTH * i, r = c / CH, col = (c % CH) * 8;
+      v[i] = load_frag_global(src + (size_t)r * ld + col, c < NC && r < rows_ok);
     }
   }
-}
+  // CONV: fp16 source values stored as bf16
+  template <bool CONV>
+  __device__ __forceinline__ void store(u16* dst, int LD, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int c = tid + NTH * i, r = c / CH, col = (c % CH) * 8;
+      if (c < NC) *(uint4*)(dst + r * LD + col) = CONV ? f16x8_to_bf16x8(v[i]) : v[i];
+    }
+  }
+};
+
+// 8 x 8 blocks of an R x C tile: block b covers rows 8 (b % RB) .. +8 and columns
+// 8 (b / RB) .. +8, so one load feeds a row-major copy (store_n) and a transposed copy
+// dst[col][row] (store_t) of the tile.
+template <int R, int C, int NTH>
+struct StageB {
+  static constexpr int RB = R / 8, CB = C / 8, NB = RB * CB, N = (NB + NTH - 1) / NTH;
+  uint4 v[N][8];
+  __device__ __forceinline__ void load(const u16* src, size_t ld, int rows_ok, int tid) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int b = tid + NTH * i, rb = b % RB, cb = b / RB;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int r = rb * 8 + j;
+        v[i][j] = load_frag_global(src + (size_t)r * ld + cb * 8, b < NB && r < rows_ok);
+      }
+    }
+  }
+  template <bool CONV>
+  __device__ __forceinline__ void store_n(u16* dst, int LD, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int b = tid + NTH * i, rb = b % RB, cb = b / RB;
+      if (b >= NB) continue;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) *(uint4*)(dst + (rb * 8 + j) * LD + cb * 8) = CONV ? f16x8_to_bf16x8(v[i][j]) : v[i][j];
+    }
+  }
+  template <bool CONV>
+  __device__ __forceinline__ void store_t(u16* dst, int LD, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int b = tid + NTH * i, rb = b % RB, cb = b / RB;
+      if (b >= NB) continue;
+      uint32_t in[8][4];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint4 x = CONV ? f16x8_to_bf16x8(v[i][j]) : v[i][j];
+        in[j][0] = x.x; in[j][1] = x.y; in[j][2] = x.z; in[j][3] = x.w;
+      }
+#pragma unroll
+      for (int jc = 0; jc < 8; ++jc) {
+        const int d = jc >> 1;
+        uint4 o;
+        if (jc & 1) {
+          o = make_uint4(perm_hi16(in[0][d], in[1][d]), perm_hi16(in[2][d], in[3][d]), perm_hi16(in[4][d], in[5][d]),
+                         perm_hi16(in[6][d], in[7][d]));
+        } else {
+          o = make_uint4(perm_lo16(in[0][d], in[1][d]), perm_lo16(in[2][d], in[3][d]), perm_lo16(in[4][d], in[5][d]),
+                         perm_lo16(in[6][d], in[7][d]));
+        }
+        *(uint4*)(dst + (cb * 8 + jc) * LD + rb * 8) = o;
+      }
+    }
+  }
+};
 
 // A/B fragment from an LDS tile stored [row][k] (k contiguous): lane l reads
 // row row0 + l%16, k0 + 8*(l/16) .. +8.
@@ -97,19 +138,40 @@ template <class Op>
 DEV uint4 pack_frag(const f32x4& t0, const f32x4& t1) {
   return make_uint4(Op::pack(t0[0], t0[1]), Op::pack(t0[2], t0[3]), Op::pack(t1[0], t1[1]), Op::pack(t1[2], t1[3]));
 }
-DEV uint4 load_frag_global(const void* p, bool ok) { return ok ? *(const uint4*)p : make_uint4(0, 0, 0, 0); }
-
 // ------------------------------------------------------------------------------ forward
+// 64 queries (4 waves of 16) of one head per workgroup, 64-key blocks. With `nck` > 0 the
+// key range of the query tile is split into chunks of `ck` keys, one per workgroup
+// (blockIdx.x = tile * nck + chunk): short sequences then still give enough workgroups
+// to fill the chip. A chunk stores its unnormalised output and its row statistics
+// (max, sum, base-2 domain) in fp32 and k_attn_fwd_combine merges the chunks in order.
 template <int DH>
-__global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
+__global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a, float* part, int nck, int ck) {
   constexpr int KB = 64, LDK = DH + 8, LDV = KB + 8, NKS = DH / 32, NT = DH / 16;
   __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDK];
   __shared__ __attribute__((aligned(16))) u16 Vt[DH * LDV];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tile = nck ? (int)blockIdx.x / nck : (int)blockIdx.x, chunk = nck ? (int)blockIdx.x % nck : 0;
   const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
-  const int q0 = blockIdx.x * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
+  const int q0 = tile * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
+
+  int kv_lo = 0;
+  if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
+  int kv_hi = min(T, q0 + 64);
+  if (nck) {
+    kv_lo += chunk * ck;
+    if (kv_lo >= kv_hi) return;  // the whole workgroup: no chunk here
+    kv_hi = min(kv_hi, kv_lo + ck);
+  }
+
+  StageN<KB, DH, 256> kst;  // K row-major (A operand of S^T = K Q^T)
+  StageB<KB, DH, 256> vst;  // V, stored transposed (A operand of O^T += V^T P^T)
+  auto gload = [&](int kv0) {
+    kst.load((const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
+    vst.load((const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
+  };
+  gload(kv_lo);
 
   uint4 qf[NKS];
 #pragma unroll
@@ -120,15 +182,12 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
   for (int t = 0; t < NT; ++t) oacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_i = -1e30f, l_i = 0.f;
 
-  int kv_lo = 0;
-  if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
-  const int kv_hi = min(T, q0 + 64);
   for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += KB) {
-    const u16* kb = (const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH;
-    const u16* vb = (const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH;
-    load_tile_n<KB, DH, LDK>(kb, a.ldk, T - kv0, Ks, tid, 256);
-    load_tile_t<KB, DH, LDV>(vb, a.ldk, T - kv0, Vt, tid, 256);
+    __syncthreads();  // every wave is done with the previous block's tiles
+    kst.template store<false>(Ks, LDK, tid);
+    vst.template store_t<false>(Vt, LDV, tid);
     __syncthreads();
+    if (kv0 + KB < kv_hi) gload(kv0 + KB);  // next block in flight during this one
     f32x4 s[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
@@ -173,19 +232,72 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) oacc[t] = mfma16_raw<OpF16>(frag_perm(Vt, LDV, t * 16, kp * 32, lane), pf, oacc[t]);
     }
-    __syncthreads();
   }
-  if (q < T) {
-    const float inv = 1.0f / l_i;
-    f16* orow = a.o + (rowb + q) * a.ldq + h * DH;
+  if (q >= T) return;
+  if (nck) {
+    // chunk partial: [B][Hq][nck][T][DH] unnormalised output, then [B][Hq][nck][T] (max, sum)
+    const size_t pr = (((size_t)b * a.Hq + h) * nck + chunk) * T + q;
+    float* op = part + pr * DH;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int e = t * 16 + 4 * (lane >> 4);
-      *(uint2*)(orow + e) = make_uint2(pack_f16x2(oacc[t][0] * inv, oacc[t][1] * inv),
-                                       pack_f16x2(oacc[t][2] * inv, oacc[t][3] * inv));
-    }
-    if ((lane >> 4) == 0) a.lse[((size_t)b * a.Hq + h) * T + q] = (m_i + log2f(l_i)) / LOG2E;
+    for (int t = 0; t < NT; ++t)
+      *(float4*)(op + t * 16 + 4 * (lane >> 4)) = make_float4(oacc[t][0], oacc[t][1], oacc[t][2], oacc[t][3]);
+    if ((lane >> 4) == 0)
+      ((float2*)(part + (size_t)a.B * a.Hq * nck * T * DH))[pr] = make_float2(m_i, l_i);
+    return;
   }
+  const float inv = 1.0f / l_i;
+  f16* orow = a.o + (rowb + q) * a.ldq + h * DH;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int e = t * 16 + 4 * (lane >> 4);
+    *(uint2*)(orow + e) = make_uint2(pack_f16x2(oacc[t][0] * inv, oacc[t][1] * inv),
+                                     pack_f16x2(oacc[t][2] * inv, oacc[t][3] * inv));
+  }
+  if ((lane >> 4) == 0) a.lse[((size_t)b * a.Hq + h) * T + q] = (m_i + log2f(l_i)) / LOG2E;
+}
+
+// Number of key chunks of `ck` keys that query tile `tile` (64 queries) of k_attn_fwd and
+// k_attn_bwd_dq visits (key blocks of KB, aligned as in those kernels).
+__host__ __device__ inline int fwd_tile_chunks(int tile, int T, int window, int KB, int ck) {
+  const int q0 = tile * 64;
+  const int lo = window ? (q0 - window + 1 > 0 ? q0 - window + 1 : 0) & ~(KB - 1) : 0;
+  const int hi = T < q0 + 64 ? T : q0 + 64;
+  return hi > lo ? (hi - lo + ck - 1) / ck : 0;
+}
+
+// Merge of the key chunks of k_attn_fwd: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c
+// with M = max_c m_c, chunks in order; also the row log-sum-exp. One thread per (batch,
+// head, query, 8 columns).
+template <int DH>
+__global__ void k_attn_fwd_combine(const AttnArgs a, const float* part, int nck, int ck) {
+  constexpr int G = DH / 8;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int T = a.T;
+  if (i >= (size_t)a.B * a.Hq * T * G) return;
+  const int g = (int)(i % G);
+  const size_t row = i / G;  // (b * Hq + h) * T + q
+  const int q = (int)(row % T);
+  const size_t bh = row / T;
+  const int h = (int)(bh % a.Hq), b = (int)(bh / a.Hq);
+  const int n = fwd_tile_chunks(q / 64, T, a.window, 64, ck);
+  const float2* ml = (const float2*)(part + (size_t)a.B * a.Hq * nck * T * DH);
+  float M = -1e30f;
+  for (int c = 0; c < n; ++c) M = fmaxf(M, ml[(bh * nck + c) * T + q].x);
+  float L = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < n; ++c) {
+    const size_t pr = (bh * nck + c) * T + q;
+    const float2 st = ml[pr];
+    const float wgt = exp2f(st.x - M);
+    L += wgt * st.y;
+    const float4 x0 = *(const float4*)(part + pr * DH + 8 * g), x1 = *(const float4*)(part + pr * DH + 8 * g + 4);
+    acc[0] += wgt * x0.x; acc[1] += wgt * x0.y; acc[2] += wgt * x0.z; acc[3] += wgt * x0.w;
+    acc[4] += wgt * x1.x; acc[5] += wgt * x1.y; acc[6] += wgt * x1.z; acc[7] += wgt * x1.w;
+  }
+  const float inv = 1.0f / L;
+  f16* orow = a.o + ((size_t)b * T + q) * a.ldq + h * DH + 8 * g;
+  *(uint4*)orow = make_uint4(pack_f16x2(acc[0] * inv, acc[1] * inv), pack_f16x2(acc[2] * inv, acc[3] * inv),
+                             pack_f16x2(acc[4] * inv, acc[5] * inv), pack_f16x2(acc[6] * inv, acc[7] * inv));
+  if (g == 0) a.lse[row] = (M + log2f(L)) / LOG2E;
 }
 
 // ------------------------------------------------------------- forward, 32-query waves
@@ -366,30 +478,39 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
 
 // ------------------------------------------------------------------------------ backward
 // delta[b][h][t] = sum_e dO[b*T+t][h*dh+e] * O[b*T+t][h*dh+e]
+// One thread per (row, head, 8 columns); the dh/8 threads of a (row, head) are
+// consecutive lanes of one wave and combine their sums with butterfly shuffles.
 __global__ void k_attn_delta(const bf16* dO, const f16* O, int ld, int B, int T, int H, int dh, float* delta) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (size_t)B * T * H) return;
-  const int h = (int)(i % H);
-  const size_t row = i / H;
-  const uint4* pa = (const uint4*)(dO + row * ld + h * dh);
-  const uint4* pb = (const uint4*)(O + row * ld + h * dh);
+  const int G = dh / 8;
+  const bool ok = i < (size_t)B * T * H * G;
+  const int c = (int)(i % G);
+  const size_t rh = i / G;
+  const int h = (int)(rh % H);
+  const size_t row = rh / H;
   float acc = 0.f;
-  for (int c = 0; c < dh / 8; ++c) {
-    const uint4 x = pa[c], y = pb[c];
+  if (ok) {
+    const uint4 x = *(const uint4*)(dO + row * ld + h * dh + 8 * c), y = *(const uint4*)(O + row * ld + h * dh + 8 * c);
     const uint32_t* xp = (const uint32_t*)&x;
     const uint32_t* yp = (const uint32_t*)&y;
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc += bf16_lo(xp[j]) * f16_lo(yp[j]) + bf16_hi(xp[j]) * f16_hi(yp[j]);
   }
-  const int b = (int)(row / T), t = (int)(row % T);
-  delta[((size_t)b * H + h) * T + t] = acc;
+  for (int m = 1; m < G; m <<= 1) acc += __shfl_xor(acc, m, 64);
+  if (ok && c == 0) {
+    const int b = (int)(row / T), t = (int)(row % T);
+    delta[((size_t)b * H + h) * T + t] = acc;
+  }
 }
 
-// dK, dV for a block of 64 keys and one query head. With grouped-query attention the
-// heads of a KV group run in separate workgroups; each stores its fp32 partial dK/dV and
-// a reduce kernel sums them in head order (deterministic).
+// dK, dV for a block of 64 keys (4 waves of 16) and one query head. The workgroup walks
+// the query tiles (QB queries) that can see its keys; with `nck` > 0 that query range is
+// split into chunks of `cq` queries, one per workgroup (blockIdx.x = key block * nck +
+// chunk). Partial results: with grouped-query attention, or with chunks, each workgroup
+// stores fp32 partial dK / dV and k_attn_dkdv_reduce sums them in (chunk, head) order
+// (deterministic); otherwise the epilogue finishes dK (scale, RoPE backward) and dV itself.
 template <int DH, int QB>
-__global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* part) {
+__global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* part, int nck, int cq) {
   constexpr int LDN = DH + 8, LDT_ = QB + 8, NKS = DH / 32, NT = DH / 16, NQT = QB / 16;
   __shared__ __attribute__((aligned(16))) u16 Qs[QB * LDN];   // fp16 (scores)
   __shared__ __attribute__((aligned(16))) u16 dOs[QB * LDN];  // bf16
@@ -397,10 +518,34 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
   __shared__ __attribute__((aligned(16))) u16 dOt[DH * LDT_]; // bf16
   __shared__ float lse_s[QB], del_s[QB];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int kblk = nck ? (int)blockIdx.x / nck : (int)blockIdx.x, chunk = nck ? (int)blockIdx.x % nck : 0;
   const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
-  const int k0 = blockIdx.x * 64, kw = k0 + 16 * w, key = kw + (lane & 15);
+  const int k0 = kblk * 64, kw = k0 + 16 * w, key = kw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
+
+  int q_lo = k0 & ~(QB - 1);
+  int q_hi = T;
+  if (a.window) q_hi = min(T, k0 + 64 + a.window - 1);
+  if (nck) {
+    q_lo += chunk * cq;
+    if (q_lo >= q_hi) return;  // the whole workgroup: no chunk here
+    q_hi = min(q_hi, q_lo + cq);
+  }
+
+  StageB<QB, DH, 256> qst, dst;  // Q and dO tiles: row-major and transposed LDS copies
+  float st_lse = 0.f, st_del = 0.f;
+  auto gload = [&](int qb0) {
+    qst.load((const u16*)a.q + (rowb + qb0) * a.ldq + h * DH, a.ldq, T - qb0, tid);
+    dst.load((const u16*)a.dO + (rowb + qb0) * a.ldq + h * DH, a.ldq, T - qb0, tid);
+    if (tid < QB) {
+      const int qq = qb0 + tid;
+      const size_t si = ((size_t)b * a.Hq + h) * T + qq;
+      st_lse = qq < T ? a.lse[si] * LOG2E : 0.f;
+      st_del = qq < T ? a.delta[si] : 0.f;
+    }
+  };
+  gload(q_lo);
 
   uint4 kf[NKS], vf[NKS];  // K fp16 (scores), V converted to bf16 (dP = dO V^T)
 #pragma unroll
@@ -415,63 +560,55 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
     dk[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     dv[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const int q_lo = k0 & ~(QB - 1);
-  int q_hi = T;
-  if (a.window) q_hi = min(T, k0 + 64 + a.window - 1);
-  {
-    for (int qb0 = q_lo; qb0 < q_hi; qb0 += QB) {
-      const u16* qsrc = (const u16*)a.q + (rowb + qb0) * a.ldq + h * DH;
-      const u16* dsrc = (const u16*)a.dO + (rowb + qb0) * a.ldq + h * DH;
-      load_tile_n<QB, DH, LDN>(qsrc, a.ldq, T - qb0, Qs, tid, 256);
-      load_tile_n<QB, DH, LDN>(dsrc, a.ldq, T - qb0, dOs, tid, 256);
-      load_tile_t<QB, DH, LDT_, true>(qsrc, a.ldq, T - qb0, Qt, tid, 256);
-      load_tile_t<QB, DH, LDT_>(dsrc, a.ldq, T - qb0, dOt, tid, 256);
-      if (tid < QB) {
-        const int qq = qb0 + tid;
-        const size_t si = ((size_t)b * a.Hq + h) * T + qq;
-        lse_s[tid] = qq < T ? a.lse[si] * LOG2E : 0.f;
-        del_s[tid] = qq < T ? a.delta[si] : 0.f;
+  for (int qb0 = q_lo; qb0 < q_hi; qb0 += QB) {
+    __syncthreads();  // every wave is done with the previous tile
+    qst.template store_n<false>(Qs, LDN, tid);
+    qst.template store_t<true>(Qt, LDT_, tid);
+    dst.template store_n<false>(dOs, LDN, tid);
+    dst.template store_t<false>(dOt, LDT_, tid);
+    if (tid < QB) {
+      lse_s[tid] = st_lse;
+      del_s[tid] = st_del;
+    }
+    __syncthreads();
+    if (qb0 + QB < q_hi) gload(qb0 + QB);  // next tile in flight during this one
+    f32x4 s[NQT], dp[NQT];
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      s[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        s[qt] = mfma16_raw<OpF16>(frag_rows(Qs, LDN, qt * 16, ks * 32, lane), kf[ks], s[qt]);
+        dp[qt] = mfma16_raw<OpBF16>(frag_rows(dOs, LDN, qt * 16, ks * 32, lane), vf[ks], dp[qt]);
       }
-      __syncthreads();
-      f32x4 s[NQT], dp[NQT];
+    }
 #pragma unroll
-      for (int qt = 0; qt < NQT; ++qt) {
-        s[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        dp[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int qt = 0; qt < NQT; ++qt)
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          s[qt] = mfma16_raw<OpF16>(frag_rows(Qs, LDN, qt * 16, ks * 32, lane), kf[ks], s[qt]);
-          dp[qt] = mfma16_raw<OpBF16>(frag_rows(dOs, LDN, qt * 16, ks * 32, lane), vf[ks], dp[qt]);
-        }
+      for (int r = 0; r < 4; ++r) {
+        const int ql = qt * 16 + 4 * (lane >> 4) + r, qq = qb0 + ql;
+        const bool vis = key <= qq && qq < T && key < T && (a.window == 0 || qq - key < a.window);
+        const float p = vis ? exp2f(s[qt][r] * sc - lse_s[ql]) : 0.f;
+        s[qt][r] = p;
+        dp[qt][r] = p * (dp[qt][r] - del_s[ql]);
       }
 #pragma unroll
-      for (int qt = 0; qt < NQT; ++qt)
+    for (int qp = 0; qp < NQT / 2; ++qp) {
+      const uint4 pf = pack_frag<OpBF16>(s[2 * qp], s[2 * qp + 1]);
+      const uint4 df = pack_frag<OpBF16>(dp[2 * qp], dp[2 * qp + 1]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int ql = qt * 16 + 4 * (lane >> 4) + r, qq = qb0 + ql;
-          const bool vis = key <= qq && qq < T && key < T && (a.window == 0 || qq - key < a.window);
-          const float p = vis ? exp2f(s[qt][r] * sc - lse_s[ql]) : 0.f;
-          s[qt][r] = p;
-          dp[qt][r] = p * (dp[qt][r] - del_s[ql]);
-        }
-#pragma unroll
-      for (int qp = 0; qp < NQT / 2; ++qp) {
-        const uint4 pf = pack_frag<OpBF16>(s[2 * qp], s[2 * qp + 1]);
-        const uint4 df = pack_frag<OpBF16>(dp[2 * qp], dp[2 * qp + 1]);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          dv[t] = mfma16_raw<OpBF16>(pf, frag_perm(dOt, LDT_, t * 16, qp * 32, lane), dv[t]);
-          dk[t] = mfma16_raw<OpBF16>(df, frag_perm(Qt, LDT_, t * 16, qp * 32, lane), dk[t]);
-        }
+      for (int t = 0; t < NT; ++t) {
+        dv[t] = mfma16_raw<OpBF16>(pf, frag_perm(dOt, LDT_, t * 16, qp * 32, lane), dv[t]);
+        dk[t] = mfma16_raw<OpBF16>(df, frag_perm(Qt, LDT_, t * 16, qp * 32, lane), dk[t]);
       }
-      __syncthreads();
     }
   }
   // epilogue: lane holds rows key kw + 4g + r, column e = 16t + lane%16
-  if (grp > 1) {
-    // grouped-query attention: store this head's fp32 partials; k_attn_dkdv_reduce sums
-    // the heads of the group in head order and finishes dK (scale, RoPE backward) and dV
+  if (grp > 1 || nck) {
+    // fp32 partials, planes [chunk][dk: heads of the group, dv: heads of the group]
     const size_t plane = (size_t)a.B * T * a.Hkv * DH;
+    float* base = part + (size_t)chunk * 2 * grp * plane;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int kk = kw + 4 * (lane >> 4) + r;
@@ -479,8 +616,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
       const size_t o = (rowb + kk) * (size_t)(a.Hkv * DH) + kvh * DH + (lane & 15);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        part[(size_t)hh * plane + o + 16 * t] = dk[t][r];
-        part[(size_t)(grp + hh) * plane + o + 16 * t] = dv[t][r];
+        base[(size_t)hh * plane + o + 16 * t] = dk[t][r];
+        base[(size_t)(grp + hh) * plane + o + 16 * t] = dv[t][r];
       }
     }
     return;
@@ -506,18 +643,43 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
   }
 }
 
-// dQ for a block of 64 queries of one head.
-template <int DH, int KB>
-__global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
+// dQ for a block of 64 queries (4 waves of 16) of one head, key blocks of KB. With
+// `nck` > 0 the key range is split into chunks of `ck` keys, one per workgroup
+// (blockIdx.x = query tile * nck + chunk), each storing its fp32 partial dQ^T rows;
+// k_attn_dq_reduce sums them in chunk order and finishes dQ (scale, RoPE backward).
+//
+// PF: the next key block is loaded into registers while the current one is multiplied.
+// Without it (head dim 256) the kernel stays within 256 registers per lane, so that two
+// workgroups share a compute unit and hide each other's load latency instead.
+template <int DH, int KB, bool PF>
+__global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a, float* part, int nck, int ck) {
   constexpr int LDN = DH + 8, LDT_ = KB + 8, NKS = DH / 32, NT = DH / 16, NKT = KB / 16;
   __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDN];   // fp16 (scores)
   __shared__ __attribute__((aligned(16))) u16 Vs[KB * LDN];   // bf16 (dP)
   __shared__ __attribute__((aligned(16))) u16 Kt[DH * LDT_];  // bf16 (dQ product)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tile = nck ? (int)blockIdx.x / nck : (int)blockIdx.x, chunk = nck ? (int)blockIdx.x % nck : 0;
   const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
-  const int q0 = blockIdx.x * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
+  const int q0 = tile * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
+
+  int kv_lo = 0;
+  if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
+  int kv_hi = min(T, q0 + 64);
+  if (nck) {
+    kv_lo += chunk * ck;
+    if (kv_lo >= kv_hi) return;  // the whole workgroup: no chunk here
+    kv_hi = min(kv_hi, kv_lo + ck);
+  }
+
+  StageB<KB, DH, 256> kst;  // K: row-major fp16 (scores) and transposed bf16 (dQ product)
+  StageN<KB, DH, 256> vst;  // V: row-major, converted to bf16
+  auto gload = [&](int kv0) {
+    kst.load((const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
+    vst.load((const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
+  };
+  if (PF) gload(kv_lo);
 
   uint4 qf[NKS], dof[NKS];  // Q fp16, dO bf16
 #pragma unroll
@@ -533,16 +695,14 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
 #pragma unroll
   for (int t = 0; t < NT; ++t) dq[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  int kv_lo = 0;
-  if (a.window) kv_lo = max(0, q0 - a.window + 1) & ~(KB - 1);
-  const int kv_hi = min(T, q0 + 64);
   for (int kv0 = kv_lo; kv0 < kv_hi; kv0 += KB) {
-    const u16* kb = (const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH;
-    const u16* vb = (const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH;
-    load_tile_n<KB, DH, LDN>(kb, a.ldk, T - kv0, Ks, tid, 256);
-    load_tile_n<KB, DH, LDN, true>(vb, a.ldk, T - kv0, Vs, tid, 256);
-    load_tile_t<KB, DH, LDT_, true>(kb, a.ldk, T - kv0, Kt, tid, 256);
+    if (!PF) gload(kv0);
+    __syncthreads();  // every wave is done with the previous block's tiles
+    kst.template store_n<false>(Ks, LDN, tid);
+    kst.template store_t<true>(Kt, LDT_, tid);
+    vst.template store<true>(Vs, LDN, tid);
     __syncthreads();
+    if (PF && kv0 + KB < kv_hi) gload(kv0 + KB);  // next block in flight during this one
     f32x4 s[NKT], dp[NKT];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt) {
@@ -569,9 +729,17 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) dq[t] = mfma16_raw<OpBF16>(frag_perm(Kt, LDT_, t * 16, kp * 32, lane), df, dq[t]);
     }
-    __syncthreads();
   }
-  if (q < T) {
+  if (q >= T) return;
+  if (nck) {
+    // chunk partial [chunk][B*T][Hq*DH], raw dQ^T sums (lane holds e = 16t + 4g + r)
+    float* pr = part + ((size_t)chunk * a.B * T + rowb + q) * (size_t)(a.Hq * DH) + h * DH;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      *(float4*)(pr + t * 16 + 4 * (lane >> 4)) = make_float4(dq[t][0], dq[t][1], dq[t][2], dq[t][3]);
+    return;
+  }
+  {
     // lane holds dQ^T rows e = 16t + 4g + r of query q; pairs (e, e + dh/2) share the lane
     const float scale = 1.0f / sqrtf((float)DH);
     const int half = DH / 2;
@@ -592,6 +760,40 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a) {
       *(uint2*)(dqr + e0 + half) = make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
     }
   }
+}
+
+// Sum of the key-chunk partials of k_attn_bwd_dq in chunk order, scale 1/sqrt(dh), RoPE
+// backward, bf16 store. One thread per (token, head, 4 columns of the first half of the
+// head) and their partners e + dh/2.
+__global__ void k_attn_dq_reduce(const AttnArgs a, const float* part, int nck, int ck, int KB) {
+  const int half = a.dh / 2, q4 = half / 4;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (size_t)a.B * a.T * a.Hq * q4) return;
+  const int e = (int)(i % q4) * 4;
+  const int h = (int)((i / q4) % a.Hq);
+  const size_t row = i / ((size_t)q4 * a.Hq);
+  const int t = (int)(row % a.T);
+  const int n = fwd_tile_chunks(t / 64, a.T, a.window, KB, ck);
+  const size_t ldp = (size_t)a.Hq * a.dh, plane = (size_t)a.B * a.T * ldp;
+  const float* p0 = part + row * ldp + h * a.dh + e;
+  float d1[4] = {0, 0, 0, 0}, d2[4] = {0, 0, 0, 0};
+  for (int c = 0; c < n; ++c) {
+    const float4 x = *(const float4*)(p0 + c * plane), y = *(const float4*)(p0 + c * plane + half);
+    d1[0] += x.x; d1[1] += x.y; d1[2] += x.z; d1[3] += x.w;
+    d2[0] += y.x; d2[1] += y.y; d2[2] += y.z; d2[3] += y.w;
+  }
+  const float scale = 1.0f / sqrtf((float)a.dh);
+  float lo[4], hi[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float2 cs = *(const float2*)(a.cs + 2 * ((size_t)t * half + e + j));
+    const float u = d1[j] * scale, v = d2[j] * scale;
+    lo[j] = u * cs.x + v * cs.y;
+    hi[j] = v * cs.x - u * cs.y;
+  }
+  bf16* dqr = a.dq + row * a.ldq + h * a.dh + e;
+  *(uint2*)dqr = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+  *(uint2*)(dqr + half) = make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
 }
 
 
@@ -786,10 +988,19 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
     }
 }
 
-// dK/dV of grouped-query attention: sum the per-head partials of each KV head in head
-// order, scale dK by 1/sqrt(dh), rotate it back (RoPE backward), store bf16. One thread
-// per (token, kv head, 4 columns of the first half of the head) and their partners.
-__global__ void k_attn_dkdv_reduce(const AttnArgs a, const float* part) {
+// Number of query chunks of `cq` queries that key block `kblk` (64 keys) of
+// k_attn_bwd_dkdv visits.
+__host__ __device__ inline int kv_block_chunks(int kblk, int T, int window, int cq) {
+  const int k0 = kblk * 64;
+  const int hi = window ? (T < k0 + 64 + window - 1 ? T : k0 + 64 + window - 1) : T;
+  return hi > k0 ? (hi - k0 + cq - 1) / cq : 0;
+}
+
+// dK/dV from the partial planes of the key-block kernels: sum the query chunks (nck > 0;
+// else one) and, within each, the query heads of the KV group, in that order; scale dK by
+// 1/sqrt(dh), rotate it back (RoPE backward), store bf16. One thread per (token, kv
+// head, 4 columns of the first half of the head) and their partners.
+__global__ void k_attn_dkdv_reduce(const AttnArgs a, const float* part, int nck, int cq) {
   const int half = a.dh / 2, q4 = half / 4;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t total = (size_t)a.B * a.T * a.Hkv * q4;
@@ -798,17 +1009,21 @@ __global__ void k_attn_dkdv_reduce(const AttnArgs a, const float* part) {
   const int kvh = (int)((i / q4) % a.Hkv);
   const size_t row = i / ((size_t)q4 * a.Hkv);
   const int t = (int)(row % a.T), grp = a.Hq / a.Hkv;
+  const int n = nck ? kv_block_chunks(t / 64, a.T, a.window, cq) : 1;
   const size_t plane = (size_t)a.B * a.T * a.Hkv * a.dh;
   const size_t o = row * (size_t)(a.Hkv * a.dh) + kvh * a.dh + e;
   float k1[4] = {0, 0, 0, 0}, k2[4] = {0, 0, 0, 0}, v1[4] = {0, 0, 0, 0}, v2[4] = {0, 0, 0, 0};
-  for (int g = 0; g < grp; ++g) {
-    const float4 a1 = *(const float4*)(part + g * plane + o), a2 = *(const float4*)(part + g * plane + o + half);
-    const float4 b1 = *(const float4*)(part + (grp + g) * plane + o);
-    const float4 b2 = *(const float4*)(part + (grp + g) * plane + o + half);
-    k1[0] += a1.x; k1[1] += a1.y; k1[2] += a1.z; k1[3] += a1.w;
-    k2[0] += a2.x; k2[1] += a2.y; k2[2] += a2.z; k2[3] += a2.w;
-    v1[0] += b1.x; v1[1] += b1.y; v1[2] += b1.z; v1[3] += b1.w;
-    v2[0] += b2.x; v2[1] += b2.y; v2[2] += b2.z; v2[3] += b2.w;
+  for (int c = 0; c < n; ++c) {
+    const float* base = part + (size_t)c * 2 * grp * plane;
+    for (int g = 0; g < grp; ++g) {
+      const float4 a1 = *(const float4*)(base + g * plane + o), a2 = *(const float4*)(base + g * plane + o + half);
+      const float4 b1 = *(const float4*)(base + (grp + g) * plane + o);
+      const float4 b2 = *(const float4*)(base + (grp + g) * plane + o + half);
+      k1[0] += a1.x; k1[1] += a1.y; k1[2] += a1.z; k1[3] += a1.w;
+      k2[0] += a2.x; k2[1] += a2.y; k2[2] += a2.z; k2[3] += a2.w;
+      v1[0] += b1.x; v1[1] += b1.y; v1[2] += b1.z; v1[3] += b1.w;
+      v2[0] += b2.x; v2[1] += b2.y; v2[2] += b2.z; v2[3] += b2.w;
+    }
   }
   const float scale = 1.0f / sqrtf((float)a.dh);
   float lo[4], hi[4];
@@ -834,17 +1049,61 @@ double visible_pairs(int T, int W) {
   return p;
 }
 
-hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st) {
-  dim3 grid((a.T + 63) / 64, a.Hq, a.B);
+namespace {
+int env_int(const char* name, int dflt) {
+  const char* e = getenv(name);
+  return e && *e ? atoi(e) : dflt;
+}
+}  // namespace
+
+// Launch plan of the attention kernels for one shape. Short sequences with few heads give
+// fewer 64-query (64-key) tiles than the chip has compute units, and each tile's loop over
+// the other axis is a serial chain; there the loop is split into chunks, one workgroup
+// each, and a merge kernel combines the chunks in a fixed order.
+AttnPlan attn_plan(int B, int T, int Hq, int Hkv, int dh, int window) {
+  // chunk lengths are whole 64-row tiles (multiples of every kernel's block)
+  static const int use32 = env_int("MEBP_ATTN32", 1), split_on = env_int("MEBP_ATTN_SPLIT", 1),
+                   CK = std::max(64, env_int("MEBP_ATTN_CK", 64) & ~63),
+                   CQ = std::max(64, env_int("MEBP_ATTN_CQ", 128) & ~63);
+  AttnPlan p{};
+  const int nt64 = (T + 63) / 64;
+  const size_t units64 = (size_t)nt64 * Hq * B;
+  p.fwd32 = use32 && (size_t)((T + 127) / 128) * Hq * B >= 256;
+  const bool split = split_on && units64 < 256 && nt64 > 1;
+  if (split && !p.fwd32) {
+    p.f_ck = CK;
+    for (int t = 0; t < nt64; ++t) p.f_nck = std::max(p.f_nck, fwd_tile_chunks(t, T, window, 64, CK));
+    // a chain of up to four key blocks costs less than the extra merge kernel
+    if (p.f_nck <= 4) p.f_nck = 0;
+  }
+  if (split) {
+    p.q_ck = CK;
+    for (int t = 0; t < nt64; ++t) p.q_nck = std::max(p.q_nck, fwd_tile_chunks(t, T, window, dh == 256 ? 32 : 64, CK));
+    if (p.q_nck <= 1) p.q_nck = 0;
+  }
+  if (split && dh != 128) {
+    p.kv_cq = CQ;
+    for (int k = 0; k < nt64; ++k) p.kv_nck = std::max(p.kv_nck, kv_block_chunks(k, T, window, CQ));
+    if (p.kv_nck <= 1) p.kv_nck = 0;
+  }
+  const size_t rows = (size_t)B * T * Hq;
+  p.fwd_floats = p.f_nck ? (size_t)p.f_nck * rows * (dh + 2) : 0;
+  p.kv_floats = (p.kv_nck || Hq > Hkv) ? (size_t)std::max(p.kv_nck, 1) * 2 * rows * dh : 0;
+  p.q_floats = p.q_nck ? (size_t)p.q_nck * rows * dh : 0;
+  return p;
+}
+
+size_t attn_part_floats(int B, int T, int Hq, int Hkv, int dh, int window) {
+  const AttnPlan p = attn_plan(B, T, Hq, Hkv, dh, window);
+  return std::max(p.fwd_floats, p.kv_floats + p.q_floats);
+}
+
+hipError_t launch_attn_fwd(const AttnArgs& a, const SplitScratch& sc, hipStream_t st) {
   const double pairs = visible_pairs(a.T, a.window) * a.Hq * a.B;
   const double flops = 4.0 * a.dh * pairs;
   const double bytes = (double)a.B * a.T * (2.0 * a.Hq * a.dh * 2 + 2.0 * a.Hkv * a.dh * 2 + a.Hq * 4);
-  static const int use32 = [] {
-    const char* e = getenv("MEBP_ATTN32");
-    return e && *e ? atoi(e) : 1;
-  }();
-  const size_t wg128 = (size_t)((a.T + 127) / 128) * a.Hq * a.B;
-  if (use32 && wg128 >= 256) {
+  const AttnPlan p = attn_plan(a.B, a.T, a.Hq, a.Hkv, a.dh, a.window);
+  if (p.fwd32) {
     // 128 queries per workgroup (4 waves of 32) when that still fills the chip
     const dim3 g2((a.T + 127) / 128, a.Hq, a.B);
 #define FWD32(D) \
@@ -858,32 +1117,51 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st) {
 #undef FWD32
     return hipGetLastError();
   }
+  if (p.f_nck && (!sc.part || sc.part_floats < p.fwd_floats)) return hipErrorInvalidValue;
+  const dim3 grid(((a.T + 63) / 64) * (p.f_nck ? p.f_nck : 1), a.Hq, a.B);
+#define FWD(D) \
+  MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<D>, grid, dim3(256), 0, st, a, sc.part, p.f_nck, p.f_ck))
   switch (a.dh) {
-    case 64: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<64>, grid, dim3(256), 0, st, a)); break;
-    case 128: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<128>, grid, dim3(256), 0, st, a)); break;
-    case 256: MEBP_TIMED(st, "attn_fwd", flops, bytes, hipLaunchKernelGGL(k_attn_fwd<256>, grid, dim3(256), 0, st, a)); break;
+    case 64: FWD(64); break;
+    case 128: FWD(128); break;
+    case 256: FWD(256); break;
     default: return hipErrorInvalidValue;
   }
+#undef FWD
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !p.f_nck) return e;
+  const size_t nc = (size_t)a.B * a.Hq * a.T * (a.dh / 8);
+  const dim3 gc((unsigned)((nc + 255) / 256));
+  const double cb = (double)p.fwd_floats * 4 + (double)a.B * a.T * a.Hq * (a.dh * 2 + 4);
+#define CMB(D) \
+  MEBP_TIMED(st, "attn_fwd_combine", 0.0, cb, hipLaunchKernelGGL(k_attn_fwd_combine<D>, gc, dim3(256), 0, st, a, (const float*)sc.part, p.f_nck, p.f_ck))
+  switch (a.dh) {
+    case 64: CMB(64); break;
+    case 128: CMB(128); break;
+    case 256: CMB(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef CMB
   return hipGetLastError();
-}
-
-size_t attn_bwd_part_floats(int B, int T, int Hq, int Hkv, int dh) {
-  return Hq > Hkv ? 2ull * B * T * Hq * dh : 0;
 }
 
 hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScratch& sc, hipStream_t st,
                            hipStream_t aux, hipEvent_t ev_go, hipEvent_t ev_done) {
   const size_t nd = (size_t)a0.B * a0.T * a0.Hq;
   MEBP_TIMED(st, "attn_delta", 0.0, (double)nd * (4.0 * a0.dh + 4),
-             hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd + 255) / 256)), dim3(256), 0, st, a0.dO,
+             hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd * (a0.dh / 8) + 255) / 256)), dim3(256), 0, st, a0.dO,
                                 (const f16*)a0.o, a0.ldq, a0.B, a0.T, a0.Hq, a0.dh, delta_ws));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   AttnArgs a = a0;
   a.delta = delta_ws;
-  dim3 gkv((a.T + 63) / 64, a.Hq, a.B), gq((a.T + 63) / 64, a.Hq, a.B);
-  if (a.Hq > a.Hkv && (!sc.part || sc.part_floats < attn_bwd_part_floats(a.B, a.T, a.Hq, a.Hkv, a.dh)))
+  const AttnPlan p = attn_plan(a.B, a.T, a.Hq, a.Hkv, a.dh, a.window);
+  if ((p.kv_floats + p.q_floats) && (!sc.part || sc.part_floats < p.kv_floats + p.q_floats))
     return hipErrorInvalidValue;
+  float* kv_part = sc.part;
+  float* q_part = sc.part + p.kv_floats;
+  const int nt64 = (a.T + 63) / 64;
+  const dim3 gkv(nt64 * (p.kv_nck ? p.kv_nck : 1), a.Hq, a.B), gq(nt64 * (p.q_nck ? p.q_nck : 1), a.Hq, a.B);
   const double pairs = visible_pairs(a.T, a.window) * a.Hq * a.B;
   // algorithmic: dV, dK and dP products in the key-block kernel, dQ in the query-block kernel
   const double f_kv = 6.0 * a.dh * pairs, f_q = 2.0 * a.dh * pairs;
@@ -896,11 +1174,22 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
     if ((e = hipEventRecord(ev_go, st)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(aux, ev_go, 0)) != hipSuccess) return e;
   }
+#define DQ(D, KB, PF) \
+  MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<D, KB, PF>), gq, dim3(256), 0, sq, a, q_part, p.q_nck, p.q_ck))
   switch (a.dh) {
-    case 64: MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<64, 64>), gq, dim3(256), 0, sq, a)); break;
-    case 128: MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<128, 64>), gq, dim3(256), 0, sq, a)); break;
-    case 256: MEBP_TIMED(sq, "attn_bwd_dq", f_q, io, hipLaunchKernelGGL((k_attn_bwd_dq<256, 32>), gq, dim3(256), 0, sq, a)); break;
+    case 64: DQ(64, 64, true); break;
+    case 128: DQ(128, 64, true); break;
+    case 256: DQ(256, 32, false); break;
     default: return hipErrorInvalidValue;
+  }
+#undef DQ
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (p.q_nck) {
+    const size_t nr = (size_t)a.B * a.T * a.Hq * (a.dh / 8);
+    MEBP_TIMED(sq, "attn_dq_reduce", 0.0, (double)p.q_floats * 4 + (double)a.B * a.T * a.Hq * a.dh * 2,
+               hipLaunchKernelGGL(k_attn_dq_reduce, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, sq, a,
+                                  (const float*)q_part, p.q_nck, p.q_ck, a.dh == 256 ? 32 : 64));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   // head dim 128: 32-key waves (four per workgroup). Head dim 64 keeps the 16-key kernel,
   // which is faster at the short sequences that use it, and 256 too: there dK^T and dV^T
@@ -908,13 +1197,15 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
   if (a.dh == 128) {
     const dim3 gkv32((a.T + 127) / 128, a.Hq, a.B);
     MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io,
-               hipLaunchKernelGGL((k_attn_bwd_kv32<128, 4>), gkv32, dim3(256), 0, st, a, sc.part));
+               hipLaunchKernelGGL((k_attn_bwd_kv32<128, 4>), gkv32, dim3(256), 0, st, a, kv_part));
   } else switch (a.dh) {
     case 64:
-      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, sc.part));
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io,
+                 hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, kv_part, p.kv_nck, p.kv_cq));
       break;
     case 256:
-      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io, hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, sc.part));
+      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io,
+                 hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, kv_part, p.kv_nck, p.kv_cq));
       break;
     default: return hipErrorInvalidValue;
   }
@@ -923,14 +1214,15 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
   if (split) {
     if ((e = hipEventRecord(ev_done, aux)) != hipSuccess) return e;
   }
-  if (a.Hq == a.Hkv) return split ? hipStreamWaitEvent(st, ev_done, 0) : hipSuccess;
-  const size_t nr = (size_t)a.B * a.T * a.Hkv * (a.dh / 8);
-  MEBP_TIMED(st, "attn_dkdv_reduce", 0.0, (double)a.B * a.T * a.Hq * a.dh * 8 + (double)a.B * a.T * a.Hkv * a.dh * 4,
-             hipLaunchKernelGGL(k_attn_dkdv_reduce, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, st, a,
-                                (const float*)sc.part));
-  e = hipGetLastError();
-  if (e != hipSuccess || !split) return e;
-  return hipStreamWaitEvent(st, ev_done, 0);
+  if (p.kv_floats) {
+    const size_t nr = (size_t)a.B * a.T * a.Hkv * (a.dh / 8);
+    MEBP_TIMED(st, "attn_dkdv_reduce", 0.0, (double)p.kv_floats * 4 + (double)a.B * a.T * a.Hkv * a.dh * 4,
+               hipLaunchKernelGGL(k_attn_dkdv_reduce, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, st, a,
+                                  (const float*)kv_part, p.kv_nck, p.kv_cq));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return split ? hipStreamWaitEvent(st, ev_done, 0) : hipSuccess;
 }
 
 }  // namespace mebp

@@ -203,14 +203,25 @@ struct AttnArgs {
   const float* cs;                               // rope table of this layer [T][dh/2][2]
   bf16* dq; bf16* dk; bf16* dv;                  // gradients (dq, dk pre-RoPE)
 };
-hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t st);
-// scratch: delta [B][Hq][T]; when Hq > Hkv, per-head dK/dV partials (2*B*T*Hq*dh floats)
-// summed over each GQA group by a reduce kernel.
-// With `aux` (and two events), the dQ kernel runs there beside dK/dV; `st` waits for it
+// Launch plan of one attention shape: which forward kernel, and the chunking of the
+// forward / dQ key loops and the dK/dV query loop when the tile grid alone would leave
+// compute units idle (0 chunks = no split). Scratch floats: forward chunk partials; dK/dV
+// partials (grouped-query heads and/or chunks); dQ chunk partials (after the dK/dV ones).
+struct AttnPlan {
+  bool fwd32;
+  int f_nck, f_ck, q_nck, q_ck, kv_nck, kv_cq;
+  size_t fwd_floats, kv_floats, q_floats;
+};
+AttnPlan attn_plan(int B, int T, int Hq, int Hkv, int dh, int window);
+// split scratch the attention of this shape needs (forward and backward use it at
+// different times)
+size_t attn_part_floats(int B, int T, int Hq, int Hkv, int dh, int window);
+hipError_t launch_attn_fwd(const AttnArgs& a, const SplitScratch& sc, hipStream_t st);
+// scratch: delta [B][Hq][T], and the partials of attn_plan in sc.
+// With `aux` (and two events), the dQ kernels run there beside dK/dV; `st` waits for them
 // before returning.
 hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, const SplitScratch& sc, hipStream_t st,
                            hipStream_t aux = nullptr, hipEvent_t ev_go = nullptr, hipEvent_t ev_done = nullptr);
-size_t attn_bwd_part_floats(int B, int T, int Hq, int Hkv, int dh);
 
 // ---------------------------------------------------------------- LM head / CE
 // lse[m], loss term per row from partial stats; loss = mean over rows with target

@@ -122,12 +122,16 @@ def test_layer_backward_parity(built_lib, gpu, name, layer, norm):
 
 # Attention head dims 128 and 256, multi-head (one query head per KV head) and grouped-query,
 # at a ragged length (T = 200: not a multiple of the 32/64/128-row attention tiles) and with
-# a sliding-window layer (0) and a global layer (1).
+# a sliding-window layer (0) and a global layer (1). These short shapes run the attention
+# loops split into chunks (few tiles per head); the last case has enough tiles to run them
+# whole.
 HEAD_DIM_CASES = {
     "dh128_mha": MINI.with_(name="dh128_mha", hidden=256, n_heads=2, n_kv_heads=2, head_dim=128, seq=200),
     "dh128_gqa": MINI.with_(name="dh128_gqa", hidden=256, n_heads=4, n_kv_heads=1, head_dim=128, seq=200),
     "dh256_mha": MINI.with_(name="dh256_mha", hidden=256, n_heads=2, n_kv_heads=2, head_dim=256, seq=200),
     "dh256_gqa": MINI.with_(name="dh256_gqa", hidden=256, n_heads=4, n_kv_heads=2, head_dim=256, seq=200),
+    # enough 64-row tiles (9 x 8 heads x 4 sequences) that no attention loop is split
+    "dh64_unsplit": MINI.with_(name="dh64_unsplit", n_heads=8, n_kv_heads=2, head_dim=64, batch=4, seq=520),
 }
 
 
