@@ -283,3 +283,26 @@ TINY = Config(name="tiny", n_layers=2, hidden=64, n_heads=4, n_kv_heads=2, head_
 MINI = Config(name="mini", n_layers=2, hidden=128, n_heads=4, n_kv_heads=2, head_dim=64, ffn=352,
               vocab=1056, act="gelu_tanh", rope_theta_global=1e6, rope_theta_local=1e4, window=96,
               global_every=2, lora_rank=16, lora_alpha=32.0, lora_modules=ALL7, batch=2, seq=160)
+
+
+def make_optimizer_inputs(cfg: Config, seed: int = 0, n_layers: Optional[int] = None):
+    """Seeded LoRA-shaped tensors for the optimizer step, per layer and adapted projection:
+    gradients ``(gA, gB)``, first moments ``(mA, mB)`` and second moments ``(vA, vB)``
+    (non-negative), all fp32. The parameters themselves are the LoRA ``A``, ``B`` of
+    ``make_inputs``."""
+    L = cfg.n_layers if n_layers is None else n_layers
+    rng = np.random.default_rng(seed)
+    r = cfg.lora_rank
+    out = []
+    for _ in range(L):
+        mods = {}
+        for p in PROJ:
+            if p not in cfg.lora_modules:
+                continue
+            o, i = cfg.proj_shape(p)
+            g = (_normal(rng, (r, i), 1e-2), _normal(rng, (o, r), 1e-2))
+            m = (_normal(rng, (r, i), 1e-3), _normal(rng, (o, r), 1e-3))
+            v = (np.abs(_normal(rng, (r, i), 1e-4)), np.abs(_normal(rng, (o, r), 1e-4)))
+            mods[p] = {"g": g, "m": m, "v": v}
+        out.append(mods)
+    return out

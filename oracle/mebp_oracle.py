@@ -478,3 +478,37 @@ def block_forward_backward(cfg, inp, l: int = 0, x=None, dy=None):
     y = layer_forward(cfg, l, P, x)
     dx, grads = layer_backward(cfg, l, P, x, dy)
     return y, dx, grads
+
+
+# ----------------------------------------------------------------------------------------
+# Optimizer on the LoRA parameters (Sec. 3, "Runtime implementation": gradients of a batch
+# by gradient accumulation, and only the LoRA weights, their gradients and the optimizer
+# state kept for the optimizer; Sec. 4.1: the optimizer is AdamW)
+# ----------------------------------------------------------------------------------------
+def grad_accumulate(acc: Optional[np.ndarray], g: np.ndarray, scale: float) -> np.ndarray:
+    """``acc + scale * g``; ``acc = None`` starts a new accumulation (``scale * g``).
+
+    With ``scale = 1/k`` over k micro-batches of equal size this is the gradient of the
+    mean loss of their union (the batch relation of the loss normalisation)."""
+    g = np.asarray(g, F64)
+    return scale * g if acc is None else np.asarray(acc, F64) + scale * g
+
+
+def adamw_step(p: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, t: int, lr: float,
+               beta1: float, beta2: float, eps: float, weight_decay: float, grad_scale: float = 1.0):
+    """One AdamW update (Adam with decoupled weight decay, Loshchilov & Hutter) of one tensor.
+
+    ``t >= 1`` is the index of this update; returns the new ``(p, m, v)``:
+        g' = grad_scale * g
+        m  = beta1 m + (1 - beta1) g'            v = beta2 v + (1 - beta2) g'^2
+        p  = p - lr (weight_decay p + m_hat / (sqrt(v_hat) + eps)),
+    with the bias-corrected moments m_hat = m / (1 - beta1^t), v_hat = v / (1 - beta2^t).
+    """
+    p, g, m, v = (np.asarray(a, F64) for a in (p, g, m, v))
+    g = grad_scale * g
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    m_hat = m / (1.0 - beta1 ** t)
+    v_hat = v / (1.0 - beta2 ** t)
+    p = p - lr * (weight_decay * p + m_hat / (np.sqrt(v_hat) + eps))
+    return p, m, v

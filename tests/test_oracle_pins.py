@@ -530,3 +530,86 @@ def test_table1_trainable_param_counts():
         alt1 = cfg.with_(lora_rank=16, lora_modules=("q", "k", "v", "o")).lora_param_count()
         alt2 = cfg.with_(lora_rank=16).lora_param_count()
         assert abs(alt1 / 1e6 - float(printed)) > 0.5 and abs(alt2 / 1e6 - float(printed)) > 0.5
+
+
+# ---------------------------------------------------------------------------------------
+# P12: optimizer step on the LoRA parameters (AdamW, gradient accumulation)
+# ---------------------------------------------------------------------------------------
+HP = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
+
+
+def test_adamw_constant_gradient_closed_form():
+    # with a constant gradient from zero moments the bias-corrected moments are exactly g
+    # and g^2, so every step moves p by lr * g / (|g| + eps) (no weight decay)
+    rng = np.random.default_rng(40)
+    p0 = rng.standard_normal(50)
+    g = rng.standard_normal(50)
+    p, m, v = p0, np.zeros(50), np.zeros(50)
+    hp = dict(HP, weight_decay=0.0)
+    for t in range(1, 8):
+        p, m, v = O.adamw_step(p, g, m, v, t, **hp)
+        np.testing.assert_allclose(p, p0 - t * hp["lr"] * g / (np.abs(g) + hp["eps"]), rtol=1e-12, atol=1e-15)
+
+
+def test_adamw_zero_gradient_is_pure_decay():
+    rng = np.random.default_rng(41)
+    p0 = rng.standard_normal(30)
+    p, m, v = p0, np.zeros(30), np.zeros(30)
+    for t in range(1, 6):
+        p, m, v = O.adamw_step(p, np.zeros(30), m, v, t, **HP)
+    np.testing.assert_allclose(p, p0 * (1 - HP["lr"] * HP["weight_decay"]) ** 5, rtol=1e-14)
+    assert not m.any() and not v.any()
+
+
+def test_adamw_matches_torch_adamw_several_steps():
+    # an independent implementation: torch.optim.AdamW in float64 on the CPU
+    import torch
+    rng = np.random.default_rng(42)
+    shape = (16, 24)
+    p0 = rng.standard_normal(shape)
+    grads = [rng.standard_normal(shape) * (0.1 + t) for t in range(6)]
+    tp = torch.tensor(p0, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.AdamW([tp], lr=HP["lr"], betas=(HP["beta1"], HP["beta2"]), eps=HP["eps"],
+                            weight_decay=HP["weight_decay"])
+    p, m, v = p0, np.zeros(shape), np.zeros(shape)
+    for t, g in enumerate(grads, start=1):
+        tp.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        p, m, v = O.adamw_step(p, g, m, v, t, **HP)
+        st = opt.state[tp]
+        np.testing.assert_allclose(p, tp.detach().numpy(), rtol=1e-13, atol=1e-15)
+        np.testing.assert_allclose(m, st["exp_avg"].numpy(), rtol=1e-13, atol=1e-15)
+        np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-13, atol=1e-15)
+
+
+def test_adamw_grad_scale_equals_scaled_gradient():
+    rng = np.random.default_rng(43)
+    p, g, m = rng.standard_normal((3, 40))
+    v = np.abs(rng.standard_normal(40))
+    a = O.adamw_step(p, g, m, v, 3, grad_scale=0.25, **HP)
+    b = O.adamw_step(p, 0.25 * g, m, v, 3, **HP)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_grad_accumulation_of_micro_batches_equals_batch_gradient():
+    # two single-sequence micro-batches accumulated with scale 1/2 give the gradient of
+    # the batch of both (mean loss over B*(T-1) targets)
+    cfg = TINY  # batch 2
+    inp = make_inputs(cfg, seed=44, norm="random")
+    full = O.train_step(cfg, inp)
+    one = cfg.with_(batch=1)
+    acc = {}
+    for b in range(2):
+        sub = make_inputs(cfg, seed=44, norm="random")
+        sub.cfg = one
+        sub.ids = inp.ids[b:b + 1]
+        res = O.train_step(one, sub)
+        for l in range(cfg.n_layers):
+            for p, (dA, dB) in res.grads[l].items():
+                acc[l, p, 0] = O.grad_accumulate(acc.get((l, p, 0)), dA, 0.5)
+                acc[l, p, 1] = O.grad_accumulate(acc.get((l, p, 1)), dB, 0.5)
+    for l in range(cfg.n_layers):
+        for p in full.grads[l]:
+            for i in range(2):
+                np.testing.assert_allclose(acc[l, p, i], full.grads[l][p][i], rtol=1e-10, atol=1e-14)
