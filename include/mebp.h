@@ -155,6 +155,43 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
                     int32_t B, int32_t T, float* ckpt, float* loss, const mebp_layer_lora_grad* grads,
                     float* dx0, void* ws, size_t ws_bytes, mebp_stream_t stream);
 
+/* ---------------- optimizer step on the LoRA parameters ------------------------------
+ * Sec. 3 ("Runtime implementation"): the gradient of a batch may be obtained by gradient
+ * accumulation over smaller inputs, and only the LoRA weights, their gradients and the
+ * optimizer state are kept for the optimizer; Sec. 4.1: the optimizer is AdamW.        */
+
+typedef struct {
+  float* A[MEBP_NPROJ];     /* [r][in] fp32, updated in place; NULL if not adapted      */
+  float* B[MEBP_NPROJ];     /* [out][r]                                                 */
+} mebp_layer_lora_state;    /* writable LoRA-shaped tensors: parameters or moments      */
+
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+  float grad_scale;         /* the gradients are multiplied by this first               */
+  int32_t step;             /* t >= 1, the index of this update (bias corrections)      */
+} mebp_adamw_hparams;
+
+/* acc = (first ? 0 : acc) + scale * grads for every adapted LoRA tensor of every layer
+ * (with scale = 1/k over k micro-batches of equal size: the gradient of their mean loss).
+ *   grads, acc  host arrays of cfg->n_layers entries; device tensors 16-byte aligned;
+ *               acc may alias grads. Enqueued on stream; returns < 0 on invalid input.  */
+int mebp_lora_grad_accumulate(const mebp_config* cfg, const mebp_layer_lora_grad* grads,
+                              const mebp_layer_lora_grad* acc, float scale, int32_t first,
+                              mebp_stream_t stream);
+
+/* One AdamW update (decoupled weight decay) of every adapted LoRA tensor of every layer,
+ * elementwise in fp32:
+ *   g = grad_scale * grad;  m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2;
+ *   p = p - lr (weight_decay p + (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)).
+ *   params, m, v  host arrays of cfg->n_layers entries, device tensors updated in place
+ *                 (callers start with m = v = 0); grads: host array, tensors read only.
+ * All device tensors 16-byte aligned and distinct. Requires 0 <= beta1, beta2 < 1,
+ * eps >= 0, step >= 1 and finite values; returns < 0 and enqueues nothing otherwise.     */
+int mebp_lora_adamw_step(const mebp_config* cfg, const mebp_layer_lora_state* params,
+                         const mebp_layer_lora_grad* grads, const mebp_layer_lora_state* m,
+                         const mebp_layer_lora_state* v, const mebp_adamw_hparams* hp,
+                         mebp_stream_t stream);
+
 /* Message for the last non-zero status returned on the calling thread ("" if none). */
 const char* mebp_last_error(void);
 

@@ -20,7 +20,7 @@ EXPORTED = (
     "mebp_workspace_bytes", "mebp_layer_forward_ckpt", "mebp_layer_recompute_backward",
     "mebp_lm_head_ce_backward", "mebp_embed", "mebp_train_step", "mebp_last_error",
     "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name", "mebp_kernel_timing",
-    "mebp_kernel_timing_report", "mebp_kernel_repeat",
+    "mebp_kernel_timing_report", "mebp_kernel_repeat", "mebp_lora_grad_accumulate", "mebp_lora_adamw_step",
 )
 
 
@@ -49,6 +49,15 @@ class MebpLayerLora(C.Structure):
 
 class MebpLayerLoraGrad(C.Structure):
     _fields_ = [("dA", C.c_void_p * NPROJ), ("dB", C.c_void_p * NPROJ)]
+
+
+class MebpLayerLoraState(C.Structure):
+    _fields_ = [("A", C.c_void_p * NPROJ), ("B", C.c_void_p * NPROJ)]
+
+
+class MebpAdamwHparams(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float), ("grad_scale", C.c_float), ("step", C.c_int32)]
 
 
 class MebpError(RuntimeError):
@@ -88,6 +97,11 @@ def lib() -> C.CDLL:
             "mebp_kernel_timing": (C.c_int, [I32, I32]),
             "mebp_kernel_timing_report": (C.c_int, [C.c_char_p, SZ]),
             "mebp_kernel_repeat": (C.c_int, [C.c_char_p, I32]),
+            "mebp_lora_grad_accumulate": (C.c_int, [cfgp, C.POINTER(MebpLayerLoraGrad), C.POINTER(MebpLayerLoraGrad),
+                                                    C.c_float, I32, P]),
+            "mebp_lora_adamw_step": (C.c_int, [cfgp, C.POINTER(MebpLayerLoraState), C.POINTER(MebpLayerLoraGrad),
+                                               C.POINTER(MebpLayerLoraState), C.POINTER(MebpLayerLoraState),
+                                               C.POINTER(MebpAdamwHparams), P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -158,6 +172,18 @@ def mebp_train_step(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt, loss, g
 
 def mebp_dequant_q4(w, rows, cols, group, out_f32, out_bf16, stream=0, check=True):
     r = lib().mebp_dequant_q4(_ref(w), rows, cols, group, out_f32, out_bf16, stream)
+    return _check(r) if check else r
+
+
+def mebp_lora_grad_accumulate(cfg, grads, acc, scale: float, first: bool, stream=0, check=True):
+    """grads, acc: ctypes arrays of MebpLayerLoraGrad (one entry per layer)."""
+    r = lib().mebp_lora_grad_accumulate(C.byref(cfg), grads, acc, scale, int(first), stream)
+    return _check(r) if check else r
+
+
+def mebp_lora_adamw_step(cfg, params, grads, m, v, hp, stream=0, check=True):
+    """params, m, v: ctypes arrays of MebpLayerLoraState; grads: of MebpLayerLoraGrad."""
+    r = lib().mebp_lora_adamw_step(C.byref(cfg), params, grads, m, v, _ref(hp), stream)
     return _check(r) if check else r
 
 

@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmebp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["api.hip", "gemm_q4.hip", "gemm_big.hip", "attention.hip", "elementwise.hip", "lora.hip", "timing.hip"]
+SOURCES = ["api.hip", "gemm_q4.hip", "gemm_big.hip", "attention.hip", "elementwise.hip", "lora.hip", "optim.hip", "timing.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
     # no packed fp32 VALU ops (v_pk_*_f32) in generated code

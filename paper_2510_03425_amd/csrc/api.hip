@@ -9,6 +9,7 @@
 #include <map>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/mebp.h"
 #include "mebp_internal.h"
@@ -926,6 +927,77 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
     }
     HIP_TRY(hipEventRecord(side->ev_bwd, x.st));
   }
+  return MEBP_OK;
+}
+
+int mebp_lora_grad_accumulate(const mebp_config* cfg, const mebp_layer_lora_grad* grads,
+                              const mebp_layer_lora_grad* acc, float scale, int32_t first, mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg))) return e;
+  if (!isfinite(scale)) return fail(MEBP_EINVAL, "scale is not finite");
+  if (!cfg->lora_mask) return MEBP_OK;
+  if (!grads || !acc) return fail(MEBP_EINVAL, "grads or acc array is NULL");
+  const Dims D = dims(cfg, 1, 1);
+  std::vector<OptSeg> segs;
+  for (int l = 0; l < cfg->n_layers; ++l)
+    for (int p = 0; p < MEBP_NPROJ; ++p) {
+      if (!(cfg->lora_mask >> p & 1)) continue;
+      const size_t n[2] = {(size_t)D.r * D.in[p], (size_t)D.out[p] * D.r};
+      float* dst[2] = {acc[l].dA[p], acc[l].dB[p]};
+      const float* src[2] = {grads[l].dA[p], grads[l].dB[p]};
+      for (int k = 0; k < 2; ++k) {
+        if (!dst[k] || !src[k]) return fail(MEBP_EINVAL, "layer %d %s: NULL tensor", l, kProjName[p]);
+        if (!aligned(dst[k], 16) || !aligned(src[k], 16))
+          return fail(MEBP_EINVAL, "layer %d %s: tensor not 16-byte aligned", l, kProjName[p]);
+        segs.push_back(OptSeg{dst[k], src[k], nullptr, nullptr, (uint32_t)(n[k] / 4)});
+      }
+    }
+  OptArgs a{};
+  HIP_TRY(launch_lora_opt(segs.data(), (int)segs.size(), a, 1, scale, first ? 1 : 0, (hipStream_t)stream));
+  return MEBP_OK;
+}
+
+int mebp_lora_adamw_step(const mebp_config* cfg, const mebp_layer_lora_state* params,
+                         const mebp_layer_lora_grad* grads, const mebp_layer_lora_state* m,
+                         const mebp_layer_lora_state* v, const mebp_adamw_hparams* hp, mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg))) return e;
+  if (!hp) return fail(MEBP_EINVAL, "hparams is NULL");
+  if (!isfinite(hp->lr) || !isfinite(hp->eps) || !isfinite(hp->weight_decay) || !isfinite(hp->grad_scale) ||
+      !(hp->beta1 >= 0.f && hp->beta1 < 1.f) || !(hp->beta2 >= 0.f && hp->beta2 < 1.f) || hp->eps < 0.f)
+    return fail(MEBP_EINVAL, "bad AdamW hyper-parameters");
+  if (hp->step < 1) return fail(MEBP_EINVAL, "step %d < 1", hp->step);
+  if (!cfg->lora_mask) return MEBP_OK;
+  if (!params || !grads || !m || !v) return fail(MEBP_EINVAL, "params, grads, m or v array is NULL");
+  const Dims D = dims(cfg, 1, 1);
+  std::vector<OptSeg> segs;
+  for (int l = 0; l < cfg->n_layers; ++l)
+    for (int p = 0; p < MEBP_NPROJ; ++p) {
+      if (!(cfg->lora_mask >> p & 1)) continue;
+      const size_t n[2] = {(size_t)D.r * D.in[p], (size_t)D.out[p] * D.r};
+      float* ps[2] = {params[l].A[p], params[l].B[p]};
+      const float* gs[2] = {grads[l].dA[p], grads[l].dB[p]};
+      float* ms[2] = {m[l].A[p], m[l].B[p]};
+      float* vs[2] = {v[l].A[p], v[l].B[p]};
+      for (int k = 0; k < 2; ++k) {
+        if (!ps[k] || !gs[k] || !ms[k] || !vs[k]) return fail(MEBP_EINVAL, "layer %d %s: NULL tensor", l, kProjName[p]);
+        if (!aligned(ps[k], 16) || !aligned(gs[k], 16) || !aligned(ms[k], 16) || !aligned(vs[k], 16))
+          return fail(MEBP_EINVAL, "layer %d %s: tensor not 16-byte aligned", l, kProjName[p]);
+        if ((const float*)ps[k] == gs[k] || ps[k] == ms[k] || ps[k] == vs[k] || ms[k] == vs[k])
+          return fail(MEBP_EINVAL, "layer %d %s: aliased optimizer tensors", l, kProjName[p]);
+        segs.push_back(OptSeg{ps[k], gs[k], ms[k], vs[k], (uint32_t)(n[k] / 4)});
+      }
+    }
+  OptArgs a{};
+  a.lr = hp->lr;
+  a.beta1 = hp->beta1;
+  a.beta2 = hp->beta2;
+  a.eps = hp->eps;
+  a.weight_decay = hp->weight_decay;
+  a.grad_scale = hp->grad_scale;
+  a.inv_bc1 = (float)(1.0 / (1.0 - pow((double)hp->beta1, (double)hp->step)));
+  a.inv_bc2 = (float)(1.0 / (1.0 - pow((double)hp->beta2, (double)hp->step)));
+  HIP_TRY(launch_lora_opt(segs.data(), (int)segs.size(), a, 0, 0.f, 0, (hipStream_t)stream));
   return MEBP_OK;
 }
 

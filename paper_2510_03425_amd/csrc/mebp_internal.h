@@ -223,6 +223,24 @@ hipError_t launch_attn_fwd(const AttnArgs& a, const SplitScratch& sc, hipStream_
 hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, const SplitScratch& sc, hipStream_t st,
                            hipStream_t aux = nullptr, hipEvent_t ev_go = nullptr, hipEvent_t ev_done = nullptr);
 
+// ---------------------------------------------------------------- optimizer
+// One LoRA tensor of an elementwise optimizer launch: n4 float4s at p (updated), g (read),
+// m, v (AdamW moments, updated; unused by accumulation). All 16-byte aligned.
+struct OptSeg {
+  float* p; const float* g; float* m; float* v;
+  uint32_t n4;
+};
+constexpr int OPT_MAXSEG = 48;
+struct OptArgs {
+  OptSeg seg[OPT_MAXSEG];
+  uint32_t blk0[OPT_MAXSEG];  // first workgroup of each segment
+  int nseg;
+  float lr, beta1, beta2, eps, weight_decay, inv_bc1, inv_bc2, grad_scale;
+};
+// mode 0: AdamW with the parameters in `a`; mode 1: p = (first ? 0 : p) + scale * g.
+hipError_t launch_lora_opt(const OptSeg* segs, int nseg, OptArgs a, int mode, float scale, int first,
+                           hipStream_t st);
+
 // ---------------------------------------------------------------- LM head / CE
 // lse[m], loss term per row from partial stats; loss = mean over rows with target
 hipError_t launch_ce_rows(const float2* stats, int ntiles, const float* tgt_logit, const int32_t* tgt,

@@ -120,3 +120,64 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(L, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         L.lib()
+
+
+def _opt_arrays(cfg, fill=0x1000):
+    """Per-layer optimizer structs whose adapted entries point at distinct fake, 16-byte
+    aligned addresses (never dereferenced: every call below fails validation first)."""
+    n = cfg.n_layers
+    arrs = [(L.MebpLayerLoraState * n)(), (L.MebpLayerLoraGrad * n)(), (L.MebpLayerLoraState * n)(),
+            (L.MebpLayerLoraState * n)()]
+    addr = fill
+    for l in range(n):
+        for i in range(L.NPROJ):
+            if not (cfg.lora_mask() >> i) & 1:
+                continue
+            for a in arrs:
+                f0, f1 = ("dA", "dB") if isinstance(a[l], L.MebpLayerLoraGrad) else ("A", "B")
+                getattr(a[l], f0)[i] = addr
+                getattr(a[l], f1)[i] = addr + 0x100
+                addr += 0x200
+    return arrs
+
+
+HP_OK = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, grad_scale=1.0, step=1)
+
+
+@pytest.mark.parametrize("bad", [dict(step=0), dict(beta1=1.0), dict(beta2=-0.1), dict(eps=-1.0),
+                                 dict(lr=float("nan")), dict(grad_scale=float("inf"))])
+def test_adamw_rejects_bad_hparams(built_lib, bad):
+    p, g, m, v = _opt_arrays(MINI)
+    hp = L.MebpAdamwHparams(**dict(HP_OK, **bad))
+    r = L.mebp_lora_adamw_step(make_config(MINI), p, g, m, v, hp, 0, check=False)
+    assert r == L.MEBP_EINVAL and L.mebp_last_error()
+
+
+def test_adamw_rejects_null_misaligned_and_aliased(built_lib):
+    c = make_config(MINI)
+    hp = L.MebpAdamwHparams(**HP_OK)
+    p, g, m, v = _opt_arrays(MINI)
+    assert L.mebp_lora_adamw_step(c, p, g, None, v, hp, 0, check=False) == L.MEBP_EINVAL
+    assert L.mebp_lora_adamw_step(c, p, g, m, v, None, 0, check=False) == L.MEBP_EINVAL
+    p[1].B[6] = 0
+    assert L.mebp_lora_adamw_step(c, p, g, m, v, hp, 0, check=False) == L.MEBP_EINVAL
+    p, g, m, v = _opt_arrays(MINI)
+    m[0].A[2] = m[0].A[2] + 4
+    assert L.mebp_lora_adamw_step(c, p, g, m, v, hp, 0, check=False) == L.MEBP_EINVAL
+    assert "aligned" in L.mebp_last_error()
+    p, g, m, v = _opt_arrays(MINI)
+    v[1].A[0] = m[1].A[0]
+    assert L.mebp_lora_adamw_step(c, p, g, m, v, hp, 0, check=False) == L.MEBP_EINVAL
+    assert "alias" in L.mebp_last_error()
+
+
+def test_grad_accumulate_rejects(built_lib):
+    c = make_config(MINI)
+    _, g, _, _ = _opt_arrays(MINI)
+    _, acc, _, _ = _opt_arrays(MINI, fill=0x900000)
+    assert L.mebp_lora_grad_accumulate(c, g, None, 0.5, True, 0, check=False) == L.MEBP_EINVAL
+    assert L.mebp_lora_grad_accumulate(c, g, acc, float("nan"), True, 0, check=False) == L.MEBP_EINVAL
+    acc[0].dB[3] = 8
+    assert L.mebp_lora_grad_accumulate(c, g, acc, 0.5, False, 0, check=False) == L.MEBP_EINVAL
+    assert C.sizeof(L.MebpAdamwHparams) == 7 * 4
+    assert C.sizeof(L.MebpLayerLoraState) == 14 * 8
