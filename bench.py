@@ -240,6 +240,149 @@ def counter_summary(args, fetch_dir, write_dir, sq_dir, cal_fetch_dir, cal_write
     print("\n".join(lines))
 
 
+def optimizer_bench(cfg, reps=20):
+    """Time mebp_lora_adamw_step over every LoRA tensor of `cfg` (fresh device tensors of the
+    adapter shapes; the update is elementwise, so the values do not matter). Returns the
+    average duration of one update (all launches) and its HBM rate at 28 bytes per
+    parameter (read p, g, m, v; write p, m, v)."""
+    import torch
+    from mebp_inputs import PROJ
+    from paper_2510_03425_amd import _lib as L
+    from paper_2510_03425_amd.device import make_config, stream_handle
+    n = cfg.n_layers
+    params, m, v = ((L.MebpLayerLoraState * n)() for _ in range(3))
+    grads = (L.MebpLayerLoraGrad * n)()
+    keep, count = [], 0
+    for l in range(n):
+        for i, p in enumerate(PROJ):
+            if p not in cfg.lora_modules:
+                continue
+            o, k = cfg.proj_shape(p)
+            for shape, fa, fg in (((cfg.lora_rank, k), "A", "dA"), ((o, cfg.lora_rank), "B", "dB")):
+                ts = [torch.randn(shape, device="cuda") * 0.01 for _ in range(3)] + [torch.zeros(shape, device="cuda")]
+                keep += ts
+                getattr(params[l], fa)[i] = ts[0].data_ptr()
+                getattr(grads[l], fg)[i] = ts[1].data_ptr()
+                getattr(m[l], fa)[i] = ts[2].data_ptr()
+                getattr(v[l], fa)[i] = ts[3].data_ptr()
+                count += shape[0] * shape[1]
+    ccfg = make_config(cfg)
+    hp = L.MebpAdamwHparams(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, grad_scale=1.0, step=1)
+    for t in range(3):
+        hp.step = t + 1
+        L.mebp_lora_adamw_step(ccfg, params, grads, m, v, hp, stream_handle())
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for t in range(reps):
+        hp.step = t + 4
+        L.mebp_lora_adamw_step(ccfg, params, grads, m, v, hp, stream_handle())
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    gbs = 28.0 * count / (us * 1e-6) / 1e9
+    return {"shape": f"{cfg.name}-shaped adapters", "params": count, "us_per_update": round(us, 2),
+            "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def experiments(cfg, seqs=(128, 256, 512, 1024, 2048, 4096)):
+    """Counterparts of the paper's sequence-length table and decompression-share table.
+
+    seq_sweep: the whole checkpointed step of `cfg`'s model at batch 1 and each sequence
+    length (the same weights; ids are the first T of one seeded draw), HIP-graph replay.
+
+    decompression: the paper's runtime decompresses each block's weights before its graph
+    runs; here decompression is folded into the GEMM operand loads instead. What the
+    separate pass would cost on this GPU is timed with the stand-alone decompression kernel
+    (int4 -> bf16 into a scratch matrix, every projection of every layer), and set against
+    the measured forward pass (every layer's mebp_layer_forward_ckpt) and backward pass
+    (every layer's mebp_layer_recompute_backward) of the fused design at the workload's
+    own batch and length. Forward and backward would each need one such pass (the backward
+    recomputes the forward from the same decompressed weights)."""
+    import torch
+    from mebp_inputs import PROJ, make_inputs
+    from paper_2510_03425_amd import _lib as L
+    from paper_2510_03425_amd.device import DeviceModel, stream_handle
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    out = {"workload": f"{cfg.name}-shaped", "seq_sweep": [], "decompression": None}
+    big = cfg.with_(batch=1, seq=max(seqs))
+    t0 = time.time()
+    inp = make_inputs(big, seed=0)
+    log(f"inputs drawn in {time.time() - t0:.1f}s")
+    for T in seqs:
+        c = cfg.with_(batch=1, seq=T)
+        inp.cfg, ids_all = c, inp.ids
+        inp.ids = ids_all[:, :T].copy()
+        dm = DeviceModel(inp, device="cuda:0")
+        inp.ids = ids_all
+        dm.train_step(None)
+        torch.cuda.synchronize()
+        s_cap = torch.cuda.Stream()
+        s_cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s_cap):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s_cap):
+                dm.train_step(None)
+        torch.cuda.current_stream().wait_stream(s_cap)
+        ms = timed(g.replay, 10 if T <= 1024 else 4)
+        out["seq_sweep"].append({"batch": 1, "seq_len": T, "ms_per_step": round(ms, 3), "tokens_per_s": round(T / ms * 1e3, 1)})
+        log(f"seq {T}: {ms:.3f} ms/step, {T / ms * 1e3:.0f} tokens/s")
+        del g, dm
+        torch.cuda.synchronize()
+    inp.cfg = big
+
+    # decompression as a separate pass, at the workload's own shape
+    inp2 = make_inputs(cfg, seed=0)
+    dm = DeviceModel(inp2, device="cuda:0")
+    Lyr = cfg.n_layers
+    biggest = max(o * i for o, i in (cfg.proj_shape(p) for p in PROJ))
+    scratch = torch.empty(biggest, dtype=torch.int16, device="cuda:0")
+
+    def decompress_all():
+        for l in range(Lyr):
+            for i, p in enumerate(PROJ):
+                o, k = cfg.proj_shape(p)
+                L.mebp_dequant_q4(dm.base[l].w[i], o, k, cfg.group, 0, scratch.data_ptr(), stream_handle())
+
+    ck = dm.alloc_ckpt()
+    dm.embed(ck[0])
+
+    def forward_all():
+        for l in range(Lyr):
+            dm.layer_forward(l, ck[l], ck[l + 1])
+
+    dy = torch.randn_like(ck[0])
+    dxb = torch.empty_like(dy)
+
+    def backward_all():
+        for l in reversed(range(Lyr)):
+            dm.layer_backward(l, ck[l], dy, dxb)
+
+    t_dec = timed(decompress_all, 5)
+    t_fwd = timed(forward_all, 3)
+    t_bwd = timed(backward_all, 3)
+    wbytes = sum(o * i for o, i in (cfg.proj_shape(p) for p in PROJ)) * Lyr
+    out["decompression"] = {
+        "batch": cfg.batch, "seq_len": cfg.seq, "weights": wbytes,
+        "separate_pass_ms": round(t_dec, 3), "separate_pass_GBps": round(wbytes * (0.5625 + 2) / (t_dec * 1e-3) / 1e9, 1),
+        "forward_ms": round(t_fwd, 3), "backward_ms": round(t_bwd, 3),
+        "share_of_forward_if_separate": round(t_dec / (t_fwd + t_dec), 4),
+        "share_of_backward_if_separate": round(t_dec / (t_bwd + t_dec), 4)}
+    log(f"decompression pass {t_dec:.3f} ms; forward {t_fwd:.3f} ms; backward {t_bwd:.3f} ms")
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,6 +402,9 @@ def main():
                     metavar=("FETCH_DIR", "WRITE_DIR", "SQ_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="per-kernel HBM GB/s and MFMA busy share from rocprofv3 --pmc runs (no GPU); writes "
                          "profiles/kernel_counters_<workload>.txt")
+    ap.add_argument("--experiments", action="store_true",
+                    help="instead of the benchmark: step time against sequence length (B = 1, T = 128 .. 4096) and "
+                         "the cost of decompressing every layer's weights as a separate pass, at --workload")
     args = ap.parse_args()
     if args.counter_summary:
         counter_summary(args, *args.counter_summary)
@@ -292,6 +438,9 @@ def main():
     from paper_2510_03425_amd.device import DeviceModel
 
     cfg = CONFIGS[args.workload]
+    if args.experiments:
+        experiments(cfg)
+        return
     t0 = time.time()
     inp = make_inputs(cfg, seed=0)
     log(f"inputs {cfg.name} drawn in {time.time() - t0:.1f}s")
@@ -421,6 +570,13 @@ def main():
             roof["all_gemms_frac"] = round(gf / gms / 1e9 / PEAK_TFLOPS_16BIT, 4)
     step_flops = algorithmic_flops(cfg)
 
+    # the optimizer step that follows a training step (AdamW over every LoRA tensor), at this
+    # workload's adapters and at the largest adapter set (Gemma3-4B shape, all 7 projections)
+    from mebp_inputs import CONFIGS
+    optim = {"bound": "hbm", "workload": optimizer_bench(cfg), "largest": optimizer_bench(CONFIGS["gemma3-4b"])}
+    log(f"adamw: {optim['workload']['us_per_update']} us per update of {optim['workload']['params']} params; "
+        f"{optim['largest']['params']} params: {optim['largest']['us_per_update']} us, {optim['largest']['achieved']} GB/s")
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle as O
@@ -464,6 +620,7 @@ def main():
         "loss": loss,
         "roofline": roof,
         "cpu_baseline": cpu,
+        "optimizer_adamw": optim,
     }
     print(json.dumps(out), flush=True)
 

@@ -230,7 +230,7 @@ struct OptSeg {
   float* p; const float* g; float* m; float* v;
   uint32_t n4;
 };
-constexpr int OPT_MAXSEG = 48;
+constexpr int OPT_MAXSEG = 80;  // keeps OptArgs (a kernel argument) under 4 KB
 struct OptArgs {
   OptSeg seg[OPT_MAXSEG];
   uint32_t blk0[OPT_MAXSEG];  // first workgroup of each segment
