@@ -380,6 +380,37 @@ def experiments(cfg, seqs=(128, 256, 512, 1024, 2048, 4096)):
         "share_of_forward_if_separate": round(t_dec / (t_fwd + t_dec), 4),
         "share_of_backward_if_separate": round(t_dec / (t_bwd + t_dec), 4)}
     log(f"decompression pass {t_dec:.3f} ms; forward {t_fwd:.3f} ms; backward {t_bwd:.3f} ms")
+
+    # checkpoints in pinned host memory through a 4-slot device ring, against the step with
+    # every checkpoint in device memory (both replayed as HIP graphs)
+    N, d, slots = cfg.n_tokens, cfg.hidden, 4
+    host = torch.empty((Lyr + 1, N, d), dtype=torch.float32).pin_memory()
+    ring = torch.empty((slots, N, d), dtype=torch.float32, device="cuda:0")
+
+    def graph_of(fn):
+        fn()
+        torch.cuda.synchronize()
+        s_cap = torch.cuda.Stream()
+        s_cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s_cap):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=s_cap):
+                fn()
+        torch.cuda.current_stream().wait_stream(s_cap)
+        return gr
+
+    g_dev = graph_of(lambda: dm.train_step(None))
+    t_dev = timed(g_dev.replay, 5)
+    g_off = graph_of(lambda: dm.train_step_offload(host, ring, None))
+    t_off = timed(g_off.replay, 5)
+    weights = sum(t.numel() * t.element_size() for t in dm.keep)
+    out["checkpoint_offload"] = {
+        "ring_slots": slots, "ms_per_step_device_ckpt": round(t_dev, 3), "ms_per_step_offload": round(t_off, 3),
+        "device_ckpt_bytes": (Lyr + 1) * N * d * 4, "device_ring_bytes": slots * N * d * 4,
+        "host_ckpt_bytes": (Lyr + 1) * N * d * 4, "weights_lora_norm_bytes": weights, "workspace_bytes": dm.ws_bytes,
+        "device_total_bytes_device_ckpt": weights + dm.ws_bytes + (Lyr + 1) * N * d * 4,
+        "device_total_bytes_offload": weights + dm.ws_bytes + slots * N * d * 4}
+    log(f"offload: {t_off:.3f} ms/step vs {t_dev:.3f} ms/step with device checkpoints")
     print(json.dumps(out), flush=True)
 
 

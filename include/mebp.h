@@ -192,6 +192,26 @@ int mebp_lora_adamw_step(const mebp_config* cfg, const mebp_layer_lora_state* pa
                          const mebp_layer_lora_state* v, const mebp_adamw_hparams* hp,
                          mebp_stream_t stream);
 
+/* Backpropagation(x) of Algorithm 1 with the checkpoints kept in host memory (Sec. 3,
+ * "Runtime implementation": the checkpoints are memory-mapped during the forward pass
+ * instead of being kept in memory). Same kernels, order and results as mebp_train_step,
+ * bit for bit; only where the checkpoints live differs. Checkpoint x_i is computed into
+ * device ring slot i % ring_slots, copied to ckpt_host[i] by a copy stream as soon as it is
+ * written, and copied back into its slot ring_slots - 1 layers before the reverse loop
+ * recomputes layer i (the last ring_slots checkpoints never leave the ring). Device memory
+ * for checkpoints drops from (L+1) to ring_slots activations of [B*T][d] fp32.
+ *   ckpt_host  [(L+1)][B*T][d] fp32 pinned host memory (hipHostMalloc; pageable memory is
+ *              refused), written; complete when the stream reaches the end of the step
+ *   ring       [ring_slots][B*T][d] fp32 device memory, 16-byte aligned (scratch)
+ *   ring_slots 4 .. 16
+ * Other arguments as mebp_train_step. Calls on one device share its copy stream and are
+ * serialised on the host.                                                              */
+int mebp_train_step_offload(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
+                            const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids, int32_t B,
+                            int32_t T, float* ckpt_host, float* ring, int32_t ring_slots, float* loss,
+                            const mebp_layer_lora_grad* grads, float* dx0, void* ws, size_t ws_bytes,
+                            mebp_stream_t stream);
+
 /* Message for the last non-zero status returned on the calling thread ("" if none). */
 const char* mebp_last_error(void);
 

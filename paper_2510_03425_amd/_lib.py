@@ -21,6 +21,7 @@ EXPORTED = (
     "mebp_lm_head_ce_backward", "mebp_embed", "mebp_train_step", "mebp_last_error",
     "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name", "mebp_kernel_timing",
     "mebp_kernel_timing_report", "mebp_kernel_repeat", "mebp_lora_grad_accumulate", "mebp_lora_adamw_step",
+    "mebp_train_step_offload",
 )
 
 
@@ -90,6 +91,9 @@ def lib() -> C.CDLL:
             "mebp_train_step": (C.c_int, [cfgp, C.POINTER(MebpQ4), C.POINTER(MebpLayerBase), P,
                                           C.POINTER(MebpLayerLora), P, I32, I32, P, P,
                                           C.POINTER(MebpLayerLoraGrad), P, P, SZ, P]),
+            "mebp_train_step_offload": (C.c_int, [cfgp, C.POINTER(MebpQ4), C.POINTER(MebpLayerBase), P,
+                                                  C.POINTER(MebpLayerLora), P, I32, I32, P, P, I32, P,
+                                                  C.POINTER(MebpLayerLoraGrad), P, P, SZ, P]),
             "mebp_last_error": (C.c_char_p, []),
             "mebp_dequant_q4": (C.c_int, [C.POINTER(MebpQ4), I32, I32, I32, P, P, P]),
             "mebp_workspace_offset": (SZ, [cfgp, I32, I32, I32]),
@@ -167,6 +171,13 @@ def mebp_train_step(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt, loss, g
                     check=True):
     r = lib().mebp_train_step(C.byref(cfg), _ref(emb), layers, norm_final, lora, ids, B, T, ckpt, loss, grads, dx0,
                               ws, ws_bytes, stream)
+    return _check(r) if check else r
+
+
+def mebp_train_step_offload(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt_host, ring, ring_slots, loss, grads,
+                            dx0, ws, ws_bytes, stream=0, check=True):
+    r = lib().mebp_train_step_offload(C.byref(cfg), _ref(emb), layers, norm_final, lora, ids, B, T, ckpt_host, ring,
+                                      ring_slots, loss, grads, dx0, ws, ws_bytes, stream)
     return _check(r) if check else r
 
 

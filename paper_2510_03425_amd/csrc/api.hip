@@ -11,6 +11,8 @@
 #include <string>
 #include <vector>
 
+#define MEBP_RING_MAX 16
+
 #include "../../include/mebp.h"
 #include "mebp_internal.h"
 
@@ -728,6 +730,190 @@ SideStream* side_stream(hipStream_t main) {
   return s;
 }
 
+// Checkpoint offload (the memory-mapped checkpoints of Sec. 3, "Runtime implementation"):
+// x_i lives in device ring slot i % R while it is computed and used; a copy stream moves
+// every checkpoint to pinned host memory as soon as it is written and brings it back into
+// its slot before the reverse loop recomputes that layer. Without it, ring = the caller's
+// full checkpoint array (slot i = x_i) and nothing is copied.
+struct Offload {
+  float* host = nullptr;  // [(L+1)][N][d] pinned host memory
+  int R = 0;              // ring slots
+  hipStream_t cp = nullptr;
+  hipEvent_t ev_in[MEBP_RING_MAX], ev_out[MEBP_RING_MAX];
+  hipEvent_t ev_go = nullptr;
+};
+
+struct OffloadStreams {
+  hipStream_t cp = nullptr;
+  hipEvent_t ev_in[MEBP_RING_MAX], ev_out[MEBP_RING_MAX], ev_go = nullptr;
+  bool ok = false;
+};
+
+OffloadStreams* offload_streams() {
+  static std::mutex mu;
+  static std::map<int, OffloadStreams*> by_dev;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> g(mu);
+  auto it = by_dev.find(dev);
+  if (it != by_dev.end()) return it->second;
+  OffloadStreams* o = new OffloadStreams();
+  bool ok = hipStreamCreateWithFlags(&o->cp, hipStreamNonBlocking) == hipSuccess &&
+            hipEventCreateWithFlags(&o->ev_go, hipEventDisableTiming) == hipSuccess;
+  for (int i = 0; ok && i < MEBP_RING_MAX; ++i)
+    ok = hipEventCreateWithFlags(&o->ev_in[i], hipEventDisableTiming) == hipSuccess &&
+         hipEventCreateWithFlags(&o->ev_out[i], hipEventDisableTiming) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  o->ok = true;
+  by_dev[dev] = o;
+  return o;
+}
+
+int train_step_impl(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
+                    const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids, int32_t B, int32_t T,
+                    float* ring, Offload* off, float* loss, const mebp_layer_lora_grad* grads, float* dx0, void* ws,
+                    mebp_stream_t stream) {
+  int e;
+  Ctx x = make_ctx(cfg, B, T, ws, stream);
+  const size_t stride = (size_t)x.D.N * x.D.d, bytes = stride * sizeof(float);
+  const int L = cfg->n_layers;
+  auto ck = [&](int i) { return ring + (off ? (size_t)(i % off->R) : (size_t)i) * stride; };
+  // x_i still in the ring after the forward loop (the last R checkpoints)
+  auto resident = [&](int i) { return !off || i > L - off->R; };
+  // D2H of checkpoint i once `after` (a stream that wrote it) has reached this point
+  auto save = [&](int i, hipStream_t after) -> int {
+    HIP_TRY(hipEventRecord(off->ev_go, after));
+    HIP_TRY(hipStreamWaitEvent(off->cp, off->ev_go, 0));
+    HIP_TRY(hipMemcpyAsync(off->host + (size_t)i * stride, ck(i), bytes, hipMemcpyDeviceToHost, off->cp));
+    HIP_TRY(hipEventRecord(off->ev_out[i % off->R], off->cp));
+    return MEBP_OK;
+  };
+  // H2D of checkpoint i into its slot once `after` is done with the slot's previous content
+  auto fetch = [&](int i, hipStream_t after) -> int {
+    HIP_TRY(hipEventRecord(off->ev_go, after));
+    HIP_TRY(hipStreamWaitEvent(off->cp, off->ev_go, 0));
+    HIP_TRY(hipMemcpyAsync(ck(i), off->host + (size_t)i * stride, bytes, hipMemcpyHostToDevice, off->cp));
+    HIP_TRY(hipEventRecord(off->ev_in[i % off->R], off->cp));
+    return MEBP_OK;
+  };
+  float* rope_g = slot<float>(ws, x.L, S_ROPE_G);
+  float* rope_l = slot<float>(ws, x.L, S_ROPE_L);
+  HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_global, rope_g, x.st));
+  HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_local, rope_l, x.st));
+  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ck(0), x.st));
+  if (off && (e = save(0, x.st))) return e;
+  SideStream* side = side_stream(x.st);
+  std::unique_lock<std::mutex> lock;
+  if (side) lock = std::unique_lock<std::mutex>(side->mu);
+  // forward loop: ckpt[l+1] = forward_l(ckpt[l]); the LoRA down-projections run on the
+  // auxiliary stream beside the base GEMMs whose finalize adds them
+  {
+    Ctx xf = x;
+    if (side) {
+      xf.aux = side->aux;
+      xf.ev_lr = side->ev_lr;
+      xf.ev_du = side->ev_du;
+    }
+    for (int l = 0; l < L; ++l) {
+      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+      // the slot of x_{l+1} last held x_{l+1-R}: its copy to the host must be done
+      if (off && l + 1 >= off->R) HIP_TRY(hipStreamWaitEvent(x.st, off->ev_out[(l + 1) % off->R], 0));
+      if ((e = layer_forward(xf, l, &layers[l], &lora[l], ck(l), ck(l + 1), rope, false))) return e;
+      if (off && (e = save(l + 1, x.st))) return e;
+    }
+  }
+  float* g = slot<float>(ws, x.L, S_GRAD);
+  // reverse loop: recompute layer l from ckpt[l], backpropagate the upstream gradient
+  Ctx top = x;
+  top.set = (L - 1) & 1;  // layer l reads bf16(dy) from set l & 1
+  bf16* dyb_top = xs<bf16>(top, S_DYB);
+  // checkpoints that left the ring come back R layers ahead: x_i returns into its slot
+  // after the backward of layer i + R (the slot's previous user), well before layer i's
+  // recompute
+  // after layer l's backward its slot is free for x_{l-R}; x_{L-R} goes into the slot of
+  // x_L, which only the LM head reads, right after the LM head
+  auto after_backward = [&](int l, hipStream_t st) -> int {
+    if (off && l - off->R >= 0) return fetch(l - off->R, st);
+    return MEBP_OK;
+  };
+  if (!side) {
+    // final linear + loss block, then the layers in reverse on the caller's stream
+    if ((e = lm_head(x, emb, norm_final, ck(L), ids, loss, g, dyb_top))) return e;
+    if (off && L - off->R >= 0 && (e = fetch(L - off->R, x.st))) return e;
+    for (int l = L - 1; l >= 0; --l) {
+      Ctx b = x;
+      b.set = l & 1;
+      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+      float* dxl = l > 0 ? g : dx0;
+      if (!resident(l)) HIP_TRY(hipStreamWaitEvent(x.st, off->ev_in[l % off->R], 0));
+      if ((e = layer_backward(b, l, &layers[l], &lora[l], ck(l), g, dxl, grads ? &grads[l] : nullptr, rope, true)))
+        return e;
+      if ((e = after_backward(l, x.st))) return e;
+    }
+  } else {
+    // Two streams: the recompute of layer l writes activation set l & 1 on the side stream
+    // (with its own split-K scratch) and may start as soon as the backward of layer l + 2,
+    // the previous user of that set, is done; the backward of layer l waits for it. The
+    // side stream's first wait is on the end of the forward loop (the checkpoints and the
+    // LM head's inputs), its last record is waited for by the caller's stream.
+    Ctx r = x;
+    r.st = side->st;
+    r.split_set = 1;
+    auto recompute = [&](int l) -> int {
+      r.set = l & 1;
+      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+      if (!resident(l)) HIP_TRY(hipStreamWaitEvent(side->st, off->ev_in[l % off->R], 0));
+      return layer_forward(r, l, &layers[l], &lora[l], ck(l), nullptr, rope, true);
+    };
+    HIP_TRY(hipEventRecord(side->ev_fwd, x.st));
+    HIP_TRY(hipStreamWaitEvent(side->st, side->ev_fwd, 0));
+    // (the LM head below is enqueued after this point on the caller's stream and overlaps
+    // the first recompute)
+    if ((e = recompute(L - 1))) return e;
+    HIP_TRY(hipEventRecord(side->ev_rec, side->st));
+    if ((e = lm_head(x, emb, norm_final, ck(L), ids, loss, g, dyb_top))) return e;
+    if (off && L - off->R >= 0 && (e = fetch(L - off->R, x.st))) return e;
+    for (int l = L - 1; l >= 0; --l) {
+      HIP_TRY(hipStreamWaitEvent(x.st, side->ev_rec, 0));  // recompute(l) done
+      if (l >= 1) {
+        // set (l - 1) & 1 was last read by the backward of layer l + 1 (or the forward loop)
+        if (l + 1 < L) HIP_TRY(hipStreamWaitEvent(side->st, side->ev_bwd, 0));
+        if ((e = recompute(l - 1))) return e;
+        HIP_TRY(hipEventRecord(side->ev_rec, side->st));
+      }
+      Ctx b = x;
+      b.set = l & 1;
+      bool aux_used = false;
+      b.aux = side->aux;
+      b.ev_lr = side->ev_lr;
+      b.ev_du = side->ev_du;
+      b.aux_used = &aux_used;
+      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
+      float* dxl = l > 0 ? g : dx0;
+      if ((e = layer_backward_only(b, l, &layers[l], &lora[l], ck(l), g, dxl, grads ? &grads[l] : nullptr, rope,
+                                   true)))
+        return e;
+      if (aux_used) {
+        // the dA / dB kernels of this layer read set l & 1, its bf16(dy) and the shared
+        // gradient slots: join them before the next layer's backward or recompute
+        HIP_TRY(hipEventRecord(side->ev_aux, side->aux));
+        HIP_TRY(hipStreamWaitEvent(x.st, side->ev_aux, 0));
+      }
+      HIP_TRY(hipEventRecord(side->ev_bwd, x.st));
+      if ((e = after_backward(l, x.st))) return e;
+    }
+  }
+  if (off) {
+    // every copy of the step is joined into the caller's stream
+    HIP_TRY(hipEventRecord(off->ev_go, off->cp));
+    HIP_TRY(hipStreamWaitEvent(x.st, off->ev_go, 0));
+  }
+  return MEBP_OK;
+}
+
 }  // namespace
 
 // ==================================================================== public entry points
@@ -813,10 +999,9 @@ int mebp_embed(const mebp_config* cfg, const mebp_q4* emb, const int32_t* ids, i
   return MEBP_OK;
 }
 
-int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
-                    const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids, int32_t B, int32_t T,
-                    float* ckpt, float* loss, const mebp_layer_lora_grad* grads, float* dx0, void* ws,
-                    size_t ws_bytes, mebp_stream_t stream) {
+int check_train_args(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
+                     const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids, int32_t B, int32_t T,
+                     float* loss, const mebp_layer_lora_grad* grads, float* dx0, void* ws, size_t ws_bytes) {
   int e;
   if ((e = check_config(cfg)) || (e = check_shape(B, T))) return e;
   if (cfg->vocab <= 0) return fail(MEBP_EINVAL, "vocab must be > 0 for a training step");
@@ -827,107 +1012,57 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
     if ((e = check_layer(cfg, l, &layers[l], &lora[l]))) return e;
     if ((e = check_grads(cfg, grads ? &grads[l] : nullptr))) return e;
   }
-  if ((e = check_q4(emb, "embedding")) || (e = check_act(norm_final, "norm_final")) || (e = check_act(ckpt, "ckpt")) ||
+  if ((e = check_q4(emb, "embedding")) || (e = check_act(norm_final, "norm_final")) ||
       (e = check_ws(cfg, B, T, ws, ws_bytes)))
     return e;
   if (dx0 && !aligned(dx0, 16)) return fail(MEBP_EINVAL, "dx0 not 16-byte aligned");
   if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
   if (!loss || !aligned(loss, 4)) return fail(MEBP_EINVAL, "loss NULL or misaligned");
-
-  Ctx x = make_ctx(cfg, B, T, ws, stream);
-  const size_t stride = (size_t)x.D.N * x.D.d;
-  float* rope_g = slot<float>(ws, x.L, S_ROPE_G);
-  float* rope_l = slot<float>(ws, x.L, S_ROPE_L);
-  HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_global, rope_g, x.st));
-  HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_local, rope_l, x.st));
-  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ckpt, x.st));
-  SideStream* side = side_stream(x.st);
-  std::unique_lock<std::mutex> lock;
-  if (side) lock = std::unique_lock<std::mutex>(side->mu);
-  // forward loop: ckpt[l+1] = forward_l(ckpt[l]); the LoRA down-projections run on the
-  // auxiliary stream beside the base GEMMs whose finalize adds them
-  {
-    Ctx xf = x;
-    if (side) {
-      xf.aux = side->aux;
-      xf.ev_lr = side->ev_lr;
-      xf.ev_du = side->ev_du;
-    }
-    for (int l = 0; l < cfg->n_layers; ++l) {
-      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
-      if ((e = layer_forward(xf, l, &layers[l], &lora[l], ckpt + l * stride, ckpt + (l + 1) * stride, rope, false)))
-        return e;
-    }
-  }
-  float* g = slot<float>(ws, x.L, S_GRAD);
-  // reverse loop: recompute layer l from ckpt[l], backpropagate the upstream gradient
-  const int L = cfg->n_layers;
-  Ctx top = x;
-  top.set = (L - 1) & 1;  // layer l reads bf16(dy) from set l & 1
-  bf16* dyb_top = xs<bf16>(top, S_DYB);
-  if (!side) {
-    // final linear + loss block, then the layers in reverse on the caller's stream
-    if ((e = lm_head(x, emb, norm_final, ckpt + L * stride, ids, loss, g, dyb_top))) return e;
-    for (int l = L - 1; l >= 0; --l) {
-      Ctx b = x;
-      b.set = l & 1;
-      const float* rope = is_global(cfg, l) ? rope_g : rope_l;
-      float* dxl = l > 0 ? g : dx0;
-      if ((e = layer_backward(b, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr,
-                              rope, true)))
-        return e;
-    }
-    return MEBP_OK;
-  }
-  // Two streams: the recompute of layer l writes activation set l & 1 on the side stream
-  // (with its own split-K scratch) and may start as soon as the backward of layer l + 2,
-  // the previous user of that set, is done; the backward of layer l waits for it. The
-  // side stream's first wait is on the end of the forward loop (the checkpoints and the
-  // LM head's inputs), its last record is waited for by the caller's stream.
-  Ctx r = x;
-  r.st = side->st;
-  r.split_set = 1;
-  auto recompute = [&](int l) -> int {
-    r.set = l & 1;
-    const float* rope = is_global(cfg, l) ? rope_g : rope_l;
-    return layer_forward(r, l, &layers[l], &lora[l], ckpt + l * stride, nullptr, rope, true);
-  };
-  HIP_TRY(hipEventRecord(side->ev_fwd, x.st));
-  HIP_TRY(hipStreamWaitEvent(side->st, side->ev_fwd, 0));
-  // (the LM head below is enqueued after this point on the caller's stream and overlaps
-  // the first recompute)
-  if ((e = recompute(L - 1))) return e;
-  HIP_TRY(hipEventRecord(side->ev_rec, side->st));
-  if ((e = lm_head(x, emb, norm_final, ckpt + L * stride, ids, loss, g, dyb_top))) return e;
-  for (int l = L - 1; l >= 0; --l) {
-    HIP_TRY(hipStreamWaitEvent(x.st, side->ev_rec, 0));  // recompute(l) done
-    if (l >= 1) {
-      // set (l - 1) & 1 was last read by the backward of layer l + 1 (or the forward loop)
-      if (l + 1 < L) HIP_TRY(hipStreamWaitEvent(side->st, side->ev_bwd, 0));
-      if ((e = recompute(l - 1))) return e;
-      HIP_TRY(hipEventRecord(side->ev_rec, side->st));
-    }
-    Ctx b = x;
-    b.set = l & 1;
-    bool aux_used = false;
-    b.aux = side->aux;
-    b.ev_lr = side->ev_lr;
-    b.ev_du = side->ev_du;
-    b.aux_used = &aux_used;
-    const float* rope = is_global(cfg, l) ? rope_g : rope_l;
-    float* dxl = l > 0 ? g : dx0;
-    if ((e = layer_backward_only(b, l, &layers[l], &lora[l], ckpt + l * stride, g, dxl, grads ? &grads[l] : nullptr,
-                                 rope, true)))
-      return e;
-    if (aux_used) {
-      // the dA / dB kernels of this layer read set l & 1, its bf16(dy) and the shared
-      // gradient slots: join them before the next layer's backward or recompute
-      HIP_TRY(hipEventRecord(side->ev_aux, side->aux));
-      HIP_TRY(hipStreamWaitEvent(x.st, side->ev_aux, 0));
-    }
-    HIP_TRY(hipEventRecord(side->ev_bwd, x.st));
-  }
   return MEBP_OK;
+}
+
+int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
+                    const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids, int32_t B, int32_t T,
+                    float* ckpt, float* loss, const mebp_layer_lora_grad* grads, float* dx0, void* ws,
+                    size_t ws_bytes, mebp_stream_t stream) {
+  int e;
+  if ((e = check_train_args(cfg, emb, layers, norm_final, lora, ids, B, T, loss, grads, dx0, ws, ws_bytes)) ||
+      (e = check_act(ckpt, "ckpt")))
+    return e;
+  return train_step_impl(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt, nullptr, loss, grads, dx0, ws, stream);
+}
+
+int mebp_train_step_offload(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
+                            const float* norm_final, const mebp_layer_lora* lora, const int32_t* ids, int32_t B,
+                            int32_t T, float* ckpt_host, float* ring, int32_t ring_slots, float* loss,
+                            const mebp_layer_lora_grad* grads, float* dx0, void* ws, size_t ws_bytes,
+                            mebp_stream_t stream) {
+  int e;
+  if ((e = check_train_args(cfg, emb, layers, norm_final, lora, ids, B, T, loss, grads, dx0, ws, ws_bytes)) ||
+      (e = check_act(ring, "ring")))
+    return e;
+  if (ring_slots < 4 || ring_slots > MEBP_RING_MAX)
+    return fail(MEBP_EINVAL, "ring_slots %d not in [4, %d]", ring_slots, MEBP_RING_MAX);
+  if (!ckpt_host || !aligned(ckpt_host, 16)) return fail(MEBP_EINVAL, "ckpt_host NULL or not 16-byte aligned");
+  hipPointerAttribute_t pa;
+  if (hipPointerGetAttributes(&pa, ckpt_host) != hipSuccess || pa.type != hipMemoryTypeHost) {
+    (void)hipGetLastError();
+    return fail(MEBP_EINVAL, "ckpt_host is not pinned host memory (allocate it with hipHostMalloc)");
+  }
+  OffloadStreams* os = offload_streams();
+  if (!os) return fail(MEBP_EHIP, "could not create the copy stream");
+  Offload off;
+  off.host = ckpt_host;
+  off.R = ring_slots;
+  off.cp = os->cp;
+  off.ev_go = os->ev_go;
+  for (int i = 0; i < MEBP_RING_MAX; ++i) {
+    off.ev_in[i] = os->ev_in[i];
+    off.ev_out[i] = os->ev_out[i];
+  }
+  static std::mutex mu;  // the copy stream and its events are shared by the calls on a device
+  std::lock_guard<std::mutex> g(mu);
+  return train_step_impl(cfg, emb, layers, norm_final, lora, ids, B, T, ring, &off, loss, grads, dx0, ws, stream);
 }
 
 int mebp_lora_grad_accumulate(const mebp_config* cfg, const mebp_layer_lora_grad* grads,

@@ -140,6 +140,15 @@ class DeviceModel:
                           self.T, ptr(ck), ptr(self.loss), self.grads, ptr(dx0), ptr(self.ws), self.ws_bytes,
                           stream_handle())
 
+    def train_step_offload(self, ckpt_host: torch.Tensor, ring: torch.Tensor, dx0: Optional[torch.Tensor] = None):
+        """The step with checkpoints in pinned host memory ``ckpt_host`` [(L+1)][N][d] and a
+        device ring ``ring`` [slots][N][d]."""
+        if self.L == 0:
+            raise ValueError("this input set has no layers")
+        L.mebp_train_step_offload(self.ccfg, self.emb, self.base, ptr(self.norm_final), self.lora, ptr(self.ids),
+                                  self.B, self.T, ptr(ckpt_host), ptr(ring), ring.shape[0], ptr(self.loss), self.grads,
+                                  ptr(dx0), ptr(self.ws), self.ws_bytes, stream_handle())
+
     def grad_probe(self) -> torch.Tensor:
         """First and last layers' LoRA gradients, concatenated (a cheap result fingerprint)."""
         parts = [t.reshape(-1) for l in {0, self.L - 1} for d in (self.dA[l], self.dB[l]) for t in d.values()]
