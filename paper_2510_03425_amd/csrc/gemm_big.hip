@@ -821,6 +821,50 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
         lora_mfma<NJ>(acc, sg.lora_du, a.r, m0 + wm * 128, a.M, 1.0f, sg.lora_A, 1, Kout, c0 + wn * 32 * NJ, Kout,
                       lane);
     }
+    if constexpr (EPI == TN_ACT_BWD && 4 * 64 * (32 * NJ + 4) * 4 <= (int)sizeof(As2)) {
+      // dz -> (dg, du) reads g, u and writes dg, du: the accumulators go through LDS so that
+      // every lane handles 4 consecutive columns of a row (8-byte accesses, a wave covers
+      // whole 128-byte row segments) instead of 2-byte accesses in the MFMA layout. Each
+      // wave stages its 128 x 32NJ block in two halves of 64 rows in its own LDS region.
+      constexpr int CW = 32 * NJ, LDE = CW + 4, CPR = CW / 4, RPP = 64 / CPR;
+      float* ep = reinterpret_cast<float*>(&As2[0][0]) + wave * 64 * LDE;
+      const int rr = lane / CPR, ch = lane % CPR;
+      const int cbase = c0 + wn * CW + 4 * ch;
+      __syncthreads();  // every wave is done with the main loop's LDS tiles
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int q = 0; q < 16; ++q)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+              ep[(32 * ii + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] =
+                  acc[2 * hh + ii][j][q];
+        __syncthreads();
+#pragma unroll 4
+        for (int pss = 0; pss < 64 / RPP; ++pss) {
+          const int r = pss * RPP + rr, m = m0 + wm * 128 + 64 * hh + r;
+          if (m >= a.M || cbase >= Kout) continue;  // Kout is a multiple of 4
+          const float4 v = *(const float4*)(ep + r * LDE + 4 * ch);
+          const size_t idx = (size_t)m * a.ldgu + cbase;
+          const uint2 gw = *(const uint2*)((const f16*)a.g + idx), uw = *(const uint2*)((const f16*)a.u + idx);
+          const float gv[4] = {f16_lo(gw.x), f16_hi(gw.x), f16_lo(gw.y), f16_hi(gw.y)};
+          const float uv[4] = {f16_lo(uw.x), f16_hi(uw.x), f16_lo(uw.y), f16_hi(uw.y)};
+          const float dz[4] = {v.x, v.y, v.z, v.w};
+          float dg[4], du[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            dg[t] = dz[t] * uv[t] * act_grad_f(gv[t], a.act);
+            du[t] = dz[t] * act_f(gv[t], a.act);
+          }
+          *(uint2*)((bf16*)a.g + idx) = make_uint2(pack_bf16x2(dg[0], dg[1]), pack_bf16x2(dg[2], dg[3]));
+          *(uint2*)((bf16*)a.u + idx) = make_uint2(pack_bf16x2(du[0], du[1]), pack_bf16x2(du[2], du[3]));
+        }
+        __syncthreads();  // before the next half overwrites the staging area
+      }
+      return;
+    }
     auto put = [&](auto FULL_) {
       constexpr bool FULL = decltype(FULL_)::value;
 #pragma unroll
