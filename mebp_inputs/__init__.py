@@ -58,6 +58,16 @@ class Config:
     lora_modules: Tuple[str, ...] = ("q", "v")
     batch: int = 1
     seq: int = 128
+    # architecture details beyond the shapes (all off: the "-shaped" models)
+    qkv_bias: bool = False  # Qwen2.5: biases on the q, k, v projections
+    qk_norm: bool = False  # Gemma3: RMSNorm over each head of q and k before RoPE
+    sandwich_norm: bool = False  # Gemma3: RMSNorm on the attention and MLP outputs before the residual
+    embed_scale: bool = False  # Gemma3: embedding output times sqrt(hidden)
+
+    @property
+    def arch_flags(self) -> int:
+        return (1 if self.qkv_bias else 0) | (2 if self.qk_norm else 0) | (4 if self.sandwich_norm else 0) | \
+            (8 if self.embed_scale else 0)
 
     @property
     def n_tokens(self) -> int:
@@ -262,6 +272,17 @@ def make_inputs(cfg: Config, seed: int = 0, norm: str = "ones", lora_b_zero: boo
     inp.norm_attn = [nw() for _ in range(L)]
     inp.norm_mlp = [nw() for _ in range(L)]
     inp.norm_final = nw() if cfg.vocab else None
+    # architecture extras, from their own stream (the draws above are unchanged): frozen
+    # fp32 vectors, like the norm weights
+    arng = np.random.default_rng(seed + 2)
+    qd, kvd, dh = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim, cfg.head_dim
+    inp.extra["bias"] = [{"q": _normal(arng, (qd,), 0.1), "k": _normal(arng, (kvd,), 0.1),
+                          "v": _normal(arng, (kvd,), 0.1)} if cfg.qkv_bias else None for _ in range(L)]
+
+    def vw(n):
+        return (1.0 + 0.1 * arng.standard_normal(n)).astype(np.float32) if norm == "random" else np.ones(n, np.float32)
+    inp.extra["qk_norm"] = [(vw(dh), vw(dh)) if cfg.qk_norm else None for _ in range(L)]
+    inp.extra["post_norm"] = [(vw(d), vw(d)) if cfg.sandwich_norm else None for _ in range(L)]
     return inp
 
 

@@ -236,6 +236,11 @@ class LayerParams:
     norm_attn: np.ndarray
     norm_mlp: np.ndarray
     lora: Dict[str, Tuple[np.ndarray, np.ndarray]]  # proj -> (A, B) fp64
+    bias: Optional[Dict[str, np.ndarray]] = None  # q, k, v biases (Qwen2.5)
+    q_norm: Optional[np.ndarray] = None  # [dh] per-head RMSNorm weights of q and k (Gemma3)
+    k_norm: Optional[np.ndarray] = None
+    post_attn_norm: Optional[np.ndarray] = None  # [d] sandwich norms (Gemma3)
+    post_mlp_norm: Optional[np.ndarray] = None
 
 
 def decompress_layer(cfg, inp, l: int) -> LayerParams:
@@ -244,7 +249,15 @@ def decompress_layer(cfg, inp, l: int) -> LayerParams:
     for p, (q4, sb) in inp.base[l].items():
         W[p] = dequant(q4, sb, cfg.proj_shape(p)[1], cfg.group)
     lora = {p: (np.asarray(A, F64), np.asarray(B, F64)) for p, (A, B) in inp.lora[l].items()}
-    return LayerParams(W, np.asarray(inp.norm_attn[l], F64), np.asarray(inp.norm_mlp[l], F64), lora)
+    P = LayerParams(W, np.asarray(inp.norm_attn[l], F64), np.asarray(inp.norm_mlp[l], F64), lora)
+    ex = inp.extra
+    if getattr(cfg, "qkv_bias", False):
+        P.bias = {p: np.asarray(b, F64) for p, b in ex["bias"][l].items()}
+    if getattr(cfg, "qk_norm", False):
+        P.q_norm, P.k_norm = (np.asarray(w, F64) for w in ex["qk_norm"][l])
+    if getattr(cfg, "sandwich_norm", False):
+        P.post_attn_norm, P.post_mlp_norm = (np.asarray(w, F64) for w in ex["post_norm"][l])
+    return P
 
 
 def _lin(P: LayerParams, p: str, x, s):
@@ -266,24 +279,43 @@ def layer_forward(cfg, l: int, P: LayerParams, x: np.ndarray, keep: bool = False
     q, uq = _lin(P, "q", a, s)
     k, uk = _lin(P, "k", a, s)
     v, uv = _lin(P, "v", a, s)
+    if P.bias is not None:  # Qwen2.5: q, k, v projections with bias
+        q, k, v = q + P.bias["q"], k + P.bias["k"], v + P.bias["v"]
+    q_pre, k_pre = q.reshape(Bsz, T, Hq, dh), k.reshape(Bsz, T, Hkv, dh)
+    rq = rk = None
+    if P.q_norm is not None:  # Gemma3: RMSNorm over each head of q and k, before RoPE
+        qn, rq = rmsnorm(q_pre, P.q_norm, cfg.rms_eps)
+        kn, rk = rmsnorm(k_pre, P.k_norm, cfg.rms_eps)
+    else:
+        qn, kn = q_pre, k_pre
     cos, sin = rope_angles(T, dh, cfg.layer_theta(l))
-    q4d = rope(q.reshape(Bsz, T, Hq, dh), cos, sin)
-    k4d = rope(k.reshape(Bsz, T, Hkv, dh), cos, sin)
+    q4d = rope(qn, cos, sin)
+    k4d = rope(kn, cos, sin)
     v4d = v.reshape(Bsz, T, Hkv, dh)
     O4d, Pm = attention(q4d, k4d, v4d, cfg.layer_window(l))
     O = O4d.reshape(Bsz * T, Hq * dh)
     ao, uo = _lin(P, "o", O, s)
-    h = x + ao
+    rpa = rpm = None
+    if P.post_attn_norm is not None:  # Gemma3 sandwich: norm the branch output, then add
+        ao_n, rpa = rmsnorm(ao, P.post_attn_norm, cfg.rms_eps)
+        h = x + ao_n
+    else:
+        h = x + ao
     c, rstd2 = rmsnorm(h, P.norm_mlp, cfg.rms_eps)
     g, ug = _lin(P, "gate", c, s)
     u, uu = _lin(P, "up", c, s)
     z = act(g, cfg.act) * u
     dn, ud = _lin(P, "down", z, s)
-    y = h + dn
+    if P.post_mlp_norm is not None:
+        dn_n, rpm = rmsnorm(dn, P.post_mlp_norm, cfg.rms_eps)
+        y = h + dn_n
+    else:
+        y = h + dn
     if not keep:
         return y
     cache = dict(x=x, a=a, rstd1=rstd1, q4d=q4d, k4d=k4d, v4d=v4d, P=Pm, O=O, h=h, c=c,
-                 rstd2=rstd2, g=g, u=u, z=z, cos=cos, sin=sin,
+                 rstd2=rstd2, g=g, u=u, z=z, cos=cos, sin=sin, q_pre=q_pre, k_pre=k_pre, rq=rq, rk=rk,
+                 ao=ao, rpa=rpa, dn=dn, rpm=rpm,
                  lu=dict(q=uq, k=uk, v=uv, o=uo, gate=ug, up=uu, down=ud))
     return y, cache
 
@@ -308,19 +340,24 @@ def layer_backward(cfg, l: int, P: LayerParams, x: np.ndarray, dy: np.ndarray, c
             grads[p] = (dA, dB)
         return dxx
 
-    # y = h + down(z)
-    dz = lin_bwd("down", cache["z"], dy)
+    # y = h + down(z)   (sandwich: y = h + RMSNorm(down(z)))
+    d_dn = dy if P.post_mlp_norm is None else rmsnorm_bwd(cache["dn"], P.post_mlp_norm, cache["rpm"], dy)
+    dz = lin_bwd("down", cache["z"], d_dn)
     g, u = cache["g"], cache["u"]
     dg = dz * u * act_grad(g, cfg.act)
     du = dz * act(g, cfg.act)
     dc = lin_bwd("gate", cache["c"], dg) + lin_bwd("up", cache["c"], du)
     d_h = dy + rmsnorm_bwd(cache["h"], P.norm_mlp, cache["rstd2"], dc)
-    # h = x + o(O)
-    dO = lin_bwd("o", cache["O"], d_h)
+    # h = x + o(O)   (sandwich: h = x + RMSNorm(o(O)))
+    d_ao = d_h if P.post_attn_norm is None else rmsnorm_bwd(cache["ao"], P.post_attn_norm, cache["rpa"], d_h)
+    dO = lin_bwd("o", cache["O"], d_ao)
     dq4, dk4, dv4 = attention_bwd(cache["q4d"], cache["k4d"], cache["v4d"], cache["P"],
                                   dO.reshape(Bsz, T, Hq, dh))
     dq4 = rope(dq4, cache["cos"], cache["sin"], inverse=True)
     dk4 = rope(dk4, cache["cos"], cache["sin"], inverse=True)
+    if P.q_norm is not None:  # through the per-head norms (biases are frozen: no gradient)
+        dq4 = rmsnorm_bwd(cache["q_pre"], P.q_norm, cache["rq"], dq4)
+        dk4 = rmsnorm_bwd(cache["k_pre"], P.k_norm, cache["rk"], dk4)
     a = cache["a"]
     da = (lin_bwd("q", a, dq4.reshape(Bsz * T, Hq * dh))
           + lin_bwd("k", a, dk4.reshape(Bsz * T, Hkv * dh))
@@ -337,9 +374,14 @@ def decompress_embedding(cfg, inp) -> np.ndarray:
     return dequant(q4, sb, cfg.hidden, cfg.group)
 
 
-def embed(E_hat: np.ndarray, ids: np.ndarray) -> np.ndarray:
-    """``x0[b*T + t] = E_hat[ids[b, t]]`` (tied int4 table, decompressed)."""
-    return E_hat[np.asarray(ids).reshape(-1)]
+def embed(E_hat: np.ndarray, ids: np.ndarray, scale: float = 1.0) -> np.ndarray:
+    """``x0[b*T + t] = scale * E_hat[ids[b, t]]`` (tied int4 table, decompressed; Gemma3
+    scales the embedding output by sqrt(hidden), the LM head uses the table unscaled)."""
+    return scale * E_hat[np.asarray(ids).reshape(-1)]
+
+
+def embed_scale(cfg) -> float:
+    return math.sqrt(cfg.hidden) if getattr(cfg, "embed_scale", False) else 1.0
 
 
 def lm_head_ce(cfg, E_hat: np.ndarray, norm_final: np.ndarray, xL: np.ndarray, ids: np.ndarray,
@@ -433,7 +475,7 @@ def train_step(cfg, inp, keep_ckpts: bool = True) -> StepResult:
     """
     L = len(inp.base)
     E_hat = decompress_embedding(cfg, inp)
-    ckpts = [embed(E_hat, inp.ids)]
+    ckpts = [embed(E_hat, inp.ids, embed_scale(cfg))]
     for l in range(L):
         P = decompress_layer(cfg, inp, l)
         ckpts.append(layer_forward(cfg, l, P, ckpts[l]))
@@ -454,7 +496,7 @@ def train_step_stored(cfg, inp) -> StepResult:
     intermediate of every block, then backward uses them (no recomputation)."""
     L = len(inp.base)
     E_hat = decompress_embedding(cfg, inp)
-    x = [embed(E_hat, inp.ids)]
+    x = [embed(E_hat, inp.ids, embed_scale(cfg))]
     caches, params = [], []
     for l in range(L):
         P = decompress_layer(cfg, inp, l)

@@ -613,3 +613,96 @@ def test_grad_accumulation_of_micro_batches_equals_batch_gradient():
         for p in full.grads[l]:
             for i in range(2):
                 np.testing.assert_allclose(acc[l, p, i], full.grads[l][p][i], rtol=1e-10, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------------------
+# P13: architecture details (Qwen2.5 QKV bias; Gemma3 QK-norm, sandwich norms, embedding
+# scale): finite differences through every new term, and invariants each one implies
+# ---------------------------------------------------------------------------------------
+ARCH = TINY.with_(qkv_bias=True, qk_norm=True, sandwich_norm=True, embed_scale=True)
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_arch_block_backward_finite_differences(layer):
+    cfg = ARCH
+    inp = make_inputs(cfg, seed=60, norm="random")
+    P = O.decompress_layer(cfg, inp, layer)
+    rng = np.random.default_rng(61)
+    x = rng.standard_normal((cfg.n_tokens, cfg.hidden))
+    dy = rng.standard_normal((cfg.n_tokens, cfg.hidden))
+    dx, grads = O.layer_backward(cfg, layer, P, x, dy)
+    _assert_fd(lambda xx: float(np.sum(dy * O.layer_forward(cfg, layer, P, xx))), x, dx)
+    for p in ("q", "k", "o", "down"):
+        A, B = P.lora[p]
+
+        def s_of_A(AA, p=p, B=B, A=A):
+            P.lora[p] = (AA, B)
+            try:
+                return float(np.sum(dy * O.layer_forward(cfg, layer, P, x)))
+            finally:
+                P.lora[p] = (A, B)
+
+        _assert_fd(s_of_A, A, grads[p][0], n_dirs=2)
+
+
+def test_arch_full_step_fd_with_embedding_scale():
+    cfg = ARCH
+    inp = make_inputs(cfg, seed=62, norm="random")
+    res = O.train_step(cfg, inp)
+    E = O.decompress_embedding(cfg, inp)
+    np.testing.assert_array_equal(res.ckpts[0], np.sqrt(cfg.hidden) * E[inp.ids.reshape(-1)])
+
+    def loss_of(val):
+        A, B = inp.lora[1]["k"]
+        inp.lora[1]["k"] = (val, B)
+        try:
+            x = O.embed(E, inp.ids, np.sqrt(cfg.hidden))
+            for j in range(cfg.n_layers):
+                x = O.layer_forward(cfg, j, O.decompress_layer(cfg, inp, j), x)
+            return O.lm_head_ce(cfg, E, inp.norm_final, x, inp.ids)[0]
+        finally:
+            inp.lora[1]["k"] = (A, B)
+
+    A = np.asarray(inp.lora[1]["k"][0], np.float64)
+    _assert_fd(loss_of, A, res.grads[1]["k"][0], n_dirs=2, tol=1e-5)
+
+
+def test_arch_norms_remove_the_scale_of_their_input():
+    # QK-norm: scaling W_q, W_k, their biases and LoRA B by c > 0 leaves the block unchanged;
+    # sandwich norms: the same for W_o (with B_o) and W_down (with B_down). Without the norm
+    # the output would change by O(1). (eps is made negligible against the rows' mean
+    # squares, which for the small o / down outputs of the tiny block are ~1e-5.)
+    cfg = ARCH.with_(batch=1, rms_eps=1e-14)
+    inp = make_inputs(cfg, seed=63, norm="random")
+    x = np.random.default_rng(64).standard_normal((cfg.n_tokens, cfg.hidden))
+    P = O.decompress_layer(cfg, inp, 0)
+    y0 = O.layer_forward(cfg, 0, P, x)
+    for group in (("q", "k"), ("o",), ("down",)):
+        Q = O.decompress_layer(cfg, inp, 0)
+        for p in group:
+            Q.W[p] = 3.0 * Q.W[p]
+            Q.lora[p] = (Q.lora[p][0], 3.0 * Q.lora[p][1])
+            if Q.bias is not None and p in Q.bias:
+                Q.bias[p] = 3.0 * Q.bias[p]
+        y = O.layer_forward(cfg, 0, Q, x)
+        assert np.max(np.abs(y - y0)) < 1e-9 * np.max(np.abs(y0)), group
+    # and the normed heads have the weight's RMS: with unit weights every rotated head
+    # vector has squared norm dh (RoPE preserves norms), up to eps
+    one = ARCH.with_(batch=1)
+    inp1 = make_inputs(one, seed=65, norm="ones")
+    _, cache = O.layer_forward(one, 0, O.decompress_layer(one, inp1, 0), x, keep=True)
+    sq = np.sum(cache["q4d"] ** 2, axis=-1)
+    np.testing.assert_allclose(sq, one.head_dim, rtol=1e-4)
+
+
+def test_arch_zero_bias_equals_no_bias():
+    cfg = ARCH.with_(qkv_bias=True)
+    inp = make_inputs(cfg, seed=66, norm="random")
+    x = np.random.default_rng(67).standard_normal((cfg.n_tokens, cfg.hidden))
+    P = O.decompress_layer(cfg, inp, 1)
+    P.bias = {p: np.zeros_like(b) for p, b in P.bias.items()}
+    Q = O.decompress_layer(cfg.with_(qkv_bias=False), inp, 1)
+    np.testing.assert_array_equal(O.layer_forward(cfg, 1, P, x), O.layer_forward(cfg, 1, Q, x))
+    # a nonzero bias changes the output
+    R = O.decompress_layer(cfg, inp, 1)
+    assert np.max(np.abs(O.layer_forward(cfg, 1, R, x) - O.layer_forward(cfg, 1, Q, x))) > 1e-3
