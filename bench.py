@@ -433,6 +433,9 @@ def main():
                     metavar=("FETCH_DIR", "WRITE_DIR", "SQ_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="per-kernel HBM GB/s and MFMA busy share from rocprofv3 --pmc runs (no GPU); writes "
                          "profiles/kernel_counters_<workload>.txt")
+    ap.add_argument("--arch", action="store_true",
+                    help="the model family's architecture details on top of the shape: QKV bias (Qwen2.5), per-head "
+                         "QK-norm, sandwich norms and embedding scale (Gemma3)")
     ap.add_argument("--experiments", action="store_true",
                     help="instead of the benchmark: step time against sequence length (B = 1, T = 128 .. 4096) and "
                          "the cost of decompressing every layer's weights as a separate pass, at --workload")
@@ -469,6 +472,10 @@ def main():
     from paper_2510_03425_amd.device import DeviceModel
 
     cfg = CONFIGS[args.workload]
+    if args.arch:
+        fam = dict(qkv_bias=True) if cfg.name.startswith("qwen") else \
+            dict(qk_norm=True, sandwich_norm=True, embed_scale=True)
+        cfg = cfg.with_(name=cfg.name + "+arch", **fam)
     if args.experiments:
         experiments(cfg)
         return

@@ -76,7 +76,21 @@ typedef struct {
   int32_t lora_rank;     /* r: 8 or 16                                                    */
   float lora_alpha;      /* LoRA scale s = alpha / r                                      */
   uint32_t lora_mask;    /* bit p set: projection p carries a LoRA adapter                */
+  uint32_t arch;         /* architecture details beyond the shapes (MEBP_ARCH_* bits); 0 =  */
+                         /* the plain pre-norm block                                      */
 } mebp_config;
+
+/* mebp_config.arch bits (Sec. 4 trains Qwen2.5 and Gemma3 models; these are the parts of
+ * their blocks beyond a plain pre-norm Llama-style block). The extra frozen weights are
+ * fp32 vectors in mebp_layer_base.                                                      */
+enum {
+  MEBP_ARCH_QKV_BIAS = 1,     /* Qwen2.5: q, k, v projections add a bias                   */
+  MEBP_ARCH_QK_NORM = 2,      /* Gemma3: RMSNorm over each head of q and of k, before RoPE */
+  MEBP_ARCH_SANDWICH = 4,     /* Gemma3: RMSNorm on the attention output and on the MLP    */
+                              /* output before each residual add                          */
+  MEBP_ARCH_EMBED_SCALE = 8   /* Gemma3: embedding output times sqrt(hidden) (the tied LM  */
+                              /* head uses the table unscaled)                            */
+};
 
 typedef struct {
   const uint8_t* q4;        /* [out][in/2]                                                */
@@ -88,6 +102,11 @@ typedef struct {
                             /* gate,up [F][d], down [d][F]                                */
   const float* norm_attn;   /* [d] fp32 RMSNorm weight before attention (frozen)          */
   const float* norm_mlp;    /* [d] fp32 RMSNorm weight before the MLP (frozen)            */
+  const float* bias[3];     /* MEBP_ARCH_QKV_BIAS: q [Hq*dh], k, v [Hkv*dh]; else unused  */
+  const float* q_norm;      /* MEBP_ARCH_QK_NORM: [dh] weights of the q and k head norms  */
+  const float* k_norm;
+  const float* post_attn_norm; /* MEBP_ARCH_SANDWICH: [d] weights of the norms on the    */
+  const float* post_mlp_norm;  /* attention output and on the MLP output                  */
 } mebp_layer_base;
 
 typedef struct {

@@ -32,7 +32,7 @@ class MebpConfig(C.Structure):
         ("vocab", C.c_int32), ("act", C.c_int32), ("rms_eps", C.c_float),
         ("rope_theta_global", C.c_float), ("rope_theta_local", C.c_float),
         ("window", C.c_int32), ("global_every", C.c_int32), ("group", C.c_int32),
-        ("lora_rank", C.c_int32), ("lora_alpha", C.c_float), ("lora_mask", C.c_uint32),
+        ("lora_rank", C.c_int32), ("lora_alpha", C.c_float), ("lora_mask", C.c_uint32), ("arch", C.c_uint32),
     ]
 
 
@@ -41,7 +41,9 @@ class MebpQ4(C.Structure):
 
 
 class MebpLayerBase(C.Structure):
-    _fields_ = [("w", MebpQ4 * NPROJ), ("norm_attn", C.c_void_p), ("norm_mlp", C.c_void_p)]
+    _fields_ = [("w", MebpQ4 * NPROJ), ("norm_attn", C.c_void_p), ("norm_mlp", C.c_void_p), ("bias", C.c_void_p * 3),
+                ("q_norm", C.c_void_p), ("k_norm", C.c_void_p), ("post_attn_norm", C.c_void_p),
+                ("post_mlp_norm", C.c_void_p)]
 
 
 class MebpLayerLora(C.Structure):

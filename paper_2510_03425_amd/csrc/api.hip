@@ -44,12 +44,13 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 enum Slot {
   S_A, S_Q, S_K, S_V, S_O, S_LSE, S_H, S_C, S_G, S_U, S_Z, S_LU, S_LDU, S_DYB, S_DC, S_DH, S_DHB, S_DO,
   S_DELTA, S_DQ, S_DK, S_DV, S_DA, S_PART, S_ROPE_G, S_ROPE_L, S_TGT, S_HF, S_LOGITS, S_STATS, S_LSEV,
-  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_COUNT
+  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_QPRE, S_KPRE, S_TO, S_TD, S_DTB, S_DTOB, S_COUNT
 };
 const char* kSlotNames[S_COUNT] = {
   "a", "q", "k", "v", "o", "lse", "h", "c", "g", "u", "z", "lora_u", "lora_du", "dy_bf16", "dc", "dh",
   "dh_bf16", "do", "delta", "dq", "dk", "dv", "da", "lora_part", "rope_global", "rope_local", "targets",
-  "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part"};
+  "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part",
+  "q_prenorm", "k_prenorm", "attn_out_prenorm", "mlp_out_prenorm", "d_mlp_out_bf16", "d_attn_out_bf16"};
 
 // Slots written by a layer's (re)computed forward and read by its backward, plus the
 // split-K scratch: the training step keeps two copies, so that the recompute of layer l-1
@@ -59,7 +60,7 @@ const char* kSlotNames[S_COUNT] = {
 bool per_set(int s) {
   switch (s) {
     case S_A: case S_Q: case S_K: case S_V: case S_O: case S_LSE: case S_H: case S_C: case S_G: case S_U:
-    case S_Z: case S_LU: case S_DYB: case S_SPLIT:
+    case S_Z: case S_LU: case S_DYB: case S_SPLIT: case S_QPRE: case S_KPRE: case S_TO: case S_TD:
       return true;
     default:
       return false;
@@ -145,6 +146,13 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   sz[S_DHF] = V ? N * d * 4 : 0;
   sz[S_LMPART] = (size_t)L->lm_splits * N * d * 4;
   sz[S_GRAD] = N * d * 4;
+  const bool qkn = c->arch & MEBP_ARCH_QK_NORM, sw = c->arch & MEBP_ARCH_SANDWICH;
+  sz[S_QPRE] = qkn ? N * qd * 2 : 0;
+  sz[S_KPRE] = qkn ? N * kvd * 2 : 0;
+  sz[S_TO] = sw ? N * d * 4 : 0;
+  sz[S_TD] = sw ? N * d * 4 : 0;
+  sz[S_DTB] = sw ? N * d * 2 : 0;
+  sz[S_DTOB] = sw ? N * d * 2 : 0;
   {
     const int M = (int)N, D = (int)d, Q = (int)qd, KV = (int)kvd, FF = (int)F, R = (int)r;
     size_t m = 0;
@@ -209,6 +217,7 @@ int check_config(const mebp_config* c) {
   if (c->lora_mask && c->lora_rank != 8 && c->lora_rank != 16)
     return fail(MEBP_EUNSUPPORTED, "lora_rank %d not in {8, 16}", c->lora_rank);
   if (c->lora_mask && !isfinite(c->lora_alpha)) return fail(MEBP_EINVAL, "bad lora_alpha");
+  if (c->arch >> 4) return fail(MEBP_EINVAL, "arch has unknown bits 0x%x", c->arch);
   return MEBP_OK;
 }
 
@@ -256,6 +265,13 @@ int check_layer(const mebp_config* c, int layer, const mebp_layer_base* base, co
   if (!base->norm_attn || !base->norm_mlp) return fail(MEBP_EINVAL, "NULL norm weight");
   if (!aligned(base->norm_attn, 16) || !aligned(base->norm_mlp, 16))
     return fail(MEBP_EINVAL, "norm weight not 16-byte aligned");
+  const float* extra[7] = {base->bias[0], base->bias[1], base->bias[2], base->q_norm, base->k_norm,
+                           base->post_attn_norm, base->post_mlp_norm};
+  const uint32_t need[7] = {MEBP_ARCH_QKV_BIAS, MEBP_ARCH_QKV_BIAS, MEBP_ARCH_QKV_BIAS, MEBP_ARCH_QK_NORM,
+                            MEBP_ARCH_QK_NORM, MEBP_ARCH_SANDWICH, MEBP_ARCH_SANDWICH};
+  for (int i = 0; i < 7; ++i)
+    if ((c->arch & need[i]) && (!extra[i] || !aligned(extra[i], 16)))
+      return fail(MEBP_EINVAL, "layer %d: architecture weight %d NULL or not 16-byte aligned", layer, i);
   return MEBP_OK;
 }
 
@@ -470,15 +486,29 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
   hipEvent_t lr;
   HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}, &lr));
+  // bias and per-head norm come between the projection and RoPE: then RoPE moves out of the
+  // GEMM's follow-up into the kernel that applies them
+  const bool qk_post = c->arch & (MEBP_ARCH_QKV_BIAS | MEBP_ARCH_QK_NORM);
+  const bool sandwich = c->arch & MEBP_ARCH_SANDWICH;
   {
     // q, k, v projections with RoPE applied to q and k on the way out
     NtSeg qs = nt_seg(x, base, lora, MEBP_Q, q, D.qd, nullptr, 0), ks = nt_seg(x, base, lora, MEBP_K, k, D.kvd, nullptr, 0);
-    qs.rope = ks.rope = 1;
+    qs.rope = ks.rope = qk_post ? 0 : 1;
     NtArgs na = nt_args(x, a, D.d, {qs, ks, nt_seg(x, base, lora, MEBP_V, v, D.kvd, nullptr, 0)});
     na.rope_cs = rope;
     na.rope_T = x.T;
     na.rope_dh = c->head_dim;
     HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st, lr));
+  }
+  if (qk_post) {
+    const bool bias = c->arch & MEBP_ARCH_QKV_BIAS, qkn = c->arch & MEBP_ARCH_QK_NORM;
+    HIP_TRY(launch_qkv_post(q, D.qd, D.N, x.T, c->n_heads, c->head_dim, bias ? base->bias[0] : nullptr,
+                            qkn ? base->q_norm : nullptr, c->rms_eps, xs<f16>(x, S_QPRE), rope, 1, x.st));
+    HIP_TRY(launch_qkv_post(k, D.kvd, D.N, x.T, c->n_kv_heads, c->head_dim, bias ? base->bias[1] : nullptr,
+                            qkn ? base->k_norm : nullptr, c->rms_eps, xs<f16>(x, S_KPRE), rope, 1, x.st));
+    if (bias)
+      HIP_TRY(launch_qkv_post(v, D.kvd, D.N, x.T, c->n_kv_heads, c->head_dim, base->bias[2], nullptr, c->rms_eps,
+                              nullptr, rope, 0, x.st));
   }
   AttnArgs at{};
   at.q = q; at.k = k; at.v = v; at.ldq = D.qd; at.ldk = D.kvd;
@@ -487,7 +517,14 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   at.o = o; at.lse = xs<float>(x, S_LSE);
   HIP_TRY(launch_attn_fwd(at, scratch(x), x.st));
   HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}, &lr));
-  {
+  if (sandwich) {
+    // t = o-projection (kept for the backward), h = x + RMSNorm(t), c = RMSNorm(h)
+    float* to = xs<float>(x, S_TO);
+    HIP_TRY(launch_gemm_nt(nt_args(x, o, D.qd, {nt_seg(x, base, lora, MEBP_O, to, D.d, nullptr, 0)}), NT_STORE_F32, x.st,
+                           lr));
+    HIP_TRY(launch_resid_rmsnorm(x_in, to, base->post_attn_norm, D.N, D.d, c->rms_eps, h, x.st));
+    HIP_TRY(launch_rmsnorm_fwd(h, base->norm_mlp, D.N, D.d, c->rms_eps, cc, nullptr, x.st));
+  } else {
     // h = x + o-projection, then c = RMSNorm(h)
     NtArgs na = nt_args(x, o, D.qd, {nt_seg(x, base, lora, MEBP_O, h, D.d, x_in, D.d)});
     na.norm_w = base->norm_mlp;
@@ -506,7 +543,13 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
     HIP_TRY(launch_gemm_nt(na, NT_STORE_F16, x.st, lr));
   }
   HIP_TRY(lora_down(x, lora, z, D.F, {MEBP_DOWN}, &lr));
-  if (!keep)
+  if (sandwich) {
+    // t = down-projection (the backward needs it, so the recompute runs it too), y = h + RMSNorm(t)
+    float* td = xs<float>(x, S_TD);
+    HIP_TRY(launch_gemm_nt(nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, td, D.d, nullptr, 0)}), NT_STORE_F32,
+                           x.st, lr));
+    if (!keep) HIP_TRY(launch_resid_rmsnorm(h, td, base->post_mlp_norm, D.N, D.d, c->rms_eps, x_out, x.st));
+  } else if (!keep)
     HIP_TRY(launch_gemm_nt(nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)}), NT_STORE_F32, x.st,
                            lr));
   else if (lr)
@@ -547,15 +590,24 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
   bf16* dv = xs<bf16>(x, S_DV);
   float* da = xs<float>(x, S_DA);
 
-  // y = h + down(z)
-  if (!dy_bf16_ready) HIP_TRY(launch_f32_to_bf16(dy, dyb, (size_t)D.N * D.d, x.st));
+  const bool sandwich = c->arch & MEBP_ARCH_SANDWICH;
+  // y = h + down(z)   (sandwich: y = h + RMSNorm(t), t = down(z): the down projection's
+  // gradient is the norm's backward of dy)
+  bf16* gdown = dyb;
+  if (sandwich) {
+    gdown = xs<bf16>(x, S_DTB);
+    HIP_TRY(launch_rmsnorm_bwd(xs<float>(x, S_TD), base->post_mlp_norm, dy, nullptr, D.N, D.d, c->rms_eps, nullptr,
+                               gdown, x.st));
+  } else if (!dy_bf16_ready) {
+    HIP_TRY(launch_f32_to_bf16(dy, dyb, (size_t)D.N * D.d, x.st));
+  }
   hipEvent_t lr;
-  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_DOWN}, {dyb}, z, &lr));
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_DOWN}, {gdown}, z, &lr));
   {
     TnArgs t{};
     set_scratch(x, t);
     t.M = D.N; t.Kout = D.F; t.nseg = 1; t.r = D.r;
-    t.seg[0] = tn_seg(x, base, lora, MEBP_DOWN, dyb);
+    t.seg[0] = tn_seg(x, base, lora, MEBP_DOWN, gdown);
     t.g = g; t.u = u; t.ldgu = D.F; t.act = c->act;
     HIP_TRY(launch_gemm_tn(t, TN_ACT_BWD, TN_A_BF16, x.st, lr));  // g <- dg, u <- d(up)
   }
@@ -574,13 +626,19 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     t.norm_x = h; t.norm_w = base->norm_mlp; t.resid2 = dy; t.out2 = dh; t.out2b = dhb; t.eps = c->rms_eps;
     HIP_TRY(launch_gemm_tn(t, TN_STORE_F32, TN_A_BF16, x.st, lr));
   }
-  // h = x + o(O)
-  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_O}, {dhb}, o, &lr));
+  // h = x + o(O)   (sandwich: h = x + RMSNorm(t), t = o(O))
+  bf16* go = dhb;
+  if (sandwich) {
+    go = xs<bf16>(x, S_DTOB);
+    HIP_TRY(launch_rmsnorm_bwd(xs<float>(x, S_TO), base->post_attn_norm, dh, nullptr, D.N, D.d, c->rms_eps, nullptr,
+                               go, x.st));
+  }
+  HIP_TRY(lora_bwd(x, lora, grads, {MEBP_O}, {go}, o, &lr));
   {
     TnArgs t{};
     set_scratch(x, t);
     t.M = D.N; t.Kout = D.qd; t.nseg = 1; t.r = D.r;
-    t.seg[0] = tn_seg(x, base, lora, MEBP_O, dhb);
+    t.seg[0] = tn_seg(x, base, lora, MEBP_O, go);
     t.outb = dO; t.ldo = D.qd;
     HIP_TRY(launch_gemm_tn(t, TN_STORE_BF16, TN_A_BF16, x.st, lr));
   }
@@ -594,6 +652,13 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
     if (x.aux && x.aux_used) *x.aux_used = true;
     HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), scratch(x), x.st, x.aux, x.ev_lr, x.ev_du));
+  }
+  if (c->arch & MEBP_ARCH_QK_NORM) {
+    // through the per-head norms (the biases are frozen and need no gradient)
+    HIP_TRY(launch_headnorm_bwd(xs<f16>(x, S_QPRE), D.qd, D.N, c->n_heads, c->head_dim, base->q_norm, c->rms_eps, dq,
+                                D.qd, x.st));
+    HIP_TRY(launch_headnorm_bwd(xs<f16>(x, S_KPRE), D.kvd, D.N, c->n_kv_heads, c->head_dim, base->k_norm, c->rms_eps,
+                                dk, D.kvd, x.st));
   }
   HIP_TRY(lora_bwd(x, lora, grads, {MEBP_Q, MEBP_K, MEBP_V}, {dq, dk, dv}, a, &lr));
   if (dx) {
@@ -803,7 +868,8 @@ int train_step_impl(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   float* rope_l = slot<float>(ws, x.L, S_ROPE_L);
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_global, rope_g, x.st));
   HIP_TRY(launch_rope_table(T, cfg->head_dim, cfg->rope_theta_local, rope_l, x.st));
-  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ck(0), x.st));
+  const float emb_mul = (cfg->arch & MEBP_ARCH_EMBED_SCALE) ? sqrtf((float)cfg->hidden) : 1.0f;
+  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, x.D.N, cfg->vocab, ck(0), x.st, emb_mul));
   if (off && (e = save(0, x.st))) return e;
   SideStream* side = side_stream(x.st);
   std::unique_lock<std::mutex> lock;
@@ -995,7 +1061,9 @@ int mebp_embed(const mebp_config* cfg, const mebp_q4* emb, const int32_t* ids, i
   if (cfg->vocab <= 0) return fail(MEBP_EINVAL, "vocab must be > 0 for the embedding");
   if ((e = check_q4(emb, "embedding")) || (e = check_act(x0, "x0"))) return e;
   if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
-  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, B * T, cfg->vocab, x0, (hipStream_t)stream));
+  const float emb_mul = (cfg->arch & MEBP_ARCH_EMBED_SCALE) ? sqrtf((float)cfg->hidden) : 1.0f;
+  HIP_TRY(launch_embed(emb->q4, emb->scale, cfg->hidden, cfg->group, ids, B * T, cfg->vocab, x0, (hipStream_t)stream,
+                       emb_mul));
   return MEBP_OK;
 }
 

@@ -35,10 +35,10 @@ __global__ void k_dequant(const uint8_t* q4, const uint16_t* scale, int rows, in
   }
 }
 
-// x0[n][:] = E[ids[n]][:] decompressed to fp32; one thread per 8 codes.
+// x0[n][:] = mul * E[ids[n]][:] decompressed to fp32; one thread per 8 codes.
 // An id outside [0, V) yields a NaN row instead of an out-of-bounds read.
 __global__ void k_embed(const uint8_t* q4, const uint16_t* scale, int d, int group, const int32_t* ids,
-                        int n, int V, float* x0) {
+                        int n, int V, float mul, float* x0) {
   const int per_row = d >> 3;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (size_t)n * per_row) return;
@@ -55,7 +55,7 @@ __global__ void k_embed(const uint8_t* q4, const uint16_t* scale, int d, int gro
   const float s = half_bits_to_f32(scale[v * ng + c / group]);
   float f[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) f[j] = (float)nib_s(w, j) * s;
+  for (int j = 0; j < 8; ++j) f[j] = (float)nib_s(w, j) * s * mul;  // mul = 1 is exact
   float4* o = (float4*)(x0 + (size_t)row * d + c);
   o[0] = make_float4(f[0], f[1], f[2], f[3]);
   o[1] = make_float4(f[4], f[5], f[6], f[7]);
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm_bwd(const float* x, const float
   const float rs = 1.0f / sqrtf(ss / (float)d + eps);
   const float mean_term = rs * sd / (float)d;  // mean(xhat * w * dy)
   const float4* rr = (const float4*)(resid ? resid + off : nullptr);
-  float4* o = (float4*)(dx + off);
+  float4* o = dx ? (float4*)(dx + off) : nullptr;
   uint2* ob = dxb ? (uint2*)(dxb + off) : nullptr;
   for (int c = lane; c < d4; c += 64) {
     const float4 v = xr[c], g = gr[c], ww = wr[c];
@@ -116,7 +116,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm_bwd(const float* x, const float
     res.y += rs * (ww.y * g.y - v.y * rs * mean_term);
     res.z += rs * (ww.z * g.z - v.z * rs * mean_term);
     res.w += rs * (ww.w * g.w - v.w * rs * mean_term);
-    o[c] = res;
+    if (o) o[c] = res;
     if (ob) ob[c] = make_uint2(pack_bf16x2(res.x, res.y), pack_bf16x2(res.z, res.w));
   }
 }
@@ -262,6 +262,138 @@ __global__ void k_splitk_reduce(const float* part, int splits, size_t n4, float*
 
 inline unsigned blocks_for(size_t n, unsigned bs) { return (unsigned)((n + bs - 1) / bs); }
 
+// ------------------------------------------------------------------ architecture extras
+// out = resid + RMSNorm(t) * w, one wave per row (the sandwich norms of the attention and
+// MLP outputs before the residual add).
+__global__ __launch_bounds__(256) void k_resid_rmsnorm(const float* resid, const float* t, const float* w, int n,
+                                                       int d, float eps, float* out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const size_t off = (size_t)row * d;
+  const float4* tr = (const float4*)(t + off);
+  const int d4 = d >> 2;
+  float ss = 0.f;
+  for (int c = lane; c < d4; c += 64) {
+    const float4 v = tr[c];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+  const float4* rr = (const float4*)(resid + off);
+  const float4* wr = (const float4*)w;
+  float4* o = (float4*)(out + off);
+  for (int c = lane; c < d4; c += 64) {
+    const float4 v = tr[c], g = wr[c], r = rr[c];
+    o[c] = make_float4(r.x + v.x * rs * g.x, r.y + v.y * rs * g.y, r.z + v.z * rs * g.z, r.w + v.w * rs * g.w);
+  }
+}
+
+// q, k heads after their projections (fp16, in place): + bias, then (with a norm weight)
+// RMSNorm over the head keeping the pre-norm values in `pre`, then RoPE; v: + bias. One
+// thread per (row, head, 4 columns e of the first half and their partners e + dh/2); the
+// dh/8 threads of a head are consecutive lanes and reduce with butterfly shuffles.
+__global__ void k_qkv_post(f16* x, int ld, int n, int T, int H, int dh, const float* bias, const float* nw,
+                           float eps, f16* pre, const float* cs, int rope) {
+  const int G = dh >> 3, half = dh >> 1;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool ok = i < (size_t)n * H * G;
+  const int j = (int)(i % G), e = 4 * j;
+  const int h = (int)((i / G) % H);
+  const size_t row = i / ((size_t)G * H);
+  float lo[4] = {0, 0, 0, 0}, hi[4] = {0, 0, 0, 0};
+  f16* p = x + row * ld + h * dh;
+  if (ok) {
+    const uint2 a = *(const uint2*)(p + e), b = *(const uint2*)(p + e + half);
+    lo[0] = f16_lo(a.x); lo[1] = f16_hi(a.x); lo[2] = f16_lo(a.y); lo[3] = f16_hi(a.y);
+    hi[0] = f16_lo(b.x); hi[1] = f16_hi(b.x); hi[2] = f16_lo(b.y); hi[3] = f16_hi(b.y);
+    if (bias) {
+      const float4 b1 = *(const float4*)(bias + h * dh + e), b2 = *(const float4*)(bias + h * dh + e + half);
+      lo[0] += b1.x; lo[1] += b1.y; lo[2] += b1.z; lo[3] += b1.w;
+      hi[0] += b2.x; hi[1] += b2.y; hi[2] += b2.z; hi[3] += b2.w;
+    }
+  }
+  if (nw) {
+    if (ok) {
+      // the pre-norm values are kept in fp16 and the statistics computed from exactly those
+      // values, which the backward reads again
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        lo[t] = (float)(f16)lo[t];
+        hi[t] = (float)(f16)hi[t];
+      }
+      f16* q = pre + row * ld + h * dh;
+      *(uint2*)(q + e) = make_uint2(pack_f16x2(lo[0], lo[1]), pack_f16x2(lo[2], lo[3]));
+      *(uint2*)(q + e + half) = make_uint2(pack_f16x2(hi[0], hi[1]), pack_f16x2(hi[2], hi[3]));
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) ss += lo[t] * lo[t] + hi[t] * hi[t];
+    for (int m = 1; m < G; m <<= 1) ss += __shfl_xor(ss, m, 64);
+    const float rs = 1.0f / sqrtf(ss / (float)dh + eps);
+    if (ok) {
+      const float4 w1 = *(const float4*)(nw + e), w2 = *(const float4*)(nw + e + half);
+      lo[0] *= rs * w1.x; lo[1] *= rs * w1.y; lo[2] *= rs * w1.z; lo[3] *= rs * w1.w;
+      hi[0] *= rs * w2.x; hi[1] *= rs * w2.y; hi[2] *= rs * w2.z; hi[3] *= rs * w2.w;
+    }
+  }
+  if (!ok) return;
+  if (rope) {
+    const int t = (int)(row % T);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float c = cs[2 * (t * half + e + u)], sn = cs[2 * (t * half + e + u) + 1];
+      const float x1 = lo[u], x2 = hi[u];
+      lo[u] = x1 * c - x2 * sn;
+      hi[u] = x2 * c + x1 * sn;
+    }
+  }
+  *(uint2*)(p + e) = make_uint2(pack_f16x2(lo[0], lo[1]), pack_f16x2(lo[2], lo[3]));
+  *(uint2*)(p + e + half) = make_uint2(pack_f16x2(hi[0], hi[1]), pack_f16x2(hi[2], hi[3]));
+}
+
+// Per-head RMSNorm backward in place on the gradient g (bf16) from the stored pre-norm
+// values (fp16): g = rstd * (w*g - xhat * mean(xhat*w*g)). Thread mapping as k_qkv_post.
+__global__ void k_headnorm_bwd(const f16* pre, int ld, int n, int H, int dh, const float* nw, float eps, bf16* g,
+                               int ldg) {
+  const int G = dh >> 3, half = dh >> 1;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool ok = i < (size_t)n * H * G;
+  const int j = (int)(i % G), e = 4 * j;
+  const int h = (int)((i / G) % H);
+  const size_t row = i / ((size_t)G * H);
+  float xv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, gv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, wv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const f16* xp = pre + row * ld + h * dh;
+  bf16* gp = g + row * ldg + h * dh;
+  if (ok) {
+    const uint2 a = *(const uint2*)(xp + e), b = *(const uint2*)(xp + e + half);
+    const uint2 c = *(const uint2*)(gp + e), d = *(const uint2*)(gp + e + half);
+    xv[0] = f16_lo(a.x); xv[1] = f16_hi(a.x); xv[2] = f16_lo(a.y); xv[3] = f16_hi(a.y);
+    xv[4] = f16_lo(b.x); xv[5] = f16_hi(b.x); xv[6] = f16_lo(b.y); xv[7] = f16_hi(b.y);
+    gv[0] = bf16_lo(c.x); gv[1] = bf16_hi(c.x); gv[2] = bf16_lo(c.y); gv[3] = bf16_hi(c.y);
+    gv[4] = bf16_lo(d.x); gv[5] = bf16_hi(d.x); gv[6] = bf16_lo(d.y); gv[7] = bf16_hi(d.y);
+    const float4 w1 = *(const float4*)(nw + e), w2 = *(const float4*)(nw + e + half);
+    wv[0] = w1.x; wv[1] = w1.y; wv[2] = w1.z; wv[3] = w1.w; wv[4] = w2.x; wv[5] = w2.y; wv[6] = w2.z; wv[7] = w2.w;
+  }
+  float ss = 0.f, sd = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    ss += xv[t] * xv[t];
+    sd += xv[t] * wv[t] * gv[t];
+  }
+  for (int m = 1; m < G; m <<= 1) {
+    ss += __shfl_xor(ss, m, 64);
+    sd += __shfl_xor(sd, m, 64);
+  }
+  if (!ok) return;
+  const float rs = 1.0f / sqrtf(ss / (float)dh + eps);
+  const float mt = rs * sd / (float)dh;  // mean(xhat * w * g)
+  float o[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) o[t] = rs * (wv[t] * gv[t] - xv[t] * rs * mt);
+  *(uint2*)(gp + e) = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+  *(uint2*)(gp + e + half) = make_uint2(pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7]));
+}
+
 }  // namespace
 
 hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, int cols, int group,
@@ -274,10 +406,33 @@ hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, in
   return hipGetLastError();
 }
 hipError_t launch_embed(const uint8_t* q4, const uint16_t* scale, int d, int group, const int32_t* ids, int n,
-                        int V, float* x0, hipStream_t st) {
+                        int V, float* x0, hipStream_t st, float mul) {
   const size_t tot = (size_t)n * (d >> 3);
   MEBP_TIMED(st, "embed", 0.0, (double)tot * 36,
-             hipLaunchKernelGGL(k_embed, dim3(blocks_for(tot, 256)), dim3(256), 0, st, q4, scale, d, group, ids, n, V, x0));
+             hipLaunchKernelGGL(k_embed, dim3(blocks_for(tot, 256)), dim3(256), 0, st, q4, scale, d, group, ids, n, V, mul,
+                                x0));
+  return hipGetLastError();
+}
+hipError_t launch_resid_rmsnorm(const float* resid, const float* t, const float* w, int n, int d, float eps,
+                                float* out, hipStream_t st) {
+  MEBP_TIMED(st, "resid_rmsnorm", 0.0, (double)n * d * 16,
+             hipLaunchKernelGGL(k_resid_rmsnorm, dim3(blocks_for(n, 4)), dim3(256), 0, st, resid, t, w, n, d, eps, out));
+  return hipGetLastError();
+}
+hipError_t launch_qkv_post(f16* x, int ld, int n, int T, int H, int dh, const float* bias, const float* nw, float eps,
+                           f16* pre, const float* cs, int rope, hipStream_t st) {
+  const size_t tot = (size_t)n * H * (dh >> 3);
+  MEBP_TIMED(st, "qkv_post", 0.0, (double)n * H * dh * (nw ? 6 : 4),
+             hipLaunchKernelGGL(k_qkv_post, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, n, T, H, dh, bias, nw, eps,
+                                pre, cs, rope));
+  return hipGetLastError();
+}
+hipError_t launch_headnorm_bwd(const f16* pre, int ld, int n, int H, int dh, const float* nw, float eps, bf16* g,
+                               int ldg, hipStream_t st) {
+  const size_t tot = (size_t)n * H * (dh >> 3);
+  MEBP_TIMED(st, "headnorm_bwd", 0.0, (double)n * H * dh * 6,
+             hipLaunchKernelGGL(k_headnorm_bwd, dim3(blocks_for(tot, 256)), dim3(256), 0, st, pre, ld, n, H, dh, nw, eps, g,
+                                ldg));
   return hipGetLastError();
 }
 hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, f16* y, float* rstd,

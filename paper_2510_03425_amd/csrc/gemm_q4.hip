@@ -863,7 +863,7 @@ static int env_int(const char* name, int dflt) {
 int gemm_splits(int tiles, int ktiles) {
   static const int max_splits = env_int("MEBP_SPLIT_MAX", 16);
   static const int target = env_int("MEBP_SPLIT_TARGET", 256);
-  static const int min_kt = env_int("MEBP_SPLIT_MIN_KTILES", 2);
+  static const int min_kt = env_int("MEBP_SPLIT_MIN_KTILES", 4);
   if (tiles >= target * 5 / 8) return 1;
   int s = (target + tiles - 1) / tiles;
   const int max_s = ktiles / (min_kt > 0 ? min_kt : 1);

@@ -135,7 +135,17 @@ hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S
 hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, int cols, int group,
                           float* out_f32, uint16_t* out_bf16, hipStream_t st);
 hipError_t launch_embed(const uint8_t* q4, const uint16_t* scale, int d, int group, const int32_t* ids,
-                        int n, int V, float* x0, hipStream_t st);
+                        int n, int V, float* x0, hipStream_t st, float mul = 1.0f);
+// out = resid + RMSNorm(t) * w (row-wise)
+hipError_t launch_resid_rmsnorm(const float* resid, const float* t, const float* w, int n, int d, float eps,
+                                float* out, hipStream_t st);
+// in place on fp16 q or k heads [n][ld]: + bias (if any), per-head RMSNorm with weight nw (if
+// any; pre-norm values to `pre`, same layout), RoPE (if rope); for v: bias only
+hipError_t launch_qkv_post(f16* x, int ld, int n, int T, int H, int dh, const float* bias, const float* nw, float eps,
+                           f16* pre, const float* cs, int rope, hipStream_t st);
+// per-head RMSNorm backward in place on bf16 g [n][ldg] from pre-norm values pre [n][ld]
+hipError_t launch_headnorm_bwd(const f16* pre, int ld, int n, int H, int dh, const float* nw, float eps, bf16* g,
+                               int ldg, hipStream_t st);
 // y = fp16(x * w * rstd); rstd optional
 hipError_t launch_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps, f16* y,
                               float* rstd, hipStream_t st);

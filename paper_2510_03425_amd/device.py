@@ -26,7 +26,7 @@ def make_config(cfg: Config) -> L.MebpConfig:
         head_dim=cfg.head_dim, ffn=cfg.ffn, vocab=cfg.vocab, act=ACT_CODE[cfg.act], rms_eps=cfg.rms_eps,
         rope_theta_global=cfg.rope_theta_global, rope_theta_local=cfg.rope_theta_local,
         window=cfg.window, global_every=cfg.global_every, group=cfg.group, lora_rank=cfg.lora_rank,
-        lora_alpha=cfg.lora_alpha, lora_mask=cfg.lora_mask())
+        lora_alpha=cfg.lora_alpha, lora_mask=cfg.lora_mask(), arch=cfg.arch_flags)
 
 
 def stream_handle() -> int:
@@ -75,6 +75,20 @@ class DeviceModel:
             self.keep += [na, nm]
             self.base[l].norm_attn = na.data_ptr()
             self.base[l].norm_mlp = nm.data_ptr()
+            ex = inp.extra
+            if ex.get("bias") and ex["bias"][l] is not None:
+                for i, p in enumerate(("q", "k", "v")):
+                    tb = _dev(ex["bias"][l][p], device)
+                    self.keep.append(tb)
+                    self.base[l].bias[i] = tb.data_ptr()
+            if ex.get("qk_norm") and ex["qk_norm"][l] is not None:
+                tq, tk = (_dev(w, device) for w in ex["qk_norm"][l])
+                self.keep += [tq, tk]
+                self.base[l].q_norm, self.base[l].k_norm = tq.data_ptr(), tk.data_ptr()
+            if ex.get("post_norm") and ex["post_norm"][l] is not None:
+                ta, tm = (_dev(w, device) for w in ex["post_norm"][l])
+                self.keep += [ta, tm]
+                self.base[l].post_attn_norm, self.base[l].post_mlp_norm = ta.data_ptr(), tm.data_ptr()
             dA, dB = {}, {}
             for i, p in enumerate(PROJ):
                 if p not in inp.lora[l]:

@@ -28,10 +28,10 @@ def test_header_symbols_exported(built_lib):
 
 
 def test_struct_sizes_match_header(built_lib):
-    # mebp_config: 17 four-byte fields; the structs are arrays of pointers
-    assert C.sizeof(L.MebpConfig) == 17 * 4
+    # mebp_config: 18 four-byte fields; the structs are arrays of pointers
+    assert C.sizeof(L.MebpConfig) == 18 * 4
     assert C.sizeof(L.MebpQ4) == 16
-    assert C.sizeof(L.MebpLayerBase) == 7 * 16 + 16
+    assert C.sizeof(L.MebpLayerBase) == 7 * 16 + 16 + 7 * 8
     assert C.sizeof(L.MebpLayerLora) == 14 * 8
 
 
@@ -49,6 +49,7 @@ def test_workspace_bytes(built_lib):
     ("n_kv_heads", 3, L.MEBP_EINVAL), ("group", 64, L.MEBP_EUNSUPPORTED),
     ("lora_rank", 4, L.MEBP_EUNSUPPORTED), ("act", 5, L.MEBP_EINVAL), ("ffn", 100, L.MEBP_EUNSUPPORTED),
     ("lora_mask", 1 << 9, L.MEBP_EINVAL), ("n_layers", 0, L.MEBP_EINVAL), ("vocab", 1000, L.MEBP_EUNSUPPORTED),
+    ("arch", 1 << 4, L.MEBP_EINVAL),
 ])
 def test_config_rejected(built_lib, field, value, code):
     c = make_config(MINI)
