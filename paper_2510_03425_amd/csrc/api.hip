@@ -468,8 +468,13 @@ hipError_t lora_bwd(const Ctx& x, const mebp_layer_lora* lora, const mebp_layer_
 
 // Forward of one layer. keep=false: full forward to x_out. keep=true: recompute for the
 // backward (stops after z and its LoRA down-projection; x_out unused).
+// next_norm (forward loop only): the RMSNorm weights of the next block's input norm; the
+// down projection's split-K finalize then also writes that block's normalised input (into
+// `next_out`, default the activation slot `a`; one row kernel fewer per layer), and a_ready
+// tells the next layer to skip its own input norm.
 int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_layer_lora* lora, const float* x_in,
-                  float* x_out, const float* rope, bool keep) {
+                  float* x_out, const float* rope, bool keep, const float* next_norm = nullptr,
+                  bool a_ready = false, f16* next_out = nullptr) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
   f16* a = xs<f16>(x, S_A);
@@ -483,7 +488,7 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   f16* u = xs<f16>(x, S_U);
   f16* z = xs<f16>(x, S_Z);
 
-  HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
+  if (!a_ready) HIP_TRY(launch_rmsnorm_fwd(x_in, base->norm_attn, D.N, D.d, c->rms_eps, a, nullptr, x.st));
   hipEvent_t lr;
   HIP_TRY(lora_down(x, lora, a, D.d, {MEBP_Q, MEBP_K, MEBP_V}, &lr));
   // bias and per-head norm come between the projection and RoPE: then RoPE moves out of the
@@ -549,10 +554,14 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
     HIP_TRY(launch_gemm_nt(nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, td, D.d, nullptr, 0)}), NT_STORE_F32,
                            x.st, lr));
     if (!keep) HIP_TRY(launch_resid_rmsnorm(h, td, base->post_mlp_norm, D.N, D.d, c->rms_eps, x_out, x.st));
-  } else if (!keep)
-    HIP_TRY(launch_gemm_nt(nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)}), NT_STORE_F32, x.st,
-                           lr));
-  else if (lr)
+  } else if (!keep) {
+    NtArgs na = nt_args(x, z, D.F, {nt_seg(x, base, lora, MEBP_DOWN, x_out, D.d, h, D.d)});
+    if (next_norm) {
+      na.norm_w = next_norm;  // y = h + down(z), and the next block's input RMSNorm(y)
+      na.norm_out = next_out ? next_out : a;
+    }
+    HIP_TRY(launch_gemm_nt(na, NT_STORE_F32, x.st, lr));
+  } else if (lr)
     HIP_TRY(hipStreamWaitEvent(x.st, lr, 0));  // u of the down projection is read by the backward
   return MEBP_OK;
 }
@@ -686,7 +695,7 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
 }
 
 int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const float* x_last, const int32_t* ids,
-            float* loss, float* dx_last, bf16* dx_last_bf16) {
+            float* loss, float* dx_last, bf16* dx_last_bf16, bool hf_ready = false) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
   const int V = c->vocab;
@@ -702,7 +711,7 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
   const float inv_n = 1.0f / (float)((long long)x.B * (x.T - 1));
 
   HIP_TRY(launch_targets(ids, x.B, x.T, c->vocab, tgt, x.st));
-  HIP_TRY(launch_rmsnorm_fwd(x_last, norm_final, D.N, D.d, c->rms_eps, hf, nullptr, x.st));
+  if (!hf_ready) HIP_TRY(launch_rmsnorm_fwd(x_last, norm_final, D.N, D.d, c->rms_eps, hf, nullptr, x.st));
   {
     NtArgs a{};
     a.X = hf; a.lda = D.d; a.M = D.N; a.K = D.d; a.nseg = 1;
@@ -887,11 +896,18 @@ int train_step_impl(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
       const float* rope = is_global(cfg, l) ? rope_g : rope_l;
       // the slot of x_{l+1} last held x_{l+1-R}: its copy to the host must be done
       if (off && l + 1 >= off->R) HIP_TRY(hipStreamWaitEvent(x.st, off->ev_out[(l + 1) % off->R], 0));
-      if ((e = layer_forward(xf, l, &layers[l], &lora[l], ck(l), ck(l + 1), rope, false))) return e;
+      // the next layer's input norm rides on this layer's down-projection finalize (not with
+      // sandwich norms, whose output norm is a kernel of its own)
+      const bool fuse = !(cfg->arch & MEBP_ARCH_SANDWICH);
+      const float* nn = !fuse ? nullptr : l + 1 < L ? layers[l + 1].norm_attn : norm_final;
+      f16* nout = l + 1 < L ? nullptr : slot<f16>(ws, x.L, S_HF);
+      if ((e = layer_forward(xf, l, &layers[l], &lora[l], ck(l), ck(l + 1), rope, false, nn, fuse && l > 0, nout)))
+        return e;
       if (off && (e = save(l + 1, x.st))) return e;
     }
   }
   float* g = slot<float>(ws, x.L, S_GRAD);
+  const bool hf_fused = !(cfg->arch & MEBP_ARCH_SANDWICH);  // the LM head's input norm ran with the last layer
   // reverse loop: recompute layer l from ckpt[l], backpropagate the upstream gradient
   Ctx top = x;
   top.set = (L - 1) & 1;  // layer l reads bf16(dy) from set l & 1
@@ -907,7 +923,7 @@ int train_step_impl(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   };
   if (!side) {
     // final linear + loss block, then the layers in reverse on the caller's stream
-    if ((e = lm_head(x, emb, norm_final, ck(L), ids, loss, g, dyb_top))) return e;
+    if ((e = lm_head(x, emb, norm_final, ck(L), ids, loss, g, dyb_top, hf_fused))) return e;
     if (off && L - off->R >= 0 && (e = fetch(L - off->R, x.st))) return e;
     for (int l = L - 1; l >= 0; --l) {
       Ctx b = x;
@@ -940,7 +956,7 @@ int train_step_impl(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
     // the first recompute)
     if ((e = recompute(L - 1))) return e;
     HIP_TRY(hipEventRecord(side->ev_rec, side->st));
-    if ((e = lm_head(x, emb, norm_final, ck(L), ids, loss, g, dyb_top))) return e;
+    if ((e = lm_head(x, emb, norm_final, ck(L), ids, loss, g, dyb_top, hf_fused))) return e;
     if (off && L - off->R >= 0 && (e = fetch(L - off->R, x.st))) return e;
     for (int l = L - 1; l >= 0; --l) {
       HIP_TRY(hipStreamWaitEvent(x.st, side->ev_rec, 0));  // recompute(l) done
