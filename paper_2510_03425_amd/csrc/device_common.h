@@ -97,6 +97,25 @@ DEV float wave_max(float v) {
   return v;
 }
 
+// Workgroup placement. The dispatcher deals consecutive workgroup ids round-robin to the
+// 8 XCDs, each with its own L2. xcd_tile() remaps the ids so that every XCD receives a
+// contiguous range of logical tiles (numbered x fastest, then y, then z): tiles that read
+// the same row block of the large operand then share one L2 instead of fetching it once per
+// XCD. A bijection for any grid size. Used by the large-tile transposed GEMM, whose gradient
+// row blocks (up to 20480 wide) are the large operand; the forward GEMMs and the 128x128
+// kernels for few tokens keep the plain order, which measured faster there (each XCD then
+// touches few weight column blocks; at few tokens everything stays in the last-level cache).
+struct TileId {
+  int x, y, z;
+};
+DEV TileId xcd_tile() {
+  const int gx = gridDim.x, gy = gridDim.y, total = gx * gy * (int)gridDim.z;
+  const int lin = (int)blockIdx.x + gx * ((int)blockIdx.y + gy * (int)blockIdx.z);
+  const int xcd = lin & 7, local = lin >> 3, per = total >> 3, rem = total & 7;
+  const int logical = xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+  return TileId{logical % gx, (logical / gx) % gy, logical / (gx * gy)};
+}
+
 // Raw buffer resources: loads through them return 0 past `bytes` (no per-element bounds
 // branches), and offsets are 32-bit VGPR values. Every resource is based at the first row
 // a workgroup touches, so a region stays far below 4 GiB.

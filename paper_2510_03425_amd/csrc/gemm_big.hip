@@ -653,9 +653,10 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   __shared__ __attribute__((aligned(16))) u16 Bs2[2][BN * LDT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int c0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  const TileId tl = xcd_tile();
+  const int c0 = tl.x * BN, m0 = tl.y * BM;
   const int Kout = a.Kout, Kh = Kout >> 1, kgroups = (Kout + 31) >> 5;
-  const int z = blockIdx.z, S = gridDim.z;
+  const int z = tl.z, S = gridDim.z;
 
   int ntl[3], total = 0;
 #pragma unroll
