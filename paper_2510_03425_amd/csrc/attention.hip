@@ -138,6 +138,14 @@ template <class Op>
 DEV uint4 pack_frag(const f32x4& t0, const f32x4& t1) {
   return make_uint4(Op::pack(t0[0], t0[1]), Op::pack(t0[2], t0[3]), Op::pack(t1[0], t1[1]), Op::pack(t1[2], t1[3]));
 }
+// Tile of this workgroup: (query or key block [x chunk], head, sequence). Unsplit grids (long
+// sequences) use the XCD-aware order, so that the blocks of one head, which read the same
+// K/V (or Q/dO) rows, share an L2; split grids keep the plain order.
+DEV TileId attn_tile(int nck) {
+  if (nck) return TileId{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+  return xcd_tile();
+}
+
 // ------------------------------------------------------------------------------ forward
 // 64 queries (4 waves of 16) of one head per workgroup, 64-key blocks. With `nck` > 0 the
 // key range of the query tile is split into chunks of `ck` keys, one per workgroup
@@ -150,8 +158,9 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a, float* part,
   __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDK];
   __shared__ __attribute__((aligned(16))) u16 Vt[DH * LDV];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int tile = nck ? (int)blockIdx.x / nck : (int)blockIdx.x, chunk = nck ? (int)blockIdx.x % nck : 0;
-  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
+  const TileId id = attn_tile(nck);
+  const int tile = nck ? id.x / nck : id.x, chunk = nck ? id.x % nck : 0;
+  const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp;
   const int q0 = tile * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
@@ -331,8 +340,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDK];
   __shared__ __attribute__((aligned(16))) u16 Vt[DH * LDV];
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), hl = lane >> 5;
-  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
-  const int q0 = blockIdx.x * (32 * NW), qw = q0 + 32 * w, q = qw + (lane & 31);
+  const TileId id = attn_tile(0);
+  const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp;
+  const int q0 = id.x * (32 * NW), qw = q0 + 32 * w, q = qw + (lane & 31);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
@@ -518,8 +528,9 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
   __shared__ __attribute__((aligned(16))) u16 dOt[DH * LDT_]; // bf16
   __shared__ float lse_s[QB], del_s[QB];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int kblk = nck ? (int)blockIdx.x / nck : (int)blockIdx.x, chunk = nck ? (int)blockIdx.x % nck : 0;
-  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
+  const TileId id = attn_tile(nck);
+  const int kblk = nck ? id.x / nck : id.x, chunk = nck ? id.x % nck : 0;
+  const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
   const int k0 = kblk * 64, kw = k0 + 16 * w, key = kw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
@@ -658,8 +669,9 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a, float* pa
   __shared__ __attribute__((aligned(16))) u16 Vs[KB * LDN];   // bf16 (dP)
   __shared__ __attribute__((aligned(16))) u16 Kt[DH * LDT_];  // bf16 (dQ product)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int tile = nck ? (int)blockIdx.x / nck : (int)blockIdx.x, chunk = nck ? (int)blockIdx.x % nck : 0;
-  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp;
+  const TileId id = attn_tile(nck);
+  const int tile = nck ? id.x / nck : id.x, chunk = nck ? id.x % nck : 0;
+  const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp;
   const int q0 = tile * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
@@ -821,8 +833,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
   __shared__ __attribute__((aligned(16))) u16 dOt[DH * LDT];  // bf16 [e][q]
   __shared__ __attribute__((aligned(16))) float lse_s[QB], del_s[QB];
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), hl = lane >> 5;
-  const int T = a.T, h = blockIdx.y, b = blockIdx.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
-  const int k0 = blockIdx.x * (32 * NW), kw = k0 + 32 * w, key = kw + (lane & 31);
+  const TileId id = attn_tile(0);
+  const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
+  const int k0 = id.x * (32 * NW), kw = k0 + 32 * w, key = kw + (lane & 31);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
