@@ -62,14 +62,40 @@ __global__ void k_embed(const uint8_t* q4, const uint16_t* scale, int d, int gro
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One wave per row, float4 accesses (d % 4 == 0).
+// One wave per row, float4 accesses (d % 4 == 0). Rows of up to 64 * RC float4s are held in
+// registers: every load of the row is issued before the reduction and the row is read once.
+constexpr int RC = 16;  // rows up to 4096 values take the register path
+constexpr int RCB = 12;  // (backward: two row arrays, up to 3072 values)
 __global__ __launch_bounds__(256) void k_rmsnorm_fwd(const float* x, const float* w, int n, int d, float eps,
                                                      f16* y, float* rstd_out) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= n) return;
   const float4* xr = (const float4*)(x + (size_t)row * d);
+  const float4* wr = (const float4*)w;
+  uint2* yr = (uint2*)(y + (size_t)row * d);
   const int d4 = d >> 2;
   float ss = 0.f;
+  if (d4 <= 64 * RC) {
+    float4 v[RC];
+#pragma unroll
+    for (int q = 0; q < RC; ++q) {
+      const int c = lane + 64 * q;
+      v[q] = c < d4 ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      ss += v[q].x * v[q].x + v[q].y * v[q].y + v[q].z * v[q].z + v[q].w * v[q].w;
+    }
+    ss = wave_sum(ss);
+    const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+    if (rstd_out && lane == 0) rstd_out[row] = rs;
+#pragma unroll
+    for (int q = 0; q < RC; ++q) {
+      const int c = lane + 64 * q;
+      if (c >= d4) break;
+      const float4 g = wr[c];
+      yr[c] = make_uint2(pack_f16x2(v[q].x * rs * g.x, v[q].y * rs * g.y),
+                         pack_f16x2(v[q].z * rs * g.z, v[q].w * rs * g.w));
+    }
+    return;
+  }
   for (int c = lane; c < d4; c += 64) {
     const float4 v = xr[c];
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
@@ -77,8 +103,6 @@ __global__ __launch_bounds__(256) void k_rmsnorm_fwd(const float* x, const float
   ss = wave_sum(ss);
   const float rs = 1.0f / sqrtf(ss / (float)d + eps);
   if (rstd_out && lane == 0) rstd_out[row] = rs;
-  const float4* wr = (const float4*)w;
-  uint2* yr = (uint2*)(y + (size_t)row * d);
   for (int c = lane; c < d4; c += 64) {
     const float4 v = xr[c], g = wr[c];
     yr[c] = make_uint2(pack_f16x2(v.x * rs * g.x, v.y * rs * g.y), pack_f16x2(v.z * rs * g.z, v.w * rs * g.w));
@@ -97,6 +121,41 @@ __global__ __launch_bounds__(256) void k_rmsnorm_bwd(const float* x, const float
   const float4* wr = (const float4*)w;
   const int d4 = d >> 2;
   float ss = 0.f, sd = 0.f;
+  const float4* rr = (const float4*)(resid ? resid + off : nullptr);
+  float4* o = dx ? (float4*)(dx + off) : nullptr;
+  uint2* ob = dxb ? (uint2*)(dxb + off) : nullptr;
+  if (d4 <= 64 * RCB) {
+    // rows of up to 64 * RCB float4s: x and dy held in registers, every load issued up front
+    float4 xv[RCB], gv[RCB];
+#pragma unroll
+    for (int q = 0; q < RCB; ++q) {
+      const int c = lane + 64 * q;
+      const bool ok = c < d4;
+      xv[q] = ok ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      gv[q] = ok ? gr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 ww = ok ? wr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      ss += xv[q].x * xv[q].x + xv[q].y * xv[q].y + xv[q].z * xv[q].z + xv[q].w * xv[q].w;
+      sd += xv[q].x * ww.x * gv[q].x + xv[q].y * ww.y * gv[q].y + xv[q].z * ww.z * gv[q].z + xv[q].w * ww.w * gv[q].w;
+    }
+    ss = wave_sum(ss);
+    sd = wave_sum(sd);
+    const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+    const float mean_term = rs * sd / (float)d;
+#pragma unroll
+    for (int q = 0; q < RCB; ++q) {
+      const int c = lane + 64 * q;
+      if (c >= d4) break;
+      const float4 v = xv[q], g = gv[q], ww = wr[c];
+      float4 res = rr ? rr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      res.x += rs * (ww.x * g.x - v.x * rs * mean_term);
+      res.y += rs * (ww.y * g.y - v.y * rs * mean_term);
+      res.z += rs * (ww.z * g.z - v.z * rs * mean_term);
+      res.w += rs * (ww.w * g.w - v.w * rs * mean_term);
+      if (o) o[c] = res;
+      if (ob) ob[c] = make_uint2(pack_bf16x2(res.x, res.y), pack_bf16x2(res.z, res.w));
+    }
+    return;
+  }
   for (int c = lane; c < d4; c += 64) {
     const float4 v = xr[c], g = gr[c], ww = wr[c];
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
@@ -106,9 +165,6 @@ __global__ __launch_bounds__(256) void k_rmsnorm_bwd(const float* x, const float
   sd = wave_sum(sd);
   const float rs = 1.0f / sqrtf(ss / (float)d + eps);
   const float mean_term = rs * sd / (float)d;  // mean(xhat * w * dy)
-  const float4* rr = (const float4*)(resid ? resid + off : nullptr);
-  float4* o = dx ? (float4*)(dx + off) : nullptr;
-  uint2* ob = dxb ? (uint2*)(dxb + off) : nullptr;
   for (int c = lane; c < d4; c += 64) {
     const float4 v = xr[c], g = gr[c], ww = wr[c];
     float4 res = rr ? rr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -139,23 +195,6 @@ __global__ void k_rope_table(int T, int dh, double theta, float* cs) {
   const double ang = (double)t * inv;
   cs[2 * i] = (float)cos(ang);
   cs[2 * i + 1] = (float)sin(ang);
-}
-
-// In place: pairs (e, e + dh/2) of every head rotate by the angle of (t, e).
-__global__ void k_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const float* cs) {
-  const int half = dh >> 1;
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t total = (size_t)B * T * H * half;
-  if (i >= total) return;
-  const int e = (int)(i % half);
-  const int h = (int)((i / half) % H);
-  const size_t row = i / ((size_t)half * H);
-  const int t = (int)(row % T);
-  f16* p = x + row * ld + h * dh;
-  const float x1 = (float)p[e], x2 = (float)p[e + half];
-  const float c = cs[2 * (t * half + e)], s = cs[2 * (t * half + e) + 1];
-  p[e] = (f16)(x1 * c - x2 * s);
-  p[e + half] = (f16)(x2 * c + x1 * s);
 }
 
 // z = act(g) * u, 8 elements per thread
@@ -459,9 +498,12 @@ hipError_t launch_rope_table(int T, int dh, double theta, float* cs, hipStream_t
   return hipGetLastError();
 }
 hipError_t launch_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st) {
-  const size_t tot = (size_t)B * T * H * (dh / 2);
-  MEBP_TIMED(st, "rope_fwd", 0.0, (double)tot * 8,
-             hipLaunchKernelGGL(k_rope_fwd, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, B, T, H, dh, cs));
+  // the bias / head-norm kernel without bias or norm: 4 columns and their partners per thread
+  const int n = B * T;
+  const size_t tot = (size_t)n * H * (dh >> 3);
+  MEBP_TIMED(st, "rope_fwd", 0.0, (double)n * H * dh * 4,
+             hipLaunchKernelGGL(k_qkv_post, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, n, T, H, dh,
+                                (const float*)nullptr, (const float*)nullptr, 0.f, (f16*)nullptr, cs, 1));
   return hipGetLastError();
 }
 hipError_t launch_act_fwd(const f16* g, const f16* u, f16* z, size_t n, int act, hipStream_t st) {
