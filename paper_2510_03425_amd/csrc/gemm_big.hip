@@ -505,6 +505,59 @@ DEV void wait_vmcnt() {
 // eight 16-byte chunks are stored at position chunk ^ (row & 7), so that the MFMA fragment
 // reads (32 rows, one chunk each) spread over all banks. The weights are loaded into
 // registers, also two tiles ahead, and decompressed by each wave for its own columns.
+// fp16 / fp32 store (LoRA up-projection and residual included) of a wave's 128 x 64 block
+// of k_gemm_nt_lds through LDS: per 32-row block the accumulators (MFMA layout) go into the
+// wave's own 32 x 68 fp32 region, and each lane reads back 8 consecutive columns of a row
+// and stores them with 16-byte accesses (a wave instruction covers 8 whole row segments)
+// instead of 2- or 4-byte stores in the MFMA layout. The residual rows of a block are all
+// loaded before its accumulators are staged. Requires N % 8 == 0 and 16-byte aligned rows.
+template <int EPI>
+DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int mw0, int wcol0, int lane,
+                      float* ep) {
+  constexpr int LDE = 68;
+  if (sg.lora_B) lora_mfma<2>(acc, sg.lora_u, a.r, mw0, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, sg.N, lane);
+  const int rr = lane >> 3, ch = lane & 7, n = wcol0 + 8 * ch;
+  const bool nok = n < sg.N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float4 res[4][2];
+    if (sg.resid) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int m = mw0 + 32 * i + 8 * p + rr;
+        const bool ok = nok && m < a.M;
+        const float* src = sg.resid + (ok ? (size_t)m * sg.ldr + n : 0);
+        res[p][0] = ok ? *(const float4*)src : make_float4(0.f, 0.f, 0.f, 0.f);
+        res[p][1] = ok ? *(const float4*)(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) ep[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] = acc[i][j][q];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int r = 8 * p + rr, m = mw0 + 32 * i + r;
+      float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
+      if (sg.resid) {
+        v0.x += res[p][0].x; v0.y += res[p][0].y; v0.z += res[p][0].z; v0.w += res[p][0].w;
+        v1.x += res[p][1].x; v1.y += res[p][1].y; v1.z += res[p][1].z; v1.w += res[p][1].w;
+      }
+      if (nok && m < a.M) {
+        if constexpr (EPI == NT_STORE_F16) {
+          const uint4 o = make_uint4(pack_f16x2(v0.x, v0.y), pack_f16x2(v0.z, v0.w), pack_f16x2(v1.x, v1.y),
+                                     pack_f16x2(v1.z, v1.w));
+          *(uint4*)((f16*)sg.out + (size_t)m * sg.ldo + n) = o;
+        } else {
+          float* dst = (float*)sg.out + (size_t)m * sg.ldo + n;
+          *(float4*)dst = v0;
+          *(float4*)(dst + 4) = v1;
+        }
+      }
+    }
+  }
+}
+
 constexpr int LDS_STAGES = 3, LDS_STAGE_BYTES = BM * BK * 2;
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
@@ -636,13 +689,39 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     if (k < kt_end) step(IC<0>{}, k);
     if (k + 1 < kt_end) step(IC<1>{}, k + 1);
   }
-  nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
+  if constexpr (EPI != NT_LOGITS) {
+    // the ring is idle once the clamped loads of the last steps have landed and every wave
+    // has read its last tile; each wave then stages through its own 32 x 68 fp32 region
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    uint8_t* reg = (wave < 3 ? lds0 : wave < 6 ? lds1 : lds2) + (wave % 3) * (32 * 68 * 4);
+    nt_lds_store<EPI>(acc, a, sg, m0 + wm * 128, wcol0, lane, reinterpret_cast<float*>(reg));
+  } else {
+    nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
+  }
 }
 
 // ---------------------------------------------------------------------------- transposed
 // C[m][c] = sum_seg sum_n G_seg[m][n] W_seg[n][c] (+ sum_seg du_seg A_seg), bf16 operands.
 // The weight tile (64 rows n x BN columns c) is decompressed per thread as RPT rows x 16
 // columns and written transposed, n-contiguous, into LDS.
+// Instruction order of one K step of k_gemm_tn_big. With one wave per SIMD nothing hides
+// the decompression of the next weight tile, its LDS stores or the fragment reads but the
+// wave's own MFMAs, so they are spread evenly between them: the first fragment reads, then
+// per MFMA four VALU instructions, one LDS store and one fragment read.
+template <int NJ>
+DEV void sched_tn_step() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 4 + NJ, 0);
+#pragma unroll
+  for (int i = 0; i < 16 * NJ; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+}
+
 template <int BN, int EPI, int AMODE>
 __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   constexpr int NJ = BN / 64;
@@ -786,6 +865,7 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
       gload(IC<I>{}, min(t + 2, t_end - 1));
       mma_tile<OpBF16, NJ>(As2[I], Bs2[I], wm, wn, lane, acc);
       sstore(IC<1 - I>{}, IC<1 - I>{});
+      sched_tn_step<NJ>();
       __syncthreads();
     };
     gload(IC<0>{}, t_begin);
@@ -824,16 +904,27 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
     }
     if constexpr (EPI == TN_ACT_BWD && 4 * 64 * (32 * NJ + 4) * 4 <= (int)sizeof(As2)) {
       // dz -> (dg, du) reads g, u and writes dg, du: the accumulators go through LDS so that
-      // every lane handles 4 consecutive columns of a row (8-byte accesses, a wave covers
-      // whole 128-byte row segments) instead of 2-byte accesses in the MFMA layout. Each
-      // wave stages its 128 x 32NJ block in two halves of 64 rows in its own LDS region.
-      constexpr int CW = 32 * NJ, LDE = CW + 4, CPR = CW / 4, RPP = 64 / CPR;
+      // every lane handles 8 consecutive columns of a row (16-byte accesses, a wave covers
+      // eight whole 128-byte row segments) instead of 2-byte accesses in the MFMA layout.
+      // Each wave stages its 128 x 32NJ block in two halves of 64 rows in its own LDS region;
+      // the g and u loads of a half are all issued before its accumulators are staged, so
+      // their latency is paid once per half. Kout is a multiple of 32 (a group divides it).
+      constexpr int CW = 32 * NJ, LDE = CW + 4, CPR = CW / 8, RPP = 64 / CPR, NP = 64 / RPP;
       float* ep = reinterpret_cast<float*>(&As2[0][0]) + wave * 64 * LDE;
       const int rr = lane / CPR, ch = lane % CPR;
-      const int cbase = c0 + wn * CW + 4 * ch;
+      const int cbase = c0 + wn * CW + 8 * ch;
       __syncthreads();  // every wave is done with the main loop's LDS tiles
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
+        uint4 gw[NP], uw[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const int m = m0 + wm * 128 + 64 * hh + p * RPP + rr;
+          const bool ok = m < a.M && cbase < Kout;
+          const size_t idx = ok ? (size_t)m * a.ldgu + cbase : 0;
+          gw[p] = ok ? *(const uint4*)((const f16*)a.g + idx) : make_uint4(0, 0, 0, 0);
+          uw[p] = ok ? *(const uint4*)((const f16*)a.u + idx) : make_uint4(0, 0, 0, 0);
+        }
 #pragma unroll
         for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
@@ -843,24 +934,23 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
               ep[(32 * ii + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] =
                   acc[2 * hh + ii][j][q];
         __syncthreads();
-#pragma unroll 4
-        for (int pss = 0; pss < 64 / RPP; ++pss) {
-          const int r = pss * RPP + rr, m = m0 + wm * 128 + 64 * hh + r;
-          if (m >= a.M || cbase >= Kout) continue;  // Kout is a multiple of 4
-          const float4 v = *(const float4*)(ep + r * LDE + 4 * ch);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const int r = p * RPP + rr, m = m0 + wm * 128 + 64 * hh + r;
+          if (m >= a.M || cbase >= Kout) continue;
+          const float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
           const size_t idx = (size_t)m * a.ldgu + cbase;
-          const uint2 gw = *(const uint2*)((const f16*)a.g + idx), uw = *(const uint2*)((const f16*)a.u + idx);
-          const float gv[4] = {f16_lo(gw.x), f16_hi(gw.x), f16_lo(gw.y), f16_hi(gw.y)};
-          const float uv[4] = {f16_lo(uw.x), f16_hi(uw.x), f16_lo(uw.y), f16_hi(uw.y)};
-          const float dz[4] = {v.x, v.y, v.z, v.w};
-          float dg[4], du[4];
+          const uint32_t gq[4] = {gw[p].x, gw[p].y, gw[p].z, gw[p].w}, uq[4] = {uw[p].x, uw[p].y, uw[p].z, uw[p].w};
+          const float dz[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+          uint32_t og[4], ou[4];
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            dg[t] = dz[t] * uv[t] * act_grad_f(gv[t], a.act);
-            du[t] = dz[t] * act_f(gv[t], a.act);
+            const float g0 = f16_lo(gq[t]), g1 = f16_hi(gq[t]), u0 = f16_lo(uq[t]), u1 = f16_hi(uq[t]);
+            og[t] = pack_bf16x2(dz[2 * t] * u0 * act_grad_f(g0, a.act), dz[2 * t + 1] * u1 * act_grad_f(g1, a.act));
+            ou[t] = pack_bf16x2(dz[2 * t] * act_f(g0, a.act), dz[2 * t + 1] * act_f(g1, a.act));
           }
-          *(uint2*)((bf16*)a.g + idx) = make_uint2(pack_bf16x2(dg[0], dg[1]), pack_bf16x2(dg[2], dg[3]));
-          *(uint2*)((bf16*)a.u + idx) = make_uint2(pack_bf16x2(du[0], du[1]), pack_bf16x2(du[2], du[3]));
+          *(uint4*)((bf16*)a.g + idx) = make_uint4(og[0], og[1], og[2], og[3]);
+          *(uint4*)((bf16*)a.u + idx) = make_uint4(ou[0], ou[1], ou[2], ou[3]);
         }
         __syncthreads();  // before the next half overwrites the staging area
       }
@@ -951,7 +1041,16 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
     const char* e = getenv("MEBP_NT_LDS");
     return e && *e ? atoi(e) : 1;
   }();
-  if (bn == 256 && use_lds && a.K % 8 == 0) {
+  // the LDS-direct kernel stores fp16 / fp32 outputs as 16-byte row chunks: one split,
+  // segment widths that are multiples of 8 and 16-byte aligned rows
+  bool vec = S == 1;
+  for (int s = 0; s < a.nseg && epi != NT_LOGITS; ++s) {
+    const NtSeg& g = a.seg[s];
+    const size_t esz = epi == NT_STORE_F16 ? 2 : 4;
+    vec = vec && g.N % 8 == 0 && (((uintptr_t)g.out | (size_t)g.ldo * esz) & 15) == 0 &&
+          (!g.resid || (((uintptr_t)g.resid | (size_t)g.ldr * 4) & 15) == 0);
+  }
+  if (bn == 256 && use_lds && a.K % 8 == 0 && (epi == NT_LOGITS || vec)) {
 #define NT_LDS(EPI_) \
   MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_nt_lds<EPI_>), grid, dim3(512), 0, st, b))
     if (epi == NT_LOGITS)
