@@ -36,6 +36,26 @@ typedef uint16_t u16;
 
 DEV uint4 load_frag_global(const void* p, bool ok) { return ok ? *(const uint4*)p : make_uint4(0, 0, 0, 0); }
 
+// The causal window mask as one unsigned compare per element. Query i sees key j iff
+// j <= i < T, j < T and (W == 0 or i - j < W): for a fixed query the visible keys form the
+// range lo .. lo + span, and so do the visible queries of a fixed key. An empty range is
+// lo = 2^30, span = 0 (x - lo is then negative, i.e. a huge unsigned value).
+struct VisRange {
+  int lo;
+  uint32_t span;
+};
+DEV VisRange keys_of_query(int q, int T, int W) {
+  if (q >= T) return {1 << 30, 0u};
+  const int lo = W ? max(0, q - W + 1) : 0;
+  return {lo, (uint32_t)(q - lo)};
+}
+DEV VisRange queries_of_key(int key, int T, int W) {
+  if (key >= T) return {1 << 30, 0u};
+  const int hi = W ? min(T - 1, key + W - 1) : T - 1;
+  return {key, (uint32_t)(hi - key)};
+}
+DEV bool visible(const VisRange& v, int x) { return (uint32_t)(x - v.lo) <= v.span; }
+
 // Tile staging through registers: load() issues every global load of a tile at once (rows
 // at or past `rows_ok` read as zero), the store functions write it to LDS. Kernels load
 // the next tile before the products of the current one and store it after them, so the
@@ -162,6 +182,7 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a, float* part,
   const int tile = nck ? id.x / nck : id.x, chunk = nck ? id.x % nck : 0;
   const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp;
   const int q0 = tile * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
+  const VisRange kvis = keys_of_query(q, a.T, a.window);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
@@ -210,8 +231,7 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a, float* part,
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int key = kv0 + kt * 16 + 4 * (lane >> 4) + r;
-        const bool vis = key <= q && key < T && (a.window == 0 || q - key < a.window);
+        const bool vis = visible(kvis, kv0 + kt * 16 + 4 * (lane >> 4) + r);
         const float v = vis ? s[kt][r] * sc : -INFINITY;
         s[kt][r] = v;
         mloc = fmaxf(mloc, v);
@@ -362,6 +382,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
   const int kv_hi = min(T, q0 + 32 * NW);
   // wave's own visible key range (for skipping fully masked blocks)
   const int w_lo = a.window ? max(0, qw - a.window + 1) : 0, w_hi = min(T, qw + 32) - 1;
+  const VisRange kvis = keys_of_query(q, T, a.window);
 
   uint4 kr[KCH], vr[VBL][8];
   auto gload = [&](int kv0) {
@@ -434,15 +455,18 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = kv0 + kt * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-        const bool vis = key <= q && key < T && (a.window == 0 || q - key < a.window);
+        const bool vis = visible(kvis, kv0 + kt * 32 + 8 * (r >> 2) + 4 * hl + (r & 3));
         const float v = vis ? s[kt][r] * sc : -INFINITY;
         s[kt][r] = v;
         mloc = fmaxf(mloc, v);
       }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_i, mloc);
-    const float alpha = exp2f(m_i - m_new);
+    // The running maximum only moves when a row's block maximum exceeds it by more than
+    // 2^8 (base-2 domain): the probabilities stay below 256 and the sum and the output are
+    // both taken relative to the same stale maximum, so the result is unchanged; most
+    // blocks then skip the rescale of the output accumulators. (Head dim 256 rescales
+    // every block: the branch would push its 256 accumulators past the register file.)
+    const float m_new = mloc > m_i + 8.f ? mloc : m_i;
     float ls = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -453,10 +477,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
         ls += p;
       }
     ls += __shfl_xor(ls, 32, 64);
-    l_i = l_i * alpha + ls;
-    m_i = m_new;
+    if (DH == 256 || __builtin_amdgcn_ballot_w64(m_new != m_i)) {
+      const float alpha = exp2f(m_i - m_new);
+      l_i *= alpha;
 #pragma unroll
-    for (int t = 0; t < NTO; ++t) oacc[t] *= alpha;
+      for (int t = 0; t < NTO; ++t) oacc[t] *= alpha;
+    }
+    l_i += ls;
+    m_i = m_new;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const f32x16& st = s[kk >> 1];
@@ -532,6 +560,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
   const int kblk = nck ? id.x / nck : id.x, chunk = nck ? id.x % nck : 0;
   const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
   const int k0 = kblk * 64, kw = k0 + 16 * w, key = kw + (lane & 15);
+  const VisRange qvis = queries_of_key(key, T, a.window);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
@@ -598,8 +627,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
     for (int qt = 0; qt < NQT; ++qt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int ql = qt * 16 + 4 * (lane >> 4) + r, qq = qb0 + ql;
-        const bool vis = key <= qq && qq < T && key < T && (a.window == 0 || qq - key < a.window);
+        const int ql = qt * 16 + 4 * (lane >> 4) + r;
+        const bool vis = visible(qvis, qb0 + ql);
         const float p = vis ? exp2f(s[qt][r] * sc - lse_s[ql]) : 0.f;
         s[qt][r] = p;
         dp[qt][r] = p * (dp[qt][r] - del_s[ql]);
@@ -663,7 +692,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
 // Without it (head dim 256) the kernel stays within 256 registers per lane, so that two
 // workgroups share a compute unit and hide each other's load latency instead.
 template <int DH, int KB, bool PF>
-__global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a, float* part, int nck, int ck) {
+__global__ __launch_bounds__(256, PF ? 1 : 2) void k_attn_bwd_dq(const AttnArgs a, float* part, int nck, int ck) {
   constexpr int LDN = DH + 8, LDT_ = KB + 8, NKS = DH / 32, NT = DH / 16, NKT = KB / 16;
   __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDN];   // fp16 (scores)
   __shared__ __attribute__((aligned(16))) u16 Vs[KB * LDN];   // bf16 (dP)
@@ -673,6 +702,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a, float* pa
   const int tile = nck ? id.x / nck : id.x, chunk = nck ? id.x % nck : 0;
   const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp;
   const int q0 = tile * 64, qw = q0 + 16 * w, q = qw + (lane & 15);
+  const VisRange kvis = keys_of_query(q, a.T, a.window);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
@@ -730,8 +760,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dq(const AttnArgs a, float* pa
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int key = kv0 + kt * 16 + 4 * (lane >> 4) + r;
-        const bool vis = key <= q && key < T && q < T && (a.window == 0 || q - key < a.window);
+        const bool vis = visible(kvis, kv0 + kt * 16 + 4 * (lane >> 4) + r);
         const float p = vis ? exp2f(s[kt][r] * sc - lse2) : 0.f;
         dp[kt][r] = p * (dp[kt][r] - del);
       }
@@ -836,6 +865,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
   const TileId id = attn_tile(0);
   const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
   const int k0 = id.x * (32 * NW), kw = k0 + 32 * w, key = kw + (lane & 31);
+  const VisRange qvis = queries_of_key(key, T, a.window);
   const float sc = LOG2E / sqrtf((float)DH);
   const size_t rowb = (size_t)b * T;
 
@@ -935,8 +965,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
       const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dl[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
-        const int r = 4 * g + rr, qq = qb0 + 8 * g + 4 * hl + rr;
-        const bool vis = key <= qq && qq < T && key < T && (a.window == 0 || qq - key < a.window);
+        const int r = 4 * g + rr;
+        const bool vis = visible(qvis, qb0 + 8 * g + 4 * hl + rr);
         const float p = vis ? exp2f(sv[r] * sc - lv[rr]) : 0.f;
         sv[r] = p;
         dp[r] = p * (dp[r] - dl[rr]);
