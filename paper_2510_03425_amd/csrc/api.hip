@@ -722,6 +722,8 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
   }
   HIP_TRY(launch_ce_rows(stats, x.L.ntiles, tl, tgt, D.N, lse, rl, x.st));
   HIP_TRY(launch_ce_loss(rl, tgt, D.N, inv_n, loss, x.st));
+  // softmax probabilities over the logits (in place, bf16), then dH = P E on plain operands
+  HIP_TRY(launch_ce_probs(reinterpret_cast<uint16_t*>(logits), D.N, V, lse, tgt, x.st));
   {
     TnArgs t{};
     set_scratch(x, t);
@@ -730,7 +732,7 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
     t.seg[0].q4 = emb->q4; t.seg[0].scale = emb->scale; t.seg[0].N = V;
     t.out = part; t.ldo = D.d; t.splits = x.L.lm_splits;
     t.lse = lse; t.tgt = tgt;
-    HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_SOFTMAX, x.st));
+    HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_BF16, x.st));
   }
   HIP_TRY(launch_ce_dh_reduce(part, x.L.lm_splits, D.N, D.d, emb->q4, emb->scale, tgt, inv_n, dhf, x.st));
   HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, D.N, D.d, c->rms_eps, dx_last,

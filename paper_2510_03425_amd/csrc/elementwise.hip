@@ -256,6 +256,35 @@ __global__ __launch_bounds__(256) void k_ce_loss(const float* row_loss, int M, f
   if (threadIdx.x == 0) loss[0] = ((red[0] + red[1]) + (red[2] + red[3])) * inv_n;
 }
 
+// Softmax probabilities of the LM head, p[m][v] = exp(logit[m][v] - lse[m]) for rows with a
+// target and 0 for the others, rounded to bf16 and written over the fp16 logits in place:
+// the A operand of the dH product, computed once instead of in every column tile of it.
+__global__ __launch_bounds__(256) void k_ce_probs(uint16_t* lg, int M, int V, const float* lse, const int32_t* tgt) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if ((V & 7) == 0) {
+    const size_t per_row = (size_t)(V >> 3);
+    if (i >= (size_t)M * per_row) return;
+    const int m = (int)(i / per_row);
+    uint4* p = reinterpret_cast<uint4*>(lg) + i;  // rows are whole 16-byte chunks
+    uint4 o = make_uint4(0, 0, 0, 0);
+    if (tgt[m] >= 0) {
+      const float l = lse[m];
+      const uint4 h = *p;
+      o = make_uint4(pack_bf16x2(__expf(f16_lo(h.x) - l), __expf(f16_hi(h.x) - l)),
+                     pack_bf16x2(__expf(f16_lo(h.y) - l), __expf(f16_hi(h.y) - l)),
+                     pack_bf16x2(__expf(f16_lo(h.z) - l), __expf(f16_hi(h.z) - l)),
+                     pack_bf16x2(__expf(f16_lo(h.w) - l), __expf(f16_hi(h.w) - l)));
+    }
+    *p = o;
+  } else {
+    if (i >= (size_t)M * V) return;
+    const int m = (int)(i / (size_t)V);
+    float v = 0.f;
+    if (tgt[m] >= 0) v = __expf(half_bits_to_f32(lg[i]) - lse[m]);
+    lg[i] = __builtin_bit_cast(uint16_t, (bf16)v);
+  }
+}
+
 // dhf[m][k] = inv_n * (sum_s part[s][m][k] - E[tgt[m]][k]) for rows with a target, else 0
 __global__ void k_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
                                const uint16_t* escale, const int32_t* tgt, float inv_n, float* dhf) {
@@ -529,6 +558,12 @@ hipError_t launch_ce_loss(const float* row_loss, const int32_t* tgt, int M, floa
   (void)tgt;
   MEBP_TIMED(st, "ce_loss", 0.0, (double)M * 4,
              hipLaunchKernelGGL(k_ce_loss, dim3(1), dim3(256), 0, st, row_loss, M, inv_n, loss));
+  return hipGetLastError();
+}
+hipError_t launch_ce_probs(uint16_t* logits, int M, int V, const float* lse, const int32_t* tgt, hipStream_t st) {
+  const size_t tot = (V & 7) == 0 ? (size_t)M * (V >> 3) : (size_t)M * V;
+  MEBP_TIMED(st, "ce_probs", 0.0, (double)M * V * 4,
+             hipLaunchKernelGGL(k_ce_probs, dim3(blocks_for(tot, 256)), dim3(256), 0, st, logits, M, V, lse, tgt));
   return hipGetLastError();
 }
 hipError_t launch_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,

@@ -1085,6 +1085,7 @@ hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S
                               hipStream_t st) {
   const dim3 grid((a.Kout + bn - 1) / bn, (a.M + BM - 1) / BM, S);
   const char* name = amode == TN_A_SOFTMAX ? "gemm_tn_softmax_dh"
+                     : epi == TN_PARTIAL_F32 ? "gemm_tn_probs_dh"
                      : epi == TN_STORE_F32  ? "gemm_tn_f32out"
                      : epi == TN_ACT_BWD    ? "gemm_tn_act_bwd"
                                             : "gemm_tn_bf16out";
@@ -1101,6 +1102,8 @@ hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S
       TN_BIG(BN_, TN_ACT_BWD, TN_A_BF16);                            \
     } else if (epi == TN_STORE_BF16) {                               \
       TN_BIG(BN_, TN_STORE_BF16, TN_A_BF16);                         \
+    } else if (epi == TN_PARTIAL_F32) {                              \
+      TN_BIG(BN_, TN_PARTIAL_F32, TN_A_BF16);                        \
     } else {                                                         \
       return hipErrorInvalidValue;                                   \
     }                                                                \

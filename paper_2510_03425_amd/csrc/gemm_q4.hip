@@ -1001,7 +1001,8 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, 
   }
   int Ns[3];
   for (int s = 0; s < a.nseg; ++s) Ns[s] = a.seg[s].N;
-  GemmPlan plan = plan_tn(a.M, a.Kout, Ns, a.nseg, amode == TN_A_SOFTMAX);
+  // (the partial-plane epilogue is the LM head's dH product, planned as such in both A modes)
+  GemmPlan plan = plan_tn(a.M, a.Kout, Ns, a.nseg, epi == TN_PARTIAL_F32);
   int S;
   if (epi == TN_PARTIAL_F32) {
     S = a.splits;
@@ -1038,6 +1039,10 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, 
       case TN_STORE_BF16:
         MEBP_TIMED(st, "gemm_tn_bf16out", flops, bytes,
                    hipLaunchKernelGGL((k_gemm_tn<TN_STORE_BF16, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+        break;
+      case TN_PARTIAL_F32:
+        MEBP_TIMED(st, "gemm_tn_probs_dh", flops, bytes,
+                   hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
         break;
       default: return hipErrorInvalidValue;
     }
