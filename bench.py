@@ -81,10 +81,10 @@ KERNEL_PATTERNS = {
     "gemm_nt_f16out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?0>",
     "gemm_nt_f32out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?1>",
     "gemm_nt_logits": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?2>",
-    "gemm_tn_f32out": r"k_gemm_tn(_big)?<(\d+, )?0, 0>",
-    "gemm_tn_act_bwd": r"k_gemm_tn(_big)?<(\d+, )?1, 0>",
-    "gemm_tn_softmax_dh": r"k_gemm_tn(_big)?<(\d+, )?2, 1>",
-    "gemm_tn_bf16out": r"k_gemm_tn(_big)?<(\d+, )?3, 0>",
+    "gemm_tn_f32out": r"k_gemm_tn(_big)?<(\d+, )?0>",
+    "gemm_tn_act_bwd": r"k_gemm_tn(_big)?<(\d+, )?1>",
+    "gemm_tn_probs_dh": r"k_gemm_tn(_big)?<(\d+, )?2>",
+    "gemm_tn_bf16out": r"k_gemm_tn(_big)?<(\d+, )?3>",
     "lora_rows": r"k_lora_rows<",
     "lora_outer": r"k_lora_outer<",
     "attn_fwd": r"k_attn_fwd",

@@ -731,7 +731,6 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
     t.seg[0].G = (const bf16*)logits; t.seg[0].ldg = V;
     t.seg[0].q4 = emb->q4; t.seg[0].scale = emb->scale; t.seg[0].N = V;
     t.out = part; t.ldo = D.d; t.splits = x.L.lm_splits;
-    t.lse = lse; t.tgt = tgt;
     HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_BF16, x.st));
   }
   HIP_TRY(launch_ce_dh_reduce(part, x.L.lm_splits, D.N, D.d, emb->q4, emb->scale, tgt, inv_n, dhf, x.st));

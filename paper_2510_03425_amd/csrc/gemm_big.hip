@@ -722,7 +722,7 @@ DEV void sched_tn_step() {
   }
 }
 
-template <int BN, int EPI, int AMODE>
+template <int BN, int EPI>
 __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   constexpr int NJ = BN / 64;
   constexpr int CG = BN / 16;   // 16-column groups
@@ -745,17 +745,6 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   }
   const int t_begin = (int)((long long)total * z / S), t_end = (int)((long long)total * (z + 1) / S);
 
-  float rlse[8];
-  bool rval[8];
-  if constexpr (AMODE == TN_A_SOFTMAX) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int m = m0 + ((tid + NTH * i) >> 3);
-      rval[i] = m < a.M && a.tgt[m] >= 0;
-      rlse[i] = rval[i] ? a.lse[m] : 0.f;
-    }
-  }
-
   rsrc_t rA[3], rB[3], rS[3];
 #pragma unroll
   for (int s = 0; s < 3; ++s) {
@@ -773,7 +762,6 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   uint4 ra[2][8];
   uint2 rw[2][RPT];
   uint32_t rsc[2][RPT];
-  int cur_n0[2], cur_N[2];
   f32x16 acc[4][NJ];
   zero_acc(acc);
 
@@ -800,8 +788,6 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
       const rsrc_t ra_ = s == 0 ? rA[0] : s == 1 ? rA[1] : rA[2];
       const rsrc_t rb_ = s == 0 ? rB[0] : s == 1 ? rB[1] : rB[2];
       const rsrc_t rs_ = s == 0 ? rS[0] : s == 1 ? rS[1] : rS[2];
-      cur_n0[st] = n0;
-      cur_N[st] = sg.N;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int c = tid + NTH * i;
@@ -822,25 +808,7 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
     };
     auto sstore = [&](auto S_, auto B_) {
       constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
-      if constexpr (AMODE == TN_A_SOFTMAX) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int c = tid + NTH * i;
-          uint4 p = make_uint4(0, 0, 0, 0);
-          // chunks past the reduction length were zero-filled; they must stay 0, not exp(-lse)
-          if (rval[i] && cur_n0[st] + (c & 7) * 8 < cur_N[st]) {
-            const uint32_t* h = (const uint32_t*)&ra[st][i];
-            uint32_t o[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              o[j] = pack_bf16x2(__expf(f16_lo(h[j]) - rlse[i]), __expf(f16_hi(h[j]) - rlse[i]));
-            p = make_uint4(o[0], o[1], o[2], o[3]);
-          }
-          *(uint4*)(As2[bf] + (c >> 3) * LDT + (c & 7) * 8) = p;
-        }
-      } else {
-        store_a_tile(As2[bf], tid, ra[st]);
-      }
+      store_a_tile(As2[bf], tid, ra[st]);
       float v[RPT][16];
 #pragma unroll
       for (int i = 0; i < RPT; ++i) {
@@ -1084,29 +1052,26 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
 hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S, double flops, double bytes,
                               hipStream_t st) {
   const dim3 grid((a.Kout + bn - 1) / bn, (a.M + BM - 1) / BM, S);
-  const char* name = amode == TN_A_SOFTMAX ? "gemm_tn_softmax_dh"
-                     : epi == TN_PARTIAL_F32 ? "gemm_tn_probs_dh"
+  if (amode != TN_A_BF16) return hipErrorInvalidValue;
+  const char* name = epi == TN_PARTIAL_F32 ? "gemm_tn_probs_dh"
                      : epi == TN_STORE_F32  ? "gemm_tn_f32out"
                      : epi == TN_ACT_BWD    ? "gemm_tn_act_bwd"
                                             : "gemm_tn_bf16out";
-#define TN_BIG(BN_, EPI_, AM_) \
-  MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_big<BN_, EPI_, AM_>), grid, dim3(NTH), 0, st, a))
-#define TN_BIG_EPI(BN_)                                              \
-  do {                                                               \
-    if (amode == TN_A_SOFTMAX) {                                     \
-      if (epi != TN_PARTIAL_F32) return hipErrorInvalidValue;        \
-      TN_BIG(BN_, TN_PARTIAL_F32, TN_A_SOFTMAX);                     \
-    } else if (epi == TN_STORE_F32) {                                \
-      TN_BIG(BN_, TN_STORE_F32, TN_A_BF16);                          \
-    } else if (epi == TN_ACT_BWD) {                                  \
-      TN_BIG(BN_, TN_ACT_BWD, TN_A_BF16);                            \
-    } else if (epi == TN_STORE_BF16) {                               \
-      TN_BIG(BN_, TN_STORE_BF16, TN_A_BF16);                         \
-    } else if (epi == TN_PARTIAL_F32) {                              \
-      TN_BIG(BN_, TN_PARTIAL_F32, TN_A_BF16);                        \
-    } else {                                                         \
-      return hipErrorInvalidValue;                                   \
-    }                                                                \
+#define TN_BIG(BN_, EPI_) \
+  MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_big<BN_, EPI_>), grid, dim3(NTH), 0, st, a))
+#define TN_BIG_EPI(BN_)                     \
+  do {                                      \
+    if (epi == TN_STORE_F32) {              \
+      TN_BIG(BN_, TN_STORE_F32);            \
+    } else if (epi == TN_ACT_BWD) {         \
+      TN_BIG(BN_, TN_ACT_BWD);              \
+    } else if (epi == TN_STORE_BF16) {      \
+      TN_BIG(BN_, TN_STORE_BF16);           \
+    } else if (epi == TN_PARTIAL_F32) {     \
+      TN_BIG(BN_, TN_PARTIAL_F32);          \
+    } else {                                \
+      return hipErrorInvalidValue;          \
+    }                                       \
   } while (0)
   // the transposed weight tile goes through LDS; 256-wide tiles would need more than the
   // 512 registers a lane has next to 256 accumulators

@@ -311,7 +311,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
 }
 
 // ---------------------------------------------------------------------------- transposed
-template <int EPI, int AMODE>
+template <int EPI>
 __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
   __shared__ __attribute__((aligned(16))) u16 As2[2][BM * LDT];
   __shared__ __attribute__((aligned(16))) u16 Bs2[2][BN * LDT];
@@ -331,24 +331,11 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
   }
   const int t_begin = (int)((long long)total * z / S), t_end = (int)((long long)total * (z + 1) / S);
 
-  // softmax-mode row data (rows fixed per thread for the 4 A chunks)
-  float rlse[4];
-  bool rval[4];
-  if constexpr (AMODE == TN_A_SOFTMAX) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + ((tid + NTHREADS * i) >> 3);
-      rval[i] = m < a.M && a.tgt[m] >= 0;
-      rlse[i] = rval[i] ? a.lse[m] : 0.f;
-    }
-  }
-
   // three register stages of prefetched tiles, two LDS buffers; loads through buffer
   // resources (rows past M or past a segment's N read as 0, see the forward kernel)
   uint4 ra[3][4];
   uint32_t rw[3][4];
   uint32_t rsc[3][4];  // raw fp16 scale bits
-  int cur_n0[3], cur_N[3];  // reduction offset / length of the tile held in a stage
   const int rq = tid >> 4, co = tid & 15;
   const int kc = c0 + 8 * co;
   const int Kh = Kout >> 1;
@@ -390,8 +377,6 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
       const rsrc_t ra_ = s == 0 ? rA[0] : s == 1 ? rA[1] : rA[2];
       const rsrc_t rb_ = s == 0 ? rB[0] : s == 1 ? rB[1] : rB[2];
       const rsrc_t rs_ = s == 0 ? rS[0] : s == 1 ? rS[1] : rS[2];
-      cur_n0[st] = n0;
-      cur_N[st] = sg.N;
   #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int c = tid + NTHREADS * i;
@@ -412,24 +397,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_tn(const TnArgs a) {
     };
     auto sstore = [&](auto S_, auto B_) {
       constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
-      if constexpr (AMODE == TN_A_SOFTMAX) {
-  #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int c = tid + NTHREADS * i;
-          uint4 p = make_uint4(0, 0, 0, 0);
-          // chunks past the reduction length were zero-filled; they must stay 0, not exp(-lse)
-          if (rval[i] && cur_n0[st] + (c & 7) * 8 < cur_N[st]) {
-            const uint32_t* h = (const uint32_t*)&ra[st][i];
-            uint32_t o[4];
-  #pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = pack_bf16x2(__expf(f16_lo(h[j]) - rlse[i]), __expf(f16_hi(h[j]) - rlse[i]));
-            p = make_uint4(o[0], o[1], o[2], o[3]);
-          }
-          *(uint4*)(As2[bf] + (c >> 3) * LDT + (c & 7) * 8) = p;
-        }
-      } else {
-        store_a_tile(As2[bf], tid, ra[st]);
-      }
+      store_a_tile(As2[bf], tid, ra[st]);
       float v[4][8];
   #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -990,6 +958,7 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st, hipEvent_t 
 }
 
 hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, hipEvent_t lora_ready) {
+  if (amode != TN_A_BF16) return hipErrorInvalidValue;
   TnArgs a = a0;
   const int ct = (a.Kout + BN - 1) / BN, mt = (a.M + BM - 1) / BM;
   double flops = 0, bytes = 0;
@@ -1022,27 +991,23 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, 
   if (plan.big) {
     hipError_t eb = launch_gemm_tn_big(a, epi, amode, plan.bn, S, flops, bytes, st);
     if (eb != hipSuccess) return eb;
-  } else if (amode == TN_A_SOFTMAX) {
-    if (epi != TN_PARTIAL_F32) return hipErrorInvalidValue;
-    MEBP_TIMED(st, "gemm_tn_softmax_dh", flops, bytes,
-               hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32, TN_A_SOFTMAX>), grid, dim3(NTHREADS), 0, st, a));
   } else {
     switch (epi) {
       case TN_STORE_F32:
         MEBP_TIMED(st, "gemm_tn_f32out", flops, bytes,
-                   hipLaunchKernelGGL((k_gemm_tn<TN_STORE_F32, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+                   hipLaunchKernelGGL((k_gemm_tn<TN_STORE_F32>), grid, dim3(NTHREADS), 0, st, a));
         break;
       case TN_ACT_BWD:
         MEBP_TIMED(st, "gemm_tn_act_bwd", flops, bytes,
-                   hipLaunchKernelGGL((k_gemm_tn<TN_ACT_BWD, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+                   hipLaunchKernelGGL((k_gemm_tn<TN_ACT_BWD>), grid, dim3(NTHREADS), 0, st, a));
         break;
       case TN_STORE_BF16:
         MEBP_TIMED(st, "gemm_tn_bf16out", flops, bytes,
-                   hipLaunchKernelGGL((k_gemm_tn<TN_STORE_BF16, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+                   hipLaunchKernelGGL((k_gemm_tn<TN_STORE_BF16>), grid, dim3(NTHREADS), 0, st, a));
         break;
       case TN_PARTIAL_F32:
         MEBP_TIMED(st, "gemm_tn_probs_dh", flops, bytes,
-                   hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32, TN_A_BF16>), grid, dim3(NTHREADS), 0, st, a));
+                   hipLaunchKernelGGL((k_gemm_tn<TN_PARTIAL_F32>), grid, dim3(NTHREADS), 0, st, a));
         break;
       default: return hipErrorInvalidValue;
     }

@@ -86,10 +86,10 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
 // with W_seg int4 [N_seg][Kout/2]; reduction over the weight's output dim; G bf16 (bf16
 // MFMA operands).
 enum TnEpi { TN_STORE_F32 = 0, TN_ACT_BWD = 1, TN_PARTIAL_F32 = 2, TN_STORE_BF16 = 3 };
-enum TnAMode { TN_A_BF16 = 0, TN_A_SOFTMAX = 1 };
+enum TnAMode { TN_A_BF16 = 0 };  // the A operand is a bf16 matrix
 
 struct TnSeg {
-  const bf16* G;           // [M][ldg] (TN_A_BF16) or fp16 logits (TN_A_SOFTMAX)
+  const bf16* G;           // [M][ldg]
   int ldg;
   const uint8_t* q4;
   const uint16_t* scale;
@@ -113,9 +113,6 @@ struct TnArgs {
   void* u;
   int ldgu;
   int act;
-  // TN_A_SOFTMAX: p[m][v] = exp(logit - lse[m]) for rows with a target, else 0
-  const float* lse;
-  const int32_t* tgt;
   // split-K scratch for the stored epilogues (unused with one split)
   float* part;
   size_t part_floats;
