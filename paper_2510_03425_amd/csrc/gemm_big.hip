@@ -498,13 +498,6 @@ DEV void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Forward product with 256 x 256 tiles and 8 waves (2 along m x 4 along n, 128 x 64 each),
-// K step 64. The activation tile goes from global memory straight into LDS (buffer loads
-// with the LDS flag: no staging registers, no LDS stores) through a ring of three stages
-// filled two K tiles ahead. A stage holds the 256 x 64 fp16 tile as 128-byte rows whose
-// eight 16-byte chunks are stored at position chunk ^ (row & 7), so that the MFMA fragment
-// reads (32 rows, one chunk each) spread over all banks. The weights are loaded into
-// registers, also two tiles ahead, and decompressed by each wave for its own columns.
 // fp16 / fp32 store (LoRA up-projection and residual included) of a wave's 128 x 64 block
 // of k_gemm_nt_lds through LDS: per 32-row block the accumulators (MFMA layout) go into the
 // wave's own 32 x 68 fp32 region, and each lane reads back 8 consecutive columns of a row
@@ -558,6 +551,13 @@ DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int
   }
 }
 
+// Forward product with 256 x 256 tiles and 8 waves (2 along m x 4 along n, 128 x 64 each),
+// K step 64. The activation tile goes from global memory straight into LDS (buffer loads
+// with the LDS flag: no staging registers, no LDS stores) through a ring of three stages
+// filled two K tiles ahead. A stage holds the 256 x 64 fp16 tile as 128-byte rows whose
+// eight 16-byte chunks are stored at position chunk ^ (row & 7), so that the MFMA fragment
+// reads (32 rows, one chunk each) spread over all banks. The weights are loaded into
+// registers, also two tiles ahead, and decompressed by each wave for its own columns.
 constexpr int LDS_STAGES = 3, LDS_STAGE_BYTES = BM * BK * 2;
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
