@@ -142,6 +142,20 @@ def pmc_per_dispatch(pmc_dir, counter):
     return out
 
 
+def pmc_command_lines(workload):
+    """Header lines naming the rocprofv3 counter passes the summaries are made from."""
+    a = "--steps 2 --warmup 1 --profile-steps 1" if workload == "qwen2.5-0.5b" else "--steps 1 --warmup 0 --profile-steps 0"
+    run = f"python3 -u bench.py --workload {workload} {a} --graph 0 --no-cpu-baseline"
+    return [f"# command: cd /tmp && export TMPDIR=/tmp && cd /root/repo && rocprofv3 --pmc <counters> --output-format csv "
+            f"-d gpurun_out/cnt_{workload}/<pass> -o run -- {run}",
+            "# passes: fetch = FETCH_SIZE; write = WRITE_SIZE; sq = SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+            "SQ_INSTS_VALU SQ_INSTS_MFMA (counter table only)",
+            "# calibration: the FETCH_SIZE and WRITE_SIZE passes around python3 -u bench.py --calibrate-copy 1024 "
+            "(-d gpurun_out/pmc_cal_fetch, gpurun_out/pmc_cal_write)",
+            f"# summary: python bench.py --workload {workload} --calibrate-copy 1024 --traffic-summary | --counter-summary "
+            "<the pass folders>"]
+
+
 def traffic_summary(args, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir):
     """Scale FETCH_SIZE / WRITE_SIZE (KiB per dispatch) by what the same counters read for a
     plain device copy of known size, and write per-kernel HBM bytes per launch."""
@@ -156,6 +170,7 @@ def traffic_summary(args, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir):
     fe = pmc_per_dispatch(fetch_dir, "FETCH_SIZE")
     wr = pmc_per_dispatch(write_dir, "WRITE_SIZE")
     lines = [f"# HBM traffic per launch (rocprofv3 FETCH_SIZE, WRITE_SIZE), workload {args.workload}",
+             *pmc_command_lines(args.workload),
              f"# copy calibration: {cal_n} B read counted as {f_cal:.0f} B (x{kf:.4f}), "
              f"{cal_n} B written counted as {w_cal:.0f} B (x{kw:.4f})",
              "# traffic <timing-report name> <bytes per launch> <fetch> <write> <dispatches>",
@@ -217,6 +232,7 @@ def counter_summary(args, fetch_dir, write_dir, sq_dir, cal_fetch_dir, cal_write
             a["mfma"] += rec.get("SQ_INSTS_MFMA", 0.0)
             a["nsq"] += 1
     lines = [f"# per-kernel counters, workload {args.workload} (rocprofv3 --pmc, kernels serialized by the counter runs)",
+             *pmc_command_lines(args.workload),
              f"# copy calibration: reads x{kf:.4f}, writes x{kw:.4f} (a plain {cal_n} B device copy)",
              f"# HBM GB/s = (fetch + write bytes) / serialized duration, against {PEAK_HBM_GBS:.0f} GB/s; MFMA busy = "
              "SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs)",
@@ -593,7 +609,10 @@ def main():
                 best = (r, dur_ms, per_step)
         dom, per_launch_ms, per_step = best
         traffic = measured_traffic(dom["kernel"], cfg.name)
-        if dom["flops"] > 0:
+        # the dense contractions (dequant GEMMs, attention) are priced against the MFMA peak;
+        # the LoRA, norm and elementwise kernels are bound by HBM and priced by their bytes
+        mfma_bound = dom["kernel"].startswith(("gemm_", "attn_fwd", "attn_bwd")) and dom["flops"] > 0
+        if mfma_bound:
             ach = dom["flops"] / dom["launches"] / (per_launch_ms / 1e3) / 1e12
             roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS_16BIT, "unit": "TFLOP/s",
                     "frac": round(ach / PEAK_TFLOPS_16BIT, 4), "traffic": traffic}
