@@ -649,6 +649,8 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     t.M = D.N; t.Kout = D.qd; t.nseg = 1; t.r = D.r;
     t.seg[0] = tn_seg(x, base, lora, MEBP_O, go);
     t.outb = dO; t.ldo = D.qd;
+    // the attention backward's delta = rowsum(dO * O) comes with dO
+    t.delta_o = o; t.delta = xs<float>(x, S_DELTA); t.delta_T = x.T; t.delta_dh = c->head_dim;
     HIP_TRY(launch_gemm_tn(t, TN_STORE_BF16, TN_A_BF16, x.st, lr));
   }
   // attention (RoPE backward fused into the dq / dk stores)
@@ -660,7 +662,7 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     at.o = o; at.lse = xs<float>(x, S_LSE);
     at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
     if (x.aux && x.aux_used) *x.aux_used = true;
-    HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), scratch(x), x.st, x.aux, x.ev_lr, x.ev_du));
+    HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), scratch(x), x.st, x.aux, x.ev_lr, x.ev_du, true));
   }
   if (c->arch & MEBP_ARCH_QK_NORM) {
     // through the per-head norms (the biases are frozen and need no gradient)

@@ -1188,14 +1188,21 @@ hipError_t launch_attn_fwd(const AttnArgs& a, const SplitScratch& sc, hipStream_
   return hipGetLastError();
 }
 
+hipError_t launch_attn_delta(const bf16* dO, const f16* O, int ld, int B, int T, int H, int dh, float* delta,
+                             hipStream_t st) {
+  const size_t nd = (size_t)B * T * H;
+  MEBP_TIMED(st, "attn_delta", 0.0, (double)nd * (4.0 * dh + 4),
+             hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd * (dh / 8) + 255) / 256)), dim3(256), 0, st, dO, O, ld,
+                                B, T, H, dh, delta));
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScratch& sc, hipStream_t st,
-                           hipStream_t aux, hipEvent_t ev_go, hipEvent_t ev_done) {
-  const size_t nd = (size_t)a0.B * a0.T * a0.Hq;
-  MEBP_TIMED(st, "attn_delta", 0.0, (double)nd * (4.0 * a0.dh + 4),
-             hipLaunchKernelGGL(k_attn_delta, dim3((unsigned)((nd * (a0.dh / 8) + 255) / 256)), dim3(256), 0, st, a0.dO,
-                                (const f16*)a0.o, a0.ldq, a0.B, a0.T, a0.Hq, a0.dh, delta_ws));
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+                           hipStream_t aux, hipEvent_t ev_go, hipEvent_t ev_done, bool delta_ready) {
+  hipError_t e;
+  if (!delta_ready &&
+      (e = launch_attn_delta(a0.dO, (const f16*)a0.o, a0.ldq, a0.B, a0.T, a0.Hq, a0.dh, delta_ws, st)) != hipSuccess)
+    return e;
   AttnArgs a = a0;
   a.delta = delta_ws;
   const AttnPlan p = attn_plan(a.B, a.T, a.Hq, a.Hkv, a.dh, a.window);

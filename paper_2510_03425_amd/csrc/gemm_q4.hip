@@ -756,7 +756,22 @@ __global__ __launch_bounds__(256) void k_tn_finalize(const TnArgs a, int S) {
   if constexpr (EPI == TN_STORE_F32) {
     *(float4*)(a.out + (size_t)m * a.ldo + c) = make_float4(o[0], o[1], o[2], o[3]);
   } else if constexpr (EPI == TN_STORE_BF16) {
-    *(uint2*)(a.outb + (size_t)m * a.ldo + c) = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+    const uint2 ob = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+    *(uint2*)(a.outb + (size_t)m * a.ldo + c) = ob;
+    if (a.delta) {
+      // the attention backward's delta from the stored (bf16) values: the dh/4 threads of a
+      // (row, head) are consecutive lanes (Kout/4 threads per row, a multiple of dh/4)
+      const uint2 ov = *(const uint2*)(a.delta_o + (size_t)m * a.ldo + c);
+      float acc = bf16_lo(ob.x) * f16_lo(ov.x) + bf16_hi(ob.x) * f16_hi(ov.x) + bf16_lo(ob.y) * f16_lo(ov.y) +
+                  bf16_hi(ob.y) * f16_hi(ov.y);
+      const int G = a.delta_dh >> 2;
+      for (int k = 1; k < G; k <<= 1) acc += __shfl_xor(acc, k, 64);
+      if (c % a.delta_dh == 0) {
+        const int T = a.delta_T, H = a.Kout / a.delta_dh;
+        const int b = m / T, t = m % T, h = c / a.delta_dh;
+        a.delta[((size_t)b * H + h) * T + t] = acc;
+      }
+    }
   } else {  // TN_ACT_BWD
     const size_t idx = (size_t)m * a.ldgu + c;
     const uint2 gv = *(const uint2*)((const f16*)a.g + idx), uv = *(const uint2*)((const f16*)a.u + idx);
@@ -959,6 +974,9 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st, hipEvent_t 
 
 hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, hipEvent_t lora_ready) {
   if (amode != TN_A_BF16) return hipErrorInvalidValue;
+  if (a0.delta && (epi != TN_STORE_BF16 || !a0.delta_o || a0.delta_T <= 0 || a0.M % a0.delta_T ||
+                   (a0.delta_dh != 64 && a0.delta_dh != 128 && a0.delta_dh != 256) || a0.Kout % a0.delta_dh))
+    return hipErrorInvalidValue;
   TnArgs a = a0;
   const int ct = (a.Kout + BN - 1) / BN, mt = (a.M + BM - 1) / BM;
   double flops = 0, bytes = 0;
@@ -1017,6 +1035,9 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, 
   const bool norm = epi == TN_STORE_F32 && a.out2;
   if (S == 1) {
     if (norm) return launch_rmsnorm_bwd(a.norm_x, a.norm_w, a.out, a.resid2, a.M, a.Kout, a.eps, a.out2, a.out2b, st);
+    if (epi == TN_STORE_BF16 && a.delta)
+      return launch_attn_delta(a.outb, a.delta_o, a.ldo, a.M / a.delta_T, a.delta_T, a.Kout / a.delta_dh, a.delta_dh,
+                               a.delta, st);
     return hipSuccess;
   }
   const double fb = 4.0 * S * a.M * a.Kout + outb * (epi == TN_ACT_BWD ? 8 : epi == TN_STORE_BF16 ? 2 : 4);

@@ -113,6 +113,11 @@ struct TnArgs {
   void* u;
   int ldgu;
   int act;
+  // TN_STORE_BF16 follow-up for the attention backward: delta[b][h][t] = sum_e dO[n][h*dh+e] *
+  // delta_o[n][h*dh+e] over the stored bf16 dO (n = b*delta_T + t, O with the same pitch ldo)
+  const f16* delta_o;
+  float* delta;
+  int delta_T, delta_dh;
   // split-K scratch for the stored epilogues (unused with one split)
   float* part;
   size_t part_floats;
@@ -227,8 +232,13 @@ hipError_t launch_attn_fwd(const AttnArgs& a, const SplitScratch& sc, hipStream_
 // scratch: delta [B][Hq][T], and the partials of attn_plan in sc.
 // With `aux` (and two events), the dQ kernels run there beside dK/dV; `st` waits for them
 // before returning.
+// delta_ready: delta_ws already holds rowsum(dO * O) (computed with dO, see TnArgs::delta).
 hipError_t launch_attn_bwd(const AttnArgs& a, float* delta_ws, const SplitScratch& sc, hipStream_t st,
-                           hipStream_t aux = nullptr, hipEvent_t ev_go = nullptr, hipEvent_t ev_done = nullptr);
+                           hipStream_t aux = nullptr, hipEvent_t ev_go = nullptr, hipEvent_t ev_done = nullptr,
+                           bool delta_ready = false);
+// delta[b][h][t] = sum_e dO[b*T+t][h*dh+e] * O[b*T+t][h*dh+e] (rows of pitch ld)
+hipError_t launch_attn_delta(const bf16* dO, const f16* O, int ld, int B, int T, int H, int dh, float* delta,
+                             hipStream_t st);
 
 // ---------------------------------------------------------------- optimizer
 // One LoRA tensor of an elementwise optimizer launch: n4 float4s at p (updated), g (read),
