@@ -321,10 +321,64 @@ DEV void nt_big_epilogue(f32x16 (&acc)[4][BN / (32 * WNW)], const NtArgs& a, con
   }
 }
 
+// fp16 / fp32 store (LoRA up-projection and residual included) of a wave's 128 x 64 block
+// of the large-tile forward kernels through LDS: per 32-row block the accumulators (MFMA layout) go into the
+// wave's own 32 x 68 fp32 region, and each lane reads back 8 consecutive columns of a row
+// and stores them with 16-byte accesses (a wave instruction covers 8 whole row segments)
+// instead of 2- or 4-byte stores in the MFMA layout. The residual rows of a block are all
+// loaded before its accumulators are staged. Requires N % 8 == 0 and 16-byte aligned rows.
+template <int EPI>
+DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int mw0, int wcol0, int lane,
+                      float* ep) {
+  constexpr int LDE = 68;
+  if (sg.lora_B) lora_mfma<2>(acc, sg.lora_u, a.r, mw0, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, sg.N, lane);
+  const int rr = lane >> 3, ch = lane & 7, n = wcol0 + 8 * ch;
+  const bool nok = n < sg.N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float4 res[4][2];
+    if (sg.resid) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int m = mw0 + 32 * i + 8 * p + rr;
+        const bool ok = nok && m < a.M;
+        const float* src = sg.resid + (ok ? (size_t)m * sg.ldr + n : 0);
+        res[p][0] = ok ? *(const float4*)src : make_float4(0.f, 0.f, 0.f, 0.f);
+        res[p][1] = ok ? *(const float4*)(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) ep[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] = acc[i][j][q];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int r = 8 * p + rr, m = mw0 + 32 * i + r;
+      float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
+      if (sg.resid) {
+        v0.x += res[p][0].x; v0.y += res[p][0].y; v0.z += res[p][0].z; v0.w += res[p][0].w;
+        v1.x += res[p][1].x; v1.y += res[p][1].y; v1.z += res[p][1].z; v1.w += res[p][1].w;
+      }
+      if (nok && m < a.M) {
+        if constexpr (EPI == NT_STORE_F16) {
+          const uint4 o = make_uint4(pack_f16x2(v0.x, v0.y), pack_f16x2(v0.z, v0.w), pack_f16x2(v1.x, v1.y),
+                                     pack_f16x2(v1.z, v1.w));
+          *(uint4*)((f16*)sg.out + (size_t)m * sg.ldo + n) = o;
+        } else {
+          float* dst = (float*)sg.out + (size_t)m * sg.ldo + n;
+          *(float4*)dst = v0;
+          *(float4*)(dst + 4) = v1;
+        }
+      }
+    }
+  }
+}
+
 // WNW waves along n (2 or 4), two along m: 128 x WNW threads, each wave 128 x BN/WNW. With
 // four (512 threads) two waves share each SIMD, so one wave's decompression (VALU) runs
 // beside the other's MFMAs.
-template <int BN, int WNW, int EPI>
+// VEC: fp16 / fp32 outputs through nt_lds_store (one split, N % 8 == 0, 16-byte aligned rows).
+template <int BN, int WNW, int EPI, bool VEC>
 __global__ __launch_bounds__(128 * WNW, 1) void k_gemm_nt_big(const NtArgs a) {
   constexpr int NT = 128 * WNW;
   constexpr int NJ = BN / (32 * WNW);  // 32-column blocks per wave
@@ -467,7 +521,12 @@ __global__ __launch_bounds__(128 * WNW, 1) void k_gemm_nt_big(const NtArgs a) {
       run(IC<0>{});
   }
 
-  nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
+  if constexpr (VEC && EPI != NT_LOGITS && NJ == 2) {
+    __syncthreads();  // every wave is done with the main loop's LDS tiles
+    nt_lds_store<EPI>(acc, a, sg, m0 + wm * 128, wcol0, lane, reinterpret_cast<float*>(&As2[0][0]) + wave * 32 * 68);
+  } else {
+    nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
+  }
 }
 
 
@@ -496,59 +555,6 @@ template <int N>
 DEV void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// fp16 / fp32 store (LoRA up-projection and residual included) of a wave's 128 x 64 block
-// of k_gemm_nt_lds through LDS: per 32-row block the accumulators (MFMA layout) go into the
-// wave's own 32 x 68 fp32 region, and each lane reads back 8 consecutive columns of a row
-// and stores them with 16-byte accesses (a wave instruction covers 8 whole row segments)
-// instead of 2- or 4-byte stores in the MFMA layout. The residual rows of a block are all
-// loaded before its accumulators are staged. Requires N % 8 == 0 and 16-byte aligned rows.
-template <int EPI>
-DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int mw0, int wcol0, int lane,
-                      float* ep) {
-  constexpr int LDE = 68;
-  if (sg.lora_B) lora_mfma<2>(acc, sg.lora_u, a.r, mw0, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, sg.N, lane);
-  const int rr = lane >> 3, ch = lane & 7, n = wcol0 + 8 * ch;
-  const bool nok = n < sg.N;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float4 res[4][2];
-    if (sg.resid) {
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int m = mw0 + 32 * i + 8 * p + rr;
-        const bool ok = nok && m < a.M;
-        const float* src = sg.resid + (ok ? (size_t)m * sg.ldr + n : 0);
-        res[p][0] = ok ? *(const float4*)src : make_float4(0.f, 0.f, 0.f, 0.f);
-        res[p][1] = ok ? *(const float4*)(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 16; ++q)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) ep[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] = acc[i][j][q];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int r = 8 * p + rr, m = mw0 + 32 * i + r;
-      float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
-      if (sg.resid) {
-        v0.x += res[p][0].x; v0.y += res[p][0].y; v0.z += res[p][0].z; v0.w += res[p][0].w;
-        v1.x += res[p][1].x; v1.y += res[p][1].y; v1.z += res[p][1].z; v1.w += res[p][1].w;
-      }
-      if (nok && m < a.M) {
-        if constexpr (EPI == NT_STORE_F16) {
-          const uint4 o = make_uint4(pack_f16x2(v0.x, v0.y), pack_f16x2(v0.z, v0.w), pack_f16x2(v1.x, v1.y),
-                                     pack_f16x2(v1.z, v1.w));
-          *(uint4*)((f16*)sg.out + (size_t)m * sg.ldo + n) = o;
-        } else {
-          float* dst = (float*)sg.out + (size_t)m * sg.ldo + n;
-          *(float4*)dst = v0;
-          *(float4*)(dst + 4) = v1;
-        }
-      }
-    }
-  }
 }
 
 // Forward product with 256 x 256 tiles and 8 waves (2 along m x 4 along n, 128 x 64 each),
@@ -1002,15 +1008,16 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
     t += (b.seg[s].N + bn - 1) / bn;
   }
   const char* name = epi == NT_STORE_F16 ? "gemm_nt_f16out" : epi == NT_STORE_F32 ? "gemm_nt_f32out" : "gemm_nt_logits";
-#define NT_BIG(BN_, EPI_)                                                                                 \
-  MEBP_TIMED(st, name, flops, bytes,                                                                      \
-             hipLaunchKernelGGL((k_gemm_nt_big<BN_, BN_ / 64, EPI_>), grid, dim3(2 * BN_), 0, st, b))
+#define NT_BIG(BN_, EPI_, VEC_)                                                                       \
+  MEBP_TIMED(st, name, flops, bytes,                                                                  \
+             hipLaunchKernelGGL((k_gemm_nt_big<BN_, BN_ / 64, EPI_, VEC_>), grid, dim3(2 * BN_), 0, st, b))
   static const int use_lds = [] {
     const char* e = getenv("MEBP_NT_LDS");
     return e && *e ? atoi(e) : 1;
   }();
-  // the LDS-direct kernel stores fp16 / fp32 outputs as 16-byte row chunks: one split,
-  // segment widths that are multiples of 8 and 16-byte aligned rows
+  // fp16 / fp32 outputs as 16-byte row chunks through LDS (required by the LDS-direct kernel,
+  // chosen in the other one): one split, segment widths that are multiples of 8 and 16-byte
+  // aligned rows
   bool vec = S == 1;
   for (int s = 0; s < a.nseg && epi != NT_LOGITS; ++s) {
     const NtSeg& g = a.seg[s];
@@ -1029,19 +1036,25 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
       NT_LDS(NT_STORE_F32);
 #undef NT_LDS
   } else if (bn == 256) {
-    if (epi == NT_LOGITS)
-      NT_BIG(256, NT_LOGITS);
-    else if (epi == NT_STORE_F16)
-      NT_BIG(256, NT_STORE_F16);
-    else
-      NT_BIG(256, NT_STORE_F32);
+    if (epi == NT_LOGITS) {
+      NT_BIG(256, NT_LOGITS, false);
+    } else if (epi == NT_STORE_F16) {
+      if (vec) NT_BIG(256, NT_STORE_F16, true);
+      else NT_BIG(256, NT_STORE_F16, false);
+    } else {
+      if (vec) NT_BIG(256, NT_STORE_F32, true);
+      else NT_BIG(256, NT_STORE_F32, false);
+    }
   } else if (bn == 128) {
-    if (epi == NT_LOGITS)
-      NT_BIG(128, NT_LOGITS);
-    else if (epi == NT_STORE_F16)
-      NT_BIG(128, NT_STORE_F16);
-    else
-      NT_BIG(128, NT_STORE_F32);
+    if (epi == NT_LOGITS) {
+      NT_BIG(128, NT_LOGITS, false);
+    } else if (epi == NT_STORE_F16) {
+      if (vec) NT_BIG(128, NT_STORE_F16, true);
+      else NT_BIG(128, NT_STORE_F16, false);
+    } else {
+      if (vec) NT_BIG(128, NT_STORE_F32, true);
+      else NT_BIG(128, NT_STORE_F32, false);
+    }
   } else {
     return hipErrorInvalidValue;
   }
