@@ -78,9 +78,9 @@ def measured_traffic(kernel, workload):
 # Timing-report names -> the HIP kernels they launch (demangled-name patterns), for reading
 # rocprofv3 output of the same run.
 KERNEL_PATTERNS = {
-    "gemm_nt_f16out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?0>",
-    "gemm_nt_f32out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?1>",
-    "gemm_nt_logits": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?2>",
+    "gemm_nt_f16out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?0(, (true|false))?>",
+    "gemm_nt_f32out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?1(, (true|false))?>",
+    "gemm_nt_logits": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?2(, (true|false))?>",
     "gemm_tn_f32out": r"k_gemm_tn(_big)?<(\d+, )?0>",
     "gemm_tn_act_bwd": r"k_gemm_tn(_big)?<(\d+, )?1>",
     "gemm_tn_probs_dh": r"k_gemm_tn(_big)?<(\d+, )?2>",
@@ -88,7 +88,7 @@ KERNEL_PATTERNS = {
     "lora_rows": r"k_lora_rows<",
     "lora_outer": r"k_lora_outer<",
     "attn_fwd": r"k_attn_fwd",
-    "attn_bwd_dkdv": r"k_attn_bwd_dkdv<",
+    "attn_bwd_dkdv": r"k_attn_bwd_(dkdv|kv32)<",
     "attn_bwd_dq": r"k_attn_bwd_dq<",
 }
 
