@@ -813,7 +813,8 @@ SideStream* side_stream(hipStream_t main) {
 // its slot before the reverse loop recomputes that layer. Without it, ring = the caller's
 // full checkpoint array (slot i = x_i) and nothing is copied.
 struct Offload {
-  float* host = nullptr;  // [(L+1)][N][d] pinned host memory
+  float* host = nullptr;      // [(L+1)][N][d] pinned host memory
+  float* host_dev = nullptr;  // the same memory's device address (null: copies through hipMemcpyAsync)
   int R = 0;              // ring slots
   hipStream_t cp = nullptr;
   hipEvent_t ev_in[MEBP_RING_MAX], ev_out[MEBP_RING_MAX];
@@ -864,7 +865,12 @@ int train_step_impl(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   auto save = [&](int i, hipStream_t after) -> int {
     HIP_TRY(hipEventRecord(off->ev_go, after));
     HIP_TRY(hipStreamWaitEvent(off->cp, off->ev_go, 0));
-    HIP_TRY(hipMemcpyAsync(off->host + (size_t)i * stride, ck(i), bytes, hipMemcpyDeviceToHost, off->cp));
+    // (the runtime's device-to-host copy is a kernel that holds many compute units for the
+    // whole transfer over the host link; the few-workgroup copy leaves them to the layers)
+    if (off->host_dev)
+      HIP_TRY(launch_copy_host(ck(i), off->host_dev + (size_t)i * stride, bytes, off->cp));
+    else
+      HIP_TRY(hipMemcpyAsync(off->host + (size_t)i * stride, ck(i), bytes, hipMemcpyDeviceToHost, off->cp));
     HIP_TRY(hipEventRecord(off->ev_out[i % off->R], off->cp));
     return MEBP_OK;
   };
@@ -872,7 +878,10 @@ int train_step_impl(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   auto fetch = [&](int i, hipStream_t after) -> int {
     HIP_TRY(hipEventRecord(off->ev_go, after));
     HIP_TRY(hipStreamWaitEvent(off->cp, off->ev_go, 0));
-    HIP_TRY(hipMemcpyAsync(ck(i), off->host + (size_t)i * stride, bytes, hipMemcpyHostToDevice, off->cp));
+    if (off->host_dev)
+      HIP_TRY(launch_copy_host(off->host_dev + (size_t)i * stride, ck(i), bytes, off->cp));
+    else
+      HIP_TRY(hipMemcpyAsync(ck(i), off->host + (size_t)i * stride, bytes, hipMemcpyHostToDevice, off->cp));
     HIP_TRY(hipEventRecord(off->ev_in[i % off->R], off->cp));
     return MEBP_OK;
   };
@@ -1140,6 +1149,10 @@ int mebp_train_step_offload(const mebp_config* cfg, const mebp_q4* emb, const me
   if (!os) return fail(MEBP_EHIP, "could not create the copy stream");
   Offload off;
   off.host = ckpt_host;
+  // the device address of the pinned buffer, when the runtime reports it for exactly this
+  // pointer and with the same alignment
+  if (pa.hostPointer == (void*)ckpt_host && pa.devicePointer && aligned(pa.devicePointer, 16))
+    off.host_dev = (float*)pa.devicePointer;
   off.R = ring_slots;
   off.cp = os->cp;
   off.ev_go = os->ev_go;

@@ -256,6 +256,17 @@ __global__ __launch_bounds__(256) void k_ce_loss(const float* row_loss, int M, f
   if (threadIdx.x == 0) loss[0] = ((red[0] + red[1]) + (red[2] + red[3])) * inv_n;
 }
 
+// Copy between device memory and pinned host memory (its device address) by a few
+// workgroups (16-byte accesses, grid-stride): the host link, not the chip, bounds it, so it
+// needs few compute units, and unlike a copy kernel sized to the buffer it leaves the others
+// to the layer kernels running beside it. 8192 threads keep 128 KB in flight, enough for the
+// link's bandwidth-latency product.
+constexpr int COPY_WGS = 32;
+__global__ __launch_bounds__(256) void k_copy_host(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                   size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)COPY_WGS * 256) dst[i] = src[i];
+}
+
 // Softmax probabilities of the LM head, p[m][v] = exp(logit[m][v] - lse[m]) for rows with a
 // target and 0 for the others, rounded to bf16 and written over the fp16 logits in place:
 // the A operand of the dH product, computed once instead of in every column tile of it.
@@ -558,6 +569,13 @@ hipError_t launch_ce_loss(const float* row_loss, const int32_t* tgt, int M, floa
   (void)tgt;
   MEBP_TIMED(st, "ce_loss", 0.0, (double)M * 4,
              hipLaunchKernelGGL(k_ce_loss, dim3(1), dim3(256), 0, st, row_loss, M, inv_n, loss));
+  return hipGetLastError();
+}
+hipError_t launch_copy_host(const void* src, void* dst, size_t bytes, hipStream_t st) {
+  if ((bytes & 15) || ((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return hipErrorInvalidValue;
+  MEBP_TIMED(st, "copy_host", 0.0, (double)bytes * 2,
+             hipLaunchKernelGGL(k_copy_host, dim3(COPY_WGS), dim3(256), 0, st, (const uint4*)src, (uint4*)dst,
+                                bytes >> 4));
   return hipGetLastError();
 }
 hipError_t launch_ce_probs(uint16_t* logits, int M, int V, const float* lse, const int32_t* tgt, hipStream_t st) {

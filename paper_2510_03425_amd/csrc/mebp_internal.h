@@ -265,6 +265,9 @@ hipError_t launch_ce_rows(const float2* stats, int ntiles, const float* tgt_logi
 hipError_t launch_ce_loss(const float* row_loss, const int32_t* tgt, int M, float inv_n, float* loss,
                           hipStream_t st);
 // dhf[m][:] = inv_n * (sum_s part[s][m][:] - E[tgt[m]][:]) (rows with target), else 0
+// bytes (a multiple of 16) between device memory and pinned host memory addressed through
+// its device address (both 16-byte aligned), by a few workgroups on `st`
+hipError_t launch_copy_host(const void* src, void* dst, size_t bytes, hipStream_t st);
 // in place: fp16 logits -> bf16 softmax probabilities (0 on rows without a target)
 hipError_t launch_ce_probs(uint16_t* logits, int M, int V, const float* lse, const int32_t* tgt, hipStream_t st);
 hipError_t launch_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
