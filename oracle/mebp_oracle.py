@@ -87,6 +87,40 @@ def dequant_bf16_bits(q4: np.ndarray, scale_bits: np.ndarray, n_in: int, group: 
     return bf16_rne_bits(dequant(q4, scale_bits, n_in, group).astype(np.float32))
 
 
+def fp16_rne_bits(x) -> np.ndarray:
+    """IEEE binary16 bit pattern of finite values, rounded to nearest, ties to even.
+
+    Written from the format's definition in exact fp64 arithmetic: magnitudes below
+    2^-14 are subnormal multiples of 2^-24; a normal value ``f * 2^e`` (``1 <= f < 2``)
+    keeps 10 fraction bits; a rounded magnitude of 2^16 or more is infinity.
+    """
+    x = np.asarray(x, dtype=F64)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("fp16_rne_bits takes finite values")
+    sign = np.where(np.signbit(x), 0x8000, 0).astype(np.int64)
+    a = np.abs(x)
+    out = np.zeros(a.shape, np.int64)
+    sub = a < 2.0 ** -14
+    # subnormal (and zero): the integer number of 2^-24 units, ties to even
+    out[sub] = np.rint(a[sub] * 2.0 ** 24).astype(np.int64)
+    nrm = ~sub
+    if np.any(nrm):
+        f, e = np.frexp(a[nrm])  # a = f * 2^e with 0.5 <= f < 1
+        e = e.astype(np.int64) - 1  # a = (2 f) * 2^e, 1 <= 2 f < 2
+        m = np.rint((2.0 * f - 1.0) * 1024.0).astype(np.int64)  # 10 fraction bits, ties to even
+        carry = m == 1024
+        e = e + carry
+        m = np.where(carry, 0, m)
+        bits = (e + 15) * 1024 + m
+        out[nrm] = np.where(e + 15 >= 31, 0x7C00, bits)
+    return (out | sign).astype(np.uint16)
+
+
+def dequant_fp16_bits(q4: np.ndarray, scale_bits: np.ndarray, n_in: int, group: int = 32) -> np.ndarray:
+    """fp16 bits of ``q*s`` rounded to nearest even (the forward GEMMs' operand type)."""
+    return fp16_rne_bits(dequant(q4, scale_bits, n_in, group))
+
+
 # ----------------------------------------------------------------------------------------
 # Elementary blocks
 # ----------------------------------------------------------------------------------------

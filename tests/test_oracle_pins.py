@@ -82,6 +82,73 @@ def test_dequant_value_exact_in_fp32_and_bf16_bits():
     np.testing.assert_array_equal(got, ref)
 
 
+def test_dequant_hand_set_codes_and_scales_one_by_one():
+    # a ragged row length (688 = 21 full groups of 32 and one of 16), every group with its
+    # own scale (subnormal, small, ordinary and large fp16 values), codes chosen by hand and
+    # packed here; each decompressed value is checked against code * scale in Python floats
+    n_out, n_in = 3, 688
+    ng = (n_in + 31) // 32
+    # (the largest, times 1.5 and 7, stays below the fp16 maximum 65504)
+    scale_vals = [2.0 ** -24 * 3, 2.0 ** -20, 1.5e-3, 0.0078125, 0.01, 0.02, 1.0, 3.25, 2.0 ** 10, 6000.0]
+    s16 = np.empty((n_out, ng), np.float16)
+    for o in range(n_out):
+        for g in range(ng):
+            s16[o, g] = np.float16(scale_vals[(o * ng + g) % len(scale_vals)] * (1 + (g % 5) / 8))
+    codes = [[((7 * o + 3 * i + (i // 32)) % 15) - 7 for i in range(n_in)] for o in range(n_out)]
+    codes[0][0], codes[0][1], codes[1][687], codes[2][686] = -8, 7, -8, -7  # both nibble positions
+    q4 = np.zeros((n_out, n_in // 2), np.uint8)
+    for o in range(n_out):
+        for i in range(n_in):
+            q4[o, i // 2] |= (codes[o][i] & 0xF) << (4 * (i % 2))
+    W = O.dequant(q4, s16.view(np.uint16), n_in, 32)
+    for o in range(n_out):
+        for i in range(n_in):
+            assert W[o, i] == codes[o][i] * float(s16[o, i // 32]), (o, i)
+    # the same values rounded to the forward GEMMs' fp16 operand
+    f16 = O.dequant_fp16_bits(q4, s16.view(np.uint16), n_in, 32)
+    for o in range(n_out):
+        for i in range(n_in):
+            assert f16[o, i] == np.float16(codes[o][i] * float(s16[o, i // 32])).view(np.uint16), (o, i)
+
+
+def test_dequant_of_quantizer_output_within_half_a_step_ragged_row():
+    # the decompressed weight of the offline quantiser's output is within half a
+    # quantisation step of the original weight, group by group, including the 16-wide last
+    # group of a 688-wide row; the step is the fp16 scale decoded by numpy
+    rng = np.random.default_rng(11)
+    w = (rng.standard_normal((48, 688)) * 0.02).astype(np.float32)
+    w[5, 672:] *= 50.0  # a last group with a much larger scale than its row
+    w[7, :32] = 0.0  # an all-zero group
+    q4, sb = quantize_q4(w, 32)
+    W = O.dequant(q4, sb, 688, 32)
+    s = sb.view(np.float16).astype(np.float64)
+    for g in range(22):
+        cols = slice(32 * g, min(688, 32 * g + 32))
+        err = np.abs(W[:, cols] - w[:, cols].astype(np.float64))
+        assert np.all(err <= 0.5 * s[:, g:g + 1] * (1 + 2.0 ** -20)), g
+    assert np.all(W[7, :32] == 0.0)
+    # max |q| = 7 in each nonzero group: the group's largest weight maps to +-7 steps
+    for g in range(22):
+        cols = slice(32 * g, min(688, 32 * g + 32))
+        nz = s[:, g] > 0
+        ratio = np.max(np.abs(W[nz, cols]), axis=1) / s[nz, g]
+        np.testing.assert_array_equal(ratio, 7.0)
+
+
+def test_fp16_rne_matches_numpy_half_conversion():
+    # every float32 value that lies on the fp16 grid or halfway between two neighbours
+    # (ties), plus random values across the whole range including subnormals and overflow
+    rng = np.random.default_rng(12)
+    h = np.arange(0, 0x7C00, dtype=np.uint32).astype(np.uint16).view(np.float16).astype(np.float64)
+    mids = (h[:-1] + h[1:]) / 2.0
+    vals = np.concatenate([h, mids, mids * (1 + 2.0 ** -30), mids * (1 - 2.0 ** -30),
+                           np.exp(rng.uniform(np.log(2.0 ** -26), np.log(7e4), 200000)), [65519.0, 65520.0, 1e6]])
+    vals = np.concatenate([vals, -vals]).astype(np.float32)
+    with np.errstate(over="ignore"):  # 65520 and above overflow to infinity on purpose
+        ref = vals.astype(np.float16).view(np.uint16)
+    np.testing.assert_array_equal(O.fp16_rne_bits(vals), ref)
+
+
 # ---------------------------------------------------------------------------------------
 # P2: quantiser bounds (the compressed input format)
 # ---------------------------------------------------------------------------------------
