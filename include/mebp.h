@@ -242,6 +242,28 @@ const char* mebp_last_error(void);
 int mebp_dequant_q4(const mebp_q4* w, int32_t rows, int32_t cols, int32_t group, float* out_f32,
                     uint16_t* out_bf16, mebp_stream_t stream);
 
+/* One production dequant-GEMM kernel on caller operands (test aid for the bit-exact check of
+ * the decompression fused into the products, Algorithm 1's LazyLoadAndDecompressWeights):
+ * one split, no LoRA term, no residual, fp32 outputs.
+ *   forward kinds (the layer projections and the LM-head logits):
+ *     out[m][n] = sum_k X[m][k] * fp16_rne(W[n][k]),   X fp16 [M][n_in], out [M][n_out]
+ *   transposed kinds (the input gradients and the LM head's dH):
+ *     out[m][c] = sum_n G[m][n] * bf16_rne(W[n][c]),   G bf16 [M][n_out], out [M][n_in]
+ * with W [n_out][n_in] the decompressed weight (int4 codes times fp16 scale per 32 inputs).
+ * A one-hot X (or G) makes each output one decompressed weight in the kernel's operand
+ * type, exactly. n_in and n_out multiples of 16, 1 <= M <= 65536, n_in, n_out <= 65536,
+ * x and out 16-byte aligned; MEBP_EINVAL / MEBP_EUNSUPPORTED otherwise.                  */
+enum {
+  MEBP_TEST_GEMM_NT = 0,        /* forward, 128 x 128 tiles (few tokens)                  */
+  MEBP_TEST_GEMM_NT_BIG128 = 1, /* forward, 256 x 128 tiles, weights staged in registers  */
+  MEBP_TEST_GEMM_NT_BIG256 = 2, /* forward, 256 x 256 tiles, weights staged in registers  */
+  MEBP_TEST_GEMM_NT_LDS = 3,    /* forward, 256 x 256 tiles, activations loaded into LDS  */
+  MEBP_TEST_GEMM_TN = 4,        /* transposed, 128 x 128 tiles                            */
+  MEBP_TEST_GEMM_TN_BIG = 5     /* transposed, 256 x 128 tiles                            */
+};
+int mebp_test_gemm(int32_t kind, const mebp_q4* w, int32_t n_out, int32_t n_in, const void* x, int32_t M,
+                   float* out, mebp_stream_t stream);
+
 /* Byte offset inside the workspace of an intermediate kept by the last
  * mebp_layer_recompute_backward / mebp_layer_forward_ckpt on that workspace (for tests).
  * Returns (size_t)-1 for an unknown slot. Slots are listed by mebp_workspace_slot_name. */
@@ -262,10 +284,11 @@ int mebp_kernel_timing_report(char* buf, size_t len);
 
 /* Measurement aid. From this call on, every launch of the kernel named `kernel` (a name
  * as it appears in the timing report) is issued `times` times back to back on its stream;
- * kernel = NULL or times <= 1 switches it off. Results are unchanged, since every such
- * kernel computes its outputs from inputs it does not overwrite; the two kernels that
- * update a buffer in place ("gemm_tn_act_bwd", "splitk_finalize_actbwd") are refused with
- * MEBP_EINVAL. With timing enabled, each burst of repeated launches is bracketed by one
+ * kernel = NULL or times <= 1 switches it off. Results are unchanged, since every kernel
+ * that may be repeated computes its outputs from inputs it does not overwrite; the kernels
+ * that update a buffer in place are refused with MEBP_EINVAL ("gemm_tn_act_bwd",
+ * "splitk_finalize_actbwd", "rope_fwd", "qkv_post", "headnorm_bwd", "ce_chunk_stats",
+ * "ce_probs", "ce_dh_accum", "ce_final", "lora_adamw", "lora_grad_accumulate"). With timing enabled, each burst of repeated launches is bracketed by one
  * event pair and reported as `times` launches, so the report's average is the kernel's
  * back-to-back in-stream duration. Host-thread-unsafe; for benchmarks only. */
 int mebp_kernel_repeat(const char* kernel, int32_t times);

@@ -21,8 +21,12 @@ EXPORTED = (
     "mebp_lm_head_ce_backward", "mebp_embed", "mebp_train_step", "mebp_last_error",
     "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name", "mebp_kernel_timing",
     "mebp_kernel_timing_report", "mebp_kernel_repeat", "mebp_lora_grad_accumulate", "mebp_lora_adamw_step",
-    "mebp_train_step_offload",
+    "mebp_train_step_offload", "mebp_test_gemm",
 )
+
+
+# mebp_test_gemm kinds
+TEST_GEMM_NT, TEST_GEMM_NT_BIG128, TEST_GEMM_NT_BIG256, TEST_GEMM_NT_LDS, TEST_GEMM_TN, TEST_GEMM_TN_BIG = range(6)
 
 
 class MebpConfig(C.Structure):
@@ -98,6 +102,7 @@ def lib() -> C.CDLL:
                                                   C.POINTER(MebpLayerLoraGrad), P, P, SZ, P]),
             "mebp_last_error": (C.c_char_p, []),
             "mebp_dequant_q4": (C.c_int, [C.POINTER(MebpQ4), I32, I32, I32, P, P, P]),
+            "mebp_test_gemm": (C.c_int, [I32, C.POINTER(MebpQ4), I32, I32, P, I32, P, P]),
             "mebp_workspace_offset": (SZ, [cfgp, I32, I32, I32]),
             "mebp_workspace_slot_name": (C.c_char_p, [I32]),
             "mebp_kernel_timing": (C.c_int, [I32, I32]),
@@ -185,6 +190,11 @@ def mebp_train_step_offload(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt_
 
 def mebp_dequant_q4(w, rows, cols, group, out_f32, out_bf16, stream=0, check=True):
     r = lib().mebp_dequant_q4(_ref(w), rows, cols, group, out_f32, out_bf16, stream)
+    return _check(r) if check else r
+
+
+def mebp_test_gemm(kind, w, n_out, n_in, x, M, out, stream=0, check=True):
+    r = lib().mebp_test_gemm(kind, _ref(w), n_out, n_in, x, M, out, stream)
     return _check(r) if check else r
 
 

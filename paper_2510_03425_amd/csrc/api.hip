@@ -2,6 +2,7 @@
 // checkpointed LoRA step (Algorithm 1) out of the gfx950 kernels. Every entry point
 // validates everything before enqueuing anything; nothing here allocates device memory.
 #include <math.h>
+#include <stdlib.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -44,13 +45,15 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 enum Slot {
   S_A, S_Q, S_K, S_V, S_O, S_LSE, S_H, S_C, S_G, S_U, S_Z, S_LU, S_LDU, S_DYB, S_DC, S_DH, S_DHB, S_DO,
   S_DELTA, S_DQ, S_DK, S_DV, S_DA, S_PART, S_ROPE_G, S_ROPE_L, S_TGT, S_HF, S_LOGITS, S_STATS, S_LSEV,
-  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_QPRE, S_KPRE, S_TO, S_TD, S_DTB, S_DTOB, S_COUNT
+  S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_QPRE, S_KPRE, S_TO, S_TD, S_DTB, S_DTOB, S_CEMAX,
+  S_CESUM, S_CEALPHA, S_COUNT
 };
 const char* kSlotNames[S_COUNT] = {
   "a", "q", "k", "v", "o", "lse", "h", "c", "g", "u", "z", "lora_u", "lora_du", "dy_bf16", "dc", "dh",
   "dh_bf16", "do", "delta", "dq", "dk", "dv", "da", "lora_part", "rope_global", "rope_local", "targets",
   "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part",
-  "q_prenorm", "k_prenorm", "attn_out_prenorm", "mlp_out_prenorm", "d_mlp_out_bf16", "d_attn_out_bf16"};
+  "q_prenorm", "k_prenorm", "attn_out_prenorm", "mlp_out_prenorm", "d_mlp_out_bf16", "d_attn_out_bf16", "ce_max",
+  "ce_sum", "ce_alpha"};
 
 // Slots written by a layer's (re)computed forward and read by its backward, plus the
 // split-K scratch: the training step keeps two copies, so that the recompute of layer l-1
@@ -71,8 +74,9 @@ struct Layout {
   size_t off[S_COUNT];
   size_t off1[S_COUNT];  // second copy of the per-set slots (equal to off[] for the others)
   size_t total;
-  int lm_splits;
-  int ntiles;
+  int lm_chunk;   // vocabulary columns per LM-head chunk
+  int lm_splits;  // split-K factor of a whole chunk's dH product (narrower chunks use fewer)
+  int ntiles;     // statistics tiles of a whole chunk (the stats row pitch)
   size_t split_floats;
   size_t lora_part_floats;
 };
@@ -91,6 +95,20 @@ size_t tn_part(int M, int Kout, std::initializer_list<int> Ns) {
   return gemm_part_floats(M, Kout, plan_tn(M, Kout, v, n, false).splits);
 }
 
+// Columns of one LM-head vocabulary chunk: the chunk's fp16 logits [N][chunk] take at most
+// MEBP_LM_CHUNK_MB (default 512) MiB; a multiple of 256 columns, the whole vocabulary when
+// it fits.
+int lm_chunk_cols(size_t N, int V) {
+  static const size_t budget = [] {
+    const char* e = getenv("MEBP_LM_CHUNK_MB");
+    const long v = e && *e ? atol(e) : 512;
+    return (size_t)(v > 0 ? v : 512) << 20;
+  }();
+  size_t c = budget / (N * 2) / 256 * 256;
+  if (c < 256) c = 256;
+  return c >= (size_t)V ? V : (int)c;
+}
+
 int lm_head_splits(int N, int d, int V) {
   // token tiles are 256 rows in the large-tile kernel, 128 in the other
   const int bm = plan_tn(N, d, &V, 1, true).big ? 256 : 128;
@@ -107,8 +125,10 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   const size_t N = (size_t)B * T, d = c->hidden, qd = (size_t)c->n_heads * c->head_dim,
                kvd = (size_t)c->n_kv_heads * c->head_dim, F = c->ffn, r = c->lora_rank > 0 ? c->lora_rank : 16,
                V = c->vocab, H = c->n_heads;
-  L->lm_splits = V ? lm_head_splits((int)N, (int)d, (int)V) : 0;
-  L->ntiles = V ? gemm_logit_stat_tiles((int)N, (int)V, (int)d) : 0;
+  L->lm_chunk = V ? lm_chunk_cols(N, (int)V) : 0;
+  const size_t Vc = L->lm_chunk;
+  L->lm_splits = V ? lm_head_splits((int)N, (int)d, (int)Vc) : 0;
+  L->ntiles = V ? gemm_logit_stat_tiles((int)Vc) : 0;
   size_t sz[S_COUNT] = {};
   sz[S_A] = N * d * 2;
   sz[S_Q] = N * qd * 2;
@@ -138,7 +158,7 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   sz[S_ROPE_L] = (size_t)T * c->head_dim * 4;
   sz[S_TGT] = N * 4;
   sz[S_HF] = V ? N * d * 2 : 0;
-  sz[S_LOGITS] = N * V * 2;
+  sz[S_LOGITS] = N * Vc * 2;
   sz[S_STATS] = N * (size_t)L->ntiles * 8;
   sz[S_LSEV] = V ? N * 4 : 0;
   sz[S_TGTLOGIT] = V ? N * 4 : 0;
@@ -146,6 +166,9 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
   sz[S_DHF] = V ? N * d * 4 : 0;
   sz[S_LMPART] = (size_t)L->lm_splits * N * d * 4;
   sz[S_GRAD] = N * d * 4;
+  sz[S_CEMAX] = V ? N * 4 : 0;
+  sz[S_CESUM] = V ? N * 4 : 0;
+  sz[S_CEALPHA] = V ? N * 4 : 0;
   const bool qkn = c->arch & MEBP_ARCH_QK_NORM, sw = c->arch & MEBP_ARCH_SANDWICH;
   sz[S_QPRE] = qkn ? N * qd * 2 : 0;
   sz[S_KPRE] = qkn ? N * kvd * 2 : 0;
@@ -334,7 +357,7 @@ Tp* xs(const Ctx& x, int s) {
   return (Tp*)((char*)x.ws + (which ? x.L.off1[s] : x.L.off[s]));
 }
 
-SplitScratch scratch(const Ctx& x) {
+SplitScratch split_scratch(const Ctx& x) {
   SplitScratch sc;
   sc.part = xs<float>(x, S_SPLIT);
   sc.part_floats = x.L.split_floats;
@@ -369,7 +392,7 @@ NtArgs nt_args(const Ctx& x, const f16* X, int K, std::initializer_list<NtSeg> s
   for (const NtSeg& s : segs) a.seg[a.nseg++] = s;
   a.lora_s = x.D.s;
   a.r = x.D.r;
-  const SplitScratch sc = scratch(x);
+  const SplitScratch sc = split_scratch(x);
   a.part = sc.part;
   a.part_floats = sc.part_floats;
   a.eps = x.c->rms_eps;
@@ -377,7 +400,7 @@ NtArgs nt_args(const Ctx& x, const f16* X, int K, std::initializer_list<NtSeg> s
 }
 
 void set_scratch(const Ctx& x, TnArgs& t) {
-  const SplitScratch sc = scratch(x);
+  const SplitScratch sc = split_scratch(x);
   t.part = sc.part;
   t.part_floats = sc.part_floats;
 }
@@ -520,7 +543,7 @@ int layer_forward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_l
   at.B = x.B; at.T = x.T; at.Hq = c->n_heads; at.Hkv = c->n_kv_heads; at.dh = c->head_dim;
   at.window = is_global(c, l) ? 0 : c->window;
   at.o = o; at.lse = xs<float>(x, S_LSE);
-  HIP_TRY(launch_attn_fwd(at, scratch(x), x.st));
+  HIP_TRY(launch_attn_fwd(at, split_scratch(x), x.st));
   HIP_TRY(lora_down(x, lora, o, D.qd, {MEBP_O}, &lr));
   if (sandwich) {
     // t = o-projection (kept for the backward), h = x + RMSNorm(t), c = RMSNorm(h)
@@ -662,7 +685,7 @@ int layer_backward_only(const Ctx& x, int l, const mebp_layer_base* base, const 
     at.o = o; at.lse = xs<float>(x, S_LSE);
     at.dO = dO; at.cs = rope; at.dq = dq; at.dk = dk; at.dv = dv;
     if (x.aux && x.aux_used) *x.aux_used = true;
-    HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), scratch(x), x.st, x.aux, x.ev_lr, x.ev_du, true));
+    HIP_TRY(launch_attn_bwd(at, xs<float>(x, S_DELTA), split_scratch(x), x.st, x.aux, x.ev_lr, x.ev_du, true));
   }
   if (c->arch & MEBP_ARCH_QK_NORM) {
     // through the per-head norms (the biases are frozen and need no gradient)
@@ -696,11 +719,19 @@ int layer_backward(const Ctx& x, int l, const mebp_layer_base* base, const mebp_
   return layer_backward_only(x, l, base, lora, x_ckpt, dy, dx, grads, rope, dy_bf16_ready);
 }
 
+// The final block (Sec. 4.2: the final linear layer and the loss layer are one block of the
+// checkpointed graph): final RMSNorm, logits against the tied int4 embedding, next-token
+// cross-entropy and its gradient. The vocabulary is processed in chunks so that only one
+// chunk's logits exist at a time: per chunk the logits product (tile statistics and
+// tile-relative fp16 logits), the merge of its statistics into each row's running maximum
+// and sum, its softmax weights relative to the running maximum (in place, bf16), and the dH
+// product accumulated into an fp32 row accumulator rescaled to the new maximum. Every logit
+// is computed once (4 N d V flops for both products).
 int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const float* x_last, const int32_t* ids,
             float* loss, float* dx_last, bf16* dx_last_bf16, bool hf_ready = false) {
   const mebp_config* c = x.c;
   const Dims& D = x.D;
-  const int V = c->vocab;
+  const int V = c->vocab, d = D.d, N = D.N;
   int32_t* tgt = xs<int32_t>(x, S_TGT);
   f16* hf = xs<f16>(x, S_HF);
   _Float16* logits = xs<_Float16>(x, S_LOGITS);
@@ -710,34 +741,42 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
   float* rl = xs<float>(x, S_ROWLOSS);
   float* dhf = xs<float>(x, S_DHF);
   float* part = xs<float>(x, S_LMPART);
+  float* mrun = xs<float>(x, S_CEMAX);
+  float* lrun = xs<float>(x, S_CESUM);
+  float* alpha = xs<float>(x, S_CEALPHA);
   const float inv_n = 1.0f / (float)((long long)x.B * (x.T - 1));
+  const int Vc = x.L.lm_chunk, ldt = x.L.ntiles, kg = (d + 31) / 32;
 
   HIP_TRY(launch_targets(ids, x.B, x.T, c->vocab, tgt, x.st));
-  if (!hf_ready) HIP_TRY(launch_rmsnorm_fwd(x_last, norm_final, D.N, D.d, c->rms_eps, hf, nullptr, x.st));
-  {
-    NtArgs a{};
-    a.X = hf; a.lda = D.d; a.M = D.N; a.K = D.d; a.nseg = 1;
-    a.seg[0].q4 = emb->q4; a.seg[0].scale = emb->scale; a.seg[0].N = V; a.seg[0].tile0 = 0;
-    a.seg[0].out = logits; a.seg[0].ldo = V;
-    a.stats = stats; a.tgt = tgt; a.tgt_logit = tl; a.ntiles = x.L.ntiles;
-    HIP_TRY(launch_gemm_nt(a, NT_LOGITS, x.st));
+  if (!hf_ready) HIP_TRY(launch_rmsnorm_fwd(x_last, norm_final, N, d, c->rms_eps, hf, nullptr, x.st));
+  for (int v0 = 0; v0 < V; v0 += Vc) {
+    const int w = V - v0 < Vc ? V - v0 : Vc;
+    const int first = v0 == 0;
+    const uint8_t* eq4 = emb->q4 + (size_t)v0 * (d / 2);
+    const uint16_t* esc = emb->scale + (size_t)v0 * kg;
+    {
+      NtArgs a{};
+      a.X = hf; a.lda = d; a.M = N; a.K = d; a.nseg = 1;
+      a.seg[0].q4 = eq4; a.seg[0].scale = esc; a.seg[0].N = w; a.seg[0].tile0 = 0;
+      a.seg[0].out = logits; a.seg[0].ldo = Vc;
+      a.stats = stats; a.tgt = tgt; a.tgt_logit = tl; a.ntiles = ldt; a.vbase = v0;
+      HIP_TRY(launch_gemm_nt(a, NT_LOGITS, x.st));
+    }
+    HIP_TRY(launch_ce_chunk_stats(stats, ldt, gemm_logit_stat_tiles(w), N, mrun, lrun, alpha, first, x.st));
+    HIP_TRY(launch_ce_probs(reinterpret_cast<uint16_t*>(logits), N, w, Vc, stats, ldt, mrun, tgt, v0, x.st));
+    {
+      TnArgs t{};
+      t.M = N; t.Kout = d; t.nseg = 1; t.r = 0;
+      t.seg[0].G = (const bf16*)logits; t.seg[0].ldg = Vc;
+      t.seg[0].q4 = eq4; t.seg[0].scale = esc; t.seg[0].N = w;
+      t.out = part; t.ldo = d; t.splits = lm_head_splits(N, d, w);
+      HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_BF16, x.st));
+      HIP_TRY(launch_ce_dh_accum(part, t.splits, N, d, alpha, first, dhf, x.st));
+    }
   }
-  HIP_TRY(launch_ce_rows(stats, x.L.ntiles, tl, tgt, D.N, lse, rl, x.st));
-  HIP_TRY(launch_ce_loss(rl, tgt, D.N, inv_n, loss, x.st));
-  // softmax probabilities over the logits (in place, bf16), then dH = P E on plain operands
-  HIP_TRY(launch_ce_probs(reinterpret_cast<uint16_t*>(logits), D.N, V, lse, tgt, x.st));
-  {
-    TnArgs t{};
-    set_scratch(x, t);
-    t.M = D.N; t.Kout = D.d; t.nseg = 1; t.r = 0;
-    t.seg[0].G = (const bf16*)logits; t.seg[0].ldg = V;
-    t.seg[0].q4 = emb->q4; t.seg[0].scale = emb->scale; t.seg[0].N = V;
-    t.out = part; t.ldo = D.d; t.splits = x.L.lm_splits;
-    HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_BF16, x.st));
-  }
-  HIP_TRY(launch_ce_dh_reduce(part, x.L.lm_splits, D.N, D.d, emb->q4, emb->scale, tgt, inv_n, dhf, x.st));
-  HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, D.N, D.d, c->rms_eps, dx_last,
-                             dx_last_bf16, x.st));
+  HIP_TRY(launch_ce_final(N, d, emb->q4, emb->scale, tgt, tl, mrun, lrun, inv_n, dhf, lse, rl, x.st));
+  HIP_TRY(launch_ce_loss(rl, tgt, N, inv_n, loss, x.st));
+  HIP_TRY(launch_rmsnorm_bwd(x_last, norm_final, dhf, nullptr, N, d, c->rms_eps, dx_last, dx_last_bf16, x.st));
   return MEBP_OK;
 }
 
@@ -1247,6 +1286,19 @@ int mebp_dequant_q4(const mebp_q4* w, int32_t rows, int32_t cols, int32_t group,
   if ((out_f32 && !aligned(out_f32, 16)) || (out_bf16 && !aligned(out_bf16, 16)))
     return fail(MEBP_EINVAL, "outputs must be 16-byte aligned");
   HIP_TRY(launch_dequant(w->q4, w->scale, rows, cols, group, out_f32, out_bf16, (hipStream_t)stream));
+  return MEBP_OK;
+}
+
+int mebp_test_gemm(int32_t kind, const mebp_q4* w, int32_t n_out, int32_t n_in, const void* x, int32_t M, float* out,
+                   mebp_stream_t stream) {
+  int e;
+  if ((e = check_q4(w, "weight"))) return e;
+  if (kind < MEBP_TEST_GEMM_NT || kind > MEBP_TEST_GEMM_TN_BIG) return fail(MEBP_EINVAL, "unknown GEMM kind %d", kind);
+  if (M < 1 || n_out < 1 || n_in < 1) return fail(MEBP_EINVAL, "non-positive size");
+  if (M > 65536 || n_out > 65536 || n_in > 65536) return fail(MEBP_EUNSUPPORTED, "size above 65536");
+  if (n_in % 16 || n_out % 16) return fail(MEBP_EUNSUPPORTED, "n_in %d / n_out %d not multiples of 16", n_in, n_out);
+  if ((e = check_act(x, "x")) || (e = check_act(out, "out"))) return e;
+  HIP_TRY(launch_gemm_probe(kind, w->q4, w->scale, n_out, n_in, x, M, out, (hipStream_t)stream));
   return MEBP_OK;
 }
 

@@ -226,23 +226,37 @@ __global__ void k_targets(const int32_t* ids, int B, int T, int V, int32_t* tgt)
   tgt[i] = v;
 }
 
-// one wave per row: lse = M + log(sum s_i exp(m_i - M)); row_loss = lse - logit[target]
-__global__ __launch_bounds__(256) void k_ce_rows(const float2* stats, int ntiles, const float* tgt_logit,
-                                                 const int32_t* tgt, int M, float* lse, float* row_loss) {
+// The LM head runs over the vocabulary in chunks (columns [v0, v0 + w) at a time) with
+// per-row running statistics: m = the largest logit so far, l = sum of exp(logit - m) so
+// far. The logits GEMM leaves per (row, 64-column tile) its maximum and its sum of
+// exp(logit - max), and the logits themselves relative to that maximum (fp16).
+
+// One wave per row: the chunk's (max, sum) from its tiles, merged into the running (m, l);
+// alpha = exp(m_old - m_new), the factor that moves the row's dH accumulator to the new
+// maximum (unused on the first chunk, which sets m and l).
+__global__ __launch_bounds__(256) void k_ce_chunk_stats(const float2* stats, int ld, int nt, int M, float* mrun,
+                                                        float* lrun, float* alpha, int first) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= M) return;
-  const float2* st = stats + (size_t)row * ntiles;
+  const float2* st = stats + (size_t)row * ld;
   float mx = -INFINITY;
-  for (int i = lane; i < ntiles; i += 64) mx = fmaxf(mx, st[i].x);
+  for (int i = lane; i < nt; i += 64) mx = fmaxf(mx, st[i].x);
   mx = wave_max(mx);
   float se = 0.f;
-  for (int i = lane; i < ntiles; i += 64) se += st[i].y * __expf(st[i].x - mx);
+  for (int i = lane; i < nt; i += 64) se += st[i].y * __expf(st[i].x - mx);
   se = wave_sum(se);
   if (lane == 0) {
-    const float l = mx + logf(se);
-    lse[row] = l;
-    const int tg = tgt[row];
-    row_loss[row] = tg >= 0 ? l - tgt_logit[row] : (tg == -1 ? 0.f : NAN);
+    if (first) {
+      mrun[row] = mx;
+      lrun[row] = se;
+      alpha[row] = 0.f;
+    } else {
+      const float mo = mrun[row], mn = fmaxf(mo, mx);
+      const float a = __expf(mo - mn);
+      lrun[row] = lrun[row] * a + se * __expf(mx - mn);
+      mrun[row] = mn;
+      alpha[row] = a;
+    }
   }
 }
 
@@ -267,76 +281,93 @@ __global__ __launch_bounds__(256) void k_copy_host(const uint4* __restrict__ src
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)COPY_WGS * 256) dst[i] = src[i];
 }
 
-// Softmax probabilities of the LM head, p[m][v] = exp(logit[m][v] - lse[m]) for rows with a
-// target and 0 for the others, rounded to bf16 and written over the fp16 logits in place:
-// the A operand of the dH product, computed once instead of in every column tile of it.
-__global__ __launch_bounds__(256) void k_ce_probs(uint16_t* lg, int M, int V, const float* lse, const int32_t* tgt) {
+// Unnormalised softmax weights of one vocabulary chunk, written in place over its fp16
+// logits as the bf16 A operand of the dH product: p = exp(logit - m) with m the row's
+// running maximum after this chunk (logit - m = stored value + tile maximum - m, so the
+// fp16 rounding applies to the small tile-relative value only). The target column is
+// left out (0): its term (P_target - 1) E[target] is added in fp32 by k_ce_final, so the
+// cancellation of a confident row's gradient does not go through 16-bit operands. Rows
+// without a target get zeros. One thread per 8 columns (w % 8 == 0, rows 16-byte aligned).
+__global__ __launch_bounds__(256) void k_ce_probs(uint16_t* lg, int M, int w, int ld, const float2* stats,
+                                                  int ld_tiles, const float* mrun, const int32_t* tgt, int v0) {
+  const int per_row = w >> 3;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if ((V & 7) == 0) {
-    const size_t per_row = (size_t)(V >> 3);
-    if (i >= (size_t)M * per_row) return;
-    const int m = (int)(i / per_row);
-    uint4* p = reinterpret_cast<uint4*>(lg) + i;  // rows are whole 16-byte chunks
-    uint4 o = make_uint4(0, 0, 0, 0);
-    if (tgt[m] >= 0) {
-      const float l = lse[m];
-      const uint4 h = *p;
-      o = make_uint4(pack_bf16x2(__expf(f16_lo(h.x) - l), __expf(f16_hi(h.x) - l)),
-                     pack_bf16x2(__expf(f16_lo(h.y) - l), __expf(f16_hi(h.y) - l)),
-                     pack_bf16x2(__expf(f16_lo(h.z) - l), __expf(f16_hi(h.z) - l)),
-                     pack_bf16x2(__expf(f16_lo(h.w) - l), __expf(f16_hi(h.w) - l)));
+  if (i >= (size_t)M * per_row) return;
+  const int m = (int)(i / per_row), c = (int)(i % per_row) * 8;
+  uint4* p = reinterpret_cast<uint4*>(lg + (size_t)m * ld + c);
+  const int tg = tgt[m];
+  uint4 o = make_uint4(0, 0, 0, 0);
+  if (tg >= 0) {
+    const float shift = stats[(size_t)m * ld_tiles + (c >> 6)].x - mrun[m];
+    const uint4 h = *p;
+    const uint32_t hw[4] = {h.x, h.y, h.z, h.w};
+    float e[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      e[2 * j] = __expf(f16_lo(hw[j]) + shift);
+      e[2 * j + 1] = __expf(f16_hi(hw[j]) + shift);
     }
-    *p = o;
-  } else {
-    if (i >= (size_t)M * V) return;
-    const int m = (int)(i / (size_t)V);
-    float v = 0.f;
-    if (tgt[m] >= 0) v = __expf(half_bits_to_f32(lg[i]) - lse[m]);
-    lg[i] = __builtin_bit_cast(uint16_t, (bf16)v);
+    const int tl = tg - v0 - c;
+    if (tl >= 0 && tl < 8) e[tl] = 0.f;
+    o = make_uint4(pack_bf16x2(e[0], e[1]), pack_bf16x2(e[2], e[3]), pack_bf16x2(e[4], e[5]), pack_bf16x2(e[6], e[7]));
   }
+  *p = o;
 }
 
-// dhf[m][k] = inv_n * (sum_s part[s][m][k] - E[tgt[m]][k]) for rows with a target, else 0
-__global__ void k_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
-                               const uint16_t* escale, const int32_t* tgt, float inv_n, float* dhf) {
+// dH accumulator of the LM head: dh = (first ? 0 : alpha[m] dh) + sum_s part[s] (split-K
+// planes of this chunk's product, summed in split order). One thread per 4 values.
+__global__ __launch_bounds__(256) void k_ce_dh_accum(const float* part, int splits, int M, int d, const float* alpha,
+                                                     int first, float* dh) {
+  const size_t n4 = (size_t)M * d / 4;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  float4 v = ((const float4*)part)[i];
+  for (int s = 1; s < splits; ++s) {
+    const float4 t = ((const float4*)part)[(size_t)s * n4 + i];
+    v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
+  }
+  if (!first) {
+    const float a = alpha[(i * 4) / d];
+    const float4 o = ((const float4*)dh)[i];
+    v.x += a * o.x; v.y += a * o.y; v.z += a * o.z; v.w += a * o.w;
+  }
+  ((float4*)dh)[i] = v;
+}
+
+// End of the LM head, per row: lse = m + log l, the row's loss term lse - logit[target],
+// and, in place, dhf = inv_n (dh / l + (P_target - 1) E[target]) with P_target - 1 =
+// expm1(logit[target] - lse) and E[target] decompressed exactly in fp32; rows without a
+// target get zeros, an id outside [0, V) a NaN loss term. One thread per 8 columns.
+__global__ __launch_bounds__(256) void k_ce_final(int M, int d, const uint8_t* eq4, const uint16_t* escale,
+                                                  const int32_t* tgt, const float* tgt_logit, const float* mrun,
+                                                  const float* lrun, float inv_n, float* dhf, float* lse,
+                                                  float* row_loss) {
   const int per_row = d >> 3;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (size_t)M * per_row) return;
   const int m = (int)(i / per_row), c = (int)(i % per_row) * 8;
   const int tg = tgt[m];
-  float o[8];
-  if (tg < 0) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) o[j] = 0.f;
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) o[j] = 0.f;
-    for (int sp = 0; sp < splits; ++sp) {
-      const float4* p = (const float4*)(part + ((size_t)sp * M + m) * d + c);
-      const float4 a = p[0], b = p[1];
-      o[0] += a.x; o[1] += a.y; o[2] += a.z; o[3] += a.w;
-      o[4] += b.x; o[5] += b.y; o[6] += b.z; o[7] += b.w;
-    }
-    const int ng = (d + 31) >> 5;
-    const uint32_t w = *(const uint32_t*)(eq4 + (size_t)tg * (d >> 1) + (c >> 1));
-    const float s = half_bits_to_f32(escale[(size_t)tg * ng + (c >> 5)]);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) o[j] = inv_n * (o[j] - (float)nib_s(w, j) * s);
+  const float l = lrun[m], L = mrun[m] + logf(l);
+  if (c == 0) {
+    lse[m] = L;
+    row_loss[m] = tg >= 0 ? L - tgt_logit[m] : (tg == -1 ? 0.f : NAN);
   }
   float4* out = (float4*)(dhf + (size_t)m * d + c);
+  if (tg < 0) {
+    out[0] = out[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
+  const float pt1 = expm1f(tgt_logit[m] - L), inv_l = 1.0f / l;
+  const int ng = (d + 31) >> 5;
+  const uint32_t w = *(const uint32_t*)(eq4 + (size_t)tg * (d >> 1) + (c >> 1));
+  const float s = half_bits_to_f32(escale[(size_t)tg * ng + (c >> 5)]);
+  const float4 a = out[0], b = out[1];
+  const float h[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  float o[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) o[j] = inv_n * (h[j] * inv_l + pt1 * ((float)nib_s(w, j) * s));
   out[0] = make_float4(o[0], o[1], o[2], o[3]);
   out[1] = make_float4(o[4], o[5], o[6], o[7]);
-}
-
-__global__ void k_splitk_reduce(const float* part, int splits, size_t n4, float* out) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n4) return;
-  float4 acc = ((const float4*)part)[i];
-  for (int s = 1; s < splits; ++s) {
-    const float4 v = ((const float4*)part)[(size_t)s * n4 + i];
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-  }
-  ((float4*)out)[i] = acc;
 }
 
 inline unsigned blocks_for(size_t n, unsigned bs) { return (unsigned)((n + bs - 1) / bs); }
@@ -557,11 +588,11 @@ hipError_t launch_targets(const int32_t* ids, int B, int T, int V, int32_t* tgt,
              hipLaunchKernelGGL(k_targets, dim3(blocks_for((size_t)B * T, 256)), dim3(256), 0, st, ids, B, T, V, tgt));
   return hipGetLastError();
 }
-hipError_t launch_ce_rows(const float2* stats, int ntiles, const float* tgt_logit, const int32_t* tgt, int M,
-                          float* lse, float* row_loss, hipStream_t st) {
-  MEBP_TIMED(st, "ce_rows", 0.0, (double)M * ntiles * 8,
-             hipLaunchKernelGGL(k_ce_rows, dim3(blocks_for(M, 4)), dim3(256), 0, st, stats, ntiles, tgt_logit, tgt, M, lse,
-                     row_loss));
+hipError_t launch_ce_chunk_stats(const float2* stats, int ld, int nt, int M, float* mrun, float* lrun, float* alpha,
+                                 int first, hipStream_t st) {
+  MEBP_TIMED(st, "ce_chunk_stats", 0.0, (double)M * nt * 8 + (double)M * 12,
+             hipLaunchKernelGGL(k_ce_chunk_stats, dim3(blocks_for(M, 4)), dim3(256), 0, st, stats, ld, nt, M, mrun, lrun,
+                                alpha, first));
   return hipGetLastError();
 }
 hipError_t launch_ce_loss(const float* row_loss, const int32_t* tgt, int M, float inv_n, float* loss,
@@ -578,26 +609,32 @@ hipError_t launch_copy_host(const void* src, void* dst, size_t bytes, hipStream_
                                 bytes >> 4));
   return hipGetLastError();
 }
-hipError_t launch_ce_probs(uint16_t* logits, int M, int V, const float* lse, const int32_t* tgt, hipStream_t st) {
-  const size_t tot = (V & 7) == 0 ? (size_t)M * (V >> 3) : (size_t)M * V;
-  MEBP_TIMED(st, "ce_probs", 0.0, (double)M * V * 4,
-             hipLaunchKernelGGL(k_ce_probs, dim3(blocks_for(tot, 256)), dim3(256), 0, st, logits, M, V, lse, tgt));
+hipError_t launch_ce_probs(uint16_t* logits, int M, int w, int ld, const float2* stats, int ld_tiles,
+                           const float* mrun, const int32_t* tgt, int v0, hipStream_t st) {
+  if ((w & 7) || (ld & 7)) return hipErrorInvalidValue;
+  const size_t tot = (size_t)M * (w >> 3);
+  MEBP_TIMED(st, "ce_probs", 0.0, (double)M * w * 4,
+             hipLaunchKernelGGL(k_ce_probs, dim3(blocks_for(tot, 256)), dim3(256), 0, st, logits, M, w, ld, stats,
+                                ld_tiles, mrun, tgt, v0));
   return hipGetLastError();
 }
-hipError_t launch_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
-                               const uint16_t* escale, const int32_t* tgt, float inv_n, float* dhf,
-                               hipStream_t st) {
+hipError_t launch_ce_dh_accum(const float* part, int splits, int M, int d, const float* alpha, int first, float* dh,
+                              hipStream_t st) {
+  if (d & 3) return hipErrorInvalidValue;
+  const size_t n4 = (size_t)M * d / 4;
+  MEBP_TIMED(st, "ce_dh_accum", 0.0, (double)n4 * 16 * (splits + (first ? 1 : 2)),
+             hipLaunchKernelGGL(k_ce_dh_accum, dim3(blocks_for(n4, 256)), dim3(256), 0, st, part, splits, M, d, alpha,
+                                first, dh));
+  return hipGetLastError();
+}
+hipError_t launch_ce_final(int M, int d, const uint8_t* eq4, const uint16_t* escale, const int32_t* tgt,
+                           const float* tgt_logit, const float* mrun, const float* lrun, float inv_n, float* dhf,
+                           float* lse, float* row_loss, hipStream_t st) {
+  if (d & 7) return hipErrorInvalidValue;
   const size_t tot = (size_t)M * (d >> 3);
-  MEBP_TIMED(st, "ce_dh_reduce", 0.0, (double)tot * 8 * 4 * (splits + 1),
-             hipLaunchKernelGGL(k_ce_dh_reduce, dim3(blocks_for(tot, 256)), dim3(256), 0, st, part, splits, M, d, eq4, escale,
-                     tgt, inv_n, dhf));
+  MEBP_TIMED(st, "ce_final", 0.0, (double)M * d * 8.5,
+             hipLaunchKernelGGL(k_ce_final, dim3(blocks_for(tot, 256)), dim3(256), 0, st, M, d, eq4, escale, tgt,
+                                tgt_logit, mrun, lrun, inv_n, dhf, lse, row_loss));
   return hipGetLastError();
 }
-hipError_t launch_splitk_reduce(const float* part, int splits, size_t n, float* out, hipStream_t st) {
-  const size_t n4 = n >> 2;
-  MEBP_TIMED(st, "splitk_reduce", 0.0, (double)n4 * 16 * (splits + 1),
-             hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks_for(n4, 256)), dim3(256), 0, st, part, splits, n4, out));
-  return hipGetLastError();
-}
-
 }  // namespace mebp

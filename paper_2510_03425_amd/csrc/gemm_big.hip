@@ -249,7 +249,9 @@ DEV void nt_big_epilogue(f32x16 (&acc)[4][BN / (32 * WNW)], const NtArgs& a, con
   constexpr int NJ = BN / (32 * WNW);
   const int Nn = sg.N;
   if constexpr (EPI == NT_LOGITS) {
-    // every wave covers one statistics tile of 32 NJ columns
+    // every wave covers one statistics tile of 32 NJ = 64 columns: per row its max, its
+    // sum of exp(v - max), the logits minus that max (fp16), and the fp32 target logit
+    static_assert(32 * NJ == 64, "statistics tiles are 64 columns wide");
     _Float16* out = (_Float16*)sg.out;
     const int cw0 = wcol0;
     const int stile = cw0 / (32 * NJ);
@@ -273,8 +275,8 @@ DEV void nt_big_epilogue(f32x16 (&acc)[4][BN / (32 * WNW)], const NtArgs& a, con
             const float v = acc[i][j][q];
             se += __expf(v - mx);
             if (m < a.M) {
-              out[(size_t)m * sg.ldo + n] = (_Float16)v;
-              if (n == tg) a.tgt_logit[m] = v;
+              out[(size_t)m * sg.ldo + n] = (_Float16)(v - mx);
+              if (n + a.vbase == tg) a.tgt_logit[m] = v;
             }
           }
         }
@@ -1092,6 +1094,38 @@ hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S
   TN_BIG_EPI(128);
 #undef TN_BIG_EPI
 #undef TN_BIG
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_probe_big(int kind, const uint8_t* q4, const uint16_t* scale, int n_out, int n_in,
+                                 const void* x, int M, float* out, hipStream_t st) {
+  NtArgs a{};
+  a.X = x; a.lda = n_in; a.M = M; a.K = n_in; a.nseg = 1;
+  a.seg[0].q4 = q4; a.seg[0].scale = scale; a.seg[0].N = n_out; a.seg[0].out = out; a.seg[0].ldo = n_out;
+  const int mt = (M + BM - 1) / BM;
+  switch (kind) {
+    case 1:  // register-staged forward, 256 x 128 tiles
+      hipLaunchKernelGGL((k_gemm_nt_big<128, 2, NT_STORE_F32, true>), dim3((n_out + 127) / 128, mt, 1), dim3(256), 0,
+                         st, a);
+      break;
+    case 2:  // register-staged forward, 256 x 256 tiles
+      hipLaunchKernelGGL((k_gemm_nt_big<256, 4, NT_STORE_F32, true>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0,
+                         st, a);
+      break;
+    case 3:  // LDS-direct forward, 256 x 256 tiles
+      hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0, st, a);
+      break;
+    case 5: {  // transposed, 256 x 128 tiles
+      TnArgs t{};
+      t.M = M; t.Kout = n_in; t.nseg = 1;
+      t.seg[0].G = (const bf16*)x; t.seg[0].ldg = n_out; t.seg[0].q4 = q4; t.seg[0].scale = scale; t.seg[0].N = n_out;
+      t.out = out; t.ldo = n_in; t.splits = 1;
+      hipLaunchKernelGGL((k_gemm_tn_big<128, TN_STORE_F32>), dim3((n_in + 127) / 128, mt, 1), dim3(NTH), 0, st, t);
+      break;
+    }
+    default:
+      return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -215,19 +215,20 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
   }
 
   if constexpr (EPI == NT_LOGITS) {
-    // fp16 logits, per-row partial (max, sum exp) over this 128-column tile, target logit
-    float* red = (float*)As;  // [2 waves along n][BM] max, then sum
+    // per row and this wave's 64 columns (one statistics tile): max, sum of exp(v - max);
+    // the logits stored relative to that max (fp16); the fp32 target logit
     _Float16* out = (_Float16*)sg.out;
+    const int cw0 = n0 + wn * 64;
+    const int stile = cw0 >> 6;
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm) {
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
-        const int ml = wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
-        const int m = m0 + ml;
+        const int m = m0 + wm * 64 + tm * 16 + 4 * (lane >> 4) + rr;
         float mx = -INFINITY;
 #pragma unroll
         for (int tn = 0; tn < 4; ++tn) {
-          const int n = n0 + wn * 64 + tn * 16 + (lane & 15);
+          const int n = cw0 + tn * 16 + (lane & 15);
           if (n < Nn) mx = fmaxf(mx, acc[tm][tn][rr]);
         }
 #pragma unroll
@@ -236,28 +237,20 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm_nt(const NtArgs a) {
         const int tg = m < a.M ? a.tgt[m] : -1;
 #pragma unroll
         for (int tn = 0; tn < 4; ++tn) {
-          const int n = n0 + wn * 64 + tn * 16 + (lane & 15);
+          const int n = cw0 + tn * 16 + (lane & 15);
           const float v = acc[tm][tn][rr];
           if (n < Nn) {
             se += __expf(v - mx);
-            if (m < a.M) out[(size_t)m * sg.ldo + n] = (_Float16)v;
-            if (n == tg) a.tgt_logit[m] = v;
+            if (m < a.M) {
+              out[(size_t)m * sg.ldo + n] = (_Float16)(v - mx);
+              if (n + a.vbase == tg) a.tgt_logit[m] = v;
+            }
           }
         }
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) se += __shfl_xor(se, o, 64);
-        if ((lane & 15) == 0) {
-          red[wn * BM + ml] = mx;
-          red[2 * BM + wn * BM + ml] = se;
-        }
+        if ((lane & 15) == 0 && m < a.M && cw0 < Nn) a.stats[(size_t)m * a.ntiles + stile] = make_float2(mx, se);
       }
-    }
-    __syncthreads();
-    if (tid < BM && m0 + tid < a.M) {
-      const float m1 = red[tid], m2 = red[BM + tid];
-      const float mx = fmaxf(m1, m2);
-      const float se = red[2 * BM + tid] * __expf(m1 - mx) + red[3 * BM + tid] * __expf(m2 - mx);
-      a.stats[(size_t)(m0 + tid) * a.ntiles + nt] = make_float2(mx, se);
     }
     return;
   } else {
@@ -872,11 +865,7 @@ GemmPlan plan_nt(int M, const int* Ns, int nseg, int K, int epi) {
   return p;
 }
 
-int gemm_logit_stat_tiles(int M, int V, int K) {
-  // the large-tile kernels give every wave 64 columns, the 128 x 128 kernel 128 per tile
-  const GemmPlan p = plan_nt(M, &V, 1, K, NT_LOGITS);
-  return p.big ? (V + 63) / 64 : (V + BN - 1) / BN;
-}
+int gemm_logit_stat_tiles(int V) { return (V + 63) / 64; }  // every kernel's waves cover 64 columns
 
 GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg, bool softmax) {
   int kt = 0;
@@ -1061,6 +1050,28 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, 
       break;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_probe(int kind, const uint8_t* q4, const uint16_t* scale, int n_out, int n_in, const void* x,
+                             int M, float* out, hipStream_t st) {
+  if (kind == 0) {
+    NtArgs a{};
+    a.X = x; a.lda = n_in; a.M = M; a.K = n_in; a.nseg = 1;
+    a.seg[0].q4 = q4; a.seg[0].scale = scale; a.seg[0].N = n_out; a.seg[0].out = out; a.seg[0].ldo = n_out;
+    const dim3 grid(gemm_nt_tiles(n_out), (M + BM - 1) / BM, 1);
+    hipLaunchKernelGGL(k_gemm_nt<NT_STORE_F32>, grid, dim3(NTHREADS), 0, st, a);
+    return hipGetLastError();
+  }
+  if (kind == 4) {
+    TnArgs a{};
+    a.M = M; a.Kout = n_in; a.nseg = 1;
+    a.seg[0].G = (const bf16*)x; a.seg[0].ldg = n_out; a.seg[0].q4 = q4; a.seg[0].scale = scale; a.seg[0].N = n_out;
+    a.out = out; a.ldo = n_in; a.splits = 1;
+    const dim3 grid((n_in + BN - 1) / BN, (M + BM - 1) / BM, 1);
+    hipLaunchKernelGGL((k_gemm_tn<TN_STORE_F32>), grid, dim3(NTHREADS), 0, st, a);
+    return hipGetLastError();
+  }
+  return launch_gemm_probe_big(kind, q4, scale, n_out, n_in, x, M, out, st);
 }
 
 }  // namespace mebp

@@ -40,12 +40,15 @@ struct NtArgs {
   NtSeg seg[3];
   float lora_s;
   int r;
-  // NT_LOGITS: fp16 logits into seg[0].out, per (row, 128-col tile) partial (max, sum exp)
-  // into `stats` [M][ntiles] float2, the fp32 logit of the target into tgt_logit[m].
+  // NT_LOGITS: per (row, 64-column tile) the maximum and the sum of exp(logit - max) into
+  // `stats` [M][ntiles] float2 (ntiles = row pitch), the logits minus their tile's maximum
+  // as fp16 into seg[0].out, and the fp32 logit of the target into tgt_logit[m] (target ids
+  // are global vocabulary columns; the segment's first column is vbase).
   float2* stats;
   const int32_t* tgt;     // [M] target id or -1
   float* tgt_logit;
   int ntiles;
+  int vbase;
   // split-K scratch (unused when the launcher picks one split)
   float* part;
   size_t part_floats;
@@ -78,8 +81,8 @@ struct GemmPlan {
 GemmPlan plan_big(int M, int ntiles256, int ntiles128, int ktiles, bool logits, int max_bn);
 GemmPlan plan_nt(int M, const int* Ns, int nseg, int K, int epi);
 GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg, bool softmax);  // softmax: the LM head's dH
-// statistics tiles per row of the LM-head logits GEMM (the column width its waves cover)
-int gemm_logit_stat_tiles(int M, int V, int K);
+// statistics tiles per row of the LM-head logits GEMM over V columns (64 columns each)
+int gemm_logit_stat_tiles(int V);
 hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double flops, double bytes, hipStream_t st);
 
 // Transposed orientation (input gradients): C[m][c] = sum_seg sum_n G_seg[m][n] * W_seg[n][c]
@@ -132,6 +135,16 @@ struct TnArgs {
 hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st, hipEvent_t lora_ready = nullptr);
 hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S, double flops, double bytes,
                               hipStream_t st);
+
+// Test aid: one production GEMM kernel chosen by `kind` (the MEBP_TEST_GEMM_* values of the
+// C ABI) on caller operands, one split, no LoRA term or residual, fp32 outputs. Forward
+// kinds: out[M][n_out] = X fp16 [M][n_in] times W^T; transposed kinds: out[M][n_in] =
+// G bf16 [M][n_out] times W. launch_gemm_probe handles the 128 x 128 kernels and hands the
+// large-tile kinds to launch_gemm_probe_big.
+hipError_t launch_gemm_probe(int kind, const uint8_t* q4, const uint16_t* scale, int n_out, int n_in, const void* x,
+                             int M, float* out, hipStream_t st);
+hipError_t launch_gemm_probe_big(int kind, const uint8_t* q4, const uint16_t* scale, int n_out, int n_in,
+                                 const void* x, int M, float* out, hipStream_t st);
 
 // ---------------------------------------------------------------- elementwise / norms
 hipError_t launch_dequant(const uint8_t* q4, const uint16_t* scale, int rows, int cols, int group,
@@ -259,22 +272,29 @@ hipError_t launch_lora_opt(const OptSeg* segs, int nseg, OptArgs a, int mode, fl
                            hipStream_t st);
 
 // ---------------------------------------------------------------- LM head / CE
-// lse[m], loss term per row from partial stats; loss = mean over rows with target
-hipError_t launch_ce_rows(const float2* stats, int ntiles, const float* tgt_logit, const int32_t* tgt,
-                          int M, float* lse, float* row_loss, hipStream_t st);
+// The vocabulary is processed in chunks of columns [v0, v0 + w) (see k_ce_* in
+// elementwise.hip): running per-row maximum m and sum l, a rescaled fp32 dH accumulator.
+// chunk statistics from the logits GEMM's per-(row, 64-column tile) (max, sum exp) into
+// the running (m, l); alpha = exp(m_old - m_new)
+hipError_t launch_ce_chunk_stats(const float2* stats, int ld, int nt, int M, float* mrun, float* lrun, float* alpha,
+                                 int first, hipStream_t st);
+// in place: tile-relative fp16 logits of the chunk -> bf16 exp(logit - m), 0 at the target
+// column and on rows without a target
+hipError_t launch_ce_probs(uint16_t* logits, int M, int w, int ld, const float2* stats, int ld_tiles,
+                           const float* mrun, const int32_t* tgt, int v0, hipStream_t st);
+// dh = (first ? 0 : alpha[m] dh) + sum of the chunk product's split planes
+hipError_t launch_ce_dh_accum(const float* part, int splits, int M, int d, const float* alpha, int first, float* dh,
+                              hipStream_t st);
+// lse, row loss terms, and dhf = inv_n (dh / l + (P_target - 1) E[target]) in place
+hipError_t launch_ce_final(int M, int d, const uint8_t* eq4, const uint16_t* escale, const int32_t* tgt,
+                           const float* tgt_logit, const float* mrun, const float* lrun, float inv_n, float* dhf,
+                           float* lse, float* row_loss, hipStream_t st);
 hipError_t launch_ce_loss(const float* row_loss, const int32_t* tgt, int M, float inv_n, float* loss,
                           hipStream_t st);
-// dhf[m][:] = inv_n * (sum_s part[s][m][:] - E[tgt[m]][:]) (rows with target), else 0
 // bytes (a multiple of 16) between device memory and pinned host memory addressed through
 // its device address (both 16-byte aligned), by a few workgroups on `st`
 hipError_t launch_copy_host(const void* src, void* dst, size_t bytes, hipStream_t st);
-// in place: fp16 logits -> bf16 softmax probabilities (0 on rows without a target)
-hipError_t launch_ce_probs(uint16_t* logits, int M, int V, const float* lse, const int32_t* tgt, hipStream_t st);
-hipError_t launch_ce_dh_reduce(const float* part, int splits, int M, int d, const uint8_t* eq4,
-                               const uint16_t* escale, const int32_t* tgt, float inv_n, float* dhf,
-                               hipStream_t st);
 hipError_t launch_targets(const int32_t* ids, int B, int T, int V, int32_t* tgt, hipStream_t st);
-hipError_t launch_splitk_reduce(const float* part, int splits, size_t n, float* out, hipStream_t st);
 
 // ---------------------------------------------------------------- diagnostics
 // Per-kernel event timing (see timing.hip). timer_begin returns -1 when disabled.

@@ -60,8 +60,15 @@ int set_repeat(const char* name, int times) {
     s.repeat_times = 1;
     return 0;
   }
-  // kernels that overwrite one of their own inputs would not give the same result twice
-  if (!strcmp(name, "gemm_tn_act_bwd") || !strcmp(name, "splitk_finalize_actbwd")) return -1;
+  // kernels that update a buffer they also read (in place) would not give the same result
+  // twice in a row
+  static const char* const in_place[] = {
+      "gemm_tn_act_bwd", "splitk_finalize_actbwd",  // fp16 g, u -> bf16 dg, du
+      "rope_fwd", "qkv_post", "headnorm_bwd",       // q, k (or dq, dk) rotated / normalised
+      "ce_chunk_stats", "ce_probs", "ce_dh_accum", "ce_final",  // LM-head running state
+      "lora_adamw", "lora_grad_accumulate"};        // parameters, moments, accumulators
+  for (const char* n : in_place)
+    if (!strcmp(name, n)) return -1;
   s.repeat_name = name;
   s.repeat_times = times;
   return 0;

@@ -182,3 +182,32 @@ def test_grad_accumulate_rejects(built_lib):
     assert L.mebp_lora_grad_accumulate(c, g, acc, 0.5, False, 0, check=False) == L.MEBP_EINVAL
     assert C.sizeof(L.MebpAdamwHparams) == 7 * 4
     assert C.sizeof(L.MebpLayerLoraState) == 14 * 8
+
+
+def test_test_gemm_validates_first(built_lib):
+    w = L.MebpQ4(q4=0x1000, scale=0x2000)
+    X, OUT = 0x400000, 0x800000
+    g = lambda **kw: L.mebp_test_gemm(kw.get("kind", L.TEST_GEMM_NT), kw.get("w", w), kw.get("n_out", 64),
+                                      kw.get("n_in", 64), kw.get("x", X), kw.get("M", 32), kw.get("out", OUT), 0,
+                                      check=False)
+    assert g(kind=6) == L.MEBP_EINVAL and g(kind=-1) == L.MEBP_EINVAL
+    assert g(n_in=40) == L.MEBP_EUNSUPPORTED and g(n_out=8) == L.MEBP_EUNSUPPORTED
+    assert g(M=0) == L.MEBP_EINVAL and g(M=70000) == L.MEBP_EUNSUPPORTED
+    assert g(x=X + 8) == L.MEBP_EINVAL and g(out=0) == L.MEBP_EINVAL and g(w=None) == L.MEBP_EINVAL
+
+
+IN_PLACE = ["gemm_tn_act_bwd", "splitk_finalize_actbwd", "rope_fwd", "qkv_post", "headnorm_bwd", "ce_chunk_stats",
+            "ce_probs", "ce_dh_accum", "ce_final", "lora_adamw", "lora_grad_accumulate"]
+
+
+@pytest.mark.parametrize("name", IN_PLACE)
+def test_kernel_repeat_refuses_in_place_kernels(built_lib, name):
+    # repeating a kernel that updates its own input would change the result
+    assert built_lib.mebp_kernel_repeat(name.encode(), 3) == L.MEBP_EINVAL
+    assert "cannot be repeated" in L.mebp_last_error()
+
+
+def test_kernel_repeat_accepts_pure_kernels_and_switches_off(built_lib):
+    for name in ("gemm_nt_f16out", "gemm_tn_probs_dh", "attn_fwd", "lora_rows"):
+        assert built_lib.mebp_kernel_repeat(name.encode(), 3) == L.MEBP_OK
+    assert built_lib.mebp_kernel_repeat(None, 1) == L.MEBP_OK

@@ -13,7 +13,7 @@ from mebp_inputs import CONFIGS, MINI, PROJ, layer_input, make_inputs
 from paper_2510_03425_amd import _lib as L
 from paper_2510_03425_amd.device import DeviceModel, slot_index
 
-from gpu_util import TOL, rel_l2, say, to_np
+from gpu_util import ROW_TOL, TOL, max_row_rel_l2, rel_l2, say, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -95,9 +95,14 @@ def test_layer_forward_parity(built_lib, gpu, name, layer, norm):
            "v": cache["v4d"].reshape(N, -1), "o": cache["O"], "h": cache["h"], "c": cache["c"], "z": cache["z"]}
     errs = {k: rel_l2(to_np(got[k]), v) for k, v in ref.items()}
     errs["y"] = rel_l2(to_np(ty), y_ref)
+    rows = {k: max_row_rel_l2(to_np(got[k]), v) for k, v in ref.items()}
+    rows["y"] = max_row_rel_l2(to_np(ty), y_ref)
     say("rel-L2", {k: f"{v:.2e}" for k, v in errs.items()})
+    say("max row rel-L2", {k: f"{v:.2e}" for k, v in rows.items()})
     for k, e in errs.items():
         assert e <= TOL, (k, e)
+    for k, e in rows.items():
+        assert e <= ROW_TOL, (k, "row", e)
 
 
 @pytest.mark.parametrize("name,layer,norm", LAYER_CASES)
@@ -115,9 +120,48 @@ def test_layer_backward_parity(built_lib, gpu, name, layer, norm):
     for p, (dA, dB) in grads.items():
         errs["dA_" + p] = rel_l2(to_np(dm.dA[layer][p]), dA)
         errs["dB_" + p] = rel_l2(to_np(dm.dB[layer][p]), dB)
-    say("rel-L2", {k: f"{v:.2e}" for k, v in errs.items()})
+    row = max_row_rel_l2(to_np(tdx), dx_ref)
+    say("rel-L2", {k: f"{v:.2e}" for k, v in errs.items()}, "dx max row", f"{row:.2e}")
     for k, e in errs.items():
         assert e <= TOL, (k, e)
+    assert row <= ROW_TOL, ("dx row", row)
+
+
+# Larger magnitudes than the random-init inputs: the layer input scaled by 30 (the residual
+# stream of a deep model), and norm weights scaled by 8 (every normalised activation 8 times
+# larger: attention scores 64 times, a sharply peaked softmax, gate/up products 64 times).
+@pytest.mark.parametrize("case", ["x_times_30", "norm_times_8"])
+def test_layer_parity_large_magnitudes(built_lib, gpu, case):
+    cfg = MINI
+    inp = make_inputs(cfg, seed=21, norm="random")
+    x, dy = layer_input(cfg, 121)
+    if case == "x_times_30":
+        x = (x * 30.0).astype(np.float32)
+    else:
+        inp.norm_attn = [(w * 8.0).astype(np.float32) for w in inp.norm_attn]
+        inp.norm_mlp = [(w * 8.0).astype(np.float32) for w in inp.norm_mlp]
+    dm = _dm(inp, gpu)
+    tx, tdy = torch.from_numpy(x).to(gpu), torch.from_numpy(dy).to(gpu)
+    ty, tdx = torch.empty_like(tx), torch.empty_like(tx)
+    say("large magnitudes", case)
+    for layer in (0, 1):
+        dm.layer_forward(layer, tx, ty)
+        dm.layer_backward(layer, tx, tdy, tdx)
+        torch.cuda.synchronize()
+        P = O.decompress_layer(cfg, inp, layer)
+        y_ref = O.layer_forward(cfg, layer, P, x)
+        dx_ref, grads = O.layer_backward(cfg, layer, P, x, dy)
+        errs = {"y": rel_l2(to_np(ty), y_ref), "dx": rel_l2(to_np(tdx), dx_ref)}
+        for p, (dA, dB) in grads.items():
+            errs["dA_" + p] = rel_l2(to_np(dm.dA[layer][p]), dA)
+            errs["dB_" + p] = rel_l2(to_np(dm.dB[layer][p]), dB)
+        rows = {"y": max_row_rel_l2(to_np(ty), y_ref), "dx": max_row_rel_l2(to_np(tdx), dx_ref)}
+        say("layer", layer, "rel-L2", {k: f"{v:.2e}" for k, v in errs.items()},
+            "max row", {k: f"{v:.2e}" for k, v in rows.items()})
+        for k, e in errs.items():
+            assert e <= TOL, (case, layer, k, e)
+        for k, e in rows.items():
+            assert e <= ROW_TOL, (case, layer, k, "row", e)
 
 
 # Attention head dims 128 and 256, multi-head (one query head per KV head) and grouped-query,
@@ -228,11 +272,54 @@ def test_lm_head_parity(built_lib, gpu):
     torch.cuda.synchronize()
     E = O.decompress_embedding(cfg, inp)
     loss, dx = O.lm_head_ce(cfg, E, inp.norm_final, xL, inp.ids)
-    say("loss", dm.loss.item(), loss, "dx rel-L2", rel_l2(to_np(tdx), dx))
+    row = max_row_rel_l2(to_np(tdx), dx)
+    say("loss", dm.loss.item(), loss, "dx rel-L2", rel_l2(to_np(tdx), dx), "max row", row)
     assert abs(dm.loss.item() - loss) <= 1e-3 * abs(loss)
     assert rel_l2(to_np(tdx), dx) <= TOL
+    assert row <= ROW_TOL
     # rows without a target (last position of each sequence) get exactly zero gradient
     assert torch.count_nonzero(tdx.view(cfg.batch, cfg.seq, -1)[:, -1]).item() == 0
+
+
+# Logits far from the random-init regime. "wide": final-norm weight 45, so the logits have a
+# standard deviation near 10 and row maxima near 35. "peaked": half of the rows are the
+# decompressed embedding row of their own target (plus noise) and the final-norm weight is
+# 4.75, which gives the target a probability near 0.99; the gradient of such a row is the
+# small difference (P - onehot) E, where cancellation shows any rounding of the target term.
+@pytest.mark.parametrize("case", ["wide", "peaked"])
+def test_lm_head_parity_large_and_peaked_logits(built_lib, gpu, case):
+    cfg = MINI
+    inp = make_inputs(cfg, seed=33, norm="random")
+    rng = np.random.default_rng(34)
+    N, T = cfg.n_tokens, cfg.seq
+    xL = rng.standard_normal((N, cfg.hidden)).astype(np.float32)
+    E = O.decompress_embedding(cfg, inp)
+    tgt = np.full(N, -1)
+    tgt.reshape(cfg.batch, T)[:, :-1] = inp.ids[:, 1:]
+    if case == "wide":
+        inp.norm_final = np.full(cfg.hidden, 45.0, np.float32)
+    else:
+        inp.norm_final = np.full(cfg.hidden, 4.75, np.float32)
+        rows = np.nonzero((tgt >= 0) & (np.arange(N) % 2 == 0))[0]
+        xL[rows] = (E[tgt[rows]] * 50.0 + 0.05 * rng.standard_normal((rows.size, cfg.hidden))).astype(np.float32)
+    dm = _dm(inp, gpu)
+    tx = torch.from_numpy(xL).to(gpu)
+    tdx = torch.empty_like(tx)
+    say("lm head", case)
+    dm.lm_head(tx, tdx)
+    torch.cuda.synchronize()
+    loss, dx = O.lm_head_ce(cfg, E, inp.norm_final, xL, inp.ids)
+    if case == "peaked":
+        z = O.lm_head_logits(cfg, E, inp.norm_final, xL[rows])
+        p = np.exp(z - z.max(1, keepdims=True))
+        pt = (p / p.sum(1, keepdims=True))[np.arange(rows.size), tgt[rows]]
+        say("target probability of the peaked rows: median", float(np.median(pt)), "min", float(pt.min()))
+        assert np.median(pt) > 0.95
+    err, row = rel_l2(to_np(tdx), dx), max_row_rel_l2(to_np(tdx), dx)
+    say("loss", dm.loss.item(), loss, "dx rel-L2", f"{err:.2e}", "max row", f"{row:.2e}")
+    assert abs(dm.loss.item() - loss) <= 1e-3 * abs(loss)
+    assert err <= TOL
+    assert row <= ROW_TOL
 
 
 def _step_parity(cfg, inp, gpu, ref=None):
