@@ -231,6 +231,26 @@ int mebp_train_step_offload(const mebp_config* cfg, const mebp_q4* emb, const me
                             const mebp_layer_lora_grad* grads, float* dx0, void* ws, size_t ws_bytes,
                             mebp_stream_t stream);
 
+/* ---------------- entry point for callers that cannot allocate ----------------------
+ * For callers that can neither allocate device memory nor hand over a workspace: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * mebp_layer_recompute_backward with its scratch in a buffer of MEBP_STATIC_SCRATCH_BYTES
+ * that the library holds on every device it runs on (reserved with the library's code on
+ * that device and kept until the process ends) instead of a caller workspace: same kernels,
+ * same order, same results. The call allocates nothing; arguments as
+ * mebp_layer_recompute_backward without ws / ws_bytes. The layer must fit:
+ * mebp_workspace_bytes() of the same config with vocab = 0 must not exceed
+ * MEBP_STATIC_SCRATCH_BYTES (a Qwen2.5-0.5B-shaped layer at 256 tokens does), else the
+ * call returns MEBP_EWORKSPACE and enqueues nothing. Every call on a device shares that
+ * device's buffer and leaves its contents behind (no result depends on them): calls that
+ * overlap on one device, from two streams or two host threads, race and must be
+ * serialised by the caller.                                                            */
+#define MEBP_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int mebp_layer_recompute_backward_static(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
+                                         const mebp_layer_lora* lora, const float* x_ckpt, const float* dy,
+                                         float* dx, const mebp_layer_lora_grad* grads, int32_t B, int32_t T,
+                                         mebp_stream_t stream);
+
 /* Message for the last non-zero status returned on the calling thread ("" if none). */
 const char* mebp_last_error(void);
 

@@ -21,9 +21,10 @@ EXPORTED = (
     "mebp_lm_head_ce_backward", "mebp_embed", "mebp_train_step", "mebp_last_error",
     "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name", "mebp_kernel_timing",
     "mebp_kernel_timing_report", "mebp_kernel_repeat", "mebp_lora_grad_accumulate", "mebp_lora_adamw_step",
-    "mebp_train_step_offload", "mebp_test_gemm",
+    "mebp_train_step_offload", "mebp_test_gemm", "mebp_layer_recompute_backward_static",
 )
 
+STATIC_SCRATCH_BYTES = 64 << 20  # MEBP_STATIC_SCRATCH_BYTES
 
 # mebp_test_gemm kinds
 TEST_GEMM_NT, TEST_GEMM_NT_BIG128, TEST_GEMM_NT_BIG256, TEST_GEMM_NT_LDS, TEST_GEMM_TN, TEST_GEMM_TN_BIG = range(6)
@@ -92,6 +93,9 @@ def lib() -> C.CDLL:
             "mebp_layer_recompute_backward": (C.c_int, [cfgp, I32, C.POINTER(MebpLayerBase),
                                                         C.POINTER(MebpLayerLora), P, P, P,
                                                         C.POINTER(MebpLayerLoraGrad), I32, I32, P, SZ, P]),
+            "mebp_layer_recompute_backward_static": (C.c_int, [cfgp, I32, C.POINTER(MebpLayerBase),
+                                                               C.POINTER(MebpLayerLora), P, P, P,
+                                                               C.POINTER(MebpLayerLoraGrad), I32, I32, P]),
             "mebp_lm_head_ce_backward": (C.c_int, [cfgp, C.POINTER(MebpQ4), P, P, P, I32, I32, P, P, P, SZ, P]),
             "mebp_embed": (C.c_int, [cfgp, C.POINTER(MebpQ4), P, I32, I32, P, P]),
             "mebp_train_step": (C.c_int, [cfgp, C.POINTER(MebpQ4), C.POINTER(MebpLayerBase), P,
@@ -159,6 +163,13 @@ def mebp_layer_recompute_backward(cfg, layer, base, lora, x_ckpt, dy, dx, grads,
                                   check=True):
     r = lib().mebp_layer_recompute_backward(C.byref(cfg), layer, _ref(base), _ref(lora), x_ckpt, dy, dx,
                                             _ref(grads), B, T, ws, ws_bytes, stream)
+    return _check(r) if check else r
+
+
+def mebp_layer_recompute_backward_static(cfg, layer, base, lora, x_ckpt, dy, dx, grads, B, T, stream=0,
+                                         check=True):
+    r = lib().mebp_layer_recompute_backward_static(C.byref(cfg), layer, _ref(base), _ref(lora), x_ckpt, dy, dx,
+                                                   _ref(grads), B, T, stream)
     return _check(r) if check else r
 
 

@@ -19,6 +19,11 @@
 
 using namespace mebp;
 
+// Scratch of mebp_layer_recompute_backward_static: one copy per device, reserved with the
+// library's code object. In host code this name is only a handle for the runtime's symbol
+// lookup, never an address (see static_scratch()).
+static __device__ __attribute__((aligned(256))) uint8_t scratch[MEBP_STATIC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -1100,6 +1105,61 @@ int mebp_layer_recompute_backward(const mebp_config* cfg, int32_t layer, const m
   if (dx && !aligned(dx, 16)) return fail(MEBP_EINVAL, "dx not 16-byte aligned");
   if (dx && dx == x_ckpt) return fail(MEBP_EINVAL, "dx must not alias x_ckpt");
   Ctx x = make_ctx(cfg, B, T, ws, stream);
+  float* rope;
+  if ((e = rope_table(x, layer, &rope))) return e;
+  return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
+}
+
+}  // extern "C"
+
+namespace {
+// Device address of the current device's copy of `scratch`, looked up once per device (with
+// that device current) and kept; null on failure (the message is recorded).
+void* static_scratch() {
+  static std::mutex mu;
+  static std::map<int, void*> by_dev;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    fail(MEBP_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> g(mu);
+  auto it = by_dev.find(dev);
+  if (it != by_dev.end()) return it->second;
+  void* p = nullptr;
+  e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || !p) {
+    fail(MEBP_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    return nullptr;
+  }
+  by_dev[dev] = p;
+  return p;
+}
+}  // namespace
+
+extern "C" {
+
+int mebp_layer_recompute_backward_static(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
+                                         const mebp_layer_lora* lora, const float* x_ckpt, const float* dy, float* dx,
+                                         const mebp_layer_lora_grad* grads, int32_t B, int32_t T,
+                                         mebp_stream_t stream) {
+  int e;
+  if ((e = check_config(cfg)) || (e = check_shape(B, T)) || (e = check_layer(cfg, layer, base, lora)) ||
+      (e = check_act(x_ckpt, "x_ckpt")) || (e = check_act(dy, "dy")) || (e = check_grads(cfg, grads)))
+    return e;
+  if (dx && !aligned(dx, 16)) return fail(MEBP_EINVAL, "dx not 16-byte aligned");
+  if (dx && dx == x_ckpt) return fail(MEBP_EINVAL, "dx must not alias x_ckpt");
+  // the layer's own slots only: the LM head's are not part of this call
+  mebp_config c0 = *cfg;
+  c0.vocab = 0;
+  const size_t need = mebp_workspace_bytes(&c0, B, T);
+  if (need > MEBP_STATIC_SCRATCH_BYTES)
+    return fail(MEBP_EWORKSPACE, "layer needs %zu bytes of scratch, more than the %zu the library holds", need,
+                (size_t)MEBP_STATIC_SCRATCH_BYTES);
+  void* ws = static_scratch();
+  if (!ws) return MEBP_EHIP;
+  Ctx x = make_ctx(&c0, B, T, ws, stream);
   float* rope;
   if ((e = rope_table(x, layer, &rope))) return e;
   return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);

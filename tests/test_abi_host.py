@@ -184,7 +184,7 @@ def test_grad_accumulate_rejects(built_lib):
     assert C.sizeof(L.MebpLayerLoraState) == 14 * 8
 
 
-def test_test_gemm_validates_first(built_lib):
+def test_test_gemm_and_static_entry_validate_first(built_lib):
     w = L.MebpQ4(q4=0x1000, scale=0x2000)
     X, OUT = 0x400000, 0x800000
     g = lambda **kw: L.mebp_test_gemm(kw.get("kind", L.TEST_GEMM_NT), kw.get("w", w), kw.get("n_out", 64),
@@ -194,6 +194,22 @@ def test_test_gemm_validates_first(built_lib):
     assert g(n_in=40) == L.MEBP_EUNSUPPORTED and g(n_out=8) == L.MEBP_EUNSUPPORTED
     assert g(M=0) == L.MEBP_EINVAL and g(M=70000) == L.MEBP_EUNSUPPORTED
     assert g(x=X + 8) == L.MEBP_EINVAL and g(out=0) == L.MEBP_EINVAL and g(w=None) == L.MEBP_EINVAL
+    # the static-scratch layer backward refuses a layer larger than the library's buffer
+    # (a Gemma3-1B-shaped layer at 512 tokens) before any device work
+    cfg = CONFIGS["gemma3-1b"].with_(vocab=0)
+    c = make_config(cfg)
+    base, lora = _fake_layer()
+    grads = L.MebpLayerLoraGrad()
+    for i in range(7):
+        grads.dA[i], grads.dB[i] = 0x1000000 + 0x1000 * i, 0x2000000 + 0x1000 * i
+    need = L.mebp_workspace_bytes(c, 1, 512)
+    assert need > L.STATIC_SCRATCH_BYTES
+    r = L.mebp_layer_recompute_backward_static(c, 0, base, lora, X, OUT, 0, grads, 1, 512, 0, check=False)
+    assert r == L.MEBP_EWORKSPACE and "scratch" in L.mebp_last_error()
+    # ... and accepts the workspace sizes of the single block and a Qwen2.5-0.5B-shaped layer
+    for name in ("block", "qwen2.5-0.5b"):
+        cf = CONFIGS[name].with_(vocab=0)
+        assert L.mebp_workspace_bytes(make_config(cf), cf.batch, cf.seq) <= L.STATIC_SCRATCH_BYTES, name
 
 
 IN_PLACE = ["gemm_tn_act_bwd", "splitk_finalize_actbwd", "rope_fwd", "qkv_post", "headnorm_bwd", "ce_chunk_stats",
