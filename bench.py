@@ -6,6 +6,11 @@ reverse: recompute from its checkpoint, backpropagate into the LoRA A/B gradient
 layer-input gradient. Inputs are synthetic, seeded, resident in device memory before the
 timed region. Prints one JSON line.
 
+The default workload is the largest single-GPU shape: Gemma3-4B-shaped (34 layers, hidden
+2560, 8 x 256 heads / 4 KV, GeGLU 10240, vocab 262144, batch 8 x 2048 tokens, LoRA r16 on
+all seven projections). The Qwen2.5-0.5B-shaped step is measured too and reported as an
+extra field.
+
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 """
 import argparse
@@ -435,7 +440,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="qwen2.5-0.5b")
+    ap.add_argument("--workload", default="gemma3-4b")
+    ap.add_argument("--extra-workload", default="qwen2.5-0.5b",
+                    help="a second workload timed after the first and reported as an extra field ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=3, help="extra steps with per-kernel event timing")
     ap.add_argument("--graph", type=int, default=1, help="replay the step as one captured HIP graph (1) or launch eagerly (0)")
@@ -495,9 +502,65 @@ def main():
     if args.experiments:
         experiments(cfg)
         return
+    res = measure(cfg, args, profile=True)
+    extra = None
+    if args.extra_workload and args.extra_workload != cfg.name:
+        ecfg = CONFIGS[args.extra_workload]
+        e = measure(ecfg, argparse.Namespace(**{**vars(args), "steps": 20, "warmup": 3}), profile=False)
+        extra = {"workload": f"{ecfg.name}-shaped full LoRA step", "global_batch": ecfg.batch, "seq_len": ecfg.seq,
+                 "ms_per_step": e["ms"], "tokens_per_s": round(e["value"], 1), "step_mfma_frac": e["step_frac"],
+                 "launch": e["launch"]}
+    # the optimizer step that follows a training step (AdamW over every LoRA tensor), at this
+    # workload's adapters and at the largest adapter set (Gemma3-4B shape, all 7 projections)
+    optim = {"bound": "hbm", "workload": optimizer_bench(cfg), "largest": optimizer_bench(CONFIGS["gemma3-4b"])}
+    log(f"adamw: {optim['workload']['us_per_update']} us per update of {optim['workload']['params']} params; "
+        f"{optim['largest']['params']} params: {optim['largest']['us_per_update']} us, {optim['largest']['achieved']} GB/s")
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, res["inp"], res["loss"])
+    out = {
+        "metric": "LoRA train tokens/s per checkpointed step",
+        "value": round(res["value"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(res["ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16/bf16 MFMA, fp32 accumulate",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shaped full LoRA step", "layers": cfg.n_layers, "hidden": cfg.hidden,
+                   "heads": f"{cfg.n_heads}x{cfg.head_dim}/{cfg.n_kv_heads}kv", "ffn": cfg.ffn, "vocab": cfg.vocab,
+                   "global_batch": cfg.batch, "seq_len": cfg.seq, "lora": f"r{cfg.lora_rank} a{cfg.lora_alpha:g} "
+                   + ",".join(cfg.lora_modules), "weights": "int4 group-32, fp16 scales", "parallelism": "none"},
+        "step_mfma_frac": res["step_frac"],
+        "launch": res["launch"],
+        "loss": res["loss"],
+        "roofline": res["roofline"],
+        "cpu_baseline": cpu,
+        "memory": res["memory"],
+        "extra_workload": extra,
+        "optimizer_adamw": optim,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def measure(cfg, args, profile=True):
+    """Time `args.steps` whole steps of `cfg` (HIP-graph replay unless --graph 0) after
+    `args.warmup` eager ones; with `profile`, also the per-kernel event pass, the in-stream
+    duration of the leading kernels and the roofline of the dominant one, and the device
+    memory the step holds."""
+    import torch
+    from mebp_inputs import make_inputs
+    from paper_2510_03425_amd import _lib as L
+    from paper_2510_03425_amd.device import DeviceModel
+
     t0 = time.time()
     inp = make_inputs(cfg, seed=0)
     log(f"inputs {cfg.name} drawn in {time.time() - t0:.1f}s")
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
     dm = DeviceModel(inp, device="cuda:0")
     dx0 = None
     stream = torch.cuda.current_stream()
@@ -506,6 +569,7 @@ def main():
         dm.train_step(dx0)
     torch.cuda.synchronize()
     log("warmup done")
+
     def capture():
         # one whole step (every kernel of the library, no allocation, no host sync) captured
         # on a side stream; the eager steps before it already validated the inputs
@@ -527,16 +591,6 @@ def main():
         run_step = graph.replay
         log("captured the step as a HIP graph")
 
-    def time_steps(fn, n):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(n):
-            fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n
-
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
@@ -549,8 +603,28 @@ def main():
     ms = ev0.elapsed_time(ev1) / args.steps
     tokens = cfg.n_tokens
     value = tokens / (ms / 1e3)
-    log(f"{ms:.3f} ms/step, {value:.0f} tokens/s (wall {wall / args.steps * 1e3:.3f} ms/step)")
+    log(f"{cfg.name}: {ms:.3f} ms/step, {value:.0f} tokens/s (wall {wall / args.steps * 1e3:.3f} ms/step)")
     loss = dm.loss.item()
+    step_flops = algorithmic_flops(cfg)
+    res = {"ms": ms, "value": value, "loss": loss, "inp": inp, "launch": "hip_graph" if graph is not None else "eager",
+           "step_frac": round(step_flops / (ms / 1e3) / 1e12 / PEAK_TFLOPS_16BIT, 4), "roofline": None,
+           "memory": None}
+    if not profile:
+        del graph, dm
+        torch.cuda.synchronize()
+        return res
+
+    # device memory held by the step: every device buffer comes from torch's allocator (the
+    # library allocates nothing), so its peak is the step's footprint
+    ckpt_bytes = (cfg.n_layers + 1) * cfg.n_tokens * cfg.hidden * 4
+    free, total = torch.cuda.mem_get_info()
+    res["memory"] = {"peak_device_bytes": int(torch.cuda.max_memory_allocated()),
+                     "workspace_bytes": int(dm.ws_bytes), "checkpoint_bytes": ckpt_bytes,
+                     "weights_lora_grads_bytes": int(sum(t.numel() * t.element_size() for t in dm.keep)
+                                                     + sum(t.numel() * 4 for d in dm.dA + dm.dB for t in d.values())),
+                     "device_used_bytes": int(total - free), "device_total_bytes": int(total)}
+    log(f"memory: peak allocated {res['memory']['peak_device_bytes'] / 2**30:.2f} GiB (workspace "
+        f"{dm.ws_bytes / 2**30:.2f} GiB, checkpoints {ckpt_bytes / 2**30:.2f} GiB)")
 
     # profile pass: a few extra eager steps with HIP events around every launch, recorded on
     # the stream the library launches on (the step's stream)
@@ -564,7 +638,7 @@ def main():
         L.mebp_kernel_timing(False)
         total_k = sum(r["ms"] for r in rep)
         rep.sort(key=lambda r: -r["ms"])
-        for r in rep[:16]:
+        for r in rep[:20]:
             log(f"  {r['kernel']:24s} {r['ms'] / args.profile_steps:8.3f} ms/step  {r['launches'] // args.profile_steps:4d}"
                 f" launches  {r['flops'] / r['ms'] / 1e9 if r['ms'] else 0:8.1f} TFLOP/s"
                 f"  {r['bytes'] / r['ms'] / 1e6 if r['ms'] else 0:8.1f} GB/s")
@@ -625,24 +699,55 @@ def main():
                      "kernel_share_of_step": round(per_launch_ms * per_step / ms, 3)})
         if gemm:
             roof["all_gemms_frac"] = round(gf / gms / 1e9 / PEAK_TFLOPS_16BIT, 4)
-    step_flops = algorithmic_flops(cfg)
+    res["roofline"] = roof
+    del graph, dm
+    torch.cuda.synchronize()
+    return res
 
-    # the optimizer step that follows a training step (AdamW over every LoRA tensor), at this
-    # workload's adapters and at the largest adapter set (Gemma3-4B shape, all 7 projections)
-    from mebp_inputs import CONFIGS
-    optim = {"bound": "hbm", "workload": optimizer_bench(cfg), "largest": optimizer_bench(CONFIGS["gemma3-4b"])}
-    log(f"adamw: {optim['workload']['us_per_update']} us per update of {optim['workload']['params']} params; "
-        f"{optim['largest']['params']} params: {optim['largest']['us_per_update']} us, {optim['largest']['achieved']} GB/s")
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        import oracle as O
-        try:
-            from threadpoolctl import threadpool_info
-            cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-        except Exception:
-            cores = os.cpu_count()
-        # whole fp64 steps of the same workload until about 10 s of CPU work (at most 3)
+def host_info():
+    """CPU model, BLAS and thread count of the host the oracle runs on."""
+    import numpy as np
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = "unknown"
+    try:
+        deps = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{deps.get('name')} {deps.get('version', '')}".strip()
+    except Exception:
+        pass
+    threads = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        threads = max((i.get("num_threads", 1) for i in info), default=threads)
+        blas = ", ".join(sorted({f"{i.get('internal_api')} {i.get('version')}" for i in info if i.get("user_api") == "blas"})) or blas
+    except Exception:
+        pass
+    return {"cores": threads, "cpu": model, "blas": blas, "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def cpu_baseline(cfg, inp, gpu_loss):
+    """The fp64 oracle timed on this host's cores, as a baseline (not a target).
+
+    Whole steps for shapes the oracle finishes in seconds. For the large shapes one step
+    would take hours, so a bounded sample is timed and extrapolated linearly: one layer
+    (forward of the first loop, then recompute + backward of the second) on one whole
+    sequence of the batch (every row, every column; the oracle's attention costs the same
+    for local and global layers), scaled by layers x sequences, plus the LM head on a sample
+    of rows (loss and gradient rows are independent of each other), scaled by rows."""
+    import numpy as np
+    import oracle as O
+    hi = host_info()
+    N, L = cfg.n_tokens, cfg.n_layers
+    if algorithmic_flops(cfg) <= 1e12:  # whole steps take seconds
         n_steps, t0 = 0, time.perf_counter()
         while True:
             ref = O.train_step(cfg, inp, keep_ckpts=False)
@@ -650,36 +755,32 @@ def main():
             dt = time.perf_counter() - t0
             if dt > 10.0 or n_steps >= 3:
                 break
-        cpu = {"value": round(n_steps * tokens / dt, 3), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-               "sample": f"{n_steps} full fp64 step(s) of the same workload ({tokens} tokens each) in {dt:.1f} s",
-               "loss_oracle": ref.loss}
-        log(f"oracle {n_steps} step(s) {dt:.1f}s on {cores} threads; loss gpu {loss:.6f} oracle {ref.loss:.6f}")
-
-    out = {
-        "metric": "LoRA train tokens/s per checkpointed step",
-        "value": round(value, 1),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f16/bf16 MFMA, fp32 accumulate",
-        "data": "synthetic",
-        "config": {"workload": f"{cfg.name}-shaped full LoRA step", "layers": cfg.n_layers, "hidden": cfg.hidden,
-                   "heads": f"{cfg.n_heads}x{cfg.head_dim}/{cfg.n_kv_heads}kv", "ffn": cfg.ffn, "vocab": cfg.vocab,
-                   "global_batch": cfg.batch, "seq_len": cfg.seq, "lora": f"r{cfg.lora_rank} a{cfg.lora_alpha:g} "
-                   + ",".join(cfg.lora_modules), "weights": "int4 group-32, fp16 scales", "parallelism": "none"},
-        "step_mfma_frac": round(step_flops / (ms / 1e3) / 1e12 / PEAK_TFLOPS_16BIT, 4),
-        "launch": "hip_graph" if graph is not None else "eager",
-        "loss": loss,
-        "roofline": roof,
-        "cpu_baseline": cpu,
-        "optimizer_adamw": optim,
-    }
-    print(json.dumps(out), flush=True)
+        log(f"oracle {n_steps} step(s) {dt:.1f}s on {hi['cores']} threads; loss gpu {gpu_loss:.6f} oracle {ref.loss:.6f}")
+        return {"value": round(n_steps * N / dt, 3), "unit": "tokens/s", "kind": "oracle", **hi,
+                "sample": f"{n_steps} full fp64 step(s) of the same workload ({N} tokens each) in {dt:.1f} s",
+                "loss_oracle": ref.loss}
+    one = cfg.with_(batch=1)
+    T, d = cfg.seq, cfg.hidden
+    E = O.decompress_embedding(cfg, inp)
+    x = O.embed(E, inp.ids[:1], O.embed_scale(cfg))
+    dy = np.random.default_rng(5).standard_normal(x.shape)
+    t0 = time.perf_counter()
+    P = O.decompress_layer(one, inp, 0)
+    O.layer_forward(one, 0, P, x)
+    O.layer_backward(one, 0, P, x, dy)
+    t_layer = time.perf_counter() - t0
+    rows = np.arange(min(128, T - 1))
+    tgt = inp.ids[0, 1:][rows]
+    t0 = time.perf_counter()
+    O.lm_head_ce_rows(cfg, E, inp.norm_final, x[rows], tgt, cfg.batch * (T - 1))
+    t_rows = time.perf_counter() - t0
+    total = t_layer * L * cfg.batch + t_rows * N / len(rows)
+    log(f"oracle sample: one layer on one sequence {t_layer:.1f}s, LM head on {len(rows)} rows {t_rows:.1f}s "
+        f"-> {total:.0f}s per step extrapolated ({hi['cores']} threads)")
+    return {"value": round(N / total, 4), "unit": "tokens/s", "kind": "oracle", **hi, "extrapolated": True,
+            "sample": f"extrapolated: one layer (decompression, forward, recompute + backward) on one whole sequence "
+                      f"of {T} tokens in {t_layer:.1f} s, x {L} layers x {cfg.batch} sequences; LM head on {len(rows)} "
+                      f"rows in {t_rows:.1f} s, x {N} rows / {len(rows)}; {total:.0f} s per step"}
 
 
 if __name__ == "__main__":

@@ -566,8 +566,21 @@ DEV void wait_vmcnt() {
 // eight 16-byte chunks are stored at position chunk ^ (row & 7), so that the MFMA fragment
 // reads (32 rows, one chunk each) spread over all banks. The weights are loaded into
 // registers, also two tiles ahead, and decompressed by each wave for its own columns.
+//
+// W16: the weights are plain 16-bit values [N][K] (seg.q4 points at them, no scales) that
+// go straight into the MFMA B operand: the same kernel without the decompression, used
+// to measure what the decompression costs (W16 = false is the production kernel).
 constexpr int LDS_STAGES = 3, LDS_STAGE_BYTES = BM * BK * 2;
-template <int EPI>
+template <bool W16>
+struct LdsWeightRegs {  // int4 codes (one 16-byte load per 32 values) and raw fp16 scales
+  uint4 rb[LDS_STAGES][2];
+  uint32_t rsc[LDS_STAGES][2];
+};
+template <>
+struct LdsWeightRegs<true> {  // 16-bit weights: four 16-byte loads per 32 values
+  uint4 rw[LDS_STAGES][2][4];
+};
+template <int EPI, bool W16 = false>
 __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   constexpr int BN = 256, WNW = 4, NJ = 2;
   // one LDS object per ring stage, so that the compiler can tell the fragment reads of one
@@ -595,8 +608,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   const rsrc_t rA = make_rsrc((const u16*)a.X + (size_t)m0 * a.lda, (size_t)min(BM, a.M - m0) * a.lda * 2);
   const int wcol0 = n0 + wn * 32 * NJ;
   const int wrows = max(0, min(32 * NJ, Nn - wcol0));
-  const rsrc_t rB = make_rsrc(sg.q4 + (size_t)min(wcol0, Nn) * Kh, (size_t)wrows * Kh);
-  const rsrc_t rS = make_rsrc(sg.scale + (size_t)min(wcol0, Nn) * kgroups, (size_t)wrows * kgroups * 2);
+  const rsrc_t rB = W16 ? make_rsrc((const u16*)sg.q4 + (size_t)min(wcol0, Nn) * K, (size_t)wrows * K * 2)
+                       : make_rsrc(sg.q4 + (size_t)min(wcol0, Nn) * Kh, (size_t)wrows * Kh);
+  const rsrc_t rS = make_rsrc(W16 ? nullptr : sg.scale + (size_t)min(wcol0, Nn) * kgroups,
+                              W16 ? 0 : (size_t)wrows * kgroups * 2);
   // activation loads: instruction i of wave w fills tile rows 8 (w + 8 i) .. +8, lane l row
   // 8 (w + 8 i) + l / 8, LDS position l % 8, i.e. global chunk (l % 8) ^ (row & 7)
   uint32_t offA[4];
@@ -607,12 +622,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     chunkA[i] = (lane & 7) ^ (row & 7);
     offA[i] = (uint32_t)((row * a.lda + 8 * chunkA[i]) * 2);
   }
-  const uint32_t offB = (uint32_t)((lane & 31) * Kh + 16 * h), offS = (uint32_t)(((lane & 31) * kgroups + h) * 2);
+  const uint32_t offB = W16 ? (uint32_t)(((lane & 31) * K + 32 * h) * 2) : (uint32_t)((lane & 31) * Kh + 16 * h);
+  const uint32_t offS = (uint32_t)(((lane & 31) * kgroups + h) * 2);
   // fragment reads: row wm*128 + 32 i + (l % 32), chunk 4h + t at position (4h + t) ^ (l & 7)
   const uint32_t rowA = (uint32_t)((wm * 128 + (lane & 31)) * 128);
 
-  uint4 rb[LDS_STAGES][NJ];
-  uint32_t rsc[LDS_STAGES][NJ];
+  LdsWeightRegs<W16> wr;
   f32x16 acc[4][NJ];
   zero_acc(acc);
   const bool tail = (K % BK) != 0;
@@ -627,20 +642,35 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
       const uint32_t off = (!tail || k0 + 8 * chunkA[i] < K) ? offA[i] + 2 * k0 : 0x80000000u;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, dst + 1024 * (wave + 8 * i), 16, off, 0, 0, 0);
     }
+    if constexpr (W16) {
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      rb[st][j] = bload128(rB, offB + (uint32_t)(32 * j * Kh) + (k0 >> 1));
-      rsc[st][j] = bload16(rS, offS + (uint32_t)(32 * j * kgroups * 2) + 2 * (k0 >> 5));
-    }
-    if (tail && k0 + BK > K) {
-      const int kb = k0 + 32 * h;
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) wr.rw[st][j][t] = bload128(rB, offB + (uint32_t)((32 * j * K + k0 + 8 * t) * 2));
+      if (tail && k0 + BK > K) {
+        const int kb = k0 + 32 * h;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            if (kb + 8 * t >= K) wr.rw[st][j][t] = make_uint4(0, 0, 0, 0);
+      }
+    } else {
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
-        if (kb >= K) rsc[st][j] = 0u;
-        if (kb + 0 >= K) rb[st][j].x = 0u;
-        if (kb + 8 >= K) rb[st][j].y = 0u;
-        if (kb + 16 >= K) rb[st][j].z = 0u;
-        if (kb + 24 >= K) rb[st][j].w = 0u;
+        wr.rb[st][j] = bload128(rB, offB + (uint32_t)(32 * j * Kh) + (k0 >> 1));
+        wr.rsc[st][j] = bload16(rS, offS + (uint32_t)(32 * j * kgroups * 2) + 2 * (k0 >> 5));
+      }
+      if (tail && k0 + BK > K) {
+        const int kb = k0 + 32 * h;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          if (kb >= K) wr.rsc[st][j] = 0u;
+          if (kb + 0 >= K) wr.rb[st][j].x = 0u;
+          if (kb + 8 >= K) wr.rb[st][j].y = 0u;
+          if (kb + 16 >= K) wr.rb[st][j].z = 0u;
+          if (kb + 24 >= K) wr.rb[st][j].w = 0u;
+        }
       }
     }
   };
@@ -648,10 +678,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     constexpr int st = decltype(S_)::value;
     const uint8_t* As = stage_ptr(S_) + rowA;
     f16x2 sc[NJ];
+    if constexpr (!W16) {
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)rsc[st][j]);
-      sc[j] = f16x2{v, v};
+      for (int j = 0; j < NJ; ++j) {
+        const _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)wr.rsc[st][j]);
+        sc[j] = f16x2{v, v};
+      }
     }
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -661,8 +693,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
       for (int i = 0; i < 4; ++i) af[i] = *(const uint4*)(As + 4096 * i + pos);
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
-        const uint32_t w = t == 0 ? rb[st][j].x : t == 1 ? rb[st][j].y : t == 2 ? rb[st][j].z : rb[st][j].w;
-        bfr[j] = dequant8_natural(w, sc[j]);
+        if constexpr (W16) {
+          bfr[j] = wr.rw[st][j][t];
+        } else {
+          const uint32_t w = t == 0 ? wr.rb[st][j].x : t == 1 ? wr.rb[st][j].y : t == 2 ? wr.rb[st][j].z : wr.rb[st][j].w;
+          bfr[j] = dequant8_natural(w, sc[j]);
+        }
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -674,18 +710,20 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   // tile k-1, before the previous barrier), the MFMAs of tile k, then wait until this
   // thread's activation loads of tile k+1 have landed (the loads issued after them: the
   // weights of k+1 and all of k+2, 2 NJ + 4 + 2 NJ) and meet the other waves at the barrier.
+  // vector-memory instructions of one gload: 4 activation loads plus the weight loads
+  constexpr int VMI = 4 + (W16 ? 4 * NJ : 2 * NJ);
   auto step = [&](auto I_, int k) {
     constexpr int I = decltype(I_)::value;
     gload(IC<(I + 2) % LDS_STAGES>{}, min(k + 2, kt_end - 1));
     mma(IC<I>{});
-    wait_vmcnt<4 * NJ + 4>();
+    wait_vmcnt<VMI + (W16 ? 4 * NJ : 2 * NJ)>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");  // no LDS access moves across the barrier
   };
   if (kt_begin < kt_end) {
     gload(IC<0>{}, kt_begin);
     gload(IC<1>{}, min(kt_begin + 1, kt_end - 1));
-    wait_vmcnt<4 * NJ + 4>();  // tile kt_begin's activations (weights and tile +1 may fly)
+    wait_vmcnt<VMI + (W16 ? 4 * NJ : 2 * NJ)>();  // tile kt_begin's activations (weights and tile +1 may fly)
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     int k = kt_begin;
@@ -1114,6 +1152,9 @@ hipError_t launch_gemm_probe_big(int kind, const uint8_t* q4, const uint16_t* sc
       break;
     case 3:  // LDS-direct forward, 256 x 256 tiles
       hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0, st, a);
+      break;
+    case 6:  // the LDS-direct forward kernel on plain fp16 weights [n_out][n_in] (seg.q4)
+      hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32, true>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0, st, a);
       break;
     case 5: {  // transposed, 256 x 128 tiles
       TnArgs t{};
