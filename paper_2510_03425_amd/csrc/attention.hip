@@ -1031,6 +1031,218 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
     }
 }
 
+
+// dK, dV at head dim 256 with 32-key wave pairs (v_mfma_f32_32x32x16). The 32-key kernel
+// above would need K, V (128 registers) and dK^T, dV^T (256 accumulators) in every wave;
+// here the two waves of a pair share those 32 keys: the first keeps K and accumulates
+// dV^T, the second keeps V and accumulates dK^T. Per query tile (32 queries, staged as in
+// k_attn_bwd_kv32): the first wave computes S = Q K^T and P = exp(S - lse), hands P to its
+// partner through LDS (fp32, one 16-value slot per lane: the partner's dP tile has the same
+// lane layout) and adds dO^T P into dV^T; the second computes dP = dO V^T, then dS = P (dP -
+// delta) and adds Q^T dS into dK^T. Each wave thus holds 64 operand registers and 128
+// accumulators, and every Q / dO fragment read from LDS feeds a 32-key MFMA.
+template <int NP>
+__global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, float* part) {
+  constexpr int DH = 256, NTH = 128 * NP, QB = 32, LDN = DH + 8, LDT = QB + 8;
+  constexpr int NKS = DH / 16, NTO = DH / 32;
+  constexpr int NBT = (QB / 8) * (DH / 8);   // 8x8 blocks per tensor (Q, dO) and tile
+  constexpr int BPT = (2 * NBT + NTH - 1) / NTH;
+  __shared__ __attribute__((aligned(16))) u16 Qs[QB * LDN];   // fp16 [q][e]
+  __shared__ __attribute__((aligned(16))) u16 dOs[QB * LDN];  // bf16 [q][e]
+  __shared__ __attribute__((aligned(16))) u16 Qt[DH * LDT];   // bf16 [e][q]
+  __shared__ __attribute__((aligned(16))) u16 dOt[DH * LDT];  // bf16 [e][q]
+  __shared__ __attribute__((aligned(16))) float Ps[NP][16][64];  // P of each pair, [r][lane]
+  __shared__ __attribute__((aligned(16))) float lse_s[QB], del_s[QB];
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), hl = lane >> 5;
+  const int pair = w >> 1, role = w & 1;  // role 0: K, P, dV; role 1: V, dP, dS, dK
+  const TileId id = attn_tile(0);
+  const int T = a.T, h = id.y, b = id.z, grp = a.Hq / a.Hkv, kvh = h / grp, hh = h % grp;
+  const int k0 = id.x * (32 * NP), kw = k0 + 32 * pair, key = kw + (lane & 31);
+  const VisRange qvis = queries_of_key(key, T, a.window);
+  const float sc = LOG2E / sqrtf((float)DH);
+  const size_t rowb = (size_t)b * T;
+
+  uint4 kv[NKS];  // K (fp16) or V (bf16) of the pair's keys
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const size_t off = (rowb + key) * a.ldk + kvh * DH + 16 * ks + 8 * hl;
+    const uint4 x = load_frag_global((role == 0 ? a.k : a.v) + off, key < T);
+    kv[ks] = role == 0 ? x : f16x8_to_bf16x8(x);
+  }
+  f32x16 acc[NTO];  // dV^T (role 0) or dK^T (role 1)
+#pragma unroll
+  for (int t = 0; t < NTO; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
+
+  const int q_lo = k0 & ~(QB - 1);
+  const int q_hi = a.window ? min(T, k0 + 32 * NP - 1 + a.window) : T;
+
+  uint4 br[BPT][8];
+  float st_lse = 0.f, st_del = 0.f;
+  auto gload = [&](int qb0) {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int bl = tid + NTH * i, tens = bl / NBT, lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
+      const u16* src = tens == 0 ? (const u16*)a.q : (const u16*)a.dO;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int qq = qb0 + rb * 8 + j;
+        br[i][j] = load_frag_global(src + (rowb + qq) * a.ldq + h * DH + cb * 8, bl < 2 * NBT && qq < T);
+      }
+    }
+    if (tid < QB) {
+      const int qq = qb0 + tid;
+      const size_t si = ((size_t)b * a.Hq + h) * T + qq;
+      st_lse = qq < T ? a.lse[si] * LOG2E : 0.f;
+      st_del = qq < T ? a.delta[si] : 0.f;
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int bl = tid + NTH * i, tens = bl / NBT, lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
+      if (bl >= 2 * NBT) continue;
+      u16* nrm = tens == 0 ? Qs : dOs;
+      u16* trn = tens == 0 ? Qt : dOt;
+      uint32_t in[8][4];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        *(uint4*)(nrm + (rb * 8 + j) * LDN + cb * 8) = br[i][j];
+        const uint4 v = tens == 0 ? f16x8_to_bf16x8(br[i][j]) : br[i][j];
+        in[j][0] = v.x; in[j][1] = v.y; in[j][2] = v.z; in[j][3] = v.w;
+      }
+#pragma unroll
+      for (int jc = 0; jc < 8; ++jc) {
+        const int d = jc >> 1;
+        uint4 o;
+        if (jc & 1) {
+          o = make_uint4(perm_hi16(in[0][d], in[1][d]), perm_hi16(in[2][d], in[3][d]), perm_hi16(in[4][d], in[5][d]),
+                         perm_hi16(in[6][d], in[7][d]));
+        } else {
+          o = make_uint4(perm_lo16(in[0][d], in[1][d]), perm_lo16(in[2][d], in[3][d]), perm_lo16(in[4][d], in[5][d]),
+                         perm_lo16(in[6][d], in[7][d]));
+        }
+        *(uint4*)(trn + (cb * 8 + jc) * LDT + rb * 8) = o;
+      }
+    }
+    if (tid < QB) {
+      lse_s[tid] = st_lse;
+      del_s[tid] = st_del;
+    }
+  };
+
+  if (q_lo < q_hi) gload(q_lo);
+  for (int qb0 = q_lo; qb0 < q_hi; qb0 += QB) {
+    __syncthreads();  // every wave is done with the previous tile (and its P slot)
+    sstore();
+    __syncthreads();
+    if (qb0 + QB < q_hi) gload(qb0 + QB);  // next tile in flight during this one
+    // nothing visible for this pair: all queries before its keys, or past its window (the
+    // barriers below are still met)
+    const bool act = !(qb0 + QB - 1 < kw || (a.window && qb0 > kw + 31 + a.window - 1));
+    f32x16 x;  // S then P (role 0), dP then dS (role 1)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x[r] = 0.f;
+    if (act) {
+      const u16* src = (role == 0 ? Qs : dOs) + (lane & 31) * LDN + 8 * hl;
+      if (role == 0) {
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) x = mfma32_f16(*(const uint4*)(src + 16 * ks), kv[ks], x);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const float4 l4 = *(const float4*)(lse_s + 8 * g + 4 * hl);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int r = 4 * g + rr;
+            const bool vis = visible(qvis, qb0 + 8 * g + 4 * hl + rr);
+            x[r] = vis ? exp2f(x[r] * sc - lv[rr]) : 0.f;
+            Ps[pair][r][lane] = x[r];
+          }
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) x = mfma32_bf16(*(const uint4*)(src + 16 * ks), kv[ks], x);
+      }
+    }
+    __syncthreads();  // P of every pair is in LDS
+    if (act) {
+      if (role == 1) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const float4 d4 = *(const float4*)(del_s + 8 * g + 4 * hl);
+          const float dl[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int r = 4 * g + rr;
+            x[r] = Ps[pair][r][lane] * (x[r] - dl[rr]);
+          }
+        }
+      }
+      const u16* opnd = role == 0 ? dOt : Qt;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int r0 = 8 * kk;
+        const uint4 f = make_uint4(pack_bf16x2(x[r0 + 0], x[r0 + 1]), pack_bf16x2(x[r0 + 2], x[r0 + 3]),
+                                   pack_bf16x2(x[r0 + 4], x[r0 + 5]), pack_bf16x2(x[r0 + 6], x[r0 + 7]));
+#pragma unroll
+        for (int t = 0; t < NTO; ++t) {
+          const int rowoff = (t * 32 + (lane & 31)) * LDT + kk * 16 + 4 * hl;
+          const uint2 o0 = *(const uint2*)(opnd + rowoff), o1 = *(const uint2*)(opnd + rowoff + 8);
+          acc[t] = mfma32_bf16(make_uint4(o0.x, o0.y, o1.x, o1.y), f, acc[t]);
+        }
+      }
+    }
+  }
+  if (key >= T) return;
+  // lane holds dK^T or dV^T rows e = 32t + 8g + 4h + rr of key `key`
+  if (grp > 1) {
+    const size_t plane = (size_t)a.B * T * a.Hkv * DH;
+    const size_t o = (rowb + key) * (size_t)(a.Hkv * DH) + kvh * DH;
+    float* dst = part + (size_t)(role == 0 ? grp + hh : hh) * plane + o;
+#pragma unroll
+    for (int t = 0; t < NTO; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int e0 = 32 * t + 8 * g + 4 * hl;
+        *(float4*)(dst + e0) = make_float4(acc[t][4 * g], acc[t][4 * g + 1], acc[t][4 * g + 2], acc[t][4 * g + 3]);
+      }
+    return;
+  }
+  constexpr int half = DH / 2;
+  if (role == 0) {
+    bf16* dvr = a.dv + (rowb + key) * a.ldk + kvh * DH;
+#pragma unroll
+    for (int t = 0; t < NTO; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int e0 = 32 * t + 8 * g + 4 * hl;
+        *(uint2*)(dvr + e0) =
+            make_uint2(pack_bf16x2(acc[t][4 * g], acc[t][4 * g + 1]), pack_bf16x2(acc[t][4 * g + 2], acc[t][4 * g + 3]));
+      }
+    return;
+  }
+  const float scale = 1.0f / sqrtf((float)DH);
+  bf16* dkr = a.dk + (rowb + key) * a.ldk + kvh * DH;
+#pragma unroll
+  for (int t = 0; t < NTO / 2; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int e0 = 32 * t + 8 * g + 4 * hl;
+      float lo[4], hi[4];
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const float2 cs = *(const float2*)(a.cs + 2 * ((size_t)key * half + e0 + rr));
+        const float d1 = acc[t][4 * g + rr] * scale, d2 = acc[t + NTO / 2][4 * g + rr] * scale;
+        lo[rr] = d1 * cs.x + d2 * cs.y;
+        hi[rr] = d2 * cs.x - d1 * cs.y;
+      }
+      *(uint2*)(dkr + e0) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+      *(uint2*)(dkr + e0 + half) = make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
+    }
+}
+
 // Number of query chunks of `cq` queries that key block `kblk` (64 keys) of
 // k_attn_bwd_dkdv visits.
 __host__ __device__ inline int kv_block_chunks(int kblk, int T, int window, int cq) {
@@ -1254,8 +1466,15 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
                  hipLaunchKernelGGL((k_attn_bwd_dkdv<64, 64>), gkv, dim3(256), 0, st, a, kv_part, p.kv_nck, p.kv_cq));
       break;
     case 256:
-      MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io,
-                 hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, kv_part, p.kv_nck, p.kv_cq));
+      if (!p.kv_nck) {
+        // 64 keys per workgroup: two wave pairs of 32 keys, one wave per SIMD
+        const dim3 gp((a.T + 63) / 64, a.Hq, a.B);
+        MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io,
+                   hipLaunchKernelGGL((k_attn_bwd_kv32p<2>), gp, dim3(256), 0, st, a, kv_part));
+      } else {
+        MEBP_TIMED(st, "attn_bwd_dkdv", f_kv, io,
+                   hipLaunchKernelGGL((k_attn_bwd_dkdv<256, 32>), gkv, dim3(256), 0, st, a, kv_part, p.kv_nck, p.kv_cq));
+      }
       break;
     default: return hipErrorInvalidValue;
   }

@@ -563,8 +563,8 @@ DEV void wait_vmcnt() {
 // K step 64. The activation tile goes from global memory straight into LDS (buffer loads
 // with the LDS flag: no staging registers, no LDS stores) through a ring of three stages
 // filled two K tiles ahead. A stage holds the 256 x 64 fp16 tile as 128-byte rows whose
-// eight 16-byte chunks are stored at position chunk ^ (row & 7), so that the MFMA fragment
-// reads (32 rows, one chunk each) spread over all banks. The weights are loaded into
+// eight 16-byte chunks are stored at position chunk ^ ((row / 2) % 8), so that the MFMA
+// fragment reads (32 rows, one chunk each) spread over all banks. The weights are loaded into
 // registers, also two tiles ahead, and decompressed by each wave for its own columns.
 //
 // W16: the weights are plain 16-bit values [N][K] (seg.q4 points at them, no scales) that
@@ -594,12 +594,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   };
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WNW, wn = wave % WNW, h = lane >> 5;
-  const int nt = blockIdx.x;
+  const int nt = blockIdx.x, mt = blockIdx.y;
   int s = 0;
   if (a.nseg > 1 && nt >= a.seg[1].tile0) s = 1;
   if (a.nseg > 2 && nt >= a.seg[2].tile0) s = 2;
   const NtSeg sg = pick_seg(a, s);
-  const int n0 = (nt - sg.tile0) * BN, m0 = blockIdx.y * BM;
+  const int n0 = (nt - sg.tile0) * BN, m0 = mt * BM;
   const int K = a.K, Nn = sg.N, Kh = K >> 1;
   const int nk = (K + BK - 1) / BK, kgroups = (K + 31) >> 5;
   const int z = blockIdx.z, S = gridDim.z;
@@ -613,18 +613,21 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   const rsrc_t rS = make_rsrc(W16 ? nullptr : sg.scale + (size_t)min(wcol0, Nn) * kgroups,
                               W16 ? 0 : (size_t)wrows * kgroups * 2);
   // activation loads: instruction i of wave w fills tile rows 8 (w + 8 i) .. +8, lane l row
-  // 8 (w + 8 i) + l / 8, LDS position l % 8, i.e. global chunk (l % 8) ^ (row & 7)
+  // 8 (w + 8 i) + l / 8, LDS position l % 8, i.e. global chunk (l % 8) ^ swz(row)
   uint32_t offA[4];
   int chunkA[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = 8 * (wave + 8 * i) + (lane >> 3);
-    chunkA[i] = (lane & 7) ^ (row & 7);
+    chunkA[i] = (lane & 7) ^ ((row >> 1) & 7);
     offA[i] = (uint32_t)((row * a.lda + 8 * chunkA[i]) * 2);
   }
   const uint32_t offB = W16 ? (uint32_t)(((lane & 31) * K + 32 * h) * 2) : (uint32_t)((lane & 31) * Kh + 16 * h);
   const uint32_t offS = (uint32_t)(((lane & 31) * kgroups + h) * 2);
-  // fragment reads: row wm*128 + 32 i + (l % 32), chunk 4h + t at position (4h + t) ^ (l & 7)
+  // fragment reads: row wm*128 + 32 i + (l % 32), chunk 4h + t at position (4h + t) ^ swz(row)
+  // with swz(row) = (row / 2) % 8 = (l / 2) % 8: the 16 lanes that read in one LDS cycle
+  // (16 consecutive rows) hit 16 distinct 16-byte bank groups (rows r and r + 8 no longer
+  // share one: with swz = row % 8 half of the LDS cycles were bank conflicts)
   const uint32_t rowA = (uint32_t)((wm * 128 + (lane & 31)) * 128);
 
   LdsWeightRegs<W16> wr;
@@ -687,7 +690,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     }
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const int pos = ((4 * h + t) ^ (lane & 7)) * 16;
+      const int pos = ((4 * h + t) ^ ((lane >> 1) & 7)) * 16;
       uint4 af[4], bfr[NJ];
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[i] = *(const uint4*)(As + 4096 * i + pos);

@@ -176,6 +176,12 @@ HEAD_DIM_CASES = {
     "dh256_gqa": MINI.with_(name="dh256_gqa", hidden=256, n_heads=4, n_kv_heads=2, head_dim=256, seq=200),
     # enough 64-row tiles (9 x 8 heads x 4 sequences) that no attention loop is split
     "dh64_unsplit": MINI.with_(name="dh64_unsplit", n_heads=8, n_kv_heads=2, head_dim=64, batch=4, seq=520),
+    # head dim 256 unsplit (17 x 4 heads x 4 sequences, 18 x 2 x 8 tiles of 64): the 32-key
+    # wave-pair dK/dV kernel, grouped (partials) and ungrouped (direct store), ragged T
+    "dh256_gqa_unsplit": MINI.with_(name="dh256_gqa_unsplit", hidden=256, n_heads=4, n_kv_heads=2, head_dim=256,
+                                    batch=4, seq=1040),
+    "dh256_mha_unsplit": MINI.with_(name="dh256_mha_unsplit", hidden=256, n_heads=2, n_kv_heads=2, head_dim=256,
+                                    batch=8, seq=1100),
 }
 
 
