@@ -312,14 +312,18 @@ def experiments(cfg, seqs=(128, 256, 512, 1024, 2048, 4096)):
     seq_sweep: the whole checkpointed step of `cfg`'s model at batch 1 and each sequence
     length (the same weights; ids are the first T of one seeded draw), HIP-graph replay.
 
-    decompression: the paper's runtime decompresses each block's weights before its graph
-    runs; here decompression is folded into the GEMM operand loads instead. What the
-    separate pass would cost on this GPU is timed with the stand-alone decompression kernel
-    (int4 -> bf16 into a scratch matrix, every projection of every layer), and set against
-    the measured forward pass (every layer's mebp_layer_forward_ckpt) and backward pass
-    (every layer's mebp_layer_recompute_backward) of the fused design at the workload's
-    own batch and length. Forward and backward would each need one such pass (the backward
-    recomputes the forward from the same decompressed weights)."""
+    decompression_in_gemm: the cost of the decompression fused into the GEMMs (see
+    decompression_overhead).
+
+    decompression_as_separate_pass: the paper's runtime decompresses each block's weights
+    before its graph runs. What such a separate pass would cost on this GPU is timed with
+    the stand-alone decompression kernel (int4 -> bf16 into a scratch matrix, every
+    projection of every layer), and set against the measured forward pass (every layer's
+    mebp_layer_forward_ckpt) and backward pass (every layer's mebp_layer_recompute_backward)
+    of the fused design at the workload's own batch and length.
+
+    checkpoint_offload: step time and peak device memory with the checkpoints in pinned
+    host memory (4-slot device ring) against device checkpoints."""
     import torch
     from mebp_inputs import PROJ, make_inputs
     from paper_2510_03425_amd import _lib as L
@@ -336,7 +340,7 @@ def experiments(cfg, seqs=(128, 256, 512, 1024, 2048, 4096)):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
 
-    out = {"workload": f"{cfg.name}-shaped", "seq_sweep": [], "decompression": None}
+    out = {"workload": f"{cfg.name}-shaped", "seq_sweep": []}
     big = cfg.with_(batch=1, seq=max(seqs))
     t0 = time.time()
     inp = make_inputs(big, seed=0)
@@ -362,6 +366,9 @@ def experiments(cfg, seqs=(128, 256, 512, 1024, 2048, 4096)):
         del g, dm
         torch.cuda.synchronize()
     inp.cfg = big
+
+    # Table 2 analog: the fused decompression's cost inside the GEMMs
+    out["decompression_in_gemm"] = decompression_overhead(cfg)
 
     # decompression as a separate pass, at the workload's own shape
     inp2 = make_inputs(cfg, seed=0)
@@ -394,19 +401,20 @@ def experiments(cfg, seqs=(128, 256, 512, 1024, 2048, 4096)):
     t_fwd = timed(forward_all, 3)
     t_bwd = timed(backward_all, 3)
     wbytes = sum(o * i for o, i in (cfg.proj_shape(p) for p in PROJ)) * Lyr
-    out["decompression"] = {
+    out["decompression_as_separate_pass"] = {
         "batch": cfg.batch, "seq_len": cfg.seq, "weights": wbytes,
         "separate_pass_ms": round(t_dec, 3), "separate_pass_GBps": round(wbytes * (0.5625 + 2) / (t_dec * 1e-3) / 1e9, 1),
         "forward_ms": round(t_fwd, 3), "backward_ms": round(t_bwd, 3),
         "share_of_forward_if_separate": round(t_dec / (t_fwd + t_dec), 4),
         "share_of_backward_if_separate": round(t_dec / (t_bwd + t_dec), 4)}
     log(f"decompression pass {t_dec:.3f} ms; forward {t_fwd:.3f} ms; backward {t_bwd:.3f} ms")
+    del scratch, ck, dy, dxb
 
     # checkpoints in pinned host memory through a 4-slot device ring, against the step with
-    # every checkpoint in device memory (both replayed as HIP graphs)
+    # every checkpoint in device memory (both replayed as HIP graphs); the device memory each
+    # configuration holds is measured on a model of its own (torch's allocator peak: every
+    # device buffer comes from it)
     N, d, slots = cfg.n_tokens, cfg.hidden, 4
-    host = torch.empty((Lyr + 1, N, d), dtype=torch.float32).pin_memory()
-    ring = torch.empty((slots, N, d), dtype=torch.float32, device="cuda:0")
 
     def graph_of(fn):
         fn()
@@ -420,19 +428,103 @@ def experiments(cfg, seqs=(128, 256, 512, 1024, 2048, 4096)):
         torch.cuda.current_stream().wait_stream(s_cap)
         return gr
 
+    def fresh_peak():
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+
+    del dm
+    fresh_peak()
+    dm = DeviceModel(inp2, device="cuda:0")
     g_dev = graph_of(lambda: dm.train_step(None))
     t_dev = timed(g_dev.replay, 5)
+    peak_dev = torch.cuda.max_memory_allocated()
+    ws_bytes = dm.ws_bytes
+    weights = sum(t.numel() * t.element_size() for t in dm.keep)
+    del g_dev, dm
+    fresh_peak()
+    dm = DeviceModel(inp2, device="cuda:0")
+    host = torch.empty((Lyr + 1, N, d), dtype=torch.float32).pin_memory()
+    ring = torch.empty((slots, N, d), dtype=torch.float32, device="cuda:0")
     g_off = graph_of(lambda: dm.train_step_offload(host, ring, None))
     t_off = timed(g_off.replay, 5)
-    weights = sum(t.numel() * t.element_size() for t in dm.keep)
+    peak_off = torch.cuda.max_memory_allocated()
     out["checkpoint_offload"] = {
         "ring_slots": slots, "ms_per_step_device_ckpt": round(t_dev, 3), "ms_per_step_offload": round(t_off, 3),
+        "peak_device_bytes_device_ckpt": int(peak_dev), "peak_device_bytes_offload": int(peak_off),
         "device_ckpt_bytes": (Lyr + 1) * N * d * 4, "device_ring_bytes": slots * N * d * 4,
-        "host_ckpt_bytes": (Lyr + 1) * N * d * 4, "weights_lora_norm_bytes": weights, "workspace_bytes": dm.ws_bytes,
-        "device_total_bytes_device_ckpt": weights + dm.ws_bytes + (Lyr + 1) * N * d * 4,
-        "device_total_bytes_offload": weights + dm.ws_bytes + slots * N * d * 4}
-    log(f"offload: {t_off:.3f} ms/step vs {t_dev:.3f} ms/step with device checkpoints")
+        "host_ckpt_bytes": (Lyr + 1) * N * d * 4, "weights_lora_norm_bytes": weights, "workspace_bytes": ws_bytes}
+    log(f"offload: {t_off:.3f} ms/step vs {t_dev:.3f} ms/step with device checkpoints; peak device memory "
+        f"{peak_off / 2**30:.2f} GiB vs {peak_dev / 2**30:.2f} GiB")
+    del g_off, dm, ring, host
     print(json.dumps(out), flush=True)
+
+
+def decompression_overhead(cfg, reps=5):
+    """Counterpart of the paper's decompression-share table for this design, where the
+    decompression is fused into the GEMMs: the production dequant-GEMM kernels timed on the
+    workload's projection shapes (M = B*T tokens) once on the int4 weights and once on the
+    same weights already decompressed to 16 bits (the same kernels with the decompression
+    taken out; mebp_test_gemm kinds NT_LDS / NT_LDS_W16 for the forward products, fp16
+    operands, and TN_BIG / TN_BIG_W16 for the input-gradient products, bf16). Per step every
+    projection runs twice forward (forward pass and recompute) and once backward, in each
+    of the L layers. overhead = t_int4 / t_16bit - 1 (negative: the int4 kernel is faster,
+    its weight operand being a quarter of the bytes)."""
+    import numpy as np
+    import torch
+    from mebp_inputs import PROJ, quantize_q4
+    from paper_2510_03425_amd import _lib as L
+    from paper_2510_03425_amd.device import stream_handle
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    M, st = cfg.n_tokens, stream_handle()
+    rows, tot = {}, {"fwd_int4": 0.0, "fwd_16": 0.0, "bwd_int4": 0.0, "bwd_16": 0.0}
+    for p in PROJ:
+        n_out, n_in = cfg.proj_shape(p)
+        rng = np.random.default_rng(0)
+        q4, sb = quantize_q4((rng.standard_normal((n_out, n_in), dtype=np.float32) * 0.02))
+        tq, ts = torch.from_numpy(q4).cuda(), torch.from_numpy(sb.view(np.int16)).cuda()
+        wq = L.MebpQ4(q4=tq.data_ptr(), scale=ts.data_ptr())
+        wf = torch.empty((n_out, n_in), dtype=torch.float32, device="cuda")
+        L.mebp_dequant_q4(wq, n_out, n_in, cfg.group, wf.data_ptr(), 0, st)
+        w_h, w_b = wf.half().contiguous(), wf.bfloat16().contiguous()
+        x = (torch.randn(M, n_in, device="cuda") * 0.5).half()
+        g = (torch.randn(M, n_out, device="cuda") * 0.01).bfloat16()
+        out_f = torch.empty(M, n_out, device="cuda")
+        out_b = torch.empty(M, n_in, device="cuda")
+        w16 = L.MebpQ4(q4=w_h.data_ptr(), scale=0)
+        b16 = L.MebpQ4(q4=w_b.data_ptr(), scale=0)
+        r = {"fwd_int4": timed(lambda: L.mebp_test_gemm(L.TEST_GEMM_NT_LDS, wq, n_out, n_in, x.data_ptr(), M,
+                                                         out_f.data_ptr(), st)),
+             "fwd_16": timed(lambda: L.mebp_test_gemm(L.TEST_GEMM_NT_LDS_W16, w16, n_out, n_in, x.data_ptr(), M,
+                                                       out_f.data_ptr(), st)),
+             "bwd_int4": timed(lambda: L.mebp_test_gemm(L.TEST_GEMM_TN_BIG, wq, n_out, n_in, g.data_ptr(), M,
+                                                         out_b.data_ptr(), st)),
+             "bwd_16": timed(lambda: L.mebp_test_gemm(L.TEST_GEMM_TN_BIG_W16, b16, n_out, n_in, g.data_ptr(), M,
+                                                       out_b.data_ptr(), st))}
+        rows[p] = {k: round(v, 4) for k, v in r.items()}
+        for k in tot:
+            tot[k] += r[k] * cfg.n_layers * (2 if k.startswith("fwd") else 1)
+        del tq, ts, wf, w_h, w_b, x, g, out_f, out_b
+        torch.cuda.empty_cache()
+    res = {"tokens": M, "per_projection_ms": rows,
+           "forward_ms_per_step": {"int4": round(tot["fwd_int4"], 2), "16bit": round(tot["fwd_16"], 2)},
+           "backward_ms_per_step": {"int4": round(tot["bwd_int4"], 2), "16bit": round(tot["bwd_16"], 2)},
+           "overhead_forward": round(tot["fwd_int4"] / tot["fwd_16"] - 1, 4),
+           "overhead_backward": round(tot["bwd_int4"] / tot["bwd_16"] - 1, 4)}
+    log(f"decompression inside the GEMMs ({cfg.name}): forward {res['overhead_forward']:+.1%}, backward "
+        f"{res['overhead_backward']:+.1%} (int4 against pre-decompressed 16-bit weights, same kernels)")
+    return res
 
 
 def main():

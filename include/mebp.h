@@ -280,9 +280,10 @@ enum {
   MEBP_TEST_GEMM_NT_LDS = 3,    /* forward, 256 x 256 tiles, activations loaded into LDS  */
   MEBP_TEST_GEMM_TN = 4,        /* transposed, 128 x 128 tiles                            */
   MEBP_TEST_GEMM_TN_BIG = 5,    /* transposed, 256 x 128 tiles                            */
-  MEBP_TEST_GEMM_NT_LDS_W16 = 6 /* MEBP_TEST_GEMM_NT_LDS on plain fp16 weights: w->q4 points */
-                                /* at W fp16 [n_out][n_in], w->scale is unused (the same    */
-                                /* kernel without the decompression, for measuring its cost) */
+  MEBP_TEST_GEMM_NT_LDS_W16 = 6, /* MEBP_TEST_GEMM_NT_LDS on plain fp16 weights: w->q4      */
+                                 /* points at W fp16 [n_out][n_in], w->scale is unused (the */
+                                 /* same kernel without the decompression, to measure it)   */
+  MEBP_TEST_GEMM_TN_BIG_W16 = 7  /* MEBP_TEST_GEMM_TN_BIG on plain bf16 weights, likewise   */
 };
 int mebp_test_gemm(int32_t kind, const mebp_q4* w, int32_t n_out, int32_t n_in, const void* x, int32_t M,
                    float* out, mebp_stream_t stream);

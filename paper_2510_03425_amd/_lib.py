@@ -28,7 +28,7 @@ STATIC_SCRATCH_BYTES = 64 << 20  # MEBP_STATIC_SCRATCH_BYTES
 
 # mebp_test_gemm kinds
 (TEST_GEMM_NT, TEST_GEMM_NT_BIG128, TEST_GEMM_NT_BIG256, TEST_GEMM_NT_LDS, TEST_GEMM_TN, TEST_GEMM_TN_BIG,
- TEST_GEMM_NT_LDS_W16) = range(7)
+ TEST_GEMM_NT_LDS_W16, TEST_GEMM_TN_BIG_W16) = range(8)
 
 
 class MebpConfig(C.Structure):

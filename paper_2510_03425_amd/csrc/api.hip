@@ -1352,9 +1352,9 @@ int mebp_dequant_q4(const mebp_q4* w, int32_t rows, int32_t cols, int32_t group,
 int mebp_test_gemm(int32_t kind, const mebp_q4* w, int32_t n_out, int32_t n_in, const void* x, int32_t M, float* out,
                    mebp_stream_t stream) {
   int e;
-  if (kind < MEBP_TEST_GEMM_NT || kind > MEBP_TEST_GEMM_NT_LDS_W16) return fail(MEBP_EINVAL, "unknown GEMM kind %d", kind);
-  if (kind == MEBP_TEST_GEMM_NT_LDS_W16) {
-    if (!w || !w->q4 || !aligned(w->q4, 16)) return fail(MEBP_EINVAL, "fp16 weight NULL or not 16-byte aligned");
+  if (kind < MEBP_TEST_GEMM_NT || kind > MEBP_TEST_GEMM_TN_BIG_W16) return fail(MEBP_EINVAL, "unknown GEMM kind %d", kind);
+  if (kind == MEBP_TEST_GEMM_NT_LDS_W16 || kind == MEBP_TEST_GEMM_TN_BIG_W16) {
+    if (!w || !w->q4 || !aligned(w->q4, 16)) return fail(MEBP_EINVAL, "16-bit weight NULL or not 16-byte aligned");
   } else if ((e = check_q4(w, "weight"))) {
     return e;
   }

@@ -16,10 +16,11 @@
 //  forward : S^T = K Q^T (A = K rows from LDS, B = Q rows kept in registers);
 //            O^T += V^T P^T (A = V^T from LDS, B = P from registers); row stats live in
 //            the lane of their query, so rescaling needs no cross-lane traffic.
-//  backward: dK/dV kernel owns a key block of one query head (the heads of a GQA group
-//            are summed by the group's last workgroup, in head order); dQ kernel owns a
-//            query block. RoPE backward (rotation by minus the
-//            angle) is applied in both epilogues before the bf16 store.
+//  backward: the dK/dV kernels own a key block of one query head; with grouped-query
+//            attention (or a split query loop) each stores fp32 partials and
+//            k_attn_dkdv_reduce sums the heads of a group (and the chunks) in a fixed order.
+//            The dQ kernel owns a query block. RoPE backward (rotation by minus the angle) is
+//            applied where dK and dQ are finished, before the bf16 store.
 #include <stdlib.h>
 
 #include <algorithm>
@@ -239,13 +240,13 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a, float* part,
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
     const float m_new = fmaxf(m_i, mloc);
-    const float alpha = exp2f(m_i - m_new);
+    const float alpha = exp2_fast(m_i - m_new);
     float ls = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(s[kt][r] - m_new);
+        const float p = exp2_fast(s[kt][r] - m_new);
         s[kt][r] = p;
         ls += p;
       }
@@ -316,7 +317,7 @@ __global__ void k_attn_fwd_combine(const AttnArgs a, const float* part, int nck,
   for (int c = 0; c < n; ++c) {
     const size_t pr = (bh * nck + c) * T + q;
     const float2 st = ml[pr];
-    const float wgt = exp2f(st.x - M);
+    const float wgt = exp2_fast(st.x - M);
     L += wgt * st.y;
     const float4 x0 = *(const float4*)(part + pr * DH + 8 * g), x1 = *(const float4*)(part + pr * DH + 8 * g + 4);
     acc[0] += wgt * x0.x; acc[1] += wgt * x0.y; acc[2] += wgt * x0.z; acc[3] += wgt * x0.w;
@@ -464,21 +465,20 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
     // The running maximum only moves when a row's block maximum exceeds it by more than
     // 2^8 (base-2 domain): the probabilities stay below 256 and the sum and the output are
     // both taken relative to the same stale maximum, so the result is unchanged; most
-    // blocks then skip the rescale of the output accumulators. (Head dim 256 rescales
-    // every block: the branch would push its 256 accumulators past the register file.)
+    // blocks then skip the rescale of the output accumulators.
     const float m_new = mloc > m_i + 8.f ? mloc : m_i;
     float ls = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[kt][r] - m_new);
+        const float p = exp2_fast(s[kt][r] - m_new);
         s[kt][r] = p;
         ls += p;
       }
     ls += __shfl_xor(ls, 32, 64);
-    if (DH == 256 || __builtin_amdgcn_ballot_w64(m_new != m_i)) {
-      const float alpha = exp2f(m_i - m_new);
+    if (__builtin_amdgcn_ballot_w64(m_new != m_i)) {
+      const float alpha = exp2_fast(m_i - m_new);
       l_i *= alpha;
 #pragma unroll
       for (int t = 0; t < NTO; ++t) oacc[t] *= alpha;
@@ -629,7 +629,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
       for (int r = 0; r < 4; ++r) {
         const int ql = qt * 16 + 4 * (lane >> 4) + r;
         const bool vis = visible(qvis, qb0 + ql);
-        const float p = vis ? exp2f(s[qt][r] * sc - lse_s[ql]) : 0.f;
+        const float p = vis ? exp2_fast(s[qt][r] * sc - lse_s[ql]) : 0.f;
         s[qt][r] = p;
         dp[qt][r] = p * (dp[qt][r] - del_s[ql]);
       }
@@ -761,7 +761,7 @@ __global__ __launch_bounds__(256, PF ? 1 : 2) void k_attn_bwd_dq(const AttnArgs 
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const bool vis = visible(kvis, kv0 + kt * 16 + 4 * (lane >> 4) + r);
-        const float p = vis ? exp2f(s[kt][r] * sc - lse2) : 0.f;
+        const float p = vis ? exp2_fast(s[kt][r] * sc - lse2) : 0.f;
         dp[kt][r] = p * (dp[kt][r] - del);
       }
 #pragma unroll
@@ -967,7 +967,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
       for (int rr = 0; rr < 4; ++rr) {
         const int r = 4 * g + rr;
         const bool vis = visible(qvis, qb0 + 8 * g + 4 * hl + rr);
-        const float p = vis ? exp2f(sv[r] * sc - lv[rr]) : 0.f;
+        const float p = vis ? exp2_fast(sv[r] * sc - lv[rr]) : 0.f;
         sv[r] = p;
         dp[r] = p * (dp[r] - dl[rr]);
       }
@@ -1157,7 +1157,7 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
           for (int rr = 0; rr < 4; ++rr) {
             const int r = 4 * g + rr;
             const bool vis = visible(qvis, qb0 + 8 * g + 4 * hl + rr);
-            x[r] = vis ? exp2f(x[r] * sc - lv[rr]) : 0.f;
+            x[r] = vis ? exp2_fast(x[r] * sc - lv[rr]) : 0.f;
             Ps[pair][r][lane] = x[r];
           }
         }

@@ -145,6 +145,11 @@ DEV uint32_t perm_hi16(uint32_t a, uint32_t b) {  // (a.hi, b.hi) -> lo=a.hi, hi
   return __builtin_amdgcn_perm(b, a, 0x07060302u);
 }
 
+// 2^x by the hardware instruction alone (v_exp_f32; exp2f adds a range check and rescale
+// that keep results below 2^-126 as denormals). For softmax weights, which are at most 2^8
+// here: results below 2^-126 become 0, which no fp32 sum of them can notice.
+DEV float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // tanh(x) = 1 - 2 / (exp(2x) + 1) with the hardware exp and reciprocal (absolute error
 // around 1e-7, saturating to +-1 for large |x|)
 DEV float tanh_fast(float x) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * x) + 1.0f); }

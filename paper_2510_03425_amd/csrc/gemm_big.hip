@@ -771,7 +771,10 @@ DEV void sched_tn_step() {
   }
 }
 
-template <int BN, int EPI>
+// W16: the weights are plain bf16 values [N][Kout] (seg.q4 points at them, no scales), copied
+// into the transposed LDS tile without decompression: the same kernel without the
+// decompression, for measuring its cost (W16 = false is the production kernel).
+template <int BN, int EPI, bool W16 = false>
 __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   constexpr int NJ = BN / 64;
   constexpr int CG = BN / 16;   // 16-column groups
@@ -799,18 +802,19 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   for (int s = 0; s < 3; ++s) {
     const TnSeg& sg = a.seg[s < a.nseg ? s : 0];
     rA[s] = make_rsrc((const u16*)sg.G + (size_t)m0 * sg.ldg, (size_t)min(BM, a.M - m0) * sg.ldg * 2);
-    rB[s] = make_rsrc(sg.q4, (size_t)sg.N * Kh);
-    rS[s] = make_rsrc(sg.scale, (size_t)sg.N * kgroups * 2);
+    rB[s] = W16 ? make_rsrc(sg.q4, (size_t)sg.N * Kout * 2) : make_rsrc(sg.q4, (size_t)sg.N * Kh);
+    rS[s] = make_rsrc(W16 ? nullptr : sg.scale, W16 ? 0 : (size_t)sg.N * kgroups * 2);
   }
   // row group varies fastest across lanes so that the transposed LDS writes do not collide
   const int rq = tid % RG, cq = tid / RG;
   const int kc = c0 + 16 * cq;
-  const uint32_t offB = (uint32_t)(RPT * rq * Kh + (kc >> 1));
+  const uint32_t offB = W16 ? (uint32_t)((RPT * rq * Kout + kc) * 2) : (uint32_t)(RPT * rq * Kh + (kc >> 1));
   const uint32_t offS = (uint32_t)((RPT * rq * kgroups + (kc >> 5)) * 2);
 
   uint4 ra[2][8];
   uint2 rw[2][RPT];
   uint32_t rsc[2][RPT];
+  uint4 rw16[W16 ? 2 : 1][W16 ? RPT : 1][2];  // W16: 16 bf16 weights of each row
   f32x16 acc[4][NJ];
   zero_acc(acc);
 
@@ -844,8 +848,13 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
       }
 #pragma unroll
       for (int i = 0; i < RPT; ++i) {
-        rw[st][i] = bload64(rb_, offB + (uint32_t)((n0 + i) * Kh));
-        rsc[st][i] = bload16(rs_, offS + (uint32_t)((n0 + i) * kgroups * 2));
+        if constexpr (W16) {
+          rw16[st][i][0] = bload128(rb_, offB + (uint32_t)((n0 + i) * Kout * 2));
+          rw16[st][i][1] = bload128(rb_, offB + (uint32_t)((n0 + i) * Kout * 2 + 16));
+        } else {
+          rw[st][i] = bload64(rb_, offB + (uint32_t)((n0 + i) * Kh));
+          rsc[st][i] = bload16(rs_, offS + (uint32_t)((n0 + i) * kgroups * 2));
+        }
       }
       if constexpr (TAIL) {
         if (n0 + BK > sg.N) {  // reduction tail: A columns past N must be 0 (B rows already are)
@@ -861,11 +870,18 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
       float v[RPT][16];
 #pragma unroll
       for (int i = 0; i < RPT; ++i) {
-        const float sc = half_bits_to_f32((uint16_t)rsc[st][i]);
+        if constexpr (W16) {
+          const uint32_t wd[8] = {rw16[st][i][0].x, rw16[st][i][0].y, rw16[st][i][0].z, rw16[st][i][0].w,
+                                  rw16[st][i][1].x, rw16[st][i][1].y, rw16[st][i][1].z, rw16[st][i][1].w};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          v[i][e] = (float)nib_s(rw[st][i].x, e) * sc;
-          v[i][8 + e] = (float)nib_s(rw[st][i].y, e) * sc;
+          for (int e = 0; e < 16; ++e) v[i][e] = (e & 1) ? bf16_hi(wd[e >> 1]) : bf16_lo(wd[e >> 1]);
+        } else {
+          const float sc = half_bits_to_f32((uint16_t)rsc[st][i]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            v[i][e] = (float)nib_s(rw[st][i].x, e) * sc;
+            v[i][8 + e] = (float)nib_s(rw[st][i].y, e) * sc;
+          }
         }
       }
 #pragma unroll
@@ -1156,6 +1172,14 @@ hipError_t launch_gemm_probe_big(int kind, const uint8_t* q4, const uint16_t* sc
     case 3:  // LDS-direct forward, 256 x 256 tiles
       hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0, st, a);
       break;
+    case 7: {  // the transposed 256 x 128 kernel on plain bf16 weights [n_out][n_in] (seg.q4)
+      TnArgs t{};
+      t.M = M; t.Kout = n_in; t.nseg = 1;
+      t.seg[0].G = (const bf16*)x; t.seg[0].ldg = n_out; t.seg[0].q4 = q4; t.seg[0].N = n_out;
+      t.out = out; t.ldo = n_in; t.splits = 1;
+      hipLaunchKernelGGL((k_gemm_tn_big<128, TN_STORE_F32, true>), dim3((n_in + 127) / 128, mt, 1), dim3(NTH), 0, st, t);
+      break;
+    }
     case 6:  // the LDS-direct forward kernel on plain fp16 weights [n_out][n_in] (seg.q4)
       hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32, true>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0, st, a);
       break;

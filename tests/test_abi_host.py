@@ -190,7 +190,7 @@ def test_test_gemm_and_static_entry_validate_first(built_lib):
     g = lambda **kw: L.mebp_test_gemm(kw.get("kind", L.TEST_GEMM_NT), kw.get("w", w), kw.get("n_out", 64),
                                       kw.get("n_in", 64), kw.get("x", X), kw.get("M", 32), kw.get("out", OUT), 0,
                                       check=False)
-    assert g(kind=7) == L.MEBP_EINVAL and g(kind=-1) == L.MEBP_EINVAL
+    assert g(kind=8) == L.MEBP_EINVAL and g(kind=-1) == L.MEBP_EINVAL
     assert g(n_in=40) == L.MEBP_EUNSUPPORTED and g(n_out=8) == L.MEBP_EUNSUPPORTED
     assert g(M=0) == L.MEBP_EINVAL and g(M=70000) == L.MEBP_EUNSUPPORTED
     assert g(x=X + 8) == L.MEBP_EINVAL and g(out=0) == L.MEBP_EINVAL and g(w=None) == L.MEBP_EINVAL

@@ -96,3 +96,30 @@ def test_transposed_kernel_decompression_bit_exact(built_lib, gpu, kind, shape):
     bad = np.argwhere(got.view(np.uint32) != exp.view(np.uint32))
     assert bad.size == 0, f"{len(bad)} mismatches, first at (m, c) = {bad[0].tolist()}: " \
                           f"{got[tuple(bad[0])]!r} vs {exp[tuple(bad[0])]!r}"
+
+
+@pytest.mark.parametrize("fwd", [True, False], ids=["forward", "transposed"])
+def test_16bit_weight_mode_is_the_same_kernel(built_lib, gpu, fwd):
+    # the 16-bit-weight modes (used to measure what the decompression costs) fed the
+    # decompressed weights multiply exactly the operands of the int4 kernels in the same
+    # order: outputs identical bit for bit on random inputs
+    n_out, n_in, M = 592, 688, 808
+    q4, sb = _weights(n_out, n_in, seed=5)
+    tq, ts, w = _upload(q4, sb, gpu)
+    wf = torch.from_numpy(O.dequant(q4, sb, n_in, 32).astype(np.float32)).to(gpu)
+    w16 = (wf.half() if fwd else wf.bfloat16()).contiguous()
+    ww = L.MebpQ4(q4=w16.data_ptr(), scale=0)
+    if fwd:
+        x = (torch.randn(M, n_in, device=gpu)).half()
+        kinds, cols = (L.TEST_GEMM_NT_LDS, L.TEST_GEMM_NT_LDS_W16), n_out
+    else:
+        x = (torch.randn(M, n_out, device=gpu) * 0.01).bfloat16()
+        kinds, cols = (L.TEST_GEMM_TN_BIG, L.TEST_GEMM_TN_BIG_W16), n_in
+    outs = []
+    for kind, wt in zip(kinds, (w, ww)):
+        out = torch.full((M, cols), float("nan"), dtype=torch.float32, device=gpu)
+        say("16-bit weight mode", "forward" if fwd else "transposed", kind)
+        L.mebp_test_gemm(kind, wt, n_out, n_in, x.data_ptr(), M, out.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
