@@ -11,7 +11,9 @@ import ctypes as C
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmebp.so")
+# MEBP_LIB selects another build of the same library (the sanitizer build of the host-only
+# tests); there is no fallback: a missing library raises.
+LIB_PATH = os.environ.get("MEBP_LIB") or os.path.join(_HERE, "libmebp.so")
 
 MEBP_OK, MEBP_EINVAL, MEBP_EUNSUPPORTED, MEBP_EWORKSPACE, MEBP_EHIP = 0, -1, -2, -3, -4
 NPROJ = 7
