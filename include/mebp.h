@@ -256,6 +256,23 @@ const char* mebp_last_error(void);
 
 /* ---------------- test and diagnostic entry points ---------------------------------- */
 
+/* Workspace guards, a debug mode (also on when MEBP_WS_GUARD=1 is in the environment when
+ * the library loads). On, every workspace slot is followed by a guard region of at least
+ * 256 bytes holding a known pattern, so mebp_workspace_bytes() returns more (size the
+ * workspace with the mode already set; a workspace sized without it is refused with
+ * MEBP_EWORKSPACE) and mebp_workspace_offset() moves. Every entry point that takes a
+ * workspace (the static-scratch one included) then fills the guards before its first
+ * kernel, checks them after its last one on the caller's stream and waits for that stream
+ * (so a guarded call cannot be captured into a graph); an overwritten guard fails the call
+ * with MEBP_EWORKSPACE, the message naming the slot. Results are those of the unguarded
+ * call. mebp_set_workspace_guards returns the previous mode (0 off, 1 on); switch it only
+ * while no call is in flight. mebp_workspace_guard_check checks the guards of a workspace
+ * that a guarded call used, without filling them first: MEBP_OK, MEBP_EWORKSPACE (names
+ * the slot), or MEBP_EINVAL when the mode is off or an argument is bad.                  */
+int mebp_set_workspace_guards(int32_t on);
+int mebp_workspace_guard_check(const mebp_config* cfg, int32_t B, int32_t T, void* ws, size_t ws_bytes,
+                               mebp_stream_t stream);
+
 /* Decompression alone (Algorithm 1, decompress): out_f32[r][c] = q*s exactly and/or
  * out_bf16[r][c] = bf16 bits of that value rounded to nearest even (either may be NULL).
  * cols must be a multiple of 8; group as in mebp_config.                                 */

@@ -24,6 +24,7 @@ EXPORTED = (
     "mebp_dequant_q4", "mebp_workspace_offset", "mebp_workspace_slot_name", "mebp_kernel_timing",
     "mebp_kernel_timing_report", "mebp_kernel_repeat", "mebp_lora_grad_accumulate", "mebp_lora_adamw_step",
     "mebp_train_step_offload", "mebp_test_gemm", "mebp_layer_recompute_backward_static",
+    "mebp_set_workspace_guards", "mebp_workspace_guard_check",
 )
 
 STATIC_SCRATCH_BYTES = 64 << 20  # MEBP_STATIC_SCRATCH_BYTES
@@ -112,6 +113,8 @@ def lib() -> C.CDLL:
             "mebp_test_gemm": (C.c_int, [I32, C.POINTER(MebpQ4), I32, I32, P, I32, P, P]),
             "mebp_workspace_offset": (SZ, [cfgp, I32, I32, I32]),
             "mebp_workspace_slot_name": (C.c_char_p, [I32]),
+            "mebp_set_workspace_guards": (C.c_int, [I32]),
+            "mebp_workspace_guard_check": (C.c_int, [cfgp, I32, I32, P, SZ, P]),
             "mebp_kernel_timing": (C.c_int, [I32, I32]),
             "mebp_kernel_timing_report": (C.c_int, [C.c_char_p, SZ]),
             "mebp_kernel_repeat": (C.c_int, [C.c_char_p, I32]),
@@ -149,6 +152,16 @@ def mebp_workspace_bytes(cfg: MebpConfig, B: int, T: int) -> int:
 
 def mebp_workspace_offset(cfg: MebpConfig, B: int, T: int, slot: int) -> int:
     return lib().mebp_workspace_offset(C.byref(cfg), B, T, slot)
+
+
+def mebp_set_workspace_guards(on: bool) -> bool:
+    """Workspace guard debug mode on or off; returns the previous mode."""
+    return bool(lib().mebp_set_workspace_guards(1 if on else 0))
+
+
+def mebp_workspace_guard_check(cfg, B, T, ws, ws_bytes, stream=0, check=True):
+    r = lib().mebp_workspace_guard_check(C.byref(cfg), B, T, ws, ws_bytes, stream)
+    return _check(r) if check else r
 
 
 def mebp_workspace_slot_name(slot: int):

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <map>
 #include <mutex>
 #include <string>
@@ -75,10 +76,30 @@ bool per_set(int s) {
   }
 }
 
+// Debug mode of the workspace (mebp_set_workspace_guards, or MEBP_WS_GUARD=1 in the
+// environment when the library loads): every slot, both copies of the per-set ones, is
+// followed by a guard region (its padding up to the 256-byte boundary plus 256 bytes) that
+// holds a known pattern. The entry points that take a workspace fill the guards before
+// their first kernel and check them after their last one on the caller's stream, then wait
+// for the stream: an overwritten guard fails the call with MEBP_EWORKSPACE and the slot's
+// name. The layout, and so mebp_workspace_bytes, depends on the mode.
+std::atomic<int> g_guards{[] {
+  const char* e = getenv("MEBP_WS_GUARD");
+  return e && *e && *e != '0' ? 1 : 0;
+}()};
+constexpr size_t kGuardBytes = 256;
+constexpr int kMaxGuards = 2 * S_COUNT;
+
 struct Layout {
   size_t off[S_COUNT];
   size_t off1[S_COUNT];  // second copy of the per-set slots (equal to off[] for the others)
   size_t total;
+  bool guards;                // debug mode: guard regions after the slots
+  int nguard;
+  size_t g_off[kMaxGuards];   // guard regions: byte offset, length (multiples of 4) and
+  uint32_t g_len[kMaxGuards]; // tag = slot + S_COUNT * copy
+  int32_t g_tag[kMaxGuards];
+  size_t status_off;          // one word: the smallest tag of an overwritten guard
   int lm_chunk;   // vocabulary columns per LM-head chunk
   int lm_splits;  // split-K factor of a whole chunk's dH product (narrower chunks use fewer)
   int ntiles;     // statistics tiles of a whole chunk (the stats row pitch)
@@ -206,16 +227,24 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
     sz[S_PART] = lp * 4;
   }
   size_t o = 0;
-  for (int i = 0; i < S_COUNT; ++i) {
-    L->off[i] = o;
-    o += (sz[i] + 255) & ~(size_t)255;
-  }
-  for (int i = 0; i < S_COUNT; ++i) {
-    L->off1[i] = L->off[i];
-    if (!per_set(i)) continue;
-    L->off1[i] = o;
-    o += (sz[i] + 255) & ~(size_t)255;
-  }
+  L->guards = g_guards.load() != 0;
+  L->nguard = 0;
+  auto place = [&](int i, int copy) {
+    const size_t at = o;
+    o += ((sz[i] + 255) & ~(size_t)255) + (L->guards ? kGuardBytes : 0);
+    if (L->guards) {
+      const size_t g = at + ((sz[i] + 3) & ~(size_t)3);
+      L->g_off[L->nguard] = g;
+      L->g_len[L->nguard] = (uint32_t)(o - g);
+      L->g_tag[L->nguard] = i + S_COUNT * copy;
+      ++L->nguard;
+    }
+    return at;
+  };
+  for (int i = 0; i < S_COUNT; ++i) L->off[i] = place(i, 0);
+  for (int i = 0; i < S_COUNT; ++i) L->off1[i] = per_set(i) ? place(i, 1) : L->off[i];
+  L->status_off = o;
+  if (L->guards) o += 256;
   L->total = o;
   return true;
 }
@@ -223,6 +252,82 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
 template <class Tp>
 Tp* slot(void* ws, const Layout& L, int s) {
   return (Tp*)((char*)ws + L.off[s]);
+}
+
+// ------------------------------------------------------------------ workspace guards
+struct GuardList {
+  int n;
+  uint32_t len[kMaxGuards];
+  int32_t tag[kMaxGuards];
+  unsigned long long off[kMaxGuards];
+};
+
+__device__ uint32_t guard_word(int32_t tag, uint32_t i) {
+  return 0xA5C3E1F7u ^ ((uint32_t)tag * 0x9E3779B9u) ^ (i * 0x85EBCA6Bu);
+}
+
+// one block per guard region
+__global__ void k_guard_fill(uint8_t* ws, GuardList g) {
+  const int r = blockIdx.x;
+  uint32_t* p = (uint32_t*)(ws + g.off[r]);
+  for (uint32_t i = threadIdx.x; i < g.len[r] / 4; i += blockDim.x) p[i] = guard_word(g.tag[r], i);
+}
+
+__global__ void k_guard_reset(uint32_t* status) { *status = 0xFFFFFFFFu; }
+
+__global__ void k_guard_check(const uint8_t* ws, GuardList g, uint32_t* status) {
+  const int r = blockIdx.x;
+  const uint32_t* p = (const uint32_t*)(ws + g.off[r]);
+  bool bad = false;
+  for (uint32_t i = threadIdx.x; i < g.len[r] / 4; i += blockDim.x) bad |= p[i] != guard_word(g.tag[r], i);
+  if (bad) atomicMin(status, (uint32_t)g.tag[r]);
+}
+
+int guard_launch(const Layout& L, void* ws, hipStream_t st, bool fill) {
+  GuardList g;
+  g.n = L.nguard;
+  for (int i = 0; i < L.nguard; ++i) {
+    g.off[i] = L.g_off[i];
+    g.len[i] = L.g_len[i];
+    g.tag[i] = L.g_tag[i];
+  }
+  uint32_t* status = (uint32_t*)((char*)ws + L.status_off);
+  if (fill) {
+    hipLaunchKernelGGL(k_guard_fill, dim3(g.n), dim3(128), 0, st, (uint8_t*)ws, g);
+  } else {
+    // a check may follow another check: the status word starts over
+    hipLaunchKernelGGL(k_guard_reset, dim3(1), dim3(1), 0, st, status);
+    hipLaunchKernelGGL(k_guard_check, dim3(g.n), dim3(128), 0, st, (const uint8_t*)ws, g, status);
+  }
+  HIP_TRY(hipGetLastError());
+  return MEBP_OK;
+}
+
+// Checks every guard on `st` and waits for it: MEBP_EWORKSPACE names the first slot (in
+// layout order) whose guard no longer holds its pattern.
+int guard_verdict(const Layout& L, void* ws, hipStream_t st) {
+  int e = guard_launch(L, ws, st, false);
+  if (e) return e;
+  uint32_t h = 0;
+  HIP_TRY(hipMemcpyAsync(&h, (char*)ws + L.status_off, 4, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  if (h != 0xFFFFFFFFu)
+    return fail(MEBP_EWORKSPACE, "workspace guard after slot '%s'%s was overwritten", kSlotNames[h % S_COUNT],
+                h >= (uint32_t)S_COUNT ? " (second copy)" : "");
+  return MEBP_OK;
+}
+
+// Runs `body` (the launches of one entry point on `stream`) between a fill and a check of
+// the guards when the layout has them; otherwise just runs it.
+template <class F>
+int guarded(const mebp_config* c, int B, int T, void* ws, mebp_stream_t stream, F&& body) {
+  if (!g_guards.load()) return body();
+  Layout L;
+  make_layout(c, B, T, &L);
+  if (!L.guards) return body();
+  int e = guard_launch(L, ws, (hipStream_t)stream, true);
+  if (e || (e = body())) return e;
+  return guard_verdict(L, ws, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ validation
@@ -1079,6 +1184,18 @@ const char* mebp_workspace_slot_name(int32_t s) { return (s >= 0 && s < S_COUNT)
 
 const char* mebp_last_error(void) { return g_last_error.c_str(); }
 
+int mebp_set_workspace_guards(int32_t on) { return g_guards.exchange(on ? 1 : 0); }
+
+int mebp_workspace_guard_check(const mebp_config* cfg, int32_t B, int32_t T, void* ws, size_t ws_bytes,
+                               mebp_stream_t stream) {
+  int e;
+  if (!g_guards.load()) return fail(MEBP_EINVAL, "workspace guards are off");
+  if ((e = check_config(cfg)) || (e = check_shape(B, T)) || (e = check_ws(cfg, B, T, ws, ws_bytes))) return e;
+  Layout L;
+  make_layout(cfg, B, T, &L);
+  return guard_verdict(L, ws, (hipStream_t)stream);
+}
+
 int mebp_layer_forward_ckpt(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
                             const mebp_layer_lora* lora, const float* x_in, float* x_out, int32_t B, int32_t T,
                             void* ws, size_t ws_bytes, mebp_stream_t stream) {
@@ -1087,10 +1204,13 @@ int mebp_layer_forward_ckpt(const mebp_config* cfg, int32_t layer, const mebp_la
       (e = check_act(x_in, "x_in")) || (e = check_act(x_out, "x_out")) || (e = check_ws(cfg, B, T, ws, ws_bytes)))
     return e;
   if (x_in == x_out) return fail(MEBP_EINVAL, "x_out must not alias x_in");
-  Ctx x = make_ctx(cfg, B, T, ws, stream);
-  float* rope;
-  if ((e = rope_table(x, layer, &rope))) return e;
-  return layer_forward(x, layer, base, lora, x_in, x_out, rope, false);
+  return guarded(cfg, B, T, ws, stream, [&] {
+    Ctx x = make_ctx(cfg, B, T, ws, stream);
+    float* rope;
+    int e2;
+    if ((e2 = rope_table(x, layer, &rope))) return e2;
+    return layer_forward(x, layer, base, lora, x_in, x_out, rope, false);
+  });
 }
 
 int mebp_layer_recompute_backward(const mebp_config* cfg, int32_t layer, const mebp_layer_base* base,
@@ -1104,10 +1224,13 @@ int mebp_layer_recompute_backward(const mebp_config* cfg, int32_t layer, const m
     return e;
   if (dx && !aligned(dx, 16)) return fail(MEBP_EINVAL, "dx not 16-byte aligned");
   if (dx && dx == x_ckpt) return fail(MEBP_EINVAL, "dx must not alias x_ckpt");
-  Ctx x = make_ctx(cfg, B, T, ws, stream);
-  float* rope;
-  if ((e = rope_table(x, layer, &rope))) return e;
-  return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
+  return guarded(cfg, B, T, ws, stream, [&] {
+    Ctx x = make_ctx(cfg, B, T, ws, stream);
+    float* rope;
+    int e2;
+    if ((e2 = rope_table(x, layer, &rope))) return e2;
+    return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
+  });
 }
 
 }  // extern "C"
@@ -1159,10 +1282,13 @@ int mebp_layer_recompute_backward_static(const mebp_config* cfg, int32_t layer, 
                 (size_t)MEBP_STATIC_SCRATCH_BYTES);
   void* ws = static_scratch();
   if (!ws) return MEBP_EHIP;
-  Ctx x = make_ctx(&c0, B, T, ws, stream);
-  float* rope;
-  if ((e = rope_table(x, layer, &rope))) return e;
-  return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
+  return guarded(&c0, B, T, ws, stream, [&] {
+    Ctx x = make_ctx(&c0, B, T, ws, stream);
+    float* rope;
+    int e2;
+    if ((e2 = rope_table(x, layer, &rope))) return e2;
+    return layer_backward(x, layer, base, lora, x_ckpt, dy, dx, grads, rope);
+  });
 }
 
 int mebp_lm_head_ce_backward(const mebp_config* cfg, const mebp_q4* emb, const float* norm_final,
@@ -1177,8 +1303,10 @@ int mebp_lm_head_ce_backward(const mebp_config* cfg, const mebp_q4* emb, const f
     return e;
   if (!ids || !aligned(ids, 4)) return fail(MEBP_EINVAL, "ids NULL or misaligned");
   if (!loss || !aligned(loss, 4)) return fail(MEBP_EINVAL, "loss NULL or misaligned");
-  Ctx x = make_ctx(cfg, B, T, ws, stream);
-  return lm_head(x, emb, norm_final, x_last, ids, loss, dx_last, xs<bf16>(x, S_DYB));
+  return guarded(cfg, B, T, ws, stream, [&] {
+    Ctx x = make_ctx(cfg, B, T, ws, stream);
+    return lm_head(x, emb, norm_final, x_last, ids, loss, dx_last, xs<bf16>(x, S_DYB));
+  });
 }
 
 int mebp_embed(const mebp_config* cfg, const mebp_q4* emb, const int32_t* ids, int32_t B, int32_t T, float* x0,
@@ -1224,7 +1352,9 @@ int mebp_train_step(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer
   if ((e = check_train_args(cfg, emb, layers, norm_final, lora, ids, B, T, loss, grads, dx0, ws, ws_bytes)) ||
       (e = check_act(ckpt, "ckpt")))
     return e;
-  return train_step_impl(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt, nullptr, loss, grads, dx0, ws, stream);
+  return guarded(cfg, B, T, ws, stream, [&] {
+    return train_step_impl(cfg, emb, layers, norm_final, lora, ids, B, T, ckpt, nullptr, loss, grads, dx0, ws, stream);
+  });
 }
 
 int mebp_train_step_offload(const mebp_config* cfg, const mebp_q4* emb, const mebp_layer_base* layers,
@@ -1261,7 +1391,9 @@ int mebp_train_step_offload(const mebp_config* cfg, const mebp_q4* emb, const me
   }
   static std::mutex mu;  // the copy stream and its events are shared by the calls on a device
   std::lock_guard<std::mutex> g(mu);
-  return train_step_impl(cfg, emb, layers, norm_final, lora, ids, B, T, ring, &off, loss, grads, dx0, ws, stream);
+  return guarded(cfg, B, T, ws, stream, [&] {
+    return train_step_impl(cfg, emb, layers, norm_final, lora, ids, B, T, ring, &off, loss, grads, dx0, ws, stream);
+  });
 }
 
 int mebp_lora_grad_accumulate(const mebp_config* cfg, const mebp_layer_lora_grad* grads,

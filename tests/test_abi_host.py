@@ -227,3 +227,35 @@ def test_kernel_repeat_accepts_pure_kernels_and_switches_off(built_lib):
     for name in ("gemm_nt_f16out", "gemm_tn_probs_dh", "attn_fwd", "lora_rows"):
         assert built_lib.mebp_kernel_repeat(name.encode(), 3) == L.MEBP_OK
     assert built_lib.mebp_kernel_repeat(None, 1) == L.MEBP_OK
+
+
+def test_workspace_guard_mode_changes_the_layout_and_validates(built_lib):
+    c = make_config(MINI)
+    n = 0
+    while L.mebp_workspace_slot_name(n) is not None:
+        n += 1
+    plain = L.mebp_workspace_bytes(c, 2, 160)
+    offs = [L.mebp_workspace_offset(c, 2, 160, s) for s in range(n)]
+    r = L.mebp_workspace_guard_check(c, 2, 160, 256, plain, 0, check=False)
+    assert r == L.MEBP_EINVAL and "off" in L.mebp_last_error()
+    assert L.mebp_set_workspace_guards(True) is False
+    try:
+        guarded = L.mebp_workspace_bytes(c, 2, 160)
+        goffs = [L.mebp_workspace_offset(c, 2, 160, s) for s in range(n)]
+        # every slot and every second copy gains a guard region of at least 256 bytes, plus
+        # the status word's 256
+        assert guarded >= plain + 256 * (n + 1)
+        assert all(g >= o for g, o in zip(goffs, offs)) and all(g % 256 == 0 for g in goffs)
+        assert all(b - a >= 256 for a, b in zip(goffs, goffs[1:]))
+        # a workspace sized without the guards is refused, before anything is enqueued
+        r = L.mebp_layer_forward_ckpt(c, 0, None, None, 0, 0, 2, 160, 256, plain, 0, check=False)
+        assert r == L.MEBP_EINVAL  # base NULL is checked first
+        r = L.mebp_workspace_guard_check(c, 2, 160, 256, plain, 0, check=False)
+        assert r == L.MEBP_EWORKSPACE
+        r = L.mebp_workspace_guard_check(c, 2, 160, 0, guarded, 0, check=False)
+        assert r == L.MEBP_EINVAL
+        r = L.mebp_workspace_guard_check(c, 0, 160, 256, guarded, 0, check=False)
+        assert r == L.MEBP_EINVAL
+    finally:
+        assert L.mebp_set_workspace_guards(False) is True
+    assert L.mebp_workspace_bytes(c, 2, 160) == plain

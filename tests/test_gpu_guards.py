@@ -1,0 +1,112 @@
+"""Workspace guard debug mode on the GPU (mebp_set_workspace_guards).
+
+With the mode on, every workspace slot is followed by a guard region with a known pattern
+that each entry point fills before its kernels and checks after them. Here every entry point
+that takes a workspace runs guarded on the mini model: no kernel may write past its slot (the
+calls return MEBP_OK), and the results equal those of the unguarded calls bit for bit (the
+guards move the slots, not the arithmetic). Then one guard word is changed from the host
+(an ordinary in-bounds write into the workspace tensor) and the standalone check must name
+the slot it follows.
+"""
+import numpy as np
+import pytest
+import torch
+
+from mebp_inputs import MINI, layer_input, make_inputs
+from paper_2510_03425_amd import _lib as L
+from paper_2510_03425_amd.device import DeviceModel, ptr, slot_index, stream_handle
+
+from gpu_util import say
+
+pytestmark = pytest.mark.gpu
+
+
+class _Guards:
+    def __init__(self, on):
+        self.on = on
+
+    def __enter__(self):
+        self.prev = L.mebp_set_workspace_guards(self.on)
+
+    def __exit__(self, *exc):
+        L.mebp_set_workspace_guards(self.prev)
+
+
+def _every_entry_point(inp, gpu):
+    cfg = inp.cfg
+    dm = DeviceModel(inp, device=str(gpu))
+    out = {}
+    dx0 = torch.empty((dm.N, cfg.hidden), dtype=torch.float32, device=gpu)
+    say("train step", "ws bytes", dm.ws_bytes)
+    dm.train_step(dx0)
+    torch.cuda.synchronize()
+    out["step_loss"], out["step_dx0"], out["step_grads"] = dm.loss.clone(), dx0.clone(), dm.grad_probe().clone()
+    out["ckpt"] = dm.ckpt.clone()
+
+    say("offload train step")
+    ckpt_host = torch.empty((dm.L + 1, dm.N, cfg.hidden), dtype=torch.float32, pin_memory=True)
+    ring = torch.empty((4, dm.N, cfg.hidden), dtype=torch.float32, device=gpu)
+    dx0o = torch.empty_like(dx0)
+    dm.train_step_offload(ckpt_host, ring, dx0o)
+    torch.cuda.synchronize()
+    out["offload_loss"], out["offload_dx0"] = dm.loss.clone(), dx0o.clone()
+
+    x, dy = layer_input(cfg, 7)
+    tx, tdy = torch.from_numpy(x).to(gpu), torch.from_numpy(dy).to(gpu)
+    y = torch.empty_like(tx)
+    say("layer forward / backward, LM head")
+    dm.layer_forward(1, tx, y)
+    dx = torch.empty_like(tx)
+    dm.layer_backward(1, tx, tdy, dx)
+    torch.cuda.synchronize()
+    out["y"], out["dx"], out["layer_grads"] = y.clone(), dx.clone(), dm.grad_probe().clone()
+    dxl = torch.empty_like(tx)
+    dm.lm_head(tx, dxl)
+    torch.cuda.synchronize()
+    out["lm_loss"], out["lm_dx"] = dm.loss.clone(), dxl.clone()
+
+    say("static-scratch layer backward")
+    dxs = torch.empty_like(tx)
+    L.mebp_layer_recompute_backward_static(dm.ccfg, 0, dm.base[0], dm.lora[0], ptr(tx), ptr(tdy), ptr(dxs),
+                                           dm.grads[0], dm.B, dm.T, stream_handle())
+    torch.cuda.synchronize()
+    out["static_dx"], out["static_grads"] = dxs.clone(), dm.grad_probe().clone()
+    return dm, out
+
+
+def test_guarded_entry_points_pass_and_match_unguarded(built_lib, gpu):
+    inp = make_inputs(MINI, seed=4, norm="random")
+    with _Guards(False):
+        dm0, plain = _every_entry_point(inp, gpu)
+    with _Guards(True):
+        dm1, guarded = _every_entry_point(inp, gpu)
+    assert dm1.ws_bytes > dm0.ws_bytes
+    for k in plain:
+        assert torch.equal(plain[k], guarded[k]), k
+
+
+def test_overwritten_guard_is_named(built_lib, gpu):
+    inp = make_inputs(MINI, seed=5, norm="random")
+    with _Guards(True):
+        dm = DeviceModel(inp, device=str(gpu))
+        dx0 = torch.empty((dm.N, MINI.hidden), dtype=torch.float32, device=gpu)
+        say("guarded train step, then a changed guard word")
+        dm.train_step(dx0)
+        torch.cuda.synchronize()
+        L.mebp_workspace_guard_check(dm.ccfg, dm.B, dm.T, ptr(dm.ws), dm.ws_bytes, stream_handle())
+        for name in ("q", "lora_u", "logits"):
+            s = slot_index(name)
+            end = L.mebp_workspace_offset(dm.ccfg, dm.B, dm.T, s + 1)  # the guard of slot s ends here
+            word = dm.ws[end - 4:end].clone()
+            dm.ws[end - 4:end] = 255 - word
+            r = L.mebp_workspace_guard_check(dm.ccfg, dm.B, dm.T, ptr(dm.ws), dm.ws_bytes, stream_handle(),
+                                             check=False)
+            msg = L.mebp_last_error()
+            say(name, r, msg)
+            assert r == L.MEBP_EWORKSPACE and f"'{name}'" in msg and "second copy" not in msg
+            dm.ws[end - 4:end] = word
+            L.mebp_workspace_guard_check(dm.ccfg, dm.B, dm.T, ptr(dm.ws), dm.ws_bytes, stream_handle())
+        # the next guarded call refills the guards and passes
+        dm.train_step(dx0)
+        torch.cuda.synchronize()
+        assert np.isfinite(dm.loss.item())
