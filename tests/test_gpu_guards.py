@@ -110,3 +110,38 @@ def test_overwritten_guard_is_named(built_lib, gpu):
         dm.train_step(dx0)
         torch.cuda.synchronize()
         assert np.isfinite(dm.loss.item())
+
+
+def test_guarded_full_size_gemma3_4b_shapes(built_lib, gpu):
+    # the launch configuration of the Gemma3-4B-shaped step (8 x 2048 tokens): a sliding-
+    # window and a global layer, forward and backward, and the LM head over the whole
+    # vocabulary in chunks; guarded results equal the unguarded ones bit for bit
+    from mebp_inputs import CONFIGS
+    cfg = CONFIGS["gemma3-4b"]
+    layers = [0, cfg.global_every - 1]
+    say("draw layers and embedding", cfg.name, "B", cfg.batch, "T", cfg.seq)
+    inp = make_inputs(cfg, seed=3, norm="random", n_layers=max(layers) + 1)
+    x, dy = layer_input(cfg, 9)
+    tx, tdy = torch.from_numpy(x).to(gpu), torch.from_numpy(dy).to(gpu)
+    res = []
+    for on in (False, True):
+        with _Guards(on):
+            dm = DeviceModel(inp, device=str(gpu))
+            out = {}
+            for l in layers:
+                y, dx = torch.empty_like(tx), torch.empty_like(tx)
+                say("guards", on, "layer", l, "forward + backward")
+                dm.layer_forward(l, tx, y)
+                dm.layer_backward(l, tx, tdy, dx)
+                torch.cuda.synchronize()
+                out[f"y{l}"], out[f"dx{l}"] = y, dx
+                out[f"g{l}"] = torch.cat([t.reshape(-1) for d in (dm.dA[l], dm.dB[l]) for t in d.values()]).clone()
+            dxl = torch.empty_like(tx)
+            say("guards", on, "LM head")
+            dm.lm_head(tx, dxl)
+            torch.cuda.synchronize()
+            out["loss"], out["dxl"] = dm.loss.clone(), dxl
+            res.append(out)
+            del dm
+    for k in res[0]:
+        assert torch.equal(res[0][k], res[1][k]), k
