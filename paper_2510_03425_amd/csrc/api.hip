@@ -219,9 +219,12 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
     mx(attn_part_floats(B, T, c->n_heads, c->n_kv_heads, c->head_dim, 0));
     L->split_floats = m;
     sz[S_SPLIT] = m * 4;
+    // every dB / dA launch of a layer: (widest column count, jobs)
     size_t lp = 0;
-    for (size_t v : {lora_outer_part_floats(M, D > Q ? D : Q, R, 3), lora_outer_part_floats(M, FF > D ? FF : D, R, 2),
-                     lora_outer_part_floats(M, D, R, 1)})
+    for (size_t v : {lora_outer_part_floats(M, Q > KV ? Q : KV, R, 3), lora_outer_part_floats(M, D, R, 3),
+                     lora_outer_part_floats(M, D, R, 1), lora_outer_part_floats(M, Q, R, 1),
+                     lora_outer_part_floats(M, FF, R, 2), lora_outer_part_floats(M, D, R, 2),
+                     lora_outer_part_floats(M, FF, R, 1)})
       lp = v > lp ? v : lp;
     L->lora_part_floats = lp;
     sz[S_PART] = lp * 4;

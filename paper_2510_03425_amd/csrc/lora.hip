@@ -8,7 +8,7 @@
 // (A, B) and fp32 u / du enter the MFMA as a hi + lo pair of 16-bit values (two MFMAs),
 // which keeps their operand rounding near 2^-17 instead of 2^-9.
 //
-// "rows" keeps the whole reduction inside one workgroup (its 4 waves split K, partial
+// "rows" keeps the whole reduction inside one workgroup (its waves split K, partial
 // tiles summed through LDS in wave order). "outer" splits the token range over
 // blockIdx.z when there are many tokens; the split partials are then summed in split
 // order by a small reduce kernel. Both are deterministic.
@@ -33,31 +33,34 @@ DEV void split_hi_lo(const float (&f)[8], uint4& hi, uint4& lo) {
 }
 
 // ------------------------------------------------------------------------------ rows
-// out[m][j] = s * sum_k X[m][k] W(j,k); workgroup = 64 rows x 16 outputs of one job and
-// LR_WAVES waves that take interleaved 64-wide K super-steps (every row segment a lane
-// group loads is 128 contiguous bytes), two super-steps in flight per iteration; the
+// out[m][j] = s * sum_k X[m][k] W(j,k); workgroup = 64 rows x 16 outputs and LR_WAVES waves
+// that take interleaved 64-wide K super-steps (every row segment a lane group loads is 128
+// contiguous bytes), two super-steps in flight per iteration (one with three jobs); the
 // per-wave partial tiles are summed through LDS in wave order. The many waves keep enough
 // loads in flight to stream X near the HBM rate even with few row blocks.
+// NJ = 1: blockIdx.y selects the job. NJ > 1: the NJ jobs share X (the q, k, v or gate, up
+// down-projections of one normalised input), read once for all of them.
 constexpr int LR_ROWS = 64, LR_WAVES = 8;
-template <class Op>
+template <class Op, int NJ>
 __global__ __launch_bounds__(64 * LR_WAVES) void k_lora_rows(const LoraRowsArgs a) {
   __shared__ float red[LR_WAVES][LR_ROWS][17];
-  const LoraRowsJob& jb = a.job[blockIdx.y];
-  const u16* X = (const u16*)jb.X;
+  const int jb0 = NJ > 1 ? 0 : blockIdx.y;
+  const LoraRowsJob& jx = a.job[jb0];
+  const u16* X = (const u16*)jx.X;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int m0 = blockIdx.x * LR_ROWS, M = a.M, K = jb.K, r = a.r;
+  const int m0 = blockIdx.x * LR_ROWS, M = a.M, K = jx.K, r = a.r;
   const int nsup = (K + 63) / 64;
   const int j = lane & 15;
 
-  auto load_w = [&](int k, uint4& bh, uint4& bl) {
+  auto load_w = [&](const float* W, int k, uint4& bh, uint4& bl) {
     float f[8];
     if (k < K && j < r) {
       if (a.wt == 0) {
-        const float4 p = *(const float4*)(jb.W + (size_t)j * K + k), q = *(const float4*)(jb.W + (size_t)j * K + k + 4);
+        const float4 p = *(const float4*)(W + (size_t)j * K + k), q = *(const float4*)(W + (size_t)j * K + k + 4);
         f[0] = p.x; f[1] = p.y; f[2] = p.z; f[3] = p.w; f[4] = q.x; f[5] = q.y; f[6] = q.z; f[7] = q.w;
       } else {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) f[i] = jb.W[(size_t)(k + i) * r + j];
+        for (int i = 0; i < 8; ++i) f[i] = W[(size_t)(k + i) * r + j];
       }
     } else {
 #pragma unroll
@@ -73,68 +76,90 @@ __global__ __launch_bounds__(64 * LR_WAVES) void k_lora_rows(const LoraRowsArgs 
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int m = m0 + t * 16 + (lane & 15), kk = k + 32 * hh;
-        xv[hh][t] = (kk < K && m < M) ? *(const uint4*)(X + (size_t)m * jb.ldx + kk) : make_uint4(0, 0, 0, 0);
+        xv[hh][t] = (kk < K && m < M) ? *(const uint4*)(X + (size_t)m * jx.ldx + kk) : make_uint4(0, 0, 0, 0);
       }
   };
-  auto mma = [&](int k, const uint4 (&xv)[2][4], f32x4 (&acc)[4]) {
+  auto mma = [&](int k, const uint4 (&xv)[2][4], f32x4 (&acc)[NJ][4]) {
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      uint4 bh, bl;
-      load_w(k + 32 * hh, bh, bl);
+    for (int q = 0; q < NJ; ++q)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        acc[t] = mfma16_raw<Op>(xv[hh][t], bh, acc[t]);
-        acc[t] = mfma16_raw<Op>(xv[hh][t], bl, acc[t]);
+      for (int hh = 0; hh < 2; ++hh) {
+        uint4 bh, bl;
+        load_w(a.job[jb0 + q].W, k + 32 * hh, bh, bl);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          acc[q][t] = mfma16_raw<Op>(xv[hh][t], bh, acc[q][t]);
+          acc[q][t] = mfma16_raw<Op>(xv[hh][t], bl, acc[q][t]);
+        }
       }
-    }
   };
 
-  f32x4 acc[4];
+  f32x4 acc[NJ][4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int q = 0; q < NJ; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[q][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int ko = 8 * (lane >> 4);
-  for (int ss = w; ss < nsup; ss += 2 * LR_WAVES) {
-    const int k0 = ss * 64 + ko, k1 = (ss + LR_WAVES) * 64 + ko;
-    uint4 x0[2][4], x1[2][4];
-    load_x(k0, x0);
-    load_x(k1, x1);
-    mma(k0, x0, acc);
-    mma(k1, x1, acc);
+  if constexpr (NJ < 3) {
+    for (int ss = w; ss < nsup; ss += 2 * LR_WAVES) {
+      const int k0 = ss * 64 + ko, k1 = (ss + LR_WAVES) * 64 + ko;
+      uint4 x0[2][4], x1[2][4];
+      load_x(k0, x0);
+      load_x(k1, x1);
+      mma(k0, x0, acc);
+      mma(k1, x1, acc);
+    }
+  } else {
+    // three jobs' accumulators leave registers for one super-step in flight
+    for (int ss = w; ss < nsup; ss += LR_WAVES) {
+      const int k0 = ss * 64 + ko;
+      uint4 x0[2][4];
+      load_x(k0, x0);
+      mma(k0, x0, acc);
+    }
   }
-  // lane holds rows t*16 + 4g + rr, column j
+  // lane holds rows t*16 + 4g + rr, column j; one job at a time through the LDS tile
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int q = 0; q < NJ; ++q) {
+    if (q) __syncthreads();  // the previous job's sums have been read
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) red[w][t * 16 + 4 * (lane >> 4) + rr][j] = acc[t][rr];
-  __syncthreads();
-  for (int o = tid; o < LR_ROWS * 16; o += 64 * LR_WAVES) {
-    const int mm = o >> 4, jj = o & 15, m = m0 + mm;
-    if (m < M && jj < r) {
-      float v = 0.f;
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int ww = 0; ww < LR_WAVES; ++ww) v += red[ww][mm][jj];
-      jb.out[(size_t)m * r + jj] = a.s * v;
+      for (int rr = 0; rr < 4; ++rr) red[w][t * 16 + 4 * (lane >> 4) + rr][j] = acc[q][t][rr];
+    __syncthreads();
+    float* out = a.job[jb0 + q].out;
+    for (int o = tid; o < LR_ROWS * 16; o += 64 * LR_WAVES) {
+      const int mm = o >> 4, jj = o & 15, m = m0 + mm;
+      if (m < M && jj < r) {
+        float v = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < LR_WAVES; ++ww) v += red[ww][mm][jj];
+        out[(size_t)m * r + jj] = a.s * v;
+      }
     }
   }
 }
 
 // ----------------------------------------------------------------------------- outer
-// R(c, j) = s * sum_m Mx[m][c] V[m][j]; workgroup = 128 columns c x 16 j of one job (each
-// wave 32 c); per iteration 64 tokens are staged transposed in LDS (c-major,
-// token-contiguous) together with V^T as hi/lo planes. The products run in bf16 (V may be
-// a tiny gradient); an fp16 Mx is converted to bf16 while staged. The LDS tiles are
-// double-buffered and the next iteration's tokens are loaded into registers while the
-// current ones are multiplied, so one barrier per iteration suffices and loads overlap.
+// R(c, j) = s * sum_m Mx[m][c] V[m][j]; workgroup = 128 columns c x 16 j (each wave 32 c);
+// per iteration 64 tokens are staged transposed in LDS (c-major, token-contiguous) together
+// with V^T as hi/lo planes. The products run in bf16 (V may be a tiny gradient); an fp16 Mx
+// is converted to bf16 while staged. The LDS tiles are double-buffered and the next
+// iteration's tokens are loaded into registers while the current ones are multiplied, so
+// one barrier per iteration suffices and loads overlap.
+// NJ = 1: blockIdx.y selects the job. NJ > 1: the NJ jobs share Mx (dA of q, k, v or of
+// gate, up: one layer input against each projection's du), staged once for all of them.
 constexpr int LO_C = 128, LO_M = 64, LO_LD = LO_M + 8;
-template <bool MX_F16>
+template <bool MX_F16, int NJ>
 __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
   __shared__ __attribute__((aligned(16))) u16 Mt[2][LO_C * LO_LD];
-  __shared__ __attribute__((aligned(16))) u16 Vh[2][16 * LO_LD];
-  __shared__ __attribute__((aligned(16))) u16 Vl[2][16 * LO_LD];
-  const LoraOuterJob& jb = a.job[blockIdx.y];
-  const u16* Mx = (const u16*)jb.Mx;
+  __shared__ __attribute__((aligned(16))) u16 Vh[2][NJ][16 * LO_LD];
+  __shared__ __attribute__((aligned(16))) u16 Vl[2][NJ][16 * LO_LD];
+  const int jb0 = NJ > 1 ? 0 : blockIdx.y;
+  const LoraOuterJob& jx = a.job[jb0];
+  const u16* Mx = (const u16*)jx.Mx;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int C = jb.C, M = a.M, r = a.r;
+  const int C = jx.C, M = a.M, r = a.r;
   const int c0 = blockIdx.x * LO_C, ms = blockIdx.z, MS = gridDim.z;
   if (c0 >= C) return;
   const int nsteps = (M + LO_M - 1) / LO_M;
@@ -144,7 +169,7 @@ __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
   const int rb = tid & 7, cb = (tid >> 3) & 15;      // Mx role: token block, column block
   const int jv = (tid - 128) & 15, mq = (tid - 128) >> 4;  // V role: output j, token group
   uint32_t in[8][4];
-  float f[8];
+  float f[NJ][8];
   auto load = [&](int st) {
     const int mb = st * LO_M;
     if (mx_role) {
@@ -152,15 +177,17 @@ __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
       for (int i = 0; i < 8; ++i) {
         const int m = mb + rb * 8 + i, c = c0 + cb * 8;
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (m < M && c < C) v = *(const uint4*)(Mx + (size_t)m * jb.ldm + c);
+        if (m < M && c < C) v = *(const uint4*)(Mx + (size_t)m * jx.ldm + c);
         in[i][0] = v.x; in[i][1] = v.y; in[i][2] = v.z; in[i][3] = v.w;
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int m = mb + mq * 8 + i;
-        f[i] = (m < M && jv < r) ? jb.V[(size_t)m * r + jv] : 0.f;
-      }
+      for (int q = 0; q < NJ; ++q)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int m = mb + mq * 8 + i;
+          f[q][i] = (m < M && jv < r) ? a.job[jb0 + q].V[(size_t)m * r + jv] : 0.f;
+        }
     }
   };
   auto store = [&](int buf) {
@@ -185,13 +212,18 @@ __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
         *(uint4*)(Mt[buf] + (cb * 8 + jc) * LO_LD + rb * 8) = o;
       }
     } else {
-      uint4 hi, lo;
-      split_hi_lo<OpBF16>(f, hi, lo);
-      *(uint4*)(Vh[buf] + jv * LO_LD + mq * 8) = hi;
-      *(uint4*)(Vl[buf] + jv * LO_LD + mq * 8) = lo;
+#pragma unroll
+      for (int q = 0; q < NJ; ++q) {
+        uint4 hi, lo;
+        split_hi_lo<OpBF16>(f[q], hi, lo);
+        *(uint4*)(Vh[buf][q] + jv * LO_LD + mq * 8) = hi;
+        *(uint4*)(Vl[buf][q] + jv * LO_LD + mq * 8) = lo;
+      }
     }
   };
-  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  f32x4 acc[NJ][2];
+#pragma unroll
+  for (int q = 0; q < NJ; ++q) acc[q][0] = acc[q][1] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (sb < se) load(sb);
   for (int st = sb; st < se; ++st) {
     const int buf = (st - sb) & 1;
@@ -200,29 +232,40 @@ __global__ __launch_bounds__(256) void k_lora_outer(const LoraOuterArgs a) {
     if (st + 1 < se) load(st + 1);
 #pragma unroll
     for (int kk = 0; kk < LO_M; kk += 32) {
-      const uint4 bh = *(const uint4*)(Vh[buf] + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
-      const uint4 bl = *(const uint4*)(Vl[buf] + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
+      uint4 av[2];
 #pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
-        const uint4 av = *(const uint4*)(Mt[buf] + (w * 32 + ct * 16 + (lane & 15)) * LO_LD + kk + 8 * (lane >> 4));
-        acc[ct] = mfma16_raw<OpBF16>(av, bh, acc[ct]);
-        acc[ct] = mfma16_raw<OpBF16>(av, bl, acc[ct]);
+      for (int ct = 0; ct < 2; ++ct)
+        av[ct] = *(const uint4*)(Mt[buf] + (w * 32 + ct * 16 + (lane & 15)) * LO_LD + kk + 8 * (lane >> 4));
+#pragma unroll
+      for (int q = 0; q < NJ; ++q) {
+        const uint4 bh = *(const uint4*)(Vh[buf][q] + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
+        const uint4 bl = *(const uint4*)(Vl[buf][q] + (lane & 15) * LO_LD + kk + 8 * (lane >> 4));
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+          acc[q][ct] = mfma16_raw<OpBF16>(av[ct], bh, acc[q][ct]);
+          acc[q][ct] = mfma16_raw<OpBF16>(av[ct], bl, acc[q][ct]);
+        }
       }
     }
   }
   // lane holds R rows c = c0 + w*32 + ct*16 + 4g + rr, column j = lane%16
   const int j = lane & 15;
 #pragma unroll
-  for (int ct = 0; ct < 2; ++ct)
+  for (int q = 0; q < NJ; ++q) {
+    const LoraOuterJob& jb = a.job[jb0 + q];
+    const int y = jb0 + q;
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int c = c0 + w * 32 + ct * 16 + 4 * (lane >> 4) + rr;
-      if (c >= C || j >= r) continue;
-      if (MS > 1)
-        a.part[(((size_t)blockIdx.y * MS + ms) * a.cmax + c) * r + j] = acc[ct][rr];
-      else
-        jb.out[a.layout == 0 ? (size_t)c * r + j : (size_t)j * C + c] = jb.s * acc[ct][rr];
-    }
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int c = c0 + w * 32 + ct * 16 + 4 * (lane >> 4) + rr;
+        if (c >= C || j >= r) continue;
+        if (MS > 1)
+          a.part[(((size_t)y * MS + ms) * a.cmax + c) * r + j] = acc[q][ct][rr];
+        else
+          jb.out[a.layout == 0 ? (size_t)c * r + j : (size_t)j * C + c] = jb.s * acc[q][ct][rr];
+      }
+  }
 }
 
 // sum the token-split partials of every job in split order and write with layout / scale
@@ -242,8 +285,10 @@ __global__ void k_fill_i32(int* p, int n, int v) {
   if (i < n) p[i] = v;
 }
 
-int outer_splits(int M, int cmax, int njobs) {
-  const int cb = ((cmax + LO_C - 1) / LO_C) * njobs, steps = (M + LO_M - 1) / LO_M;
+// token splits of an outer launch with `groups` workgroup columns per split (column blocks
+// times the jobs that do not share their input)
+int outer_splits(int M, int cmax, int groups) {
+  const int cb = ((cmax + LO_C - 1) / LO_C) * groups, steps = (M + LO_M - 1) / LO_M;
   if (steps < 16) return 1;
   int s = (256 + cb - 1) / cb;
   if (s > steps / 4) s = steps / 4;
@@ -251,45 +296,66 @@ int outer_splits(int M, int cmax, int njobs) {
   return s < 1 ? 1 : s;
 }
 
+// jobs that read the same input (pointer, leading dimension and width) run in one workgroup
+template <class J>
+bool same_input(const J* job, int n, const void* J::*x, int J::*ld, int J::*w) {
+  for (int i = 1; i < n; ++i)
+    if (job[i].*x != job[0].*x || job[i].*ld != job[0].*ld || job[i].*w != job[0].*w) return false;
+  return n > 1;
+}
+
 }  // namespace
 
 size_t lora_outer_part_floats(int M, int cmax, int r, int njobs) {
-  const int s = outer_splits(M, cmax, njobs);
+  // the most splits any grouping of the jobs uses (one workgroup column group per split)
+  const int s = outer_splits(M, cmax, 1);
   return s > 1 ? (size_t)njobs * s * cmax * r : 0;
 }
 
 hipError_t launch_lora_rows(const LoraRowsArgs& a, int xbf16, hipStream_t st) {
-  dim3 grid((a.M + LR_ROWS - 1) / LR_ROWS, a.njobs);
+  const bool shared = same_input(a.job, a.njobs, &LoraRowsJob::X, &LoraRowsJob::ldx, &LoraRowsJob::K);
+  dim3 grid((a.M + LR_ROWS - 1) / LR_ROWS, shared ? 1 : a.njobs);
   double flops = 0, bytes = 0;
   for (int i = 0; i < a.njobs; ++i) {
     flops += 2.0 * a.M * a.job[i].K * a.r;
-    bytes += (double)a.M * a.job[i].K * 2 + (double)a.job[i].K * a.r * 4 + (double)a.M * a.r * 4;
+    bytes += (i == 0 || !shared ? (double)a.M * a.job[i].K * 2 : 0.0) + (double)a.job[i].K * a.r * 4 +
+             (double)a.M * a.r * 4;
   }
-  if (xbf16)
-    MEBP_TIMED(st, "lora_rows", flops, bytes,
-               hipLaunchKernelGGL(k_lora_rows<OpBF16>, grid, dim3(64 * LR_WAVES), 0, st, a));
-  else
-    MEBP_TIMED(st, "lora_rows", flops, bytes,
-               hipLaunchKernelGGL(k_lora_rows<OpF16>, grid, dim3(64 * LR_WAVES), 0, st, a));
+  const dim3 blk(64 * LR_WAVES);
+#define LR_GO(OP, NJ) MEBP_TIMED(st, "lora_rows", flops, bytes, hipLaunchKernelGGL((k_lora_rows<OP, NJ>), grid, blk, 0, st, a))
+  const int nj = shared ? a.njobs : 1;
+  if (xbf16) {
+    if (nj == 3) LR_GO(OpBF16, 3); else if (nj == 2) LR_GO(OpBF16, 2); else LR_GO(OpBF16, 1);
+  } else {
+    if (nj == 3) LR_GO(OpF16, 3); else if (nj == 2) LR_GO(OpF16, 2); else LR_GO(OpF16, 1);
+  }
+#undef LR_GO
   return hipGetLastError();
 }
 
 hipError_t launch_lora_outer(const LoraOuterArgs& a0, int mbf16, hipStream_t st) {
   LoraOuterArgs a = a0;
+  const bool shared = same_input(a.job, a.njobs, &LoraOuterJob::Mx, &LoraOuterJob::ldm, &LoraOuterJob::C);
   a.cmax = 0;
   double flops = 0, bytes = 0;
   for (int i = 0; i < a.njobs; ++i) {
     a.cmax = a.job[i].C > a.cmax ? a.job[i].C : a.cmax;
     flops += 2.0 * a.M * a.job[i].C * a.r;
-    bytes += (double)a.M * a.job[i].C * 2 + (double)a.M * a.r * 4 + (double)a.job[i].C * a.r * 4;
+    bytes += (i == 0 || !shared ? (double)a.M * a.job[i].C * 2 : 0.0) + (double)a.M * a.r * 4 +
+             (double)a.job[i].C * a.r * 4;
   }
-  int MS = outer_splits(a.M, a.cmax, a.njobs);
+  const int groups = shared ? 1 : a.njobs;
+  int MS = outer_splits(a.M, a.cmax, groups);
   if (MS > 1 && (!a.part || a.part_floats < (size_t)a.njobs * MS * a.cmax * a.r)) MS = 1;
-  dim3 grid((a.cmax + LO_C - 1) / LO_C, a.njobs, MS);
-  if (mbf16)
-    MEBP_TIMED(st, "lora_outer", flops, bytes, hipLaunchKernelGGL(k_lora_outer<false>, grid, dim3(256), 0, st, a));
-  else
-    MEBP_TIMED(st, "lora_outer", flops, bytes, hipLaunchKernelGGL(k_lora_outer<true>, grid, dim3(256), 0, st, a));
+  dim3 grid((a.cmax + LO_C - 1) / LO_C, groups, MS);
+  const int nj = shared ? a.njobs : 1;
+#define LO_GO(F16, NJ) MEBP_TIMED(st, "lora_outer", flops, bytes, hipLaunchKernelGGL((k_lora_outer<F16, NJ>), grid, dim3(256), 0, st, a))
+  if (mbf16) {
+    if (nj == 3) LO_GO(false, 3); else if (nj == 2) LO_GO(false, 2); else LO_GO(false, 1);
+  } else {
+    if (nj == 3) LO_GO(true, 3); else if (nj == 2) LO_GO(true, 2); else LO_GO(true, 1);
+  }
+#undef LO_GO
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || MS == 1) return e;
   dim3 rg((a.cmax * a.r + 255) / 256, a.njobs);
