@@ -52,14 +52,14 @@ enum Slot {
   S_A, S_Q, S_K, S_V, S_O, S_LSE, S_H, S_C, S_G, S_U, S_Z, S_LU, S_LDU, S_DYB, S_DC, S_DH, S_DHB, S_DO,
   S_DELTA, S_DQ, S_DK, S_DV, S_DA, S_PART, S_ROPE_G, S_ROPE_L, S_TGT, S_HF, S_LOGITS, S_STATS, S_LSEV,
   S_TGTLOGIT, S_ROWLOSS, S_DHF, S_LMPART, S_GRAD, S_SPLIT, S_QPRE, S_KPRE, S_TO, S_TD, S_DTB, S_DTOB, S_CEMAX,
-  S_CESUM, S_CEALPHA, S_COUNT
+  S_CESUM, S_CEALPHA, S_W16, S_COUNT
 };
 const char* kSlotNames[S_COUNT] = {
   "a", "q", "k", "v", "o", "lse", "h", "c", "g", "u", "z", "lora_u", "lora_du", "dy_bf16", "dc", "dh",
   "dh_bf16", "do", "delta", "dq", "dk", "dv", "da", "lora_part", "rope_global", "rope_local", "targets",
   "hf", "logits", "ce_stats", "ce_lse", "ce_target_logit", "ce_row_loss", "dhf", "lm_part", "grad", "split_part",
   "q_prenorm", "k_prenorm", "attn_out_prenorm", "mlp_out_prenorm", "d_mlp_out_bf16", "d_attn_out_bf16", "ce_max",
-  "ce_sum", "ce_alpha"};
+  "ce_sum", "ce_alpha", "w16"};
 
 // Slots written by a layer's (re)computed forward and read by its backward, plus the
 // split-K scratch: the training step keeps two copies, so that the recompute of layer l-1
@@ -105,6 +105,7 @@ struct Layout {
   int ntiles;     // statistics tiles of a whole chunk (the stats row pitch)
   size_t split_floats;
   size_t lora_part_floats;
+  size_t w16_elems;  // transient bf16 weights of the large-tile transposed products
 };
 
 size_t nt_part(int M, int K, std::initializer_list<int> Ns) {
@@ -228,6 +229,16 @@ bool make_layout(const mebp_config* c, int B, int T, Layout* L) {
       lp = v > lp ? v : lp;
     L->lora_part_floats = lp;
     sz[S_PART] = lp * 4;
+    // the transposed products of the backward (down, gate + up, o, q + k + v) and the LM
+    // head's dH product over one vocabulary chunk, one at a time
+    size_t w = 0;
+    const int n_down[1] = {D}, n_gu[2] = {FF, FF}, n_o[1] = {D}, n_qkv[3] = {Q, KV, KV}, n_lm[1] = {(int)Vc};
+    for (size_t v : {gemm_tn_w16_elems(M, FF, n_down, 1, false), gemm_tn_w16_elems(M, D, n_gu, 2, false),
+                     gemm_tn_w16_elems(M, Q, n_o, 1, false), gemm_tn_w16_elems(M, D, n_qkv, 3, false),
+                     V ? gemm_tn_w16_elems(M, D, n_lm, 1, true) : (size_t)0})
+      w = v > w ? v : w;
+    L->w16_elems = w;
+    sz[S_W16] = w * 2;
   }
   size_t o = 0;
   L->guards = g_guards.load() != 0;
@@ -516,6 +527,9 @@ void set_scratch(const Ctx& x, TnArgs& t) {
   const SplitScratch sc = split_scratch(x);
   t.part = sc.part;
   t.part_floats = sc.part_floats;
+  // one copy: the transposed products run on the context's main stream, one after another
+  t.w16 = slot<uint16_t>(x.ws, x.L, S_W16);
+  t.w16_elems = x.L.w16_elems;
 }
 
 TnSeg tn_seg(const Ctx& x, const mebp_layer_base* base, const mebp_layer_lora* lora, int p, const bf16* G) {
@@ -883,6 +897,7 @@ int lm_head(const Ctx& x, const mebp_q4* emb, const float* norm_final, const flo
       t.seg[0].G = (const bf16*)logits; t.seg[0].ldg = Vc;
       t.seg[0].q4 = eq4; t.seg[0].scale = esc; t.seg[0].N = w;
       t.out = part; t.ldo = d; t.splits = lm_head_splits(N, d, w);
+      t.w16 = slot<uint16_t>(x.ws, x.L, S_W16); t.w16_elems = x.L.w16_elems;
       HIP_TRY(launch_gemm_tn(t, TN_PARTIAL_F32, TN_A_BF16, x.st));
       HIP_TRY(launch_ce_dh_accum(part, t.splits, N, d, alpha, first, dhf, x.st));
     }

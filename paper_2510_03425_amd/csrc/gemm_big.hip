@@ -771,9 +771,10 @@ DEV void sched_tn_step() {
   }
 }
 
-// W16: the weights are plain bf16 values [N][Kout] (seg.q4 points at them, no scales), copied
-// into the transposed LDS tile without decompression: the same kernel without the
-// decompression, for measuring its cost (W16 = false is the production kernel).
+// W16: the weights are bf16 values [N][Kout] (seg.q4 points at them, no scales), moved into
+// the transposed LDS tile without decompression. The training path uses it on a transient
+// copy that a decompression pass writes just before (the same operands as the int4 kernel,
+// with the conversion's VALU work taken out of the main loop).
 template <int BN, int EPI, bool W16 = false>
 __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   constexpr int NJ = BN / 64;
@@ -867,15 +868,30 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
     auto sstore = [&](auto S_, auto B_) {
       constexpr int st = decltype(S_)::value, bf = decltype(B_)::value;
       store_a_tile(As2[bf], tid, ra[st]);
-      float v[RPT][16];
+      if constexpr (W16) {
+        // bf16 weights: column e of rows i, i+1 is one 16-bit permute of their words
+        uint32_t wd[RPT][8];
 #pragma unroll
-      for (int i = 0; i < RPT; ++i) {
-        if constexpr (W16) {
-          const uint32_t wd[8] = {rw16[st][i][0].x, rw16[st][i][0].y, rw16[st][i][0].z, rw16[st][i][0].w,
-                                  rw16[st][i][1].x, rw16[st][i][1].y, rw16[st][i][1].z, rw16[st][i][1].w};
+        for (int i = 0; i < RPT; ++i) {
+          wd[i][0] = rw16[st][i][0].x; wd[i][1] = rw16[st][i][0].y; wd[i][2] = rw16[st][i][0].z;
+          wd[i][3] = rw16[st][i][0].w; wd[i][4] = rw16[st][i][1].x; wd[i][5] = rw16[st][i][1].y;
+          wd[i][6] = rw16[st][i][1].z; wd[i][7] = rw16[st][i][1].w;
+        }
+        auto pair = [&](int i, int e) {
+          return (e & 1) ? perm_hi16(wd[i][e >> 1], wd[i + 1][e >> 1]) : perm_lo16(wd[i][e >> 1], wd[i + 1][e >> 1]);
+        };
 #pragma unroll
-          for (int e = 0; e < 16; ++e) v[i][e] = (e & 1) ? bf16_hi(wd[e >> 1]) : bf16_lo(wd[e >> 1]);
-        } else {
+        for (int e = 0; e < 16; ++e) {
+          u16* dst = Bs2[bf] + (16 * cq + e) * LDT + RPT * rq;
+          if constexpr (RPT == 4)
+            *(uint2*)dst = make_uint2(pair(0, e), pair(2, e));
+          else
+            *(uint32_t*)dst = pair(0, e);
+        }
+      } else {
+        float v[RPT][16];
+#pragma unroll
+        for (int i = 0; i < RPT; ++i) {
           const float sc = half_bits_to_f32((uint16_t)rsc[st][i]);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -883,14 +899,14 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
             v[i][8 + e] = (float)nib_s(rw[st][i].y, e) * sc;
           }
         }
-      }
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        u16* dst = Bs2[bf] + (16 * cq + e) * LDT + RPT * rq;
-        if constexpr (RPT == 4)
-          *(uint2*)dst = make_uint2(pack_bf16x2(v[0][e], v[1][e]), pack_bf16x2(v[2][e], v[3][e]));
-        else
-          *(uint32_t*)dst = pack_bf16x2(v[0][e], v[1][e]);
+        for (int e = 0; e < 16; ++e) {
+          u16* dst = Bs2[bf] + (16 * cq + e) * LDT + RPT * rq;
+          if constexpr (RPT == 4)
+            *(uint2*)dst = make_uint2(pack_bf16x2(v[0][e], v[1][e]), pack_bf16x2(v[2][e], v[3][e]));
+          else
+            *(uint32_t*)dst = pack_bf16x2(v[0][e], v[1][e]);
+        }
       }
     };
     auto step = [&](auto I_, int t) {
@@ -1122,15 +1138,20 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
 }
 
 hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S, double flops, double bytes,
-                              hipStream_t st) {
+                              hipStream_t st, bool w16) {
   const dim3 grid((a.Kout + bn - 1) / bn, (a.M + BM - 1) / BM, S);
   if (amode != TN_A_BF16) return hipErrorInvalidValue;
   const char* name = epi == TN_PARTIAL_F32 ? "gemm_tn_probs_dh"
                      : epi == TN_STORE_F32  ? "gemm_tn_f32out"
                      : epi == TN_ACT_BWD    ? "gemm_tn_act_bwd"
                                             : "gemm_tn_bf16out";
-#define TN_BIG(BN_, EPI_) \
-  MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_big<BN_, EPI_>), grid, dim3(NTH), 0, st, a))
+#define TN_BIG(BN_, EPI_)                                                                                    \
+  do {                                                                                                       \
+    if (w16)                                                                                                 \
+      MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_big<BN_, EPI_, true>), grid, dim3(NTH), 0, st, a)); \
+    else                                                                                                     \
+      MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_big<BN_, EPI_>), grid, dim3(NTH), 0, st, a));       \
+  } while (0)
 #define TN_BIG_EPI(BN_)                     \
   do {                                      \
     if (epi == TN_STORE_F32) {              \

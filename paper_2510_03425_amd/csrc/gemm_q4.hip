@@ -961,6 +961,13 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st, hipEvent_t 
   return hipGetLastError();
 }
 
+size_t gemm_tn_w16_elems(int M, int Kout, const int* Ns, int nseg, bool softmax) {
+  if (!plan_tn(M, Kout, Ns, nseg, softmax).big) return 0;
+  size_t n = 0;
+  for (int s = 0; s < nseg; ++s) n += (size_t)Ns[s] * Kout;
+  return n;
+}
+
 hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, hipEvent_t lora_ready) {
   if (amode != TN_A_BF16) return hipErrorInvalidValue;
   if (a0.delta && (epi != TN_STORE_BF16 || !a0.delta_o || a0.delta_T <= 0 || a0.M % a0.delta_T ||
@@ -991,12 +998,31 @@ hipError_t launch_gemm_tn(const TnArgs& a0, int epi, int amode, hipStream_t st, 
   bytes += epi == TN_STORE_BF16 ? 2 * outb : epi == TN_ACT_BWD ? 8 * outb
          : epi == TN_PARTIAL_F32 ? 4 * outb * S : 4 * outb;
   dim3 grid(ct, mt, S);
+  // the large-tile kernel on a transient bf16 copy of the weights (written before the wait
+  // for the LoRA projection, so the two may overlap)
+  bool w16 = false;
+  if (plan.big && a.w16) {
+    size_t need = 0;
+    for (int s = 0; s < a.nseg; ++s) need += (size_t)a.seg[s].N * a.Kout;
+    if (need <= a.w16_elems) {
+      size_t off = 0;
+      for (int s = 0; s < a.nseg; ++s) {
+        const hipError_t ed =
+            launch_dequant(a.seg[s].q4, a.seg[s].scale, a.seg[s].N, a.Kout, 32, nullptr, a.w16 + off, st);
+        if (ed != hipSuccess) return ed;
+        a.seg[s].q4 = reinterpret_cast<const uint8_t*>(a.w16 + off);
+        a.seg[s].scale = nullptr;
+        off += (size_t)a.seg[s].N * a.Kout;
+      }
+      w16 = true;
+    }
+  }
   if (lora_ready && S == 1) {
     const hipError_t ew = hipStreamWaitEvent(st, lora_ready, 0);
     if (ew != hipSuccess) return ew;
   }
   if (plan.big) {
-    hipError_t eb = launch_gemm_tn_big(a, epi, amode, plan.bn, S, flops, bytes, st);
+    hipError_t eb = launch_gemm_tn_big(a, epi, amode, plan.bn, S, flops, bytes, st, w16);
     if (eb != hipSuccess) return eb;
   } else {
     switch (epi) {

@@ -131,10 +131,20 @@ struct TnArgs {
   float* out2;
   bf16* out2b;
   float eps;
+  // optional scratch for a transient bf16 copy of the segments' weights: when the large-tile
+  // kernel is chosen and sum_seg N_seg * Kout <= w16_elems, the weights are decompressed
+  // into it first (bf16 of q * s, rounded to nearest even, [N_seg][Kout] back to back) and
+  // the kernel reads them without decompressing (identical operands, identical results)
+  uint16_t* w16;
+  size_t w16_elems;
 };
 hipError_t launch_gemm_tn(const TnArgs& a, int epi, int amode, hipStream_t st, hipEvent_t lora_ready = nullptr);
+// w16: seg.q4 points at bf16 weights [N][Kout] (no scales)
 hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S, double flops, double bytes,
-                              hipStream_t st);
+                              hipStream_t st, bool w16 = false);
+// bf16 elements of the transient weight copy that launch_gemm_tn would use for these
+// segments (0 when the large-tile kernel is not chosen)
+size_t gemm_tn_w16_elems(int M, int Kout, const int* Ns, int nseg, bool softmax);
 
 // Test aid: one production GEMM kernel chosen by `kind` (the MEBP_TEST_GEMM_* values of the
 // C ABI) on caller operands, one split, no LoRA term or residual, fp32 outputs. Forward
