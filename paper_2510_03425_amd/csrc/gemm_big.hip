@@ -688,25 +688,54 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
         sc[j] = f16x2{v, v};
       }
     }
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    auto rd = [&](int t, uint4 (&dst)[4]) {
       const int pos = ((4 * h + t) ^ ((lane >> 1) & 7)) * 16;
-      uint4 af[4], bfr[NJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = *(const uint4*)(As + 4096 * i + pos);
+      for (int i = 0; i < 4; ++i) dst[i] = *(const uint4*)(As + 4096 * i + pos);
+    };
+    if constexpr (W16) {
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        if constexpr (W16) {
-          bfr[j] = wr.rw[st][j][t];
-        } else {
-          const uint32_t w = t == 0 ? wr.rb[st][j].x : t == 1 ? wr.rb[st][j].y : t == 2 ? wr.rb[st][j].z : wr.rb[st][j].w;
-          bfr[j] = dequant8_natural(w, sc[j]);
-        }
+      for (int t = 0; t < 4; ++t) {
+        uint4 af[4];
+        rd(t, af);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpF16>(af[i], wr.rw[st][j][t], acc[i][j]);
       }
+    } else {
+      // software pipeline over the four substeps: the fragments of substep t + 1 are read,
+      // and its weights decompressed, while the MFMAs of substep t run (scheduling barriers
+      // keep the compiler from moving the reads next to their use; the decompression is
+      // interleaved one MFMA to five VALU instructions)
+      uint4 af[2][4], bq[2][NJ];
+      auto dq = [&](int t, uint4 (&dst)[NJ]) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < NJ; ++j) {
+          const uint32_t w = t == 0 ? wr.rb[st][j].x : t == 1 ? wr.rb[st][j].y : t == 2 ? wr.rb[st][j].z : wr.rb[st][j].w;
+          dst[j] = dequant8_natural(w, sc[j]);
+        }
+      };
+      rd(0, af[0]);
+      dq(0, bq[0]);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpF16>(af[i], bfr[j], acc[i][j]);
+      for (int t = 0; t < 4; ++t) {
+        if (t < 3) rd(t + 1, af[(t + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (t < 3) dq(t + 1, bq[(t + 1) & 1]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpF16>(af[t & 1][i], bq[t & 1][j], acc[i][j]);
+        if (t < 3) {
+#pragma unroll
+          for (int q = 0; q < 4 * NJ; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // five VALU
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   };
   // Step of tile k (ring stage I): issue the loads of tile k+2 into stage I+2 (last read by
