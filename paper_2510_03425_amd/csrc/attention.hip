@@ -386,23 +386,29 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
   const VisRange kvis = keys_of_query(q, T, a.window);
 
   uint4 kr[KCH], vr[VBL][8];
+  // K / V rows of this sequence and KV head as buffer resources: rows past T read as zero;
+  // each load is one per-lane offset fixed for the kernel plus a wave-uniform row offset
+  const size_t kvbytes = ((size_t)(T - 1) * a.ldk + DH) * 2;
+  const rsrc_t rK = make_rsrc((const u16*)a.k + rowb * a.ldk + kvh * DH, kvbytes);
+  const rsrc_t rV = make_rsrc((const u16*)a.v + rowb * a.ldk + kvh * DH, kvbytes);
+  const uint32_t rowB = (uint32_t)a.ldk * 2;
+  // K: chunk c = tid + NTH i is row c / (DH/8) = tid / (DH/8) + i NTH / (DH/8), column (c % (DH/8)) 8
+  const uint32_t offK = (uint32_t)(((tid / (DH / 8)) * a.ldk + (tid % (DH / 8)) * 8) * 2);
+  // V: block bl = tid + NTH i, rows 8 (bl % (KB/8)) + j, columns 8 (bl / (KB/8))
+  uint32_t offV[VBL];
+#pragma unroll
+  for (int i = 0; i < VBL; ++i) {
+    const int bl = min(tid + NTH * i, NVB - 1);
+    offV[i] = (uint32_t)((((bl % (KB / 8)) * 8) * a.ldk + (bl / (KB / 8)) * 8) * 2);
+  }
   auto gload = [&](int kv0) {
-    const u16* kb = (const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH;
-    const u16* vb = (const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH;
+    const uint32_t s0 = (uint32_t)kv0 * rowB;
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + NTH * i, r = c / (DH / 8), col = (c % (DH / 8)) * 8;
-      kr[i] = load_frag_global(kb + (size_t)r * a.ldk + col, kv0 + r < T);
-    }
+    for (int i = 0; i < KCH; ++i) kr[i] = bload128s(rK, offK, s0 + (uint32_t)(i * (NTH / (DH / 8))) * rowB);
 #pragma unroll
-    for (int i = 0; i < VBL; ++i) {
-      const int bl = tid + NTH * i, rb = bl % (KB / 8), cb = bl / (KB / 8);
+    for (int i = 0; i < VBL; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int r = rb * 8 + j;
-        vr[i][j] = load_frag_global(vb + (size_t)r * a.ldk + cb * 8, bl < NVB && kv0 + r < T);
-      }
-    }
+      for (int j = 0; j < 8; ++j) vr[i][j] = bload128s(rV, offV[i], s0 + (uint32_t)j * rowB);
   };
   auto sstore = [&]() {
 #pragma unroll
@@ -1359,6 +1365,8 @@ hipError_t launch_attn_fwd(const AttnArgs& a, const SplitScratch& sc, hipStream_
   const double bytes = (double)a.B * a.T * (2.0 * a.Hq * a.dh * 2 + 2.0 * a.Hkv * a.dh * 2 + a.Hq * 4);
   const AttnPlan p = attn_plan(a.B, a.T, a.Hq, a.Hkv, a.dh, a.window);
   if (p.fwd32) {
+    // (the kernel addresses a sequence's K / V rows with 32-bit buffer offsets)
+    if ((double)a.T * a.ldk * 2 >= 2147483648.0) return hipErrorInvalidValue;
     // 128 queries per workgroup (4 waves of 32) when that still fills the chip
     const dim3 g2((a.T + 127) / 128, a.Hq, a.B);
 #define FWD32(D) \

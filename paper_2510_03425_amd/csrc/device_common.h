@@ -129,6 +129,12 @@ DEV uint4 bload128(rsrc_t r, uint32_t off) {
   const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
+// with a wave-uniform byte offset added by the buffer unit (no per-lane address arithmetic)
+DEV uint4 bload128s(rsrc_t r, uint32_t voff, uint32_t soff) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 DEV uint2 bload64(rsrc_t r, uint32_t off) {
   typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
   const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);

@@ -461,6 +461,41 @@ __global__ void k_qkv_post(f16* x, int ld, int n, int T, int H, int dh, const fl
   *(uint2*)(p + e + half) = make_uint2(pack_f16x2(hi[0], hi[1]), pack_f16x2(hi[2], hi[3]));
 }
 
+// RoPE in place on fp16 q or k (rotate-half pairs (e, e + dh/2), angles from the cos/sin
+// table of the row's position). One thread per (row, 8 columns e of the first half): the
+// table entries of those columns are read once (four 16-byte loads) and applied to every
+// head of the row, 16-byte accesses to the values.
+__global__ void k_rope_fwd(f16* x, int ld, int n, int T, int H, int dh, const float* cs) {
+  const int half = dh >> 1, C = half >> 3;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (size_t)n * C) return;
+  const int e = 8 * (int)(i % C);
+  const size_t row = i / C;
+  const int t = (int)(row % T);
+  const float4* tp = (const float4*)(cs + 2 * ((size_t)t * half + e));
+  float c[8], sn[8];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const float4 v = tp[u];
+    c[2 * u] = v.x; sn[2 * u] = v.y; c[2 * u + 1] = v.z; sn[2 * u + 1] = v.w;
+  }
+  f16* p = x + row * ld + e;
+  for (int h = 0; h < H; ++h, p += dh) {
+    const uint4 a = *(const uint4*)p, b = *(const uint4*)(p + half);
+    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+    uint32_t lo[4], hi[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float x1a = f16_lo(av[w]), x1b = f16_hi(av[w]), x2a = f16_lo(bv[w]), x2b = f16_hi(bv[w]);
+      const int u0 = 2 * w, u1 = 2 * w + 1;
+      lo[w] = pack_f16x2(x1a * c[u0] - x2a * sn[u0], x1b * c[u1] - x2b * sn[u1]);
+      hi[w] = pack_f16x2(x2a * c[u0] + x1a * sn[u0], x2b * c[u1] + x1b * sn[u1]);
+    }
+    *(uint4*)p = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    *(uint4*)(p + half) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  }
+}
+
 // Per-head RMSNorm backward in place on the gradient g (bf16) from the stored pre-norm
 // values (fp16): g = rstd * (w*g - xhat * mean(xhat*w*g)). Thread mapping as k_qkv_post.
 __global__ void k_headnorm_bwd(const f16* pre, int ld, int n, int H, int dh, const float* nw, float eps, bf16* g,
@@ -569,12 +604,11 @@ hipError_t launch_rope_table(int T, int dh, double theta, float* cs, hipStream_t
   return hipGetLastError();
 }
 hipError_t launch_rope_fwd(f16* x, int ld, int B, int T, int H, int dh, const float* cs, hipStream_t st) {
-  // the bias / head-norm kernel without bias or norm: 4 columns and their partners per thread
   const int n = B * T;
-  const size_t tot = (size_t)n * H * (dh >> 3);
+  if ((ld & 7) || (dh & 15) || ((uintptr_t)x & 15)) return hipErrorInvalidValue;  // 16-byte accesses
+  const size_t tot = (size_t)n * (dh >> 4);
   MEBP_TIMED(st, "rope_fwd", 0.0, (double)n * H * dh * 4,
-             hipLaunchKernelGGL(k_qkv_post, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, n, T, H, dh,
-                                (const float*)nullptr, (const float*)nullptr, 0.f, (f16*)nullptr, cs, 1));
+             hipLaunchKernelGGL(k_rope_fwd, dim3(blocks_for(tot, 256)), dim3(256), 0, st, x, ld, n, T, H, dh, cs));
   return hipGetLastError();
 }
 hipError_t launch_act_fwd(const f16* g, const f16* u, f16* z, size_t n, int act, hipStream_t st) {
