@@ -57,6 +57,12 @@ DEV VisRange queries_of_key(int key, int T, int W) {
 }
 DEV bool visible(const VisRange& v, int x) { return (uint32_t)(x - v.lo) <= v.span; }
 
+// Buffer resource over the T rows of one sequence and one head (dh columns from `head0`
+// elements into each row of pitch ld): loads past the last row return zero.
+DEV rsrc_t seq_rsrc(const void* base, size_t row_first, int T, int ld, int head0, int dh) {
+  return make_rsrc((const u16*)base + row_first * ld + head0, ((size_t)(T - 1) * ld + dh) * 2);
+}
+
 // Tile staging through registers: load() issues every global load of a tile at once (rows
 // at or past `rows_ok` read as zero), the store functions write it to LDS. Kernels load
 // the next tile before the products of the current one and store it after them, so the
@@ -74,6 +80,16 @@ struct StageN {
       const int c = tid + NTH * i, r = c / CH, col = (c % CH) * 8;
       v[i] = load_frag_global(src + (size_t)r * ld + col, c < NC && r < rows_ok);
     }
+  }
+  // The same tile through a buffer resource over the sequence's rows (rows past its end
+  // read as zero) starting `row0` rows in: one per-lane offset and wave-uniform row
+  // offsets, no per-load address arithmetic. Chunks past the tile (c >= NC) load rows of
+  // the sequence that the store skips.
+  __device__ __forceinline__ void load_rs(rsrc_t rs, int row0, int ld, int tid) {
+    static_assert(NTH % CH == 0, "threads must cover whole rows");
+    const uint32_t vo = (uint32_t)(((tid / CH) * ld + (tid % CH) * 8) * 2), rowB = (uint32_t)ld * 2;
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = bload128s(rs, vo, (uint32_t)(row0 + i * (NTH / CH)) * rowB);
   }
   // CONV: fp16 source values stored as bf16
   template <bool CONV>
@@ -102,6 +118,17 @@ struct StageB {
         const int r = rb * 8 + j;
         v[i][j] = load_frag_global(src + (size_t)r * ld + cb * 8, b < NB && r < rows_ok);
       }
+    }
+  }
+  // buffer-resource form of load (see StageN::load_rs)
+  __device__ __forceinline__ void load_rs(rsrc_t rs, int row0, int ld, int tid) {
+    const uint32_t rowB = (uint32_t)ld * 2;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int b = min(tid + NTH * i, NB - 1), rb = b % RB, cb = b / RB;
+      const uint32_t vo = (uint32_t)(((rb * 8) * ld + cb * 8) * 2);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[i][j] = bload128s(rs, vo, (uint32_t)(row0 + j) * rowB);
     }
   }
   template <bool CONV>
@@ -198,9 +225,10 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a, float* part,
 
   StageN<KB, DH, 256> kst;  // K row-major (A operand of S^T = K Q^T)
   StageB<KB, DH, 256> vst;  // V, stored transposed (A operand of O^T += V^T P^T)
+  const rsrc_t rK = seq_rsrc(a.k, rowb, T, a.ldk, kvh * DH, DH), rV = seq_rsrc(a.v, rowb, T, a.ldk, kvh * DH, DH);
   auto gload = [&](int kv0) {
-    kst.load((const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
-    vst.load((const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
+    kst.load_rs(rK, kv0, a.ldk, tid);
+    vst.load_rs(rV, kv0, a.ldk, tid);
   };
   gload(kv_lo);
 
@@ -580,10 +608,11 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
   }
 
   StageB<QB, DH, 256> qst, dst;  // Q and dO tiles: row-major and transposed LDS copies
+  const rsrc_t rQ = seq_rsrc(a.q, rowb, T, a.ldq, h * DH, DH), rdO = seq_rsrc(a.dO, rowb, T, a.ldq, h * DH, DH);
   float st_lse = 0.f, st_del = 0.f;
   auto gload = [&](int qb0) {
-    qst.load((const u16*)a.q + (rowb + qb0) * a.ldq + h * DH, a.ldq, T - qb0, tid);
-    dst.load((const u16*)a.dO + (rowb + qb0) * a.ldq + h * DH, a.ldq, T - qb0, tid);
+    qst.load_rs(rQ, qb0, a.ldq, tid);
+    dst.load_rs(rdO, qb0, a.ldq, tid);
     if (tid < QB) {
       const int qq = qb0 + tid;
       const size_t si = ((size_t)b * a.Hq + h) * T + qq;
@@ -723,9 +752,10 @@ __global__ __launch_bounds__(256, PF ? 1 : 2) void k_attn_bwd_dq(const AttnArgs 
 
   StageB<KB, DH, 256> kst;  // K: row-major fp16 (scores) and transposed bf16 (dQ product)
   StageN<KB, DH, 256> vst;  // V: row-major, converted to bf16
+  const rsrc_t rK = seq_rsrc(a.k, rowb, T, a.ldk, kvh * DH, DH), rV = seq_rsrc(a.v, rowb, T, a.ldk, kvh * DH, DH);
   auto gload = [&](int kv0) {
-    kst.load((const u16*)a.k + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
-    vst.load((const u16*)a.v + (rowb + kv0) * a.ldk + kvh * DH, a.ldk, T - kv0, tid);
+    kst.load_rs(rK, kv0, a.ldk, tid);
+    vst.load_rs(rV, kv0, a.ldk, tid);
   };
   if (PF) gload(kv_lo);
 
@@ -893,16 +923,24 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
 
   uint4 br[BPT][8];
   float st_lse = 0.f, st_del = 0.f;
+  // Q and dO rows of this sequence and head through buffer resources (rows past T read as
+  // zero); per-lane offsets fixed for the kernel, wave-uniform row offsets
+  const rsrc_t rQ = seq_rsrc(a.q, rowb, T, a.ldq, h * DH, DH), rdO = seq_rsrc(a.dO, rowb, T, a.ldq, h * DH, DH);
+  uint32_t boff[BPT];
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int bl = min(tid + NTH * i, 2 * NBT - 1), lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
+    boff[i] = (uint32_t)(((rb * 8) * a.ldq + cb * 8) * 2);
+  }
+  const uint32_t rowB = (uint32_t)a.ldq * 2;
   auto gload = [&](int qb0) {
 #pragma unroll
     for (int i = 0; i < BPT; ++i) {
-      const int bl = tid + NTH * i, tens = bl / NBT, lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
-      const u16* src = tens == 0 ? (const u16*)a.q : (const u16*)a.dO;
+      // wave-uniform (NBT is a multiple of 64): the resource stays in scalar registers
+      const bool q_tens = min(__builtin_amdgcn_readfirstlane(tid) + NTH * i, 2 * NBT - 1) < NBT;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int qq = qb0 + rb * 8 + j;
-        br[i][j] = load_frag_global(src + (rowb + qq) * a.ldq + h * DH + cb * 8, bl < 2 * NBT && qq < T);
-      }
+      for (int j = 0; j < 8; ++j)
+        br[i][j] = bload128s(q_tens ? rQ : rdO, boff[i], (uint32_t)(qb0 + j) * rowB);
     }
     if (tid < QB) {
       const int qq = qb0 + tid;
@@ -1086,16 +1124,24 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
 
   uint4 br[BPT][8];
   float st_lse = 0.f, st_del = 0.f;
+  // Q and dO rows of this sequence and head through buffer resources (rows past T read as
+  // zero); per-lane offsets fixed for the kernel, wave-uniform row offsets
+  const rsrc_t rQ = seq_rsrc(a.q, rowb, T, a.ldq, h * DH, DH), rdO = seq_rsrc(a.dO, rowb, T, a.ldq, h * DH, DH);
+  uint32_t boff[BPT];
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int bl = min(tid + NTH * i, 2 * NBT - 1), lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
+    boff[i] = (uint32_t)(((rb * 8) * a.ldq + cb * 8) * 2);
+  }
+  const uint32_t rowB = (uint32_t)a.ldq * 2;
   auto gload = [&](int qb0) {
 #pragma unroll
     for (int i = 0; i < BPT; ++i) {
-      const int bl = tid + NTH * i, tens = bl / NBT, lb = bl % NBT, rb = lb % (QB / 8), cb = lb / (QB / 8);
-      const u16* src = tens == 0 ? (const u16*)a.q : (const u16*)a.dO;
+      // wave-uniform (NBT is a multiple of 64): the resource stays in scalar registers
+      const bool q_tens = min(__builtin_amdgcn_readfirstlane(tid) + NTH * i, 2 * NBT - 1) < NBT;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int qq = qb0 + rb * 8 + j;
-        br[i][j] = load_frag_global(src + (rowb + qq) * a.ldq + h * DH + cb * 8, bl < 2 * NBT && qq < T);
-      }
+      for (int j = 0; j < 8; ++j)
+        br[i][j] = bload128s(q_tens ? rQ : rdO, boff[i], (uint32_t)(qb0 + j) * rowB);
     }
     if (tid < QB) {
       const int qq = qb0 + tid;
@@ -1364,9 +1410,9 @@ hipError_t launch_attn_fwd(const AttnArgs& a, const SplitScratch& sc, hipStream_
   const double flops = 4.0 * a.dh * pairs;
   const double bytes = (double)a.B * a.T * (2.0 * a.Hq * a.dh * 2 + 2.0 * a.Hkv * a.dh * 2 + a.Hq * 4);
   const AttnPlan p = attn_plan(a.B, a.T, a.Hq, a.Hkv, a.dh, a.window);
+  // (the kernels address a sequence's rows with 32-bit buffer offsets)
+  if ((double)a.T * (a.ldq > a.ldk ? a.ldq : a.ldk) * 2 >= 2147483648.0) return hipErrorInvalidValue;
   if (p.fwd32) {
-    // (the kernel addresses a sequence's K / V rows with 32-bit buffer offsets)
-    if ((double)a.T * a.ldk * 2 >= 2147483648.0) return hipErrorInvalidValue;
     // 128 queries per workgroup (4 waves of 32) when that still fills the chip
     const dim3 g2((a.T + 127) / 128, a.Hq, a.B);
 #define FWD32(D) \
@@ -1425,6 +1471,8 @@ hipError_t launch_attn_bwd(const AttnArgs& a0, float* delta_ws, const SplitScrat
     return e;
   AttnArgs a = a0;
   a.delta = delta_ws;
+  // (the kernels address a sequence's rows with 32-bit buffer offsets)
+  if ((double)a.T * (a.ldq > a.ldk ? a.ldq : a.ldk) * 2 >= 2147483648.0) return hipErrorInvalidValue;
   const AttnPlan p = attn_plan(a.B, a.T, a.Hq, a.Hkv, a.dh, a.window);
   if ((p.kv_floats + p.q_floats) && (!sc.part || sc.part_floats < p.kv_floats + p.q_floats))
     return hipErrorInvalidValue;
