@@ -86,14 +86,14 @@ KERNEL_PATTERNS = {
     "gemm_nt_f16out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?0(, (true|false))?>",
     "gemm_nt_f32out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?1(, (true|false))?>",
     "gemm_nt_logits": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?2(, (true|false))?>",
-    "gemm_tn_f32out": r"k_gemm_tn(_big)?<(\d+, )?0>",
-    "gemm_tn_act_bwd": r"k_gemm_tn(_big)?<(\d+, )?1>",
-    "gemm_tn_probs_dh": r"k_gemm_tn(_big)?<(\d+, )?2>",
-    "gemm_tn_bf16out": r"k_gemm_tn(_big)?<(\d+, )?3>",
+    "gemm_tn_f32out": r"k_gemm_tn(_big)?<(\d+, )?0(, (true|false))?>",
+    "gemm_tn_act_bwd": r"k_gemm_tn(_big)?<(\d+, )?1(, (true|false))?>",
+    "gemm_tn_probs_dh": r"k_gemm_tn(_big)?<(\d+, )?2(, (true|false))?>",
+    "gemm_tn_bf16out": r"k_gemm_tn(_big)?<(\d+, )?3(, (true|false))?>",
     "lora_rows": r"k_lora_rows<",
     "lora_outer": r"k_lora_outer<",
     "attn_fwd": r"k_attn_fwd",
-    "attn_bwd_dkdv": r"k_attn_bwd_(dkdv|kv32)<",
+    "attn_bwd_dkdv": r"k_attn_bwd_(dkdv|kv32p?)<",
     "attn_bwd_dq": r"k_attn_bwd_dq<",
 }
 
@@ -150,7 +150,7 @@ def pmc_per_dispatch(pmc_dir, counter):
 def pmc_command_lines(workload):
     """Header lines naming the rocprofv3 counter passes the summaries are made from."""
     a = "--steps 2 --warmup 1 --profile-steps 1" if workload == "qwen2.5-0.5b" else "--steps 1 --warmup 0 --profile-steps 0"
-    run = f"python3 -u bench.py --workload {workload} {a} --graph 0 --no-cpu-baseline"
+    run = f"python3 -u bench.py --workload {workload} {a} --graph 0 --no-cpu-baseline --extra-workload ''"
     return [f"# command: cd /tmp && export TMPDIR=/tmp && cd /root/repo && rocprofv3 --pmc <counters> --output-format csv "
             f"-d gpurun_out/cnt_{workload}/<pass> -o run -- {run}",
             "# passes: fetch = FETCH_SIZE; write = WRITE_SIZE; sq = SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "

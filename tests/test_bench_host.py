@@ -50,10 +50,15 @@ KERNELS = [
     ("k_gemm_tn_big<128, 2>", "gemm_tn_probs_dh"),
     ("k_gemm_tn<3>", "gemm_tn_bf16out"),
     ("k_gemm_tn_big<128, 3>", "gemm_tn_bf16out"),
+    ("k_gemm_tn_big<128, 0, true>", "gemm_tn_f32out"),
+    ("k_gemm_tn_big<128, 1, true>", "gemm_tn_act_bwd"),
     ("k_lora_rows<OpF16>", "lora_rows"),
     ("k_lora_outer<true>", "lora_outer"),
     ("k_attn_fwd32<256, 4>", "attn_fwd"),
     ("k_attn_bwd_kv32<128, 4>", "attn_bwd_dkdv"),
+    ("k_attn_bwd_kv32p<2>", "attn_bwd_dkdv"),
+    ("k_lora_rows<OpF16, 3>", "lora_rows"),
+    ("k_lora_outer<true, 2>", "lora_outer"),
     ("k_attn_bwd_dkdv<64, 64>", "attn_bwd_dkdv"),
     ("k_attn_bwd_dq<256, 32, false>", "attn_bwd_dq"),
     ("k_nt_finalize<0>", None),
