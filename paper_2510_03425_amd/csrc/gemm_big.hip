@@ -329,11 +329,54 @@ DEV void nt_big_epilogue(f32x16 (&acc)[4][BN / (32 * WNW)], const NtArgs& a, con
 // and stores them with 16-byte accesses (a wave instruction covers 8 whole row segments)
 // instead of 2- or 4-byte stores in the MFMA layout. The residual rows of a block are all
 // loaded before its accumulators are staged. Requires N % 8 == 0 and 16-byte aligned rows.
-template <int EPI>
+// lora_mfma with u and B already in LDS (rows of r floats: the tile's u rows from urow0, its
+// B rows from bcol0), copied there while the main loop ran
+template <int NJ>
+DEV void lora_mfma_lds(f32x16 (&acc)[4][NJ], const float* Us, const float* Bs, int r, int urow0, float s, int bcol0,
+                       int lane) {
+  const int q0 = 8 * (lane >> 5);
+  const bool keep = q0 < r;  // select, not multiply (see lora_mfma)
+  const int qe = keep ? q0 : 0;
+  uint4 bh[NJ], bl[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const float* p = Bs + (bcol0 + 32 * j + (lane & 31)) * r + qe;
+    const float4 x0 = *(const float4*)p, x1 = *(const float4*)(p + 4);
+    float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = keep ? v[e] : 0.f;
+    split_bf16(v, bh[j], bl[j]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float* p = Us + (urow0 + 32 * i + (lane & 31)) * r + qe;
+    const float4 x0 = *(const float4*)p, x1 = *(const float4*)(p + 4);
+    float u[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) u[e] = keep ? s * u[e] : 0.f;
+    uint4 ah, al;
+    split_bf16(u, ah, al);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      acc[i][j] = mfma32<OpBF16>(ah, bh[j], acc[i][j]);
+      acc[i][j] = mfma32<OpBF16>(ah, bl[j], acc[i][j]);
+      acc[i][j] = mfma32<OpBF16>(al, bh[j], acc[i][j]);
+    }
+  }
+}
+
+// LORA_LDS: the tile's u and B rows are in LDS at lora_lds (u rows from urow0 and B rows
+// from bcol0 for this wave), else they are read from global memory
+template <int EPI, bool LORA_LDS = false>
 DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int mw0, int wcol0, int lane,
-                      float* ep) {
+                      float* ep, const float* lora_lds = nullptr, int urow0 = 0, int bcol0 = 0) {
   constexpr int LDE = 68;
-  if (sg.lora_B) lora_mfma<2>(acc, sg.lora_u, a.r, mw0, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, sg.N, lane);
+  if (sg.lora_B) {
+    if constexpr (LORA_LDS)
+      lora_mfma_lds<2>(acc, lora_lds, lora_lds + BM * 16, a.r, urow0, a.lora_s, bcol0, lane);
+    else
+      lora_mfma<2>(acc, sg.lora_u, a.r, mw0, a.M, a.lora_s, sg.lora_B, a.r, 1, wcol0, sg.N, lane);
+  }
   const int rr = lane >> 3, ch = lane & 7, n = wcol0 + 8 * ch;
   const bool nok = n < sg.N;
 #pragma unroll
@@ -588,6 +631,9 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds0[LDS_STAGE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t lds1[LDS_STAGE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t lds2[LDS_STAGE_BYTES];
+  // the LoRA up-projection's operands of this tile (u rows, then B rows; r <= 16 floats each),
+  // copied at the start of the tile so that the epilogue does not wait for them
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_lora[2 * BM * 16 * 4];
   auto stage_ptr = [&](auto S_) -> uint8_t* {
     constexpr int st = decltype(S_)::value;
     return st == 0 ? lds0 : st == 1 ? lds1 : lds2;
@@ -634,6 +680,22 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   f32x16 acc[4][NJ];
   zero_acc(acc);
   const bool tail = (K % BK) != 0;
+  // (the rank is 8 or 16 whenever a LoRA factor is given)
+  const bool lora_lds = EPI != NT_LOGITS && sg.lora_B;
+  if (lora_lds) {
+    // BM rows of r floats = r KiB each for u and B: one 1 KiB copy per wave and instruction
+    // (rows past M or N read as zero)
+    const int nin = a.r;
+    const rsrc_t rU = make_rsrc(sg.lora_u, (size_t)a.M * a.r * 4);
+    const rsrc_t rL = make_rsrc(sg.lora_B, (size_t)Nn * a.r * 4);
+    typedef __attribute__((address_space(3))) uint8_t lds_u8;
+    for (int i = wave; i < nin; i += 8) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rU, (lds_u8*)(lds_lora + 1024 * i), 16,
+                                               (uint32_t)(m0 * a.r * 4 + 1024 * i + 16 * lane), 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rL, (lds_u8*)(lds_lora + BM * 16 * 4 + 1024 * i), 16,
+                                               (uint32_t)(n0 * a.r * 4 + 1024 * i + 16 * lane), 0, 0, 0);
+    }
+  }
 
   auto gload = [&](auto S_, int kt) {
     constexpr int st = decltype(S_)::value;  // ring stage (registers and LDS)
@@ -774,7 +836,8 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     uint8_t* reg = (wave < 3 ? lds0 : wave < 6 ? lds1 : lds2) + (wave % 3) * (32 * 68 * 4);
-    nt_lds_store<EPI>(acc, a, sg, m0 + wm * 128, wcol0, lane, reinterpret_cast<float*>(reg));
+    nt_lds_store<EPI, true>(acc, a, sg, m0 + wm * 128, wcol0, lane, reinterpret_cast<float*>(reg),
+                            reinterpret_cast<const float*>(lds_lora), wm * 128, wn * 32 * NJ);
   } else {
     nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
   }
