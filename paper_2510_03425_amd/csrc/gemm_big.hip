@@ -602,8 +602,12 @@ DEV void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Forward product with 256 x 256 tiles and 8 waves (2 along m x 4 along n, 128 x 64 each),
-// K step 64. The activation tile goes from global memory straight into LDS (buffer loads
+// Forward product with 256 x 256 tiles, K step 64, on NW waves: 4 waves of 256 x 64 (one
+// wave per SIMD, 256 accumulator registers each; the fp16 and fp32 outputs) or 8 waves of
+// 128 x 64 (2 along m x 4 along n; the LM head's logits, whose epilogue takes 128-row waves).
+// With 4 waves each weight column block is decompressed by one wave instead of two, which
+// halves the decompression's VALU work per MFMA: 5-6 % faster than 8 waves on the Gemma3-4B
+// shapes. The activation tile goes from global memory straight into LDS (buffer loads
 // with the LDS flag: no staging registers, no LDS stores) through a ring of three stages
 // filled two K tiles ahead. A stage holds the 256 x 64 fp16 tile as 128-byte rows whose
 // eight 16-byte chunks are stored at position chunk ^ ((row / 2) % 8), so that the MFMA
@@ -623,9 +627,10 @@ template <>
 struct LdsWeightRegs<true> {  // 16-bit weights: four 16-byte loads per 32 values
   uint4 rw[LDS_STAGES][2][4];
 };
-template <int EPI, bool W16 = false>
-__global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
-  constexpr int BN = 256, WNW = 4, NJ = 2;
+template <int EPI, bool W16 = false, int NW = 8>
+__global__ __launch_bounds__(64 * NW, 1) void k_gemm_nt_lds(const NtArgs a) {
+  constexpr int BN = 256, WNW = 4, NJ = 2, MI = 32 / NW, NA = 32 / NW;
+  static_assert(NW == 8 || EPI != NT_LOGITS, "the logits epilogue takes 128-row waves");
   // one LDS object per ring stage, so that the compiler can tell the fragment reads of one
   // stage from the LDS-direct loads in flight into another
   __shared__ __attribute__((aligned(1024))) uint8_t lds0[LDS_STAGE_BYTES];
@@ -660,11 +665,11 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
                               W16 ? 0 : (size_t)wrows * kgroups * 2);
   // activation loads: instruction i of wave w fills tile rows 8 (w + 8 i) .. +8, lane l row
   // 8 (w + 8 i) + l / 8, LDS position l % 8, i.e. global chunk (l % 8) ^ swz(row)
-  uint32_t offA[4];
-  int chunkA[4];
+  uint32_t offA[NA];
+  int chunkA[NA];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 8 * (wave + 8 * i) + (lane >> 3);
+  for (int i = 0; i < NA; ++i) {
+    const int row = 8 * (wave + NW * i) + (lane >> 3);
     chunkA[i] = (lane & 7) ^ ((row >> 1) & 7);
     offA[i] = (uint32_t)((row * a.lda + 8 * chunkA[i]) * 2);
   }
@@ -674,11 +679,16 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   // with swz(row) = (row / 2) % 8 = (l / 2) % 8: the 16 lanes that read in one LDS cycle
   // (16 consecutive rows) hit 16 distinct 16-byte bank groups (rows r and r + 8 no longer
   // share one: with swz = row % 8 half of the LDS cycles were bank conflicts)
-  const uint32_t rowA = (uint32_t)((wm * 128 + (lane & 31)) * 128);
+  const uint32_t rowA = (uint32_t)((wm * 32 * MI + (lane & 31)) * 128);
 
   LdsWeightRegs<W16> wr;
-  f32x16 acc[4][NJ];
-  zero_acc(acc);
+  f32x16 acc[MI][NJ];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
   const bool tail = (K % BK) != 0;
   // (the rank is 8 or 16 whenever a LoRA factor is given)
   const bool lora_lds = EPI != NT_LOGITS && sg.lora_B;
@@ -689,7 +699,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     const rsrc_t rU = make_rsrc(sg.lora_u, (size_t)a.M * a.r * 4);
     const rsrc_t rL = make_rsrc(sg.lora_B, (size_t)Nn * a.r * 4);
     typedef __attribute__((address_space(3))) uint8_t lds_u8;
-    for (int i = wave; i < nin; i += 8) {
+    for (int i = wave; i < nin; i += NW) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rU, (lds_u8*)(lds_lora + 1024 * i), 16,
                                                (uint32_t)(m0 * a.r * 4 + 1024 * i + 16 * lane), 0, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rL, (lds_u8*)(lds_lora + BM * 16 * 4 + 1024 * i), 16,
@@ -702,10 +712,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     const int k0 = kt * BK;
     __attribute__((address_space(3))) uint8_t* dst = (__attribute__((address_space(3))) uint8_t*)stage_ptr(S_);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NA; ++i) {
       // chunks past the reduction length read as zero (out-of-range offset)
       const uint32_t off = (!tail || k0 + 8 * chunkA[i] < K) ? offA[i] + 2 * k0 : 0x80000000u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, dst + 1024 * (wave + 8 * i), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, dst + 1024 * (wave + NW * i), 16, off, 0, 0, 0);
     }
     if constexpr (W16) {
 #pragma unroll
@@ -750,18 +760,18 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
         sc[j] = f16x2{v, v};
       }
     }
-    auto rd = [&](int t, uint4 (&dst)[4]) {
+    auto rd = [&](int t, uint4 (&dst)[MI]) {
       const int pos = ((4 * h + t) ^ ((lane >> 1) & 7)) * 16;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dst[i] = *(const uint4*)(As + 4096 * i + pos);
+      for (int i = 0; i < MI; ++i) dst[i] = *(const uint4*)(As + 4096 * i + pos);
     };
     if constexpr (W16) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        uint4 af[4];
+        uint4 af[MI];
         rd(t, af);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
           for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpF16>(af[i], wr.rw[st][j][t], acc[i][j]);
       }
@@ -770,7 +780,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
       // and its weights decompressed, while the MFMAs of substep t run (scheduling barriers
       // keep the compiler from moving the reads next to their use; the decompression is
       // interleaved one MFMA to five VALU instructions)
-      uint4 af[2][4], bq[2][NJ];
+      uint4 af[2][MI], bq[2][NJ];
       auto dq = [&](int t, uint4 (&dst)[NJ]) {
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -786,14 +796,16 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
         __builtin_amdgcn_sched_barrier(0);
         if (t < 3) dq(t + 1, bq[(t + 1) & 1]);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
           for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpF16>(af[t & 1][i], bq[t & 1][j], acc[i][j]);
         if (t < 3) {
 #pragma unroll
-          for (int q = 0; q < 4 * NJ; ++q) {
+          for (int q = 0; q < MI * NJ; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // five VALU
+            // VALU per MFMA: five with 128-row waves, three with 256-row waves (two or four
+            // measured slower)
+            __builtin_amdgcn_sched_group_barrier(0x002, MI == 4 ? 5 : 3, 0);
           }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -805,7 +817,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
   // thread's activation loads of tile k+1 have landed (the loads issued after them: the
   // weights of k+1 and all of k+2, 2 NJ + 4 + 2 NJ) and meet the other waves at the barrier.
   // vector-memory instructions of one gload: 4 activation loads plus the weight loads
-  constexpr int VMI = 4 + (W16 ? 4 * NJ : 2 * NJ);
+  constexpr int VMI = NA + (W16 ? 4 * NJ : 2 * NJ);
   auto step = [&](auto I_, int k) {
     constexpr int I = decltype(I_)::value;
     gload(IC<(I + 2) % LDS_STAGES>{}, min(k + 2, kt_end - 1));
@@ -836,9 +848,14 @@ __global__ __launch_bounds__(512, 1) void k_gemm_nt_lds(const NtArgs a) {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     uint8_t* reg = (wave < 3 ? lds0 : wave < 6 ? lds1 : lds2) + (wave % 3) * (32 * 68 * 4);
-    nt_lds_store<EPI, true>(acc, a, sg, m0 + wm * 128, wcol0, lane, reinterpret_cast<float*>(reg),
-                            reinterpret_cast<const float*>(lds_lora), wm * 128, wn * 32 * NJ);
-  } else {
+#pragma unroll
+    for (int hh = 0; hh < MI / 4; ++hh) {
+      f32x16 (&ah)[4][NJ] = *reinterpret_cast<f32x16 (*)[4][NJ]>(&acc[4 * hh][0]);
+      const int r0 = wm * 32 * MI + 128 * hh;
+      nt_lds_store<EPI, true>(ah, a, sg, m0 + r0, wcol0, lane, reinterpret_cast<float*>(reg),
+                              reinterpret_cast<const float*>(lds_lora), r0, wn * 32 * NJ);
+    }
+  } else if constexpr (NW == 8) {
     nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
   }
 }
@@ -1211,14 +1228,14 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
           (!g.resid || (((uintptr_t)g.resid | (size_t)g.ldr * 4) & 15) == 0);
   }
   if (bn == 256 && use_lds && a.K % 8 == 0 && (epi == NT_LOGITS || vec)) {
-#define NT_LDS(EPI_) \
-  MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_nt_lds<EPI_>), grid, dim3(512), 0, st, b))
+#define NT_LDS(EPI_, NW_) \
+  MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_nt_lds<EPI_, false, NW_>), grid, dim3(64 * NW_), 0, st, b))
     if (epi == NT_LOGITS)
-      NT_LDS(NT_LOGITS);
+      NT_LDS(NT_LOGITS, 8);
     else if (epi == NT_STORE_F16)
-      NT_LDS(NT_STORE_F16);
+      NT_LDS(NT_STORE_F16, 4);
     else
-      NT_LDS(NT_STORE_F32);
+      NT_LDS(NT_STORE_F32, 4);
 #undef NT_LDS
   } else if (bn == 256) {
     if (epi == NT_LOGITS) {
@@ -1301,7 +1318,7 @@ hipError_t launch_gemm_probe_big(int kind, const uint8_t* q4, const uint16_t* sc
                          st, a);
       break;
     case 3:  // LDS-direct forward, 256 x 256 tiles
-      hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0, st, a);
+      hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32, false, 4>), dim3((n_out + 255) / 256, mt, 1), dim3(256), 0, st, a);
       break;
     case 7: {  // the transposed 256 x 128 kernel on plain bf16 weights [n_out][n_in] (seg.q4)
       TnArgs t{};
@@ -1312,7 +1329,7 @@ hipError_t launch_gemm_probe_big(int kind, const uint8_t* q4, const uint16_t* sc
       break;
     }
     case 6:  // the LDS-direct forward kernel on plain fp16 weights [n_out][n_in] (seg.q4)
-      hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32, true>), dim3((n_out + 255) / 256, mt, 1), dim3(512), 0, st, a);
+      hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F32, true, 4>), dim3((n_out + 255) / 256, mt, 1), dim3(256), 0, st, a);
       break;
     case 5: {  // transposed, 256 x 128 tiles
       TnArgs t{};
