@@ -329,6 +329,61 @@ DEV void nt_big_epilogue(f32x16 (&acc)[4][BN / (32 * WNW)], const NtArgs& a, con
 // and stores them with 16-byte accesses (a wave instruction covers 8 whole row segments)
 // instead of 2- or 4-byte stores in the MFMA layout. The residual rows of a block are all
 // loaded before its accumulators are staged. Requires N % 8 == 0 and 16-byte aligned rows.
+// LM-head logits epilogue through a per-wave LDS region (32 x 68 fp32): for each 32-row block
+// of the wave's 128 x 64 tile, lane (row r = 8p + lane / 8, columns 8 (lane % 8) ..) takes 8
+// consecutive values of one row, so that the statistics of a row's 64-column tile reduce over
+// the 8 lanes that hold it (three shuffle steps) and its fp16 values leave as one 16-byte store.
+// Per row and tile: max, sum of exp(v - max), the values minus the max (fp16), and the fp32
+// logit of the target (vocabulary columns are offset by vbase). The segment width is a
+// multiple of 32, so an 8-column group is either wholly inside it or wholly past it.
+DEV void nt_lds_logits_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int mw0, int wcol0, int lane,
+                             float* ep) {
+  constexpr int LDE = 68;
+  const int rr = lane >> 3, ch = lane & 7, n = wcol0 + 8 * ch, Nn = sg.N;
+  const bool nok = n < Nn, tile_ok = wcol0 < Nn;
+  const int stile = wcol0 / 64;
+  _Float16* out = (_Float16*)sg.out;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) ep[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] = acc[i][j][q];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int r = 8 * p + rr, m = mw0 + 32 * i + r;
+      const float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
+      const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      float mx = -INFINITY;
+      if (nok) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, v[e]);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 4, 64));
+      float se = 0.f;
+      if (nok) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) se += __expf(v[e] - mx);
+      }
+      se += __shfl_xor(se, 1, 64);
+      se += __shfl_xor(se, 2, 64);
+      se += __shfl_xor(se, 4, 64);
+      if (m < a.M) {
+        if (nok) {
+          const uint4 o = make_uint4(pack_f16x2(v[0] - mx, v[1] - mx), pack_f16x2(v[2] - mx, v[3] - mx),
+                                     pack_f16x2(v[4] - mx, v[5] - mx), pack_f16x2(v[6] - mx, v[7] - mx));
+          *(uint4*)(out + (size_t)m * sg.ldo + n) = o;
+          const int tg = a.tgt[m] - a.vbase - n;
+          if (tg >= 0 && tg < 8) a.tgt_logit[m] = v[tg];
+        }
+        if (ch == 0 && tile_ok) a.stats[(size_t)m * a.ntiles + stile] = make_float2(mx, se);
+      }
+    }
+  }
+}
+
 // lora_mfma with u and B already in LDS (rows of r floats: the tile's u rows from urow0, its
 // B rows from bcol0), copied there while the main loop ran
 template <int NJ>
@@ -856,7 +911,12 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_nt_lds(const NtArgs a) {
                               reinterpret_cast<const float*>(lds_lora), r0, wn * 32 * NJ);
     }
   } else if constexpr (NW == 8) {
-    nt_big_epilogue<BN, WNW, EPI>(acc, a, sg, m0, n0, wcol0, wm, wn, lane, z, S);
+    // (one split: the logits GEMM runs unsplit)
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    uint8_t* reg = (wave < 3 ? lds0 : wave < 6 ? lds1 : lds2) + (wave % 3) * (32 * 68 * 4);
+    nt_lds_logits_store(acc, a, sg, m0 + wm * 128, wcol0, lane, reinterpret_cast<float*>(reg));
   }
 }
 
