@@ -175,3 +175,18 @@ DEV float act_grad_f(float g, int kind) {
   const float t = tanh_fast(c * (g + 0.044715f * g * g * g));
   return 0.5f * (1.0f + t) + 0.5f * g * (1.0f - t * t) * c * (1.0f + 3.0f * 0.044715f * g * g);
 }
+// act(g) and act'(g) of one kind, known at compile time, from one exponential and one
+// reciprocal (the same expressions as act_f and act_grad_f)
+template <int KIND>
+DEV void act_and_grad(float g, float& act, float& grad) {
+  if constexpr (KIND == 0) {
+    const float s = sigmoid_fast(g);
+    act = g * s;
+    grad = s * (1.0f + g * (1.0f - s));
+  } else {
+    const float c = 0.7978845608028654f;
+    const float t = tanh_fast(c * (g + 0.044715f * g * g * g));
+    act = 0.5f * g * (1.0f + t);
+    grad = 0.5f * (1.0f + t) + 0.5f * g * (1.0f - t * t) * c * (1.0f + 3.0f * 0.044715f * g * g);
+  }
+}

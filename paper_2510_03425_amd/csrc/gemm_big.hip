@@ -1170,24 +1170,36 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
               ep[(32 * ii + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] =
                   acc[2 * hh + ii][j][q];
         __syncthreads();
+        // the activation kind is a template argument here, so the element loop has no branch
+        // on it, and each element takes one exponential for act and act'
+        auto finish = [&](auto K_) {
+          constexpr int KIND = decltype(K_)::value;
 #pragma unroll
-        for (int p = 0; p < NP; ++p) {
-          const int r = p * RPP + rr, m = m0 + wm * 128 + 64 * hh + r;
-          if (m >= a.M || cbase >= Kout) continue;
-          const float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
-          const size_t idx = (size_t)m * a.ldgu + cbase;
-          const uint32_t gq[4] = {gw[p].x, gw[p].y, gw[p].z, gw[p].w}, uq[4] = {uw[p].x, uw[p].y, uw[p].z, uw[p].w};
-          const float dz[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-          uint32_t og[4], ou[4];
+          for (int p = 0; p < NP; ++p) {
+            const int r = p * RPP + rr, m = m0 + wm * 128 + 64 * hh + r;
+            if (m >= a.M || cbase >= Kout) continue;
+            const float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
+            const size_t idx = (size_t)m * a.ldgu + cbase;
+            const uint32_t gq[4] = {gw[p].x, gw[p].y, gw[p].z, gw[p].w}, uq[4] = {uw[p].x, uw[p].y, uw[p].z, uw[p].w};
+            const float dz[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            uint32_t og[4], ou[4];
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const float g0 = f16_lo(gq[t]), g1 = f16_hi(gq[t]), u0 = f16_lo(uq[t]), u1 = f16_hi(uq[t]);
-            og[t] = pack_bf16x2(dz[2 * t] * u0 * act_grad_f(g0, a.act), dz[2 * t + 1] * u1 * act_grad_f(g1, a.act));
-            ou[t] = pack_bf16x2(dz[2 * t] * act_f(g0, a.act), dz[2 * t + 1] * act_f(g1, a.act));
+            for (int t = 0; t < 4; ++t) {
+              const float g0 = f16_lo(gq[t]), g1 = f16_hi(gq[t]), u0 = f16_lo(uq[t]), u1 = f16_hi(uq[t]);
+              float a0, d0, a1, d1;
+              act_and_grad<KIND>(g0, a0, d0);
+              act_and_grad<KIND>(g1, a1, d1);
+              og[t] = pack_bf16x2(dz[2 * t] * u0 * d0, dz[2 * t + 1] * u1 * d1);
+              ou[t] = pack_bf16x2(dz[2 * t] * a0, dz[2 * t + 1] * a1);
+            }
+            *(uint4*)((bf16*)a.g + idx) = make_uint4(og[0], og[1], og[2], og[3]);
+            *(uint4*)((bf16*)a.u + idx) = make_uint4(ou[0], ou[1], ou[2], ou[3]);
           }
-          *(uint4*)((bf16*)a.g + idx) = make_uint4(og[0], og[1], og[2], og[3]);
-          *(uint4*)((bf16*)a.u + idx) = make_uint4(ou[0], ou[1], ou[2], ou[3]);
-        }
+        };
+        if (a.act == 0)
+          finish(IC<0>{});
+        else
+          finish(IC<1>{});
         __syncthreads();  // before the next half overwrites the staging area
       }
       return;
