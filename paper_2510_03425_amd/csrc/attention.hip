@@ -381,6 +381,7 @@ DEV f32x16 mfma32_bf16(uint4 a, uint4 b, f32x16 c) {
 template <int DH, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
   constexpr int NTH = 64 * NW, KB = 64, LDK = DH + 8, LDV = KB + 8;
+  constexpr int FA = 3;  // LDS fragment reads in flight ahead of the MFMAs
   constexpr int NKS = DH / 16, NTO = DH / 32;
   constexpr int KCH = KB * DH / 8 / NTH;                // K chunks (8 halves) per thread
   constexpr int NVB = (KB / 8) * (DH / 8);               // 8x8 blocks of the V tile
@@ -478,12 +479,31 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
     if (kv0 > w_hi || kv0 + KB - 1 < w_lo) continue;  // nothing visible for this wave
     f32x16 s[2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
+    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kt][r] = 0.f;
-      const u16* kp = Ks + (kt * 32 + (lane & 31)) * LDK + 8 * hl;
+    {
+      // the 2 x NKS score MFMAs in (key tile, depth) order, each K fragment read from LDS FA
+      // MFMAs ahead of its use, so that no MFMA waits for the round trip of its own read
+      // (the scheduling groups keep the compiler from moving the reads next to their use)
+      constexpr int NR = 2 * NKS;
+      uint4 kb[FA + 2];
+      auto rdk = [&](int i) {
+        return *(const uint4*)(Ks + ((i / NKS) * 32 + (lane & 31)) * LDK + 8 * hl + 16 * (i % NKS));
+      };
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) s[kt] = mfma32_f16(*(const uint4*)(kp + 16 * ks), qf[ks], s[kt]);
+      for (int i = 0; i < FA; ++i) kb[i] = rdk(i);
+#pragma unroll
+      for (int i = 0; i < NR; ++i) {
+        if (i + FA < NR) kb[(i + FA) % (FA + 2)] = rdk(i + FA);
+        s[i / NKS] = mfma32_f16(kb[i % (FA + 2)], qf[i % NKS], s[i / NKS]);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, FA, 0);
+#pragma unroll
+      for (int i = 0; i < NR; ++i) {
+        if (i + FA < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
     }
     float mloc = -1e30f;
 #pragma unroll
@@ -519,17 +539,36 @@ __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
     }
     l_i += ls;
     m_i = m_new;
+    {
+      // O^T += V^T P^T: 4 x NTO MFMAs in (key step, output tile) order, the V^T fragments read
+      // FA MFMAs ahead as above
+      constexpr int NPV = 4 * NTO;
+      uint4 pf[4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const f32x16& st = s[kk >> 1];
-      const int r0 = 8 * (kk & 1);
-      const uint4 pf = make_uint4(pack_f16x2(st[r0 + 0], st[r0 + 1]), pack_f16x2(st[r0 + 2], st[r0 + 3]),
-                                  pack_f16x2(st[r0 + 4], st[r0 + 5]), pack_f16x2(st[r0 + 6], st[r0 + 7]));
-#pragma unroll
-      for (int t = 0; t < NTO; ++t) {
-        const u16* vp = Vt + (t * 32 + (lane & 31)) * LDV + kk * 16 + 4 * hl;
+      for (int kk = 0; kk < 4; ++kk) {
+        const f32x16& st = s[kk >> 1];
+        const int r0 = 8 * (kk & 1);
+        pf[kk] = make_uint4(pack_f16x2(st[r0 + 0], st[r0 + 1]), pack_f16x2(st[r0 + 2], st[r0 + 3]),
+                            pack_f16x2(st[r0 + 4], st[r0 + 5]), pack_f16x2(st[r0 + 6], st[r0 + 7]));
+      }
+      uint4 vb[FA + 2];
+      auto rdv = [&](int i) {
+        const u16* vp = Vt + ((i % NTO) * 32 + (lane & 31)) * LDV + (i / NTO) * 16 + 4 * hl;
         const uint2 x0 = *(const uint2*)vp, x1 = *(const uint2*)(vp + 8);
-        oacc[t] = mfma32_f16(make_uint4(x0.x, x0.y, x1.x, x1.y), pf, oacc[t]);
+        return make_uint4(x0.x, x0.y, x1.x, x1.y);
+      };
+#pragma unroll
+      for (int i = 0; i < FA; ++i) vb[i] = rdv(i);
+#pragma unroll
+      for (int i = 0; i < NPV; ++i) {
+        if (i + FA < NPV) vb[(i + FA) % (FA + 2)] = rdv(i + FA);
+        oacc[i % NTO] = mfma32_f16(vb[i % (FA + 2)], pf[i / NTO], oacc[i % NTO]);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, FA, 0);
+#pragma unroll
+      for (int i = 0; i < NPV; ++i) {
+        if (i + FA < NPV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       }
     }
   }
