@@ -378,6 +378,28 @@ DEV f32x16 mfma32_bf16(uint4 a, uint4 b, f32x16 c) {
                                                  0);
 }
 
+// x += sum_i A_i B_i over N MFMAs whose A fragments are 16-byte LDS reads at p + 16 i (halves):
+// each read is issued FA MFMAs ahead of its use (scheduling groups keep the compiler from
+// moving it next to the MFMA), so that no MFMA waits for the round trip of its own read
+template <int FA, int N, class MF>
+DEV f32x16 lds_chain(const u16* p, const uint4 (&b)[N], f32x16 x, MF mf) {
+  uint4 buf[FA + 2];
+#pragma unroll
+  for (int i = 0; i < FA; ++i) buf[i] = *(const uint4*)(p + 16 * i);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if (i + FA < N) buf[(i + FA) % (FA + 2)] = *(const uint4*)(p + 16 * (i + FA));
+    x = mf(buf[i % (FA + 2)], b[i], x);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, FA, 0);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if (i + FA < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+  return x;
+}
+
 template <int DH, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn_fwd32(const AttnArgs a) {
   constexpr int NTH = 64 * NW, KB = 64, LDK = DH + 8, LDV = KB + 8;
@@ -1238,8 +1260,7 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
     if (act) {
       const u16* src = (role == 0 ? Qs : dOs) + (lane & 31) * LDN + 8 * hl;
       if (role == 0) {
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) x = mfma32_f16(*(const uint4*)(src + 16 * ks), kv[ks], x);
+        x = lds_chain<3>(src, kv, x, [](uint4 p, uint4 q, f32x16 c) { return mfma32_f16(p, q, c); });
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const float4 l4 = *(const float4*)(lse_s + 8 * g + 4 * hl);
@@ -1253,8 +1274,7 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
           }
         }
       } else {
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) x = mfma32_bf16(*(const uint4*)(src + 16 * ks), kv[ks], x);
+        x = lds_chain<3>(src, kv, x, [](uint4 p, uint4 q, f32x16 c) { return mfma32_bf16(p, q, c); });
       }
     }
     __syncthreads();  // P of every pair is in LDS
@@ -1272,17 +1292,33 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
         }
       }
       const u16* opnd = role == 0 ? dOt : Qt;
+      uint4 f[2];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         const int r0 = 8 * kk;
-        const uint4 f = make_uint4(pack_bf16x2(x[r0 + 0], x[r0 + 1]), pack_bf16x2(x[r0 + 2], x[r0 + 3]),
-                                   pack_bf16x2(x[r0 + 4], x[r0 + 5]), pack_bf16x2(x[r0 + 6], x[r0 + 7]));
+        f[kk] = make_uint4(pack_bf16x2(x[r0 + 0], x[r0 + 1]), pack_bf16x2(x[r0 + 2], x[r0 + 3]),
+                           pack_bf16x2(x[r0 + 4], x[r0 + 5]), pack_bf16x2(x[r0 + 6], x[r0 + 7]));
+      }
+      // 2 x NTO MFMAs in (key step, output tile) order, operand fragments read three ahead
+      constexpr int FA = 3, NM = 2 * NTO;
+      uint4 ob[FA + 2];
+      auto rdo = [&](int i) {
+        const int rowoff = ((i % NTO) * 32 + (lane & 31)) * LDT + (i / NTO) * 16 + 4 * hl;
+        const uint2 o0 = *(const uint2*)(opnd + rowoff), o1 = *(const uint2*)(opnd + rowoff + 8);
+        return make_uint4(o0.x, o0.y, o1.x, o1.y);
+      };
 #pragma unroll
-        for (int t = 0; t < NTO; ++t) {
-          const int rowoff = (t * 32 + (lane & 31)) * LDT + kk * 16 + 4 * hl;
-          const uint2 o0 = *(const uint2*)(opnd + rowoff), o1 = *(const uint2*)(opnd + rowoff + 8);
-          acc[t] = mfma32_bf16(make_uint4(o0.x, o0.y, o1.x, o1.y), f, acc[t]);
-        }
+      for (int i = 0; i < FA; ++i) ob[i] = rdo(i);
+#pragma unroll
+      for (int i = 0; i < NM; ++i) {
+        if (i + FA < NM) ob[(i + FA) % (FA + 2)] = rdo(i + FA);
+        acc[i % NTO] = mfma32_bf16(ob[i % (FA + 2)], f[i / NTO], acc[i % NTO]);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, FA, 0);
+#pragma unroll
+      for (int i = 0; i < NM; ++i) {
+        if (i + FA < NM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       }
     }
   }
