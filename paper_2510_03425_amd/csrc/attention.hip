@@ -164,7 +164,11 @@ struct StageB {
           o = make_uint4(perm_lo16(in[0][d], in[1][d]), perm_lo16(in[2][d], in[3][d]), perm_lo16(in[4][d], in[5][d]),
                          perm_lo16(in[6][d], in[7][d]));
         }
-        *(uint4*)(dst + (cb * 8 + jc) * LD + rb * 8) = o;
+        // two 8-byte stores: transposed rows are padded by 4 halves (8-byte aligned), which
+        // keeps the 8-byte fragment reads of 16 consecutive rows on distinct banks
+        uint2* dt = (uint2*)(dst + (cb * 8 + jc) * LD + rb * 8);
+        dt[0] = make_uint2(o.x, o.y);
+        dt[1] = make_uint2(o.z, o.w);
       }
     }
   }
@@ -202,7 +206,7 @@ DEV TileId attn_tile(int nck) {
 // (max, sum, base-2 domain) in fp32 and k_attn_fwd_combine merges the chunks in order.
 template <int DH>
 __global__ __launch_bounds__(256) void k_attn_fwd(const AttnArgs a, float* part, int nck, int ck) {
-  constexpr int KB = 64, LDK = DH + 8, LDV = KB + 8, NKS = DH / 32, NT = DH / 16;
+  constexpr int KB = 64, LDK = DH + 8, LDV = KB + 4, NKS = DH / 32, NT = DH / 16;
   __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDK];
   __shared__ __attribute__((aligned(16))) u16 Vt[DH * LDV];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -796,7 +800,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
 // workgroups share a compute unit and hide each other's load latency instead.
 template <int DH, int KB, bool PF>
 __global__ __launch_bounds__(256, PF ? 1 : 2) void k_attn_bwd_dq(const AttnArgs a, float* part, int nck, int ck) {
-  constexpr int LDN = DH + 8, LDT_ = KB + 8, NKS = DH / 32, NT = DH / 16, NKT = KB / 16;
+  constexpr int LDN = DH + 8, LDT_ = KB + 4, NKS = DH / 32, NT = DH / 16, NKT = KB / 16;
   __shared__ __attribute__((aligned(16))) u16 Ks[KB * LDN];   // fp16 (scores)
   __shared__ __attribute__((aligned(16))) u16 Vs[KB * LDN];   // bf16 (dP)
   __shared__ __attribute__((aligned(16))) u16 Kt[DH * LDT_];  // bf16 (dQ product)
