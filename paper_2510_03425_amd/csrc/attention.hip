@@ -1262,13 +1262,14 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
     sstore();
     __syncthreads();
     if (qb0 + QB < q_hi) gload(qb0 + QB);  // next tile in flight during this one
-    // nothing visible for this pair: all queries before its keys, or past its window (the
-    // barriers below are still met)
-    const bool act = !(qb0 + QB - 1 < kw || (a.window && qb0 > kw + 31 + a.window - 1));
+    // A pair with nothing visible in this tile (all its queries before its keys, or past its
+    // window) runs the MFMAs anyway: its P and dS are masked to zero, so they add nothing.
+    // Without a branch around them the accumulators stay in the accumulator registers across
+    // tiles (with one, the compiler copied all 128 out and back on every tile).
     f32x16 x;  // S then P (role 0), dP then dS (role 1)
 #pragma unroll
     for (int r = 0; r < 16; ++r) x[r] = 0.f;
-    if (act) {
+    {
       const u16* src = (role == 0 ? Qs : dOs) + (lane & 31) * LDN + 8 * hl;
       if (role == 0) {
         x = lds_chain<3>(src, kv, x, [](uint4 p, uint4 q, f32x16 c) { return mfma32_f16(p, q, c); });
@@ -1289,7 +1290,7 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
       }
     }
     __syncthreads();  // P of every pair is in LDS
-    if (act) {
+    {
       if (role == 1) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
