@@ -682,14 +682,19 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
   StageB<QB, DH, 256> qst, dst;  // Q and dO tiles: row-major and transposed LDS copies
   const rsrc_t rQ = seq_rsrc(a.q, rowb, T, a.ldq, h * DH, DH), rdO = seq_rsrc(a.dO, rowb, T, a.ldq, h * DH, DH);
   float st_lse = 0.f, st_del = 0.f;
+  const size_t stat0 = ((size_t)b * a.Hq + h) * T;  // this (sequence, head)'s row statistics
+  const rsrc_t rL = make_rsrc(a.lse + stat0, (size_t)T * 4), rD = make_rsrc(a.delta + stat0, (size_t)T * 4);
   auto gload = [&](int qb0) {
     qst.load_rs(rQ, qb0, a.ldq, tid);
     dst.load_rs(rdO, qb0, a.ldq, tid);
-    if (tid < QB) {
+    // the row statistics of queries qb0 + tid (tid < QB) through buffer loads, without a
+    // branch, and scaled only when stored: a use right after the load would make the wave wait
+    // for it, and so for every tile load issued before it
+    {
       const int qq = qb0 + tid;
-      const size_t si = ((size_t)b * a.Hq + h) * T + qq;
-      st_lse = qq < T ? a.lse[si] * LOG2E : 0.f;
-      st_del = qq < T ? a.delta[si] : 0.f;
+      const uint32_t so = (tid < QB && qq < T) ? (uint32_t)qq * 4 : 0x80000000u;
+      st_lse = __uint_as_float(bload32(rL, so));
+      st_del = __uint_as_float(bload32(rD, so));
     }
   };
   gload(q_lo);
@@ -714,11 +719,14 @@ __global__ __launch_bounds__(256) void k_attn_bwd_dkdv(const AttnArgs a, float* 
     dst.template store_n<false>(dOs, LDN, tid);
     dst.template store_t<false>(dOt, LDT_, tid);
     if (tid < QB) {
-      lse_s[tid] = st_lse;
+      lse_s[tid] = st_lse * LOG2E;
       del_s[tid] = st_del;
     }
     __syncthreads();
-    if (qb0 + QB < q_hi) gload(qb0 + QB);  // next tile in flight during this one
+    // next tile in flight during this one; issued after the last tile too (rows past T read as
+    // zero, rows past the range are unused), since loads behind a branch leave the compiler
+    // only a full wait for them before the next MFMA
+    gload(qb0 + QB);
     f32x4 s[NQT], dp[NQT];
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
@@ -995,6 +1003,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
 
   uint4 br[BPT][8];
   float st_lse = 0.f, st_del = 0.f;
+  const size_t stat0 = ((size_t)b * a.Hq + h) * T;  // this (sequence, head)'s row statistics
+  const rsrc_t rL = make_rsrc(a.lse + stat0, (size_t)T * 4), rD = make_rsrc(a.delta + stat0, (size_t)T * 4);
   // Q and dO rows of this sequence and head through buffer resources (rows past T read as
   // zero); per-lane offsets fixed for the kernel, wave-uniform row offsets
   const rsrc_t rQ = seq_rsrc(a.q, rowb, T, a.ldq, h * DH, DH), rdO = seq_rsrc(a.dO, rowb, T, a.ldq, h * DH, DH);
@@ -1014,11 +1024,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
       for (int j = 0; j < 8; ++j)
         br[i][j] = bload128s(q_tens ? rQ : rdO, boff[i], (uint32_t)(qb0 + j) * rowB);
     }
-    if (tid < QB) {
+    // the row statistics of queries qb0 + tid (tid < QB) through buffer loads, without a
+    // branch, and scaled only when stored: a use right after the load would make the wave wait
+    // for it, and so for every tile load issued before it
+    {
       const int qq = qb0 + tid;
-      const size_t si = ((size_t)b * a.Hq + h) * T + qq;
-      st_lse = qq < T ? a.lse[si] * LOG2E : 0.f;
-      st_del = qq < T ? a.delta[si] : 0.f;
+      const uint32_t so = (tid < QB && qq < T) ? (uint32_t)qq * 4 : 0x80000000u;
+      st_lse = __uint_as_float(bload32(rL, so));
+      st_del = __uint_as_float(bload32(rD, so));
     }
   };
   auto sstore = [&]() {
@@ -1050,7 +1063,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
       }
     }
     if (tid < QB) {
-      lse_s[tid] = st_lse;
+      lse_s[tid] = st_lse * LOG2E;
       del_s[tid] = st_del;
     }
   };
@@ -1060,7 +1073,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bwd_kv32(const AttnArgs a, flo
     __syncthreads();  // every wave is done with the previous tile
     sstore();
     __syncthreads();
-    if (qb0 + QB < q_hi) gload(qb0 + QB);  // next tile in flight during this one
+    // next tile in flight during this one; issued after the last tile too (rows past T read as
+    // zero, rows past the range are unused), since loads behind a branch leave the compiler
+    // only a full wait for them before the next MFMA
+    gload(qb0 + QB);
     // nothing visible for this wave: all queries before its keys, or past its window
     if (qb0 + QB - 1 < kw || (a.window && qb0 > kw + 31 + a.window - 1)) continue;
     f32x16 sv, dp;
@@ -1196,6 +1212,8 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
 
   uint4 br[BPT][8];
   float st_lse = 0.f, st_del = 0.f;
+  const size_t stat0 = ((size_t)b * a.Hq + h) * T;  // this (sequence, head)'s row statistics
+  const rsrc_t rL = make_rsrc(a.lse + stat0, (size_t)T * 4), rD = make_rsrc(a.delta + stat0, (size_t)T * 4);
   // Q and dO rows of this sequence and head through buffer resources (rows past T read as
   // zero); per-lane offsets fixed for the kernel, wave-uniform row offsets
   const rsrc_t rQ = seq_rsrc(a.q, rowb, T, a.ldq, h * DH, DH), rdO = seq_rsrc(a.dO, rowb, T, a.ldq, h * DH, DH);
@@ -1215,11 +1233,14 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
       for (int j = 0; j < 8; ++j)
         br[i][j] = bload128s(q_tens ? rQ : rdO, boff[i], (uint32_t)(qb0 + j) * rowB);
     }
-    if (tid < QB) {
+    // the row statistics of queries qb0 + tid (tid < QB) through buffer loads, without a
+    // branch, and scaled only when stored: a use right after the load would make the wave wait
+    // for it, and so for every tile load issued before it
+    {
       const int qq = qb0 + tid;
-      const size_t si = ((size_t)b * a.Hq + h) * T + qq;
-      st_lse = qq < T ? a.lse[si] * LOG2E : 0.f;
-      st_del = qq < T ? a.delta[si] : 0.f;
+      const uint32_t so = (tid < QB && qq < T) ? (uint32_t)qq * 4 : 0x80000000u;
+      st_lse = __uint_as_float(bload32(rL, so));
+      st_del = __uint_as_float(bload32(rD, so));
     }
   };
   auto sstore = [&]() {
@@ -1251,7 +1272,7 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
       }
     }
     if (tid < QB) {
-      lse_s[tid] = st_lse;
+      lse_s[tid] = st_lse * LOG2E;
       del_s[tid] = st_del;
     }
   };
@@ -1261,7 +1282,10 @@ __global__ __launch_bounds__(128 * NP) void k_attn_bwd_kv32p(const AttnArgs a, f
     __syncthreads();  // every wave is done with the previous tile (and its P slot)
     sstore();
     __syncthreads();
-    if (qb0 + QB < q_hi) gload(qb0 + QB);  // next tile in flight during this one
+    // next tile in flight during this one; issued after the last tile too (rows past T read as
+    // zero, rows past the range are unused), since loads behind a branch leave the compiler
+    // only a full wait for them before the next MFMA
+    gload(qb0 + QB);
     // A pair with nothing visible in this tile (all its queries before its keys, or past its
     // window) runs the MFMAs anyway: its P and dS are masked to zero, so they add nothing.
     // Without a branch around them the accumulators stay in the accumulator registers across
