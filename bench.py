@@ -83,9 +83,9 @@ def measured_traffic(kernel, workload):
 # Timing-report names -> the HIP kernels they launch (demangled-name patterns), for reading
 # rocprofv3 output of the same run.
 KERNEL_PATTERNS = {
-    "gemm_nt_f16out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?0(, (true|false))?(, \d+)?>",
-    "gemm_nt_f32out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?1(, (true|false))?(, \d+)?>",
-    "gemm_nt_logits": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?2(, (true|false))?(, \d+)?>",
+    "gemm_nt_f16out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?0(, (true|false))?(, \d+)?(, (true|false))?>",
+    "gemm_nt_f32out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?1(, (true|false))?(, \d+)?(, (true|false))?>",
+    "gemm_nt_logits": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?2(, (true|false))?(, \d+)?(, (true|false))?>",
     "gemm_tn_f32out": r"k_gemm_tn(_big)?<(\d+, )?0(, (true|false))?>",
     "gemm_tn_act_bwd": r"k_gemm_tn(_big)?<(\d+, )?1(, (true|false))?>",
     "gemm_tn_probs_dh": r"k_gemm_tn(_big)?<(\d+, )?2(, (true|false))?>",

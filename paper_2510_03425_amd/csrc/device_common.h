@@ -166,6 +166,14 @@ DEV float gelu_tanh_f(float g) {
   return 0.5f * g * (1.0f + tanh_fast(c * (g + 0.044715f * g * g * g)));
 }
 DEV float act_f(float g, int kind) { return kind == 0 ? silu_f(g) : gelu_tanh_f(g); }
+// the same with the kind known at compile time (no branch per element)
+template <int KIND>
+DEV float act_k(float g) {
+  if constexpr (KIND == 0)
+    return silu_f(g);
+  else
+    return gelu_tanh_f(g);
+}
 DEV float act_grad_f(float g, int kind) {
   if (kind == 0) {
     const float s = sigmoid_fast(g);

@@ -474,6 +474,59 @@ DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int
   }
 }
 
+// Gated MLP epilogue (Sec. 3's per-layer graph: z = act(g) * u): the tile holds 128 gate
+// and the same 128 up features, waves 0, 1 the gate columns and waves 2, 3 the up columns
+// (wave w and w ^ 2 cover the same 64 features). Each wave stages a 32-row chunk of its
+// fp32 outputs in its own LDS region (ep); after a barrier the gate wave forms z for the
+// chunk's first 16 rows and the up wave for the last 16, reading g and u from both regions,
+// with the same fp16 roundings as the stand-alone activation kernel (g and u rounded to
+// fp16, z = fp16(act(g) * u)). g and u are stored only with store_gu (the recompute keeps
+// them for the backward; the forward pass needs z alone). KIND is the activation (0 SiLU,
+// 1 tanh-GELU).
+template <int KIND>
+DEV void nt_lds_store_gated(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int mw0, int f0w, int lane,
+                            float* ep, const float* pep, const float* Us, const float* Bs, int urow0, int bcol0,
+                            int is_up) {
+  constexpr int LDE = 68;
+  if (sg.lora_B) lora_mfma_lds<2>(acc, Us, Bs, a.r, urow0, a.lora_s, bcol0, lane);
+  const int rr = lane >> 3, ch = lane & 7, n = f0w + 8 * ch;
+  const bool nok = n < sg.N;
+  const float* gsrc = is_up ? pep : ep;
+  const float* usrc = is_up ? ep : pep;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) ep[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] = acc[i][j][q];
+    __syncthreads();  // the partner wave's chunk is staged
+    if (a.store_gu) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int r = 8 * p + rr, m = mw0 + 32 * i + r;
+        const float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
+        if (nok && m < a.M)
+          *(uint4*)((f16*)sg.out + (size_t)m * sg.ldo + n) =
+              make_uint4(pack_f16x2(v0.x, v0.y), pack_f16x2(v0.z, v0.w), pack_f16x2(v1.x, v1.y), pack_f16x2(v1.z, v1.w));
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int r = 16 * is_up + 8 * p + rr, m = mw0 + 32 * i + r;
+      const float4 g0 = *(const float4*)(gsrc + r * LDE + 8 * ch), g1 = *(const float4*)(gsrc + r * LDE + 8 * ch + 4);
+      const float4 u0 = *(const float4*)(usrc + r * LDE + 8 * ch), u1 = *(const float4*)(usrc + r * LDE + 8 * ch + 4);
+      const uint32_t gq[4] = {pack_f16x2(g0.x, g0.y), pack_f16x2(g0.z, g0.w), pack_f16x2(g1.x, g1.y), pack_f16x2(g1.z, g1.w)};
+      const uint32_t uq[4] = {pack_f16x2(u0.x, u0.y), pack_f16x2(u0.z, u0.w), pack_f16x2(u1.x, u1.y), pack_f16x2(u1.z, u1.w)};
+      uint32_t o[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        o[t] = pack_f16x2(act_k<KIND>(f16_lo(gq[t])) * f16_lo(uq[t]), act_k<KIND>(f16_hi(gq[t])) * f16_hi(uq[t]));
+      if (nok && m < a.M) *(uint4*)(a.z_out + (size_t)m * sg.N + n) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+    __syncthreads();  // both waves are done with the chunk before the next one is staged
+  }
+}
+
 // WNW waves along n (2 or 4), two along m: 128 x WNW threads, each wave 128 x BN/WNW. With
 // four (512 threads) two waves share each SIMD, so one wave's decompression (VALU) runs
 // beside the other's MFMAs.
@@ -682,18 +735,25 @@ template <>
 struct LdsWeightRegs<true> {  // 16-bit weights: four 16-byte loads per 32 values
   uint4 rw[LDS_STAGES][2][4];
 };
-template <int EPI, bool W16 = false, int NW = 8>
+//
+// GATED: the gate/up product of the MLP with z = act(g) * u formed in the epilogue
+// (nt_lds_store_gated); column tile t covers features 128 t .. 128 t + 127 of both segments.
+template <int EPI, bool W16 = false, int NW = 8, bool GATED = false>
 __global__ __launch_bounds__(64 * NW, 1) void k_gemm_nt_lds(const NtArgs a) {
   constexpr int BN = 256, WNW = 4, NJ = 2, MI = 32 / NW, NA = 32 / NW;
+  // (with four waves the logits epilogue spills: measured 2.7 ms per Gemma3-4B-shaped vocabulary
+  // chunk against 1.6 ms with eight)
   static_assert(NW == 8 || EPI != NT_LOGITS, "the logits epilogue takes 128-row waves");
+  static_assert(!GATED || (EPI == NT_STORE_F16 && NW == 4 && !W16), "the gated epilogue is the fp16 4-wave kernel's");
   // one LDS object per ring stage, so that the compiler can tell the fragment reads of one
   // stage from the LDS-direct loads in flight into another
   __shared__ __attribute__((aligned(1024))) uint8_t lds0[LDS_STAGE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t lds1[LDS_STAGE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t lds2[LDS_STAGE_BYTES];
   // the LoRA up-projection's operands of this tile (u rows, then B rows; r <= 16 floats each),
-  // copied at the start of the tile so that the epilogue does not wait for them
-  __shared__ __attribute__((aligned(1024))) uint8_t lds_lora[2 * BM * 16 * 4];
+  // copied at the start of the tile so that the epilogue does not wait for them (GATED: the
+  // u rows of both segments, then the 128 B rows of each)
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_lora[(GATED ? 3 : 2) * BM * 16 * 4];
   auto stage_ptr = [&](auto S_) -> uint8_t* {
     constexpr int st = decltype(S_)::value;
     return st == 0 ? lds0 : st == 1 ? lds1 : lds2;
@@ -702,17 +762,21 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_nt_lds(const NtArgs a) {
   const int wm = wave / WNW, wn = wave % WNW, h = lane >> 5;
   const int nt = blockIdx.x, mt = blockIdx.y;
   int s = 0;
-  if (a.nseg > 1 && nt >= a.seg[1].tile0) s = 1;
-  if (a.nseg > 2 && nt >= a.seg[2].tile0) s = 2;
+  if constexpr (GATED) {
+    s = wn >> 1;  // waves 0, 1: gate; 2, 3: up
+  } else {
+    if (a.nseg > 1 && nt >= a.seg[1].tile0) s = 1;
+    if (a.nseg > 2 && nt >= a.seg[2].tile0) s = 2;
+  }
   const NtSeg sg = pick_seg(a, s);
-  const int n0 = (nt - sg.tile0) * BN, m0 = mt * BM;
+  const int n0 = GATED ? nt * (BN / 2) : (nt - sg.tile0) * BN, m0 = mt * BM;
   const int K = a.K, Nn = sg.N, Kh = K >> 1;
   const int nk = (K + BK - 1) / BK, kgroups = (K + 31) >> 5;
   const int z = blockIdx.z, S = gridDim.z;
   const int kt_begin = (int)((long long)nk * z / S), kt_end = (int)((long long)nk * (z + 1) / S);
 
   const rsrc_t rA = make_rsrc((const u16*)a.X + (size_t)m0 * a.lda, (size_t)min(BM, a.M - m0) * a.lda * 2);
-  const int wcol0 = n0 + wn * 32 * NJ;
+  const int wcol0 = GATED ? n0 + (wn & 1) * 32 * NJ : n0 + wn * 32 * NJ;
   const int wrows = max(0, min(32 * NJ, Nn - wcol0));
   const rsrc_t rB = W16 ? make_rsrc((const u16*)sg.q4 + (size_t)min(wcol0, Nn) * K, (size_t)wrows * K * 2)
                        : make_rsrc(sg.q4 + (size_t)min(wcol0, Nn) * Kh, (size_t)wrows * Kh);
@@ -746,14 +810,30 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_nt_lds(const NtArgs a) {
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
   const bool tail = (K % BK) != 0;
   // (the rank is 8 or 16 whenever a LoRA factor is given)
-  const bool lora_lds = EPI != NT_LOGITS && sg.lora_B;
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
+  if constexpr (GATED) {
+    // per segment: BM u rows (r KiB) and the tile's 128 B rows (r / 2 KiB), 1 KiB per wave
+    // and instruction
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      if (!a.seg[t].lora_B) continue;
+      const rsrc_t rU = make_rsrc(a.seg[t].lora_u, (size_t)a.M * a.r * 4);
+      const rsrc_t rL = make_rsrc(a.seg[t].lora_B, (size_t)a.seg[t].N * a.r * 4);
+      for (int i = wave; i < a.r; i += NW)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rU, (lds_u8*)(lds_lora + t * (BM * 16 * 4) + 1024 * i), 16,
+                                                 (uint32_t)(m0 * a.r * 4 + 1024 * i + 16 * lane), 0, 0, 0);
+      for (int i = wave; i < a.r / 2; i += NW)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rL, (lds_u8*)(lds_lora + 2 * (BM * 16 * 4) + t * (128 * 16 * 4) + 1024 * i),
+                                                 16, (uint32_t)(n0 * a.r * 4 + 1024 * i + 16 * lane), 0, 0, 0);
+    }
+  }
+  const bool lora_lds = !GATED && EPI != NT_LOGITS && sg.lora_B;
   if (lora_lds) {
     // BM rows of r floats = r KiB each for u and B: one 1 KiB copy per wave and instruction
     // (rows past M or N read as zero)
     const int nin = a.r;
     const rsrc_t rU = make_rsrc(sg.lora_u, (size_t)a.M * a.r * 4);
     const rsrc_t rL = make_rsrc(sg.lora_B, (size_t)Nn * a.r * 4);
-    typedef __attribute__((address_space(3))) uint8_t lds_u8;
     for (int i = wave; i < nin; i += NW) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rU, (lds_u8*)(lds_lora + 1024 * i), 16,
                                                (uint32_t)(m0 * a.r * 4 + 1024 * i + 16 * lane), 0, 0, 0);
@@ -896,7 +976,29 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_nt_lds(const NtArgs a) {
     if (k < kt_end) step(IC<0>{}, k);
     if (k + 1 < kt_end) step(IC<1>{}, k + 1);
   }
-  if constexpr (EPI != NT_LOGITS) {
+  if constexpr (GATED) {
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    auto region = [&](int w) -> float* {
+      return reinterpret_cast<float*>((w < 3 ? lds0 : lds1) + (w % 3) * (32 * 68 * 4));
+    };
+    const float* Us = reinterpret_cast<const float*>(lds_lora + s * (BM * 16 * 4));
+    const float* Bs = reinterpret_cast<const float*>(lds_lora + 2 * (BM * 16 * 4) + s * (128 * 16 * 4));
+    auto epi = [&](auto K_) {
+      constexpr int KIND = decltype(K_)::value;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        f32x16 (&ah)[4][NJ] = *reinterpret_cast<f32x16 (*)[4][NJ]>(&acc[4 * hh][0]);
+        nt_lds_store_gated<KIND>(ah, a, sg, m0 + 128 * hh, wcol0, lane, region(wave), region(wave ^ 2), Us, Bs,
+                                 128 * hh, (wn & 1) * 32 * NJ, s);
+      }
+    };
+    if (a.act == 0)
+      epi(IC<0>{});
+    else
+      epi(IC<1>{});
+  } else if constexpr (EPI != NT_LOGITS) {
     // the ring is idle once the clamped loads of the last steps have landed and every wave
     // has read its last tile; each wave then stages through its own 32 x 68 fp32 region
     wait_vmcnt<0>();
@@ -1271,7 +1373,48 @@ GemmPlan plan_big(int M, int ntiles256, int ntiles128, int ktiles, bool logits, 
   return p;
 }
 
+static int nt_use_lds() {
+  static const int v = [] {
+    const char* e = getenv("MEBP_NT_LDS");
+    return e && *e ? atoi(e) : 1;
+  }();
+  return v;
+}
+
+// fp16 / fp32 outputs as 16-byte row chunks through LDS (required by the LDS-direct kernel,
+// chosen in the other one): one split, segment widths that are multiples of 8 and 16-byte
+// aligned rows
+static bool nt_vec_ok(const NtArgs& a, int epi, int S) {
+  bool vec = S == 1;
+  for (int s = 0; s < a.nseg && epi != NT_LOGITS; ++s) {
+    const NtSeg& g = a.seg[s];
+    const size_t esz = epi == NT_STORE_F16 ? 2 : 4;
+    vec = vec && g.N % 8 == 0 && (((uintptr_t)g.out | (size_t)g.ldo * esz) & 15) == 0 &&
+          (!g.resid || (((uintptr_t)g.resid | (size_t)g.ldr * 4) & 15) == 0);
+  }
+  return vec;
+}
+
+bool nt_gated_fused(const NtArgs& a, int epi, int bn, int S) {
+  static const int on = [] {
+    const char* e = getenv("MEBP_NT_GATED");
+    return e && *e ? atoi(e) : 1;
+  }();
+  return on && a.gated && epi == NT_STORE_F16 && bn == 256 && nt_use_lds() && a.K % 8 == 0 && nt_vec_ok(a, epi, S) &&
+         a.nseg == 2 && a.seg[0].N == a.seg[1].N && a.seg[0].ldo == a.seg[0].N && a.seg[1].ldo == a.seg[1].N &&
+         !a.seg[0].resid && !a.seg[1].resid && !a.seg[0].rope && !a.seg[1].rope && (a.r == 8 || a.r == 16 ||
+         (!a.seg[0].lora_B && !a.seg[1].lora_B)) && ((uintptr_t)a.z_out & 15) == 0;
+}
+
 hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double flops, double bytes, hipStream_t st) {
+  const char* name = epi == NT_STORE_F16 ? "gemm_nt_f16out" : epi == NT_STORE_F32 ? "gemm_nt_f32out" : "gemm_nt_logits";
+  if (nt_gated_fused(a, epi, bn, S)) {
+    // gate/up with the activation in the epilogue: one column tile per 128 features
+    const dim3 gg((a.seg[0].N + 127) / 128, (a.M + BM - 1) / BM, 1);
+    MEBP_TIMED(st, name, flops, bytes,
+               hipLaunchKernelGGL((k_gemm_nt_lds<NT_STORE_F16, false, 4, true>), gg, dim3(256), 0, st, a));
+    return hipGetLastError();
+  }
   int tiles = 0;
   for (int s = 0; s < a.nseg; ++s) tiles += (a.seg[s].N + bn - 1) / bn;
   const dim3 grid(tiles, (a.M + BM - 1) / BM, S);
@@ -1281,25 +1424,11 @@ hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double fl
     b.seg[s].tile0 = t;
     t += (b.seg[s].N + bn - 1) / bn;
   }
-  const char* name = epi == NT_STORE_F16 ? "gemm_nt_f16out" : epi == NT_STORE_F32 ? "gemm_nt_f32out" : "gemm_nt_logits";
 #define NT_BIG(BN_, EPI_, VEC_)                                                                       \
   MEBP_TIMED(st, name, flops, bytes,                                                                  \
              hipLaunchKernelGGL((k_gemm_nt_big<BN_, BN_ / 64, EPI_, VEC_>), grid, dim3(2 * BN_), 0, st, b))
-  static const int use_lds = [] {
-    const char* e = getenv("MEBP_NT_LDS");
-    return e && *e ? atoi(e) : 1;
-  }();
-  // fp16 / fp32 outputs as 16-byte row chunks through LDS (required by the LDS-direct kernel,
-  // chosen in the other one): one split, segment widths that are multiples of 8 and 16-byte
-  // aligned rows
-  bool vec = S == 1;
-  for (int s = 0; s < a.nseg && epi != NT_LOGITS; ++s) {
-    const NtSeg& g = a.seg[s];
-    const size_t esz = epi == NT_STORE_F16 ? 2 : 4;
-    vec = vec && g.N % 8 == 0 && (((uintptr_t)g.out | (size_t)g.ldo * esz) & 15) == 0 &&
-          (!g.resid || (((uintptr_t)g.resid | (size_t)g.ldr * 4) & 15) == 0);
-  }
-  if (bn == 256 && use_lds && a.K % 8 == 0 && (epi == NT_LOGITS || vec)) {
+  const bool vec = nt_vec_ok(a, epi, S);
+  if (bn == 256 && nt_use_lds() && a.K % 8 == 0 && (epi == NT_LOGITS || vec)) {
 #define NT_LDS(EPI_, NW_) \
   MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_nt_lds<EPI_, false, NW_>), grid, dim3(64 * NW_), 0, st, b))
     if (epi == NT_LOGITS)

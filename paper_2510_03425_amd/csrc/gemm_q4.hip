@@ -905,7 +905,9 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st, hipEvent_t 
     const hipError_t ew = hipStreamWaitEvent(st, lora_ready, 0);
     if (ew != hipSuccess) return ew;
   }
+  bool fused_act = false;
   if (plan.big) {
+    fused_act = nt_gated_fused(a, epi, plan.bn, S);
     hipError_t eb = launch_gemm_nt_big(a, epi, plan.bn, S, flops, bytes, st);
     if (eb != hipSuccess) return eb;
   } else switch (epi) {
@@ -933,7 +935,7 @@ hipError_t launch_gemm_nt(const NtArgs& a0, int epi, hipStream_t st, hipEvent_t 
                           a.rope_dh, a.rope_cs, st);
       if (e != hipSuccess) return e;
     }
-    if (a.gated)
+    if (a.gated && !fused_act)
       return launch_act_fwd((const f16*)a.seg[0].out, (const f16*)a.seg[1].out, a.z_out, (size_t)a.M * a.seg[0].N,
                             a.act, st);
     if (a.norm_w)

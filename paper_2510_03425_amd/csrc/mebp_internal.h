@@ -84,6 +84,8 @@ GemmPlan plan_tn(int M, int Kout, const int* Ns, int nseg, bool softmax);  // so
 // statistics tiles per row of the LM-head logits GEMM over V columns (64 columns each)
 int gemm_logit_stat_tiles(int V);
 hipError_t launch_gemm_nt_big(const NtArgs& a, int epi, int bn, int S, double flops, double bytes, hipStream_t st);
+// whether launch_gemm_nt_big forms z = act(g) * u of a gated product in its epilogue
+bool nt_gated_fused(const NtArgs& a, int epi, int bn, int S);
 
 // Transposed orientation (input gradients): C[m][c] = sum_seg sum_n G_seg[m][n] * W_seg[n][c]
 // with W_seg int4 [N_seg][Kout/2]; reduction over the weight's output dim; G bf16 (bf16

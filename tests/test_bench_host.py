@@ -37,6 +37,10 @@ KERNELS = [
     ("k_gemm_nt_lds<0, false, 4>", "gemm_nt_f16out"),
     ("k_gemm_nt_lds<1, false, 4>", "gemm_nt_f32out"),
     ("k_gemm_nt_lds<2, false, 8>", "gemm_nt_logits"),
+    ("k_gemm_nt_lds<0, false, 4, true>", "gemm_nt_f16out"),
+    ("k_gemm_nt_lds<0, false, 4, false>", "gemm_nt_f16out"),
+    ("k_gemm_nt_lds<1, false, 4, false>", "gemm_nt_f32out"),
+    ("k_gemm_nt_lds<2, false, 8, false>", "gemm_nt_logits"),
     ("k_gemm_nt_big<256, 4, 0, true>", "gemm_nt_f16out"),
     ("k_gemm_nt_big<128, 2, 0, false>", "gemm_nt_f16out"),
     ("k_gemm_nt<1>", "gemm_nt_f32out"),
