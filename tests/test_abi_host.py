@@ -27,6 +27,21 @@ def test_header_symbols_exported(built_lib):
     assert set(names) == set(L.EXPORTED)
 
 
+def test_every_kernel_launch_stub_is_defined(built_lib):
+    """Each launched kernel has its host-side launch stub in the library. The host pass can
+    drop a kernel template's stub without an error (for instance when an argument of a target
+    builtin in it needs an implicit conversion that only the device pass accepts); the library
+    then fails to load with an undefined __device_stub__ symbol."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm is not available")
+    out = subprocess.run([nm, "-u", L.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    missing = [ln.split()[-1] for ln in out.splitlines() if "__device_stub__" in ln]
+    assert not missing, missing
+
+
 def test_struct_sizes_match_header(built_lib):
     # mebp_config: 18 four-byte fields; the structs are arrays of pointers
     assert C.sizeof(L.MebpConfig) == 18 * 4
