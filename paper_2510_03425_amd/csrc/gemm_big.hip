@@ -480,9 +480,8 @@ DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int
 // fp32 outputs in its own LDS region (ep); after a barrier the gate wave forms z for the
 // chunk's first 16 rows and the up wave for the last 16, reading g and u from both regions,
 // with the same fp16 roundings as the stand-alone activation kernel (g and u rounded to
-// fp16, z = fp16(act(g) * u)). g and u are stored only with store_gu (the recompute keeps
-// them for the backward; the forward pass needs z alone). KIND is the activation (0 SiLU,
-// 1 tanh-GELU).
+// fp16, z = fp16(act(g) * u)). Used where z alone is needed (the forward pass); g and u are
+// not stored. KIND is the activation (0 SiLU, 1 tanh-GELU).
 template <int KIND>
 DEV void nt_lds_store_gated(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int mw0, int f0w, int lane,
                             float* ep, const float* pep, const float* Us, const float* Bs, int urow0, int bcol0,
@@ -500,16 +499,6 @@ DEV void nt_lds_store_gated(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& s
 #pragma unroll
       for (int j = 0; j < 2; ++j) ep[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] = acc[i][j][q];
     __syncthreads();  // the partner wave's chunk is staged
-    if (a.store_gu) {
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int r = 8 * p + rr, m = mw0 + 32 * i + r;
-        const float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
-        if (nok && m < a.M)
-          *(uint4*)((f16*)sg.out + (size_t)m * sg.ldo + n) =
-              make_uint4(pack_f16x2(v0.x, v0.y), pack_f16x2(v0.z, v0.w), pack_f16x2(v1.x, v1.y), pack_f16x2(v1.z, v1.w));
-      }
-    }
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const int r = 16 * is_up + 8 * p + rr, m = mw0 + 32 * i + r;
@@ -1400,7 +1389,11 @@ bool nt_gated_fused(const NtArgs& a, int epi, int bn, int S) {
     const char* e = getenv("MEBP_NT_GATED");
     return e && *e ? atoi(e) : 1;
   }();
-  return on && a.gated && epi == NT_STORE_F16 && bn == 256 && nt_use_lds() && a.K % 8 == 0 && nt_vec_ok(a, epi, S) &&
+  // Only where g and u are not kept (the forward pass). The recompute, which keeps them for
+  // the backward, runs the plain product and the activation kernel: fused there too, the step
+  // measured 494 ms against 488 ms (the epilogue's activation work then delays the backward
+  // that runs beside the recompute).
+  return on && !a.store_gu && a.gated && epi == NT_STORE_F16 && bn == 256 && nt_use_lds() && a.K % 8 == 0 && nt_vec_ok(a, epi, S) &&
          a.nseg == 2 && a.seg[0].N == a.seg[1].N && a.seg[0].ldo == a.seg[0].N && a.seg[1].ldo == a.seg[1].N &&
          !a.seg[0].resid && !a.seg[1].resid && !a.seg[0].rope && !a.seg[1].rope && (a.r == 8 || a.r == 16 ||
          (!a.seg[0].lora_B && !a.seg[1].lora_B)) && ((uintptr_t)a.z_out & 15) == 0;
