@@ -188,13 +188,28 @@ HEAD_DIM_CASES = {
 @pytest.mark.parametrize("layer", [0, 1])
 @pytest.mark.parametrize("name", list(HEAD_DIM_CASES))
 def test_layer_head_dims_parity(built_lib, gpu, name, layer):
-    cfg = HEAD_DIM_CASES[name]
+    _layer_parity(HEAD_DIM_CASES[name], layer, gpu, name)
+
+
+# The forward pass's gate/up product with z = act(g) * u formed in its epilogue (the
+# large-tile kernel: 8192 tokens, 256 x 256 tiles) at an FFN width that is no multiple of its
+# 128-feature column tile: 688 = 5 x 128 + 48, so in the last tile the first gate / up wave
+# pair holds 48 of its 64 features and the second none.
+RAGGED_FFN = MINI.with_(name="ragged_ffn", hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn=688, batch=4,
+                        seq=2048)
+
+
+def test_layer_parity_fused_activation_ragged_ffn(built_lib, gpu):
+    _layer_parity(RAGGED_FFN, 0, gpu, "ragged_ffn", rows=True)
+
+
+def _layer_parity(cfg, layer, gpu, name, rows=False):
     inp = make_inputs(cfg, seed=7, norm="random")
     x, dy = layer_input(cfg, 107)
     dm = _dm(inp, gpu)
     tx, tdy = torch.from_numpy(x).to(gpu), torch.from_numpy(dy).to(gpu)
     ty, tdx = torch.empty_like(tx), torch.empty_like(tx)
-    say("head-dim case", name, "layer", layer, "window", cfg.layer_window(layer))
+    say("layer case", name, "layer", layer, "window", cfg.layer_window(layer))
     dm.layer_forward(layer, tx, ty)
     dm.layer_backward(layer, tx, tdy, tdx)
     torch.cuda.synchronize()
@@ -208,6 +223,11 @@ def test_layer_head_dims_parity(built_lib, gpu, name, layer):
     say("rel-L2", {k: f"{v:.2e}" for k, v in errs.items()})
     for k, e in errs.items():
         assert e <= TOL, (k, e)
+    if rows:
+        row = {"y": max_row_rel_l2(to_np(ty), y_ref), "dx": max_row_rel_l2(to_np(tdx), dx_ref)}
+        say("max row rel-L2", {k: f"{v:.2e}" for k, v in row.items()})
+        for k, e in row.items():
+            assert e <= ROW_TOL, (k, "row", e)
 
 
 def test_dx_may_alias_dy(built_lib, gpu):
