@@ -474,7 +474,7 @@ DEV void nt_lds_store(f32x16 (&acc)[4][2], const NtArgs& a, const NtSeg& sg, int
   }
 }
 
-// Gated MLP epilogue (Sec. 3's per-layer graph: z = act(g) * u): the tile holds 128 gate
+// Gated MLP epilogue (the model's MLP: z = act(g) * u): the tile holds 128 gate
 // and the same 128 up features, waves 0, 1 the gate columns and waves 2, 3 the up columns
 // (wave w and w ^ 2 cover the same 64 features). Each wave stages a 32-row chunk of its
 // fp32 outputs in its own LDS region (ep); after a barrier the gate wave forms z for the
