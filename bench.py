@@ -86,10 +86,10 @@ KERNEL_PATTERNS = {
     "gemm_nt_f16out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?0(, (true|false))?(, \d+)?(, (true|false))?>",
     "gemm_nt_f32out": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?1(, (true|false))?(, \d+)?(, (true|false))?>",
     "gemm_nt_logits": r"k_gemm_nt(_big|_lds)?<(\d+, \d+, )?2(, (true|false))?(, \d+)?(, (true|false))?>",
-    "gemm_tn_f32out": r"k_gemm_tn(_big)?<(\d+, )?0(, (true|false))?>",
-    "gemm_tn_act_bwd": r"k_gemm_tn(_big)?<(\d+, )?1(, (true|false))?>",
-    "gemm_tn_probs_dh": r"k_gemm_tn(_big)?<(\d+, )?2(, (true|false))?>",
-    "gemm_tn_bf16out": r"k_gemm_tn(_big)?<(\d+, )?3(, (true|false))?>",
+    "gemm_tn_f32out": r"k_gemm_tn(_big|_lds)?<(\d+, )?0(, (true|false))?>",
+    "gemm_tn_act_bwd": r"k_gemm_tn(_big|_lds)?<(\d+, )?1(, (true|false))?>",
+    "gemm_tn_probs_dh": r"k_gemm_tn(_big|_lds)?<(\d+, )?2(, (true|false))?>",
+    "gemm_tn_bf16out": r"k_gemm_tn(_big|_lds)?<(\d+, )?3(, (true|false))?>",
     "lora_rows": r"k_lora_rows<",
     "lora_outer": r"k_lora_outer<",
     "attn_fwd": r"k_attn_fwd",

@@ -1328,6 +1328,241 @@ __global__ __launch_bounds__(NTH, 1) void k_gemm_tn_big(const TnArgs a) {
   }
 }
 
+
+// Transposed product with both operands copied into LDS by LDS-direct loads in their stored
+// layouts: the gradient tile G [256 rows m][64 n] (rows of 128 B, chunks XOR-swizzled as in
+// the forward kernel) and the 16-bit weight tile W [64 rows n][256 columns c] (rows of 512 B,
+// 16-byte chunk c at position c ^ (2 (n % 4) + (n / 4) % 2)). The MFMA B fragments (8
+// consecutive n of one column) come from gfx950's transposing LDS read (8 bytes: in each
+// group of 16 lanes, lane s points at row R0 + s / 4, columns C0 + 4 (s % 4); lane i then
+// receives rows R0 .. R0 + 3 of column C0 + i). Four waves of 256 rows x 64 columns; two
+// ring stages (128 KiB), the next tile's copies issued before the current tile's MFMAs.
+template <int EPI>
+__global__ __launch_bounds__(256, 1) void k_gemm_tn_lds(const TnArgs a) {
+  constexpr int NW = 4, NJ = 2, MI = 8, BNT = 256, NA = 8, NB = 8;
+  constexpr int SA = BM * BK * 2, SB = BK * BNT * 2;
+  static_assert(EPI == TN_ACT_BWD || EPI == TN_STORE_BF16, "the activation-backward and bf16 epilogues");
+  __shared__ __attribute__((aligned(1024))) uint8_t st0[SA + SB];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1[SA + SB];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), h = lane >> 5;
+  const TileId tl = xcd_tile();
+  const int c0 = tl.x * BNT, m0 = tl.y * BM;
+  const int Kout = a.Kout;
+  int ntl[3], total = 0;
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    ntl[s] = s < a.nseg ? (a.seg[s].N + BK - 1) / BK : 0;
+    total += ntl[s];
+  }
+  rsrc_t rA[3], rB[3];
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    const TnSeg& sg = a.seg[s < a.nseg ? s : 0];
+    rA[s] = make_rsrc((const u16*)sg.G + (size_t)m0 * sg.ldg, (size_t)min(BM, a.M - m0) * sg.ldg * 2);
+    rB[s] = make_rsrc((const u16*)sg.q4 + c0, ((size_t)(sg.N - 1) * Kout + min(BNT, Kout - c0)) * 2);
+  }
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
+  auto swzb = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
+  // A copies: instruction i of the wave fills rows 8 (wave + 4 i) .. + 8
+  const int rowA0 = 8 * wave + (lane >> 3), chunkA = (lane & 7) ^ ((rowA0 >> 1) & 7);
+  // B copies: instruction i fills rows 2 (wave + 4 i), + 1; lane l row + l / 32, position l % 32
+  int rowB[NB];
+  uint32_t colB[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    rowB[i] = 2 * (wave + NW * i) + (lane >> 5);
+    colB[i] = (uint32_t)(8 * ((lane & 31) ^ swzb(rowB[i])) * 2);
+  }
+  f32x16 acc[MI][NJ];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+
+  auto stage = [&](auto S_) -> uint8_t* { return decltype(S_)::value == 0 ? st0 : st1; };
+  auto gload = [&](auto S_, int t) {
+    int s = 0, tt = t;
+    if (tt >= ntl[0]) {
+      tt -= ntl[0];
+      s = 1;
+      if (tt >= ntl[1]) {
+        tt -= ntl[1];
+        s = 2;
+      }
+    }
+    const TnSeg& sg = a.seg[s];
+    const rsrc_t ra = s == 0 ? rA[0] : s == 1 ? rA[1] : rA[2];
+    const rsrc_t rb = s == 0 ? rB[0] : s == 1 ? rB[1] : rB[2];
+    const int n0 = tt * BK, Ns = sg.N, ldg = sg.ldg;
+    lds_u8* dst = (lds_u8*)stage(S_);
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      // reduction columns past the segment read as zero
+      const int row = rowA0 + 32 * i;
+      const uint32_t off = n0 + 8 * chunkA < Ns ? (uint32_t)((row * ldg + n0 + 8 * chunkA) * 2) : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, dst + 1024 * (wave + NW * i), 16, (int)off, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      // rows past the segment are past the resource: zero
+      const uint32_t off = (uint32_t)((n0 + rowB[i]) * Kout * 2) + colB[i];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst + SA + 1024 * (wave + NW * i), 16, (int)off, 0, 0, 0);
+    }
+  };
+  // fragment reads
+  const uint32_t rowA = (uint32_t)((lane & 31) * 128);
+  const int tg = lane >> 4, ts = lane & 15;
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4s lds_v4s;
+  auto mma = [&](auto S_) {
+    const uint8_t* As = stage(S_) + rowA;
+    const uint8_t* Bs = stage(S_) + SA;
+    auto rda = [&](int t, uint4 (&dst)[MI]) {
+      const int pos = ((4 * h + t) ^ ((lane >> 1) & 7)) * 16;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) dst[i] = *(const uint4*)(As + 4096 * i + pos);
+    };
+    // B fragment of column block j, substep t: k = 32 h + 8 t + (0..7)
+    auto rdb = [&](int t, uint4 (&dst)[NJ]) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        uint2 v[2];
+#pragma unroll
+        for (int rd = 0; rd < 2; ++rd) {
+          const int r = 32 * h + 8 * t + 4 * rd + (ts >> 2);
+          const int col = 64 * wave + 32 * j + 16 * (tg & 1) + 4 * (ts & 3);
+          const int off = r * (BNT * 2) + (((col >> 3) ^ swzb(r)) << 4) + ((col & 7) << 1);
+          v[rd] = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Bs + off)));
+        }
+        dst[j] = make_uint4(v[0].x, v[0].y, v[1].x, v[1].y);
+      }
+    };
+    uint4 af[2][MI], bf[2][NJ];
+    rda(0, af[0]);
+    rdb(0, bf[0]);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      if (t < 3) {
+        rda(t + 1, af[(t + 1) & 1]);
+        rdb(t + 1, bf[(t + 1) & 1]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32<OpBF16>(af[t & 1][i], bf[t & 1][j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto step = [&](auto I_, int t) {
+    constexpr int I = decltype(I_)::value;
+    gload(IC<1 - I>{}, min(t + 1, total - 1));
+    mma(IC<I>{});
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  gload(IC<0>{}, 0);
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  int t = 0;
+  for (; t + 2 <= total; t += 2) {
+    step(IC<0>{}, t);
+    step(IC<1>{}, t + 1);
+  }
+  if (t < total) step(IC<0>{}, t);
+
+  // epilogue per 128-row half (the accumulators of rows 128 hh .. + 128 in the layout of the
+  // 128-row waves of k_gemm_tn_big, with wm = hh and wn = wave)
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    f32x16 (&ah)[4][NJ] = *reinterpret_cast<f32x16 (*)[4][NJ]>(&acc[4 * hh][0]);
+    for (int s = 0; s < a.nseg; ++s) {
+      const TnSeg& sg = a.seg[s];
+      if (sg.lora_A)
+        lora_mfma<NJ>(ah, sg.lora_du, a.r, m0 + 128 * hh, a.M, 1.0f, sg.lora_A, 1, Kout, c0 + wave * 64, Kout, lane);
+    }
+    if constexpr (EPI == TN_ACT_BWD) {
+      // 32-row chunks (one accumulator block each) through the wave's own 32 x 68 fp32 region:
+      // each lane handles 8 consecutive columns of a row; the chunk's g and u loads are issued
+      // before its accumulators are staged
+      constexpr int CW = 64, LDE = CW + 4, CPR = CW / 8, RPP = 64 / CPR, NP = 32 / RPP;
+      float* ep = reinterpret_cast<float*>(st0) + wave * 32 * LDE;
+      const int rr = lane / CPR, ch = lane % CPR;
+      const int cbase = c0 + wave * CW + 8 * ch;
+#pragma unroll
+      for (int h2 = 0; h2 < 4; ++h2) {
+        uint4 gw[NP], uw[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const int m = m0 + 128 * hh + 32 * h2 + p * RPP + rr;
+          const bool ok = m < a.M && cbase < Kout;
+          const size_t idx = ok ? (size_t)m * a.ldgu + cbase : 0;
+          gw[p] = ok ? *(const uint4*)((const f16*)a.g + idx) : make_uint4(0, 0, 0, 0);
+          uw[p] = ok ? *(const uint4*)((const f16*)a.u + idx) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j)
+            ep[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * LDE + 32 * j + (lane & 31)] = ah[h2][j][q];
+        auto finish = [&](auto K_) {
+          constexpr int KIND = decltype(K_)::value;
+#pragma unroll
+          for (int p = 0; p < NP; ++p) {
+            const int r = p * RPP + rr, m = m0 + 128 * hh + 32 * h2 + r;
+            const float4 v0 = *(const float4*)(ep + r * LDE + 8 * ch), v1 = *(const float4*)(ep + r * LDE + 8 * ch + 4);
+            const uint32_t gq[4] = {gw[p].x, gw[p].y, gw[p].z, gw[p].w}, uq[4] = {uw[p].x, uw[p].y, uw[p].z, uw[p].w};
+            const float dz[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            uint32_t og[4], ou[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              const float g0 = f16_lo(gq[k]), g1 = f16_hi(gq[k]), u0 = f16_lo(uq[k]), u1 = f16_hi(uq[k]);
+              float a0, d0, a1, d1;
+              act_and_grad<KIND>(g0, a0, d0);
+              act_and_grad<KIND>(g1, a1, d1);
+              og[k] = pack_bf16x2(dz[2 * k] * u0 * d0, dz[2 * k + 1] * u1 * d1);
+              ou[k] = pack_bf16x2(dz[2 * k] * a0, dz[2 * k + 1] * a1);
+            }
+            if (m < a.M && cbase < Kout) {
+              const size_t idx = (size_t)m * a.ldgu + cbase;
+              *(uint4*)((bf16*)a.g + idx) = make_uint4(og[0], og[1], og[2], og[3]);
+              *(uint4*)((bf16*)a.u + idx) = make_uint4(ou[0], ou[1], ou[2], ou[3]);
+            }
+          }
+        };
+        if (a.act == 0)
+          finish(IC<0>{});
+        else
+          finish(IC<1>{});
+      }
+    } else {
+      auto put = [&](auto FULL_) {
+        constexpr bool FULL = decltype(FULL_)::value;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const int m = m0 + acc_row(hh, i, q, lane);
+            if (!FULL && m >= a.M) continue;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+              const int c = c0 + acc_col<NJ>(wave, j, lane);
+              if (!FULL && c >= Kout) continue;
+              a.outb[(size_t)m * a.ldo + c] = (bf16)ah[i][j][q];
+            }
+          }
+      };
+      if (m0 + BM <= a.M && c0 + BNT <= Kout)
+        put(IC<1>{});
+      else
+        put(IC<0>{});
+    }
+  }
+}
 }  // namespace
 
 // ------------------------------------------------------------------------------ planning
@@ -1490,6 +1725,26 @@ hipError_t launch_gemm_tn_big(const TnArgs& a, int epi, int amode, int bn, int S
   // the transposed weight tile goes through LDS; 256-wide tiles would need more than the
   // 512 registers a lane has next to 256 accumulators
   if (bn != 128) return hipErrorInvalidValue;
+  // the activation-backward and bf16-output products (column counts that are multiples of
+  // 256 here: 10 240, 2048) on the LDS-direct kernel with 256-wide tiles; the fp32-output
+  // products keep 128-wide tiles (2560 columns: 10 tiles of 256 would leave half of the last
+  // round of workgroups idle)
+  static const int tl = [] {
+    const char* e = getenv("MEBP_TN_LDS");
+    return e && *e ? atoi(e) : 1;
+  }();
+  if (tl && w16 && S == 1 && (epi == TN_ACT_BWD || epi == TN_STORE_BF16) && a.Kout % 8 == 0) {
+    bool ok = true;
+    for (int s = 0; s < a.nseg; ++s) ok = ok && a.seg[s].N % 8 == 0 && a.seg[s].ldg % 8 == 0;
+    if (ok) {
+      const dim3 g2((a.Kout + 255) / 256, (a.M + BM - 1) / BM, 1);
+      if (epi == TN_ACT_BWD)
+        MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_lds<TN_ACT_BWD>), g2, dim3(256), 0, st, a));
+      else
+        MEBP_TIMED(st, name, flops, bytes, hipLaunchKernelGGL((k_gemm_tn_lds<TN_STORE_BF16>), g2, dim3(256), 0, st, a));
+      return hipGetLastError();
+    }
+  }
   TN_BIG_EPI(128);
 #undef TN_BIG_EPI
 #undef TN_BIG

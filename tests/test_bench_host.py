@@ -59,6 +59,8 @@ KERNELS = [
     ("k_gemm_tn_big<128, 3>", "gemm_tn_bf16out"),
     ("k_gemm_tn_big<128, 0, true>", "gemm_tn_f32out"),
     ("k_gemm_tn_big<128, 1, true>", "gemm_tn_act_bwd"),
+    ("k_gemm_tn_lds<1>", "gemm_tn_act_bwd"),
+    ("k_gemm_tn_lds<3>", "gemm_tn_bf16out"),
     ("k_lora_rows<OpF16>", "lora_rows"),
     ("k_lora_outer<true>", "lora_outer"),
     ("k_attn_fwd32<256, 4>", "attn_fwd"),
